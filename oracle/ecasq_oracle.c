@@ -1,0 +1,588 @@
+/*
+ * ECASQ approximate-DP oracle (plain C, fp64, slow, obviously correct).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only tests/, __graft_entry__.smoke() and the
+ * cpu_baseline leg of bench.py may load this library.  It shares no code with
+ * the GPU library; the two meet only through the canonical arithmetic stated
+ * below, which each side implements on its own.
+ *
+ * What it computes (paper: arXiv 2608.18147):
+ *   - interval quantities C, U, D from prefix sums        (App. D, closed forms)
+ *   - Phi and Phi^first surrogate-entropy terms           (Sec. 5, def. of Phi)
+ *   - dp_APX base, recurrence and final minimum           (Sec. 5, eq. apx_base,
+ *                                                          apx_rec, apx_final)
+ *   - Hirschberg recovery of the codebook in O(p) space   (Sec. 5, last paragraph
+ *                                                          before Lemma 4; Sec. 4.2)
+ *   - a backpointer traceback, used as a cross-check
+ *   - the lambda search for a budget b                    (Sec. 3 Lagrangian;
+ *                                                          Sec. 5 budget tuning;
+ *                                                          App. F.7 slope queries)
+ *   - the three-colour refinement                         (Sec. 6)
+ *
+ * Canonical arithmetic (both sides evaluate exactly this, -ffp-contract=off,
+ * fma only where written):
+ *   interval (v_a, v_b], a < b:
+ *     n  = N[b]-N[a]   sa = S[b]-S[a]   s2 = S2[b]-S2[a]   w = v_b - v_a
+ *     tu = fma(-v_a, n, sa)        td = fma(v_b, n, -sa)
+ *     C  = fma(v_b, tu, fma(v_a, sa, -s2))
+ *   DP cell entropy (g form):
+ *     g = 1/(w*d)   yu = tu*g   yd = td*g  (+ c0/d if a == 0, first interval)
+ *     P = fma(max(yu,0), log2c(yu), max(yd,0)*log2c(yd))      (P = -Phi)
+ *     cand = fma(-lambda', P, F_prev + C)
+ *   refinement / output-entropy (inv form):
+ *     U = tu*(1/w)   D = td*(1/w)   h(f) = -(max(y,0)*log2c(y)), y = f/d
+ *   log2c: table-driven, see log2c() below.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define OFF_HI 0x3FE6A800u /* entry 149 is centred on 1.0 */
+#define TBITS 8
+#define TSIZE (1 << TBITS)
+
+static double g_invc[TSIZE];
+static double g_lc[TSIZE];
+
+void orc_set_log2_table(const double *invc, const double *lc)
+{
+    memcpy(g_invc, invc, sizeof g_invc);
+    memcpy(g_lc, lc, sizeof g_lc);
+}
+
+/* Canonical base-2 logarithm.  For a positive normal y it returns log2(y) to
+ * about one ulp; for any other finite y it returns some finite value (callers
+ * multiply it by max(y, 0)).  Steps: y = 2^e * z with z in [~0.7073, ~1.4147)
+ * selected by subtracting an offset from y's high word; table entry i (top 8
+ * bits of the reduced mantissa) gives invc ~ 1/z and lc = log2(1/invc);
+ * r = z*invc - 1 with |r| <= 2^-9; log2(1+r) from the degree-6 Taylor series of
+ * log1p times RN(1/ln 2). */
+static double log2c(double y)
+{
+    uint64_t bits;
+    memcpy(&bits, &y, 8);
+    uint32_t hi = (uint32_t)(bits >> 32);
+    uint32_t lo = (uint32_t)bits;
+    uint32_t tmp = hi - OFF_HI;
+    int32_t e = ((int32_t)tmp) >> 20;
+    uint32_t i = (tmp >> (20 - TBITS)) & (TSIZE - 1);
+    uint32_t zhi = hi - (tmp & 0xFFF00000u);
+    uint64_t zb = ((uint64_t)zhi << 32) | lo;
+    double z;
+    memcpy(&z, &zb, 8);
+    double r = fma(z, g_invc[i], -1.0);
+    double q = -1.0 / 6.0;
+    q = fma(q, r, 1.0 / 5.0);
+    q = fma(q, r, -0.25);
+    q = fma(q, r, 1.0 / 3.0);
+    q = fma(q, r, -0.5);
+    q = fma(q, r, 1.0);
+    double lp = r * q;
+    double base = (double)e + g_lc[i];
+    return fma(0x1.71547652b82fep+0, lp, base);
+}
+
+double orc_log2c(double y) { return log2c(y); }
+
+/* h(y) = -y log2 y for y > 0, 0 otherwise (Sec. 4, definition of h). */
+static double hfun(double y) { return -(fmax(y, 0.0) * log2c(y)); }
+
+double orc_h(double y) { return hfun(y); }
+
+typedef struct {
+    const double *v;  /* sorted unique values v_0 < ... < v_{p-1} */
+    const double *N;  /* inclusive prefix counts (exact in fp64) */
+    const double *S;  /* inclusive prefix sums of c*v, correctly rounded */
+    const double *S2; /* inclusive prefix sums of c*v^2, correctly rounded */
+    int64_t p;
+    double dd;  /* d as a double */
+    double c0;  /* count of v_0 */
+    double c0d; /* RN(c0 / d) */
+    double s2tot; /* ||X||^2 = S2[p-1] */
+} hist_t;
+
+/* C[a,b] and the DP-form P = -Phi (Phi^first when a == 0) of the interval
+ * (v_a, v_b].  App. D closed forms; Sec. 5 definition of Phi and Phi^first. */
+static void cell_terms(const hist_t *H, int64_t a, int64_t b, double *C, double *P)
+{
+    double va = H->v[a], vb = H->v[b];
+    double n = H->N[b] - H->N[a];
+    double sa = H->S[b] - H->S[a];
+    double s2 = H->S2[b] - H->S2[a];
+    double w = vb - va;
+    double tu = fma(-va, n, sa);
+    double td = fma(vb, n, -sa);
+    *C = fma(vb, tu, fma(va, sa, -s2));
+    double wd = w * H->dd;
+    double g = 1.0 / wd;
+    double yu = tu * g;
+    double yd = td * g;
+    if (a == 0)
+        yd = yd + H->c0d;
+    double lu = log2c(yu);
+    double ld = log2c(yd);
+    *P = fma(fmax(yu, 0.0), lu, fmax(yd, 0.0) * ld);
+}
+
+/* U[a,b] and D[a,b] of (v_a, v_b] in the inv form (App. D closed forms). */
+static void interval_ud(const hist_t *H, int64_t a, int64_t b, double *U, double *D)
+{
+    double va = H->v[a], vb = H->v[b];
+    double n = H->N[b] - H->N[a];
+    double sa = H->S[b] - H->S[a];
+    double w = vb - va;
+    double tu = fma(-va, n, sa);
+    double td = fma(vb, n, -sa);
+    double inv = 1.0 / w;
+    *U = tu * inv;
+    *D = td * inv;
+}
+
+static double interval_c(const hist_t *H, int64_t a, int64_t b)
+{
+    double C, P;
+    cell_terms(H, a, b, &C, &P);
+    return C;
+}
+
+static double hf(const hist_t *H, double f) { return hfun(f / H->dd); }
+
+/* Interval quantities of (v_a, v_b] for tests: C, U, D (inv form), P (DP form). */
+void orc_interval(const double *v, const double *N, const double *S, const double *S2,
+                  int64_t p, int64_t d, int64_t a, int64_t b, double *out)
+{
+    hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
+    double C, P, U, D;
+    cell_terms(&H, a, b, &C, &P);
+    interval_ud(&H, a, b, &U, &D);
+    out[0] = C; out[1] = U; out[2] = D; out[3] = P;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Approximate DP, forward, O(p) rolling layers (Sec. 5).                      */
+
+typedef struct {
+    double J;    /* min_i F_i[p-1], MSE units */
+    double mse;  /* MSE of the minimising path (accumulated along argmins) */
+    double phi;  /* H(I,B) of that path, bits */
+    int32_t t;   /* number of values i* */
+    int64_t cells;
+} dp_result;
+
+/*
+ * F_2[j]   = C[0,j] + lambda' Phi^first[0,j]                      (eq. apx_base)
+ * F_i[j]   = min_{i-2 <= k < j} F_{i-1}[k] + C[k,j] + lambda' Phi[k,j]  (eq. apx_rec)
+ * answer   = min_{2 <= i <= min(s,p)} F_i[p-1]                       (eq. apx_final)
+ * Ties: lowest k, lowest i.  mse/phi are carried along the chosen k.
+ * bp (optional, (s+1)*p int32): bp[i*p+j] = argmin k of layer i.
+ * fdump (optional, (s+1)*p doubles): F_i[j] for every layer.
+ */
+int orc_dp_forward(const double *v, const double *N, const double *S, const double *S2,
+                   int64_t p, int64_t d, int32_t s, int32_t exact_s, double lamp,
+                   double *out /* J, mse, phi, t, cells */, int32_t *bp, double *fdump,
+                   double *lastF /* optional [s+1] */)
+{
+    hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
+    dp_result R = {0.0, 0.0, 0.0, 1, 0};
+    if (p == 1) {
+        out[0] = 0.0; out[1] = 0.0; out[2] = 0.0; out[3] = 1; out[4] = 0;
+        return 0;
+    }
+    int32_t imax = (int32_t)((int64_t)s < p ? s : p);
+    double *F0 = malloc(sizeof(double) * p), *F1 = malloc(sizeof(double) * p);
+    double *M0 = malloc(sizeof(double) * p), *M1 = malloc(sizeof(double) * p);
+    double *P0 = malloc(sizeof(double) * p), *P1 = malloc(sizeof(double) * p);
+    if (!F0 || !F1 || !M0 || !M1 || !P0 || !P1)
+        return -4;
+    double bestJ = INFINITY, bestM = 0, bestP = 0;
+    int32_t bestI = 2;
+    /* layer 2 */
+    F0[0] = INFINITY; M0[0] = 0; P0[0] = 0;
+    for (int64_t j = 1; j < p; j++) {
+        double C, P;
+        cell_terms(&H, 0, j, &C, &P);
+        F0[j] = fma(-lamp, P, 0.0 + C);
+        M0[j] = 0.0 + C;
+        P0[j] = 0.0 - P;
+        if (bp) bp[2 * p + j] = 0;
+    }
+    R.cells += p - 1;
+    if (fdump) memcpy(fdump + 2 * p, F0, sizeof(double) * p);
+    if (lastF) lastF[2] = F0[p - 1];
+    bestJ = F0[p - 1]; bestM = M0[p - 1]; bestP = P0[p - 1]; bestI = 2;
+    for (int32_t i = 3; i <= imax; i++) {
+        int64_t klo = i - 2, jlo = i - 1;
+        for (int64_t j = 0; j < jlo; j++) { F1[j] = INFINITY; M1[j] = 0; P1[j] = 0; }
+#pragma omp parallel for schedule(dynamic, 64)
+        for (int64_t j = jlo; j < p; j++) {
+            double best = INFINITY;
+            int64_t bk = -1;
+            for (int64_t k = klo; k < j; k++) {
+                double C, P;
+                cell_terms(&H, k, j, &C, &P);
+                double cand = fma(-lamp, P, F0[k] + C);
+                if (cand < best) { best = cand; bk = k; }
+            }
+            F1[j] = best;
+            if (bk >= 0) {
+                double C, P;
+                cell_terms(&H, bk, j, &C, &P);
+                M1[j] = M0[bk] + C;
+                P1[j] = P0[bk] - P;
+            } else {
+                M1[j] = 0; P1[j] = 0;
+            }
+            if (bp) bp[(int64_t)i * p + j] = (int32_t)bk;
+        }
+        for (int64_t j = jlo; j < p; j++) R.cells += j - klo;
+        if (fdump) memcpy(fdump + (int64_t)i * p, F1, sizeof(double) * p);
+        if (lastF) lastF[i] = F1[p - 1];
+        if (exact_s ? (i == imax) : (F1[p - 1] < bestJ)) {
+            bestJ = F1[p - 1]; bestM = M1[p - 1]; bestP = P1[p - 1]; bestI = i;
+        }
+        double *t;
+        t = F0; F0 = F1; F1 = t;
+        t = M0; M0 = M1; M1 = t;
+        t = P0; P0 = P1; P1 = t;
+    }
+    free(F0); free(F1); free(M0); free(M1); free(P0); free(P1);
+    out[0] = bestJ; out[1] = bestM; out[2] = bestP; out[3] = bestI; out[4] = (double)R.cells;
+    return 0;
+}
+
+/* Traceback through stored argmins (cross-check for Hirschberg). */
+void orc_traceback(const int32_t *bp, int64_t p, int32_t t, int32_t *chain)
+{
+    chain[t - 1] = (int32_t)(p - 1);
+    for (int32_t i = t; i >= 3; i--)
+        chain[i - 2] = bp[(int64_t)i * p + chain[i - 1]];
+    chain[0] = 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Hirschberg recovery (Sec. 5, specialised from Sec. 4.2): find the best chain
+ * lo = u_0 < ... < u_{n-1} = hi by a forward half-DP over r+1 values from lo,
+ * a backward half-DP over n-r values to hi, a split at the lowest m minimising
+ * Fw[m] + Bw[m], and recursion on both halves.  r = floor((n-1)/2).            */
+
+static int64_t g_hb_cells;
+
+static void hb_forward(const hist_t *H, double lamp, int64_t lo, int64_t hi, int n, int q_end,
+                       double *F /* indexed by j - lo */)
+{
+    int64_t len = hi - lo + 1;
+    double *G = malloc(sizeof(double) * len);
+    for (int64_t x = 0; x < len; x++) F[x] = INFINITY;
+    F[0] = 0.0;
+    for (int q = 2; q <= q_end; q++) {
+        int64_t jl = lo + q - 1, jh = hi - (n - q);
+        int64_t kl = lo + q - 2;
+        for (int64_t x = 0; x < len; x++) G[x] = INFINITY;
+#pragma omp parallel for schedule(dynamic, 64)
+        for (int64_t j = jl; j <= jh; j++) {
+            double best = INFINITY;
+            for (int64_t k = kl; k < j; k++) {
+                double C, P;
+                cell_terms(H, k, j, &C, &P);
+                double cand = fma(-lamp, P, F[k - lo] + C);
+                if (cand < best) best = cand;
+            }
+            G[j - lo] = best;
+        }
+        for (int64_t j = jl; j <= jh; j++) g_hb_cells += j - kl;
+        memcpy(F, G, sizeof(double) * len);
+    }
+    free(G);
+}
+
+static void hb_backward(const hist_t *H, double lamp, int64_t lo, int64_t hi, int n, int q_end,
+                        double *B /* indexed by j - lo */)
+{
+    int64_t len = hi - lo + 1;
+    double *G = malloc(sizeof(double) * len);
+    for (int64_t x = 0; x < len; x++) B[x] = INFINITY;
+    B[len - 1] = 0.0;
+    for (int q = 2; q <= q_end; q++) {
+        int64_t jl = lo + (n - q), jh = hi - q + 1;
+        int64_t kh = hi - q + 2;
+        for (int64_t x = 0; x < len; x++) G[x] = INFINITY;
+#pragma omp parallel for schedule(dynamic, 64)
+        for (int64_t j = jl; j <= jh; j++) {
+            double best = INFINITY;
+            for (int64_t k = j + 1; k <= kh; k++) {
+                double C, P;
+                cell_terms(H, j, k, &C, &P);
+                double cand = fma(-lamp, P, B[k - lo] + C);
+                if (cand < best) best = cand;
+            }
+            G[j - lo] = best;
+        }
+        for (int64_t j = jl; j <= jh; j++) g_hb_cells += kh - j;
+        memcpy(B, G, sizeof(double) * len);
+    }
+    free(G);
+}
+
+static void hb_solve(const hist_t *H, double lamp, int64_t lo, int64_t hi, int n, int32_t *out)
+{
+    if (n == 2) { out[0] = (int32_t)lo; out[1] = (int32_t)hi; return; }
+    if (hi - lo + 1 == n) {
+        for (int x = 0; x < n; x++) out[x] = (int32_t)(lo + x);
+        return;
+    }
+    int r = (n - 1) / 2;
+    int64_t len = hi - lo + 1;
+    double *Fw = malloc(sizeof(double) * len), *Bw = malloc(sizeof(double) * len);
+    hb_forward(H, lamp, lo, hi, n, r + 1, Fw);
+    hb_backward(H, lamp, lo, hi, n, n - r, Bw);
+    int64_t m = -1;
+    double best = INFINITY;
+    for (int64_t x = lo + r; x <= hi - (n - 1 - r); x++) {
+        double tot = Fw[x - lo] + Bw[x - lo];
+        if (tot < best) { best = tot; m = x; }
+    }
+    free(Fw); free(Bw);
+    hb_solve(H, lamp, lo, m, r + 1, out);
+    hb_solve(H, lamp, m, hi, n - r, out + r);
+}
+
+int orc_hirschberg(const double *v, const double *N, const double *S, const double *S2,
+                   int64_t p, int64_t d, int32_t t, double lamp, int32_t *chain, int64_t *cells)
+{
+    hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
+    g_hb_cells = 0;
+    if (t == 1) { chain[0] = 0; if (cells) *cells = 0; return 0; }
+    hb_solve(&H, lamp, 0, p - 1, t, chain);
+    if (cells) *cells = g_hb_cells;
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Metrics of a chain of unique indices u_0 = 0 < ... < u_{t-1} = p-1.        */
+
+/* Expected frequency of every value (Sec. 4: f = U[k,l] + D[l,j]; the first
+ * value also takes every entry equal to it, the last takes the round-up mass
+ * of the last interval). */
+static void chain_freqs(const hist_t *H, int32_t t, const int32_t *u, double *f)
+{
+    if (t == 1) { f[0] = H->dd; return; }
+    double Uprev = 0;
+    for (int32_t r = 0; r < t; r++) {
+        double Ur = 0, Dr = 0;
+        if (r + 1 < t) interval_ud(H, u[r], u[r + 1], &Ur, &Dr);
+        if (r == 0) f[0] = H->c0 + Dr;
+        else if (r == t - 1) f[r] = Uprev;
+        else f[r] = Uprev + Dr;
+        Uprev = Ur;
+    }
+}
+
+static double chain_hout(const hist_t *H, int32_t t, const int32_t *u)
+{
+    double *f = malloc(sizeof(double) * t);
+    chain_freqs(H, t, u, f);
+    double Hs = 0.0;
+    for (int32_t r = 0; r < t; r++) Hs = Hs + hf(H, f[r]);
+    free(f);
+    return Hs;
+}
+
+/* out: mse, vnmse, H(Xhat), H(I,B), J = vNMSE + lambda*H(Xhat), R_tot */
+void orc_chain_metrics(const double *v, const double *N, const double *S, const double *S2,
+                       int64_t p, int64_t d, int32_t t, const int32_t *u, double lam, double *out)
+{
+    hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
+    double mse = 0.0, hs = 0.0;
+    for (int32_t r = 0; r + 1 < t; r++) {
+        double C, P;
+        cell_terms(&H, u[r], u[r + 1], &C, &P);
+        mse = mse + C;
+        hs = hs - P;
+    }
+    double ho = chain_hout(&H, t, u);
+    double vn = H.s2tot > 0 ? mse / H.s2tot : 0.0;
+    double lr = isfinite(lam) ? lam : 0.0;
+    out[0] = mse;
+    out[1] = vn;
+    out[2] = ho;
+    out[3] = hs;
+    out[4] = fma(lr, ho, vn);
+    out[5] = ho + (32.0 * (double)t) / H.dd;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Three-colour refinement (Sec. 6).                                           */
+
+/* Local objective of moving u_r to m with u_{r-1}, u_{r+1} (and u_{r-2},
+ * u_{r+2}) fixed: the two interval MSEs plus lambda' times the entropy terms of
+ * the three values whose expected frequencies change. */
+static double refine_local(const hist_t *H, int32_t t, const int32_t *u, int32_t r, int64_t m,
+                           double lamp)
+{
+    int64_t L = u[r - 1], R = u[r + 1];
+    double Cl = interval_c(H, L, m), Cr = interval_c(H, m, R);
+    double Ulm, Dlm, Umr, Dmr;
+    interval_ud(H, L, m, &Ulm, &Dlm);
+    interval_ud(H, m, R, &Umr, &Dmr);
+    double fprev, fnext;
+    if (r - 1 == 0) {
+        fprev = H->c0 + Dlm;
+    } else {
+        double Ua, Da;
+        interval_ud(H, u[r - 2], L, &Ua, &Da);
+        fprev = Ua + Dlm;
+    }
+    double fcur = Ulm + Dmr;
+    if (r + 1 == t - 1) {
+        fnext = Umr;
+    } else {
+        double Ub, Db;
+        interval_ud(H, R, u[r + 2], &Ub, &Db);
+        fnext = Umr + Db;
+    }
+    double Hl = (hf(H, fprev) + hf(H, fcur)) + hf(H, fnext);
+    return fma(lamp, Hl, Cl + Cr);
+}
+
+/* Refines u in place.  Returns the number of rounds run.  In budget mode a
+ * colour substep whose result has H(Xhat) > b is undone. */
+int orc_refine(const double *v, const double *N, const double *S, const double *S2, int64_t p,
+               int64_t d, int32_t t, int32_t *u, double lamp, double b, int32_t budget_mode,
+               int32_t rounds, int32_t exhaustive, int32_t *moves_out)
+{
+    hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
+    int32_t nrun = 0, nmoves = 0;
+    if (t < 3) { if (moves_out) *moves_out = 0; return 0; }
+    int32_t *nu = malloc(sizeof(int32_t) * t);
+    for (int32_t rd = 0; rd < rounds; rd++) {
+        int any = 0;
+        for (int32_t c = 0; c < 3; c++) {
+            memcpy(nu, u, sizeof(int32_t) * t);
+            int moved = 0;
+            for (int32_t r = 1; r <= t - 2; r++) {
+                if (r % 3 != c) continue;
+                int64_t L = u[r - 1], R = u[r + 1];
+                if (R - L < 3) continue; /* the open range holds u_r only */
+                int64_t m;
+                if (exhaustive) {
+                    double bv = INFINITY;
+                    m = -1;
+                    for (int64_t x = L + 1; x < R; x++) {
+                        double val = refine_local(&H, t, u, r, x, lamp);
+                        if (val < bv) { bv = val; m = x; }
+                    }
+                } else {
+                    int64_t lo = L + 1, hi = R - 1;
+                    while (lo < hi) {
+                        int64_t mid = lo + (hi - lo) / 2;
+                        if (refine_local(&H, t, u, r, mid + 1, lamp) <
+                            refine_local(&H, t, u, r, mid, lamp))
+                            lo = mid + 1;
+                        else
+                            hi = mid;
+                    }
+                    m = lo;
+                }
+                if (m != u[r] &&
+                    refine_local(&H, t, u, r, m, lamp) < refine_local(&H, t, u, r, u[r], lamp)) {
+                    nu[r] = (int32_t)m;
+                    moved++;
+                }
+            }
+            if (moved && budget_mode && chain_hout(&H, t, nu) > b)
+                moved = 0;
+            if (moved) {
+                memcpy(u, nu, sizeof(int32_t) * t);
+                any = 1;
+                nmoves += moved;
+            }
+        }
+        nrun++;
+        if (!any) break;
+    }
+    free(nu);
+    if (moves_out) *moves_out = nmoves;
+    return nrun;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Lambda search for a budget b (Sec. 3: binary search on lambda; Sec. 5: keep
+ * the lowest-MSE solution with H(I,B) <= b).  The search is a slope (chord)
+ * query between an infeasible point A and a feasible point B, as used for the
+ * frontier in App. F.7.  lambda is in vNMSE units; the DP uses
+ * lambda' = RN(lambda * ||X||^2).
+ *
+ * traj (optional, 4 doubles per solve): lambda, H(I,B), vNMSE, t.
+ * out: lambda_B, H_B, M_B, t_B, solves, cells, status (0 ok, -3 infeasible),
+ *      closed_form (1 if B is {v_0, v_{p-1}} from the closed form)
+ */
+int orc_search(const double *v, const double *N, const double *S, const double *S2, int64_t p,
+               int64_t d, int32_t s, double b, int32_t exact_s, int32_t max_iters, double *traj,
+               int32_t traj_cap, double *out)
+{
+    hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
+    double r[5];
+    int32_t nsol = 0;
+    double cells = 0;
+    double A_l, A_h, A_m, B_l, B_h, B_m;
+    int32_t A_t, B_t, closed = 0, status = 0;
+#define SOLVE(lam_, l_, h_, m_, t_)                                                           \
+    do {                                                                                      \
+        double lp_ = (lam_) * H.s2tot;                                                        \
+        orc_dp_forward(v, N, S, S2, p, d, s, exact_s, lp_, r, NULL, NULL, NULL);              \
+        l_ = (lam_); h_ = r[2]; m_ = r[1] / H.s2tot; t_ = (int32_t)r[3]; cells += r[4];       \
+        if (traj && nsol < traj_cap) {                                                        \
+            traj[4 * nsol] = l_; traj[4 * nsol + 1] = h_; traj[4 * nsol + 2] = m_;           \
+            traj[4 * nsol + 3] = t_;                                                          \
+        }                                                                                     \
+        nsol++;                                                                               \
+    } while (0)
+
+    if (p <= 2) {
+        /* every value is used; nothing to search */
+        out[0] = 0.0; out[1] = 0.0; out[2] = 0.0; out[3] = (double)p; out[4] = 0; out[5] = 0;
+        out[6] = 0; out[7] = 0;
+        if (p == 2) {
+            double C, P;
+            cell_terms(&H, 0, 1, &C, &P);
+            out[1] = 0.0 - P;
+            out[2] = (0.0 + C) / H.s2tot;
+            if (out[1] > b) out[6] = -3;
+        }
+        return 0;
+    }
+    SOLVE(0.0, A_l, A_h, A_m, A_t);
+    if (A_h <= b) {
+        out[0] = A_l; out[1] = A_h; out[2] = A_m; out[3] = A_t; out[4] = nsol; out[5] = cells;
+        out[6] = 0; out[7] = 0;
+        return 0;
+    }
+    if (b >= 1.0) {
+        double C, P;
+        cell_terms(&H, 0, p - 1, &C, &P);
+        B_l = INFINITY; B_h = 0.0 - P; B_m = (0.0 + C) / H.s2tot; B_t = 2; closed = 1;
+    } else {
+        SOLVE(0x1p40, B_l, B_h, B_m, B_t);
+        if (B_h > b) {
+            out[0] = B_l; out[1] = B_h; out[2] = B_m; out[3] = B_t; out[4] = nsol; out[5] = cells;
+            out[6] = -3; out[7] = 0;
+            return 0;
+        }
+    }
+    for (int32_t it = 0; it < max_iters; it++) {
+        double lc = (B_m - A_m) / (A_h - B_h);
+        if (!(lc > 0.0)) break;
+        double C_l, C_h, C_m;
+        int32_t C_t;
+        SOLVE(lc, C_l, C_h, C_m, C_t);
+        if ((C_h == A_h && C_m == A_m) || (C_h == B_h && C_m == B_m))
+            break;
+        if (C_h > b) { A_l = C_l; A_h = C_h; A_m = C_m; A_t = C_t; }
+        else { B_l = C_l; B_h = C_h; B_m = C_m; B_t = C_t; closed = 0; }
+    }
+#undef SOLVE
+    out[0] = B_l; out[1] = B_h; out[2] = B_m; out[3] = B_t; out[4] = nsol; out[5] = cells;
+    out[6] = status; out[7] = closed;
+    return 0;
+}

@@ -1,0 +1,259 @@
+"""Oracle pipeline: histogram, exact prefix sums, search, recovery, refinement,
+final stochastic rounding.
+
+TEST INFRASTRUCTURE ONLY.  Plain Python/numpy for the O(d) steps, the C oracle
+(native.py) for the O(s p^2) dynamic programs.
+
+Paper references (arXiv 2608.18147):
+  weighted histogram of the sorted input       Sec. 2 (sorting, duplicates)
+  prefix sums N, S, S2 and closed forms        App. D
+  budget search on lambda                      Sec. 3 and Sec. 5 (lambda tuning)
+  Hirschberg recovery                          Sec. 5 / Sec. 4.2
+  three-colour refinement                      Sec. 6
+  SQ rounding                                  Sec. 2
+"""
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+from . import native
+from .philox import philox4x32_10
+
+F32_LSB_EXP = 149  # every float32 is an integer multiple of 2^-149
+
+
+def histogram(x):
+    """Sorted distinct values and their counts.  -0 is folded into +0.
+
+    x: any float array whose values are exact in float32 (f32/f16/bf16)."""
+    xf = np.asarray(x).astype(np.float64).ravel()
+    if not np.all(np.isfinite(xf)):
+        raise ValueError("non-finite input")
+    xf = xf + 0.0
+    v, c = np.unique(xf, return_counts=True)
+    return v, c.astype(np.int64)
+
+
+def exact_prefix(v, c):
+    """Inclusive prefix sums N, S = sum c v, S2 = sum c v^2, each the correctly
+    rounded fp64 value of the exact sum (App. D prefix quantities).
+
+    Exactness: every value is K * 2^-149 with integer K, so the sums are exact
+    Python integers; int -> float conversion rounds to nearest even and the
+    power-of-two rescale is exact."""
+    p = len(v)
+    N = np.empty(p)
+    S = np.empty(p)
+    S2 = np.empty(p)
+    scale = 1 << F32_LSB_EXP
+    acc_n = acc_s = acc_s2 = 0
+    for k in range(p):
+        num, den = float(v[k]).as_integer_ratio()
+        K = num * (scale // den)
+        ck = int(c[k])
+        acc_n += ck
+        acc_s += ck * K
+        acc_s2 += ck * K * K
+        N[k] = float(acc_n)
+        S[k] = math.ldexp(float(acc_s), -F32_LSB_EXP)
+        S2[k] = math.ldexp(float(acc_s2), -2 * F32_LSB_EXP)
+    return N, S, S2
+
+
+@dataclass
+class Hist:
+    v: np.ndarray
+    c: np.ndarray
+    N: np.ndarray
+    S: np.ndarray
+    S2: np.ndarray
+    d: int
+
+    @property
+    def p(self):
+        return len(self.v)
+
+    @property
+    def s2tot(self):
+        return float(self.S2[-1])
+
+    def args(self):
+        return (native.dptr(self.v), native.dptr(self.N), native.dptr(self.S),
+                native.dptr(self.S2), self.p, self.d)
+
+
+def prepare(x):
+    v, c = histogram(x)
+    N, S, S2 = exact_prefix(v, c)
+    return Hist(np.ascontiguousarray(v), c, N, S, S2, int(np.asarray(x).size))
+
+
+def interval(H, a, b):
+    """(C, U, D, P) of (v_a, v_b] in the canonical arithmetic."""
+    out = np.zeros(4)
+    native.lib().orc_interval(*H.args(), a, b, native.dptr(out))
+    return tuple(out)
+
+
+def dp_forward(H, s, lamp, exact_s=False, backpointers=False, dump=False):
+    """One approximate-DP solve at lambda' (MSE units).  Returns dict."""
+    L = native.lib()
+    out = np.zeros(5)
+    bp = np.zeros((s + 1) * H.p, dtype=np.int32) if backpointers else None
+    fd = np.full((s + 1) * H.p, np.inf) if dump else None
+    lastF = np.full(s + 1, np.inf)
+    L.orc_dp_forward(*H.args(), s, int(exact_s), lamp, native.dptr(out),
+                     native.iptr(bp) if bp is not None else None,
+                     native.dptr(fd) if fd is not None else None, native.dptr(lastF))
+    r = dict(J=out[0], mse=out[1], phi=out[2], t=int(out[3]), cells=int(out[4]), lastF=lastF)
+    if bp is not None:
+        r["bp"] = bp.reshape(s + 1, H.p)
+        chain = np.zeros(r["t"], dtype=np.int32)
+        L.orc_traceback(native.iptr(bp), H.p, r["t"], native.iptr(chain))
+        r["chain_bp"] = chain
+    if fd is not None:
+        r["F"] = fd.reshape(s + 1, H.p)
+    return r
+
+
+def hirschberg(H, t, lamp):
+    chain = np.zeros(t, dtype=np.int32)
+    import ctypes
+    cells = ctypes.c_int64(0)
+    native.lib().orc_hirschberg(*H.args(), t, lamp, native.iptr(chain), ctypes.byref(cells))
+    return chain, int(cells.value)
+
+
+def chain_metrics(H, chain, lam):
+    out = np.zeros(6)
+    chain = np.ascontiguousarray(chain, dtype=np.int32)
+    native.lib().orc_chain_metrics(*H.args(), len(chain), native.iptr(chain), lam,
+                                   native.dptr(out))
+    return dict(mse=out[0], vnmse=out[1], entropy=out[2], entropy_surrogate=out[3],
+                objective=out[4], rate_total=out[5])
+
+
+def refine(H, chain, lamp, b=math.inf, budget=False, rounds=5, exhaustive=False):
+    import ctypes
+    u = np.ascontiguousarray(chain, dtype=np.int32).copy()
+    moves = ctypes.c_int32(0)
+    n = native.lib().orc_refine(*H.args(), len(u), native.iptr(u), lamp, b, int(budget), rounds,
+                                int(exhaustive), ctypes.byref(moves))
+    return u, int(n), int(moves.value)
+
+
+def search(H, s, b, exact_s=False, max_iters=64):
+    out = np.zeros(8)
+    cap = 256
+    traj = np.zeros(4 * cap)
+    native.lib().orc_search(*H.args(), s, b, int(exact_s), max_iters, native.dptr(traj), cap,
+                            native.dptr(out))
+    n = int(out[4])
+    return dict(lam=out[0], H=out[1], M=out[2], t=int(out[3]), solves=n, cells=int(out[5]),
+                status=int(out[6]), traj=traj[: 4 * min(n, cap)].reshape(-1, 4))
+
+
+@dataclass
+class Result:
+    codebook: np.ndarray
+    rank: np.ndarray
+    t: int
+    p: int
+    lam: float
+    mse: float
+    vnmse: float
+    entropy: float
+    entropy_surrogate: float
+    objective: float
+    rate_total: float
+    dp_solves: int
+    refine_rounds: int
+    cells: int
+    status: int
+    traj: np.ndarray = field(default=None)
+
+
+def _finish(H, chain, lam, solves, rounds, cells, status, traj=None):
+    m = chain_metrics(H, chain, lam)
+    return Result(codebook=H.v[chain].copy(), rank=np.asarray(chain, dtype=np.int32), t=len(chain),
+                  p=H.p, lam=lam, mse=m["mse"], vnmse=m["vnmse"], entropy=m["entropy"],
+                  entropy_surrogate=m["entropy_surrogate"], objective=m["objective"],
+                  rate_total=m["rate_total"], dp_solves=solves, refine_rounds=rounds,
+                  cells=cells, status=status, traj=traj)
+
+
+def _recover(H, t, lam):
+    """Codebook (unique indices) with t values at lambda (vNMSE units)."""
+    if H.p == 1:
+        return np.zeros(1, dtype=np.int32), 0
+    if t == 2 or not math.isfinite(lam):
+        return np.array([0, H.p - 1], dtype=np.int32), 0
+    return hirschberg(H, t, lam * H.s2tot)
+
+
+def solve(x, s, b, refine_rounds=5, exhaustive=False, exact_s=False, max_iters=64):
+    """Budget mode: the lowest-MSE supported solution with H(I,B) <= b, then
+    refinement at its multiplier with the budget guard on H(Xhat)."""
+    H = prepare(x)
+    sr = search(H, s, b, exact_s, max_iters)
+    chain, hcells = _recover(H, sr["t"], sr["lam"])
+    rounds = 0
+    if refine_rounds > 0 and math.isfinite(sr["lam"]) and len(chain) >= 3:
+        chain, rounds, _ = refine(H, chain, sr["lam"] * H.s2tot, b, True, refine_rounds,
+                                  exhaustive)
+    return _finish(H, chain, sr["lam"], sr["solves"], rounds, sr["cells"] + hcells,
+                   sr["status"], sr["traj"])
+
+
+def solve_lagrangian(x, s, lam, refine_rounds=0, exhaustive=False, exact_s=False):
+    """Fixed-multiplier mode: min vNMSE + lambda H(I,B), then refinement on
+    vNMSE + lambda H(Xhat) without a budget guard."""
+    H = prepare(x)
+    if H.p == 1:
+        return _finish(H, np.zeros(1, dtype=np.int32), lam, 0, 0, 0, 0)
+    r = dp_forward(H, s, lam * H.s2tot, exact_s)
+    chain, hcells = _recover(H, r["t"], lam)
+    rounds = 0
+    if refine_rounds > 0 and len(chain) >= 3:
+        chain, rounds, _ = refine(H, chain, lam * H.s2tot, math.inf, False, refine_rounds,
+                                  exhaustive)
+    return _finish(H, chain, lam, 1, rounds, r["cells"] + hcells, 0)
+
+
+def uniforms(n, seed):
+    """u_i in [0,1): 53 bits of Philox4x32-10(counter=(i_lo, i_hi, 0, 0),
+    key=(seed_lo, seed_hi)), words 0 and 1."""
+    i = np.arange(n, dtype=np.uint64)
+    c0 = (i & np.uint64(0xFFFFFFFF)).astype(np.uint64)
+    c1 = (i >> np.uint64(32)).astype(np.uint64)
+    z = np.zeros(n, dtype=np.uint64)
+    k0 = np.full(n, seed & 0xFFFFFFFF, dtype=np.uint64)
+    k1 = np.full(n, (seed >> 32) & 0xFFFFFFFF, dtype=np.uint64)
+    w0, w1, _, _ = philox4x32_10(c0, c1, z, z, k0, k1)
+    bits = ((w1 << np.uint64(32)) | w0) >> np.uint64(11)
+    return bits.astype(np.float64) * 2.0 ** -53
+
+
+def quantize(x, codebook, seed):
+    """Unbiased SQ of every entry in its original order (Sec. 2): bracket
+    q_r < x <= q_{r+1} (x <= q_0 maps to r = 0), round up iff u < (x-q_r)/(q_{r+1}-q_r).
+    Returns (symbols uint8, histogram int64, plug-in entropy of the symbols)."""
+    xf = np.asarray(x).astype(np.float64).ravel() + 0.0
+    q = np.asarray(codebook, dtype=np.float64)
+    t = len(q)
+    n = len(xf)
+    if t == 1:
+        sym = np.zeros(n, dtype=np.uint8)
+    else:
+        r = np.clip(np.searchsorted(q, xf, side="left") - 1, 0, t - 2)
+        pu = (xf - q[r]) / (q[r + 1] - q[r])
+        u = uniforms(n, seed)
+        sym = (r + (u < pu)).astype(np.uint8)
+    hist = np.bincount(sym, minlength=t).astype(np.int64)
+    ent = 0.0
+    for nq in hist:
+        if nq > 0:
+            y = nq / n
+            ent -= y * math.log2(y)
+    return sym, hist, ent

@@ -1,0 +1,475 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test names the passage it checks.  None of them compares the oracle with
+itself: the references are printed values (tests/golden), brute force over all
+codebooks, textbook recurrences, closed forms, exact rational arithmetic,
+mpmath, math.fsum and published Philox test vectors.
+"""
+import math
+from fractions import Fraction
+
+import mpmath
+import numpy as np
+import pytest
+
+from oracle import native, pipeline, plain
+from oracle.log2_table import build_table
+from oracle.philox import philox4x32_10
+from tests.conftest import golden
+
+
+def fr(s):
+    return Fraction(s)
+
+
+# --------------------------------------------------------------------------
+# Printed examples
+
+
+def test_worked_entropy_example():
+    """Sec. 3: X=<0,1,10>, Q={0,10} gives H ~ 0.948 bits/entry."""
+    g = golden("worked_example.txt")
+    x = [float(a) for a in g["x"].split()]
+    Q = [float(a) for a in g["Q"].split()]
+    Qs, f = plain.freqs(x, Q)
+    assert [fq / len(x) for fq in f] == [fr(a) for a in g["f_over_d"].split()]
+    H = plain.entropy_out(x, Q)
+    assert round(H, int(g["H_out_digits"])) == float(g["H_out"])
+    assert plain.mse(x, Q) == 9
+    # the C oracle's closed forms give the same numbers
+    Hh = pipeline.prepare(np.array(x, dtype=np.float32))
+    m = pipeline.chain_metrics(Hh, np.array([0, 2], dtype=np.int32), 0.0)
+    assert m["mse"] == 9.0
+    assert abs(m["entropy"] - H) < 1e-15
+    # one interval: the surrogate equals the true entropy
+    assert abs(m["entropy_surrogate"] - H) < 1e-15
+    assert abs(m["vnmse"] - 9 / 101) < 1e-16
+
+
+def test_app_e1_quantizers_and_thresholds():
+    """App. E.1: table of A, B, C and the multiplier thresholds."""
+    g = golden("app_e1_lagrange.txt")
+    x = [0.0] * 4 + [2.0] * 4
+    dig = int(g["H_digits"])
+    for name in "ABC":
+        Q = [float(a) for a in g[name].split()]
+        _, f = plain.freqs(x, Q)
+        assert [fq / len(x) for fq in f] == [fr(a) for a in g[name + "_dist"].split()]
+        assert round(plain.entropy_out(x, Q), dig) == float(g[name + "_H"])
+        assert plain.vnmse(x, Q) == fr(g[name + "_vnmse"])
+    HA = plain.entropy_out(x, [0, 4])
+    HB = plain.entropy_out(x, [0, 3])
+    assert round(HB, 6) == float(g["B_H_6"]) and round(HA, 6) == float(g["A_H_6"])
+    lam_bc = 0.5 / (1 - HB)
+    lam_ba = 0.5 / (HB - HA)
+    assert lam_bc > float(g["B_over_C_lambda_above"])
+    assert lam_ba < float(g["B_over_A_lambda_below"])
+    # lambda is in vNMSE units: the crossings happen exactly there
+    J = lambda Q, lam: plain.objective(x, Q, lam, "out")
+    assert J([0, 3], lam_bc * 1.001) < J([0, 2], lam_bc * 1.001)
+    assert J([0, 3], lam_bc * 0.999) > J([0, 2], lam_bc * 0.999)
+    assert J([0, 3], lam_ba * 0.999) < J([0, 4], lam_ba * 0.999)
+    # no lambda makes B the Lagrangian optimum
+    for lam in np.linspace(0, 20, 401):
+        assert min(J([0, 4], lam), J([0, 2], lam)) <= J([0, 3], lam) + 1e-15
+    # time-sharing A and C at b = 0.95
+    b = float(g["b_ts"])
+    alpha = (b - HA) / (1 - HA)
+    dts = int(g["ts_digits"])
+    assert round(alpha, dts) == float(g["alpha_ts"])
+    assert round((1 - alpha) * 1.0, dts) == float(g["vnmse_ts"])
+
+
+def test_app_e2_nonadjacent_and_solvers():
+    """App. E.2: with 0,1,2 each d/3, s=3, b=3/2 the adjacent solution is {0,2}."""
+    g = golden("app_e2_nonadjacent.txt")
+    x = [0.0] * 3 + [1.0] * 3 + [2.0] * 3
+    assert abs(plain.entropy_out(x, [0, 1, 2]) - math.log2(3)) < 1e-15
+    _, f = plain.freqs(x, [0, 2])
+    assert [fq / len(x) for fq in f] == [fr(a) for a in g["Q2_dist"].split()]
+    assert plain.entropy_out(x, [0, 2]) == float(g["Q2_H"])
+    assert plain.vnmse(x, [0, 2]) == fr(g["Q2_vnmse"])
+    # the non-adjacent rule's entropy as printed
+    Hn = sum(plain.h(fr(a)) for a in g["nonadj_dist"].split())
+    assert round(Hn, int(g["nonadj_H_digits"])) == float(g["nonadj_H"])
+    alpha = (1.5 - 1) / (math.log2(3) - 1)
+    assert round(alpha, int(g["alpha_digits"])) == float(g["alpha"])
+    assert round((1 - alpha) / 5, int(g["ts_vnmse_digits"])) == float(g["ts_vnmse"])
+    # exact optimum and both of our solvers return {0, 2} at b = 3/2
+    s, b = int(g["s"]), float(g["b"])
+    m, Q = plain.brute_force_budget(x, s, b, "out")
+    assert Q == (0.0, 2.0) and m == 3.0
+    r = pipeline.solve(np.array(x, dtype=np.float32), s, b)
+    assert list(r.codebook) == [0.0, 2.0]
+    assert r.entropy == 1.0
+
+
+# --------------------------------------------------------------------------
+# Canonical log2, exact prefix sums
+
+
+def test_log2c_accuracy():
+    """The canonical log2 stays within 2.5 ulp of the true value (mpmath)."""
+    L = native.lib()
+    rng = np.random.default_rng(5)
+    ys = np.concatenate([rng.uniform(0, 1, 4000), 10 ** rng.uniform(-300, 300, 4000),
+                         1 + rng.uniform(-2e-2, 2e-2, 4000), 1 + rng.uniform(-1e-9, 1e-9, 500)])
+    mpmath.mp.prec = 120
+    worst = 0.0
+    for y in ys:
+        got = L.orc_log2c(float(y))
+        ref = mpmath.log(mpmath.mpf(float(y)), 2)
+        worst = max(worst, float(abs((mpmath.mpf(got) - ref) / math.ulp(float(ref)))))
+    assert worst <= 2.5
+    for k in range(-1000, 1000, 37):
+        assert L.orc_log2c(2.0 ** k) == k
+    assert L.orc_log2c(1.0) == 0.0
+
+
+def test_log2_table_correctly_rounded():
+    """Each table entry is the correctly rounded log2 (checked at 400 bits)."""
+    invc, lc = build_table()
+    mpmath.mp.prec = 400
+    for ic, l in zip(invc, lc):
+        exact = -mpmath.log(mpmath.mpf(ic), 2)
+        err = abs(mpmath.mpf(l) - exact)
+        assert err <= mpmath.mpf(math.ulp(l)) / 2
+
+
+def test_h_zero_and_negative():
+    """h(y) = 0 for y <= 0 and -y log2 y otherwise (Sec. 4)."""
+    L = native.lib()
+    assert L.orc_h(0.0) == 0.0 and L.orc_h(-1e-300) == 0.0 and L.orc_h(-3.0) == 0.0
+    assert L.orc_h(1.0) == 0.0
+    assert abs(L.orc_h(0.25) - 0.5) < 1e-16
+
+
+def test_exact_prefix_sums_against_fsum():
+    """S and S2 equal the correctly rounded exact sums (math.fsum is exact)."""
+    rng = np.random.default_rng(2)
+    x = np.concatenate([rng.standard_normal(300) * 10.0 ** rng.integers(-30, 30, 300),
+                        rng.standard_normal(50)]).astype(np.float32)
+    x = np.concatenate([x, x[:40]])  # duplicates
+    v, c = pipeline.histogram(x)
+    N, S, S2 = pipeline.exact_prefix(v, c)
+    for k in range(0, len(v), 7):
+        terms = [float(v[i]) for i in range(k + 1) for _ in range(int(c[i]))]
+        assert S[k] == math.fsum(terms)
+        assert S2[k] == math.fsum(float(Fraction(t) ** 2) for t in terms) or \
+            S2[k] == float(sum(Fraction(t) ** 2 for t in terms))
+        assert N[k] == len(terms)
+
+
+# --------------------------------------------------------------------------
+# Closed forms
+
+
+def test_unit_grid_closed_forms():
+    """X = 0..w with unit weights: C[0,w] = (w^3-w)/6, U = (w+1)/2, D = (w-1)/2
+    (App. D definitions of C_P, U_P, D_P on the half-open interval)."""
+    for w in (1, 2, 3, 7, 30, 100):
+        x = np.arange(w + 1, dtype=np.float32)
+        H = pipeline.prepare(x)
+        C, U, D, P = pipeline.interval(H, 0, w)
+        assert C == (w ** 3 - w) / 6
+        assert U == (w + 1) / 2 and D == (w - 1) / 2
+
+
+def test_s2_closed_form():
+    """s = 2 forces Q = {min, max}: MSE = sum (max-x)(x-min), H(I,B) = H(Xhat)."""
+    rng = np.random.default_rng(3)
+    for _ in range(5):
+        x = rng.standard_normal(200).astype(np.float32)
+        r = pipeline.solve_lagrangian(x, 2, 0.3)
+        xs = [Fraction(float(a)) for a in x]
+        lo, hi = min(xs), max(xs)
+        m = sum((hi - a) * (a - lo) for a in xs)
+        assert r.t == 2 and list(r.codebook) == [float(lo), float(hi)]
+        assert abs(r.mse - float(m)) <= 1e-12 * float(m)
+        assert abs(r.entropy - r.entropy_surrogate) < 1e-14
+        assert abs(r.entropy - plain.entropy_out(x, [float(lo), float(hi)])) < 1e-13
+
+
+def test_frequency_identity_and_expected_frequency():
+    """For unbiased SQ, MSE = sum_q f_q q^2 - ||X||^2 (App. E.3 lemma), and the
+    interior frequency is U[k,l] + D[l,j] with sum f = d (Sec. 4)."""
+    rng = np.random.default_rng(4)
+    x = np.round(rng.standard_normal(40) * 4).astype(np.float32)
+    v = sorted(set(float(a) for a in x))
+    Q = [v[0], v[3], v[7], v[-1]]
+    Qs, f = plain.freqs(x, Q)
+    assert sum(f) == len(x)
+    assert plain.mse(x, Q) == sum(fq * q * q for fq, q in zip(f, Qs)) - plain.norm2(x)
+    H = pipeline.prepare(x)
+    idx = [v.index(q) for q in Q]
+    _, U01, D01, _ = pipeline.interval(H, idx[0], idx[1])
+    _, U12, D12, _ = pipeline.interval(H, idx[1], idx[2])
+    assert abs((U01 + D12) - float(f[1])) < 1e-12
+
+
+def test_monotone_round_masses():
+    """U(k,l) is non-increasing in k and D(l,j) non-decreasing in j (App. B)."""
+    rng = np.random.default_rng(6)
+    x = rng.standard_normal(60).astype(np.float32)
+    H = pipeline.prepare(x)
+    l = 30
+    Us = [pipeline.interval(H, k, l)[1] for k in range(l)]
+    Ds = [pipeline.interval(H, l, j)[2] for j in range(l + 1, H.p)]
+    assert all(a >= b - 1e-12 for a, b in zip(Us, Us[1:]))
+    assert all(a <= b + 1e-12 for a, b in zip(Ds, Ds[1:]))
+
+
+# --------------------------------------------------------------------------
+# The DPs against brute force
+
+
+def _tiny_inputs(n, seed):
+    rng = np.random.default_rng(seed)
+    for _ in range(n):
+        d = int(rng.integers(2, 11))
+        if rng.random() < 0.5:
+            x = rng.integers(-5, 6, size=d).astype(np.float32) * np.float32(rng.choice([0.5, 1, 3]))
+        else:
+            x = rng.standard_normal(d).astype(np.float32)
+        s = int(rng.integers(2, 6))
+        lam = 0.0 if rng.random() < 0.15 else float(10 ** rng.uniform(-3, 1))
+        if np.all(x == 0) or len(set(x.tolist())) < 2:
+            continue
+        yield x, s, lam
+
+
+def test_apx_dp_equals_brute_force():
+    """eq. apx_base/apx_rec/apx_final minimise vNMSE + lambda H(I,B) over all
+    spanning Q with |Q| <= s; Hirschberg and the backpointer traceback recover a
+    minimiser."""
+    for x, s, lam in _tiny_inputs(120, 11):
+        H = pipeline.prepare(x)
+        r = pipeline.dp_forward(H, s, lam * H.s2tot, backpointers=True)
+        Jb, _ = plain.brute_force(x, s, lam, "sur")
+        assert abs(r["J"] / H.s2tot - Jb) <= 1e-12 * max(1.0, Jb)
+        ch, _ = pipeline.hirschberg(H, r["t"], lam * H.s2tot)
+        m = pipeline.chain_metrics(H, ch, lam)
+        assert abs(m["vnmse"] + lam * m["entropy_surrogate"] - Jb) <= 1e-12 * max(1.0, Jb)
+        assert list(ch) == list(r["chain_bp"])
+        # carried accumulators describe the chosen path
+        assert abs(r["mse"] - m["mse"]) <= 1e-12 * max(1.0, m["mse"])
+        assert abs(r["phi"] - m["entropy_surrogate"]) <= 1e-12
+
+
+def test_optimal_dp_equals_brute_force_and_sandwich():
+    """Sec. 4 optimal DP = brute-force min of vNMSE + lambda H(Xhat); and
+    J_opt <= J_apx <= J_opt + lambda (from H(Xhat) <= H(I,B) <= H(Xhat)+1)."""
+    for x, s, lam in _tiny_inputs(80, 12):
+        Jo, _ = plain.optimal_dp(x, s, lam)
+        Jbo, _ = plain.brute_force(x, s, lam, "out")
+        assert abs(Jo - Jbo) <= 1e-12 * max(1.0, Jbo)
+        H = pipeline.prepare(x)
+        Ja = pipeline.dp_forward(H, s, lam * H.s2tot)["J"] / H.s2tot
+        assert Jbo <= Ja + 1e-12 and Ja <= Jbo + lam + 1e-12
+
+
+def test_entropy_sandwich_per_codebook():
+    """eq. apx_entropy_sandwich: H(Xhat) <= H(I,B) <= H(Xhat) + 1 for every Q."""
+    rng = np.random.default_rng(7)
+    for _ in range(40):
+        x = rng.integers(-4, 5, size=int(rng.integers(2, 12))).astype(np.float32)
+        for Q in list(plain.spanning_codebooks(x, 5))[:20]:
+            a, b = plain.entropy_out(x, Q), plain.entropy_surrogate(x, Q)
+            assert a <= b + 1e-12 and b <= a + 1 + 1e-12
+
+
+def test_lambda_zero_is_asq():
+    """lambda = 0 reduces to ASQ (Sec. 3): the approx DP equals the textbook
+    DP eq. (1) and the brute-force minimum MSE."""
+    for x, s, _ in _tiny_inputs(60, 13):
+        H = pipeline.prepare(x)
+        r = pipeline.dp_forward(H, s, 0.0)
+        a = plain.asq_dp(x, s)
+        bf = min(plain.mse(x, Q) for Q in plain.spanning_codebooks(x, s))
+        assert a == bf
+        assert abs(r["J"] - float(a)) <= 1e-12 * max(1.0, float(a)) + 1e-13 * H.s2tot
+
+
+def test_lemma4_on_brute_force():
+    """Lemma 4: the minimum-MSE Q with H(I,B) <= b has H(Xhat) <= b and MSE no
+    larger than OPT(b - 1)."""
+    rng = np.random.default_rng(8)
+    for _ in range(25):
+        x = rng.integers(-5, 6, size=int(rng.integers(4, 10))).astype(np.float32)
+        if len(set(x.tolist())) < 3:
+            continue
+        for b in (1.2, 1.6, 2.0, 2.5):
+            m_apx, Q = plain.brute_force_budget(x, 5, b, "sur")
+            if Q is None:
+                continue
+            assert plain.entropy_out(x, Q) <= b + 1e-12
+            m_opt, _ = plain.brute_force_budget(x, 5, b - 1, "out")
+            assert m_apx <= m_opt + 1e-9
+
+
+def test_mse_monotone_in_s_and_b():
+    """The exact constrained optimum is non-increasing in s and in b; the
+    budget solver's MSE is non-increasing in b (it returns hull vertices)."""
+    rng = np.random.default_rng(9)
+    x = rng.integers(-6, 7, size=9).astype(np.float32)
+    prev = math.inf
+    for s in (2, 3, 4, 5):
+        m, _ = plain.brute_force_budget(x, s, 2.0, "out")
+        assert m <= prev + 1e-12
+        prev = m
+    prev = math.inf
+    for b in (1.0, 1.5, 2.0, 2.5, 3.0):
+        m, _ = plain.brute_force_budget(x, 5, b, "out")
+        assert m <= prev + 1e-12
+        prev = m
+    y = np.random.default_rng(10).standard_normal(400).astype(np.float32)
+    prev = math.inf
+    for b in (1.0, 1.5, 2.0, 2.5, 3.0, 3.5):
+        r = pipeline.solve(y, 12, b, refine_rounds=0)
+        assert r.entropy_surrogate <= b
+        assert r.mse <= prev * (1 + 1e-12)
+        prev = r.mse
+
+
+# --------------------------------------------------------------------------
+# Search, recovery, refinement
+
+
+def test_search_matches_dense_lambda_grid():
+    """The slope search returns the best feasible supported point: among DP
+    solutions over a dense lambda grid, none with H(I,B) <= b has lower vNMSE."""
+    rng = np.random.default_rng(14)
+    x = rng.standard_normal(120).astype(np.float32)
+    s = 8
+    H = pipeline.prepare(x)
+    pts = []
+    for lam in np.concatenate([[0.0], np.logspace(-4, 2, 1500)]):
+        r = pipeline.dp_forward(H, s, lam * H.s2tot)
+        pts.append((r["phi"], r["mse"] / H.s2tot))
+    for b in (1.3, 1.8, 2.2, 2.9):
+        sr = pipeline.search(H, s, b)
+        assert sr["H"] <= b
+        best = min(m for hh, m in pts if hh <= b)
+        assert sr["M"] <= best * (1 + 1e-12)
+
+
+def test_hirschberg_matches_backpointers_at_scale():
+    """Hirschberg recovery (Sec. 5) equals the stored-argmin traceback and its
+    recomputed cost equals the DP optimum."""
+    rng = np.random.default_rng(15)
+    for d, s, lam in ((700, 12, 0.05), (1500, 20, 0.01), (900, 7, 0.0)):
+        x = rng.standard_normal(d).astype(np.float32)
+        H = pipeline.prepare(x)
+        r = pipeline.dp_forward(H, s, lam * H.s2tot, backpointers=True)
+        ch, _ = pipeline.hirschberg(H, r["t"], lam * H.s2tot)
+        assert list(ch) == list(r["chain_bp"])
+        m = pipeline.chain_metrics(H, ch, lam)
+        J = m["mse"] + lam * H.s2tot * m["entropy_surrogate"]
+        assert abs(J - r["J"]) <= 1e-12 * abs(r["J"])
+
+
+def test_refinement_never_worsens_and_colours_separate():
+    """Sec. 6: each committed colour substep lowers vNMSE + lambda H(Xhat);
+    moves inside one colour class are independent (their objective changes add
+    up exactly), which is what allows updating them in parallel."""
+    rng = np.random.default_rng(16)
+    x = np.round(rng.standard_normal(300) * 8).astype(np.float32)
+    lam = 0.02
+    H = pipeline.prepare(x)
+    r = pipeline.dp_forward(H, 10, lam * H.s2tot, backpointers=True)
+    chain = r["chain_bp"]
+    base = pipeline.chain_metrics(H, chain, lam)["objective"]
+    for rounds in (1, 2, 5):
+        u, _, _ = pipeline.refine(H, chain, lam * H.s2tot, rounds=rounds)
+        assert pipeline.chain_metrics(H, u, lam)["objective"] <= base + 1e-15
+    # additivity, checked with the plain (exact-frequency) objective
+    xs = [float(a) for a in x]
+    vals = [float(a) for a in H.v]
+    Q0 = [vals[k] for k in chain]
+    J0 = plain.objective(xs, Q0, lam, "out")
+    t = len(chain)
+    for c in range(3):
+        movers = [r_ for r_ in range(1, t - 1) if r_ % 3 == c]
+        deltas, newQ = [], list(Q0)
+        for r_ in movers:
+            lo, hi = chain[r_ - 1], chain[r_ + 1]
+            if hi - lo < 3:
+                continue
+            m = lo + 1 if chain[r_] != lo + 1 else lo + 2
+            Q1 = list(Q0)
+            Q1[r_] = vals[m]
+            deltas.append(plain.objective(xs, Q1, lam, "out") - J0)
+            newQ[r_] = vals[m]
+        Jall = plain.objective(xs, newQ, lam, "out")
+        assert abs((Jall - J0) - sum(deltas)) < 1e-12
+
+
+def test_refinement_two_colours_would_not_separate():
+    """Why three colours: moving q_r and q_{r+2} together changes f_{r+1}
+    through both, so their objective changes do not add up."""
+    x = [float(a) for a in range(0, 13)]
+    Q0 = [0.0, 3.0, 6.0, 9.0, 12.0]
+    lam = 0.5
+    J0 = plain.objective(x, Q0, lam, "out")
+    d1 = plain.objective(x, [0.0, 4.0, 6.0, 9.0, 12.0], lam, "out") - J0
+    d3 = plain.objective(x, [0.0, 3.0, 6.0, 11.0, 12.0], lam, "out") - J0
+    both = plain.objective(x, [0.0, 4.0, 6.0, 11.0, 12.0], lam, "out") - J0
+    assert abs(both - (d1 + d3)) > 1e-6
+
+
+# --------------------------------------------------------------------------
+# Final rounding
+
+
+def test_philox_known_answers():
+    """Philox4x32-10 test vectors published with Random123 (Salmon et al., SC'11)."""
+    cases = [
+        ((0, 0, 0, 0), (0, 0), (0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8)),
+        ((0xFFFFFFFF,) * 4, (0xFFFFFFFF,) * 2, (0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD)),
+        ((0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344), (0xA4093822, 0x299F31D0),
+         (0xD16CFE09, 0x94FDCCEB, 0x5001E420, 0x24126EA1)),
+    ]
+    for ctr, key, want in cases:
+        a = [np.array([c], dtype=np.uint64) for c in ctr]
+        got = philox4x32_10(*a, np.array([key[0]], dtype=np.uint64),
+                            np.array([key[1]], dtype=np.uint64))
+        assert tuple(int(g[0]) for g in got) == want
+
+
+def test_uniforms_are_uniform():
+    u = pipeline.uniforms(200000, 12345)
+    assert u.min() >= 0 and u.max() < 1
+    hist, _ = np.histogram(u, bins=50, range=(0, 1))
+    chi2 = ((hist - 4000) ** 2 / 4000).sum()
+    assert chi2 < 100  # 49 dof, p ~ 1e-5
+
+
+def test_quantize_is_unbiased():
+    """E[xhat] = x for SQ (Sec. 2): mean over K seeds within 5 sigma per entry,
+    and the empirical MSE matches sum (b-x)(x-a)."""
+    x = np.random.default_rng(17).standard_normal(300).astype(np.float32)
+    q = np.array([x.min(), -0.7, 0.0, 0.4, 1.3, x.max()], dtype=np.float64)
+    K = 400
+    acc = np.zeros(len(x))
+    sq = np.zeros(len(x))
+    for seed in range(K):
+        sym, hist, _ = pipeline.quantize(x, q, seed)
+        xh = q[sym]
+        acc += xh
+        sq += (xh - x.astype(np.float64)) ** 2
+    xf = x.astype(np.float64)
+    r = np.clip(np.searchsorted(q, xf, side="left") - 1, 0, len(q) - 2)
+    var = (q[r + 1] - xf) * (xf - q[r])
+    z = (acc / K - xf) / np.sqrt(np.maximum(var, 1e-30) / K)
+    assert np.all(np.abs(z[var > 0]) < 5.5)
+    assert abs(sq.sum() / K - var.sum()) < 0.05 * var.sum()
+
+
+def test_quantize_edges():
+    """x = q_0 maps to symbol 0; x = q_{r+1} maps to r+1; t = 1 maps to 0."""
+    q = np.array([-1.0, 0.0, 2.0])
+    sym, hist, ent = pipeline.quantize(np.array([-1.0, 0.0, 2.0], dtype=np.float32), q, 0)
+    assert list(sym) == [0, 1, 2] and list(hist) == [1, 1, 1]
+    assert abs(ent - math.log2(3)) < 1e-15
+    sym, hist, ent = pipeline.quantize(np.array([5.0, 5.0], dtype=np.float32), np.array([5.0]), 0)
+    assert list(sym) == [0, 0] and ent == 0.0
