@@ -1,0 +1,170 @@
+/*
+ * ecasq.h - C ABI of libecasq, an MI355X (gfx950) implementation of the
+ * approximate dynamic program of Entropy-Constrained Adaptive Stochastic
+ * Quantization (ECASQ, arXiv 2608.18147) and the steps around it.
+ *
+ * Problem (Sec. 1 and Sec. 3): given X in R^d, a maximum codebook size s and
+ * an entropy budget b (bits per entry), choose an ordered codebook Q drawn
+ * from the input values (P = X) that spans X, has |Q| <= s, and minimises the
+ * MSE of unbiased stochastic quantization (SQ, Sec. 2) subject to
+ * H(Xhat) <= b.  The library solves the Lagrangian surrogate of Sec. 5
+ * (vNMSE + lambda * H(I,B), dp_APX, eq. apx_base / apx_rec / apx_final)
+ * exactly, searches lambda for the budget (Sec. 3 and Sec. 5), recovers the
+ * codebook with Hirschberg's method in O(d) space (Sec. 5), refines it with
+ * the three-colour pass of Sec. 6, and rounds the input stochastically
+ * (Sec. 2) with Philox4x32-10.
+ *
+ * Conventions for every entry point:
+ *   - Array arguments named x, codebook*, symbols, hist, t_out, infos_dev and
+ *     workspace are DEVICE pointers (HIP memory on the current device); info
+ *     is a HOST pointer.  The caller owns all memory; the library never frees
+ *     caller memory.
+ *   - stream is a hipStream_t passed as void* (NULL = the null stream).  All
+ *     device work is ordered on it.  The solve entry points block the calling
+ *     thread until their results are in device memory, because the budget
+ *     search and the recovery read small results back between steps.
+ *   - Argument errors are reported before any work is enqueued.  Data errors
+ *     (NaN or Inf in x) are detected on the device and returned as
+ *     ECASQ_ENONFINITE.
+ *   - Ties are broken to the lowest index everywhere (lowest predecessor k,
+ *     lowest number of values i, lowest Hirschberg split m); a refinement move
+ *     is taken only on a strict improvement.
+ *   - All arithmetic of the DP is fp64 and follows one fixed operation order,
+ *     so results are reproducible bit for bit across runs.
+ */
+#ifndef ECASQ_H
+#define ECASQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { ECASQ_F32 = 0, ECASQ_F16 = 1, ECASQ_BF16 = 2 } ecasq_dtype;
+
+typedef enum {
+    ECASQ_OK = 0,
+    ECASQ_EINVAL = -1,      /* bad argument (sizes, null pointers, NaN budget) */
+    ECASQ_ENONFINITE = -2,  /* x holds NaN or Inf */
+    ECASQ_EINFEASIBLE = -3, /* b below the smallest reachable H(I,B); the
+                               lowest-entropy codebook found is still returned */
+    ECASQ_ENOMEM = -4,      /* device allocation failed */
+    ECASQ_EHIP = -5,        /* a HIP runtime call failed */
+    ECASQ_EWORKSPACE = -6   /* caller workspace smaller than ecasq_workspace_size */
+} ecasq_status;
+
+typedef struct {
+    int32_t refine_rounds;     /* Sec. 6 rounds, upper bound (default 5; 0 = off) */
+    int32_t refine_exhaustive; /* 0: binary search of Sec. 6 (default); 1: full scan */
+    int32_t exact_s;           /* 0: at most s values (default); 1: exactly min(s, p) */
+    int32_t max_search_iters;  /* lambda-search queries after the first (default 64) */
+    int32_t recovery;          /* 0: Hirschberg, O(d) space (default); 1: stored argmins */
+} ecasq_options;
+
+typedef struct {
+    int32_t t;                /* codebook size actually used */
+    int32_t p;                /* number of distinct input values */
+    double lambda;            /* multiplier of the returned solution, vNMSE units */
+    double mse;               /* MSE(Q, X) = sum (b_x - x)(x - a_x), Sec. 2 */
+    double vnmse;             /* MSE / ||X||^2 */
+    double entropy;           /* H(Xhat) from expected frequencies, bits/entry */
+    double entropy_surrogate; /* H(I,B) of Sec. 5 */
+    double objective;         /* vNMSE + lambda * H(Xhat) */
+    double rate_total;        /* H(Xhat) + 32 t / d (App. F.1 rate accounting) */
+    int32_t dp_solves;        /* full DP solves run by the search */
+    int32_t refine_rounds_run;
+    int64_t cells;            /* DP cells evaluated (search + recovery) */
+    int32_t status;           /* ecasq_status of the solve */
+    int32_t reserved;
+} ecasq_info;
+
+/* Defaults listed in ecasq_options. */
+void ecasq_default_options(ecasq_options *opts);
+
+/*
+ * Budget mode (Sec. 3 problem; Sec. 5 lambda tuning; Sec. 6 refinement).
+ * x: d entries of type dt in device memory, any order.  s >= 2.  b >= 0.
+ * Output codebook: t <= s ascending fp64 values (codebook[0] = min X,
+ * codebook[t-1] = max X) in codebook (device, length >= s); codebook_rank
+ * (device, length >= s, may be NULL) receives each value's index among the
+ * sorted distinct inputs.  Entries past t are left untouched.  info may be NULL.
+ * The returned codebook has H(Xhat) <= b whenever the status is ECASQ_OK.
+ */
+ecasq_status ecasq_solve(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
+                         double bits_per_entry, void *stream, double *codebook,
+                         int32_t *codebook_rank, ecasq_info *info);
+
+/* ecasq_solve with options and an optional caller workspace (device memory of
+ * at least ecasq_workspace_size(d, s, 0) bytes; NULL = allocate internally). */
+ecasq_status ecasq_solve_ex(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
+                            double bits_per_entry, const ecasq_options *opts, void *stream,
+                            double *codebook, int32_t *codebook_rank, ecasq_info *info,
+                            void *workspace, size_t workspace_bytes);
+
+/* Fixed-multiplier mode: minimise vNMSE + lambda H(I,B) (lambda in vNMSE units,
+ * Sec. 3), then refine vNMSE + lambda H(Xhat) without a budget guard. */
+ecasq_status ecasq_solve_lagrangian(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
+                                    double lambda, const ecasq_options *opts, void *stream,
+                                    double *codebook, int32_t *codebook_rank,
+                                    ecasq_info *info);
+
+/*
+ * Final stochastic rounding (Sec. 2): symbol i in [0, t) for every entry of x
+ * in its original order.  The bracket is q_r < x <= q_{r+1} (x <= q_0 gives
+ * r = 0; x > q_{t-1} is clamped to t-1); the entry rounds up iff
+ * u < (x - q_r) / (q_{r+1} - q_r), where u is 53 bits of Philox4x32-10 with
+ * counter (i mod 2^32, i / 2^32, 0, 0) and key (seed mod 2^32, seed / 2^32).
+ * codebook: device, t ascending fp64 values, 1 <= t <= 256.  symbols: device,
+ * d bytes.  empirical_entropy: device scalar, plug-in entropy of the symbol
+ * histogram in bits/entry.  hist: device, t int64 counts, may be NULL.
+ */
+ecasq_status ecasq_quantize(const void *x, ecasq_dtype dt, int64_t d, const double *codebook,
+                            int32_t t, uint64_t seed, void *stream, uint8_t *symbols,
+                            double *empirical_entropy, int64_t *hist);
+
+/*
+ * Many independent short vectors in one launch (one workgroup per row):
+ * x is n rows of d entries, row-major.  Each row is solved as ecasq_solve_ex
+ * would with opts->recovery = 1 (argmins kept in LDS).  codebooks: device,
+ * n x s fp64 (row r's t_out[r] values first); t_out: device, n int32;
+ * infos_dev: device, n ecasq_info, may be NULL.  d <= 512, s <= 32.
+ */
+ecasq_status ecasq_solve_batched(const void *x, ecasq_dtype dt, int64_t n, int64_t d,
+                                 int32_t s, double bits_per_entry, const ecasq_options *opts,
+                                 void *stream, double *codebooks, int32_t *t_out,
+                                 ecasq_info *infos_dev);
+
+/* Bytes of device workspace a single-vector solve of d entries with at most s
+ * values needs (flags reserved, pass 0). */
+size_t ecasq_workspace_size(int64_t d, int32_t s, int32_t flags);
+
+/* Static string for a status code. */
+const char *ecasq_status_string(ecasq_status st);
+
+/*
+ * Inspection entry points used by the parity tests.
+ *
+ * ecasq_histogram: the sorted distinct values v (ascending, -0 folded into
+ * +0), inclusive prefix counts N, and the correctly rounded inclusive prefix
+ * sums S = sum c v and S2 = sum c v^2 (App. D prefix quantities).  All outputs
+ * are device arrays of length >= d; *p_out (host) receives p.
+ *
+ * ecasq_dp_trace: one forward DP solve of dp_APX at lambda (vNMSE units) on
+ * the histogram of x, recording for every layer i in [2, min(s,p)] the values
+ * F_i[j] (device, (s+1) x d fp64, row i; entries outside the layer's valid
+ * columns are left untouched) and argmins k*_i[j] (device, (s+1) x d int32).
+ * out5 (host): J (MSE units), MSE, H(I,B) of the minimising path, i*, cells.
+ */
+ecasq_status ecasq_histogram(const void *x, ecasq_dtype dt, int64_t d, void *stream, double *v,
+                             double *N, double *S, double *S2, int64_t *p_out);
+
+ecasq_status ecasq_dp_trace(const void *x, ecasq_dtype dt, int64_t d, int32_t s, double lambda,
+                            void *stream, double *F, int32_t *kstar, double *out5);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ECASQ_H */

@@ -278,11 +278,13 @@ static void hb_forward(const hist_t *H, double lamp, int64_t lo, int64_t hi, int
     for (int q = 2; q <= q_end; q++) {
         int64_t jl = lo + q - 1, jh = hi - (n - q);
         int64_t kl = lo + q - 2;
+        /* at q = 2 the only finite predecessor is lo itself */
         for (int64_t x = 0; x < len; x++) G[x] = INFINITY;
 #pragma omp parallel for schedule(dynamic, 64)
         for (int64_t j = jl; j <= jh; j++) {
             double best = INFINITY;
-            for (int64_t k = kl; k < j; k++) {
+            int64_t ke = (q == 2) ? lo : j - 1;
+            for (int64_t k = kl; k <= ke; k++) {
                 double C, P;
                 cell_terms(H, k, j, &C, &P);
                 double cand = fma(-lamp, P, F[k - lo] + C);
@@ -290,7 +292,7 @@ static void hb_forward(const hist_t *H, double lamp, int64_t lo, int64_t hi, int
             }
             G[j - lo] = best;
         }
-        for (int64_t j = jl; j <= jh; j++) g_hb_cells += j - kl;
+        for (int64_t j = jl; j <= jh; j++) g_hb_cells += (q == 2) ? 1 : j - kl;
         memcpy(F, G, sizeof(double) * len);
     }
     free(G);
@@ -310,7 +312,8 @@ static void hb_backward(const hist_t *H, double lamp, int64_t lo, int64_t hi, in
 #pragma omp parallel for schedule(dynamic, 64)
         for (int64_t j = jl; j <= jh; j++) {
             double best = INFINITY;
-            for (int64_t k = j + 1; k <= kh; k++) {
+            int64_t ks = (q == 2) ? hi : j + 1; /* at q = 2 only hi is finite */
+            for (int64_t k = ks; k <= kh; k++) {
                 double C, P;
                 cell_terms(H, j, k, &C, &P);
                 double cand = fma(-lamp, P, B[k - lo] + C);
@@ -318,7 +321,7 @@ static void hb_backward(const hist_t *H, double lamp, int64_t lo, int64_t hi, in
             }
             G[j - lo] = best;
         }
-        for (int64_t j = jl; j <= jh; j++) g_hb_cells += kh - j;
+        for (int64_t j = jl; j <= jh; j++) g_hb_cells += (q == 2) ? 1 : kh - j;
         memcpy(B, G, sizeof(double) * len);
     }
     free(G);

@@ -1,0 +1,599 @@
+// libecasq host library: argument checks, workspace layout and the launch
+// sequence of one ECASQ solve (see include/ecasq.h for the contract).
+//
+//   prep        sort + weighted histogram + exact prefix sums (Sec. 2, App. D)
+//   search      slope search on lambda, one full dp_APX solve per query
+//               (Sec. 3 and Sec. 5; supporting-line queries as in App. F.7)
+//   recovery    Hirschberg on the final multiplier (Sec. 5 / Sec. 4.2), or a
+//               traceback through stored argmins
+//   refinement  three-colour pass (Sec. 6), one kernel
+//   metrics     MSE, vNMSE, H(Xhat), H(I,B), objective, total rate
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "../../include/ecasq.h"
+#include "launch.hpp"
+
+using namespace ecasq;
+
+namespace {
+
+#define HIP_TRY(expr)                               \
+    do {                                            \
+        hipError_t e_ = (expr);                     \
+        if (e_ != hipSuccess) return ECASQ_EHIP;    \
+    } while (0)
+
+#define ECASQ_TRY(expr)                             \
+    do {                                            \
+        ecasq_status s_ = (expr);                   \
+        if (s_ != ECASQ_OK) return s_;              \
+    } while (0)
+
+struct Layout {
+    size_t v, N, S, S2, F0, F1, M0, M1, P0, P1, pval, pidx, last, res, small, chain, kstar, prep;
+    size_t total;
+};
+
+Layout layout(int64_t d, int32_t s, bool kstar) {
+    Layout L;
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        size_t at = o;
+        o += align256(bytes);
+        return at;
+    };
+    const size_t nd = sizeof(double) * (size_t)d;
+    L.v = take(nd);
+    L.N = take(nd);
+    L.S = take(nd);
+    L.S2 = take(nd);
+    L.F0 = take(nd);
+    L.F1 = take(nd);
+    L.M0 = take(nd);
+    L.M1 = take(nd);
+    L.P0 = take(nd);
+    L.P1 = take(nd);
+    const size_t np = (size_t)dp_partial_entries(d);
+    L.pval = take(sizeof(double) * np);
+    L.pidx = take(sizeof(int32_t) * np);
+    L.last = take(sizeof(double) * 3 * (size_t)(s + 1));
+    L.res = take(sizeof(double) * 32);
+    L.small = take(sizeof(int64_t) * 8);
+    L.chain = take(sizeof(int32_t) * (size_t)(s + 8));
+    L.kstar = kstar ? take(sizeof(int32_t) * (size_t)(s + 1) * (size_t)d) : 0;
+    L.prep = take(prep_scratch_bytes(d));
+    L.total = o;
+    return L;
+}
+
+struct Point {
+    double lam, H, M;
+    int32_t t;
+};
+
+struct Ctx {
+    hipStream_t st;
+    char* base;
+    Layout L;
+    int64_t d;
+    int32_t s;
+    int64_t p;
+    double s2tot;
+    Hist H;
+    int64_t cells;
+    int32_t solves;
+    bool own;
+
+    template <class T>
+    T* at(size_t off) const {
+        return reinterpret_cast<T*>(base + off);
+    }
+};
+
+ecasq_status check_x(const void* x, int dt, int64_t d) {
+    if (!x || d < 1 || d > ((int64_t)1 << 28)) return ECASQ_EINVAL;
+    if (dt < 0 || dt > 2) return ECASQ_EINVAL;
+    return ECASQ_OK;
+}
+
+ecasq_status ctx_open(Ctx& c, int64_t d, int32_t s, bool kstar, void* stream, void* ws,
+                      size_t ws_bytes) {
+    c.st = static_cast<hipStream_t>(stream);
+    c.d = d;
+    c.s = s;
+    c.L = layout(d, s, kstar);
+    c.cells = 0;
+    c.solves = 0;
+    c.own = ws == nullptr;
+    if (ws) {
+        if (ws_bytes < c.L.total) return ECASQ_EWORKSPACE;
+        c.base = static_cast<char*>(ws);
+    } else {
+        void* p = nullptr;
+        if (hipMallocAsync(&p, c.L.total, c.st) != hipSuccess) return ECASQ_ENOMEM;
+        c.base = static_cast<char*>(p);
+    }
+    return ECASQ_OK;
+}
+
+void ctx_close(Ctx& c) {
+    if (c.own && c.base) {
+        (void)hipFreeAsync(c.base, c.st);
+        (void)hipStreamSynchronize(c.st);
+    }
+    c.base = nullptr;
+}
+
+// Sort, histogram, exact prefix sums; reads p, N[0] and ||X||^2 back.
+ecasq_status ctx_prep(Ctx& c, const void* x, int dt) {
+    int64_t* small = c.at<int64_t>(c.L.small);
+    uint32_t* flags = reinterpret_cast<uint32_t*>(small + 1);
+    HIP_TRY(hipMemsetAsync(small, 0, sizeof(int64_t) * 8, c.st));
+    HIP_TRY(launch_prep(x, dt, c.d, c.base + c.L.prep, c.st, c.at<double>(c.L.v),
+                        c.at<double>(c.L.N), c.at<double>(c.L.S), c.at<double>(c.L.S2), small,
+                        flags));
+    int64_t hs[2] = {0, 0};
+    HIP_TRY(hipMemcpyAsync(hs, small, sizeof hs, hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    if ((uint32_t)hs[1] & 1u) return ECASQ_ENONFINITE;
+    c.p = hs[0];
+    double c0 = 0, s2 = 0;
+    HIP_TRY(hipMemcpyAsync(&c0, c.at<double>(c.L.N), sizeof(double), hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipMemcpyAsync(&s2, c.at<double>(c.L.S2) + (c.p - 1), sizeof(double),
+                           hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    c.s2tot = s2;
+    c.H.v = c.at<double>(c.L.v);
+    c.H.N = c.at<double>(c.L.N);
+    c.H.S = c.at<double>(c.L.S);
+    c.H.S2 = c.at<double>(c.L.S2);
+    c.H.p = c.p;
+    c.H.dd = (double)c.d;
+    c.H.c0 = c0;
+    c.H.c0d = c0 / (double)c.d;
+    return ECASQ_OK;
+}
+
+int64_t tri_cells(int64_t n) { return n * (n + 1) / 2; }
+
+// One full dp_APX solve at lambda (vNMSE units).  Optional per-layer dumps
+// (row i of Fdump / Kdump, row stride `stride`).
+ecasq_status dp_solve(Ctx& c, double lam, int32_t exact_s, Point& out, double* J_out,
+                      double* Fdump, int32_t* Kdump, int64_t stride) {
+    const double lamp = lam * c.s2tot;
+    const int64_t p = c.p;
+    const int32_t imax = (int32_t)std::min<int64_t>(c.s, p);
+    const int32_t ls = c.s + 1;
+    double* F[2] = {c.at<double>(c.L.F0), c.at<double>(c.L.F1)};
+    double* M[2] = {c.at<double>(c.L.M0), c.at<double>(c.L.M1)};
+    double* Ph[2] = {c.at<double>(c.L.P0), c.at<double>(c.L.P1)};
+    double* last = c.at<double>(c.L.last);
+    double* res = c.at<double>(c.L.res);
+    HIP_TRY(launch_dp_init_fwd(c.H, 0, 1, p - 1, lamp, F[0], M[0], Ph[0],
+                               Kdump ? Kdump + 2 * stride : nullptr, last, ls, c.st));
+    if (Fdump)
+        HIP_TRY(hipMemcpyAsync(Fdump + 2 * stride + 1, F[0] + 1, sizeof(double) * (p - 1),
+                               hipMemcpyDeviceToDevice, c.st));
+    c.cells += p - 1;
+    int cur = 0;
+    for (int32_t i = 3; i <= imax; i++) {
+        DpLayer L;
+        L.H = c.H;
+        L.Fin = F[cur];
+        L.Fout = F[1 - cur];
+        L.pval = c.at<double>(c.L.pval);
+        L.pidx = c.at<int32_t>(c.L.pidx);
+        L.kb = i - 2;
+        L.jlo = i - 1;
+        L.jhi = p - 1;
+        L.backward = false;
+        L.lam = lamp;
+        L.Min = M[cur];
+        L.Pin = Ph[cur];
+        L.Mout = M[1 - cur];
+        L.Pout = Ph[1 - cur];
+        L.kstar = Kdump ? Kdump + (int64_t)i * stride : nullptr;
+        L.last = last;
+        L.layer = i;
+        L.last_stride = ls;
+        HIP_TRY(launch_dp_layer(L, c.st));
+        if (Fdump)
+            HIP_TRY(hipMemcpyAsync(Fdump + (int64_t)i * stride + (i - 1), F[1 - cur] + (i - 1),
+                                   sizeof(double) * (p - i + 1), hipMemcpyDeviceToDevice, c.st));
+        c.cells += tri_cells(p - i + 1);
+        cur = 1 - cur;
+    }
+    HIP_TRY(launch_dp_final(last, ls, imax, exact_s, res, c.st));
+    double r[4];
+    HIP_TRY(hipMemcpyAsync(r, res, sizeof r, hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    out.lam = lam;
+    out.H = r[2];
+    out.M = r[1] / c.s2tot;
+    out.t = (int32_t)r[3];
+    if (J_out) {
+        J_out[0] = r[0];
+        J_out[1] = r[1];
+        J_out[2] = r[2];
+        J_out[3] = r[3];
+    }
+    c.solves++;
+    return ECASQ_OK;
+}
+
+// Slope search for the budget b.  A: infeasible point (starts at lambda = 0),
+// B: feasible point (starts at {v_0, v_{p-1}} for b >= 1, else the solve at
+// lambda = 2^40).  Query the slope of the chord AB; stop when the answer is A
+// or B again.  Returns B.
+ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_iters, Point& B,
+                    ecasq_status& status) {
+    status = ECASQ_OK;
+    Point A;
+    ECASQ_TRY(dp_solve(c, 0.0, exact_s, A, nullptr, nullptr, nullptr, 0));
+    if (A.H <= b) {
+        B = A;
+        return ECASQ_OK;
+    }
+    if (b >= 1.0) {
+        // closed form of the two-value codebook {v_0, v_{p-1}}
+        int32_t two[2] = {0, (int32_t)(c.p - 1)};
+        int32_t* ch = c.at<int32_t>(c.L.chain);
+        double* res = c.at<double>(c.L.res) + 8;
+        HIP_TRY(hipMemcpyAsync(ch, two, sizeof two, hipMemcpyHostToDevice, c.st));
+        HIP_TRY(launch_metrics(c.H, 2, ch, 0.0, c.s2tot, res, c.st));
+        double m[6];
+        HIP_TRY(hipMemcpyAsync(m, res, sizeof m, hipMemcpyDeviceToHost, c.st));
+        HIP_TRY(hipStreamSynchronize(c.st));
+        B.lam = HUGE_VAL;
+        B.H = m[3];
+        B.M = (0.0 + m[0]) / c.s2tot;
+        B.t = 2;
+    } else {
+        ECASQ_TRY(dp_solve(c, 0x1p40, exact_s, B, nullptr, nullptr, nullptr, 0));
+        if (B.H > b) {
+            status = ECASQ_EINFEASIBLE;
+            return ECASQ_OK;
+        }
+    }
+    for (int32_t it = 0; it < max_iters; it++) {
+        const double lc = (B.M - A.M) / (A.H - B.H);
+        if (!(lc > 0.0)) break;
+        Point C;
+        ECASQ_TRY(dp_solve(c, lc, exact_s, C, nullptr, nullptr, nullptr, 0));
+        if ((C.H == A.H && C.M == A.M) || (C.H == B.H && C.M == B.M)) break;
+        if (C.H > b) A = C;
+        else B = C;
+    }
+    return ECASQ_OK;
+}
+
+// Hirschberg recovery of the best chain lo = u_0 < ... < u_{n-1} = hi.
+ecasq_status hirschberg(Ctx& c, double lamp, int64_t lo, int64_t hi, int32_t n, int32_t* out) {
+    if (n == 2) {
+        out[0] = (int32_t)lo;
+        out[1] = (int32_t)hi;
+        return ECASQ_OK;
+    }
+    if (hi - lo + 1 == n) {
+        for (int32_t x = 0; x < n; x++) out[x] = (int32_t)(lo + x);
+        return ECASQ_OK;
+    }
+    const int32_t r = (n - 1) / 2;
+    double* Fw[2] = {c.at<double>(c.L.F0), c.at<double>(c.L.F1)};
+    double* Bw[2] = {c.at<double>(c.L.M0), c.at<double>(c.L.M1)};
+    // forward half: r+1 values starting at lo
+    {
+        const int64_t jl = lo + 1, jh = hi - (n - 2);
+        HIP_TRY(launch_dp_init_fwd(c.H, lo, jl, jh, lamp, Fw[0], nullptr, nullptr, nullptr,
+                                   nullptr, 0, c.st));
+        c.cells += jh - jl + 1;
+    }
+    int fc = 0;
+    for (int32_t q = 3; q <= r + 1; q++) {
+        DpLayer L;
+        std::memset(&L, 0, sizeof L);
+        L.H = c.H;
+        L.Fin = Fw[fc];
+        L.Fout = Fw[1 - fc];
+        L.pval = c.at<double>(c.L.pval);
+        L.pidx = c.at<int32_t>(c.L.pidx);
+        L.kb = lo + q - 2;
+        L.jlo = lo + q - 1;
+        L.jhi = hi - (n - q);
+        L.backward = false;
+        L.lam = lamp;
+        HIP_TRY(launch_dp_layer(L, c.st));
+        for (int64_t j = L.jlo; j <= L.jhi; j++) c.cells += j - L.kb;
+        fc = 1 - fc;
+    }
+    // backward half: n-r values ending at hi
+    {
+        const int64_t jl = lo + n - 2, jh = hi - 1;
+        HIP_TRY(launch_dp_init_bwd(c.H, hi, jl, jh, lamp, Bw[0], c.st));
+        c.cells += jh - jl + 1;
+    }
+    int bc = 0;
+    for (int32_t q = 3; q <= n - r; q++) {
+        DpLayer L;
+        std::memset(&L, 0, sizeof L);
+        L.H = c.H;
+        L.Fin = Bw[bc];
+        L.Fout = Bw[1 - bc];
+        L.pval = c.at<double>(c.L.pval);
+        L.pidx = c.at<int32_t>(c.L.pidx);
+        L.kb = hi - q + 2;
+        L.jlo = lo + n - q;
+        L.jhi = hi - q + 1;
+        L.backward = true;
+        L.lam = lamp;
+        HIP_TRY(launch_dp_layer(L, c.st));
+        for (int64_t j = L.jlo; j <= L.jhi; j++) c.cells += L.kb - j;
+        bc = 1 - bc;
+    }
+    int64_t* mdev = c.at<int64_t>(c.L.small) + 4;
+    HIP_TRY(launch_split(Fw[fc], Bw[bc], lo + r, hi - (n - 1 - r), mdev, c.st));
+    int64_t m = -1;
+    HIP_TRY(hipMemcpyAsync(&m, mdev, sizeof m, hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    if (m < lo + r || m > hi - (n - 1 - r)) return ECASQ_EHIP;
+    ECASQ_TRY(hirschberg(c, lamp, lo, m, r + 1, out));
+    ECASQ_TRY(hirschberg(c, lamp, m, hi, n - r, out + r));
+    return ECASQ_OK;
+}
+
+// Codebook with t values at lambda (vNMSE units), written to chain (host).
+ecasq_status recover(Ctx& c, int32_t t, double lam, int32_t exact_s, int32_t mode,
+                     std::vector<int32_t>& chain) {
+    chain.assign(t, 0);
+    if (c.p == 1) return ECASQ_OK;
+    if (t == 2 || !std::isfinite(lam)) {
+        chain.assign({0, (int32_t)(c.p - 1)});
+        return ECASQ_OK;
+    }
+    if (mode == 1) {
+        int32_t* K = c.at<int32_t>(c.L.kstar);
+        Point P;
+        ECASQ_TRY(dp_solve(c, lam, exact_s, P, nullptr, nullptr, K, c.p));
+        c.solves--;  // a repeat of a search solve, not a new query
+        if (P.t != t) return ECASQ_EHIP;
+        chain[t - 1] = (int32_t)(c.p - 1);
+        for (int32_t i = t; i >= 3; i--) {
+            int32_t k = -1;
+            HIP_TRY(hipMemcpyAsync(&k, K + (int64_t)i * c.p + chain[i - 1], sizeof k,
+                                   hipMemcpyDeviceToHost, c.st));
+            HIP_TRY(hipStreamSynchronize(c.st));
+            chain[i - 2] = k;
+        }
+        chain[0] = 0;
+        return ECASQ_OK;
+    }
+    return hirschberg(c, lam * c.s2tot, 0, c.p - 1, t, chain.data());
+}
+
+ecasq_status finish(Ctx& c, std::vector<int32_t>& chain, double lam, double b, bool budget,
+                    const ecasq_options& o, double* codebook, int32_t* rank, ecasq_info* info,
+                    ecasq_status status) {
+    const int32_t t = (int32_t)chain.size();
+    int32_t* ch = c.at<int32_t>(c.L.chain);
+    int32_t* stats = ch + c.s + 2;
+    HIP_TRY(hipMemcpyAsync(ch, chain.data(), sizeof(int32_t) * t, hipMemcpyHostToDevice, c.st));
+    HIP_TRY(hipMemsetAsync(stats, 0, sizeof(int32_t) * 2, c.st));
+    if (o.refine_rounds > 0 && std::isfinite(lam) && t >= 3)
+        HIP_TRY(launch_refine(c.H, t, ch, lam * c.s2tot, b, budget ? 1 : 0, o.refine_rounds,
+                              o.refine_exhaustive, stats, c.st));
+    double* mres = c.at<double>(c.L.res) + 8;
+    HIP_TRY(launch_metrics(c.H, t, ch, lam, c.s2tot, mres, c.st));
+    HIP_TRY(launch_gather(c.H.v, ch, t, codebook, rank, c.st));
+    double m[6];
+    int32_t stt[2];
+    HIP_TRY(hipMemcpyAsync(m, mres, sizeof m, hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipMemcpyAsync(stt, stats, sizeof stt, hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    if (info) {
+        std::memset(info, 0, sizeof *info);
+        info->t = t;
+        info->p = (int32_t)c.p;
+        info->lambda = lam;
+        info->mse = m[0];
+        info->vnmse = m[1];
+        info->entropy = m[2];
+        info->entropy_surrogate = m[3];
+        info->objective = m[4];
+        info->rate_total = m[5];
+        info->dp_solves = c.solves;
+        info->refine_rounds_run = stt[0];
+        info->cells = c.cells;
+        info->status = status;
+    }
+    return status;
+}
+
+ecasq_options defaults() {
+    ecasq_options o;
+    o.refine_rounds = 5;
+    o.refine_exhaustive = 0;
+    o.exact_s = 0;
+    o.max_search_iters = 64;
+    o.recovery = 0;
+    return o;
+}
+
+ecasq_status solve_budget(const void* x, int dt, int64_t d, int32_t s, double b,
+                          const ecasq_options& o, void* stream, double* codebook, int32_t* rank,
+                          ecasq_info* info, void* ws, size_t wsb) {
+    Ctx c;
+    ECASQ_TRY(ctx_open(c, d, s, o.recovery == 1, stream, ws, wsb));
+    struct Closer {
+        Ctx& c;
+        ~Closer() { ctx_close(c); }
+    } closer{c};
+    ECASQ_TRY(ctx_prep(c, x, dt));
+    std::vector<int32_t> chain;
+    ecasq_status status = ECASQ_OK;
+    double lam = 0.0;
+    if (c.p <= 2) {
+        for (int64_t k = 0; k < c.p; k++) chain.push_back((int32_t)k);
+    } else {
+        Point B;
+        ECASQ_TRY(search(c, b, o.exact_s, o.max_search_iters, B, status));
+        lam = B.lam;
+        ECASQ_TRY(recover(c, B.t, B.lam, o.exact_s, o.recovery, chain));
+    }
+    ecasq_status st = finish(c, chain, lam, b, true, o, codebook, rank, info, status);
+    if (c.p == 2 && info && info->entropy_surrogate > b) {
+        info->status = ECASQ_EINFEASIBLE;
+        st = ECASQ_EINFEASIBLE;
+    }
+    return st;
+}
+
+}  // namespace
+
+extern "C" {
+
+void ecasq_default_options(ecasq_options* opts) {
+    if (opts) *opts = defaults();
+}
+
+size_t ecasq_workspace_size(int64_t d, int32_t s, int32_t flags) {
+    if (d < 1 || s < 2) return 0;
+    return layout(d, s, (flags & 1) != 0).total;
+}
+
+const char* ecasq_status_string(ecasq_status st) {
+    switch (st) {
+        case ECASQ_OK: return "ok";
+        case ECASQ_EINVAL: return "invalid argument";
+        case ECASQ_ENONFINITE: return "input holds NaN or Inf";
+        case ECASQ_EINFEASIBLE: return "entropy budget below the smallest reachable surrogate entropy";
+        case ECASQ_ENOMEM: return "device allocation failed";
+        case ECASQ_EHIP: return "HIP runtime error";
+        case ECASQ_EWORKSPACE: return "workspace too small";
+    }
+    return "unknown status";
+}
+
+ecasq_status ecasq_solve_ex(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
+                            double bits_per_entry, const ecasq_options* opts, void* stream,
+                            double* codebook, int32_t* codebook_rank, ecasq_info* info,
+                            void* workspace, size_t workspace_bytes) {
+    ECASQ_TRY(check_x(x, dt, d));
+    if (s < 2 || s > 255 || !codebook) return ECASQ_EINVAL;
+    if (!(bits_per_entry >= 0.0)) return ECASQ_EINVAL;  // also rejects NaN
+    const ecasq_options o = opts ? *opts : defaults();
+    if (o.refine_rounds < 0 || o.max_search_iters < 0 || o.recovery < 0 || o.recovery > 1)
+        return ECASQ_EINVAL;
+    return solve_budget(x, dt, d, s, bits_per_entry, o, stream, codebook, codebook_rank, info,
+                        workspace, workspace_bytes);
+}
+
+ecasq_status ecasq_solve(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
+                         double bits_per_entry, void* stream, double* codebook,
+                         int32_t* codebook_rank, ecasq_info* info) {
+    return ecasq_solve_ex(x, dt, d, s, bits_per_entry, nullptr, stream, codebook, codebook_rank,
+                          info, nullptr, 0);
+}
+
+ecasq_status ecasq_solve_lagrangian(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
+                                    double lambda, const ecasq_options* opts, void* stream,
+                                    double* codebook, int32_t* codebook_rank, ecasq_info* info) {
+    ECASQ_TRY(check_x(x, dt, d));
+    if (s < 2 || s > 255 || !codebook || !(lambda >= 0.0) || !std::isfinite(lambda))
+        return ECASQ_EINVAL;
+    const ecasq_options o = opts ? *opts : defaults();
+    if (o.refine_rounds < 0 || o.recovery < 0 || o.recovery > 1) return ECASQ_EINVAL;
+    Ctx c;
+    ECASQ_TRY(ctx_open(c, d, s, o.recovery == 1, stream, nullptr, 0));
+    struct Closer {
+        Ctx& c;
+        ~Closer() { ctx_close(c); }
+    } closer{c};
+    ECASQ_TRY(ctx_prep(c, x, dt));
+    std::vector<int32_t> chain;
+    if (c.p == 1) {
+        chain.assign(1, 0);
+    } else {
+        Point P;
+        ECASQ_TRY(dp_solve(c, lambda, o.exact_s, P, nullptr, nullptr, nullptr, 0));
+        ECASQ_TRY(recover(c, P.t, lambda, o.exact_s, o.recovery, chain));
+    }
+    return finish(c, chain, lambda, HUGE_VAL, false, o, codebook, codebook_rank, info, ECASQ_OK);
+}
+
+ecasq_status ecasq_quantize(const void* x, ecasq_dtype dt, int64_t d, const double* codebook,
+                            int32_t t, uint64_t seed, void* stream, uint8_t* symbols,
+                            double* empirical_entropy, int64_t* hist) {
+    ECASQ_TRY(check_x(x, dt, d));
+    if (!codebook || t < 1 || t > 256 || !symbols || !empirical_entropy) return ECASQ_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    void* h = nullptr;
+    if (hipMallocAsync(&h, sizeof(unsigned long long) * 256, st) != hipSuccess)
+        return ECASQ_ENOMEM;
+    unsigned long long* hh = static_cast<unsigned long long*>(h);
+    ecasq_status rc = ECASQ_OK;
+    if (hipMemsetAsync(hh, 0, sizeof(unsigned long long) * 256, st) != hipSuccess ||
+        launch_quantize(x, dt, d, codebook, t, seed, symbols, hh, st) != hipSuccess ||
+        launch_entropy(hh, t, d, empirical_entropy, hist, st) != hipSuccess)
+        rc = ECASQ_EHIP;
+    if (hipFreeAsync(h, st) != hipSuccess) rc = ECASQ_EHIP;
+    return rc;
+}
+
+ecasq_status ecasq_histogram(const void* x, ecasq_dtype dt, int64_t d, void* stream, double* v,
+                             double* N, double* S, double* S2, int64_t* p_out) {
+    ECASQ_TRY(check_x(x, dt, d));
+    if (!v || !N || !S || !S2 || !p_out) return ECASQ_EINVAL;
+    Ctx c;
+    ECASQ_TRY(ctx_open(c, d, 2, false, stream, nullptr, 0));
+    struct Closer {
+        Ctx& c;
+        ~Closer() { ctx_close(c); }
+    } closer{c};
+    ECASQ_TRY(ctx_prep(c, x, dt));
+    const size_t nb = sizeof(double) * (size_t)c.p;
+    HIP_TRY(hipMemcpyAsync(v, c.H.v, nb, hipMemcpyDeviceToDevice, c.st));
+    HIP_TRY(hipMemcpyAsync(N, c.H.N, nb, hipMemcpyDeviceToDevice, c.st));
+    HIP_TRY(hipMemcpyAsync(S, c.H.S, nb, hipMemcpyDeviceToDevice, c.st));
+    HIP_TRY(hipMemcpyAsync(S2, c.H.S2, nb, hipMemcpyDeviceToDevice, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    *p_out = c.p;
+    return ECASQ_OK;
+}
+
+ecasq_status ecasq_dp_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s, double lambda,
+                            void* stream, double* F, int32_t* kstar, double* out5) {
+    ECASQ_TRY(check_x(x, dt, d));
+    if (s < 2 || s > 255 || !F || !kstar || !out5 || !(lambda >= 0.0)) return ECASQ_EINVAL;
+    Ctx c;
+    ECASQ_TRY(ctx_open(c, d, s, false, stream, nullptr, 0));
+    struct Closer {
+        Ctx& c;
+        ~Closer() { ctx_close(c); }
+    } closer{c};
+    ECASQ_TRY(ctx_prep(c, x, dt));
+    if (c.p < 2) return ECASQ_EINVAL;
+    Point P;
+    double J[4];
+    ECASQ_TRY(dp_solve(c, lambda, 0, P, J, F, kstar, d));
+    out5[0] = J[0];
+    out5[1] = J[1];
+    out5[2] = J[2];
+    out5[3] = J[3];
+    out5[4] = (double)c.cells;
+    return ECASQ_OK;
+}
+
+ecasq_status ecasq_solve_batched(const void* x, ecasq_dtype dt, int64_t n, int64_t d, int32_t s,
+                                 double bits_per_entry, const ecasq_options* opts, void* stream,
+                                 double* codebooks, int32_t* t_out, ecasq_info* infos_dev) {
+    (void)x; (void)dt; (void)n; (void)d; (void)s; (void)bits_per_entry; (void)opts;
+    (void)stream; (void)codebooks; (void)t_out; (void)infos_dev;
+    return ECASQ_EINVAL;  // provided by batched.hip once built
+}
+
+}  // extern "C"

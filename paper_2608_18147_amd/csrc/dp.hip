@@ -1,0 +1,406 @@
+// The approximate dynamic program dp_APX of Sec. 5 (eq. apx_base, apx_rec,
+// apx_final) and the half-DPs of its Hirschberg recovery.
+//
+// One layer computes, for every column j,
+//     F_i[j] = min_{k < j} F_{i-1}[k] + C[k,j] + lambda' Phi[k,j]
+// (forward), or for the backward half of the recovery
+//     B_q[j] = min_{k > j} C[j,k] + lambda' Phi[j,k] + B_{q-1}[k].
+// The interval cost is evaluated on the fly from prefix sums; nothing of size
+// p x p is stored.
+//
+// Mapping on CDNA4: one lane owns one column j (R columns per lane, strided by
+// the block size, so column data sits in VGPRs and loads coalesce).  The
+// predecessor index k is uniform across the block: a tile of 256 predecessors
+// (v, N, S, S2, F) is staged through LDS and read as broadcasts, so the k loop
+// needs no cross-lane reduction at all.  The min over k of one column is split
+// into chunks of kc predecessors; each (column block, chunk) pair is one
+// workgroup, which balances the triangular work and fills all 256 CUs, and a
+// second kernel reduces the per-chunk (value, index) partials in increasing k
+// order (lowest k wins ties).  The 256-entry log2 table also lives in LDS.
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace ecasq {
+
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kTK = 256;
+
+struct LayerArgs {
+    const double* v;
+    const double* N;
+    const double* S;
+    const double* S2;
+    const double* Fin;  // previous layer, indexed by absolute k
+    double* pval;
+    int32_t* pidx;
+    int64_t kb;   // forward: first predecessor; backward: last predecessor (khi)
+    int64_t jlo;  // first column
+    int64_t jhi;  // last column (inclusive)
+    int64_t kc;   // predecessors per chunk (multiple of kTK)
+    int32_t maxch;
+    double dd;
+    double lam;  // lambda' (MSE units)
+};
+
+// Predecessor range of block b: forward [kb, jend-1]; backward [j0+1, khi].
+template <bool BWD>
+__device__ __forceinline__ void block_krange(const LayerArgs& a, int64_t CB, int64_t b,
+                                             int64_t& j0, int64_t& jend, int64_t& klo,
+                                             int64_t& khi) {
+    j0 = a.jlo + b * CB;
+    jend = j0 + CB - 1 < a.jhi ? j0 + CB - 1 : a.jhi;
+    if (BWD) {
+        klo = j0 + 1;
+        khi = a.kb;
+    } else {
+        klo = a.kb;
+        khi = jend - 1;
+    }
+}
+
+template <int R, bool BWD>
+__global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a) {
+    __shared__ double2 tab[256];
+    __shared__ double sv[kTK], sN[kTK], sS[kTK], sS2[kTK], sF[kTK];
+    constexpr int64_t CB = (int64_t)kBlock * R;
+    const int tid = threadIdx.x;
+    const int64_t b = blockIdx.y;
+    const int64_t c = blockIdx.x;
+    int64_t j0, jend, klo, khi;
+    block_krange<BWD>(a, CB, b, j0, jend, klo, khi);
+    const int64_t len = khi - klo + 1;
+    const int64_t nch = (len + a.kc - 1) / a.kc;
+    if (c >= nch) return;  // uniform across the block
+    load_log2_table(tab);
+    const int64_t cs = klo + c * a.kc;
+    const int64_t ce = cs + a.kc - 1 < khi ? cs + a.kc - 1 : khi;
+
+    int64_t col[R];
+    double cv[R], cN[R], cS[R], cS2[R], best[R];
+    int32_t bk[R];
+#pragma unroll
+    for (int r = 0; r < R; r++) {
+        col[r] = j0 + r * kBlock + tid;
+        const int64_t jj = col[r] <= jend ? col[r] : jend;
+        cv[r] = a.v[jj];
+        cN[r] = a.N[jj];
+        cS[r] = a.S[jj];
+        cS2[r] = a.S2[jj];
+        best[r] = __builtin_huge_val();
+        bk[r] = -1;
+    }
+    const double lam = a.lam, dd = a.dd;
+    for (int64_t t0 = cs; t0 <= ce; t0 += kTK) {
+        const int nk = (int)(ce - t0 + 1 < kTK ? ce - t0 + 1 : kTK);
+        __syncthreads();
+        if (tid < nk) {
+            const int64_t k = t0 + tid;
+            sv[tid] = a.v[k];
+            sN[tid] = a.N[k];
+            sS[tid] = a.S[k];
+            sS2[tid] = a.S2[k];
+            sF[tid] = a.Fin[k];
+        }
+        __syncthreads();
+        const bool nomask = BWD ? (t0 > jend) : (t0 + nk - 1 < j0);
+        if (nomask) {
+            for (int kk = 0; kk < nk; kk++) {
+                const double pv = sv[kk], pN = sN[kk], pS = sS[kk], pS2 = sS2[kk], pF = sF[kk];
+#pragma unroll
+                for (int r = 0; r < R; r++) {
+                    double C, P;
+                    if (BWD)
+                        cell_terms(cv[r], cN[r], cS[r], cS2[r], pv, pN, pS, pS2, dd, false, 0.0,
+                                   tab, C, P);
+                    else
+                        cell_terms(pv, pN, pS, pS2, cv[r], cN[r], cS[r], cS2[r], dd, false, 0.0,
+                                   tab, C, P);
+                    const double cand = __builtin_fma(-lam, P, pF + C);
+                    if (cand < best[r]) {
+                        best[r] = cand;
+                        bk[r] = (int32_t)(t0 + kk);
+                    }
+                }
+            }
+        } else {
+            for (int kk = 0; kk < nk; kk++) {
+                const int64_t k = t0 + kk;
+                const double pv = sv[kk], pN = sN[kk], pS = sS[kk], pS2 = sS2[kk], pF = sF[kk];
+#pragma unroll
+                for (int r = 0; r < R; r++) {
+                    const bool ok = BWD ? (k > col[r]) : (k < col[r]);
+                    double C, P;
+                    if (BWD)
+                        cell_terms(cv[r], cN[r], cS[r], cS2[r], pv, pN, pS, pS2, dd, false, 0.0,
+                                   tab, C, P);
+                    else
+                        cell_terms(pv, pN, pS, pS2, cv[r], cN[r], cS[r], cS2[r], dd, false, 0.0,
+                                   tab, C, P);
+                    const double cand = __builtin_fma(-lam, P, pF + C);
+                    if (ok && cand < best[r]) {
+                        best[r] = cand;
+                        bk[r] = (int32_t)k;
+                    }
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < R; r++) {
+        if (col[r] <= jend) {
+            const int64_t idx = (b * a.maxch + c) * CB + r * kBlock + tid;
+            a.pval[idx] = best[r];
+            a.pidx[idx] = bk[r];
+        }
+    }
+}
+
+struct ReduceArgs {
+    LayerArgs L;
+    int64_t CB;
+    double* Fout;
+    // forward main-DP extras (null in the recovery half-DPs)
+    const double* Min;
+    const double* Pin;
+    double* Mout;
+    double* Pout;
+    int32_t* kstar;
+    double* last;  // [3][s+1]: F, MSE, H(I,B) of column p-1 per layer
+    int32_t layer;
+    int32_t last_stride;
+    int64_t p;
+    double c0d;
+};
+
+template <bool BWD>
+__global__ __launch_bounds__(256) void k_dp_reduce(ReduceArgs a) {
+    __shared__ double2 tab[256];
+    load_log2_table(tab);
+    __syncthreads();
+    const int64_t j = a.L.jlo + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j > a.L.jhi) return;
+    const int64_t b = (j - a.L.jlo) / a.CB;
+    const int64_t off = (j - a.L.jlo) - b * a.CB;
+    int64_t j0, jend, klo, khi;
+    block_krange<BWD>(a.L, a.CB, b, j0, jend, klo, khi);
+    const int64_t nch = (khi - klo + 1 + a.L.kc - 1) / a.L.kc;
+    double best = __builtin_huge_val();
+    int32_t bk = -1;
+    for (int64_t c = 0; c < nch; c++) {
+        const int64_t idx = (b * a.L.maxch + c) * a.CB + off;
+        const double val = a.L.pval[idx];
+        if (val < best) {
+            best = val;
+            bk = a.L.pidx[idx];
+        }
+    }
+    a.Fout[j] = best;
+    if (a.Mout && bk >= 0) {
+        double C, P;
+        cell_terms(a.L.v[bk], a.L.N[bk], a.L.S[bk], a.L.S2[bk], a.L.v[j], a.L.N[j], a.L.S[j],
+                   a.L.S2[j], a.L.dd, bk == 0, a.c0d, tab, C, P);
+        const double m = a.Min[bk] + C;
+        const double ph = a.Pin[bk] - P;
+        a.Mout[j] = m;
+        a.Pout[j] = ph;
+        if (a.kstar) a.kstar[j] = bk;
+        if (j == a.p - 1) {
+            a.last[a.layer] = best;
+            a.last[a.last_stride + a.layer] = m;
+            a.last[2 * a.last_stride + a.layer] = ph;
+        }
+    }
+}
+
+// Forward layer 2 from `lo`: F[j] = C[lo,j] + lambda' Phi'[lo,j] (Phi^first
+// when lo == 0), eq. apx_base.  With M non-null also starts the accumulators.
+__global__ __launch_bounds__(256) void k_dp_init_fwd(Hist H, int64_t lo, int64_t jl, int64_t jh,
+                                                     double lam, double* F, double* M, double* Ph,
+                                                     int32_t* kstar, double* last,
+                                                     int32_t last_stride) {
+    __shared__ double2 tab[256];
+    load_log2_table(tab);
+    __syncthreads();
+    const int64_t j = jl + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j > jh) return;
+    double C, P;
+    cell_at(H, lo, j, tab, C, P);
+    const double f = __builtin_fma(-lam, P, 0.0 + C);
+    F[j] = f;
+    if (M) {
+        const double m = 0.0 + C;
+        const double ph = 0.0 - P;
+        M[j] = m;
+        Ph[j] = ph;
+        if (kstar) kstar[j] = (int32_t)lo;
+        if (j == H.p - 1) {
+            last[2] = f;
+            last[last_stride + 2] = m;
+            last[2 * last_stride + 2] = ph;
+        }
+    }
+}
+
+// Backward layer 2 into `hi`: B[j] = C[j,hi] + lambda' Phi[j,hi].
+__global__ __launch_bounds__(256) void k_dp_init_bwd(Hist H, int64_t hi, int64_t jl, int64_t jh,
+                                                     double lam, double* B) {
+    __shared__ double2 tab[256];
+    load_log2_table(tab);
+    __syncthreads();
+    const int64_t j = jl + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j > jh) return;
+    double C, P;
+    cell_at(H, j, hi, tab, C, P);
+    B[j] = __builtin_fma(-lam, P, 0.0 + C);
+}
+
+// eq. apx_final: lowest i in [2, imax] minimising F_i[p-1] (or i = imax when
+// exactly min(s, p) values are required).  out: J, MSE, H(I,B), i*.
+__global__ void k_dp_final(const double* last, int32_t stride, int32_t imax, int32_t exact_s,
+                           double* out) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    int32_t bi = 2;
+    double bj = last[2];
+    for (int32_t i = 3; i <= imax; i++) {
+        const double f = last[i];
+        if (exact_s ? (i == imax) : (f < bj)) {
+            bj = f;
+            bi = i;
+        }
+    }
+    out[0] = bj;
+    out[1] = last[stride + bi];
+    out[2] = last[2 * stride + bi];
+    out[3] = (double)bi;
+}
+
+// Hirschberg split: lowest m in [ml, mh] minimising Fw[m] + Bw[m].
+__global__ __launch_bounds__(256) void k_split(const double* Fw, const double* Bw, int64_t ml,
+                                               int64_t mh, int64_t* m_out) {
+    __shared__ double sv[256];
+    __shared__ int64_t si[256];
+    const int tid = threadIdx.x;
+    double best = __builtin_huge_val();
+    int64_t bm = -1;
+    for (int64_t m = ml + tid; m <= mh; m += 256) {
+        const double tot = Fw[m] + Bw[m];
+        if (tot < best) {
+            best = tot;
+            bm = m;
+        }
+    }
+    sv[tid] = best;
+    si[tid] = bm;
+    __syncthreads();
+    for (int off = 128; off > 0; off >>= 1) {
+        if (tid < off) {
+            const double ov = sv[tid + off];
+            const int64_t oi = si[tid + off];
+            if (oi >= 0 && (si[tid] < 0 || ov < sv[tid] || (ov == sv[tid] && oi < si[tid]))) {
+                sv[tid] = ov;
+                si[tid] = oi;
+            }
+        }
+        __syncthreads();
+    }
+    if (tid == 0) *m_out = si[0];
+}
+
+int64_t choose_kc(int64_t lenmax) {
+    int64_t kc = (lenmax + 31) / 32;
+    kc = (kc + kTK - 1) / kTK * kTK;
+    return kc < kTK ? kTK : kc;
+}
+
+}  // namespace
+
+int64_t dp_partial_entries(int64_t p) {
+    // nblk * maxch * CB with maxch <= 32 and nblk * CB <= p + CB
+    const int64_t CB = kBlock * kColsPerLane;
+    return (p + CB) * 33;
+}
+
+hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st) {
+    constexpr int R = kColsPerLane;
+    const int64_t CB = (int64_t)kBlock * R;
+    const int64_t ncol = L.jhi - L.jlo + 1;
+    if (ncol <= 0) return hipSuccess;
+    const int64_t nblk = (ncol + CB - 1) / CB;
+    // longest predecessor range: last block (forward) or first block (backward)
+    const int64_t lenmax = L.backward ? (L.kb - L.jlo) : (L.jhi - L.kb);
+    const int64_t kc = choose_kc(lenmax);
+    const int64_t maxch = (lenmax + kc - 1) / kc;
+    LayerArgs a;
+    a.v = L.H.v;
+    a.N = L.H.N;
+    a.S = L.H.S;
+    a.S2 = L.H.S2;
+    a.Fin = L.Fin;
+    a.pval = L.pval;
+    a.pidx = L.pidx;
+    a.kb = L.kb;
+    a.jlo = L.jlo;
+    a.jhi = L.jhi;
+    a.kc = kc;
+    a.maxch = (int32_t)maxch;
+    a.dd = L.H.dd;
+    a.lam = L.lam;
+    dim3 grid((unsigned)maxch, (unsigned)nblk);
+    if (L.backward)
+        k_dp_layer<R, true><<<grid, kBlock, 0, st>>>(a);
+    else
+        k_dp_layer<R, false><<<grid, kBlock, 0, st>>>(a);
+    ReduceArgs ra;
+    ra.L = a;
+    ra.CB = CB;
+    ra.Fout = L.Fout;
+    ra.Min = L.Min;
+    ra.Pin = L.Pin;
+    ra.Mout = L.Mout;
+    ra.Pout = L.Pout;
+    ra.kstar = L.kstar;
+    ra.last = L.last;
+    ra.layer = L.layer;
+    ra.last_stride = L.last_stride;
+    ra.p = L.H.p;
+    ra.c0d = L.H.c0d;
+    const unsigned rg = (unsigned)((ncol + 255) / 256);
+    if (L.backward)
+        k_dp_reduce<true><<<rg, 256, 0, st>>>(ra);
+    else
+        k_dp_reduce<false><<<rg, 256, 0, st>>>(ra);
+    return hipGetLastError();
+}
+
+hipError_t launch_dp_init_fwd(const Hist& H, int64_t lo, int64_t jl, int64_t jh, double lam,
+                              double* F, double* M, double* Ph, int32_t* kstar, double* last,
+                              int32_t last_stride, hipStream_t st) {
+    if (jh < jl) return hipSuccess;
+    const unsigned g = (unsigned)((jh - jl + 1 + 255) / 256);
+    k_dp_init_fwd<<<g, 256, 0, st>>>(H, lo, jl, jh, lam, F, M, Ph, kstar, last, last_stride);
+    return hipGetLastError();
+}
+
+hipError_t launch_dp_init_bwd(const Hist& H, int64_t hi, int64_t jl, int64_t jh, double lam,
+                              double* B, hipStream_t st) {
+    if (jh < jl) return hipSuccess;
+    const unsigned g = (unsigned)((jh - jl + 1 + 255) / 256);
+    k_dp_init_bwd<<<g, 256, 0, st>>>(H, hi, jl, jh, lam, B);
+    return hipGetLastError();
+}
+
+hipError_t launch_dp_final(const double* last, int32_t stride, int32_t imax, int32_t exact_s,
+                           double* out, hipStream_t st) {
+    k_dp_final<<<1, 64, 0, st>>>(last, stride, imax, exact_s, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_split(const double* Fw, const double* Bw, int64_t ml, int64_t mh,
+                        int64_t* m_out, hipStream_t st) {
+    k_split<<<1, 256, 0, st>>>(Fw, Bw, ml, mh, m_out);
+    return hipGetLastError();
+}
+
+}  // namespace ecasq

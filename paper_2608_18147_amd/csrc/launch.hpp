@@ -1,0 +1,69 @@
+// Host-side launchers shared by the library's translation units.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "device.hpp"
+
+namespace ecasq {
+
+inline size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// columns per lane in the DP layer kernel
+constexpr int kColsPerLane = 1;
+
+// ---- prep.hip ----
+size_t prep_scratch_bytes(int64_t d);
+hipError_t launch_prep(const void* x, int dt, int64_t d, void* scratch, hipStream_t st, double* v,
+                       double* N, double* S, double* S2, int64_t* p_dev, uint32_t* flags_dev);
+
+// ---- dp.hip ----
+struct DpLayer {
+    Hist H;
+    const double* Fin;
+    double* Fout;
+    double* pval;
+    int32_t* pidx;
+    int64_t kb;    // forward: first predecessor; backward: last predecessor
+    int64_t jlo;   // first column
+    int64_t jhi;   // last column (inclusive)
+    bool backward;
+    double lam;    // lambda' in MSE units
+    // forward main-DP accumulators (all null in the recovery half-DPs)
+    const double* Min;
+    const double* Pin;
+    double* Mout;
+    double* Pout;
+    int32_t* kstar;
+    double* last;
+    int32_t layer;
+    int32_t last_stride;
+};
+int64_t dp_partial_entries(int64_t p);
+hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st);
+hipError_t launch_dp_init_fwd(const Hist& H, int64_t lo, int64_t jl, int64_t jh, double lam,
+                              double* F, double* M, double* Ph, int32_t* kstar, double* last,
+                              int32_t last_stride, hipStream_t st);
+hipError_t launch_dp_init_bwd(const Hist& H, int64_t hi, int64_t jl, int64_t jh, double lam,
+                              double* B, hipStream_t st);
+hipError_t launch_dp_final(const double* last, int32_t stride, int32_t imax, int32_t exact_s,
+                           double* out, hipStream_t st);
+hipError_t launch_split(const double* Fw, const double* Bw, int64_t ml, int64_t mh,
+                        int64_t* m_out, hipStream_t st);
+
+// ---- post.hip ----
+hipError_t launch_refine(const Hist& H, int32_t t, int32_t* u, double lamp, double b,
+                         int32_t budget, int32_t rounds, int32_t exhaustive, int32_t* stats,
+                         hipStream_t st);
+hipError_t launch_metrics(const Hist& H, int32_t t, const int32_t* u, double lam, double s2tot,
+                          double* out, hipStream_t st);
+hipError_t launch_gather(const double* v, const int32_t* u, int32_t t, double* codebook,
+                         int32_t* rank, hipStream_t st);
+hipError_t launch_quantize(const void* x, int dt, int64_t d, const double* codebook, int32_t t,
+                           uint64_t seed, uint8_t* symbols, unsigned long long* hist,
+                           hipStream_t st);
+hipError_t launch_entropy(const unsigned long long* hist, int32_t t, int64_t d, double* ent,
+                          int64_t* hist_out, hipStream_t st);
+
+}  // namespace ecasq

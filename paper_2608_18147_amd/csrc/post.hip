@@ -1,0 +1,348 @@
+// Steps after the DP: three-colour refinement (Sec. 6), solution metrics,
+// codebook gather, and the final unbiased stochastic rounding (Sec. 2) with
+// a plug-in entropy of the symbol histogram.
+#include <hip/hip_fp16.h>
+
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace ecasq {
+
+namespace {
+
+constexpr int kMaxT = 256;
+
+__device__ __forceinline__ double interval_cost(const Hist& H, int64_t a, int64_t b,
+                                                const double2* tab) {
+    double C, P;
+    cell_at(H, a, b, tab, C, P);
+    return C;
+}
+
+// Expected frequencies of a chain u_0 < ... < u_{t-1} (Sec. 4: an interior
+// value gets U[k,l] + D[l,j]; the first value also takes every entry equal to
+// it; the last gets the round-up mass of the last interval), then
+// H(Xhat) = sum_q h(f_q / d), summed in index order.
+__device__ double chain_hout(const Hist& H, int32_t t, const int32_t* u, const double2* tab) {
+    if (t == 1) return hf(H, H.dd, tab);
+    double Hs = 0.0, Uprev = 0.0;
+    for (int32_t r = 0; r < t; r++) {
+        double Ur = 0.0, Dr = 0.0;
+        if (r + 1 < t) ud_at(H, u[r], u[r + 1], Ur, Dr);
+        double f;
+        if (r == 0) f = H.c0 + Dr;
+        else if (r == t - 1) f = Uprev;
+        else f = Uprev + Dr;
+        Hs = Hs + hf(H, f, tab);
+        Uprev = Ur;
+    }
+    return Hs;
+}
+
+// Local Sec. 6 objective of placing u_r at m (neighbours fixed): the MSE of
+// the two adjacent intervals plus lambda' times the entropy terms of the
+// three values whose expected frequencies change.
+__device__ double refine_local(const Hist& H, int32_t t, const int32_t* u, int32_t r, int64_t m,
+                               double lamp, const double2* tab) {
+    const int64_t L = u[r - 1], R = u[r + 1];
+    const double Cl = interval_cost(H, L, m, tab);
+    const double Cr = interval_cost(H, m, R, tab);
+    double Ulm, Dlm, Umr, Dmr;
+    ud_at(H, L, m, Ulm, Dlm);
+    ud_at(H, m, R, Umr, Dmr);
+    double fprev, fnext;
+    if (r - 1 == 0) {
+        fprev = H.c0 + Dlm;
+    } else {
+        double Ua, Da;
+        ud_at(H, u[r - 2], L, Ua, Da);
+        fprev = Ua + Dlm;
+    }
+    const double fcur = Ulm + Dmr;
+    if (r + 1 == t - 1) {
+        fnext = Umr;
+    } else {
+        double Ub, Db;
+        ud_at(H, R, u[r + 2], Ub, Db);
+        fnext = Umr + Db;
+    }
+    const double Hl = (hf(H, fprev, tab) + hf(H, fcur, tab)) + hf(H, fnext, tab);
+    return __builtin_fma(lamp, Hl, Cl + Cr);
+}
+
+// The whole refinement in one block: rounds of colour substeps 0, 1, 2.  All
+// movers of a colour are independent (their objectives share no frequency)
+// and are searched in parallel, one thread each; a substep whose result
+// violates the budget (budget mode) is undone; refinement stops after a round
+// without a committed move.  stats: rounds run, moves committed.
+__global__ __launch_bounds__(256) void k_refine(Hist H, int32_t t, int32_t* __restrict__ ug,
+                                                double lamp, double b, int32_t budget,
+                                                int32_t rounds, int32_t exhaustive,
+                                                int32_t* __restrict__ stats) {
+    __shared__ double2 tab[256];
+    __shared__ int32_t u[kMaxT], nu[kMaxT];
+    __shared__ int32_t moved_s, commit_s;
+    __shared__ double redv[256];
+    __shared__ int64_t redi[256];
+    const int tid = threadIdx.x;
+    load_log2_table(tab);
+    for (int r = tid; r < t; r += blockDim.x) u[r] = ug[r];
+    __syncthreads();
+    int32_t nrun = 0, nmoves = 0;
+    for (int32_t rd = 0; rd < rounds; rd++) {
+        int any = 0;
+        for (int32_t c = 0; c < 3; c++) {
+            for (int r = tid; r < t; r += blockDim.x) nu[r] = u[r];
+            if (tid == 0) moved_s = 0;
+            __syncthreads();
+            if (!exhaustive) {
+                for (int32_t r = 1 + tid; r <= t - 2; r += blockDim.x) {
+                    if (r % 3 != c) continue;
+                    const int64_t L = u[r - 1], R = u[r + 1];
+                    if (R - L < 3) continue;
+                    int64_t lo = L + 1, hi = R - 1;
+                    while (lo < hi) {
+                        const int64_t mid = lo + (hi - lo) / 2;
+                        if (refine_local(H, t, u, r, mid + 1, lamp, tab) <
+                            refine_local(H, t, u, r, mid, lamp, tab))
+                            lo = mid + 1;
+                        else
+                            hi = mid;
+                    }
+                    if (lo != u[r] && refine_local(H, t, u, r, lo, lamp, tab) <
+                                          refine_local(H, t, u, r, u[r], lamp, tab)) {
+                        nu[r] = (int32_t)lo;
+                        atomicAdd(&moved_s, 1);
+                    }
+                }
+            } else {
+                for (int32_t r = 1; r <= t - 2; r++) {
+                    if (r % 3 != c) continue;
+                    const int64_t L = u[r - 1], R = u[r + 1];
+                    if (R - L < 3) continue;
+                    double bv = __builtin_huge_val();
+                    int64_t bm = -1;
+                    for (int64_t m = L + 1 + tid; m < R; m += blockDim.x) {
+                        const double val = refine_local(H, t, u, r, m, lamp, tab);
+                        if (val < bv) {
+                            bv = val;
+                            bm = m;
+                        }
+                    }
+                    redv[tid] = bv;
+                    redi[tid] = bm;
+                    __syncthreads();
+                    for (int off = blockDim.x / 2; off > 0; off >>= 1) {
+                        if (tid < off) {
+                            const double ov = redv[tid + off];
+                            const int64_t oi = redi[tid + off];
+                            if (oi >= 0 && (redi[tid] < 0 || ov < redv[tid] ||
+                                            (ov == redv[tid] && oi < redi[tid]))) {
+                                redv[tid] = ov;
+                                redi[tid] = oi;
+                            }
+                        }
+                        __syncthreads();
+                    }
+                    if (tid == 0) {
+                        const int64_t m = redi[0];
+                        if (m != u[r] &&
+                            redv[0] < refine_local(H, t, u, r, u[r], lamp, tab)) {
+                            nu[r] = (int32_t)m;
+                            moved_s += 1;
+                        }
+                    }
+                    __syncthreads();
+                }
+            }
+            __syncthreads();
+            if (tid == 0) {
+                int32_t moved = moved_s;
+                if (moved && budget && chain_hout(H, t, nu, tab) > b) moved = 0;
+                commit_s = moved;
+            }
+            __syncthreads();
+            const int32_t moved = commit_s;
+            if (moved) {
+                for (int r = tid; r < t; r += blockDim.x) u[r] = nu[r];
+                any = 1;
+                nmoves += moved;
+            }
+            __syncthreads();
+        }
+        nrun++;
+        if (!any) break;
+    }
+    for (int r = tid; r < t; r += blockDim.x) ug[r] = u[r];
+    if (tid == 0) {
+        stats[0] = nrun;
+        stats[1] = nmoves;
+    }
+}
+
+// out: MSE, vNMSE, H(Xhat), H(I,B), vNMSE + lambda H(Xhat), H(Xhat) + 32t/d.
+__global__ void k_metrics(Hist H, int32_t t, const int32_t* __restrict__ u, double lam,
+                          double s2tot, double* __restrict__ out) {
+    __shared__ double2 tab[256];
+    load_log2_table(tab);
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    double mse = 0.0, hs = 0.0;
+    for (int32_t r = 0; r + 1 < t; r++) {
+        double C, P;
+        cell_at(H, u[r], u[r + 1], tab, C, P);
+        mse = mse + C;
+        hs = hs - P;
+    }
+    const double ho = chain_hout(H, t, u, tab);
+    const double vn = s2tot > 0.0 ? mse / s2tot : 0.0;
+    const double lr = __builtin_isfinite(lam) ? lam : 0.0;
+    out[0] = mse;
+    out[1] = vn;
+    out[2] = ho;
+    out[3] = hs;
+    out[4] = __builtin_fma(lr, ho, vn);
+    out[5] = ho + (32.0 * (double)t) / H.dd;
+}
+
+__global__ void k_gather(const double* __restrict__ v, const int32_t* __restrict__ u, int32_t t,
+                         double* __restrict__ codebook, int32_t* __restrict__ rank) {
+    const int r = blockIdx.x * blockDim.x + threadIdx.x;
+    if (r >= t) return;
+    codebook[r] = v[u[r]];
+    if (rank) rank[r] = u[r];
+}
+
+// Philox4x32-10 (Salmon et al., SC'11): ten rounds of two 32x32->64 products
+// mixed with the other words and the round key; the key advances by the two
+// Weyl increments between rounds.
+__device__ __forceinline__ void philox4x32_10(uint32_t (&c)[4], uint32_t k0, uint32_t k1) {
+#pragma unroll
+    for (int rnd = 0; rnd < 10; rnd++) {
+        if (rnd) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        const uint32_t hi0 = __umulhi(0xD2511F53u, c[0]);
+        const uint32_t lo0 = 0xD2511F53u * c[0];
+        const uint32_t hi1 = __umulhi(0xCD9E8D57u, c[2]);
+        const uint32_t lo1 = 0xCD9E8D57u * c[2];
+        const uint32_t n0 = hi1 ^ c[1] ^ k0;
+        const uint32_t n2 = hi0 ^ c[3] ^ k1;
+        c[0] = n0;
+        c[1] = lo1;
+        c[2] = n2;
+        c[3] = lo0;
+    }
+}
+
+template <int DT>
+__device__ __forceinline__ double load_x(const void* x, int64_t i) {
+    if (DT == 0) return (double)reinterpret_cast<const float*>(x)[i];
+    if (DT == 1) return (double)__half2float(reinterpret_cast<const __half*>(x)[i]);
+    const uint32_t bits = ((uint32_t)reinterpret_cast<const uint16_t*>(x)[i]) << 16;
+    return (double)__uint_as_float(bits);
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_quantize(const void* __restrict__ x, int64_t d,
+                                                  const double* __restrict__ cb, int32_t t,
+                                                  uint32_t k0, uint32_t k1,
+                                                  uint8_t* __restrict__ symbols,
+                                                  unsigned long long* __restrict__ hist) {
+    __shared__ double q[kMaxT];
+    __shared__ unsigned int lh[kMaxT];
+    for (int r = threadIdx.x; r < kMaxT; r += blockDim.x) {
+        q[r] = r < t ? cb[r] : 0.0;
+        lh[r] = 0u;
+    }
+    __syncthreads();
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < d;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        uint32_t sym = 0;
+        if (t > 1) {
+            const double xv = load_x<DT>(x, i);
+            int lo = 0, hi = t - 2;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (q[mid] < xv) lo = mid;
+                else hi = mid - 1;
+            }
+            const double pu = (xv - q[lo]) / (q[lo + 1] - q[lo]);
+            uint32_t c[4] = {(uint32_t)i, (uint32_t)((uint64_t)i >> 32), 0u, 0u};
+            philox4x32_10(c, k0, k1);
+            const uint64_t bits = ((((uint64_t)c[1]) << 32) | c[0]) >> 11;
+            const double uu = (double)bits * 0x1p-53;
+            sym = (uint32_t)lo + (uu < pu ? 1u : 0u);
+        }
+        symbols[i] = (uint8_t)sym;
+        atomicAdd(&lh[sym], 1u);
+    }
+    __syncthreads();
+    for (int r = threadIdx.x; r < t; r += blockDim.x)
+        if (lh[r]) atomicAdd(&hist[r], (unsigned long long)lh[r]);
+}
+
+__global__ void k_entropy(const unsigned long long* __restrict__ hist, int32_t t, int64_t d,
+                          double* __restrict__ ent, int64_t* __restrict__ hist_out) {
+    __shared__ double2 tab[256];
+    load_log2_table(tab);
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    double H = 0.0;
+    const double dd = (double)d;
+    for (int32_t r = 0; r < t; r++) {
+        const unsigned long long n = hist[r];
+        if (hist_out) hist_out[r] = (int64_t)n;
+        if (n) {
+            const double y = (double)n / dd;
+            H = H + hfun(y, tab);
+        }
+    }
+    *ent = H;
+}
+
+}  // namespace
+
+hipError_t launch_refine(const Hist& H, int32_t t, int32_t* u, double lamp, double b,
+                         int32_t budget, int32_t rounds, int32_t exhaustive, int32_t* stats,
+                         hipStream_t st) {
+    k_refine<<<1, 256, 0, st>>>(H, t, u, lamp, b, budget, rounds, exhaustive, stats);
+    return hipGetLastError();
+}
+
+hipError_t launch_metrics(const Hist& H, int32_t t, const int32_t* u, double lam, double s2tot,
+                          double* out, hipStream_t st) {
+    k_metrics<<<1, 64, 0, st>>>(H, t, u, lam, s2tot, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_gather(const double* v, const int32_t* u, int32_t t, double* codebook,
+                         int32_t* rank, hipStream_t st) {
+    k_gather<<<(t + 63) / 64, 64, 0, st>>>(v, u, t, codebook, rank);
+    return hipGetLastError();
+}
+
+hipError_t launch_quantize(const void* x, int dt, int64_t d, const double* codebook, int32_t t,
+                           uint64_t seed, uint8_t* symbols, unsigned long long* hist,
+                           hipStream_t st) {
+    int64_t g = (d + 255) / 256;
+    if (g > 4096) g = 4096;
+    if (g < 1) g = 1;
+    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    if (dt == 0)
+        k_quantize<0><<<(unsigned)g, 256, 0, st>>>(x, d, codebook, t, k0, k1, symbols, hist);
+    else if (dt == 1)
+        k_quantize<1><<<(unsigned)g, 256, 0, st>>>(x, d, codebook, t, k0, k1, symbols, hist);
+    else
+        k_quantize<2><<<(unsigned)g, 256, 0, st>>>(x, d, codebook, t, k0, k1, symbols, hist);
+    return hipGetLastError();
+}
+
+hipError_t launch_entropy(const unsigned long long* hist, int32_t t, int64_t d, double* ent,
+                          int64_t* hist_out, hipStream_t st) {
+    k_entropy<<<1, 64, 0, st>>>(hist, t, d, ent, hist_out);
+    return hipGetLastError();
+}
+
+}  // namespace ecasq

@@ -1,0 +1,411 @@
+// Input preparation on the device: ingest, radix sort, weighted histogram and
+// exact prefix sums (the O(d) steps before the DP).
+//
+// The paper sorts a copy of X and works on its weighted histogram (Sec. 2) and
+// evaluates interval costs from prefix counts and sums N, S, S2 (App. D).  Here
+// the prefix sums are exact: every fp32 value is an integer multiple of 2^-149,
+// so S and S2 are accumulated as wide two's-complement integers (5 and 10
+// 64-bit limbs) and rounded to fp64 once, to nearest even.  The result does not
+// depend on the summation order, which lets the scan run in parallel and still
+// match a sequential exact sum bit for bit.
+#include <hip/hip_fp16.h>
+
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace ecasq {
+
+namespace {
+
+constexpr int kSortBlock = 256;
+constexpr int kSortItems = 16;
+constexpr int kSortTile = kSortBlock * kSortItems;
+
+constexpr int kSL = 5;    // limbs of the signed S accumulator
+constexpr int kS2L = 10;  // limbs of the S2 accumulator
+constexpr int kRec = 16;  // u64 words per chunk record: S, S2, run ends
+constexpr int kChunk = 16;
+constexpr int kScanBlock = 256;
+
+// Order-preserving map from binary32 bits (finite) to uint32; -0 becomes +0.
+__device__ __forceinline__ uint32_t f32_key(uint32_t bits) {
+    if (bits == 0x80000000u) bits = 0u;
+    return (bits & 0x80000000u) ? ~bits : (bits | 0x80000000u);
+}
+
+__device__ __forceinline__ uint32_t key_bits(uint32_t k) {
+    return (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void k_ingest(const void* __restrict__ x, int64_t d,
+                                                uint32_t* __restrict__ keys,
+                                                uint32_t* __restrict__ flags) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < d;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        uint32_t bits;
+        if (DT == 0) {
+            bits = reinterpret_cast<const uint32_t*>(x)[i];
+        } else if (DT == 1) {
+            bits = __float_as_uint(__half2float(reinterpret_cast<const __half*>(x)[i]));
+        } else {
+            bits = ((uint32_t)reinterpret_cast<const uint16_t*>(x)[i]) << 16;
+        }
+        if ((bits & 0x7F800000u) == 0x7F800000u) {
+            atomicOr(flags, 1u);
+            bits = 0u;
+        }
+        keys[i] = f32_key(bits);
+    }
+}
+
+__global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t* __restrict__ keys,
+                                                           int64_t n, int shift,
+                                                           uint32_t* __restrict__ hist, int nblk) {
+    __shared__ uint32_t cnt[256];
+    const int tid = threadIdx.x;
+    cnt[tid] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kSortTile;
+    for (int it = 0; it < kSortItems; it++) {
+        const int64_t idx = base + (int64_t)it * kSortBlock + tid;
+        if (idx < n) atomicAdd(&cnt[(keys[idx] >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    hist[(int64_t)tid * nblk + blockIdx.x] = cnt[tid];
+}
+
+// Exclusive scan of m uint32 values in place, one block of 1024 threads.
+__global__ __launch_bounds__(1024) void k_scan_u32(uint32_t* __restrict__ a, int64_t m) {
+    __shared__ uint32_t part[1024];
+    const int tid = threadIdx.x;
+    const int64_t per = (m + 1023) / 1024;
+    const int64_t lo = tid * per;
+    const int64_t hi = lo + per < m ? lo + per : m;
+    uint32_t s = 0;
+    for (int64_t i = lo; i < hi; i++) s += a[i];
+    part[tid] = s;
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {
+        uint32_t t = tid >= off ? part[tid - off] : 0u;
+        __syncthreads();
+        part[tid] += t;
+        __syncthreads();
+    }
+    uint32_t run = part[tid] - s;  // exclusive
+    for (int64_t i = lo; i < hi; i++) {
+        uint32_t v = a[i];
+        a[i] = run;
+        run += v;
+    }
+}
+
+// Stable scatter of one 8-bit digit.  Items are taken in index order
+// (tile, then item slot, then thread); equal digits keep that order.
+__global__ __launch_bounds__(kSortBlock) void k_radix_scatter(const uint32_t* __restrict__ kin,
+                                                              uint32_t* __restrict__ kout,
+                                                              int64_t n, int shift,
+                                                              const uint32_t* __restrict__ hist,
+                                                              int nblk) {
+    __shared__ uint32_t base[256];
+    __shared__ uint32_t wcnt[kSortBlock / 64][256];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    base[tid] = hist[(int64_t)tid * nblk + blockIdx.x];
+    for (int w = 0; w < kSortBlock / 64; w++) wcnt[w][tid] = 0;
+    __syncthreads();
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    const int64_t tile = (int64_t)blockIdx.x * kSortTile;
+    for (int it = 0; it < kSortItems; it++) {
+        const int64_t idx = tile + (int64_t)it * kSortBlock + tid;
+        const bool valid = idx < n;
+        const uint32_t key = valid ? kin[idx] : 0u;
+        const uint32_t dig = (key >> shift) & 255u;
+        uint64_t peers = __ballot(valid);
+        for (int bit = 0; bit < 8; bit++) {
+            const bool set = (dig >> bit) & 1u;
+            const uint64_t bal = __ballot(set);
+            peers &= set ? bal : ~bal;
+        }
+        const uint32_t rank = __popcll(peers & lt_mask);
+        if (valid && rank == 0) wcnt[wave][dig] = __popcll(peers);
+        __syncthreads();
+        if (valid) {
+            uint32_t pos = base[dig] + rank;
+            for (int w = 0; w < wave; w++) pos += wcnt[w][dig];
+            kout[pos] = key;
+        }
+        __syncthreads();
+        uint32_t tot = 0;
+        for (int w = 0; w < kSortBlock / 64; w++) {
+            tot += wcnt[w][tid];
+            wcnt[w][tid] = 0;
+        }
+        base[tid] += tot;
+        __syncthreads();
+    }
+}
+
+// ---- wide integers ---------------------------------------------------------
+
+// a += (neg ? -X : X) mod 2^(64L), where X = (hi:lo) << (64*word).
+template <int L>
+__device__ __forceinline__ void wide_add(uint64_t (&a)[L], int word, uint64_t lo, uint64_t hi,
+                                         bool neg) {
+    uint64_t carry = neg ? 1ull : 0ull;
+#pragma unroll
+    for (int l = 0; l < L; l++) {
+        uint64_t x = (l == word) ? lo : ((l == word + 1) ? hi : 0ull);
+        if (neg) x = ~x;
+        const uint64_t t = a[l] + x;
+        const uint64_t c1 = t < x;
+        const uint64_t t2 = t + carry;
+        const uint64_t c2 = t2 < carry;
+        a[l] = t2;
+        carry = c1 | c2;
+    }
+}
+
+template <int L>
+__device__ __forceinline__ void wide_add_full(uint64_t* a, const uint64_t* b) {
+    uint64_t carry = 0;
+#pragma unroll
+    for (int l = 0; l < L; l++) {
+        const uint64_t t = a[l] + b[l];
+        const uint64_t c1 = t < b[l];
+        const uint64_t t2 = t + carry;
+        const uint64_t c2 = t2 < carry;
+        a[l] = t2;
+        carry = c1 | c2;
+    }
+}
+
+// Round the integer a (two's complement if is_signed) times 2^scale to the
+// nearest double, ties to even.  Requires the result to be a normal double.
+template <int L>
+__device__ double wide_to_double(const uint64_t (&a)[L], bool is_signed, int scale) {
+    uint64_t m[L];
+    const bool neg = is_signed && (a[L - 1] >> 63);
+    uint64_t carry = 1;
+#pragma unroll
+    for (int l = 0; l < L; l++) {
+        if (neg) {
+            const uint64_t t = ~a[l] + carry;
+            carry = (carry && t == 0) ? 1ull : 0ull;
+            m[l] = t;
+        } else {
+            m[l] = a[l];
+        }
+    }
+    int h = -1;
+#pragma unroll
+    for (int l = 0; l < L; l++)
+        if (m[l] != 0) h = l;
+    if (h < 0) return 0.0;
+    uint64_t top = 0, below = 0, rest = 0;
+    int lz = 0;
+#pragma unroll
+    for (int l = 0; l < L; l++) {
+        if (l == h) {
+            lz = __clzll(m[l]);
+            top = m[l] << lz;
+        }
+    }
+#pragma unroll
+    for (int l = 0; l < L; l++) {
+        if (l == h - 1) {
+            if (lz) top |= m[l] >> (64 - lz);
+            below = lz ? (m[l] << lz) : m[l];
+        }
+        if (l < h - 1) rest |= m[l];
+    }
+    const bool sticky = (below | rest) != 0;
+    uint64_t mant = top >> 11;
+    const uint32_t rem = (uint32_t)(top & 0x7FFu);
+    const bool up = rem > 0x400u || (rem == 0x400u && (sticky || (mant & 1ull)));
+    mant += up ? 1ull : 0ull;
+    const int e2 = 64 * h + (63 - lz) - 52 + scale;
+    const double r = ldexp((double)mant, e2);
+    return neg ? -r : r;
+}
+
+struct Term {
+    uint32_t M;   // integer mantissa (<= 2^24)
+    int sh;       // |x| = M * 2^(sh - 149)
+    bool neg;
+};
+
+__device__ __forceinline__ Term term_of(uint32_t bits) {
+    const uint32_t ex = (bits >> 23) & 0xFFu;
+    const uint32_t mf = bits & 0x7FFFFFu;
+    Term t;
+    t.M = ex ? (mf | 0x800000u) : mf;
+    t.sh = ex ? (int)ex - 1 : 0;
+    t.neg = (bits >> 31) != 0;
+    return t;
+}
+
+__device__ __forceinline__ void accumulate(uint64_t (&s)[kSL], uint64_t (&q)[kS2L], const Term& t) {
+    {
+        const int b = t.sh & 63;
+        const uint64_t M = t.M;
+        const uint64_t lo = M << b;
+        const uint64_t hi = b ? (M >> (64 - b)) : 0ull;
+        wide_add<kSL>(s, t.sh >> 6, lo, hi, t.neg);
+    }
+    {
+        const int sh2 = 2 * t.sh;
+        const int b = sh2 & 63;
+        const uint64_t M2 = (uint64_t)t.M * (uint64_t)t.M;
+        const uint64_t lo = M2 << b;
+        const uint64_t hi = b ? (M2 >> (64 - b)) : 0ull;
+        wide_add<kS2L>(q, sh2 >> 6, lo, hi, false);
+    }
+}
+
+// Per-chunk totals: S (5 words), S2 (10 words), number of run ends (1 word).
+__global__ __launch_bounds__(kScanBlock) void k_scan_local(const uint32_t* __restrict__ keys,
+                                                           int64_t d, int64_t nchunk,
+                                                           uint64_t* __restrict__ rec) {
+    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= nchunk) return;
+    uint64_t s[kSL] = {0}, q[kS2L] = {0};
+    uint64_t ends = 0;
+    const int64_t i0 = c * kChunk;
+    for (int e = 0; e < kChunk; e++) {
+        const int64_t i = i0 + e;
+        if (i >= d) break;
+        const uint32_t k = keys[i];
+        accumulate(s, q, term_of(key_bits(k)));
+        if (i == d - 1 || keys[i + 1] != k) ends++;
+    }
+    uint64_t* r = rec + c * kRec;
+#pragma unroll
+    for (int l = 0; l < kSL; l++) r[l] = s[l];
+#pragma unroll
+    for (int l = 0; l < kS2L; l++) r[kSL + l] = q[l];
+    r[kRec - 1] = ends;
+}
+
+__device__ __forceinline__ void rec_add(uint64_t* a, const uint64_t* b) {
+    wide_add_full<kSL>(a, b);
+    wide_add_full<kS2L>(a + kSL, b + kSL);
+    a[kRec - 1] += b[kRec - 1];
+}
+
+// Exclusive scan of the chunk records in place (one block); writes the number
+// of distinct values to *p_out.
+__global__ __launch_bounds__(kScanBlock) void k_scan_records(uint64_t* __restrict__ rec,
+                                                             int64_t nchunk,
+                                                             int64_t* __restrict__ p_out) {
+    __shared__ uint64_t part[kScanBlock][kRec];
+    const int tid = threadIdx.x;
+    const int64_t per = (nchunk + kScanBlock - 1) / kScanBlock;
+    const int64_t lo = tid * per;
+    const int64_t hi = lo + per < nchunk ? lo + per : nchunk;
+    uint64_t acc[kRec] = {0};
+    for (int64_t c = lo; c < hi; c++) rec_add(acc, rec + c * kRec);
+    for (int l = 0; l < kRec; l++) part[tid][l] = acc[l];
+    __syncthreads();
+    for (int off = 1; off < kScanBlock; off <<= 1) {
+        uint64_t t[kRec];
+        const bool on = tid >= off;
+        for (int l = 0; l < kRec; l++) t[l] = on ? part[tid - off][l] : 0ull;
+        __syncthreads();
+        if (on) rec_add(part[tid], t);
+        __syncthreads();
+    }
+    uint64_t run[kRec];
+    for (int l = 0; l < kRec; l++) run[l] = tid ? part[tid - 1][l] : 0ull;
+    if (tid == kScanBlock - 1) *p_out = (int64_t)part[tid][kRec - 1];
+    for (int64_t c = lo; c < hi; c++) {
+        uint64_t cur[kRec];
+        for (int l = 0; l < kRec; l++) cur[l] = rec[c * kRec + l];
+        for (int l = 0; l < kRec; l++) rec[c * kRec + l] = run[l];
+        rec_add(run, cur);
+    }
+}
+
+// Walk each chunk from its exclusive prefix and write the histogram entry of
+// every run end: v[u], N[u] (inclusive count), S[u], S2[u] (rounded once).
+__global__ __launch_bounds__(kScanBlock) void k_scan_emit(const uint32_t* __restrict__ keys,
+                                                          int64_t d, int64_t nchunk,
+                                                          const uint64_t* __restrict__ rec,
+                                                          double* __restrict__ v,
+                                                          double* __restrict__ N,
+                                                          double* __restrict__ S,
+                                                          double* __restrict__ S2) {
+    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= nchunk) return;
+    uint64_t s[kSL], q[kS2L];
+    const uint64_t* r = rec + c * kRec;
+#pragma unroll
+    for (int l = 0; l < kSL; l++) s[l] = r[l];
+#pragma unroll
+    for (int l = 0; l < kS2L; l++) q[l] = r[kSL + l];
+    int64_t u = (int64_t)r[kRec - 1];
+    const int64_t i0 = c * kChunk;
+    for (int e = 0; e < kChunk; e++) {
+        const int64_t i = i0 + e;
+        if (i >= d) break;
+        const uint32_t k = keys[i];
+        const uint32_t bits = key_bits(k);
+        accumulate(s, q, term_of(bits));
+        if (i == d - 1 || keys[i + 1] != k) {
+            v[u] = (double)__uint_as_float(bits);
+            N[u] = (double)(i + 1);
+            S[u] = wide_to_double<kSL>(s, true, -149);
+            S2[u] = wide_to_double<kS2L>(q, false, -298);
+            u++;
+        }
+    }
+}
+
+}  // namespace
+
+size_t prep_scratch_bytes(int64_t d) {
+    const int64_t nblk = (d + kSortTile - 1) / kSortTile;
+    const int64_t nchunk = (d + kChunk - 1) / kChunk;
+    size_t b = 0;
+    b += align256(sizeof(uint32_t) * d) * 2;           // keys, ping-pong
+    b += align256(sizeof(uint32_t) * 256 * nblk);      // digit histogram
+    b += align256(sizeof(uint64_t) * kRec * nchunk);   // chunk records
+    b += align256(sizeof(uint32_t) * 4);               // flags
+    return b;
+}
+
+hipError_t launch_prep(const void* x, int dt, int64_t d, void* scratch, hipStream_t st, double* v,
+                       double* N, double* S, double* S2, int64_t* p_dev, uint32_t* flags_dev) {
+    const int64_t nblk = (d + kSortTile - 1) / kSortTile;
+    const int64_t nchunk = (d + kChunk - 1) / kChunk;
+    char* w = static_cast<char*>(scratch);
+    uint32_t* k0 = reinterpret_cast<uint32_t*>(w);
+    w += align256(sizeof(uint32_t) * d);
+    uint32_t* k1 = reinterpret_cast<uint32_t*>(w);
+    w += align256(sizeof(uint32_t) * d);
+    uint32_t* hist = reinterpret_cast<uint32_t*>(w);
+    w += align256(sizeof(uint32_t) * 256 * nblk);
+    uint64_t* rec = reinterpret_cast<uint64_t*>(w);
+
+    const int ig = (int)((d + 255) / 256 < 65536 ? (d + 255) / 256 : 65536);
+    if (dt == 0) k_ingest<0><<<ig, 256, 0, st>>>(x, d, k0, flags_dev);
+    else if (dt == 1) k_ingest<1><<<ig, 256, 0, st>>>(x, d, k0, flags_dev);
+    else k_ingest<2><<<ig, 256, 0, st>>>(x, d, k0, flags_dev);
+    for (int pass = 0; pass < 4; pass++) {
+        const int shift = 8 * pass;
+        k_radix_hist<<<(unsigned)nblk, kSortBlock, 0, st>>>(k0, d, shift, hist, (int)nblk);
+        k_scan_u32<<<1, 1024, 0, st>>>(hist, 256 * nblk);
+        k_radix_scatter<<<(unsigned)nblk, kSortBlock, 0, st>>>(k0, k1, d, shift, hist, (int)nblk);
+        uint32_t* t = k0;
+        k0 = k1;
+        k1 = t;
+    }
+    const unsigned sg = (unsigned)((nchunk + kScanBlock - 1) / kScanBlock);
+    k_scan_local<<<sg, kScanBlock, 0, st>>>(k0, d, nchunk, rec);
+    k_scan_records<<<1, kScanBlock, 0, st>>>(rec, nchunk, p_dev);
+    k_scan_emit<<<sg, kScanBlock, 0, st>>>(k0, d, nchunk, rec, v, N, S, S2);
+    return hipGetLastError();
+}
+
+}  // namespace ecasq

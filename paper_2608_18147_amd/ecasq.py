@@ -1,0 +1,251 @@
+"""Python binding of libecasq (include/ecasq.h): argument marshalling only.
+
+Every step of the computation runs in the library's HIP kernels; PyTorch
+provides device memory and the current stream.  The functions carry the C
+names.  If libecasq.so is missing or cannot be loaded, the first call raises:
+there is no fallback.
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libecasq.so")
+
+ECASQ_OK = 0
+ECASQ_EINVAL = -1
+ECASQ_ENONFINITE = -2
+ECASQ_EINFEASIBLE = -3
+ECASQ_ENOMEM = -4
+ECASQ_EHIP = -5
+ECASQ_EWORKSPACE = -6
+
+_DTYPES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
+
+
+class ecasq_options(ctypes.Structure):
+    _fields_ = [
+        ("refine_rounds", ctypes.c_int32),
+        ("refine_exhaustive", ctypes.c_int32),
+        ("exact_s", ctypes.c_int32),
+        ("max_search_iters", ctypes.c_int32),
+        ("recovery", ctypes.c_int32),
+    ]
+
+
+class ecasq_info(ctypes.Structure):
+    _fields_ = [
+        ("t", ctypes.c_int32),
+        ("p", ctypes.c_int32),
+        ("lambda_", ctypes.c_double),
+        ("mse", ctypes.c_double),
+        ("vnmse", ctypes.c_double),
+        ("entropy", ctypes.c_double),
+        ("entropy_surrogate", ctypes.c_double),
+        ("objective", ctypes.c_double),
+        ("rate_total", ctypes.c_double),
+        ("dp_solves", ctypes.c_int32),
+        ("refine_rounds_run", ctypes.c_int32),
+        ("cells", ctypes.c_int64),
+        ("status", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+    ]
+
+    def as_dict(self):
+        d = {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+        d["lambda"] = d.pop("lambda_")
+        return d
+
+
+class EcasqError(RuntimeError):
+    def __init__(self, status):
+        self.status = status
+        super().__init__(f"ecasq status {status}: {ecasq_status_string(status)}")
+
+
+_lib = None
+EXPORTS = (
+    "ecasq_default_options", "ecasq_solve", "ecasq_solve_ex", "ecasq_solve_lagrangian",
+    "ecasq_quantize", "ecasq_solve_batched", "ecasq_workspace_size", "ecasq_status_string",
+    "ecasq_histogram", "ecasq_dp_trace",
+)
+
+
+def lib():
+    """Load libecasq.so (built in place by build.py); raises if it is absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with python -m "
+                           "paper_2608_18147_amd.build")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32, dbl = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_double
+    P = ctypes.POINTER
+    L.ecasq_default_options.argtypes = [P(ecasq_options)]
+    L.ecasq_default_options.restype = None
+    L.ecasq_solve.argtypes = [vp, i32, i64, i32, dbl, vp, vp, vp, P(ecasq_info)]
+    L.ecasq_solve_ex.argtypes = [vp, i32, i64, i32, dbl, P(ecasq_options), vp, vp, vp,
+                                 P(ecasq_info), vp, ctypes.c_size_t]
+    L.ecasq_solve_lagrangian.argtypes = [vp, i32, i64, i32, dbl, P(ecasq_options), vp, vp, vp,
+                                         P(ecasq_info)]
+    L.ecasq_quantize.argtypes = [vp, i32, i64, vp, i32, ctypes.c_uint64, vp, vp, vp, vp]
+    L.ecasq_solve_batched.argtypes = [vp, i32, i64, i64, i32, dbl, P(ecasq_options), vp, vp,
+                                      vp, vp]
+    L.ecasq_workspace_size.argtypes = [i64, i32, i32]
+    L.ecasq_workspace_size.restype = ctypes.c_size_t
+    L.ecasq_status_string.argtypes = [i32]
+    L.ecasq_status_string.restype = ctypes.c_char_p
+    L.ecasq_histogram.argtypes = [vp, i32, i64, vp, vp, vp, vp, vp, P(i64)]
+    L.ecasq_dp_trace.argtypes = [vp, i32, i64, i32, dbl, vp, vp, vp, vp]
+    for name in ("ecasq_solve", "ecasq_solve_ex", "ecasq_solve_lagrangian", "ecasq_quantize",
+                 "ecasq_solve_batched", "ecasq_histogram", "ecasq_dp_trace"):
+        getattr(L, name).restype = i32
+    _lib = L
+    return L
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _check_x(x):
+    if not isinstance(x, torch.Tensor) or not x.is_cuda:
+        raise TypeError("x must be a CUDA (HIP) tensor")
+    if x.dtype not in _DTYPES:
+        raise TypeError(f"unsupported dtype {x.dtype}")
+    return x.contiguous().reshape(-1)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else None
+
+
+def _raise(st, allow=(ECASQ_OK,)):
+    if st not in allow:
+        raise EcasqError(st)
+
+
+def ecasq_default_options(**overrides):
+    o = ecasq_options()
+    lib().ecasq_default_options(ctypes.byref(o))
+    for k, v in overrides.items():
+        setattr(o, k, int(v))
+    return o
+
+
+def ecasq_status_string(status):
+    return lib().ecasq_status_string(int(status)).decode()
+
+
+def ecasq_workspace_size(d, s, flags=0):
+    return int(lib().ecasq_workspace_size(int(d), int(s), int(flags)))
+
+
+def ecasq_solve(x, s, bits_per_entry, options=None, stream=None, workspace=None):
+    """Budget mode.  Returns (codebook fp64 [t], rank int32 [t], info dict)."""
+    x = _check_x(x)
+    cb = torch.empty(int(s), dtype=torch.float64, device=x.device)
+    rk = torch.empty(int(s), dtype=torch.int32, device=x.device)
+    info = ecasq_info()
+    if options is None and workspace is None:
+        st = lib().ecasq_solve(_ptr(x), _DTYPES[x.dtype], x.numel(), int(s),
+                               float(bits_per_entry), _stream(stream), _ptr(cb), _ptr(rk),
+                               ctypes.byref(info))
+    else:
+        o = options if options is not None else ecasq_default_options()
+        ws = _ptr(workspace)
+        nb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+        st = lib().ecasq_solve_ex(_ptr(x), _DTYPES[x.dtype], x.numel(), int(s),
+                                  float(bits_per_entry), ctypes.byref(o), _stream(stream),
+                                  _ptr(cb), _ptr(rk), ctypes.byref(info), ws, nb)
+    _raise(st, (ECASQ_OK, ECASQ_EINFEASIBLE))
+    t = info.t
+    return cb[:t], rk[:t], info.as_dict()
+
+
+ecasq_solve_ex = ecasq_solve
+
+
+def ecasq_solve_lagrangian(x, s, lam, options=None, stream=None):
+    """Fixed multiplier (vNMSE units).  Returns (codebook, rank, info dict)."""
+    x = _check_x(x)
+    cb = torch.empty(int(s), dtype=torch.float64, device=x.device)
+    rk = torch.empty(int(s), dtype=torch.int32, device=x.device)
+    info = ecasq_info()
+    o = options if options is not None else ecasq_default_options()
+    st = lib().ecasq_solve_lagrangian(_ptr(x), _DTYPES[x.dtype], x.numel(), int(s), float(lam),
+                                      ctypes.byref(o), _stream(stream), _ptr(cb), _ptr(rk),
+                                      ctypes.byref(info))
+    _raise(st)
+    t = info.t
+    return cb[:t], rk[:t], info.as_dict()
+
+
+def ecasq_quantize(x, codebook, seed, stream=None):
+    """Returns (symbols uint8 [d], empirical entropy (0-d fp64 tensor), hist int64 [t])."""
+    x = _check_x(x)
+    cb = codebook.to(device=x.device, dtype=torch.float64).contiguous()
+    t = cb.numel()
+    sym = torch.empty(x.numel(), dtype=torch.uint8, device=x.device)
+    ent = torch.empty((), dtype=torch.float64, device=x.device)
+    hist = torch.empty(t, dtype=torch.int64, device=x.device)
+    st = lib().ecasq_quantize(_ptr(x), _DTYPES[x.dtype], x.numel(), _ptr(cb), t,
+                              ctypes.c_uint64(int(seed) & (2 ** 64 - 1)), _stream(stream),
+                              _ptr(sym), _ptr(ent), _ptr(hist))
+    _raise(st)
+    return sym, ent, hist
+
+
+def ecasq_solve_batched(x, s, bits_per_entry, options=None, stream=None):
+    """x: [n, d] rows.  Returns (codebooks fp64 [n, s], t int32 [n], infos uint8 view)."""
+    if x.dim() != 2:
+        raise ValueError("x must be [n, d]")
+    n, d = x.shape
+    xc = _check_x(x)
+    cbs = torch.zeros((n, int(s)), dtype=torch.float64, device=x.device)
+    tt = torch.zeros(n, dtype=torch.int32, device=x.device)
+    infos = torch.zeros((n, ctypes.sizeof(ecasq_info)), dtype=torch.uint8, device=x.device)
+    o = options if options is not None else ecasq_default_options()
+    st = lib().ecasq_solve_batched(_ptr(xc), _DTYPES[x.dtype], n, d, int(s),
+                                   float(bits_per_entry), ctypes.byref(o), _stream(stream),
+                                   _ptr(cbs), _ptr(tt), _ptr(infos))
+    _raise(st, (ECASQ_OK, ECASQ_EINFEASIBLE))
+    return cbs, tt, infos
+
+
+def infos_to_dicts(infos):
+    """Decode the device info array of ecasq_solve_batched."""
+    raw = infos.cpu().numpy().tobytes()
+    sz = ctypes.sizeof(ecasq_info)
+    return [ecasq_info.from_buffer_copy(raw[i * sz:(i + 1) * sz]).as_dict()
+            for i in range(len(raw) // sz)]
+
+
+def ecasq_histogram(x, stream=None):
+    """Sorted distinct values and exact prefix sums: (v, N, S, S2) fp64 [p]."""
+    x = _check_x(x)
+    d = x.numel()
+    bufs = [torch.empty(d, dtype=torch.float64, device=x.device) for _ in range(4)]
+    p = ctypes.c_int64(0)
+    st = lib().ecasq_histogram(_ptr(x), _DTYPES[x.dtype], d, _stream(stream),
+                               *[_ptr(b) for b in bufs], ctypes.byref(p))
+    _raise(st)
+    return tuple(b[: p.value] for b in bufs)
+
+
+def ecasq_dp_trace(x, s, lam, stream=None):
+    """All layers of one forward solve: F [(s+1), d] fp64 (NaN where unset),
+    kstar [(s+1), d] int32 (-1 where unset) and (J, MSE, H(I,B), i*, cells)."""
+    x = _check_x(x)
+    d = x.numel()
+    F = torch.full((int(s) + 1, d), float("nan"), dtype=torch.float64, device=x.device)
+    K = torch.full((int(s) + 1, d), -1, dtype=torch.int32, device=x.device)
+    out = (ctypes.c_double * 5)()
+    st = lib().ecasq_dp_trace(_ptr(x), _DTYPES[x.dtype], d, int(s), float(lam), _stream(stream),
+                              _ptr(F), _ptr(K), out)
+    _raise(st)
+    return F, K, tuple(out)
