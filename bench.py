@@ -1,0 +1,172 @@
+#!/usr/bin/env python3
+"""Throughput of the ECASQ hot path on one MI355X.
+
+One step = the whole path on one synthetic vector already resident in HBM:
+sort + histogram + exact prefix sums, the lambda search (one full dp_APX
+solve per query), Hirschberg recovery, three-colour refinement (5 rounds at
+most) and the final Philox stochastic rounding with its empirical entropy.
+
+Default workload (weights_256k): fp32, d = 2^18, 0.9 Normal(0, 0.01) +
+0.1 Laplace(0, 0.1), s = 32, budget 2.0 bits/entry, seed 0.
+
+Printed (one JSON line): DP cell-updates/s counted as s*d^2/2 per DP solve
+(the nominal unit), the roofline of the DP layer kernel measured with HIP
+events on its own stream, and the CPU oracle timed on a bounded sample.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+# Algorithmic fp64 operations per DP cell in the canonical cell arithmetic:
+# 4 range differences, 2 fma (tu, td), 2 fma (C), w*d, one IEEE division
+# (counted as 1), 2 products (yu, yd), two log2 evaluations of 16 flops each
+# (fma for r, 5 Horner fma, 1 mul, 1 add, 1 final fma), 1 mul + 1 fma for the
+# entropy term, 1 add + 1 fma for the candidate.  fma counts 2.
+FLOPS_PER_CELL = 54
+FP64_VECTOR_PEAK_TFLOPS = 78.6
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(x, s, lam, sample_d):
+    """The oracle's forward DP on the sample_d smallest entries of the same
+    input (exact cell arithmetic, OpenMP over columns)."""
+    import numpy as np
+
+    from oracle import pipeline
+
+    xs = np.sort(x)[:sample_d]
+    H = pipeline.prepare(xs)
+    t0 = time.perf_counter()
+    r = pipeline.dp_forward(H, s, lam * H.s2tot)
+    dt = time.perf_counter() - t0
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    nominal = s * sample_d * sample_d / 2.0
+    return {
+        "value": nominal / dt,
+        "unit": "cell-updates/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"one forward dp_APX solve (s={s}, lambda={lam}) on the {sample_d} smallest "
+                   f"entries of the same input: {r['cells']} cells evaluated in {dt:.2f} s; "
+                   f"value counts s*d^2/2 with d={sample_d}"),
+        "exact_cells_per_s": r["cells"] / dt,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="weights_256k")
+    ap.add_argument("--budget", type=float, default=None)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-sample", type=int, default=16384)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the single-vector path is not sharded across "
+              "GPUs in this build (see DESIGN.md for how it would shard)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_18147_amd import ecasq, inputs
+
+    w = inputs.WORKLOADS[args.workload]
+    if "rows" in w:
+        raise SystemExit("use a single-vector workload")
+    d, s = w["d"], w["s"]
+    b = args.budget if args.budget is not None else w["budgets"][0]
+    x = inputs.make(args.workload, seed=args.seed)
+    xd = torch.from_numpy(x).to("cuda")
+    torch.cuda.synchronize()
+
+    def step():
+        cb, rk, info = ecasq.ecasq_solve(xd, s, b)
+        sym, ent, hist = ecasq.ecasq_quantize(xd, cb, args.seed)
+        return info, ent
+
+    for i in range(args.warmup):
+        t0 = time.perf_counter()
+        info, ent = step()
+        torch.cuda.synchronize()
+        log(f"warmup {i + 1}/{args.warmup}: {time.perf_counter() - t0:.2f} s, "
+            f"{info['dp_solves']} DP solves, t={info['t']}")
+
+    ecasq.ecasq_timing_enable(True)
+    ecasq.ecasq_timing_read(reset=True)
+    infos = []
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        t0 = time.perf_counter()
+        info, ent = step()
+        infos.append((info, ent))
+        log(f"step {i + 1}/{args.steps}: {time.perf_counter() - t0:.2f} s")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    ms, launches, cells = ecasq.ecasq_timing_read()
+    ecasq.ecasq_timing_enable(False)
+
+    nominal = sum(inf["dp_solves"] * s * d * d / 2.0 for inf, _ in infos)
+    exact = sum(inf["cells"] for inf, _ in infos)
+    value = nominal / elapsed
+    avg_ms = ms / max(launches, 1)
+    achieved = FLOPS_PER_CELL * (cells / max(launches, 1)) / (avg_ms * 1e-3) / 1e12
+    info, ent = infos[-1]
+    out = {
+        "metric": "DP cell-updates/s (s*d^2/2 per solve)",
+        "value": value,
+        "unit": "cell-updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload, "d": d, "s": s, "budget_bits": b, "seed": args.seed,
+            "refine_rounds": 5, "recovery": "hirschberg", "input_dtype": "f32",
+        },
+        "roofline": {
+            "bound": "alu",
+            "kernel": "k_dp_layer (fp64 VALU)",
+            "achieved": achieved,
+            "peak": FP64_VECTOR_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
+            "traffic": None,
+            "flops_per_cell": FLOPS_PER_CELL,
+            "avg_launch_ms": avg_ms,
+            "launches": launches,
+            "cells_per_s": cells / (ms * 1e-3) if ms > 0 else None,
+        },
+        "exact_cells_per_s": exact / elapsed,
+        "dp_solves_per_step": info["dp_solves"],
+        "solution": {
+            "t": info["t"], "p": info["p"], "lambda": info["lambda"], "vnmse": info["vnmse"],
+            "entropy": info["entropy"], "entropy_surrogate": info["entropy_surrogate"],
+            "empirical_entropy": float(ent), "refine_rounds_run": info["refine_rounds_run"],
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        out["cpu_baseline"] = cpu_baseline(x, s, 0.1, args.cpu_sample)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

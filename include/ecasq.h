@@ -163,6 +163,18 @@ ecasq_status ecasq_histogram(const void *x, ecasq_dtype dt, int64_t d, void *str
 ecasq_status ecasq_dp_trace(const void *x, ecasq_dtype dt, int64_t d, int32_t s, double lambda,
                             void *stream, double *F, int32_t *kstar, double *out5);
 
+/*
+ * Kernel timing for measurement tools.  While enabled (process-wide), every
+ * launch of the DP layer kernel is bracketed by two HIP events recorded on the
+ * stream it runs on; the elapsed times are read when the solve synchronizes.
+ * ecasq_timing_read returns the summed milliseconds, the number of timed
+ * launches and the DP cells those launches evaluated (host pointers, any may
+ * be NULL); reset != 0 clears the totals.  Not thread-safe.
+ */
+void ecasq_timing_enable(int32_t on);
+void ecasq_timing_read(double *layer_ms, int64_t *layer_launches, int64_t *layer_cells,
+                       int32_t reset);
+
 #ifdef __cplusplus
 }
 #endif

@@ -27,10 +27,11 @@
  *     C  = fma(v_b, tu, fma(v_a, sa, -s2))
  *   DP cell entropy (g form):
  *     g = 1/(w*d)   yu = tu*g   yd = td*g  (+ c0/d if a == 0, first interval)
- *     P = fma(max(yu,0), log2c(yu), max(yd,0)*log2c(yd))      (P = -Phi)
+ *     mu = max(yu,0)   md = max(yd,0)
+ *     P = fma(mu, log2c(mu), md*log2c(md))                      (P = -Phi)
  *     cand = fma(-lambda', P, F_prev + C)
  *   refinement / output-entropy (inv form):
- *     U = tu*(1/w)   D = td*(1/w)   h(f) = -(max(y,0)*log2c(y)), y = f/d
+ *     U = tu*(1/w)   D = td*(1/w)   h(f) = -(m*log2c(m)), m = max(f/d, 0)
  *   log2c: table-driven, see log2c() below.
  */
 #include <math.h>
@@ -52,10 +53,11 @@ void orc_set_log2_table(const double *invc, const double *lc)
 }
 
 /* Canonical base-2 logarithm.  For a positive normal y it returns log2(y) to
- * about one ulp; for any other finite y it returns some finite value (callers
- * multiply it by max(y, 0)).  Steps: y = 2^e * z with z in [~0.7073, ~1.4147)
- * selected by subtracting an offset from y's high word; table entry i (top 8
- * bits of the reduced mantissa) gives invc ~ 1/z and lc = log2(1/invc);
+ * about one ulp; for y = 0 or a subnormal y it returns some finite value (its
+ * callers multiply by y).  Steps: e = (high word of y minus an offset) >> 20
+ * and z = ldexp(y, -e), so z lies in [~0.7073, ~1.4147) for positive normal y;
+ * table entry i (top 8 bits of the reduced mantissa) gives invc ~ 1/z and
+ * lc = log2(1/invc);
  * r = z*invc - 1 with |r| <= 2^-9; log2(1+r) from the degree-6 Taylor series of
  * log1p times RN(1/ln 2). */
 static double log2c(double y)
@@ -63,14 +65,10 @@ static double log2c(double y)
     uint64_t bits;
     memcpy(&bits, &y, 8);
     uint32_t hi = (uint32_t)(bits >> 32);
-    uint32_t lo = (uint32_t)bits;
     uint32_t tmp = hi - OFF_HI;
     int32_t e = ((int32_t)tmp) >> 20;
     uint32_t i = (tmp >> (20 - TBITS)) & (TSIZE - 1);
-    uint32_t zhi = hi - (tmp & 0xFFF00000u);
-    uint64_t zb = ((uint64_t)zhi << 32) | lo;
-    double z;
-    memcpy(&z, &zb, 8);
+    double z = ldexp(y, -e);
     double r = fma(z, g_invc[i], -1.0);
     double q = -1.0 / 6.0;
     q = fma(q, r, 1.0 / 5.0);
@@ -86,7 +84,11 @@ static double log2c(double y)
 double orc_log2c(double y) { return log2c(y); }
 
 /* h(y) = -y log2 y for y > 0, 0 otherwise (Sec. 4, definition of h). */
-static double hfun(double y) { return -(fmax(y, 0.0) * log2c(y)); }
+static double hfun(double y)
+{
+    double m = fmax(y, 0.0);
+    return -(m * log2c(m));
+}
 
 double orc_h(double y) { return hfun(y); }
 
@@ -120,9 +122,9 @@ static void cell_terms(const hist_t *H, int64_t a, int64_t b, double *C, double 
     double yd = td * g;
     if (a == 0)
         yd = yd + H->c0d;
-    double lu = log2c(yu);
-    double ld = log2c(yd);
-    *P = fma(fmax(yu, 0.0), lu, fmax(yd, 0.0) * ld);
+    double mu = fmax(yu, 0.0);
+    double md = fmax(yd, 0.0);
+    *P = fma(mu, log2c(mu), md * log2c(md));
 }
 
 /* U[a,b] and D[a,b] of (v_a, v_b] in the inv form (App. D closed forms). */

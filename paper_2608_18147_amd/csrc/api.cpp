@@ -201,6 +201,7 @@ ecasq_status dp_solve(Ctx& c, double lam, int32_t exact_s, Point& out, double* J
         L.last = last;
         L.layer = i;
         L.last_stride = ls;
+        L.cells = tri_cells(p - i + 1);
         HIP_TRY(launch_dp_layer(L, c.st));
         if (Fdump)
             HIP_TRY(hipMemcpyAsync(Fdump + (int64_t)i * stride + (i - 1), F[1 - cur] + (i - 1),
@@ -212,6 +213,7 @@ ecasq_status dp_solve(Ctx& c, double lam, int32_t exact_s, Point& out, double* J
     double r[4];
     HIP_TRY(hipMemcpyAsync(r, res, sizeof r, hipMemcpyDeviceToHost, c.st));
     HIP_TRY(hipStreamSynchronize(c.st));
+    timing_flush();
     out.lam = lam;
     out.H = r[2];
     out.M = r[1] / c.s2tot;
@@ -307,8 +309,9 @@ ecasq_status hirschberg(Ctx& c, double lamp, int64_t lo, int64_t hi, int32_t n, 
         L.jhi = hi - (n - q);
         L.backward = false;
         L.lam = lamp;
+        for (int64_t j = L.jlo; j <= L.jhi; j++) L.cells += j - L.kb;
         HIP_TRY(launch_dp_layer(L, c.st));
-        for (int64_t j = L.jlo; j <= L.jhi; j++) c.cells += j - L.kb;
+        c.cells += L.cells;
         fc = 1 - fc;
     }
     // backward half: n-r values ending at hi
@@ -331,8 +334,9 @@ ecasq_status hirschberg(Ctx& c, double lamp, int64_t lo, int64_t hi, int32_t n, 
         L.jhi = hi - q + 1;
         L.backward = true;
         L.lam = lamp;
+        for (int64_t j = L.jlo; j <= L.jhi; j++) L.cells += L.kb - j;
         HIP_TRY(launch_dp_layer(L, c.st));
-        for (int64_t j = L.jlo; j <= L.jhi; j++) c.cells += L.kb - j;
+        c.cells += L.cells;
         bc = 1 - bc;
     }
     int64_t* mdev = c.at<int64_t>(c.L.small) + 4;
@@ -340,6 +344,7 @@ ecasq_status hirschberg(Ctx& c, double lamp, int64_t lo, int64_t hi, int32_t n, 
     int64_t m = -1;
     HIP_TRY(hipMemcpyAsync(&m, mdev, sizeof m, hipMemcpyDeviceToHost, c.st));
     HIP_TRY(hipStreamSynchronize(c.st));
+    timing_flush();
     if (m < lo + r || m > hi - (n - 1 - r)) return ECASQ_EHIP;
     ECASQ_TRY(hirschberg(c, lamp, lo, m, r + 1, out));
     ECASQ_TRY(hirschberg(c, lamp, m, hi, n - r, out + r));
@@ -586,6 +591,13 @@ ecasq_status ecasq_dp_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
     out5[3] = J[3];
     out5[4] = (double)c.cells;
     return ECASQ_OK;
+}
+
+void ecasq_timing_enable(int32_t on) { timing_enable(on != 0); }
+
+void ecasq_timing_read(double* layer_ms, int64_t* layer_launches, int64_t* layer_cells,
+                       int32_t reset) {
+    timing_read(layer_ms, layer_launches, layer_cells, reset != 0);
 }
 
 ecasq_status ecasq_solve_batched(const void* x, ecasq_dtype dt, int64_t n, int64_t d, int32_t s,

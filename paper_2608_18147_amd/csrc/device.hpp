@@ -11,10 +11,11 @@
 //     C  = fma(v_b, tu, fma(v_a, sa, -s2))     (= C_P[a,b])
 //   surrogate-entropy term of one interval (Sec. 5, Phi and Phi^first):
 //     g = 1/(w*d)  yu = tu*g  yd = td*g (+ c0/d for the first interval)
-//     P = fma(max(yu,0), log2c(yu), max(yd,0)*log2c(yd))     (P = -Phi)
+//     mu = max(yu,0)  md = max(yd,0)
+//     P = fma(mu, log2c(mu), md*log2c(md))                    (P = -Phi)
 //   DP candidate (eq. apx_rec):  fma(-lambda', P, F_prev + C)
 //   refinement / output entropy (Sec. 6):
-//     U = tu*(1/w)  D = td*(1/w)   h(f) = -(max(y,0)*log2c(y)),  y = f/d
+//     U = tu*(1/w)  D = td*(1/w)   h(f) = -(m*log2c(m)),  m = max(f/d, 0)
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -23,20 +24,25 @@
 
 namespace ecasq {
 
-// Table-driven log2 (Tang 1990 style).  y = 2^e z with z in [0.7073, 1.4147)
-// chosen by subtracting an offset from the high word; the top 8 bits of the
-// reduced mantissa select {1/c, log2 c}; r = z/c - 1 (|r| <= 2^-9) feeds the
-// degree-6 series of log1p, scaled by RN(1/ln 2).  Finite for every finite y;
-// about one ulp for positive normal y.  tab points to the table in LDS.
+// Table-driven log2 (Tang 1990 style).  e comes from y's high word minus an
+// offset, so that z = ldexp(y, -e) lies in [0.7073, 1.4147) for positive
+// normal y; the top 8 bits of the reduced mantissa select {1/c, log2 c};
+// r = z/c - 1 (|r| <= 2^-9) feeds the degree-6 series of log1p, scaled by
+// RN(1/ln 2).  Finite for every y >= 0 (callers pass max(y, 0)); about one ulp
+// for positive normal y.
+// tab points to the table in LDS.
+//
+// Evaluation order on the device: u = (OFF_HI + 0xFFFFF) - hi gives
+// -e = u >> 20 (arithmetic) in one subtraction and, in bits 12..19, the
+// complement 255 - i of the table index, so the LDS copy of the table is
+// stored in reverse; e + lc is formed as lc - (double)(-e), the same IEEE sum.
 __device__ __forceinline__ double log2c(double y, const double2* __restrict__ tab) {
     const uint32_t hi = (uint32_t)__double2hiint(y);
-    const uint32_t lo = (uint32_t)__double2loint(y);
-    const uint32_t tmp = hi - ECASQ_LOG2_OFF_HI;
-    const int32_t e = ((int32_t)tmp) >> 20;
-    const uint32_t i = (tmp >> 12) & 0xFFu;
-    const uint32_t zhi = hi - (tmp & 0xFFF00000u);
-    const double z = __hiloint2double((int)zhi, (int)lo);
-    const double2 t = tab[i];
+    const int32_t u = (int32_t)((ECASQ_LOG2_OFF_HI + 0xFFFFFu) - hi);
+    const int32_t ne = u >> 20;  // -e
+    const uint32_t ir = ((uint32_t)u >> 12) & 0xFFu;  // 255 - i
+    const double z = __builtin_ldexp(y, ne);
+    const double2 t = tab[ir];
     const double r = __builtin_fma(z, t.x, -1.0);
     double q = -1.0 / 6.0;
     q = __builtin_fma(q, r, 1.0 / 5.0);
@@ -45,13 +51,29 @@ __device__ __forceinline__ double log2c(double y, const double2* __restrict__ ta
     q = __builtin_fma(q, r, -0.5);
     q = __builtin_fma(q, r, 1.0);
     const double lp = r * q;
-    const double base = (double)e + t.y;
+    const double base = t.y - (double)ne;
     return __builtin_fma(0x1.71547652b82fep+0, lp, base);
+}
+
+// 1/x rounded to nearest for positive x with |log2 x| < 700: the hardware
+// reciprocal refined by two Newton steps and one residual correction.  These
+// are the same operations, in the same order, as the IEEE double division
+// 1.0/x on this target when no operand scaling is needed (true in this range),
+// so the result equals 1.0/x bit for bit.
+__device__ __forceinline__ double recip_rn(double x) {
+    double r = __builtin_amdgcn_rcp(x);
+    double e = __builtin_fma(-x, r, 1.0);
+    r = __builtin_fma(r, e, r);
+    e = __builtin_fma(-x, r, 1.0);
+    r = __builtin_fma(r, e, r);
+    e = __builtin_fma(-x, r, 1.0);
+    return __builtin_fma(e, r, r);
 }
 
 // h(y) = -y log2 y for y > 0, 0 otherwise (Sec. 4).
 __device__ __forceinline__ double hfun(double y, const double2* __restrict__ tab) {
-    return -(__builtin_fmax(y, 0.0) * log2c(y, tab));
+    const double m = __builtin_fmax(y, 0.0);
+    return -(m * log2c(m, tab));
 }
 
 // C and P (= -Phi, or -Phi^first when `first`) of the interval (v_a, v_b].
@@ -66,14 +88,14 @@ __device__ __forceinline__ void cell_terms(double va, double Na, double Sa, doub
     const double tu = __builtin_fma(-va, n, sa);
     const double td = __builtin_fma(vb, n, -sa);
     C = __builtin_fma(vb, tu, __builtin_fma(va, sa, -s2));
-    const double wd = w * dd;
-    const double g = 1.0 / wd;
+    const double wd = w * dd;  // in [2^-148, 2^157] for fp32 inputs and d <= 2^28
+    const double g = recip_rn(wd);
     const double yu = tu * g;
     double yd = td * g;
     if (first) yd = yd + c0d;
-    const double lu = log2c(yu, tab);
-    const double ld = log2c(yd, tab);
-    P = __builtin_fma(__builtin_fmax(yu, 0.0), lu, __builtin_fmax(yd, 0.0) * ld);
+    const double mu = __builtin_fmax(yu, 0.0);
+    const double md = __builtin_fmax(yd, 0.0);
+    P = __builtin_fma(mu, log2c(mu, tab), md * log2c(md, tab));
 }
 
 // U and D of (v_a, v_b] in the refinement (inv) form.
@@ -115,10 +137,11 @@ __device__ __forceinline__ double hf(const Hist& H, double f, const double2* __r
     return hfun(f / H.dd, tab);
 }
 
-// Copy the log2 table into LDS (call from all threads, then __syncthreads()).
+// Copy the log2 table into LDS in reverse order (see log2c); call from all
+// threads, then __syncthreads().
 __device__ __forceinline__ void load_log2_table(double2* lds) {
     for (int i = threadIdx.x; i < 256; i += blockDim.x)
-        lds[i] = make_double2(kLog2Table[i][0], kLog2Table[i][1]);
+        lds[255 - i] = make_double2(kLog2Table[i][0], kLog2Table[i][1]);
 }
 
 }  // namespace ecasq

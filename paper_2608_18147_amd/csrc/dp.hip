@@ -17,6 +17,8 @@
 // workgroup, which balances the triangular work and fills all 256 CUs, and a
 // second kernel reduces the per-chunk (value, index) partials in increasing k
 // order (lowest k wins ties).  The 256-entry log2 table also lives in LDS.
+#include <vector>
+
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -26,6 +28,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kTK = 256;
+constexpr int kMaxSplit = 32;
 
 struct LayerArgs {
     const double* v;
@@ -38,13 +41,24 @@ struct LayerArgs {
     int64_t kb;   // forward: first predecessor; backward: last predecessor (khi)
     int64_t jlo;  // first column
     int64_t jhi;  // last column (inclusive)
-    int64_t kc;   // predecessors per chunk (multiple of kTK)
-    int32_t maxch;
+    int64_t nblk;   // column blocks
+    int32_t nsplit; // chunks per column block (equal split of its predecessor range)
     double dd;
     double lam;  // lambda' (MSE units)
 };
 
 // Predecessor range of block b: forward [kb, jend-1]; backward [j0+1, khi].
+// Chunk c of block b's predecessor range [klo, khi], split into nsplit equal
+// parts; returns false for an empty chunk.
+__device__ __forceinline__ bool chunk_range(int64_t klo, int64_t khi, int32_t nsplit, int64_t c,
+                                            int64_t& cs, int64_t& ce) {
+    const int64_t len = khi - klo + 1;
+    const int64_t kc = (len + nsplit - 1) / nsplit;
+    cs = klo + c * kc;
+    ce = cs + kc - 1 < khi ? cs + kc - 1 : khi;
+    return cs <= khi;
+}
+
 template <bool BWD>
 __device__ __forceinline__ void block_krange(const LayerArgs& a, int64_t CB, int64_t b,
                                              int64_t& j0, int64_t& jend, int64_t& klo,
@@ -60,22 +74,53 @@ __device__ __forceinline__ void block_krange(const LayerArgs& a, int64_t CB, int
     }
 }
 
-template <int R, bool BWD>
-__global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a) {
+// One cell update of column state (cv, cN, cS, cS2 / best, bk) against the
+// predecessor (pv, pN, pS, pS2, pF); `ok` masks cells outside the triangle.
+template <bool BWD, bool MASKED>
+__device__ __forceinline__ void cell_update(double cv, double cN, double cS, double cS2, double pv,
+                                            double pN, double pS, double pS2, double pF,
+                                            int32_t k, bool ok, double dd, double lam,
+                                            const double2* __restrict__ tab, double& best,
+                                            int32_t& bk) {
+    double C, P;
+    if (BWD)
+        cell_terms(cv, cN, cS, cS2, pv, pN, pS, pS2, dd, false, 0.0, tab, C, P);
+    else
+        cell_terms(pv, pN, pS, pS2, cv, cN, cS, cS2, dd, false, 0.0, tab, C, P);
+    const double cand = __builtin_fma(-lam, P, pF + C);
+    if (MASKED) {
+        const bool lt = ok && cand < best;
+        bk = lt ? k : bk;
+        best = lt ? cand : best;
+    } else {
+        // strict '<' keeps the lowest k; min() only differs from the select in
+        // the sign of an exact zero
+        bk = cand < best ? k : bk;
+        best = __builtin_fmin(best, cand);
+    }
+}
+
+// R columns per lane; SMEM: predecessors read through the scalar cache
+// (wave-uniform k) instead of being staged through LDS.
+template <int R, bool BWD, bool SMEM>
+__global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a, const double* __restrict__ gv,
+                                                     const double* __restrict__ gN,
+                                                     const double* __restrict__ gS,
+                                                     const double* __restrict__ gS2,
+                                                     const double* __restrict__ gF) {
     __shared__ double2 tab[256];
-    __shared__ double sv[kTK], sN[kTK], sS[kTK], sS2[kTK], sF[kTK];
+    __shared__ double sv[SMEM ? 1 : kTK], sN[SMEM ? 1 : kTK], sS[SMEM ? 1 : kTK],
+        sS2[SMEM ? 1 : kTK], sF[SMEM ? 1 : kTK];
     constexpr int64_t CB = (int64_t)kBlock * R;
     const int tid = threadIdx.x;
-    const int64_t b = blockIdx.y;
+    // heaviest column blocks first: high b for forward layers, low b backward
+    const int64_t b = BWD ? (int64_t)blockIdx.y : a.nblk - 1 - (int64_t)blockIdx.y;
     const int64_t c = blockIdx.x;
     int64_t j0, jend, klo, khi;
     block_krange<BWD>(a, CB, b, j0, jend, klo, khi);
-    const int64_t len = khi - klo + 1;
-    const int64_t nch = (len + a.kc - 1) / a.kc;
-    if (c >= nch) return;  // uniform across the block
+    int64_t cs, ce;
+    if (!chunk_range(klo, khi, a.nsplit, c, cs, ce)) return;  // uniform across the block
     load_log2_table(tab);
-    const int64_t cs = klo + c * a.kc;
-    const int64_t ce = cs + a.kc - 1 < khi ? cs + a.kc - 1 : khi;
 
     int64_t col[R];
     double cv[R], cN[R], cS[R], cS2[R], best[R];
@@ -84,65 +129,68 @@ __global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a) {
     for (int r = 0; r < R; r++) {
         col[r] = j0 + r * kBlock + tid;
         const int64_t jj = col[r] <= jend ? col[r] : jend;
-        cv[r] = a.v[jj];
-        cN[r] = a.N[jj];
-        cS[r] = a.S[jj];
-        cS2[r] = a.S2[jj];
+        cv[r] = gv[jj];
+        cN[r] = gN[jj];
+        cS[r] = gS[jj];
+        cS2[r] = gS2[jj];
         best[r] = __builtin_huge_val();
         bk[r] = -1;
     }
     const double lam = a.lam, dd = a.dd;
-    for (int64_t t0 = cs; t0 <= ce; t0 += kTK) {
-        const int nk = (int)(ce - t0 + 1 < kTK ? ce - t0 + 1 : kTK);
-        __syncthreads();
-        if (tid < nk) {
-            const int64_t k = t0 + tid;
-            sv[tid] = a.v[k];
-            sN[tid] = a.N[k];
-            sS[tid] = a.S[k];
-            sS2[tid] = a.S2[k];
-            sF[tid] = a.Fin[k];
+    if (SMEM) {
+        __syncthreads();  // table visible
+        // unmasked part: every k below (forward) or above (backward) all columns
+        const int64_t us = BWD ? (jend + 1 > cs ? jend + 1 : cs) : cs;
+        const int64_t ue = BWD ? ce : (j0 - 1 < ce ? j0 - 1 : ce);
+        for (int64_t k = us; k <= ue; k++) {
+            const double pv = gv[k], pN = gN[k], pS = gS[k], pS2 = gS2[k], pF = gF[k];
+#pragma unroll
+            for (int r = 0; r < R; r++)
+                cell_update<BWD, false>(cv[r], cN[r], cS[r], cS2[r], pv, pN, pS, pS2, pF,
+                                        (int32_t)k, true, dd, lam, tab, best[r], bk[r]);
         }
-        __syncthreads();
-        const bool nomask = BWD ? (t0 > jend) : (t0 + nk - 1 < j0);
-        if (nomask) {
-            for (int kk = 0; kk < nk; kk++) {
-                const double pv = sv[kk], pN = sN[kk], pS = sS[kk], pS2 = sS2[kk], pF = sF[kk];
+        // masked part (the diagonal region)
+        const int64_t ms = BWD ? cs : (j0 > cs ? j0 : cs);
+        const int64_t me = BWD ? (jend < ce ? jend : ce) : ce;
+        for (int64_t k = ms; k <= me; k++) {
+            const double pv = gv[k], pN = gN[k], pS = gS[k], pS2 = gS2[k], pF = gF[k];
 #pragma unroll
-                for (int r = 0; r < R; r++) {
-                    double C, P;
-                    if (BWD)
-                        cell_terms(cv[r], cN[r], cS[r], cS2[r], pv, pN, pS, pS2, dd, false, 0.0,
-                                   tab, C, P);
-                    else
-                        cell_terms(pv, pN, pS, pS2, cv[r], cN[r], cS[r], cS2[r], dd, false, 0.0,
-                                   tab, C, P);
-                    const double cand = __builtin_fma(-lam, P, pF + C);
-                    if (cand < best[r]) {
-                        best[r] = cand;
-                        bk[r] = (int32_t)(t0 + kk);
-                    }
-                }
+            for (int r = 0; r < R; r++)
+                cell_update<BWD, true>(cv[r], cN[r], cS[r], cS2[r], pv, pN, pS, pS2, pF,
+                                       (int32_t)k, BWD ? (k > col[r]) : (k < col[r]), dd, lam, tab,
+                                       best[r], bk[r]);
+        }
+    } else {
+        for (int64_t t0 = cs; t0 <= ce; t0 += kTK) {
+            const int nk = (int)(ce - t0 + 1 < kTK ? ce - t0 + 1 : kTK);
+            __syncthreads();
+            if (tid < nk) {
+                const int64_t k = t0 + tid;
+                sv[tid] = gv[k];
+                sN[tid] = gN[k];
+                sS[tid] = gS[k];
+                sS2[tid] = gS2[k];
+                sF[tid] = gF[k];
             }
-        } else {
-            for (int kk = 0; kk < nk; kk++) {
-                const int64_t k = t0 + kk;
-                const double pv = sv[kk], pN = sN[kk], pS = sS[kk], pS2 = sS2[kk], pF = sF[kk];
+            __syncthreads();
+            const bool nomask = BWD ? (t0 > jend) : (t0 + nk - 1 < j0);
+            if (nomask) {
+                for (int kk = 0; kk < nk; kk++) {
 #pragma unroll
-                for (int r = 0; r < R; r++) {
-                    const bool ok = BWD ? (k > col[r]) : (k < col[r]);
-                    double C, P;
-                    if (BWD)
-                        cell_terms(cv[r], cN[r], cS[r], cS2[r], pv, pN, pS, pS2, dd, false, 0.0,
-                                   tab, C, P);
-                    else
-                        cell_terms(pv, pN, pS, pS2, cv[r], cN[r], cS[r], cS2[r], dd, false, 0.0,
-                                   tab, C, P);
-                    const double cand = __builtin_fma(-lam, P, pF + C);
-                    if (ok && cand < best[r]) {
-                        best[r] = cand;
-                        bk[r] = (int32_t)k;
-                    }
+                    for (int r = 0; r < R; r++)
+                        cell_update<BWD, false>(cv[r], cN[r], cS[r], cS2[r], sv[kk], sN[kk],
+                                                sS[kk], sS2[kk], sF[kk], (int32_t)(t0 + kk), true,
+                                                dd, lam, tab, best[r], bk[r]);
+                }
+            } else {
+                for (int kk = 0; kk < nk; kk++) {
+                    const int64_t k = t0 + kk;
+#pragma unroll
+                    for (int r = 0; r < R; r++)
+                        cell_update<BWD, true>(cv[r], cN[r], cS[r], cS2[r], sv[kk], sN[kk],
+                                               sS[kk], sS2[kk], sF[kk], (int32_t)k,
+                                               BWD ? (k > col[r]) : (k < col[r]), dd, lam, tab,
+                                               best[r], bk[r]);
                 }
             }
         }
@@ -150,7 +198,7 @@ __global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a) {
 #pragma unroll
     for (int r = 0; r < R; r++) {
         if (col[r] <= jend) {
-            const int64_t idx = (b * a.maxch + c) * CB + r * kBlock + tid;
+            const int64_t idx = (b * a.nsplit + c) * CB + r * kBlock + tid;
             a.pval[idx] = best[r];
             a.pidx[idx] = bk[r];
         }
@@ -185,11 +233,12 @@ __global__ __launch_bounds__(256) void k_dp_reduce(ReduceArgs a) {
     const int64_t off = (j - a.L.jlo) - b * a.CB;
     int64_t j0, jend, klo, khi;
     block_krange<BWD>(a.L, a.CB, b, j0, jend, klo, khi);
-    const int64_t nch = (khi - klo + 1 + a.L.kc - 1) / a.L.kc;
     double best = __builtin_huge_val();
     int32_t bk = -1;
-    for (int64_t c = 0; c < nch; c++) {
-        const int64_t idx = (b * a.L.maxch + c) * a.CB + off;
+    for (int64_t c = 0; c < a.L.nsplit; c++) {
+        int64_t cs, ce;
+        if (!chunk_range(klo, khi, a.L.nsplit, c, cs, ce)) break;
+        const int64_t idx = (b * a.L.nsplit + c) * a.CB + off;
         const double val = a.L.pval[idx];
         if (val < best) {
             best = val;
@@ -308,30 +357,92 @@ __global__ __launch_bounds__(256) void k_split(const double* Fw, const double* B
     if (tid == 0) *m_out = si[0];
 }
 
-int64_t choose_kc(int64_t lenmax) {
-    int64_t kc = (lenmax + 31) / 32;
-    kc = (kc + kTK - 1) / kTK * kTK;
-    return kc < kTK ? kTK : kc;
+// Chunks per column block: enough workgroups to fill the chip, at least ~1k
+// predecessors per chunk, and a multiple of 8 when possible so that the
+// round-robin placement of consecutive workgroups on the 8 XCDs gives every
+// XCD an equal share of every column block.
+int32_t choose_splits(int64_t lenmax) {
+    int64_t sp = lenmax / 1024;
+    if (sp >= 8) sp = sp / 8 * 8;
+    if (sp > kMaxSplit) sp = kMaxSplit;
+    return sp < 1 ? 1 : (int32_t)sp;
 }
 
 }  // namespace
 
-int64_t dp_partial_entries(int64_t p) {
-    // nblk * maxch * CB with maxch <= 32 and nblk * CB <= p + CB
-    const int64_t CB = kBlock * kColsPerLane;
-    return (p + CB) * 33;
+// Optional timing of the layer kernel: a pair of events on the launch stream
+// around every k_dp_layer launch, read back when the solve synchronizes.
+namespace {
+struct TimedLaunch {
+    hipEvent_t a, b;
+    int64_t cells;
+};
+bool g_timing = false;
+std::vector<TimedLaunch> g_pending;
+std::vector<hipEvent_t> g_pool;
+double g_ms = 0.0;
+int64_t g_launches = 0, g_cells = 0;
+
+hipEvent_t take_event() {
+    if (!g_pool.empty()) {
+        hipEvent_t e = g_pool.back();
+        g_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
 }
+}  // namespace
+
+void timing_enable(bool on) { g_timing = on; }
+
+void timing_flush() {
+    for (auto& t : g_pending) {
+        float ms = 0.f;
+        if (hipEventSynchronize(t.b) == hipSuccess && hipEventElapsedTime(&ms, t.a, t.b) == hipSuccess) {
+            g_ms += ms;
+            g_launches++;
+            g_cells += t.cells;
+        }
+        g_pool.push_back(t.a);
+        g_pool.push_back(t.b);
+    }
+    g_pending.clear();
+}
+
+void timing_read(double* ms, int64_t* launches, int64_t* cells, bool reset) {
+    timing_flush();
+    if (ms) *ms = g_ms;
+    if (launches) *launches = g_launches;
+    if (cells) *cells = g_cells;
+    if (reset) {
+        g_ms = 0.0;
+        g_launches = 0;
+        g_cells = 0;
+    }
+}
+
+int64_t dp_partial_entries(int64_t p) {
+    // nblk * nsplit * CB with nsplit <= kMaxSplit and nblk * CB <= p + CB
+    const int64_t CB = kBlock * kColsPerLane;
+    return (p + CB) * kMaxSplit;
+}
+
+#ifndef ECASQ_PRED_SMEM
+#define ECASQ_PRED_SMEM 0
+#endif
 
 hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st) {
     constexpr int R = kColsPerLane;
+    constexpr bool SM = ECASQ_PRED_SMEM != 0;
     const int64_t CB = (int64_t)kBlock * R;
     const int64_t ncol = L.jhi - L.jlo + 1;
     if (ncol <= 0) return hipSuccess;
     const int64_t nblk = (ncol + CB - 1) / CB;
     // longest predecessor range: last block (forward) or first block (backward)
     const int64_t lenmax = L.backward ? (L.kb - L.jlo) : (L.jhi - L.kb);
-    const int64_t kc = choose_kc(lenmax);
-    const int64_t maxch = (lenmax + kc - 1) / kc;
+    const int32_t nsplit = choose_splits(lenmax);
     LayerArgs a;
     a.v = L.H.v;
     a.N = L.H.N;
@@ -343,15 +454,25 @@ hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st) {
     a.kb = L.kb;
     a.jlo = L.jlo;
     a.jhi = L.jhi;
-    a.kc = kc;
-    a.maxch = (int32_t)maxch;
+    a.nblk = nblk;
+    a.nsplit = nsplit;
     a.dd = L.H.dd;
     a.lam = L.lam;
-    dim3 grid((unsigned)maxch, (unsigned)nblk);
+    dim3 grid((unsigned)nsplit, (unsigned)nblk);
+    TimedLaunch tl{nullptr, nullptr, L.cells};
+    if (g_timing) {
+        tl.a = take_event();
+        tl.b = take_event();
+        if (tl.a && tl.b) (void)hipEventRecord(tl.a, st);
+    }
     if (L.backward)
-        k_dp_layer<R, true><<<grid, kBlock, 0, st>>>(a);
+        k_dp_layer<R, true, SM><<<grid, kBlock, 0, st>>>(a, a.v, a.N, a.S, a.S2, a.Fin);
     else
-        k_dp_layer<R, false><<<grid, kBlock, 0, st>>>(a);
+        k_dp_layer<R, false, SM><<<grid, kBlock, 0, st>>>(a, a.v, a.N, a.S, a.S2, a.Fin);
+    if (g_timing && tl.a && tl.b) {
+        (void)hipEventRecord(tl.b, st);
+        g_pending.push_back(tl);
+    }
     ReduceArgs ra;
     ra.L = a;
     ra.CB = CB;

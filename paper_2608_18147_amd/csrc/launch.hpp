@@ -11,7 +11,10 @@ namespace ecasq {
 inline size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
 // columns per lane in the DP layer kernel
-constexpr int kColsPerLane = 1;
+#ifndef ECASQ_COLS_PER_LANE
+#define ECASQ_COLS_PER_LANE 2
+#endif
+constexpr int kColsPerLane = ECASQ_COLS_PER_LANE;
 
 // ---- prep.hip ----
 size_t prep_scratch_bytes(int64_t d);
@@ -39,8 +42,12 @@ struct DpLayer {
     double* last;
     int32_t layer;
     int32_t last_stride;
+    int64_t cells;  // cells this launch evaluates (for timing)
 };
 int64_t dp_partial_entries(int64_t p);
+void timing_enable(bool on);
+void timing_flush();
+void timing_read(double* ms, int64_t* launches, int64_t* cells, bool reset);
 hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st);
 hipError_t launch_dp_init_fwd(const Hist& H, int64_t lo, int64_t jl, int64_t jh, double lam,
                               double* F, double* M, double* Ph, int32_t* kstar, double* last,

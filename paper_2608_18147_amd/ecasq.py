@@ -68,7 +68,7 @@ _lib = None
 EXPORTS = (
     "ecasq_default_options", "ecasq_solve", "ecasq_solve_ex", "ecasq_solve_lagrangian",
     "ecasq_quantize", "ecasq_solve_batched", "ecasq_workspace_size", "ecasq_status_string",
-    "ecasq_histogram", "ecasq_dp_trace",
+    "ecasq_histogram", "ecasq_dp_trace", "ecasq_timing_enable", "ecasq_timing_read",
 )
 
 
@@ -99,6 +99,10 @@ def lib():
     L.ecasq_status_string.restype = ctypes.c_char_p
     L.ecasq_histogram.argtypes = [vp, i32, i64, vp, vp, vp, vp, vp, P(i64)]
     L.ecasq_dp_trace.argtypes = [vp, i32, i64, i32, dbl, vp, vp, vp, vp]
+    L.ecasq_timing_enable.argtypes = [i32]
+    L.ecasq_timing_enable.restype = None
+    L.ecasq_timing_read.argtypes = [P(dbl), P(i64), P(i64), i32]
+    L.ecasq_timing_read.restype = None
     for name in ("ecasq_solve", "ecasq_solve_ex", "ecasq_solve_lagrangian", "ecasq_quantize",
                  "ecasq_solve_batched", "ecasq_histogram", "ecasq_dp_trace"):
         getattr(L, name).restype = i32
@@ -249,3 +253,16 @@ def ecasq_dp_trace(x, s, lam, stream=None):
                               _ptr(F), _ptr(K), out)
     _raise(st)
     return F, K, tuple(out)
+
+
+def ecasq_timing_enable(on=True):
+    lib().ecasq_timing_enable(1 if on else 0)
+
+
+def ecasq_timing_read(reset=False):
+    """(milliseconds, launches, cells) of the timed DP layer kernel launches."""
+    ms = ctypes.c_double(0)
+    n = ctypes.c_int64(0)
+    c = ctypes.c_int64(0)
+    lib().ecasq_timing_read(ctypes.byref(ms), ctypes.byref(n), ctypes.byref(c), 1 if reset else 0)
+    return ms.value, n.value, c.value

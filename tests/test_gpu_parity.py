@@ -90,6 +90,7 @@ DP_CASES = [
     ("lognormal_3000_l0", 3000, 8, 0.0),
     ("weights_5000", 5000, 6, 1.0),
     ("dups_700", 700, 10, 0.3),
+    ("wide_range_2000", 2000, 10, 0.1),  # interval widths from 2^-148 to 2^128
 ]
 
 
@@ -100,6 +101,11 @@ def _dp_input(name, d):
         return inputs.lognormal_signed(d, 6)
     if name.startswith("weights"):
         return inputs.weight_mixture(d, 7)
+    if name.startswith("wide_range"):
+        rng = np.random.default_rng(9)
+        x = rng.standard_normal(d) * 10.0 ** rng.integers(-44, 38, d)
+        x[:4] = [1e-45, -1e-45, 3e-45, 3.3e38]
+        return x.astype(np.float32)
     rng = np.random.default_rng(8)
     return (rng.integers(-40, 40, d) * 0.25).astype(np.float32)
 
