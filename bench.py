@@ -23,10 +23,10 @@ import time
 
 # Algorithmic fp64 operations per DP cell in the canonical cell arithmetic:
 # 4 range differences, 2 fma (tu, td), 2 fma (C), w*d, one IEEE division
-# (counted as 1), 2 products (yu, yd), two log2 evaluations of 16 flops each
-# (fma for r, 5 Horner fma, 1 mul, 1 add, 1 final fma), 1 mul + 1 fma for the
-# entropy term, 1 add + 1 fma for the candidate.  fma counts 2.
-FLOPS_PER_CELL = 54
+# (counted as 1), 2 products (yu, yd), two log2 evaluations of 13 flops each
+# (fma for r, 4 Horner fma, 1 add, 1 final fma), 1 mul + 1 fma for the entropy
+# term, 1 add + 1 fma for the candidate.  fma counts 2.
+FLOPS_PER_CELL = 48
 FP64_VECTOR_PEAK_TFLOPS = 78.6
 
 
@@ -68,7 +68,7 @@ def main():
     ap.add_argument("--workload", default="weights_256k")
     ap.add_argument("--budget", type=float, default=None)
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-sample", type=int, default=16384)
+    ap.add_argument("--cpu-sample", type=int, default=32768)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
 

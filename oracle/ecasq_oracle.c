@@ -39,9 +39,18 @@
 #include <stdlib.h>
 #include <string.h>
 
-#define OFF_HI 0x3FE6A800u /* entry 149 is centred on 1.0 */
-#define TBITS 8
+#define OFF_HI 0x3FE6A200u /* entry 599 is centred on 1.0 */
+#define TBITS 10
 #define TSIZE (1 << TBITS)
+
+/* log2(1 + r) ~ r * (c1 + c2 r + ... + c5 r^4) with c_k = RN(RN(1/ln 2) * RN((-1)^(k+1) / k)),
+ * the degree-5 Taylor series of log1p scaled by 1/ln 2 (|r| <= 2^-11). */
+#define L2K 0x1.71547652b82fep+0
+#define L2C1 (L2K * 1.0)
+#define L2C2 (L2K * -0.5)
+#define L2C3 (L2K * (1.0 / 3.0))
+#define L2C4 (L2K * -0.25)
+#define L2C5 (L2K * (1.0 / 5.0))
 
 static double g_invc[TSIZE];
 static double g_lc[TSIZE];
@@ -56,10 +65,10 @@ void orc_set_log2_table(const double *invc, const double *lc)
  * about one ulp; for y = 0 or a subnormal y it returns some finite value (its
  * callers multiply by y).  Steps: e = (high word of y minus an offset) >> 20
  * and z = ldexp(y, -e), so z lies in [~0.7073, ~1.4147) for positive normal y;
- * table entry i (top 8 bits of the reduced mantissa) gives invc ~ 1/z and
+ * table entry i (top 10 bits of the reduced mantissa) gives invc ~ 1/z and
  * lc = log2(1/invc);
- * r = z*invc - 1 with |r| <= 2^-9; log2(1+r) from the degree-6 Taylor series of
- * log1p times RN(1/ln 2). */
+ * r = z*invc - 1 with |r| <= 2^-11; log2(1+r) from the degree-5 Taylor series of
+ * log1p with RN(1/ln 2) folded into its coefficients. */
 static double log2c(double y)
 {
     uint64_t bits;
@@ -70,15 +79,13 @@ static double log2c(double y)
     uint32_t i = (tmp >> (20 - TBITS)) & (TSIZE - 1);
     double z = ldexp(y, -e);
     double r = fma(z, g_invc[i], -1.0);
-    double q = -1.0 / 6.0;
-    q = fma(q, r, 1.0 / 5.0);
-    q = fma(q, r, -0.25);
-    q = fma(q, r, 1.0 / 3.0);
-    q = fma(q, r, -0.5);
-    q = fma(q, r, 1.0);
-    double lp = r * q;
+    double q = L2C5;
+    q = fma(q, r, L2C4);
+    q = fma(q, r, L2C3);
+    q = fma(q, r, L2C2);
+    q = fma(q, r, L2C1);
     double base = (double)e + g_lc[i];
-    return fma(0x1.71547652b82fep+0, lp, base);
+    return fma(r, q, base);
 }
 
 double orc_log2c(double y) { return log2c(y); }

@@ -7,13 +7,13 @@ the Phi terms of the surrogate entropy) need a base-2 logarithm evaluated in
 fp64.  The paper does not fix how it is computed.  For bit-exact parity the
 oracle and the GPU evaluate the same fixed operation sequence (a table-driven
 reduction in the style of Tang 1990).  This module builds the oracle's own copy
-of the 256-entry table with mpmath; the GPU library builds its copy with an
+of the 1024-entry table with mpmath; the GPU library builds its copy with an
 independent integer-arithmetic generator.  Every entry is a correctly rounded
 double, so both copies must agree bit for bit.
 
 Entry i covers the inputs whose reduced mantissa bits (y's high word minus the
-offset word OFF_HI) have i in bits 12..19:
-    c_i   = the double whose high word is OFF_HI + (2i+1)*2^11, low word 0
+offset word OFF_HI) have i in bits 10..19:
+    c_i   = the double whose high word is OFF_HI + (2i+1)*2^9, low word 0
             (OFF_HI is chosen so that the entry holding 1.0 has c = 1.0
             exactly: there r = z - 1 is exact and log2 keeps full relative
             accuracy next to 1)
@@ -24,8 +24,8 @@ import struct
 
 import mpmath
 
-OFF_HI = 0x3FE6A800  # high word of a double near 1/sqrt(2); centres an entry on 1.0
-TABLE_BITS = 8
+OFF_HI = 0x3FE6A200  # high word of a double near 1/sqrt(2); centres an entry on 1.0
+TABLE_BITS = 10
 TABLE_SIZE = 1 << TABLE_BITS
 
 

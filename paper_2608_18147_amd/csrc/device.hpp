@@ -24,35 +24,37 @@
 
 namespace ecasq {
 
+constexpr int kLog2Bits = ECASQ_LOG2_BITS;
+constexpr int kLog2Size = 1 << kLog2Bits;
+
 // Table-driven log2 (Tang 1990 style).  e comes from y's high word minus an
-// offset, so that z = ldexp(y, -e) lies in [0.7073, 1.4147) for positive
-// normal y; the top 8 bits of the reduced mantissa select {1/c, log2 c};
-// r = z/c - 1 (|r| <= 2^-9) feeds the degree-6 series of log1p, scaled by
-// RN(1/ln 2).  Finite for every y >= 0 (callers pass max(y, 0)); about one ulp
+// offset, so that z = ldexp(y, -e) lies in [0.7073, 1.4146) for positive
+// normal y; the top 10 bits of the reduced mantissa select {1/c, log2 c};
+// r = z/c - 1 (|r| <= 2^-11) feeds the degree-5 series of log1p with
+// RN(1/ln 2) folded into its coefficients, c_k = RN(RN(1/ln 2) RN(+-1/k)).  Finite for every y >= 0 (callers pass max(y, 0)); about one ulp
 // for positive normal y.
 // tab points to the table in LDS.
 //
 // Evaluation order on the device: u = (OFF_HI + 0xFFFFF) - hi gives
-// -e = u >> 20 (arithmetic) in one subtraction and, in bits 12..19, the
-// complement 255 - i of the table index, so the LDS copy of the table is
+// -e = u >> 20 (arithmetic) in one subtraction and, in bits 10..19, the
+// complement 1023 - i of the table index, so the LDS copy of the table is
 // stored in reverse; e + lc is formed as lc - (double)(-e), the same IEEE sum.
 __device__ __forceinline__ double log2c(double y, const double2* __restrict__ tab) {
     const uint32_t hi = (uint32_t)__double2hiint(y);
     const int32_t u = (int32_t)((ECASQ_LOG2_OFF_HI + 0xFFFFFu) - hi);
     const int32_t ne = u >> 20;  // -e
-    const uint32_t ir = ((uint32_t)u >> 12) & 0xFFu;  // 255 - i
+    const uint32_t ir = ((uint32_t)u >> (20 - kLog2Bits)) & (kLog2Size - 1);  // mirrored i
     const double z = __builtin_ldexp(y, ne);
     const double2 t = tab[ir];
     const double r = __builtin_fma(z, t.x, -1.0);
-    double q = -1.0 / 6.0;
-    q = __builtin_fma(q, r, 1.0 / 5.0);
-    q = __builtin_fma(q, r, -0.25);
-    q = __builtin_fma(q, r, 1.0 / 3.0);
-    q = __builtin_fma(q, r, -0.5);
-    q = __builtin_fma(q, r, 1.0);
-    const double lp = r * q;
+    constexpr double K = 0x1.71547652b82fep+0;
+    double q = K * (1.0 / 5.0);
+    q = __builtin_fma(q, r, K * -0.25);
+    q = __builtin_fma(q, r, K * (1.0 / 3.0));
+    q = __builtin_fma(q, r, K * -0.5);
+    q = __builtin_fma(q, r, K * 1.0);
     const double base = t.y - (double)ne;
-    return __builtin_fma(0x1.71547652b82fep+0, lp, base);
+    return __builtin_fma(r, q, base);
 }
 
 // 1/x rounded to nearest for positive x with |log2 x| < 700: the hardware
@@ -140,8 +142,8 @@ __device__ __forceinline__ double hf(const Hist& H, double f, const double2* __r
 // Copy the log2 table into LDS in reverse order (see log2c); call from all
 // threads, then __syncthreads().
 __device__ __forceinline__ void load_log2_table(double2* lds) {
-    for (int i = threadIdx.x; i < 256; i += blockDim.x)
-        lds[255 - i] = make_double2(kLog2Table[i][0], kLog2Table[i][1]);
+    for (int i = threadIdx.x; i < kLog2Size; i += blockDim.x)
+        lds[kLog2Size - 1 - i] = make_double2(kLog2Table[i][0], kLog2Table[i][1]);
 }
 
 }  // namespace ecasq

@@ -108,7 +108,7 @@ __global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a, const double* 
                                                      const double* __restrict__ gS,
                                                      const double* __restrict__ gS2,
                                                      const double* __restrict__ gF) {
-    __shared__ double2 tab[256];
+    __shared__ double2 tab[kLog2Size];
     __shared__ double sv[SMEM ? 1 : kTK], sN[SMEM ? 1 : kTK], sS[SMEM ? 1 : kTK],
         sS2[SMEM ? 1 : kTK], sF[SMEM ? 1 : kTK];
     constexpr int64_t CB = (int64_t)kBlock * R;
@@ -224,7 +224,7 @@ struct ReduceArgs {
 
 template <bool BWD>
 __global__ __launch_bounds__(256) void k_dp_reduce(ReduceArgs a) {
-    __shared__ double2 tab[256];
+    __shared__ double2 tab[kLog2Size];
     load_log2_table(tab);
     __syncthreads();
     const int64_t j = a.L.jlo + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -269,7 +269,7 @@ __global__ __launch_bounds__(256) void k_dp_init_fwd(Hist H, int64_t lo, int64_t
                                                      double lam, double* F, double* M, double* Ph,
                                                      int32_t* kstar, double* last,
                                                      int32_t last_stride) {
-    __shared__ double2 tab[256];
+    __shared__ double2 tab[kLog2Size];
     load_log2_table(tab);
     __syncthreads();
     const int64_t j = jl + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -295,7 +295,7 @@ __global__ __launch_bounds__(256) void k_dp_init_fwd(Hist H, int64_t lo, int64_t
 // Backward layer 2 into `hi`: B[j] = C[j,hi] + lambda' Phi[j,hi].
 __global__ __launch_bounds__(256) void k_dp_init_bwd(Hist H, int64_t hi, int64_t jl, int64_t jh,
                                                      double lam, double* B) {
-    __shared__ double2 tab[256];
+    __shared__ double2 tab[kLog2Size];
     load_log2_table(tab);
     __syncthreads();
     const int64_t j = jl + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;

@@ -79,7 +79,7 @@ __global__ __launch_bounds__(256) void k_refine(Hist H, int32_t t, int32_t* __re
                                                 double lamp, double b, int32_t budget,
                                                 int32_t rounds, int32_t exhaustive,
                                                 int32_t* __restrict__ stats) {
-    __shared__ double2 tab[256];
+    __shared__ double2 tab[kLog2Size];
     __shared__ int32_t u[kMaxT], nu[kMaxT];
     __shared__ int32_t moved_s, commit_s;
     __shared__ double redv[256];
@@ -183,7 +183,7 @@ __global__ __launch_bounds__(256) void k_refine(Hist H, int32_t t, int32_t* __re
 // out: MSE, vNMSE, H(Xhat), H(I,B), vNMSE + lambda H(Xhat), H(Xhat) + 32t/d.
 __global__ void k_metrics(Hist H, int32_t t, const int32_t* __restrict__ u, double lam,
                           double s2tot, double* __restrict__ out) {
-    __shared__ double2 tab[256];
+    __shared__ double2 tab[kLog2Size];
     load_log2_table(tab);
     __syncthreads();
     if (threadIdx.x != 0) return;
@@ -285,7 +285,7 @@ __global__ __launch_bounds__(256) void k_quantize(const void* __restrict__ x, in
 
 __global__ void k_entropy(const unsigned long long* __restrict__ hist, int32_t t, int64_t d,
                           double* __restrict__ ent, int64_t* __restrict__ hist_out) {
-    __shared__ double2 tab[256];
+    __shared__ double2 tab[kLog2Size];
     load_log2_table(tab);
     __syncthreads();
     if (threadIdx.x != 0) return;
