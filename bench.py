@@ -29,6 +29,24 @@ import time
 FLOPS_PER_CELL = 48
 FP64_VECTOR_PEAK_TFLOPS = 78.6
 
+# HBM bytes per k_dp_layer launch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs
+# (profiles/k_dp_layer_weights_256k.md), scaled by a plain copy's readings
+# (FETCH x2.0, WRITE x1.0).  Valid only for the kernel sources they were taken
+# on: reported as null once those sources change.
+TRAFFIC_BYTES_PER_LAUNCH = 283.0e6
+TRAFFIC_SOURCES_SHA = "89c9cd8d83e47782"
+KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
+
+
+def kernel_sources_sha():
+    import hashlib
+    h = hashlib.sha256()
+    here = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_18147_amd", "csrc")
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(here, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -148,7 +166,9 @@ def main():
             "peak": FP64_VECTOR_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
-            "traffic": None,
+            "traffic": (TRAFFIC_BYTES_PER_LAUNCH if kernel_sources_sha() == TRAFFIC_SOURCES_SHA
+                        else None),
+            "traffic_unit": "bytes/launch",
             "flops_per_cell": FLOPS_PER_CELL,
             "avg_launch_ms": avg_ms,
             "launches": launches,
