@@ -125,11 +125,15 @@ ecasq_status ecasq_quantize(const void *x, ecasq_dtype dt, int64_t d, const doub
                             double *empirical_entropy, int64_t *hist);
 
 /*
- * Many independent short vectors in one launch (one workgroup per row):
- * x is n rows of d entries, row-major.  Each row is solved as ecasq_solve_ex
- * would with opts->recovery = 1 (argmins kept in LDS).  codebooks: device,
- * n x s fp64 (row r's t_out[r] values first); t_out: device, n int32;
- * infos_dev: device, n ecasq_info, may be NULL.  d <= 512, s <= 32.
+ * Many independent short vectors in one launch (one wavefront per row, several
+ * rows per workgroup): x is n rows of d entries, row-major.  Each row is
+ * solved as ecasq_solve_ex would with opts->recovery = 1 (argmins kept in
+ * LDS; opts->recovery itself is ignored).  codebooks: device, n x s fp64 (row
+ * r's t_out[r] values first, the rest untouched); t_out: device, n int32
+ * (0 for a row holding NaN/Inf); infos_dev: device, n ecasq_info, may be NULL
+ * (per-row status: ECASQ_OK, ECASQ_EINFEASIBLE or ECASQ_ENONFINITE).
+ * 1 <= d <= 512, 2 <= s <= 32.  Returns after the results are in device
+ * memory.
  */
 ecasq_status ecasq_solve_batched(const void *x, ecasq_dtype dt, int64_t n, int64_t d,
                                  int32_t s, double bits_per_entry, const ecasq_options *opts,

@@ -183,21 +183,28 @@ def _finish(H, chain, lam, solves, rounds, cells, status, traj=None):
                   cells=cells, status=status, traj=traj)
 
 
-def _recover(H, t, lam):
-    """Codebook (unique indices) with t values at lambda (vNMSE units)."""
+def _recover(H, t, lam, recovery="hirschberg", s=None, exact_s=False):
+    """Codebook (unique indices) with t values at lambda (vNMSE units): by
+    Hirschberg (Sec. 5), or by a traceback through the argmins of a solve at
+    the same multiplier ('backpointers')."""
     if H.p == 1:
         return np.zeros(1, dtype=np.int32), 0
     if t == 2 or not math.isfinite(lam):
         return np.array([0, H.p - 1], dtype=np.int32), 0
+    if recovery == "backpointers":
+        r = dp_forward(H, s, lam * H.s2tot, exact_s, backpointers=True)
+        assert r["t"] == t
+        return r["chain_bp"], 0
     return hirschberg(H, t, lam * H.s2tot)
 
 
-def solve(x, s, b, refine_rounds=5, exhaustive=False, exact_s=False, max_iters=64):
+def solve(x, s, b, refine_rounds=5, exhaustive=False, exact_s=False, max_iters=64,
+          recovery="hirschberg"):
     """Budget mode: the lowest-MSE supported solution with H(I,B) <= b, then
     refinement at its multiplier with the budget guard on H(Xhat)."""
     H = prepare(x)
     sr = search(H, s, b, exact_s, max_iters)
-    chain, hcells = _recover(H, sr["t"], sr["lam"])
+    chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s)
     rounds = 0
     if refine_rounds > 0 and math.isfinite(sr["lam"]) and len(chain) >= 3:
         chain, rounds, _ = refine(H, chain, sr["lam"] * H.s2tot, b, True, refine_rounds,

@@ -603,9 +603,17 @@ void ecasq_timing_read(double* layer_ms, int64_t* layer_launches, int64_t* layer
 ecasq_status ecasq_solve_batched(const void* x, ecasq_dtype dt, int64_t n, int64_t d, int32_t s,
                                  double bits_per_entry, const ecasq_options* opts, void* stream,
                                  double* codebooks, int32_t* t_out, ecasq_info* infos_dev) {
-    (void)x; (void)dt; (void)n; (void)d; (void)s; (void)bits_per_entry; (void)opts;
-    (void)stream; (void)codebooks; (void)t_out; (void)infos_dev;
-    return ECASQ_EINVAL;  // provided by batched.hip once built
+    if (!x || n < 1 || d < 1 || d > 512 || s < 2 || s > 32 || !codebooks || !t_out)
+        return ECASQ_EINVAL;
+    if (dt < 0 || dt > 2 || !(bits_per_entry >= 0.0)) return ECASQ_EINVAL;
+    const ecasq_options o = opts ? *opts : defaults();
+    if (o.refine_rounds < 0 || o.max_search_iters < 0) return ECASQ_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    HIP_TRY(launch_batched(x, dt, n, (int32_t)d, s, bits_per_entry, o.refine_rounds,
+                           o.refine_exhaustive, o.exact_s, o.max_search_iters, codebooks, t_out,
+                           infos_dev, st));
+    HIP_TRY(hipStreamSynchronize(st));
+    return ECASQ_OK;
 }
 
 }  // extern "C"

@@ -1,0 +1,562 @@
+// Many short vectors in one launch: one wavefront solves one row end to end
+// with everything in LDS (sort, exact prefix sums, the lambda search over
+// dp_APX solves, recovery, refinement, metrics), several rows per workgroup
+// sharing one copy of the log2 table.
+//
+// Per row the steps are those of the single-vector path (Sec. 2 histogram,
+// App. D prefix sums, Sec. 5 eq. apx_base/apx_rec/apx_final, Sec. 3/Sec. 5
+// lambda search, Sec. 6 refinement).  Recovery keeps the argmins of every
+// layer (s x p int16 in LDS, two buffers so that the best feasible solve's
+// argmins survive the later queries) and traces them back: at these sizes the
+// O(s p) table is a few KB and Hirschberg's O(p) bound buys nothing.
+//
+// Columns sit in lanes (column j = 64c + lane, c < CMAX); the predecessor k is
+// uniform and read from LDS as a broadcast.  Column segments entirely at or
+// below k are skipped, so only the segment crossing the diagonal carries
+// masked lanes.
+#include <hip/hip_fp16.h>
+
+#include "../../include/ecasq.h"
+#include "chain.hpp"
+#include "device.hpp"
+#include "launch.hpp"
+#include "wide.hpp"
+
+namespace ecasq {
+
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kMaxRows = 4;
+
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+struct RowLayout {
+    uint32_t keys, v, N, S, S2, F0, F1, last, bp0, bp1, chain, nu, misc, total;
+};
+
+__host__ __device__ inline uint32_t up16(uint32_t b) { return (b + 15u) & ~15u; }
+
+// LDS bytes of one row: dpad keys, 6 fp64 arrays of dpad, s+1 last-column
+// values, two (s+1) x dpad int16 argmin tables, two int32 chains, scalars.
+__host__ __device__ inline RowLayout row_layout(int dpad, int s) {
+    RowLayout L;
+    uint32_t o = 0;
+    auto take = [&](uint32_t b) {
+        uint32_t at = o;
+        o += up16(b);
+        return at;
+    };
+    L.keys = take(4u * dpad);
+    L.v = take(8u * dpad);
+    L.N = take(8u * dpad);
+    L.S = take(8u * dpad);
+    L.S2 = take(8u * dpad);
+    L.F0 = take(8u * dpad);
+    L.F1 = take(8u * dpad);
+    L.last = take(8u * (s + 1));
+    L.bp0 = take(2u * (s + 1) * dpad);
+    L.bp1 = take(2u * (s + 1) * dpad);
+    L.chain = take(4u * (s + 1));
+    L.nu = take(4u * (s + 1));
+    L.misc = take(64);
+    L.total = o;
+    return L;
+}
+
+struct BatchArgs {
+    const void* x;
+    int64_t n;
+    int32_t d, dpad, s, rows_per_block;
+    double b;
+    int32_t refine_rounds, refine_exhaustive, exact_s, max_iters;
+    double* codebooks;
+    int32_t* t_out;
+    ecasq_info* infos;
+};
+
+struct Row {
+    const double2* tab;
+    double *v, *N, *S, *S2, *F0, *F1, *last;
+    int16_t* bp[2];
+    int32_t *chain, *nu;
+    double* misc;  // scratch scalars shared by the lanes of the row
+    int p, s, dpad, lane;
+    double dd, c0, c0d, s2tot;
+    int64_t cells;
+    int32_t solves;
+};
+
+struct Pt {
+    double lam, H, M;
+    int t, buf;  // buf: argmin buffer holding this solve (-1: closed form)
+};
+
+__device__ __forceinline__ Hist row_hist(const Row& R) {
+    Hist H;
+    H.v = R.v;
+    H.N = R.N;
+    H.S = R.S;
+    H.S2 = R.S2;
+    H.p = R.p;
+    H.dd = R.dd;
+    H.c0 = R.c0;
+    H.c0d = R.c0d;
+    return H;
+}
+
+// One dp_APX solve at lambda (vNMSE units) into argmin buffer `buf`; returns
+// the lowest i minimising F_i[p-1] and, along its path, MSE and H(I,B) summed
+// in path order (the same additions as accumulating them along the argmins).
+template <int CMAX>
+__device__ Pt row_solve(Row& R, double lam, int exact_s, int buf) {
+    const double lamp = lam * R.s2tot;
+    const int p = R.p, lane = R.lane, dp = R.dpad;
+    const int imax = R.s < p ? R.s : p;
+    int16_t* bp = R.bp[buf];
+    const Hist H = row_hist(R);
+    for (int j = 1 + lane; j < p; j += kWave) {
+        double C, P;
+        cell_at(H, 0, j, R.tab, C, P);
+        const double f = __builtin_fma(-lamp, P, 0.0 + C);
+        R.F0[j] = f;
+        bp[2 * dp + j] = 0;
+        if (j == p - 1) R.last[2] = f;
+    }
+    R.cells += p - 1;
+    wave_sync();
+    double* Fp = R.F0;
+    double* Fc = R.F1;
+    // column data of this lane
+    double cv[CMAX], cN[CMAX], cS[CMAX], cS2[CMAX];
+#pragma unroll
+    for (int c = 0; c < CMAX; c++) {
+        const int j = c * kWave + lane;
+        const int jj = j < p ? j : p - 1;
+        cv[c] = R.v[jj];
+        cN[c] = R.N[jj];
+        cS[c] = R.S[jj];
+        cS2[c] = R.S2[jj];
+    }
+    for (int i = 3; i <= imax; i++) {
+        double best[CMAX];
+        int32_t bk[CMAX];
+#pragma unroll
+        for (int c = 0; c < CMAX; c++) {
+            best[c] = __builtin_huge_val();
+            bk[c] = -1;
+        }
+        for (int k = i - 2; k <= p - 2; k++) {
+            const double pv = R.v[k], pN = R.N[k], pS = R.S[k], pS2 = R.S2[k], pF = Fp[k];
+#pragma unroll
+            for (int c = 0; c < CMAX; c++) {
+                if (c * kWave + kWave - 1 <= k) continue;  // whole segment at or below k
+                const int j = c * kWave + lane;
+                double C, P;
+                cell_terms(pv, pN, pS, pS2, cv[c], cN[c], cS[c], cS2[c], R.dd, false, 0.0, R.tab,
+                           C, P);
+                const double cand = __builtin_fma(-lamp, P, pF + C);
+                const bool lt = (j > k) && (j < p) && cand < best[c];
+                bk[c] = lt ? k : bk[c];
+                best[c] = lt ? cand : best[c];
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < CMAX; c++) {
+            const int j = c * kWave + lane;
+            if (j >= i - 1 && j < p) {
+                Fc[j] = best[c];
+                bp[i * dp + j] = (int16_t)bk[c];
+                if (j == p - 1) R.last[i] = best[c];
+            }
+        }
+        R.cells += (int64_t)(p - i + 1) * (p - i + 2) / 2;
+        wave_sync();
+        double* t = Fp;
+        Fp = Fc;
+        Fc = t;
+    }
+    // eq. apx_final, then the path's MSE and H(I,B) in path order
+    if (lane == 0) {
+        int bi = 2;
+        double bj = R.last[2];
+        for (int i = 3; i <= imax; i++) {
+            const double f = R.last[i];
+            if (exact_s ? (i == imax) : (f < bj)) {
+                bj = f;
+                bi = i;
+            }
+        }
+        int32_t* u = R.nu;  // scratch chain
+        u[bi - 1] = p - 1;
+        for (int i = bi; i >= 3; i--) u[i - 2] = bp[i * dp + u[i - 1]];
+        u[0] = 0;
+        double mse = 0.0, ph = 0.0;
+        for (int r = 0; r + 1 < bi; r++) {
+            double C, P;
+            cell_at(H, u[r], u[r + 1], R.tab, C, P);
+            mse = mse + C;
+            ph = ph - P;
+        }
+        R.misc[0] = mse;
+        R.misc[1] = ph;
+        R.misc[2] = (double)bi;
+    }
+    wave_sync();
+    Pt out;
+    out.lam = lam;
+    out.M = R.misc[0] / R.s2tot;
+    out.H = R.misc[1];
+    out.t = (int)R.misc[2];
+    out.buf = buf;
+    R.solves++;
+    wave_sync();
+    return out;
+}
+
+// Sec. 6 refinement of the chain in R.chain (t values), one wavefront.
+__device__ int row_refine(Row& R, int t, double lamp, double b, int budget, int rounds,
+                          int exhaustive) {
+    const Hist H = row_hist(R);
+    const int lane = R.lane;
+    int32_t* u = R.chain;
+    int32_t* nu = R.nu;
+    int nrun = 0;
+    for (int rd = 0; rd < rounds; rd++) {
+        bool any = false;
+        for (int c = 0; c < 3; c++) {
+            for (int r = lane; r < t; r += kWave) nu[r] = u[r];
+            wave_sync();
+            int moved = 0;
+            if (!exhaustive) {
+                bool mv = false;
+                for (int r = 1 + lane; r <= t - 2; r += kWave) {
+                    if (r % 3 != c) continue;
+                    const int L = u[r - 1], Rr = u[r + 1];
+                    if (Rr - L < 3) continue;
+                    int lo = L + 1, hi = Rr - 1;
+                    while (lo < hi) {
+                        const int mid = lo + (hi - lo) / 2;
+                        if (refine_local(H, t, u, r, mid + 1, lamp, R.tab) <
+                            refine_local(H, t, u, r, mid, lamp, R.tab))
+                            lo = mid + 1;
+                        else
+                            hi = mid;
+                    }
+                    if (lo != u[r] && refine_local(H, t, u, r, lo, lamp, R.tab) <
+                                          refine_local(H, t, u, r, u[r], lamp, R.tab)) {
+                        nu[r] = lo;
+                        mv = true;
+                    }
+                }
+                moved = __popcll(__ballot(mv));
+            } else {
+                for (int r = 1; r <= t - 2; r++) {
+                    if (r % 3 != c) continue;
+                    const int L = u[r - 1], Rr = u[r + 1];
+                    if (Rr - L < 3) continue;
+                    double bv = __builtin_huge_val();
+                    int bm = -1;
+                    for (int m = L + 1 + lane; m < Rr; m += kWave) {
+                        const double val = refine_local(H, t, u, r, m, lamp, R.tab);
+                        if (val < bv) {
+                            bv = val;
+                            bm = m;
+                        }
+                    }
+                    for (int off = 32; off > 0; off >>= 1) {
+                        const double ov = __shfl_xor(bv, off, kWave);
+                        const int om = __shfl_xor(bm, off, kWave);
+                        if (om >= 0 && (bm < 0 || ov < bv || (ov == bv && om < bm))) {
+                            bv = ov;
+                            bm = om;
+                        }
+                    }
+                    if (bm != u[r] && bv < refine_local(H, t, u, r, u[r], lamp, R.tab)) {
+                        if (lane == 0) nu[r] = bm;
+                        moved++;
+                    }
+                }
+            }
+            wave_sync();
+            if (moved && budget) {
+                if (lane == 0) R.misc[3] = chain_hout(H, t, nu, R.tab) > b ? 1.0 : 0.0;
+                wave_sync();
+                if (R.misc[3] != 0.0) moved = 0;
+            }
+            if (moved) {
+                for (int r = lane; r < t; r += kWave) u[r] = nu[r];
+                any = true;
+            }
+            wave_sync();
+        }
+        nrun++;
+        if (!any) break;
+    }
+    return nrun;
+}
+
+template <int DT>
+__device__ __forceinline__ uint32_t load_bits(const void* x, int64_t i) {
+    if (DT == 0) return reinterpret_cast<const uint32_t*>(x)[i];
+    if (DT == 1) return __float_as_uint(__half2float(reinterpret_cast<const __half*>(x)[i]));
+    return ((uint32_t)reinterpret_cast<const uint16_t*>(x)[i]) << 16;
+}
+
+template <int DT, int CMAX>
+__global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
+    extern __shared__ __align__(16) char smem[];
+    double2* tab = reinterpret_cast<double2*>(smem);
+    load_log2_table(tab);
+    __syncthreads();  // the only block-wide barrier: rows diverge from here on
+    const int wave = threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
+    const int64_t row = (int64_t)blockIdx.x * A.rows_per_block + wave;
+    if (wave >= A.rows_per_block || row >= A.n) return;
+    const RowLayout L = row_layout(A.dpad, A.s);
+    char* base = smem + sizeof(double2) * kLog2Size + (size_t)wave * L.total;
+    uint32_t* keys = reinterpret_cast<uint32_t*>(base + L.keys);
+    Row R;
+    R.tab = tab;
+    R.v = reinterpret_cast<double*>(base + L.v);
+    R.N = reinterpret_cast<double*>(base + L.N);
+    R.S = reinterpret_cast<double*>(base + L.S);
+    R.S2 = reinterpret_cast<double*>(base + L.S2);
+    R.F0 = reinterpret_cast<double*>(base + L.F0);
+    R.F1 = reinterpret_cast<double*>(base + L.F1);
+    R.last = reinterpret_cast<double*>(base + L.last);
+    R.bp[0] = reinterpret_cast<int16_t*>(base + L.bp0);
+    R.bp[1] = reinterpret_cast<int16_t*>(base + L.bp1);
+    R.chain = reinterpret_cast<int32_t*>(base + L.chain);
+    R.nu = reinterpret_cast<int32_t*>(base + L.nu);
+    R.misc = reinterpret_cast<double*>(base + L.misc);
+    R.s = A.s;
+    R.dpad = A.dpad;
+    R.lane = lane;
+    R.cells = 0;
+    R.solves = 0;
+    const int d = A.d, dpad = A.dpad;
+
+    // ingest: order-preserving keys, padding sorts last
+    bool bad = false;
+    for (int i = lane; i < dpad; i += kWave) {
+        uint32_t k = 0xFFFFFFFFu;
+        if (i < d) {
+            const uint32_t bits = load_bits<DT>(A.x, row * (int64_t)d + i);
+            if ((bits & 0x7F800000u) == 0x7F800000u) bad = true;
+            k = f32_key(bits);
+        }
+        keys[i] = k;
+    }
+    const bool nonfinite = __ballot(bad) != 0ull;
+    wave_sync();
+    // bitonic sort of dpad keys
+    for (int kk = 2; kk <= dpad; kk <<= 1) {
+        for (int jj = kk >> 1; jj > 0; jj >>= 1) {
+            for (int i = lane; i < dpad; i += kWave) {
+                const int pr = i ^ jj;
+                if (pr > i) {
+                    const uint32_t a = keys[i], c = keys[pr];
+                    const bool up = (i & kk) == 0;
+                    if ((a > c) == up) {
+                        keys[i] = c;
+                        keys[pr] = a;
+                    }
+                }
+            }
+            wave_sync();
+        }
+    }
+    // histogram + exact prefix sums (one lane; at most 512 entries)
+    if (lane == 0) {
+        uint64_t s[kSL] = {0}, q[kS2L] = {0};
+        int u = 0;
+        for (int i = 0; i < d; i++) {
+            const uint32_t k = keys[i];
+            const uint32_t bits = key_bits(k);
+            accumulate(s, q, term_of(bits));
+            if (i == d - 1 || keys[i + 1] != k) {
+                R.v[u] = (double)__uint_as_float(bits);
+                R.N[u] = (double)(i + 1);
+                R.S[u] = wide_to_double<kSL>(s, true, -149);
+                R.S2[u] = wide_to_double<kS2L>(q, false, -298);
+                u++;
+            }
+        }
+        R.misc[4] = (double)u;
+    }
+    wave_sync();
+    R.p = (int)R.misc[4];
+    R.dd = (double)d;
+    R.c0 = R.N[0];
+    R.c0d = R.c0 / R.dd;
+    R.s2tot = R.S2[R.p - 1];
+    const int p = R.p;
+    const double b = A.b;
+
+    int status = ECASQ_OK;
+    double lamB = 0.0;
+    int t = 1;
+    if (nonfinite) {
+        status = ECASQ_ENONFINITE;
+        t = 0;
+    } else if (p <= 2) {
+        t = p;
+        if (lane == 0) {
+            R.chain[0] = 0;
+            if (p == 2) R.chain[1] = 1;
+        }
+    } else {
+        // slope search (same decisions as the single-vector path)
+        Pt Ap = row_solve<CMAX>(R, 0.0, A.exact_s, 0);
+        Pt Bp;
+        bool done = false;
+        if (Ap.H <= b) {
+            Bp = Ap;
+            done = true;
+        } else if (b >= 1.0) {
+            double C, P;
+            cell_at(row_hist(R), 0, p - 1, tab, C, P);
+            Bp.lam = __builtin_huge_val();
+            Bp.H = 0.0 - P;
+            Bp.M = (0.0 + C) / R.s2tot;
+            Bp.t = 2;
+            Bp.buf = -1;
+        } else {
+            Bp = row_solve<CMAX>(R, 0x1p40, A.exact_s, 1);
+            if (Bp.H > b) {
+                status = ECASQ_EINFEASIBLE;
+                done = true;
+            }
+        }
+        if (!done) {
+            for (int it = 0; it < A.max_iters; it++) {
+                const double lc = (Bp.M - Ap.M) / (Ap.H - Bp.H);
+                if (!(lc > 0.0)) break;
+                const int free_buf = Bp.buf == 0 ? 1 : 0;
+                Pt Cp = row_solve<CMAX>(R, lc, A.exact_s, free_buf);
+                if ((Cp.H == Ap.H && Cp.M == Ap.M) || (Cp.H == Bp.H && Cp.M == Bp.M)) break;
+                if (Cp.H > b) Ap = Cp;
+                else Bp = Cp;
+            }
+        }
+        lamB = Bp.lam;
+        t = Bp.t;
+        if (lane == 0) {
+            if (t == 2 || Bp.buf < 0) {
+                R.chain[0] = 0;
+                R.chain[1] = p - 1;
+            } else {
+                const int16_t* bp = R.bp[Bp.buf];
+                R.chain[t - 1] = p - 1;
+                for (int i = t; i >= 3; i--) R.chain[i - 2] = bp[i * dpad + R.chain[i - 1]];
+                R.chain[0] = 0;
+            }
+        }
+        wave_sync();
+    }
+    int rounds_run = 0;
+    if (status != ECASQ_ENONFINITE && A.refine_rounds > 0 && t >= 3 &&
+        __builtin_isfinite(lamB))
+        rounds_run = row_refine(R, t, lamB * R.s2tot, b, 1, A.refine_rounds,
+                                A.refine_exhaustive);
+    if (lane == 0) {
+        double mse = 0.0, hs = 0.0, ho = 0.0, vn = 0.0;
+        if (status != ECASQ_ENONFINITE) {
+            const Hist H = row_hist(R);
+            for (int r = 0; r + 1 < t; r++) {
+                double C, P;
+                cell_at(H, R.chain[r], R.chain[r + 1], tab, C, P);
+                mse = mse + C;
+                hs = hs - P;
+            }
+            ho = chain_hout(H, t, R.chain, tab);
+            vn = R.s2tot > 0.0 ? mse / R.s2tot : 0.0;
+            for (int r = 0; r < t; r++) A.codebooks[row * A.s + r] = R.v[R.chain[r]];
+            if (p == 2 && hs > b) status = ECASQ_EINFEASIBLE;
+        }
+        A.t_out[row] = t;
+        if (A.infos) {
+            ecasq_info inf;
+            inf.t = t;
+            inf.p = nonfinite ? 0 : p;
+            inf.lambda = lamB;
+            inf.mse = mse;
+            inf.vnmse = vn;
+            inf.entropy = ho;
+            inf.entropy_surrogate = hs;
+            const double lr = __builtin_isfinite(lamB) ? lamB : 0.0;
+            inf.objective = __builtin_fma(lr, ho, vn);
+            inf.rate_total = ho + (32.0 * (double)t) / R.dd;
+            inf.dp_solves = R.solves;
+            inf.refine_rounds_run = rounds_run;
+            inf.cells = R.cells;
+            inf.status = status;
+            inf.reserved = 0;
+            A.infos[row] = inf;
+        }
+    }
+}
+
+template <int DT>
+hipError_t launch_dt(const BatchArgs& A, int cmax, unsigned grid, unsigned threads, size_t lds,
+                     hipStream_t st) {
+    hipError_t e = hipSuccess;
+#define ECASQ_LAUNCH(C)                                                                     \
+    do {                                                                                     \
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_batched<DT, C>),           \
+                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);      \
+        if (e != hipSuccess) return e;                                                       \
+        k_batched<DT, C><<<grid, threads, lds, st>>>(A);                                     \
+    } while (0)
+    if (cmax <= 1) ECASQ_LAUNCH(1);
+    else if (cmax <= 2) ECASQ_LAUNCH(2);
+    else if (cmax <= 4) ECASQ_LAUNCH(4);
+    else ECASQ_LAUNCH(8);
+#undef ECASQ_LAUNCH
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_batched(const void* x, int dt, int64_t n, int32_t d, int32_t s, double b,
+                          int32_t refine_rounds, int32_t refine_exhaustive, int32_t exact_s,
+                          int32_t max_iters, double* codebooks, int32_t* t_out, void* infos,
+                          hipStream_t st) {
+    int dpad = kWave;
+    while (dpad < d) dpad <<= 1;
+    const RowLayout L = row_layout(dpad, s);
+    // rows per workgroup: as many as fit next to the table in 128 KB of LDS
+    const size_t table = sizeof(double2) * kLog2Size;
+    int rows = (int)((128 * 1024 - table) / L.total);
+    if (rows > kMaxRows) rows = kMaxRows;
+    if (rows < 1) return hipErrorInvalidValue;
+    BatchArgs A;
+    A.x = x;
+    A.n = n;
+    A.d = d;
+    A.dpad = dpad;
+    A.s = s;
+    A.rows_per_block = rows;
+    A.b = b;
+    A.refine_rounds = refine_rounds;
+    A.refine_exhaustive = refine_exhaustive;
+    A.exact_s = exact_s;
+    A.max_iters = max_iters;
+    A.codebooks = codebooks;
+    A.t_out = t_out;
+    A.infos = static_cast<ecasq_info*>(infos);
+    const size_t lds = table + (size_t)rows * L.total;
+    const unsigned grid = (unsigned)((n + rows - 1) / rows);
+    const unsigned threads = (unsigned)(rows * kWave);
+    const int cmax = dpad / kWave;
+    if (dt == 0) return launch_dt<0>(A, cmax, grid, threads, lds, st);
+    if (dt == 1) return launch_dt<1>(A, cmax, grid, threads, lds, st);
+    return launch_dt<2>(A, cmax, grid, threads, lds, st);
+}
+
+}  // namespace ecasq

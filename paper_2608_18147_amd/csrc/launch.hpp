@@ -73,4 +73,10 @@ hipError_t launch_quantize(const void* x, int dt, int64_t d, const double* codeb
 hipError_t launch_entropy(const unsigned long long* hist, int32_t t, int64_t d, double* ent,
                           int64_t* hist_out, hipStream_t st);
 
+// ---- batched.hip ----
+hipError_t launch_batched(const void* x, int dt, int64_t n, int32_t d, int32_t s, double b,
+                          int32_t refine_rounds, int32_t refine_exhaustive, int32_t exact_s,
+                          int32_t max_iters, double* codebooks, int32_t* t_out, void* infos,
+                          hipStream_t st);
+
 }  // namespace ecasq

@@ -272,3 +272,84 @@ def test_quantize_solution_end_to_end():
     assert _close(float(ent), e_o, 1e-12)
     # the empirical entropy tracks H(Xhat)
     assert abs(float(ent) - info["entropy"]) < 0.05
+
+
+# ---------------------------------------------------------------- batched rows
+
+
+def _compare_row(cb, t, info, o, s):
+    assert t == o.t, (t, o.t)
+    np.testing.assert_array_equal(cb[:t], o.codebook)
+    assert info["status"] == o.status
+    for k in ("mse", "vnmse", "entropy", "entropy_surrogate", "objective", "rate_total"):
+        assert _close(info[k], getattr(o, k)), (k, info[k], getattr(o, k))
+    assert info["dp_solves"] == o.dp_solves and info["cells"] == o.cells
+    assert info["refine_rounds_run"] == o.refine_rounds
+    assert info["lambda"] == o.lam or (math.isinf(info["lambda"]) and math.isinf(o.lam))
+
+
+@pytest.mark.parametrize("R,exh", [(0, 0), (5, 0), (3, 1)])
+def test_batched_rows_parity(R, exh):
+    rows = inputs.make("kv_rows")[:48]
+    _say("batched kv rows", rows.shape, R, exh)
+    opts = ecasq.ecasq_default_options(refine_rounds=R, refine_exhaustive=exh)
+    cbs, tt, infos = ecasq.ecasq_solve_batched(_dev(rows), 16, 3.0, options=opts)
+    cbs, tt = cbs.cpu().numpy(), tt.cpu().numpy()
+    infos = ecasq.infos_to_dicts(infos)
+    for r in range(rows.shape[0]):
+        o = pipeline.solve(rows[r].astype(np.float32), 16, 3.0, refine_rounds=R,
+                           exhaustive=bool(exh), recovery="backpointers")
+        _compare_row(cbs[r], int(tt[r]), infos[r], o, 16)
+
+
+def test_batched_shapes_and_edge_rows():
+    rng = np.random.default_rng(44)
+    cases = []
+    x = rng.standard_normal((6, 100)).astype(np.float32)  # d not a power of two
+    x[1] = 2.5                                            # one distinct value
+    x[2] = np.where(rng.random(100) < 0.5, -1.0, 3.0)     # two distinct values
+    x[3, :50] = 0.0                                        # heavy duplicates
+    cases.append(("d100_s8_b2", x, 8, 2.0))
+    cases.append(("d512_s32_b3", rng.standard_t(3, (3, 512)).astype(np.float32), 32, 3.0))
+    cases.append(("d64_s4_b0.5", rng.standard_normal((4, 64)).astype(np.float32), 4, 0.5))
+    cases.append(("d200_s12_b9", rng.standard_normal((2, 200)).astype(np.float32), 12, 9.0))
+    for name, xb, s, b in cases:
+        _say("batched", name)
+        cbs, tt, infos = ecasq.ecasq_solve_batched(_dev(xb), s, b)
+        cbs, tt = cbs.cpu().numpy(), tt.cpu().numpy()
+        infos = ecasq.infos_to_dicts(infos)
+        for r in range(xb.shape[0]):
+            o = pipeline.solve(xb[r], s, b, recovery="backpointers")
+            _compare_row(cbs[r], int(tt[r]), infos[r], o, s)
+
+
+def test_batched_nonfinite_row_is_flagged():
+    x = np.random.default_rng(2).standard_normal((3, 64)).astype(np.float32)
+    x[1, 7] = np.inf
+    _say("batched nonfinite")
+    cbs, tt, infos = ecasq.ecasq_solve_batched(_dev(x), 8, 2.0)
+    infos = ecasq.infos_to_dicts(infos)
+    assert infos[1]["status"] == ecasq.ECASQ_ENONFINITE and int(tt[1]) == 0
+    for r in (0, 2):
+        o = pipeline.solve(x[r], 8, 2.0, recovery="backpointers")
+        _compare_row(cbs[r].cpu().numpy(), int(tt[r]), infos[r], o, 8)
+
+
+def test_batched_full_kv_workload_sampled():
+    """The full 4096 x 128 fp16 batch in one launch: every row feasible and
+    spanning its data; 64 sampled rows match the oracle exactly."""
+    rows = inputs.make("kv_rows")
+    _say("batched full", rows.shape)
+    cbs, tt, infos = ecasq.ecasq_solve_batched(_dev(rows), 16, 3.0)
+    cbs, tt = cbs.cpu().numpy(), tt.cpu().numpy()
+    infos = ecasq.infos_to_dicts(infos)
+    r32 = rows.astype(np.float32)
+    for r in range(rows.shape[0]):
+        t = int(tt[r])
+        assert 2 <= t <= 16
+        assert cbs[r, 0] == r32[r].min() and cbs[r, t - 1] == r32[r].max()
+        assert np.all(np.diff(cbs[r, :t]) > 0)
+        assert infos[r]["status"] == 0 and infos[r]["entropy"] <= 3.0 + 1e-12
+    for r in np.random.default_rng(0).choice(rows.shape[0], 64, replace=False):
+        o = pipeline.solve(r32[r], 16, 3.0, recovery="backpointers")
+        _compare_row(cbs[r], int(tt[r]), infos[r], o, 16)
