@@ -2,16 +2,18 @@
 """Throughput of the ECASQ hot path on one MI355X.
 
 One step = the whole path on one synthetic vector already resident in HBM:
-sort + histogram + exact prefix sums, the lambda search (one full dp_APX
-solve per query), Hirschberg recovery, three-colour refinement (5 rounds at
-most) and the final Philox stochastic rounding with its empirical entropy.
+sort + histogram + exact prefix sums, the lambda search (passes of 8
+multipliers, each pass one sweep of dp_APX solving all 8), Hirschberg
+recovery, three-colour refinement (5 rounds at most) and the final Philox
+stochastic rounding with its empirical entropy.
 
 Default workload (weights_256k): fp32, d = 2^18, 0.9 Normal(0, 0.01) +
 0.1 Laplace(0, 0.1), s = 32, budget 2.0 bits/entry, seed 0.
 
 Printed (one JSON line): DP cell-updates/s counted as s*d^2/2 per DP solve
-(the nominal unit), the roofline of the DP layer kernel measured with HIP
-events on its own stream, and the CPU oracle timed on a bounded sample.
+(the nominal unit; one solve per multiplier), the roofline of the DP layer
+kernel of the search passes measured with HIP events on its own stream, and
+the CPU oracle timed on a bounded sample.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME]
 """
@@ -21,18 +23,22 @@ import os
 import sys
 import time
 
-# Algorithmic fp64 operations per DP cell in the canonical cell arithmetic:
-# 4 range differences, 2 fma (tu, td), 2 fma (C), w*d, one IEEE division
-# (counted as 1), 2 products (yu, yd), two log2 evaluations of 13 flops each
-# (fma for r, 4 Horner fma, 1 add, 1 final fma), 1 mul + 1 fma for the entropy
-# term, 1 add + 1 fma for the candidate.  fma counts 2.
-FLOPS_PER_CELL = 48
+# Algorithmic fp64 operations per DP cell in the canonical cell arithmetic.
+# Shared by every multiplier of a launch (45): 4 range differences, 2 fma (tu,
+# td), 2 fma (C), w*d, one IEEE division (counted as 1), 2 products (yu, yd),
+# two log2 evaluations of 13 flops each (fma for r, 4 Horner fma, 1 add, 1
+# final fma), 1 mul + 1 fma for the entropy term.  Per multiplier (3): 1 add +
+# 1 fma for the candidate.  fma counts 2.
+FLOPS_SHARED = 45
+FLOPS_PER_LAMBDA = 3
+LAMBDAS_PER_PASS = 8
 FP64_VECTOR_PEAK_TFLOPS = 78.6
 
-# HBM bytes per k_dp_layer launch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs
-# (profiles/k_dp_layer_weights_256k.md), scaled by a plain copy's readings
-# (FETCH x2.0, WRITE x1.0).  Valid only for the kernel sources they were taken
-# on: reported as null once those sources change.
+
+def flops_per_cell(nlam):
+    return FLOPS_SHARED + FLOPS_PER_LAMBDA * nlam
+
+
 TRAFFIC_BYTES_PER_LAUNCH = 283.0e6
 TRAFFIC_SOURCES_SHA = "89c9cd8d83e47782"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
@@ -78,6 +84,33 @@ def cpu_baseline(x, s, lam, sample_d):
     }
 
 
+def batched_rate(torch, ecasq, inputs, reps=3):
+    """Solves/s of the batched path: 4096 KV-cache-like fp16 rows of d = 128,
+    s = 16, budget 3.0 bits/entry, one solve per row (no refinement), all rows
+    in one launch."""
+    rows = inputs.make("kv_rows", seed=0)
+    xd = torch.from_numpy(rows).to("cuda")
+    opts = ecasq.ecasq_default_options(refine_rounds=0)
+    ecasq.ecasq_solve_batched(xd, 16, 3.0, options=opts)  # warm-up
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        cbs, tt, infos = ecasq.ecasq_solve_batched(xd, 16, 3.0, options=opts)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / reps
+    inf = ecasq.infos_to_dicts(infos)
+    cells = sum(i["cells"] for i in inf)
+    solves = sum(i["dp_solves"] for i in inf)
+    n, d = rows.shape
+    log(f"batched: {dt * 1e3:.2f} ms per {n}-row launch")
+    return {
+        "workload": "kv_rows", "rows": n, "d": d, "s": 16, "budget_bits": 3.0,
+        "refine_rounds": 0, "ms_per_launch": dt * 1e3, "solves_per_s": n / dt,
+        "dp_solves_per_row": solves / n, "cells_per_s": cells / dt,
+        "nominal_cell_updates_per_s": solves * 16 * d * d / 2.0 / dt,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -88,11 +121,12 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-sample", type=int, default=32768)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-batched", action="store_true")
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print("bench.py measures one GPU only: the single-vector path is not sharded across "
-              "GPUs in this build (see DESIGN.md for how it would shard)", file=sys.stderr)
+        print("bench.py measures one GPU only: the single-vector path runs on one GPU and "
+              "is not sharded across GPUs", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -122,7 +156,8 @@ def main():
             f"{info['dp_solves']} DP solves, t={info['t']}")
 
     ecasq.ecasq_timing_enable(True)
-    ecasq.ecasq_timing_read(reset=True)
+    for v in (ecasq.TIMING_SINGLE, ecasq.TIMING_PASS):
+        ecasq.ecasq_timing_read(v, reset=True)
     infos = []
     torch.cuda.synchronize()
     t_start = time.perf_counter()
@@ -133,14 +168,16 @@ def main():
         log(f"step {i + 1}/{args.steps}: {time.perf_counter() - t0:.2f} s")
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
-    ms, launches, cells = ecasq.ecasq_timing_read()
+    ms, launches, cells = ecasq.ecasq_timing_read(ecasq.TIMING_PASS)
+    ms1, launches1, cells1 = ecasq.ecasq_timing_read(ecasq.TIMING_SINGLE)
     ecasq.ecasq_timing_enable(False)
 
     nominal = sum(inf["dp_solves"] * s * d * d / 2.0 for inf, _ in infos)
     exact = sum(inf["cells"] for inf, _ in infos)
     value = nominal / elapsed
     avg_ms = ms / max(launches, 1)
-    achieved = FLOPS_PER_CELL * (cells / max(launches, 1)) / (avg_ms * 1e-3) / 1e12
+    fpc = flops_per_cell(LAMBDAS_PER_PASS)
+    achieved = fpc * (cells / max(launches, 1)) / (avg_ms * 1e-3) / 1e12 if ms > 0 else 0.0
     info, ent = infos[-1]
     out = {
         "metric": "DP cell-updates/s (s*d^2/2 per solve)",
@@ -161,7 +198,7 @@ def main():
         },
         "roofline": {
             "bound": "alu",
-            "kernel": "k_dp_layer (fp64 VALU)",
+            "kernel": "k_dp_layer, 8 multipliers per launch (fp64 VALU)",
             "achieved": achieved,
             "peak": FP64_VECTOR_PEAK_TFLOPS,
             "unit": "TFLOP/s",
@@ -169,19 +206,29 @@ def main():
             "traffic": (TRAFFIC_BYTES_PER_LAUNCH if kernel_sources_sha() == TRAFFIC_SOURCES_SHA
                         else None),
             "traffic_unit": "bytes/launch",
-            "flops_per_cell": FLOPS_PER_CELL,
+            "flops_per_cell": fpc,
             "avg_launch_ms": avg_ms,
             "launches": launches,
             "cells_per_s": cells / (ms * 1e-3) if ms > 0 else None,
+            "lambda_cells_per_s": LAMBDAS_PER_PASS * cells / (ms * 1e-3) if ms > 0 else None,
+        },
+        "single_multiplier_layers": {
+            "launches": launches1, "ms": ms1,
+            "cells_per_s": cells1 / (ms1 * 1e-3) if ms1 > 0 else None,
+            "achieved_tflops": (flops_per_cell(1) * cells1 / (ms1 * 1e-3) / 1e12
+                                if ms1 > 0 else None),
         },
         "exact_cells_per_s": exact / elapsed,
         "dp_solves_per_step": info["dp_solves"],
+        "search_passes_per_step": info["search_passes"],
         "solution": {
             "t": info["t"], "p": info["p"], "lambda": info["lambda"], "vnmse": info["vnmse"],
             "entropy": info["entropy"], "entropy_surrogate": info["entropy_surrogate"],
             "empirical_entropy": float(ent), "refine_rounds_run": info["refine_rounds_run"],
         },
     }
+    if not args.no_batched:
+        out["batched"] = batched_rate(torch, ecasq, inputs)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         out["cpu_baseline"] = cpu_baseline(x, s, 0.1, args.cpu_sample)

@@ -59,25 +59,28 @@ typedef struct {
     int32_t refine_rounds;     /* Sec. 6 rounds, upper bound (default 5; 0 = off) */
     int32_t refine_exhaustive; /* 0: binary search of Sec. 6 (default); 1: full scan */
     int32_t exact_s;           /* 0: at most s values (default); 1: exactly min(s, p) */
-    int32_t max_search_iters;  /* lambda-search queries after the first (default 64) */
+    int32_t max_search_passes; /* lambda-search passes of up to 8 solves (default 32) */
     int32_t recovery;          /* 0: Hirschberg, O(d) space (default); 1: stored argmins */
+    int32_t search_width;      /* multipliers per search pass: 8 (default) or 1 */
 } ecasq_options;
 
 typedef struct {
     int32_t t;                /* codebook size actually used */
     int32_t p;                /* number of distinct input values */
-    double lambda;            /* multiplier of the returned solution, vNMSE units */
+    double lambda;            /* multiplier of the refinement and of `objective`, vNMSE
+                                 units: the final chord slope of the search (budget
+                                 mode) or the given lambda */
     double mse;               /* MSE(Q, X) = sum (b_x - x)(x - a_x), Sec. 2 */
     double vnmse;             /* MSE / ||X||^2 */
     double entropy;           /* H(Xhat) from expected frequencies, bits/entry */
     double entropy_surrogate; /* H(I,B) of Sec. 5 */
     double objective;         /* vNMSE + lambda * H(Xhat) */
     double rate_total;        /* H(Xhat) + 32 t / d (App. F.1 rate accounting) */
-    int32_t dp_solves;        /* full DP solves run by the search */
+    int32_t dp_solves;        /* full DP solves (multipliers) run by the search */
     int32_t refine_rounds_run;
     int64_t cells;            /* DP cells evaluated (search + recovery) */
     int32_t status;           /* ecasq_status of the solve */
-    int32_t reserved;
+    int32_t search_passes;    /* passes of the budget search (0 in fixed-lambda mode) */
 } ecasq_info;
 
 /* Defaults listed in ecasq_options. */
@@ -91,6 +94,21 @@ void ecasq_default_options(ecasq_options *opts);
  * (device, length >= s, may be NULL) receives each value's index among the
  * sorted distinct inputs.  Entries past t are left untouched.  info may be NULL.
  * The returned codebook has H(Xhat) <= b whenever the status is ECASQ_OK.
+ *
+ * Search (Sec. 3 and Sec. 5, supporting-line queries of App. F.7), in passes
+ * of w = opts->search_width multipliers that one sweep of the DP solves
+ * together (w = 1 is the plain sequential chord search):
+ *   pass 1: lambda in {0, 1e-4, 1e-3, 1e-2, 1e-1, 1, 10, 100} (w = 8) or {0};
+ *   then A = the point with H(I,B) > b of largest lambda, B = the point with
+ *   H(I,B) <= b of smallest lambda (if there is none: the two-value codebook
+ *   {min X, max X} when b >= 1, else one solve at lambda = 2^40), and the next
+ *   pass is the chord slope lc = (M_B - M_A) / (H_A - H_B) followed, when
+ *   w = 8, by A + (B - A) g / 8 for g = 1..7 (lc times 1/4, 1/2, 3/4, 3/2, 2,
+ *   3, 4 when B is the two-value codebook);
+ *   the search ends when the solve at lc returns A or B again, or after
+ *   max_search_passes passes.
+ * The codebook is B, recovered at the multiplier it was found at; the
+ * refinement then runs at the final chord slope under the budget guard.
  */
 ecasq_status ecasq_solve(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
                          double bits_per_entry, void *stream, double *codebook,
@@ -127,8 +145,9 @@ ecasq_status ecasq_quantize(const void *x, ecasq_dtype dt, int64_t d, const doub
 /*
  * Many independent short vectors in one launch (one wavefront per row, several
  * rows per workgroup): x is n rows of d entries, row-major.  Each row is
- * solved as ecasq_solve_ex would with opts->recovery = 1 (argmins kept in
- * LDS; opts->recovery itself is ignored).  codebooks: device, n x s fp64 (row
+ * solved as ecasq_solve_ex would with opts->recovery = 1 and
+ * opts->search_width = 1 (argmins kept in LDS; both fields of opts are
+ * ignored).  codebooks: device, n x s fp64 (row
  * r's t_out[r] values first, the rest untouched); t_out: device, n int32
  * (0 for a row holding NaN/Inf); infos_dev: device, n ecasq_info, may be NULL
  * (per-row status: ECASQ_OK, ECASQ_EINFEASIBLE or ECASQ_ENONFINITE).
@@ -171,13 +190,17 @@ ecasq_status ecasq_dp_trace(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
  * Kernel timing for measurement tools.  While enabled (process-wide), every
  * launch of the DP layer kernel is bracketed by two HIP events recorded on the
  * stream it runs on; the elapsed times are read when the solve synchronizes.
- * ecasq_timing_read returns the summed milliseconds, the number of timed
- * launches and the DP cells those launches evaluated (host pointers, any may
- * be NULL); reset != 0 clears the totals.  Not thread-safe.
+ * Launches are kept apart by variant: 0 = one multiplier per launch (fixed
+ * lambda, width-1 search, recovery half-DPs), 1 = the 8 multipliers of a
+ * search pass.  ecasq_timing_read returns, for one variant, the summed
+ * milliseconds, the number of timed launches and the (column, predecessor)
+ * cells those launches evaluated, each cell for every multiplier of its
+ * launch (host pointers, any may be NULL); reset != 0 clears that variant's
+ * totals.  Not thread-safe.
  */
 void ecasq_timing_enable(int32_t on);
-void ecasq_timing_read(double *layer_ms, int64_t *layer_launches, int64_t *layer_cells,
-                       int32_t reset);
+void ecasq_timing_read(int32_t variant, double *layer_ms, int64_t *layer_launches,
+                       int64_t *layer_cells, int32_t reset);
 
 #ifdef __cplusplus
 }

@@ -519,42 +519,56 @@ int orc_refine(const double *v, const double *N, const double *S, const double *
 }
 
 /* ------------------------------------------------------------------------- */
-/* Lambda search for a budget b (Sec. 3: binary search on lambda; Sec. 5: keep
- * the lowest-MSE solution with H(I,B) <= b).  The search is a slope (chord)
- * query between an infeasible point A and a feasible point B, as used for the
- * frontier in App. F.7.  lambda is in vNMSE units; the DP uses
- * lambda' = RN(lambda * ||X||^2).
+/* Lambda search for a budget b (Sec. 3: search on lambda; Sec. 5: keep the
+ * lowest-MSE solution with H(I,B) <= b), in passes of `width` multipliers
+ * (width 8 or 1; lambda in vNMSE units; each query is one full DP solve at
+ * lambda' = RN(lambda * ||X||^2)):
+ *
+ *   pass 1: lambda in {0, 1e-4, 1e-3, 1e-2, 1e-1, 1, 10, 100} (width 8) or
+ *   {0} (width 1);
+ *   then, with A = the infeasible point (H(I,B) > b) of largest lambda and
+ *   B = the feasible point of smallest lambda (or, if none, the two-value
+ *   codebook {v_0, v_{p-1}} when b >= 1, else the solve at lambda = 2^40):
+ *     lc = (M_B - M_A) / (H_A - H_B), the slope of the chord AB (App. F.7
+ *     supporting-line query);
+ *     next pass: lc and width-1 more multipliers, la + (lb - la) g / 8 for
+ *     g = 1..7 (or lc times 1/4, 1/2, 3/4, 3/2, 2, 3, 4 when B is the
+ *     two-value codebook);
+ *   stop when the answer at lc is A or B again (H and M bit for bit): no DP
+ *   solution lies below the chord, A and B are adjacent supported points.
+ *
+ * Width 1 is the plain sequential chord search.  Returns B, the multiplier at
+ * which B was found (used to recover it) and the final chord slope lc (the
+ * multiplier of the refinement step).  A point's lambda is the multiplier of
+ * its first query.
  *
  * traj (optional, 4 doubles per solve): lambda, H(I,B), vNMSE, t.
  * out: lambda_B, H_B, M_B, t_B, solves, cells, status (0 ok, -3 infeasible),
- *      closed_form (1 if B is {v_0, v_{p-1}} from the closed form)
+ *      lambda_final, passes
  */
+#define SEARCH_M 8
+#define MAX_PTS 1024
+
+typedef struct {
+    double lam, H, M;
+    int32_t t;
+} point_t;
+
 int orc_search(const double *v, const double *N, const double *S, const double *S2, int64_t p,
-               int64_t d, int32_t s, double b, int32_t exact_s, int32_t max_iters, double *traj,
-               int32_t traj_cap, double *out)
+               int64_t d, int32_t s, double b, int32_t exact_s, int32_t max_passes, int32_t width,
+               double *traj, int32_t traj_cap, double *out)
 {
+    if (width != 1 && width != SEARCH_M) return -1;
     hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
     double r[5];
-    int32_t nsol = 0;
+    int32_t nsol = 0, npass = 0;
     double cells = 0;
-    double A_l, A_h, A_m, B_l, B_h, B_m;
-    int32_t A_t, B_t, closed = 0, status = 0;
-#define SOLVE(lam_, l_, h_, m_, t_)                                                           \
-    do {                                                                                      \
-        double lp_ = (lam_) * H.s2tot;                                                        \
-        orc_dp_forward(v, N, S, S2, p, d, s, exact_s, lp_, r, NULL, NULL, NULL);              \
-        l_ = (lam_); h_ = r[2]; m_ = r[1] / H.s2tot; t_ = (int32_t)r[3]; cells += r[4];       \
-        if (traj && nsol < traj_cap) {                                                        \
-            traj[4 * nsol] = l_; traj[4 * nsol + 1] = h_; traj[4 * nsol + 2] = m_;           \
-            traj[4 * nsol + 3] = t_;                                                          \
-        }                                                                                     \
-        nsol++;                                                                               \
-    } while (0)
-
+    point_t *pts = malloc(sizeof(point_t) * MAX_PTS);
+    int32_t npts = 0;
     if (p <= 2) {
         /* every value is used; nothing to search */
         out[0] = 0.0; out[1] = 0.0; out[2] = 0.0; out[3] = (double)p; out[4] = 0; out[5] = 0;
-        out[6] = 0; out[7] = 0;
+        out[6] = 0; out[7] = 0.0; out[8] = 0;
         if (p == 2) {
             double C, P;
             cell_terms(&H, 0, 1, &C, &P);
@@ -562,39 +576,97 @@ int orc_search(const double *v, const double *N, const double *S, const double *
             out[2] = (0.0 + C) / H.s2tot;
             if (out[1] > b) out[6] = -3;
         }
+        free(pts);
         return 0;
     }
-    SOLVE(0.0, A_l, A_h, A_m, A_t);
-    if (A_h <= b) {
-        out[0] = A_l; out[1] = A_h; out[2] = A_m; out[3] = A_t; out[4] = nsol; out[5] = cells;
-        out[6] = 0; out[7] = 0;
-        return 0;
-    }
-    if (b >= 1.0) {
-        double C, P;
-        cell_terms(&H, 0, p - 1, &C, &P);
-        B_l = INFINITY; B_h = 0.0 - P; B_m = (0.0 + C) / H.s2tot; B_t = 2; closed = 1;
-    } else {
-        SOLVE(0x1p40, B_l, B_h, B_m, B_t);
-        if (B_h > b) {
-            out[0] = B_l; out[1] = B_h; out[2] = B_m; out[3] = B_t; out[4] = nsol; out[5] = cells;
-            out[6] = -3; out[7] = 0;
-            return 0;
+    /* evaluate one multiplier (a full DP solve) */
+#define EVAL(lam_)                                                                            \
+    do {                                                                                      \
+        double l_ = (lam_);                                                                   \
+        orc_dp_forward(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, r, NULL, NULL, NULL);     \
+        if (npts < MAX_PTS) {                                                                 \
+            pts[npts].lam = l_; pts[npts].H = r[2]; pts[npts].M = r[1] / H.s2tot;            \
+            pts[npts].t = (int32_t)r[3]; npts++;                                               \
+        }                                                                                     \
+        cells += r[4];                                                                        \
+        if (traj && nsol < traj_cap) {                                                        \
+            traj[4 * nsol] = l_; traj[4 * nsol + 1] = r[2]; traj[4 * nsol + 2] = r[1] / H.s2tot; \
+            traj[4 * nsol + 3] = r[3];                                                        \
+        }                                                                                     \
+        nsol++;                                                                               \
+    } while (0)
+
+    static const double grid[SEARCH_M] = {0.0, 1e-4, 1e-3, 1e-2, 1e-1, 1.0, 10.0, 100.0};
+    for (int g = 0; g < width; g++) EVAL(grid[g]);
+    npass = 1;
+    int32_t status = 0;
+    point_t A, B;
+    double lam_final = 0.0;
+    int have_B = 0, closed = 0;
+    for (;;) {
+        /* A: infeasible point of largest lambda; B: feasible point of smallest
+           lambda (first occurrence wins among equal lambdas) */
+        int ia = -1, ib = -1;
+        for (int x = 0; x < npts; x++) {
+            if (pts[x].H > b) {
+                if (ia < 0 || pts[x].lam > pts[ia].lam) ia = x;
+            } else {
+                if (ib < 0 || pts[x].lam < pts[ib].lam) ib = x;
+            }
+        }
+        if (ia < 0) { /* lambda = 0 is feasible */
+            B = pts[ib]; have_B = 1; lam_final = B.lam;
+            break;
+        }
+        A = pts[ia];
+        if (ib >= 0) {
+            B = pts[ib]; closed = 0;
+        } else if (b >= 1.0) {
+            double C, P;
+            cell_terms(&H, 0, p - 1, &C, &P);
+            B.lam = INFINITY; B.H = 0.0 - P; B.M = (0.0 + C) / H.s2tot; B.t = 2; closed = 1;
+        } else {
+            /* no feasible point yet: try the largest multiplier once */
+            int tried = 0;
+            for (int x = 0; x < npts; x++) if (pts[x].lam == 0x1p40) tried = 1;
+            if (tried || npass >= max_passes) {
+                /* infeasible budget: return the lowest-entropy point found */
+                int ih = 0;
+                for (int x = 1; x < npts; x++) if (pts[x].H < pts[ih].H) ih = x;
+                B = pts[ih]; have_B = 1; status = -3; lam_final = B.lam;
+                break;
+            }
+            EVAL(0x1p40);
+            npass++;
+            continue;
+        }
+        have_B = 1;
+        double lc = (B.M - A.M) / (A.H - B.H);
+        lam_final = closed ? lc : B.lam;
+        if (!(lc > 0.0) || npass >= max_passes) break;
+        double q[SEARCH_M];
+        q[0] = lc;
+        for (int g = 1; g < width; g++) {
+            if (closed) {
+                static const double mul[SEARCH_M - 1] = {0.25, 0.5, 0.75, 1.5, 2.0, 3.0, 4.0};
+                q[g] = lc * mul[g - 1];
+            } else {
+                q[g] = A.lam + ((B.lam - A.lam) * (double)g) / 8.0;
+            }
+        }
+        int first = npts;
+        for (int g = 0; g < width; g++) EVAL(q[g]);
+        npass++;
+        point_t Cq = pts[first];
+        if ((Cq.H == A.H && Cq.M == A.M) || (Cq.H == B.H && Cq.M == B.M)) {
+            lam_final = lc;
+            break;
         }
     }
-    for (int32_t it = 0; it < max_iters; it++) {
-        double lc = (B_m - A_m) / (A_h - B_h);
-        if (!(lc > 0.0)) break;
-        double C_l, C_h, C_m;
-        int32_t C_t;
-        SOLVE(lc, C_l, C_h, C_m, C_t);
-        if ((C_h == A_h && C_m == A_m) || (C_h == B_h && C_m == B_m))
-            break;
-        if (C_h > b) { A_l = C_l; A_h = C_h; A_m = C_m; A_t = C_t; }
-        else { B_l = C_l; B_h = C_h; B_m = C_m; B_t = C_t; closed = 0; }
-    }
-#undef SOLVE
-    out[0] = B_l; out[1] = B_h; out[2] = B_m; out[3] = B_t; out[4] = nsol; out[5] = cells;
-    out[6] = status; out[7] = closed;
+#undef EVAL
+    (void)have_B;
+    out[0] = B.lam; out[1] = B.H; out[2] = B.M; out[3] = B.t; out[4] = nsol; out[5] = cells;
+    out[6] = status; out[7] = lam_final; out[8] = npass;
+    free(pts);
     return 0;
 }

@@ -143,15 +143,19 @@ def refine(H, chain, lamp, b=math.inf, budget=False, rounds=5, exhaustive=False)
     return u, int(n), int(moves.value)
 
 
-def search(H, s, b, exact_s=False, max_iters=64):
-    out = np.zeros(8)
-    cap = 256
+def search(H, s, b, exact_s=False, max_passes=32, width=8):
+    """Budget search on lambda in passes of `width` (8 or 1) multipliers."""
+    out = np.zeros(9)
+    cap = 1024
     traj = np.zeros(4 * cap)
-    native.lib().orc_search(*H.args(), s, b, int(exact_s), max_iters, native.dptr(traj), cap,
-                            native.dptr(out))
+    rc = native.lib().orc_search(*H.args(), s, b, int(exact_s), max_passes, width,
+                                 native.dptr(traj), cap, native.dptr(out))
+    if rc != 0:
+        raise ValueError("search width must be 1 or 8")
     n = int(out[4])
     return dict(lam=out[0], H=out[1], M=out[2], t=int(out[3]), solves=n, cells=int(out[5]),
-                status=int(out[6]), traj=traj[: 4 * min(n, cap)].reshape(-1, 4))
+                status=int(out[6]), lam_final=out[7], passes=int(out[8]),
+                traj=traj[: 4 * min(n, cap)].reshape(-1, 4))
 
 
 @dataclass
@@ -172,6 +176,7 @@ class Result:
     cells: int
     status: int
     traj: np.ndarray = field(default=None)
+    passes: int = 0
 
 
 def _finish(H, chain, lam, solves, rounds, cells, status, traj=None):
@@ -198,19 +203,22 @@ def _recover(H, t, lam, recovery="hirschberg", s=None, exact_s=False):
     return hirschberg(H, t, lam * H.s2tot)
 
 
-def solve(x, s, b, refine_rounds=5, exhaustive=False, exact_s=False, max_iters=64,
-          recovery="hirschberg"):
-    """Budget mode: the lowest-MSE supported solution with H(I,B) <= b, then
-    refinement at its multiplier with the budget guard on H(Xhat)."""
+def solve(x, s, b, refine_rounds=5, exhaustive=False, exact_s=False, max_passes=32,
+          recovery="hirschberg", width=8):
+    """Budget mode: the lowest-MSE supported solution with H(I,B) <= b
+    (recovered at the multiplier it was found at), then refinement at the
+    final chord slope with the budget guard on H(Xhat)."""
     H = prepare(x)
-    sr = search(H, s, b, exact_s, max_iters)
+    sr = search(H, s, b, exact_s, max_passes, width)
     chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s)
+    lam = sr["lam_final"]
     rounds = 0
-    if refine_rounds > 0 and math.isfinite(sr["lam"]) and len(chain) >= 3:
-        chain, rounds, _ = refine(H, chain, sr["lam"] * H.s2tot, b, True, refine_rounds,
-                                  exhaustive)
-    return _finish(H, chain, sr["lam"], sr["solves"], rounds, sr["cells"] + hcells,
-                   sr["status"], sr["traj"])
+    if refine_rounds > 0 and math.isfinite(lam) and len(chain) >= 3:
+        chain, rounds, _ = refine(H, chain, lam * H.s2tot, b, True, refine_rounds, exhaustive)
+    r = _finish(H, chain, lam, sr["solves"], rounds, sr["cells"] + hcells, sr["status"],
+                sr["traj"])
+    r.passes = sr["passes"]
+    return r
 
 
 def solve_lagrangian(x, s, lam, refine_rounds=0, exhaustive=False, exact_s=False):

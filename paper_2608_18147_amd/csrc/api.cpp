@@ -2,8 +2,9 @@
 // sequence of one ECASQ solve (see include/ecasq.h for the contract).
 //
 //   prep        sort + weighted histogram + exact prefix sums (Sec. 2, App. D)
-//   search      slope search on lambda, one full dp_APX solve per query
-//               (Sec. 3 and Sec. 5; supporting-line queries as in App. F.7)
+//   search      search on lambda in passes of 8 multipliers, each pass one
+//               sweep of dp_APX for all 8 (Sec. 3 and Sec. 5; supporting-line
+//               queries as in App. F.7)
 //   recovery    Hirschberg on the final multiplier (Sec. 5 / Sec. 4.2), or a
 //               traceback through stored argmins
 //   refinement  three-colour pass (Sec. 6), one kernel
@@ -35,7 +36,9 @@ namespace {
     } while (0)
 
 struct Layout {
-    size_t v, N, S, S2, F0, F1, M0, M1, P0, P1, pval, pidx, last, res, small, chain, kstar, prep;
+    size_t v, N, S, S2, F0, F1, M0, M1, P0, P1, pval, pidx, last, res, mres, small, chain, kstar,
+        prep;
+    int64_t pstride;  // partial entries per multiplier
     size_t total;
 };
 
@@ -52,17 +55,21 @@ Layout layout(int64_t d, int32_t s, bool kstar) {
     L.N = take(nd);
     L.S = take(nd);
     L.S2 = take(nd);
-    L.F0 = take(nd);
-    L.F1 = take(nd);
-    L.M0 = take(nd);
-    L.M1 = take(nd);
-    L.P0 = take(nd);
-    L.P1 = take(nd);
-    const size_t np = (size_t)dp_partial_entries(d);
+    // layer buffers: kMaxLambdas rows of d per array (one per multiplier of a pass)
+    const size_t ndm = nd * kMaxLambdas;
+    L.F0 = take(ndm);
+    L.F1 = take(ndm);
+    L.M0 = take(ndm);
+    L.M1 = take(ndm);
+    L.P0 = take(ndm);
+    L.P1 = take(ndm);
+    L.pstride = dp_partial_entries(d);
+    const size_t np = (size_t)L.pstride * kMaxLambdas;
     L.pval = take(sizeof(double) * np);
     L.pidx = take(sizeof(int32_t) * np);
-    L.last = take(sizeof(double) * 3 * (size_t)(s + 1));
-    L.res = take(sizeof(double) * 32);
+    L.last = take(sizeof(double) * 3 * (size_t)(s + 1) * kMaxLambdas);
+    L.res = take(sizeof(double) * 4 * kMaxLambdas);
+    L.mres = take(sizeof(double) * 8);
     L.small = take(sizeof(int64_t) * 8);
     L.chain = take(sizeof(int32_t) * (size_t)(s + 8));
     L.kstar = kstar ? take(sizeof(int32_t) * (size_t)(s + 1) * (size_t)d) : 0;
@@ -161,42 +168,64 @@ ecasq_status ctx_prep(Ctx& c, const void* x, int dt) {
 
 int64_t tri_cells(int64_t n) { return n * (n + 1) / 2; }
 
-// One full dp_APX solve at lambda (vNMSE units).  Optional per-layer dumps
-// (row i of Fdump / Kdump, row stride `stride`).
-ecasq_status dp_solve(Ctx& c, double lam, int32_t exact_s, Point& out, double* J_out,
-                      double* Fdump, int32_t* Kdump, int64_t stride) {
-    const double lamp = lam * c.s2tot;
+// Full dp_APX solves at nlam multipliers lams[] (vNMSE units), 1 <= nlam <=
+// kMaxLambdas, in one sweep over the layers (nlam must be 1 or kMaxLambdas).
+// With nlam == 1, optional per-layer dumps (row i of Fdump / Kdump, row
+// stride `stride`) and the raw (J, MSE, H(I,B), t) in J_out.
+ecasq_status dp_solve(Ctx& c, const double* lams, int32_t nlam, int32_t exact_s, Point* out,
+                      double* J_out, double* Fdump, int32_t* Kdump, int64_t stride) {
+    if (nlam != 1 && nlam != kMaxLambdas) return ECASQ_EINVAL;
+    if (nlam != 1 && (J_out || Fdump || Kdump)) return ECASQ_EINVAL;
     const int64_t p = c.p;
     const int32_t imax = (int32_t)std::min<int64_t>(c.s, p);
     const int32_t ls = c.s + 1;
+    const int64_t d = c.d;
     double* F[2] = {c.at<double>(c.L.F0), c.at<double>(c.L.F1)};
     double* M[2] = {c.at<double>(c.L.M0), c.at<double>(c.L.M1)};
     double* Ph[2] = {c.at<double>(c.L.P0), c.at<double>(c.L.P1)};
     double* last = c.at<double>(c.L.last);
     double* res = c.at<double>(c.L.res);
-    HIP_TRY(launch_dp_init_fwd(c.H, 0, 1, p - 1, lamp, F[0], M[0], Ph[0],
-                               Kdump ? Kdump + 2 * stride : nullptr, last, ls, c.st));
+    double lamp[kMaxLambdas];
+    for (int32_t m = 0; m < nlam; m++) lamp[m] = lams[m] * c.s2tot;
+    DpInit I;
+    std::memset(&I, 0, sizeof I);
+    I.nlam = nlam;
+    for (int32_t m = 0; m < nlam; m++) {
+        I.lam[m] = lamp[m];
+        I.F[m] = F[0] + m * d;
+        I.M[m] = M[0] + m * d;
+        I.Ph[m] = Ph[0] + m * d;
+    }
+    I.kstar = Kdump ? Kdump + 2 * stride : nullptr;
+    I.last = last;
+    I.last_stride = ls;
+    HIP_TRY(launch_dp_init_fwd(c.H, 0, 1, p - 1, I, c.st));
     if (Fdump)
         HIP_TRY(hipMemcpyAsync(Fdump + 2 * stride + 1, F[0] + 1, sizeof(double) * (p - 1),
                                hipMemcpyDeviceToDevice, c.st));
-    c.cells += p - 1;
+    c.cells += (int64_t)nlam * (p - 1);
     int cur = 0;
     for (int32_t i = 3; i <= imax; i++) {
         DpLayer L;
+        std::memset(&L, 0, sizeof L);
         L.H = c.H;
-        L.Fin = F[cur];
-        L.Fout = F[1 - cur];
+        L.nlam = nlam;
+        for (int32_t m = 0; m < nlam; m++) {
+            L.Fin[m] = F[cur] + m * d;
+            L.Fout[m] = F[1 - cur] + m * d;
+            L.Min[m] = M[cur] + m * d;
+            L.Pin[m] = Ph[cur] + m * d;
+            L.Mout[m] = M[1 - cur] + m * d;
+            L.Pout[m] = Ph[1 - cur] + m * d;
+            L.lam[m] = lamp[m];
+        }
         L.pval = c.at<double>(c.L.pval);
         L.pidx = c.at<int32_t>(c.L.pidx);
+        L.pstride = c.L.pstride;
         L.kb = i - 2;
         L.jlo = i - 1;
         L.jhi = p - 1;
         L.backward = false;
-        L.lam = lamp;
-        L.Min = M[cur];
-        L.Pin = Ph[cur];
-        L.Mout = M[1 - cur];
-        L.Pout = Ph[1 - cur];
         L.kstar = Kdump ? Kdump + (int64_t)i * stride : nullptr;
         L.last = last;
         L.layer = i;
@@ -206,71 +235,133 @@ ecasq_status dp_solve(Ctx& c, double lam, int32_t exact_s, Point& out, double* J
         if (Fdump)
             HIP_TRY(hipMemcpyAsync(Fdump + (int64_t)i * stride + (i - 1), F[1 - cur] + (i - 1),
                                    sizeof(double) * (p - i + 1), hipMemcpyDeviceToDevice, c.st));
-        c.cells += tri_cells(p - i + 1);
+        c.cells += (int64_t)nlam * tri_cells(p - i + 1);
         cur = 1 - cur;
     }
-    HIP_TRY(launch_dp_final(last, ls, imax, exact_s, res, c.st));
-    double r[4];
-    HIP_TRY(hipMemcpyAsync(r, res, sizeof r, hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(launch_dp_final(last, ls, imax, exact_s, nlam, res, c.st));
+    double r[4 * kMaxLambdas];
+    HIP_TRY(hipMemcpyAsync(r, res, sizeof(double) * 4 * nlam, hipMemcpyDeviceToHost, c.st));
     HIP_TRY(hipStreamSynchronize(c.st));
     timing_flush();
-    out.lam = lam;
-    out.H = r[2];
-    out.M = r[1] / c.s2tot;
-    out.t = (int32_t)r[3];
-    if (J_out) {
-        J_out[0] = r[0];
-        J_out[1] = r[1];
-        J_out[2] = r[2];
-        J_out[3] = r[3];
+    for (int32_t m = 0; m < nlam; m++) {
+        out[m].lam = lams[m];
+        out[m].H = r[4 * m + 2];
+        out[m].M = r[4 * m + 1] / c.s2tot;
+        out[m].t = (int32_t)r[4 * m + 3];
     }
-    c.solves++;
+    if (J_out) std::memcpy(J_out, r, sizeof(double) * 4);
+    c.solves += nlam;
     return ECASQ_OK;
 }
 
-// Slope search for the budget b.  A: infeasible point (starts at lambda = 0),
-// B: feasible point (starts at {v_0, v_{p-1}} for b >= 1, else the solve at
-// lambda = 2^40).  Query the slope of the chord AB; stop when the answer is A
-// or B again.  Returns B.
-ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_iters, Point& B,
-                    ecasq_status& status) {
-    status = ECASQ_OK;
-    Point A;
-    ECASQ_TRY(dp_solve(c, 0.0, exact_s, A, nullptr, nullptr, nullptr, 0));
-    if (A.H <= b) {
-        B = A;
-        return ECASQ_OK;
-    }
-    if (b >= 1.0) {
-        // closed form of the two-value codebook {v_0, v_{p-1}}
-        int32_t two[2] = {0, (int32_t)(c.p - 1)};
-        int32_t* ch = c.at<int32_t>(c.L.chain);
-        double* res = c.at<double>(c.L.res) + 8;
-        HIP_TRY(hipMemcpyAsync(ch, two, sizeof two, hipMemcpyHostToDevice, c.st));
-        HIP_TRY(launch_metrics(c.H, 2, ch, 0.0, c.s2tot, res, c.st));
-        double m[6];
-        HIP_TRY(hipMemcpyAsync(m, res, sizeof m, hipMemcpyDeviceToHost, c.st));
-        HIP_TRY(hipStreamSynchronize(c.st));
-        B.lam = HUGE_VAL;
-        B.H = m[3];
-        B.M = (0.0 + m[0]) / c.s2tot;
-        B.t = 2;
-    } else {
-        ECASQ_TRY(dp_solve(c, 0x1p40, exact_s, B, nullptr, nullptr, nullptr, 0));
-        if (B.H > b) {
-            status = ECASQ_EINFEASIBLE;
-            return ECASQ_OK;
+ecasq_status dp_solve1(Ctx& c, double lam, int32_t exact_s, Point& out) {
+    return dp_solve(c, &lam, 1, exact_s, &out, nullptr, nullptr, nullptr, 0);
+}
+
+// Result of the budget search: B (the codebook to recover), the multiplier of
+// the refinement step and the number of passes.
+struct SearchResult {
+    Point B;
+    double lam_final;
+    int32_t passes;
+    ecasq_status status;
+};
+
+// The budget search on lambda in passes of kMaxLambdas multipliers (the
+// schedule is stated in include/ecasq.h).  A point's lambda is that of its
+// first query; among points of equal lambda the first one wins.
+ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32_t width,
+                    SearchResult& R) {
+    static const double kGrid[kMaxLambdas] = {0.0, 1e-4, 1e-3, 1e-2, 1e-1, 1.0, 10.0, 100.0};
+    static const double kMul[kMaxLambdas - 1] = {0.25, 0.5, 0.75, 1.5, 2.0, 3.0, 4.0};
+    if (width != 1 && width != kMaxLambdas) return ECASQ_EINVAL;
+    std::vector<Point> pts;
+    Point q[kMaxLambdas];
+    ECASQ_TRY(dp_solve(c, kGrid, width, exact_s, q, nullptr, nullptr, nullptr, 0));
+    pts.insert(pts.end(), q, q + width);
+    int32_t npass = 1;
+    R.status = ECASQ_OK;
+    R.lam_final = 0.0;
+    Point A, B;
+    Point two;
+    bool have_two = false;
+    for (;;) {
+        int ia = -1, ib = -1;
+        for (int x = 0; x < (int)pts.size(); x++) {
+            if (pts[x].H > b) {
+                if (ia < 0 || pts[x].lam > pts[ia].lam) ia = x;
+            } else {
+                if (ib < 0 || pts[x].lam < pts[ib].lam) ib = x;
+            }
+        }
+        if (ia < 0) {  // lambda = 0 is feasible
+            B = pts[ib];
+            R.lam_final = B.lam;
+            break;
+        }
+        A = pts[ia];
+        bool closed = false;
+        if (ib >= 0) {
+            B = pts[ib];
+        } else if (b >= 1.0) {
+            if (!have_two) {
+                // closed form of the two-value codebook {v_0, v_{p-1}}
+                int32_t ends[2] = {0, (int32_t)(c.p - 1)};
+                int32_t* ch = c.at<int32_t>(c.L.chain);
+                double* mres = c.at<double>(c.L.mres);
+                HIP_TRY(hipMemcpyAsync(ch, ends, sizeof ends, hipMemcpyHostToDevice, c.st));
+                HIP_TRY(launch_metrics(c.H, 2, ch, 0.0, c.s2tot, mres, c.st));
+                double m[6];
+                HIP_TRY(hipMemcpyAsync(m, mres, sizeof m, hipMemcpyDeviceToHost, c.st));
+                HIP_TRY(hipStreamSynchronize(c.st));
+                two.lam = HUGE_VAL;
+                two.H = m[3];
+                two.M = (0.0 + m[0]) / c.s2tot;
+                two.t = 2;
+                have_two = true;
+            }
+            B = two;
+            closed = true;
+        } else {
+            // no feasible point yet: try the largest multiplier once
+            bool tried = false;
+            for (const Point& x : pts)
+                if (x.lam == 0x1p40) tried = true;
+            if (tried || npass >= max_passes) {
+                // infeasible budget: the lowest-entropy point found
+                int ih = 0;
+                for (int x = 1; x < (int)pts.size(); x++)
+                    if (pts[x].H < pts[ih].H) ih = x;
+                B = pts[ih];
+                R.status = ECASQ_EINFEASIBLE;
+                R.lam_final = B.lam;
+                break;
+            }
+            Point big;
+            ECASQ_TRY(dp_solve1(c, 0x1p40, exact_s, big));
+            pts.push_back(big);
+            npass++;
+            continue;
+        }
+        const double lc = (B.M - A.M) / (A.H - B.H);
+        R.lam_final = closed ? lc : B.lam;
+        if (!(lc > 0.0) || npass >= max_passes) break;
+        double ql[kMaxLambdas];
+        ql[0] = lc;
+        for (int g = 1; g < width; g++)
+            ql[g] = closed ? lc * kMul[g - 1] : A.lam + ((B.lam - A.lam) * (double)g) / 8.0;
+        const size_t first = pts.size();
+        ECASQ_TRY(dp_solve(c, ql, width, exact_s, q, nullptr, nullptr, nullptr, 0));
+        pts.insert(pts.end(), q, q + width);
+        npass++;
+        const Point& C = pts[first];
+        if ((C.H == A.H && C.M == A.M) || (C.H == B.H && C.M == B.M)) {
+            R.lam_final = lc;
+            break;
         }
     }
-    for (int32_t it = 0; it < max_iters; it++) {
-        const double lc = (B.M - A.M) / (A.H - B.H);
-        if (!(lc > 0.0)) break;
-        Point C;
-        ECASQ_TRY(dp_solve(c, lc, exact_s, C, nullptr, nullptr, nullptr, 0));
-        if ((C.H == A.H && C.M == A.M) || (C.H == B.H && C.M == B.M)) break;
-        if (C.H > b) A = C;
-        else B = C;
-    }
+    R.B = B;
+    R.passes = npass;
     return ECASQ_OK;
 }
 
@@ -291,8 +382,12 @@ ecasq_status hirschberg(Ctx& c, double lamp, int64_t lo, int64_t hi, int32_t n, 
     // forward half: r+1 values starting at lo
     {
         const int64_t jl = lo + 1, jh = hi - (n - 2);
-        HIP_TRY(launch_dp_init_fwd(c.H, lo, jl, jh, lamp, Fw[0], nullptr, nullptr, nullptr,
-                                   nullptr, 0, c.st));
+        DpInit I;
+        std::memset(&I, 0, sizeof I);
+        I.nlam = 1;
+        I.lam[0] = lamp;
+        I.F[0] = Fw[0];
+        HIP_TRY(launch_dp_init_fwd(c.H, lo, jl, jh, I, c.st));
         c.cells += jh - jl + 1;
     }
     int fc = 0;
@@ -300,15 +395,17 @@ ecasq_status hirschberg(Ctx& c, double lamp, int64_t lo, int64_t hi, int32_t n, 
         DpLayer L;
         std::memset(&L, 0, sizeof L);
         L.H = c.H;
-        L.Fin = Fw[fc];
-        L.Fout = Fw[1 - fc];
+        L.nlam = 1;
+        L.Fin[0] = Fw[fc];
+        L.Fout[0] = Fw[1 - fc];
         L.pval = c.at<double>(c.L.pval);
         L.pidx = c.at<int32_t>(c.L.pidx);
+        L.pstride = c.L.pstride;
         L.kb = lo + q - 2;
         L.jlo = lo + q - 1;
         L.jhi = hi - (n - q);
         L.backward = false;
-        L.lam = lamp;
+        L.lam[0] = lamp;
         for (int64_t j = L.jlo; j <= L.jhi; j++) L.cells += j - L.kb;
         HIP_TRY(launch_dp_layer(L, c.st));
         c.cells += L.cells;
@@ -325,15 +422,17 @@ ecasq_status hirschberg(Ctx& c, double lamp, int64_t lo, int64_t hi, int32_t n, 
         DpLayer L;
         std::memset(&L, 0, sizeof L);
         L.H = c.H;
-        L.Fin = Bw[bc];
-        L.Fout = Bw[1 - bc];
+        L.nlam = 1;
+        L.Fin[0] = Bw[bc];
+        L.Fout[0] = Bw[1 - bc];
         L.pval = c.at<double>(c.L.pval);
         L.pidx = c.at<int32_t>(c.L.pidx);
+        L.pstride = c.L.pstride;
         L.kb = hi - q + 2;
         L.jlo = lo + n - q;
         L.jhi = hi - q + 1;
         L.backward = true;
-        L.lam = lamp;
+        L.lam[0] = lamp;
         for (int64_t j = L.jlo; j <= L.jhi; j++) L.cells += L.kb - j;
         HIP_TRY(launch_dp_layer(L, c.st));
         c.cells += L.cells;
@@ -363,7 +462,7 @@ ecasq_status recover(Ctx& c, int32_t t, double lam, int32_t exact_s, int32_t mod
     if (mode == 1) {
         int32_t* K = c.at<int32_t>(c.L.kstar);
         Point P;
-        ECASQ_TRY(dp_solve(c, lam, exact_s, P, nullptr, nullptr, K, c.p));
+        ECASQ_TRY(dp_solve(c, &lam, 1, exact_s, &P, nullptr, nullptr, K, c.p));
         c.solves--;  // a repeat of a search solve, not a new query
         if (P.t != t) return ECASQ_EHIP;
         chain[t - 1] = (int32_t)(c.p - 1);
@@ -382,7 +481,7 @@ ecasq_status recover(Ctx& c, int32_t t, double lam, int32_t exact_s, int32_t mod
 
 ecasq_status finish(Ctx& c, std::vector<int32_t>& chain, double lam, double b, bool budget,
                     const ecasq_options& o, double* codebook, int32_t* rank, ecasq_info* info,
-                    ecasq_status status) {
+                    ecasq_status status, int32_t passes) {
     const int32_t t = (int32_t)chain.size();
     int32_t* ch = c.at<int32_t>(c.L.chain);
     int32_t* stats = ch + c.s + 2;
@@ -391,7 +490,7 @@ ecasq_status finish(Ctx& c, std::vector<int32_t>& chain, double lam, double b, b
     if (o.refine_rounds > 0 && std::isfinite(lam) && t >= 3)
         HIP_TRY(launch_refine(c.H, t, ch, lam * c.s2tot, b, budget ? 1 : 0, o.refine_rounds,
                               o.refine_exhaustive, stats, c.st));
-    double* mres = c.at<double>(c.L.res) + 8;
+    double* mres = c.at<double>(c.L.mres);
     HIP_TRY(launch_metrics(c.H, t, ch, lam, c.s2tot, mres, c.st));
     HIP_TRY(launch_gather(c.H.v, ch, t, codebook, rank, c.st));
     double m[6];
@@ -414,6 +513,7 @@ ecasq_status finish(Ctx& c, std::vector<int32_t>& chain, double lam, double b, b
         info->refine_rounds_run = stt[0];
         info->cells = c.cells;
         info->status = status;
+        info->search_passes = passes;
     }
     return status;
 }
@@ -423,7 +523,8 @@ ecasq_options defaults() {
     o.refine_rounds = 5;
     o.refine_exhaustive = 0;
     o.exact_s = 0;
-    o.max_search_iters = 64;
+    o.max_search_passes = 32;
+    o.search_width = kMaxLambdas;
     o.recovery = 0;
     return o;
 }
@@ -441,15 +542,18 @@ ecasq_status solve_budget(const void* x, int dt, int64_t d, int32_t s, double b,
     std::vector<int32_t> chain;
     ecasq_status status = ECASQ_OK;
     double lam = 0.0;
+    int32_t passes = 0;
     if (c.p <= 2) {
         for (int64_t k = 0; k < c.p; k++) chain.push_back((int32_t)k);
     } else {
-        Point B;
-        ECASQ_TRY(search(c, b, o.exact_s, o.max_search_iters, B, status));
-        lam = B.lam;
-        ECASQ_TRY(recover(c, B.t, B.lam, o.exact_s, o.recovery, chain));
+        SearchResult R;
+        ECASQ_TRY(search(c, b, o.exact_s, o.max_search_passes, o.search_width, R));
+        status = R.status;
+        lam = R.lam_final;
+        passes = R.passes;
+        ECASQ_TRY(recover(c, R.B.t, R.B.lam, o.exact_s, o.recovery, chain));
     }
-    ecasq_status st = finish(c, chain, lam, b, true, o, codebook, rank, info, status);
+    ecasq_status st = finish(c, chain, lam, b, true, o, codebook, rank, info, status, passes);
     if (c.p == 2 && info && info->entropy_surrogate > b) {
         info->status = ECASQ_EINFEASIBLE;
         st = ECASQ_EINFEASIBLE;
@@ -491,7 +595,8 @@ ecasq_status ecasq_solve_ex(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
     if (s < 2 || s > 255 || !codebook) return ECASQ_EINVAL;
     if (!(bits_per_entry >= 0.0)) return ECASQ_EINVAL;  // also rejects NaN
     const ecasq_options o = opts ? *opts : defaults();
-    if (o.refine_rounds < 0 || o.max_search_iters < 0 || o.recovery < 0 || o.recovery > 1)
+    if (o.refine_rounds < 0 || o.max_search_passes < 1 || o.recovery < 0 || o.recovery > 1 ||
+        (o.search_width != 1 && o.search_width != kMaxLambdas))
         return ECASQ_EINVAL;
     return solve_budget(x, dt, d, s, bits_per_entry, o, stream, codebook, codebook_rank, info,
                         workspace, workspace_bytes);
@@ -524,10 +629,11 @@ ecasq_status ecasq_solve_lagrangian(const void* x, ecasq_dtype dt, int64_t d, in
         chain.assign(1, 0);
     } else {
         Point P;
-        ECASQ_TRY(dp_solve(c, lambda, o.exact_s, P, nullptr, nullptr, nullptr, 0));
+        ECASQ_TRY(dp_solve1(c, lambda, o.exact_s, P));
         ECASQ_TRY(recover(c, P.t, lambda, o.exact_s, o.recovery, chain));
     }
-    return finish(c, chain, lambda, HUGE_VAL, false, o, codebook, codebook_rank, info, ECASQ_OK);
+    return finish(c, chain, lambda, HUGE_VAL, false, o, codebook, codebook_rank, info, ECASQ_OK,
+                  0);
 }
 
 ecasq_status ecasq_quantize(const void* x, ecasq_dtype dt, int64_t d, const double* codebook,
@@ -584,7 +690,7 @@ ecasq_status ecasq_dp_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
     if (c.p < 2) return ECASQ_EINVAL;
     Point P;
     double J[4];
-    ECASQ_TRY(dp_solve(c, lambda, 0, P, J, F, kstar, d));
+    ECASQ_TRY(dp_solve(c, &lambda, 1, 0, &P, J, F, kstar, d));
     out5[0] = J[0];
     out5[1] = J[1];
     out5[2] = J[2];
@@ -595,9 +701,9 @@ ecasq_status ecasq_dp_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
 
 void ecasq_timing_enable(int32_t on) { timing_enable(on != 0); }
 
-void ecasq_timing_read(double* layer_ms, int64_t* layer_launches, int64_t* layer_cells,
-                       int32_t reset) {
-    timing_read(layer_ms, layer_launches, layer_cells, reset != 0);
+void ecasq_timing_read(int32_t variant, double* layer_ms, int64_t* layer_launches,
+                       int64_t* layer_cells, int32_t reset) {
+    timing_read(variant, layer_ms, layer_launches, layer_cells, reset != 0);
 }
 
 ecasq_status ecasq_solve_batched(const void* x, ecasq_dtype dt, int64_t n, int64_t d, int32_t s,
@@ -607,10 +713,10 @@ ecasq_status ecasq_solve_batched(const void* x, ecasq_dtype dt, int64_t n, int64
         return ECASQ_EINVAL;
     if (dt < 0 || dt > 2 || !(bits_per_entry >= 0.0)) return ECASQ_EINVAL;
     const ecasq_options o = opts ? *opts : defaults();
-    if (o.refine_rounds < 0 || o.max_search_iters < 0) return ECASQ_EINVAL;
+    if (o.refine_rounds < 0 || o.max_search_passes < 1) return ECASQ_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
     HIP_TRY(launch_batched(x, dt, n, (int32_t)d, s, bits_per_entry, o.refine_rounds,
-                           o.refine_exhaustive, o.exact_s, o.max_search_iters, codebooks, t_out,
+                           o.refine_exhaustive, o.exact_s, o.max_search_passes, codebooks, t_out,
                            infos_dev, st));
     HIP_TRY(hipStreamSynchronize(st));
     return ECASQ_OK;

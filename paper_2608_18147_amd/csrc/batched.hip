@@ -73,7 +73,7 @@ struct BatchArgs {
     int64_t n;
     int32_t d, dpad, s, rows_per_block;
     double b;
-    int32_t refine_rounds, refine_exhaustive, exact_s, max_iters;
+    int32_t refine_rounds, refine_exhaustive, exact_s, max_passes;
     double* codebooks;
     int32_t* t_out;
     ecasq_info* infos;
@@ -399,8 +399,8 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
     const double b = A.b;
 
     int status = ECASQ_OK;
-    double lamB = 0.0;
-    int t = 1;
+    double lamF = 0.0;  // multiplier of the refinement step and of the objective
+    int t = 1, passes = 0;
     if (nonfinite) {
         status = ECASQ_ENONFINITE;
         t = 0;
@@ -411,43 +411,70 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
             if (p == 2) R.chain[1] = 1;
         }
     } else {
-        // slope search (same decisions as the single-vector path)
-        Pt Ap = row_solve<CMAX>(R, 0.0, A.exact_s, 0);
-        Pt Bp;
-        bool done = false;
-        if (Ap.H <= b) {
-            Bp = Ap;
-            done = true;
-        } else if (b >= 1.0) {
-            double C, P;
-            cell_at(row_hist(R), 0, p - 1, tab, C, P);
-            Bp.lam = __builtin_huge_val();
-            Bp.H = 0.0 - P;
-            Bp.M = (0.0 + C) / R.s2tot;
-            Bp.t = 2;
-            Bp.buf = -1;
-        } else {
-            Bp = row_solve<CMAX>(R, 0x1p40, A.exact_s, 1);
-            if (Bp.H > b) {
-                status = ECASQ_EINFEASIBLE;
-                done = true;
+        // the budget search with one multiplier per pass (the schedule of the
+        // single-vector path at width 1): A = infeasible point of largest
+        // lambda, B = feasible point of smallest lambda, Lo = lowest H(I,B);
+        // first occurrence wins every tie
+        Pt Ap, Bf, Lo, Bp;
+        bool haveA = false, haveB = false, tried40 = false;
+        auto add = [&](const Pt& q) {
+            if (q.H > b) {
+                if (!haveA || q.lam > Ap.lam) Ap = q;
+                haveA = true;
+            } else {
+                if (!haveB || q.lam < Bf.lam) Bf = q;
+                haveB = true;
             }
-        }
-        if (!done) {
-            for (int it = 0; it < A.max_iters; it++) {
-                const double lc = (Bp.M - Ap.M) / (Ap.H - Bp.H);
-                if (!(lc > 0.0)) break;
-                const int free_buf = Bp.buf == 0 ? 1 : 0;
-                Pt Cp = row_solve<CMAX>(R, lc, A.exact_s, free_buf);
-                if ((Cp.H == Ap.H && Cp.M == Ap.M) || (Cp.H == Bp.H && Cp.M == Bp.M)) break;
-                if (Cp.H > b) Ap = Cp;
-                else Bp = Cp;
+            if (q.H < Lo.H) Lo = q;
+        };
+        Lo = row_solve<CMAX>(R, 0.0, A.exact_s, 0);
+        add(Lo);
+        int npass = 1;
+        for (;;) {
+            if (!haveA) {  // lambda = 0 is feasible
+                Bp = Bf;
+                lamF = Bp.lam;
+                break;
             }
+            bool closed = false;
+            if (haveB) {
+                Bp = Bf;
+            } else if (b >= 1.0) {
+                double C, P;
+                cell_at(row_hist(R), 0, p - 1, tab, C, P);
+                Bp.lam = __builtin_huge_val();
+                Bp.H = 0.0 - P;
+                Bp.M = (0.0 + C) / R.s2tot;
+                Bp.t = 2;
+                Bp.buf = -1;
+                closed = true;
+            } else {
+                if (tried40 || npass >= A.max_passes) {
+                    Bp = Lo;  // both solves so far still hold their argmins
+                    status = ECASQ_EINFEASIBLE;
+                    lamF = Bp.lam;
+                    break;
+                }
+                add(row_solve<CMAX>(R, 0x1p40, A.exact_s, 1));
+                tried40 = true;
+                npass++;
+                continue;
+            }
+            const double lc = (Bp.M - Ap.M) / (Ap.H - Bp.H);
+            lamF = closed ? lc : Bp.lam;
+            if (!(lc > 0.0) || npass >= A.max_passes) break;
+            const Pt Cp = row_solve<CMAX>(R, lc, A.exact_s, Bp.buf == 0 ? 1 : 0);
+            npass++;
+            if ((Cp.H == Ap.H && Cp.M == Ap.M) || (Cp.H == Bp.H && Cp.M == Bp.M)) {
+                lamF = lc;
+                break;
+            }
+            add(Cp);
         }
-        lamB = Bp.lam;
+        passes = npass;
         t = Bp.t;
         if (lane == 0) {
-            if (t == 2 || Bp.buf < 0) {
+            if (t == 2 || Bp.buf < 0 || !__builtin_isfinite(Bp.lam)) {
                 R.chain[0] = 0;
                 R.chain[1] = p - 1;
             } else {
@@ -461,8 +488,8 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
     }
     int rounds_run = 0;
     if (status != ECASQ_ENONFINITE && A.refine_rounds > 0 && t >= 3 &&
-        __builtin_isfinite(lamB))
-        rounds_run = row_refine(R, t, lamB * R.s2tot, b, 1, A.refine_rounds,
+        __builtin_isfinite(lamF))
+        rounds_run = row_refine(R, t, lamF * R.s2tot, b, 1, A.refine_rounds,
                                 A.refine_exhaustive);
     if (lane == 0) {
         double mse = 0.0, hs = 0.0, ho = 0.0, vn = 0.0;
@@ -484,19 +511,19 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
             ecasq_info inf;
             inf.t = t;
             inf.p = nonfinite ? 0 : p;
-            inf.lambda = lamB;
+            inf.lambda = lamF;
             inf.mse = mse;
             inf.vnmse = vn;
             inf.entropy = ho;
             inf.entropy_surrogate = hs;
-            const double lr = __builtin_isfinite(lamB) ? lamB : 0.0;
+            const double lr = __builtin_isfinite(lamF) ? lamF : 0.0;
             inf.objective = __builtin_fma(lr, ho, vn);
             inf.rate_total = ho + (32.0 * (double)t) / R.dd;
             inf.dp_solves = R.solves;
             inf.refine_rounds_run = rounds_run;
             inf.cells = R.cells;
             inf.status = status;
-            inf.reserved = 0;
+            inf.search_passes = passes;
             A.infos[row] = inf;
         }
     }
@@ -525,7 +552,7 @@ hipError_t launch_dt(const BatchArgs& A, int cmax, unsigned grid, unsigned threa
 
 hipError_t launch_batched(const void* x, int dt, int64_t n, int32_t d, int32_t s, double b,
                           int32_t refine_rounds, int32_t refine_exhaustive, int32_t exact_s,
-                          int32_t max_iters, double* codebooks, int32_t* t_out, void* infos,
+                          int32_t max_passes, double* codebooks, int32_t* t_out, void* infos,
                           hipStream_t st) {
     int dpad = kWave;
     while (dpad < d) dpad <<= 1;
@@ -546,7 +573,7 @@ hipError_t launch_batched(const void* x, int dt, int64_t n, int32_t d, int32_t s
     A.refine_rounds = refine_rounds;
     A.refine_exhaustive = refine_exhaustive;
     A.exact_s = exact_s;
-    A.max_iters = max_iters;
+    A.max_passes = max_passes;
     A.codebooks = codebooks;
     A.t_out = t_out;
     A.infos = static_cast<ecasq_info*>(infos);

@@ -17,6 +17,7 @@
 // workgroup, which balances the triangular work and fills all 256 CUs, and a
 // second kernel reduces the per-chunk (value, index) partials in increasing k
 // order (lowest k wins ties).  The 256-entry log2 table also lives in LDS.
+#include <cstring>
 #include <vector>
 
 #include "device.hpp"
@@ -28,6 +29,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kTK = 256;
+constexpr int kMaxLam = kMaxLambdas;
 constexpr int kMaxSplit = 32;
 
 struct LayerArgs {
@@ -35,16 +37,17 @@ struct LayerArgs {
     const double* N;
     const double* S;
     const double* S2;
-    const double* Fin;  // previous layer, indexed by absolute k
-    double* pval;
+    const double* Fin[kMaxLam];  // previous layer per multiplier, indexed by absolute k
+    double* pval;                // partials, kMaxLam slices of pstride entries
     int32_t* pidx;
+    int64_t pstride;
     int64_t kb;   // forward: first predecessor; backward: last predecessor (khi)
     int64_t jlo;  // first column
     int64_t jhi;  // last column (inclusive)
     int64_t nblk;   // column blocks
     int32_t nsplit; // chunks per column block (equal split of its predecessor range)
     double dd;
-    double lam;  // lambda' (MSE units)
+    double lam[kMaxLam];  // lambda' (MSE units) per multiplier
 };
 
 // Predecessor range of block b: forward [kb, jend-1]; backward [j0+1, khi].
@@ -74,43 +77,67 @@ __device__ __forceinline__ void block_krange(const LayerArgs& a, int64_t CB, int
     }
 }
 
-// One cell update of column state (cv, cN, cS, cS2 / best, bk) against the
-// predecessor (pv, pN, pS, pS2, pF); `ok` masks cells outside the triangle.
-template <bool BWD, bool MASKED>
-__device__ __forceinline__ void cell_update(double cv, double cN, double cS, double cS2, double pv,
-                                            double pN, double pS, double pS2, double pF,
-                                            int32_t k, bool ok, double dd, double lam,
-                                            const double2* __restrict__ tab, double& best,
-                                            int32_t& bk) {
-    double C, P;
-    if (BWD)
-        cell_terms(cv, cN, cS, cS2, pv, pN, pS, pS2, dd, false, 0.0, tab, C, P);
-    else
-        cell_terms(pv, pN, pS, pS2, cv, cN, cS, cS2, dd, false, 0.0, tab, C, P);
-    const double cand = __builtin_fma(-lam, P, pF + C);
+// Candidate update of one (column, multiplier) state; `ok` masks cells outside
+// the triangle.  Strict '<' keeps the lowest k; the unmasked form uses min(),
+// which differs from the select only in the sign of an exact zero.
+template <bool MASKED>
+__device__ __forceinline__ void take(double cand, int32_t k, bool ok, double& best, int32_t& bk) {
     if (MASKED) {
         const bool lt = ok && cand < best;
         bk = lt ? k : bk;
         best = lt ? cand : best;
     } else {
-        // strict '<' keeps the lowest k; min() only differs from the select in
-        // the sign of an exact zero
         bk = cand < best ? k : bk;
         best = __builtin_fmin(best, cand);
     }
 }
 
-// R columns per lane; SMEM: predecessors read through the scalar cache
-// (wave-uniform k) instead of being staged through LDS.
-template <int R, bool BWD, bool SMEM>
+// All cells of one LDS tile of nk predecessors against the lane's R columns.
+template <int R, bool BWD, int ML, bool MASKED>
+__device__ __forceinline__ void tile_pass(const double* sv, const double* sN, const double* sS,
+                                          const double* sS2, const double (*sF)[ML], int64_t t0,
+                                          int nk, const int64_t (&col)[R], const double (&cv)[R],
+                                          const double (&cN)[R], const double (&cS)[R],
+                                          const double (&cS2)[R], double dd,
+                                          const double (&lam)[ML], const double2* tab,
+                                          double (&best)[R][ML], int32_t (&bk)[R][ML]) {
+    for (int kk = 0; kk < nk; kk++) {
+        const int64_t k = t0 + kk;
+        const double pv = sv[kk], pN = sN[kk], pS = sS[kk], pS2 = sS2[kk];
+        double pF[ML];
+#pragma unroll
+        for (int m = 0; m < ML; m++) pF[m] = sF[kk][m];
+#pragma unroll
+        for (int r = 0; r < R; r++) {
+            double C, P;
+            if (BWD)
+                cell_terms(cv[r], cN[r], cS[r], cS2[r], pv, pN, pS, pS2, dd, false, 0.0, tab, C,
+                           P);
+            else
+                cell_terms(pv, pN, pS, pS2, cv[r], cN[r], cS[r], cS2[r], dd, false, 0.0, tab, C,
+                           P);
+            const bool ok = !MASKED || (BWD ? (k > col[r]) : (k < col[r]));
+#pragma unroll
+            for (int m = 0; m < ML; m++)
+                take<MASKED>(__builtin_fma(-lam[m], P, pF[m] + C), (int32_t)k, ok, best[r][m],
+                             bk[r][m]);
+        }
+    }
+}
+
+// R columns per lane, ML multipliers per launch (C and Phi of a cell are
+// shared by all multipliers); SMEM: predecessors read through the scalar
+// cache instead of being staged through LDS (single multiplier only).
+template <int R, bool BWD, bool SMEM, int ML>
 __global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a, const double* __restrict__ gv,
                                                      const double* __restrict__ gN,
                                                      const double* __restrict__ gS,
-                                                     const double* __restrict__ gS2,
-                                                     const double* __restrict__ gF) {
+                                                     const double* __restrict__ gS2) {
+    static_assert(!SMEM || ML == 1, "scalar-cache path is single-multiplier");
     __shared__ double2 tab[kLog2Size];
     __shared__ double sv[SMEM ? 1 : kTK], sN[SMEM ? 1 : kTK], sS[SMEM ? 1 : kTK],
-        sS2[SMEM ? 1 : kTK], sF[SMEM ? 1 : kTK];
+        sS2[SMEM ? 1 : kTK];
+    __shared__ double sF[SMEM ? 1 : kTK][ML];
     constexpr int64_t CB = (int64_t)kBlock * R;
     const int tid = threadIdx.x;
     // heaviest column blocks first: high b for forward layers, low b backward
@@ -123,8 +150,8 @@ __global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a, const double* 
     load_log2_table(tab);
 
     int64_t col[R];
-    double cv[R], cN[R], cS[R], cS2[R], best[R];
-    int32_t bk[R];
+    double cv[R], cN[R], cS[R], cS2[R], best[R][ML];
+    int32_t bk[R][ML];
 #pragma unroll
     for (int r = 0; r < R; r++) {
         col[r] = j0 + r * kBlock + tid;
@@ -133,11 +160,18 @@ __global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a, const double* 
         cN[r] = gN[jj];
         cS[r] = gS[jj];
         cS2[r] = gS2[jj];
-        best[r] = __builtin_huge_val();
-        bk[r] = -1;
+#pragma unroll
+        for (int m = 0; m < ML; m++) {
+            best[r][m] = __builtin_huge_val();
+            bk[r][m] = -1;
+        }
     }
-    const double lam = a.lam, dd = a.dd;
+    double lam[ML];
+#pragma unroll
+    for (int m = 0; m < ML; m++) lam[m] = a.lam[m];
+    const double dd = a.dd;
     if (SMEM) {
+        const double* __restrict__ gF = a.Fin[0];
         __syncthreads();  // table visible
         // unmasked part: every k below (forward) or above (backward) all columns
         const int64_t us = BWD ? (jend + 1 > cs ? jend + 1 : cs) : cs;
@@ -145,9 +179,17 @@ __global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a, const double* 
         for (int64_t k = us; k <= ue; k++) {
             const double pv = gv[k], pN = gN[k], pS = gS[k], pS2 = gS2[k], pF = gF[k];
 #pragma unroll
-            for (int r = 0; r < R; r++)
-                cell_update<BWD, false>(cv[r], cN[r], cS[r], cS2[r], pv, pN, pS, pS2, pF,
-                                        (int32_t)k, true, dd, lam, tab, best[r], bk[r]);
+            for (int r = 0; r < R; r++) {
+                double C, P;
+                if (BWD)
+                    cell_terms(cv[r], cN[r], cS[r], cS2[r], pv, pN, pS, pS2, dd, false, 0.0, tab,
+                               C, P);
+                else
+                    cell_terms(pv, pN, pS, pS2, cv[r], cN[r], cS[r], cS2[r], dd, false, 0.0, tab,
+                               C, P);
+                take<false>(__builtin_fma(-lam[0], P, pF + C), (int32_t)k, true, best[r][0],
+                            bk[r][0]);
+            }
         }
         // masked part (the diagonal region)
         const int64_t ms = BWD ? cs : (j0 > cs ? j0 : cs);
@@ -155,10 +197,17 @@ __global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a, const double* 
         for (int64_t k = ms; k <= me; k++) {
             const double pv = gv[k], pN = gN[k], pS = gS[k], pS2 = gS2[k], pF = gF[k];
 #pragma unroll
-            for (int r = 0; r < R; r++)
-                cell_update<BWD, true>(cv[r], cN[r], cS[r], cS2[r], pv, pN, pS, pS2, pF,
-                                       (int32_t)k, BWD ? (k > col[r]) : (k < col[r]), dd, lam, tab,
-                                       best[r], bk[r]);
+            for (int r = 0; r < R; r++) {
+                double C, P;
+                if (BWD)
+                    cell_terms(cv[r], cN[r], cS[r], cS2[r], pv, pN, pS, pS2, dd, false, 0.0, tab,
+                               C, P);
+                else
+                    cell_terms(pv, pN, pS, pS2, cv[r], cN[r], cS[r], cS2[r], dd, false, 0.0, tab,
+                               C, P);
+                take<true>(__builtin_fma(-lam[0], P, pF + C), (int32_t)k,
+                           BWD ? (k > col[r]) : (k < col[r]), best[r][0], bk[r][0]);
+            }
         }
     } else {
         for (int64_t t0 = cs; t0 <= ce; t0 += kTK) {
@@ -170,37 +219,28 @@ __global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a, const double* 
                 sN[tid] = gN[k];
                 sS[tid] = gS[k];
                 sS2[tid] = gS2[k];
-                sF[tid] = gF[k];
+#pragma unroll
+                for (int m = 0; m < ML; m++) sF[tid][m] = a.Fin[m][k];
             }
             __syncthreads();
             const bool nomask = BWD ? (t0 > jend) : (t0 + nk - 1 < j0);
-            if (nomask) {
-                for (int kk = 0; kk < nk; kk++) {
-#pragma unroll
-                    for (int r = 0; r < R; r++)
-                        cell_update<BWD, false>(cv[r], cN[r], cS[r], cS2[r], sv[kk], sN[kk],
-                                                sS[kk], sS2[kk], sF[kk], (int32_t)(t0 + kk), true,
-                                                dd, lam, tab, best[r], bk[r]);
-                }
-            } else {
-                for (int kk = 0; kk < nk; kk++) {
-                    const int64_t k = t0 + kk;
-#pragma unroll
-                    for (int r = 0; r < R; r++)
-                        cell_update<BWD, true>(cv[r], cN[r], cS[r], cS2[r], sv[kk], sN[kk],
-                                               sS[kk], sS2[kk], sF[kk], (int32_t)k,
-                                               BWD ? (k > col[r]) : (k < col[r]), dd, lam, tab,
-                                               best[r], bk[r]);
-                }
-            }
+            if (nomask)
+                tile_pass<R, BWD, ML, false>(sv, sN, sS, sS2, sF, t0, nk, col, cv, cN, cS, cS2,
+                                             dd, lam, tab, best, bk);
+            else
+                tile_pass<R, BWD, ML, true>(sv, sN, sS, sS2, sF, t0, nk, col, cv, cN, cS, cS2,
+                                            dd, lam, tab, best, bk);
         }
     }
 #pragma unroll
     for (int r = 0; r < R; r++) {
         if (col[r] <= jend) {
             const int64_t idx = (b * a.nsplit + c) * CB + r * kBlock + tid;
-            a.pval[idx] = best[r];
-            a.pidx[idx] = bk[r];
+#pragma unroll
+            for (int m = 0; m < ML; m++) {
+                a.pval[m * a.pstride + idx] = best[r][m];
+                a.pidx[m * a.pstride + idx] = bk[r][m];
+            }
         }
     }
 }
@@ -208,67 +248,72 @@ __global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a, const double* 
 struct ReduceArgs {
     LayerArgs L;
     int64_t CB;
-    double* Fout;
+    double* Fout[kMaxLam];
     // forward main-DP extras (null in the recovery half-DPs)
-    const double* Min;
-    const double* Pin;
-    double* Mout;
-    double* Pout;
-    int32_t* kstar;
-    double* last;  // [3][s+1]: F, MSE, H(I,B) of column p-1 per layer
+    const double* Min[kMaxLam];
+    const double* Pin[kMaxLam];
+    double* Mout[kMaxLam];
+    double* Pout[kMaxLam];
+    int32_t* kstar;   // single multiplier only
+    double* last;     // per multiplier [3][s+1]: F, MSE, H(I,B) of column p-1 per layer
     int32_t layer;
     int32_t last_stride;
     int64_t p;
     double c0d;
 };
 
+// Per (column, multiplier): lexicographic min of the chunk partials in
+// increasing k order, then the MSE / H(I,B) accumulators along the argmin.
 template <bool BWD>
 __global__ __launch_bounds__(256) void k_dp_reduce(ReduceArgs a) {
     __shared__ double2 tab[kLog2Size];
     load_log2_table(tab);
     __syncthreads();
+    const int m = blockIdx.y;
     const int64_t j = a.L.jlo + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (j > a.L.jhi) return;
     const int64_t b = (j - a.L.jlo) / a.CB;
     const int64_t off = (j - a.L.jlo) - b * a.CB;
     int64_t j0, jend, klo, khi;
     block_krange<BWD>(a.L, a.CB, b, j0, jend, klo, khi);
+    const double* pval = a.L.pval + m * a.L.pstride;
+    const int32_t* pidx = a.L.pidx + m * a.L.pstride;
     double best = __builtin_huge_val();
     int32_t bk = -1;
     for (int64_t c = 0; c < a.L.nsplit; c++) {
         int64_t cs, ce;
         if (!chunk_range(klo, khi, a.L.nsplit, c, cs, ce)) break;
         const int64_t idx = (b * a.L.nsplit + c) * a.CB + off;
-        const double val = a.L.pval[idx];
+        const double val = pval[idx];
         if (val < best) {
             best = val;
-            bk = a.L.pidx[idx];
+            bk = pidx[idx];
         }
     }
-    a.Fout[j] = best;
-    if (a.Mout && bk >= 0) {
+    a.Fout[m][j] = best;
+    if (a.Mout[m] && bk >= 0) {
         double C, P;
         cell_terms(a.L.v[bk], a.L.N[bk], a.L.S[bk], a.L.S2[bk], a.L.v[j], a.L.N[j], a.L.S[j],
                    a.L.S2[j], a.L.dd, bk == 0, a.c0d, tab, C, P);
-        const double m = a.Min[bk] + C;
-        const double ph = a.Pin[bk] - P;
-        a.Mout[j] = m;
-        a.Pout[j] = ph;
+        const double mv = a.Min[m][bk] + C;
+        const double ph = a.Pin[m][bk] - P;
+        a.Mout[m][j] = mv;
+        a.Pout[m][j] = ph;
         if (a.kstar) a.kstar[j] = bk;
         if (j == a.p - 1) {
-            a.last[a.layer] = best;
-            a.last[a.last_stride + a.layer] = m;
-            a.last[2 * a.last_stride + a.layer] = ph;
+            double* last = a.last + (int64_t)m * 3 * a.last_stride;
+            last[a.layer] = best;
+            last[a.last_stride + a.layer] = mv;
+            last[2 * a.last_stride + a.layer] = ph;
         }
     }
 }
 
 // Forward layer 2 from `lo`: F[j] = C[lo,j] + lambda' Phi'[lo,j] (Phi^first
-// when lo == 0), eq. apx_base.  With M non-null also starts the accumulators.
+// when lo == 0), eq. apx_base, for every multiplier of I.  With M non-null
+// also starts the accumulators.
 __global__ __launch_bounds__(256) void k_dp_init_fwd(Hist H, int64_t lo, int64_t jl, int64_t jh,
-                                                     double lam, double* F, double* M, double* Ph,
-                                                     int32_t* kstar, double* last,
-                                                     int32_t last_stride) {
+                                                     DpInit I) {
     __shared__ double2 tab[kLog2Size];
     load_log2_table(tab);
     __syncthreads();
@@ -276,18 +321,21 @@ __global__ __launch_bounds__(256) void k_dp_init_fwd(Hist H, int64_t lo, int64_t
     if (j > jh) return;
     double C, P;
     cell_at(H, lo, j, tab, C, P);
-    const double f = __builtin_fma(-lam, P, 0.0 + C);
-    F[j] = f;
-    if (M) {
-        const double m = 0.0 + C;
-        const double ph = 0.0 - P;
-        M[j] = m;
-        Ph[j] = ph;
-        if (kstar) kstar[j] = (int32_t)lo;
-        if (j == H.p - 1) {
-            last[2] = f;
-            last[last_stride + 2] = m;
-            last[2 * last_stride + 2] = ph;
+    if (I.kstar) I.kstar[j] = (int32_t)lo;
+    for (int m = 0; m < I.nlam; m++) {
+        const double f = __builtin_fma(-I.lam[m], P, 0.0 + C);
+        I.F[m][j] = f;
+        if (I.M[m]) {
+            const double mv = 0.0 + C;
+            const double ph = 0.0 - P;
+            I.M[m][j] = mv;
+            I.Ph[m][j] = ph;
+            if (j == H.p - 1) {
+                double* last = I.last + (int64_t)m * 3 * I.last_stride;
+                last[2] = f;
+                last[I.last_stride + 2] = mv;
+                last[2 * I.last_stride + 2] = ph;
+            }
         }
     }
 }
@@ -307,9 +355,12 @@ __global__ __launch_bounds__(256) void k_dp_init_bwd(Hist H, int64_t hi, int64_t
 
 // eq. apx_final: lowest i in [2, imax] minimising F_i[p-1] (or i = imax when
 // exactly min(s, p) values are required).  out: J, MSE, H(I,B), i*.
-__global__ void k_dp_final(const double* last, int32_t stride, int32_t imax, int32_t exact_s,
-                           double* out) {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+__global__ void k_dp_final(const double* last_all, int32_t stride, int32_t imax, int32_t exact_s,
+                           double* out_all, int32_t nlam) {
+    const int m = threadIdx.x;
+    if (m >= nlam || blockIdx.x != 0) return;
+    const double* last = last_all + (int64_t)m * 3 * stride;
+    double* out = out_all + 4 * m;
     int32_t bi = 2;
     double bj = last[2];
     for (int32_t i = 3; i <= imax; i++) {
@@ -361,10 +412,11 @@ __global__ __launch_bounds__(256) void k_split(const double* Fw, const double* B
 // predecessors per chunk, and a multiple of 8 when possible so that the
 // round-robin placement of consecutive workgroups on the 8 XCDs gives every
 // XCD an equal share of every column block.
-int32_t choose_splits(int64_t lenmax) {
+int32_t choose_splits(int64_t lenmax, int64_t cap) {
     int64_t sp = lenmax / 1024;
-    if (sp >= 8) sp = sp / 8 * 8;
     if (sp > kMaxSplit) sp = kMaxSplit;
+    if (sp > cap) sp = cap;
+    if (sp >= 8) sp = sp / 8 * 8;
     return sp < 1 ? 1 : (int32_t)sp;
 }
 
@@ -376,12 +428,16 @@ namespace {
 struct TimedLaunch {
     hipEvent_t a, b;
     int64_t cells;
+    int variant;
+};
+struct TimingTotals {
+    double ms = 0.0;
+    int64_t launches = 0, cells = 0;
 };
 bool g_timing = false;
 std::vector<TimedLaunch> g_pending;
 std::vector<hipEvent_t> g_pool;
-double g_ms = 0.0;
-int64_t g_launches = 0, g_cells = 0;
+TimingTotals g_tot[2];
 
 hipEvent_t take_event() {
     if (!g_pool.empty()) {
@@ -401,9 +457,9 @@ void timing_flush() {
     for (auto& t : g_pending) {
         float ms = 0.f;
         if (hipEventSynchronize(t.b) == hipSuccess && hipEventElapsedTime(&ms, t.a, t.b) == hipSuccess) {
-            g_ms += ms;
-            g_launches++;
-            g_cells += t.cells;
+            g_tot[t.variant].ms += ms;
+            g_tot[t.variant].launches++;
+            g_tot[t.variant].cells += t.cells;
         }
         g_pool.push_back(t.a);
         g_pool.push_back(t.b);
@@ -411,83 +467,98 @@ void timing_flush() {
     g_pending.clear();
 }
 
-void timing_read(double* ms, int64_t* launches, int64_t* cells, bool reset) {
+void timing_read(int variant, double* ms, int64_t* launches, int64_t* cells, bool reset) {
     timing_flush();
-    if (ms) *ms = g_ms;
-    if (launches) *launches = g_launches;
-    if (cells) *cells = g_cells;
-    if (reset) {
-        g_ms = 0.0;
-        g_launches = 0;
-        g_cells = 0;
+    if (variant < 0 || variant > 1) {
+        if (ms) *ms = 0.0;
+        if (launches) *launches = 0;
+        if (cells) *cells = 0;
+        return;
     }
+    const TimingTotals& t = g_tot[variant];
+    if (ms) *ms = t.ms;
+    if (launches) *launches = t.launches;
+    if (cells) *cells = t.cells;
+    if (reset) g_tot[variant] = TimingTotals();
 }
 
 int64_t dp_partial_entries(int64_t p) {
-    // nblk * nsplit * CB with nsplit <= kMaxSplit and nblk * CB <= p + CB
-    const int64_t CB = kBlock * kColsPerLane;
-    return (p + CB) * kMaxSplit;
+    // nblk * nsplit * CB <= (p + CB) * nsplit; at most 2^26 entries per
+    // multiplier once p is large (then nblk alone fills the chip)
+    const int64_t CB = kBlock * (kColsPerLane > kColsPerLaneMulti ? kColsPerLane
+                                                                   : kColsPerLaneMulti);
+    int64_t cap = ((int64_t)1 << 26) / (p + CB);
+    cap = cap < 1 ? 1 : (cap > kMaxSplit ? kMaxSplit : cap);
+    return (p + CB) * cap;
 }
 
 #ifndef ECASQ_PRED_SMEM
 #define ECASQ_PRED_SMEM 0
 #endif
 
-hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st) {
-    constexpr int R = kColsPerLane;
-    constexpr bool SM = ECASQ_PRED_SMEM != 0;
+namespace {
+
+template <int R, int ML, bool SM>
+hipError_t layer_launch(const DpLayer& L, hipStream_t st) {
     const int64_t CB = (int64_t)kBlock * R;
     const int64_t ncol = L.jhi - L.jlo + 1;
-    if (ncol <= 0) return hipSuccess;
     const int64_t nblk = (ncol + CB - 1) / CB;
     // longest predecessor range: last block (forward) or first block (backward)
     const int64_t lenmax = L.backward ? (L.kb - L.jlo) : (L.jhi - L.kb);
-    const int32_t nsplit = choose_splits(lenmax);
+    if (nblk * CB > L.pstride) return hipErrorInvalidValue;
+    const int32_t nsplit = choose_splits(lenmax, L.pstride / (nblk * CB));
     LayerArgs a;
+    std::memset(&a, 0, sizeof a);
     a.v = L.H.v;
     a.N = L.H.N;
     a.S = L.H.S;
     a.S2 = L.H.S2;
-    a.Fin = L.Fin;
     a.pval = L.pval;
     a.pidx = L.pidx;
+    a.pstride = L.pstride;
     a.kb = L.kb;
     a.jlo = L.jlo;
     a.jhi = L.jhi;
     a.nblk = nblk;
     a.nsplit = nsplit;
     a.dd = L.H.dd;
-    a.lam = L.lam;
+    for (int m = 0; m < ML; m++) {
+        a.Fin[m] = L.Fin[m];
+        a.lam[m] = L.lam[m];
+    }
     dim3 grid((unsigned)nsplit, (unsigned)nblk);
-    TimedLaunch tl{nullptr, nullptr, L.cells};
+    TimedLaunch tl{nullptr, nullptr, L.cells, ML == 1 ? 0 : 1};
     if (g_timing) {
         tl.a = take_event();
         tl.b = take_event();
         if (tl.a && tl.b) (void)hipEventRecord(tl.a, st);
     }
     if (L.backward)
-        k_dp_layer<R, true, SM><<<grid, kBlock, 0, st>>>(a, a.v, a.N, a.S, a.S2, a.Fin);
+        k_dp_layer<R, true, SM, ML><<<grid, kBlock, 0, st>>>(a, a.v, a.N, a.S, a.S2);
     else
-        k_dp_layer<R, false, SM><<<grid, kBlock, 0, st>>>(a, a.v, a.N, a.S, a.S2, a.Fin);
+        k_dp_layer<R, false, SM, ML><<<grid, kBlock, 0, st>>>(a, a.v, a.N, a.S, a.S2);
     if (g_timing && tl.a && tl.b) {
         (void)hipEventRecord(tl.b, st);
         g_pending.push_back(tl);
     }
     ReduceArgs ra;
+    std::memset(&ra, 0, sizeof ra);
     ra.L = a;
     ra.CB = CB;
-    ra.Fout = L.Fout;
-    ra.Min = L.Min;
-    ra.Pin = L.Pin;
-    ra.Mout = L.Mout;
-    ra.Pout = L.Pout;
+    for (int m = 0; m < ML; m++) {
+        ra.Fout[m] = L.Fout[m];
+        ra.Min[m] = L.Min[m];
+        ra.Pin[m] = L.Pin[m];
+        ra.Mout[m] = L.Mout[m];
+        ra.Pout[m] = L.Pout[m];
+    }
     ra.kstar = L.kstar;
     ra.last = L.last;
     ra.layer = L.layer;
     ra.last_stride = L.last_stride;
     ra.p = L.H.p;
     ra.c0d = L.H.c0d;
-    const unsigned rg = (unsigned)((ncol + 255) / 256);
+    dim3 rg((unsigned)((ncol + 255) / 256), (unsigned)ML);
     if (L.backward)
         k_dp_reduce<true><<<rg, 256, 0, st>>>(ra);
     else
@@ -495,12 +566,23 @@ hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st) {
     return hipGetLastError();
 }
 
-hipError_t launch_dp_init_fwd(const Hist& H, int64_t lo, int64_t jl, int64_t jh, double lam,
-                              double* F, double* M, double* Ph, int32_t* kstar, double* last,
-                              int32_t last_stride, hipStream_t st) {
+}  // namespace
+
+hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st) {
+    if (L.jhi < L.jlo) return hipSuccess;
+    if (L.nlam == 1)
+        return layer_launch<kColsPerLane, 1, ECASQ_PRED_SMEM != 0>(L, st);
+    if (L.nlam == kMaxLambdas && !L.kstar)
+        return layer_launch<kColsPerLaneMulti, kMaxLambdas, false>(L, st);
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_dp_init_fwd(const Hist& H, int64_t lo, int64_t jl, int64_t jh,
+                              const DpInit& I, hipStream_t st) {
     if (jh < jl) return hipSuccess;
+    if (I.nlam < 1 || I.nlam > kMaxLambdas) return hipErrorInvalidValue;
     const unsigned g = (unsigned)((jh - jl + 1 + 255) / 256);
-    k_dp_init_fwd<<<g, 256, 0, st>>>(H, lo, jl, jh, lam, F, M, Ph, kstar, last, last_stride);
+    k_dp_init_fwd<<<g, 256, 0, st>>>(H, lo, jl, jh, I);
     return hipGetLastError();
 }
 
@@ -513,8 +595,9 @@ hipError_t launch_dp_init_bwd(const Hist& H, int64_t hi, int64_t jl, int64_t jh,
 }
 
 hipError_t launch_dp_final(const double* last, int32_t stride, int32_t imax, int32_t exact_s,
-                           double* out, hipStream_t st) {
-    k_dp_final<<<1, 64, 0, st>>>(last, stride, imax, exact_s, out);
+                           int32_t nlam, double* out, hipStream_t st) {
+    if (nlam < 1 || nlam > kMaxLambdas) return hipErrorInvalidValue;
+    k_dp_final<<<1, 64, 0, st>>>(last, stride, imax, exact_s, out, nlam);
     return hipGetLastError();
 }
 

@@ -10,11 +10,19 @@ namespace ecasq {
 
 inline size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
-// columns per lane in the DP layer kernel
+// columns per lane in the DP layer kernel (single multiplier / one pass of
+// kMaxLambdas multipliers)
 #ifndef ECASQ_COLS_PER_LANE
 #define ECASQ_COLS_PER_LANE 2
 #endif
+#ifndef ECASQ_COLS_PER_LANE_MULTI
+#define ECASQ_COLS_PER_LANE_MULTI 1
+#endif
 constexpr int kColsPerLane = ECASQ_COLS_PER_LANE;
+constexpr int kColsPerLaneMulti = ECASQ_COLS_PER_LANE_MULTI;
+
+// multipliers solved together by one sweep of the DP (one search pass)
+constexpr int kMaxLambdas = 8;
 
 // ---- prep.hip ----
 size_t prep_scratch_bytes(int64_t d);
@@ -22,40 +30,56 @@ hipError_t launch_prep(const void* x, int dt, int64_t d, void* scratch, hipStrea
                        double* N, double* S, double* S2, int64_t* p_dev, uint32_t* flags_dev);
 
 // ---- dp.hip ----
+// One DP layer for nlam multipliers (1 or kMaxLambdas); every per-multiplier
+// array below holds nlam valid entries.
 struct DpLayer {
     Hist H;
-    const double* Fin;
-    double* Fout;
-    double* pval;
+    int32_t nlam;
+    const double* Fin[kMaxLambdas];
+    double* Fout[kMaxLambdas];
+    double* pval;     // nlam slices of pstride entries
     int32_t* pidx;
+    int64_t pstride;  // >= dp_partial_entries(p)
     int64_t kb;    // forward: first predecessor; backward: last predecessor
     int64_t jlo;   // first column
     int64_t jhi;   // last column (inclusive)
     bool backward;
-    double lam;    // lambda' in MSE units
+    double lam[kMaxLambdas];  // lambda' in MSE units
     // forward main-DP accumulators (all null in the recovery half-DPs)
-    const double* Min;
-    const double* Pin;
-    double* Mout;
-    double* Pout;
-    int32_t* kstar;
-    double* last;
+    const double* Min[kMaxLambdas];
+    const double* Pin[kMaxLambdas];
+    double* Mout[kMaxLambdas];
+    double* Pout[kMaxLambdas];
+    int32_t* kstar;          // nlam == 1 only
+    double* last;            // nlam blocks of 3 * last_stride doubles
     int32_t layer;
     int32_t last_stride;
-    int64_t cells;  // cells this launch evaluates (for timing)
+    int64_t cells;  // (column, predecessor) cells this launch evaluates, per multiplier
+};
+
+// Layer 2 of the forward DP for nlam multipliers.
+struct DpInit {
+    int32_t nlam;
+    double lam[kMaxLambdas];
+    double* F[kMaxLambdas];
+    double* M[kMaxLambdas];   // null: no accumulators
+    double* Ph[kMaxLambdas];
+    int32_t* kstar;
+    double* last;
+    int32_t last_stride;
 };
 int64_t dp_partial_entries(int64_t p);
 void timing_enable(bool on);
 void timing_flush();
-void timing_read(double* ms, int64_t* launches, int64_t* cells, bool reset);
+void timing_read(int variant, double* ms, int64_t* launches, int64_t* cells, bool reset);
 hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st);
-hipError_t launch_dp_init_fwd(const Hist& H, int64_t lo, int64_t jl, int64_t jh, double lam,
-                              double* F, double* M, double* Ph, int32_t* kstar, double* last,
-                              int32_t last_stride, hipStream_t st);
+hipError_t launch_dp_init_fwd(const Hist& H, int64_t lo, int64_t jl, int64_t jh,
+                              const DpInit& I, hipStream_t st);
 hipError_t launch_dp_init_bwd(const Hist& H, int64_t hi, int64_t jl, int64_t jh, double lam,
                               double* B, hipStream_t st);
+// out: 4 doubles (J, MSE, H(I,B), i*) per multiplier
 hipError_t launch_dp_final(const double* last, int32_t stride, int32_t imax, int32_t exact_s,
-                           double* out, hipStream_t st);
+                           int32_t nlam, double* out, hipStream_t st);
 hipError_t launch_split(const double* Fw, const double* Bw, int64_t ml, int64_t mh,
                         int64_t* m_out, hipStream_t st);
 
@@ -76,7 +100,7 @@ hipError_t launch_entropy(const unsigned long long* hist, int32_t t, int64_t d, 
 // ---- batched.hip ----
 hipError_t launch_batched(const void* x, int dt, int64_t n, int32_t d, int32_t s, double b,
                           int32_t refine_rounds, int32_t refine_exhaustive, int32_t exact_s,
-                          int32_t max_iters, double* codebooks, int32_t* t_out, void* infos,
+                          int32_t max_passes, double* codebooks, int32_t* t_out, void* infos,
                           hipStream_t st);
 
 }  // namespace ecasq

@@ -29,8 +29,9 @@ class ecasq_options(ctypes.Structure):
         ("refine_rounds", ctypes.c_int32),
         ("refine_exhaustive", ctypes.c_int32),
         ("exact_s", ctypes.c_int32),
-        ("max_search_iters", ctypes.c_int32),
+        ("max_search_passes", ctypes.c_int32),
         ("recovery", ctypes.c_int32),
+        ("search_width", ctypes.c_int32),
     ]
 
 
@@ -49,11 +50,11 @@ class ecasq_info(ctypes.Structure):
         ("refine_rounds_run", ctypes.c_int32),
         ("cells", ctypes.c_int64),
         ("status", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("search_passes", ctypes.c_int32),
     ]
 
     def as_dict(self):
-        d = {k: getattr(self, k) for k, _ in self._fields_ if k != "reserved"}
+        d = {k: getattr(self, k) for k, _ in self._fields_}
         d["lambda"] = d.pop("lambda_")
         return d
 
@@ -101,7 +102,7 @@ def lib():
     L.ecasq_dp_trace.argtypes = [vp, i32, i64, i32, dbl, vp, vp, vp, vp]
     L.ecasq_timing_enable.argtypes = [i32]
     L.ecasq_timing_enable.restype = None
-    L.ecasq_timing_read.argtypes = [P(dbl), P(i64), P(i64), i32]
+    L.ecasq_timing_read.argtypes = [i32, P(dbl), P(i64), P(i64), i32]
     L.ecasq_timing_read.restype = None
     for name in ("ecasq_solve", "ecasq_solve_ex", "ecasq_solve_lagrangian", "ecasq_quantize",
                  "ecasq_solve_batched", "ecasq_histogram", "ecasq_dp_trace"):
@@ -259,10 +260,17 @@ def ecasq_timing_enable(on=True):
     lib().ecasq_timing_enable(1 if on else 0)
 
 
-def ecasq_timing_read(reset=False):
-    """(milliseconds, launches, cells) of the timed DP layer kernel launches."""
+TIMING_SINGLE = 0  # one multiplier per DP layer launch
+TIMING_PASS = 1    # the 8 multipliers of a search pass per launch
+
+
+def ecasq_timing_read(variant=TIMING_PASS, reset=False):
+    """(milliseconds, launches, cells) of the timed DP layer kernel launches of
+    one variant; cells are (column, predecessor) pairs, each evaluated for
+    every multiplier of its launch."""
     ms = ctypes.c_double(0)
     n = ctypes.c_int64(0)
     c = ctypes.c_int64(0)
-    lib().ecasq_timing_read(ctypes.byref(ms), ctypes.byref(n), ctypes.byref(c), 1 if reset else 0)
+    lib().ecasq_timing_read(int(variant), ctypes.byref(ms), ctypes.byref(n), ctypes.byref(c),
+                            1 if reset else 0)
     return ms.value, n.value, c.value

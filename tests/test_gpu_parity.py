@@ -145,6 +145,7 @@ def _compare(res_gpu, res_orc):
     assert info["refine_rounds_run"] == res_orc.refine_rounds
     assert info["cells"] == res_orc.cells
     assert info["status"] == res_orc.status
+    assert info["search_passes"] == res_orc.passes
 
 
 SOLVE_CASES = [
@@ -170,6 +171,18 @@ def test_solve_parity(case):
     o = pipeline.solve(x, s, b, refine_rounds=R, exhaustive=bool(exh))
     _compare(g, o)
     assert g[2]["entropy"] <= b + 1e-12 or g[2]["status"] != 0
+
+
+@pytest.mark.parametrize("name,d,s,b", [("lognormal_3k_b2", 3000, 24, 2.0),
+                                         ("lognormal_3k_b0.6", 3000, 12, 0.6)])
+def test_solve_parity_width1(name, d, s, b):
+    """The sequential chord search (one multiplier per pass)."""
+    x = inputs.lognormal_signed(d, 5)
+    _say("solve width 1", name)
+    opts = ecasq.ecasq_default_options(search_width=1)
+    g = ecasq.ecasq_solve(_dev(x), s, b, options=opts)
+    o = pipeline.solve(x, s, b, width=1)
+    _compare(g, o)
 
 
 @pytest.mark.parametrize("lam,R,exh", [(0.05, 0, 0), (0.5, 5, 0), (0.02, 5, 1), (0.0, 2, 0)])
@@ -284,6 +297,7 @@ def _compare_row(cb, t, info, o, s):
     for k in ("mse", "vnmse", "entropy", "entropy_surrogate", "objective", "rate_total"):
         assert _close(info[k], getattr(o, k)), (k, info[k], getattr(o, k))
     assert info["dp_solves"] == o.dp_solves and info["cells"] == o.cells
+    assert info["search_passes"] == o.passes
     assert info["refine_rounds_run"] == o.refine_rounds
     assert info["lambda"] == o.lam or (math.isinf(info["lambda"]) and math.isinf(o.lam))
 
@@ -298,7 +312,7 @@ def test_batched_rows_parity(R, exh):
     infos = ecasq.infos_to_dicts(infos)
     for r in range(rows.shape[0]):
         o = pipeline.solve(rows[r].astype(np.float32), 16, 3.0, refine_rounds=R,
-                           exhaustive=bool(exh), recovery="backpointers")
+                           exhaustive=bool(exh), recovery="backpointers", width=1)
         _compare_row(cbs[r], int(tt[r]), infos[r], o, 16)
 
 
@@ -319,7 +333,7 @@ def test_batched_shapes_and_edge_rows():
         cbs, tt = cbs.cpu().numpy(), tt.cpu().numpy()
         infos = ecasq.infos_to_dicts(infos)
         for r in range(xb.shape[0]):
-            o = pipeline.solve(xb[r], s, b, recovery="backpointers")
+            o = pipeline.solve(xb[r], s, b, recovery="backpointers", width=1)
             _compare_row(cbs[r], int(tt[r]), infos[r], o, s)
 
 
@@ -331,7 +345,7 @@ def test_batched_nonfinite_row_is_flagged():
     infos = ecasq.infos_to_dicts(infos)
     assert infos[1]["status"] == ecasq.ECASQ_ENONFINITE and int(tt[1]) == 0
     for r in (0, 2):
-        o = pipeline.solve(x[r], 8, 2.0, recovery="backpointers")
+        o = pipeline.solve(x[r], 8, 2.0, recovery="backpointers", width=1)
         _compare_row(cbs[r].cpu().numpy(), int(tt[r]), infos[r], o, 8)
 
 
@@ -351,5 +365,5 @@ def test_batched_full_kv_workload_sampled():
         assert np.all(np.diff(cbs[r, :t]) > 0)
         assert infos[r]["status"] == 0 and infos[r]["entropy"] <= 3.0 + 1e-12
     for r in np.random.default_rng(0).choice(rows.shape[0], 64, replace=False):
-        o = pipeline.solve(r32[r], 16, 3.0, recovery="backpointers")
+        o = pipeline.solve(r32[r], 16, 3.0, recovery="backpointers", width=1)
         _compare_row(cbs[r], int(tt[r]), infos[r], o, 16)

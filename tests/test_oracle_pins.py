@@ -347,10 +347,18 @@ def test_search_matches_dense_lambda_grid():
         r = pipeline.dp_forward(H, s, lam * H.s2tot)
         pts.append((r["phi"], r["mse"] / H.s2tot))
     for b in (1.3, 1.8, 2.2, 2.9):
-        sr = pipeline.search(H, s, b)
-        assert sr["H"] <= b
         best = min(m for hh, m in pts if hh <= b)
-        assert sr["M"] <= best * (1 + 1e-12)
+        found = []
+        for width in (1, 8):
+            sr = pipeline.search(H, s, b, width=width)
+            assert sr["status"] == 0 and sr["H"] <= b
+            assert sr["M"] <= best * (1 + 1e-12)
+            # A and B adjacent on the lower hull: the final slope lies between
+            # the multipliers A and B were found at
+            assert sr["lam_final"] <= sr["lam"] or sr["lam"] == 0.0
+            found.append((sr["H"], sr["M"], sr["t"]))
+        # both schedules end at the same supported point
+        assert found[0] == found[1]
 
 
 def test_hirschberg_matches_backpointers_at_scale():
