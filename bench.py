@@ -39,8 +39,13 @@ def flops_per_cell(nlam):
     return FLOPS_SHARED + FLOPS_PER_LAMBDA * nlam
 
 
-TRAFFIC_BYTES_PER_LAUNCH = 283.0e6
-TRAFFIC_SOURCES_SHA = "89c9cd8d83e47782"
+# HBM bytes per launch of the pass kernel (k_dp_layer, 8 multipliers) from
+# rocprofv3 FETCH_SIZE / WRITE_SIZE runs of this bench on weights_256k
+# (profiles/k_dp_layer_pass8_weights_256k.md), scaled by a plain copy's
+# readings (FETCH x2.0, WRITE x1.0).  Valid only for the kernel sources they
+# were taken on: reported as null once those sources change.
+TRAFFIC_BYTES_PER_LAUNCH = 2.494e9
+TRAFFIC_SOURCES_SHA = "f3a631b21f5b78fb"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 
 
@@ -122,7 +127,20 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=32768)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-batched", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run one plain device copy of 2^28 bytes (the reference kernel\n"
+                         "that scales rocprofv3 FETCH_SIZE / WRITE_SIZE readings) and exit")
     args = ap.parse_args()
+
+    if args.copy_calibration:
+        import torch
+        n = 1 << 28
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        torch.cuda.synchronize()
+        dst = src.clone()
+        torch.cuda.synchronize()
+        log(f"copied {dst.numel()} bytes")
+        return
 
     if args.gpus != 1:
         print("bench.py measures one GPU only: the single-vector path runs on one GPU and "

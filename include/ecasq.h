@@ -174,17 +174,22 @@ const char *ecasq_status_string(ecasq_status st);
  * sums S = sum c v and S2 = sum c v^2 (App. D prefix quantities).  All outputs
  * are device arrays of length >= d; *p_out (host) receives p.
  *
- * ecasq_dp_trace: one forward DP solve of dp_APX at lambda (vNMSE units) on
- * the histogram of x, recording for every layer i in [2, min(s,p)] the values
- * F_i[j] (device, (s+1) x d fp64, row i; entries outside the layer's valid
- * columns are left untouched) and argmins k*_i[j] (device, (s+1) x d int32).
- * out5 (host): J (MSE units), MSE, H(I,B) of the minimising path, i*, cells.
+ * ecasq_dp_trace: forward DP solves of dp_APX (eq. apx_base, apx_rec,
+ * apx_final) on the histogram of x at nlam multipliers lambdas[] (host array,
+ * vNMSE units, nlam = 1 or 8; with 8 they run as one search pass does).  For
+ * multiplier m and every layer i in [2, min(s,p)] it records, in row
+ * (m * (s+1) + i) of device arrays of nlam * (s+1) rows of d entries: F_i[j]
+ * (F, fp64), the argmin k*_i[j] (kstar, int32), and the MSE and H(I,B)
+ * accumulated along the argmins (M and Ph, fp64; each may be NULL).  Entries
+ * outside a layer's valid columns are left untouched.  out (host, 5 * nlam):
+ * per multiplier J (MSE units), MSE, H(I,B) of the minimising path, i*, cells.
  */
 ecasq_status ecasq_histogram(const void *x, ecasq_dtype dt, int64_t d, void *stream, double *v,
                              double *N, double *S, double *S2, int64_t *p_out);
 
-ecasq_status ecasq_dp_trace(const void *x, ecasq_dtype dt, int64_t d, int32_t s, double lambda,
-                            void *stream, double *F, int32_t *kstar, double *out5);
+ecasq_status ecasq_dp_trace(const void *x, ecasq_dtype dt, int64_t d, int32_t s, int32_t nlam,
+                            const double *lambdas, void *stream, double *F, int32_t *kstar,
+                            double *M, double *Ph, double *out);
 
 /*
  * Kernel timing for measurement tools.  While enabled (process-wide), every

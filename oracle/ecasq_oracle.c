@@ -260,6 +260,51 @@ int orc_dp_forward(const double *v, const double *N, const double *S, const doub
     return 0;
 }
 
+/* Sampled columns of one layer: for each j in cols (j >= layer - 1), eq. apx_base
+ * (layer 2: the interval (v_0, v_j] with the first-interval entropy term) or
+ * eq. apx_rec (layer >= 3: min over layer-2 <= k < j of
+ * Fprev[k] + C[k,j] + lambda' Phi[k,j], lowest k on ties), and the MSE and
+ * H(I,B) accumulators carried from the argmin.  Fprev, Mprev, Pprev: the full
+ * previous layer (unused for layer 2).  Lets a caller check any column of any
+ * layer from the layer before it without running the whole DP.              */
+void orc_dp_columns(const double *v, const double *N, const double *S, const double *S2,
+                    int64_t p, int64_t d, int32_t layer, double lamp, const double *Fprev,
+                    const double *Mprev, const double *Pprev, int64_t ncols, const int64_t *cols,
+                    double *F, int32_t *K, double *M, double *Ph)
+{
+    hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t x = 0; x < ncols; x++) {
+        int64_t j = cols[x];
+        double C, P;
+        if (layer == 2) {
+            cell_terms(&H, 0, j, &C, &P);
+            F[x] = fma(-lamp, P, 0.0 + C);
+            K[x] = 0;
+            M[x] = 0.0 + C;
+            Ph[x] = 0.0 - P;
+            continue;
+        }
+        double best = INFINITY;
+        int64_t bk = -1;
+        for (int64_t k = layer - 2; k < j; k++) {
+            cell_terms(&H, k, j, &C, &P);
+            double cand = fma(-lamp, P, Fprev[k] + C);
+            if (cand < best) { best = cand; bk = k; }
+        }
+        F[x] = best;
+        K[x] = (int32_t)bk;
+        if (bk >= 0) {
+            cell_terms(&H, bk, j, &C, &P);
+            M[x] = Mprev[bk] + C;
+            Ph[x] = Pprev[bk] - P;
+        } else {
+            M[x] = 0.0;
+            Ph[x] = 0.0;
+        }
+    }
+}
+
 /* Traceback through stored argmins (cross-check for Hirschberg). */
 void orc_traceback(const int32_t *bp, int64_t p, int32_t t, int32_t *chain)
 {

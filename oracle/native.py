@@ -59,6 +59,8 @@ def lib():
     L.orc_refine.argtypes = hist + [i32, ip, d, d, i32, i32, i32, ip]
     L.orc_search.argtypes = hist + [i32, d, i32, i32, i32, dp, i32, dp]
     L.orc_interval.argtypes = hist + [i64, i64, dp]
+    L.orc_dp_columns.argtypes = hist + [i32, d, dp, dp, dp, i64, i64p, dp, ip, dp, dp]
+    L.orc_dp_columns.restype = None
     invc, lc = log2_table.build_table()
     a = np.asarray(invc, dtype=np.float64)
     b = np.asarray(lc, dtype=np.float64)

@@ -117,6 +117,24 @@ def dp_forward(H, s, lamp, exact_s=False, backpointers=False, dump=False):
     return r
 
 
+def dp_columns(H, layer, lamp, Fprev=None, Mprev=None, Pprev=None, cols=()):
+    """Columns `cols` of DP layer `layer` recomputed from the previous layer
+    (eq. apx_base for layer 2, eq. apx_rec otherwise): (F, k*, M, Ph) arrays."""
+    cols = np.ascontiguousarray(cols, dtype=np.int64)
+    n = len(cols)
+    F = np.zeros(n)
+    K = np.zeros(n, dtype=np.int32)
+    M = np.zeros(n)
+    Ph = np.zeros(n)
+    if layer == 2:
+        Fprev = Mprev = Pprev = np.zeros(1)
+    args = [np.ascontiguousarray(a, dtype=np.float64) for a in (Fprev, Mprev, Pprev)]
+    native.lib().orc_dp_columns(*H.args(), layer, lamp, *(native.dptr(a) for a in args), n,
+                                cols.ctypes.data_as(native.ctypes.POINTER(native.ctypes.c_int64)),
+                                native.dptr(F), native.iptr(K), native.dptr(M), native.dptr(Ph))
+    return F, K, M, Ph
+
+
 def hirschberg(H, t, lamp):
     chain = np.zeros(t, dtype=np.int32)
     import ctypes

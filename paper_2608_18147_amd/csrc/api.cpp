@@ -168,14 +168,22 @@ ecasq_status ctx_prep(Ctx& c, const void* x, int dt) {
 
 int64_t tri_cells(int64_t n) { return n * (n + 1) / 2; }
 
-// Full dp_APX solves at nlam multipliers lams[] (vNMSE units), 1 <= nlam <=
-// kMaxLambdas, in one sweep over the layers (nlam must be 1 or kMaxLambdas).
-// With nlam == 1, optional per-layer dumps (row i of Fdump / Kdump, row
-// stride `stride`) and the raw (J, MSE, H(I,B), t) in J_out.
+// Optional per-layer dumps of a solve: for multiplier m and layer i, row
+// (m * (s + 1) + i) of each array, row stride `stride`; any may be null.
+struct Dumps {
+    double* F = nullptr;
+    int32_t* K = nullptr;
+    double* M = nullptr;
+    double* P = nullptr;
+    int64_t stride = 0;
+};
+
+// Full dp_APX solves at nlam multipliers lams[] (vNMSE units) in one sweep
+// over the layers (nlam must be 1 or kMaxLambdas).  J_out (optional): the raw
+// (J, MSE, H(I,B), t) of every multiplier.
 ecasq_status dp_solve(Ctx& c, const double* lams, int32_t nlam, int32_t exact_s, Point* out,
-                      double* J_out, double* Fdump, int32_t* Kdump, int64_t stride) {
+                      double* J_out, const Dumps* dump) {
     if (nlam != 1 && nlam != kMaxLambdas) return ECASQ_EINVAL;
-    if (nlam != 1 && (J_out || Fdump || Kdump)) return ECASQ_EINVAL;
     const int64_t p = c.p;
     const int32_t imax = (int32_t)std::min<int64_t>(c.s, p);
     const int32_t ls = c.s + 1;
@@ -185,6 +193,27 @@ ecasq_status dp_solve(Ctx& c, const double* lams, int32_t nlam, int32_t exact_s,
     double* Ph[2] = {c.at<double>(c.L.P0), c.at<double>(c.L.P1)};
     double* last = c.at<double>(c.L.last);
     double* res = c.at<double>(c.L.res);
+    const int64_t ds = dump ? dump->stride : 0;
+    auto row = [&](auto* base, int32_t m, int32_t i) {
+        return base ? base + ((int64_t)m * ls + i) * ds : nullptr;
+    };
+    // copy columns [j0, p) of layer i (current buffers cur) into the dumps
+    auto save = [&](int32_t i, int cur, int64_t j0) -> ecasq_status {
+        if (!dump) return ECASQ_OK;
+        const size_t nb = sizeof(double) * (size_t)(p - j0);
+        for (int32_t m = 0; m < nlam; m++) {
+            if (dump->F)
+                HIP_TRY(hipMemcpyAsync(row(dump->F, m, i) + j0, F[cur] + m * d + j0, nb,
+                                       hipMemcpyDeviceToDevice, c.st));
+            if (dump->M)
+                HIP_TRY(hipMemcpyAsync(row(dump->M, m, i) + j0, M[cur] + m * d + j0, nb,
+                                       hipMemcpyDeviceToDevice, c.st));
+            if (dump->P)
+                HIP_TRY(hipMemcpyAsync(row(dump->P, m, i) + j0, Ph[cur] + m * d + j0, nb,
+                                       hipMemcpyDeviceToDevice, c.st));
+        }
+        return ECASQ_OK;
+    };
     double lamp[kMaxLambdas];
     for (int32_t m = 0; m < nlam; m++) lamp[m] = lams[m] * c.s2tot;
     DpInit I;
@@ -195,14 +224,12 @@ ecasq_status dp_solve(Ctx& c, const double* lams, int32_t nlam, int32_t exact_s,
         I.F[m] = F[0] + m * d;
         I.M[m] = M[0] + m * d;
         I.Ph[m] = Ph[0] + m * d;
+        I.kstar[m] = dump ? row(dump->K, m, 2) : nullptr;
     }
-    I.kstar = Kdump ? Kdump + 2 * stride : nullptr;
     I.last = last;
     I.last_stride = ls;
     HIP_TRY(launch_dp_init_fwd(c.H, 0, 1, p - 1, I, c.st));
-    if (Fdump)
-        HIP_TRY(hipMemcpyAsync(Fdump + 2 * stride + 1, F[0] + 1, sizeof(double) * (p - 1),
-                               hipMemcpyDeviceToDevice, c.st));
+    ECASQ_TRY(save(2, 0, 1));
     c.cells += (int64_t)nlam * (p - 1);
     int cur = 0;
     for (int32_t i = 3; i <= imax; i++) {
@@ -218,6 +245,7 @@ ecasq_status dp_solve(Ctx& c, const double* lams, int32_t nlam, int32_t exact_s,
             L.Mout[m] = M[1 - cur] + m * d;
             L.Pout[m] = Ph[1 - cur] + m * d;
             L.lam[m] = lamp[m];
+            L.kstar[m] = dump ? row(dump->K, m, i) : nullptr;
         }
         L.pval = c.at<double>(c.L.pval);
         L.pidx = c.at<int32_t>(c.L.pidx);
@@ -226,15 +254,12 @@ ecasq_status dp_solve(Ctx& c, const double* lams, int32_t nlam, int32_t exact_s,
         L.jlo = i - 1;
         L.jhi = p - 1;
         L.backward = false;
-        L.kstar = Kdump ? Kdump + (int64_t)i * stride : nullptr;
         L.last = last;
         L.layer = i;
         L.last_stride = ls;
         L.cells = tri_cells(p - i + 1);
         HIP_TRY(launch_dp_layer(L, c.st));
-        if (Fdump)
-            HIP_TRY(hipMemcpyAsync(Fdump + (int64_t)i * stride + (i - 1), F[1 - cur] + (i - 1),
-                                   sizeof(double) * (p - i + 1), hipMemcpyDeviceToDevice, c.st));
+        ECASQ_TRY(save(i, 1 - cur, i - 1));
         c.cells += (int64_t)nlam * tri_cells(p - i + 1);
         cur = 1 - cur;
     }
@@ -249,13 +274,13 @@ ecasq_status dp_solve(Ctx& c, const double* lams, int32_t nlam, int32_t exact_s,
         out[m].M = r[4 * m + 1] / c.s2tot;
         out[m].t = (int32_t)r[4 * m + 3];
     }
-    if (J_out) std::memcpy(J_out, r, sizeof(double) * 4);
+    if (J_out) std::memcpy(J_out, r, sizeof(double) * 4 * nlam);
     c.solves += nlam;
     return ECASQ_OK;
 }
 
 ecasq_status dp_solve1(Ctx& c, double lam, int32_t exact_s, Point& out) {
-    return dp_solve(c, &lam, 1, exact_s, &out, nullptr, nullptr, nullptr, 0);
+    return dp_solve(c, &lam, 1, exact_s, &out, nullptr, nullptr);
 }
 
 // Result of the budget search: B (the codebook to recover), the multiplier of
@@ -277,7 +302,7 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
     if (width != 1 && width != kMaxLambdas) return ECASQ_EINVAL;
     std::vector<Point> pts;
     Point q[kMaxLambdas];
-    ECASQ_TRY(dp_solve(c, kGrid, width, exact_s, q, nullptr, nullptr, nullptr, 0));
+    ECASQ_TRY(dp_solve(c, kGrid, width, exact_s, q, nullptr, nullptr));
     pts.insert(pts.end(), q, q + width);
     int32_t npass = 1;
     R.status = ECASQ_OK;
@@ -351,7 +376,7 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
         for (int g = 1; g < width; g++)
             ql[g] = closed ? lc * kMul[g - 1] : A.lam + ((B.lam - A.lam) * (double)g) / 8.0;
         const size_t first = pts.size();
-        ECASQ_TRY(dp_solve(c, ql, width, exact_s, q, nullptr, nullptr, nullptr, 0));
+        ECASQ_TRY(dp_solve(c, ql, width, exact_s, q, nullptr, nullptr));
         pts.insert(pts.end(), q, q + width);
         npass++;
         const Point& C = pts[first];
@@ -462,7 +487,10 @@ ecasq_status recover(Ctx& c, int32_t t, double lam, int32_t exact_s, int32_t mod
     if (mode == 1) {
         int32_t* K = c.at<int32_t>(c.L.kstar);
         Point P;
-        ECASQ_TRY(dp_solve(c, &lam, 1, exact_s, &P, nullptr, nullptr, K, c.p));
+        Dumps dk;
+        dk.K = K;
+        dk.stride = c.p;
+        ECASQ_TRY(dp_solve(c, &lam, 1, exact_s, &P, nullptr, &dk));
         c.solves--;  // a repeat of a search solve, not a new query
         if (P.t != t) return ECASQ_EHIP;
         chain[t - 1] = (int32_t)(c.p - 1);
@@ -676,10 +704,14 @@ ecasq_status ecasq_histogram(const void* x, ecasq_dtype dt, int64_t d, void* str
     return ECASQ_OK;
 }
 
-ecasq_status ecasq_dp_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s, double lambda,
-                            void* stream, double* F, int32_t* kstar, double* out5) {
+ecasq_status ecasq_dp_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s, int32_t nlam,
+                            const double* lambdas, void* stream, double* F, int32_t* kstar,
+                            double* M, double* Ph, double* out) {
     ECASQ_TRY(check_x(x, dt, d));
-    if (s < 2 || s > 255 || !F || !kstar || !out5 || !(lambda >= 0.0)) return ECASQ_EINVAL;
+    if (s < 2 || s > 255 || !F || !kstar || !out || !lambdas) return ECASQ_EINVAL;
+    if (nlam != 1 && nlam != kMaxLambdas) return ECASQ_EINVAL;
+    for (int32_t m = 0; m < nlam; m++)
+        if (!(lambdas[m] >= 0.0) || !std::isfinite(lambdas[m])) return ECASQ_EINVAL;
     Ctx c;
     ECASQ_TRY(ctx_open(c, d, s, false, stream, nullptr, 0));
     struct Closer {
@@ -688,14 +720,21 @@ ecasq_status ecasq_dp_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
     } closer{c};
     ECASQ_TRY(ctx_prep(c, x, dt));
     if (c.p < 2) return ECASQ_EINVAL;
-    Point P;
-    double J[4];
-    ECASQ_TRY(dp_solve(c, &lambda, 1, 0, &P, J, F, kstar, d));
-    out5[0] = J[0];
-    out5[1] = J[1];
-    out5[2] = J[2];
-    out5[3] = J[3];
-    out5[4] = (double)c.cells;
+    Point P[kMaxLambdas];
+    double J[4 * kMaxLambdas];
+    Dumps dk;
+    dk.F = F;
+    dk.K = kstar;
+    dk.M = M;
+    dk.P = Ph;
+    dk.stride = d;
+    const int64_t cells0 = c.cells;
+    ECASQ_TRY(dp_solve(c, lambdas, nlam, 0, P, J, &dk));
+    const double per = (double)((c.cells - cells0) / nlam);
+    for (int32_t m = 0; m < nlam; m++) {
+        for (int q = 0; q < 4; q++) out[5 * m + q] = J[4 * m + q];
+        out[5 * m + 4] = per;
+    }
     return ECASQ_OK;
 }
 

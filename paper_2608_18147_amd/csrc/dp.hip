@@ -30,7 +30,10 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kTK = 256;
 constexpr int kMaxLam = kMaxLambdas;
-constexpr int kMaxSplit = 32;
+#ifndef ECASQ_MAX_SPLIT
+#define ECASQ_MAX_SPLIT 32
+#endif
+constexpr int kMaxSplit = ECASQ_MAX_SPLIT;  // chunks per column block, at most
 
 struct LayerArgs {
     const double* v;
@@ -254,7 +257,7 @@ struct ReduceArgs {
     const double* Pin[kMaxLam];
     double* Mout[kMaxLam];
     double* Pout[kMaxLam];
-    int32_t* kstar;   // single multiplier only
+    int32_t* kstar[kMaxLam];  // argmin rows per multiplier (may be null)
     double* last;     // per multiplier [3][s+1]: F, MSE, H(I,B) of column p-1 per layer
     int32_t layer;
     int32_t last_stride;
@@ -299,7 +302,7 @@ __global__ __launch_bounds__(256) void k_dp_reduce(ReduceArgs a) {
         const double ph = a.Pin[m][bk] - P;
         a.Mout[m][j] = mv;
         a.Pout[m][j] = ph;
-        if (a.kstar) a.kstar[j] = bk;
+        if (a.kstar[m]) a.kstar[m][j] = bk;
         if (j == a.p - 1) {
             double* last = a.last + (int64_t)m * 3 * a.last_stride;
             last[a.layer] = best;
@@ -321,8 +324,8 @@ __global__ __launch_bounds__(256) void k_dp_init_fwd(Hist H, int64_t lo, int64_t
     if (j > jh) return;
     double C, P;
     cell_at(H, lo, j, tab, C, P);
-    if (I.kstar) I.kstar[j] = (int32_t)lo;
     for (int m = 0; m < I.nlam; m++) {
+        if (I.kstar[m]) I.kstar[m][j] = (int32_t)lo;
         const double f = __builtin_fma(-I.lam[m], P, 0.0 + C);
         I.F[m][j] = f;
         if (I.M[m]) {
@@ -533,10 +536,14 @@ hipError_t layer_launch(const DpLayer& L, hipStream_t st) {
         tl.b = take_event();
         if (tl.a && tl.b) (void)hipEventRecord(tl.a, st);
     }
-    if (L.backward)
-        k_dp_layer<R, true, SM, ML><<<grid, kBlock, 0, st>>>(a, a.v, a.N, a.S, a.S2);
-    else
+    if constexpr (ML == 1) {
+        if (L.backward)
+            k_dp_layer<R, true, SM, 1><<<grid, kBlock, 0, st>>>(a, a.v, a.N, a.S, a.S2);
+        else
+            k_dp_layer<R, false, SM, 1><<<grid, kBlock, 0, st>>>(a, a.v, a.N, a.S, a.S2);
+    } else {
         k_dp_layer<R, false, SM, ML><<<grid, kBlock, 0, st>>>(a, a.v, a.N, a.S, a.S2);
+    }
     if (g_timing && tl.a && tl.b) {
         (void)hipEventRecord(tl.b, st);
         g_pending.push_back(tl);
@@ -551,8 +558,8 @@ hipError_t layer_launch(const DpLayer& L, hipStream_t st) {
         ra.Pin[m] = L.Pin[m];
         ra.Mout[m] = L.Mout[m];
         ra.Pout[m] = L.Pout[m];
+        ra.kstar[m] = L.kstar[m];
     }
-    ra.kstar = L.kstar;
     ra.last = L.last;
     ra.layer = L.layer;
     ra.last_stride = L.last_stride;
@@ -572,7 +579,7 @@ hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st) {
     if (L.jhi < L.jlo) return hipSuccess;
     if (L.nlam == 1)
         return layer_launch<kColsPerLane, 1, ECASQ_PRED_SMEM != 0>(L, st);
-    if (L.nlam == kMaxLambdas && !L.kstar)
+    if (L.nlam == kMaxLambdas && !L.backward)
         return layer_launch<kColsPerLaneMulti, kMaxLambdas, false>(L, st);
     return hipErrorInvalidValue;
 }

@@ -50,7 +50,7 @@ struct DpLayer {
     const double* Pin[kMaxLambdas];
     double* Mout[kMaxLambdas];
     double* Pout[kMaxLambdas];
-    int32_t* kstar;          // nlam == 1 only
+    int32_t* kstar[kMaxLambdas];  // argmin rows per multiplier (null: not recorded)
     double* last;            // nlam blocks of 3 * last_stride doubles
     int32_t layer;
     int32_t last_stride;
@@ -64,7 +64,7 @@ struct DpInit {
     double* F[kMaxLambdas];
     double* M[kMaxLambdas];   // null: no accumulators
     double* Ph[kMaxLambdas];
-    int32_t* kstar;
+    int32_t* kstar[kMaxLambdas];
     double* last;
     int32_t last_stride;
 };

@@ -99,7 +99,7 @@ def lib():
     L.ecasq_status_string.argtypes = [i32]
     L.ecasq_status_string.restype = ctypes.c_char_p
     L.ecasq_histogram.argtypes = [vp, i32, i64, vp, vp, vp, vp, vp, P(i64)]
-    L.ecasq_dp_trace.argtypes = [vp, i32, i64, i32, dbl, vp, vp, vp, vp]
+    L.ecasq_dp_trace.argtypes = [vp, i32, i64, i32, i32, P(dbl), vp, vp, vp, vp, vp, P(dbl)]
     L.ecasq_timing_enable.argtypes = [i32]
     L.ecasq_timing_enable.restype = None
     L.ecasq_timing_read.argtypes = [i32, P(dbl), P(i64), P(i64), i32]
@@ -242,18 +242,32 @@ def ecasq_histogram(x, stream=None):
     return tuple(b[: p.value] for b in bufs)
 
 
-def ecasq_dp_trace(x, s, lam, stream=None):
-    """All layers of one forward solve: F [(s+1), d] fp64 (NaN where unset),
-    kstar [(s+1), d] int32 (-1 where unset) and (J, MSE, H(I,B), i*, cells)."""
+def ecasq_dp_trace(x, s, lam, stream=None, accumulators=False):
+    """All layers of forward solves at one multiplier (lam a number) or at the
+    8 multipliers of a search pass (lam a sequence of 8).  Returns F
+    [nlam, s+1, d] fp64 (NaN where unset), kstar [nlam, s+1, d] int32 (-1
+    where unset), the accumulators M and Ph like F (None unless asked for),
+    and per multiplier (J, MSE, H(I,B), i*, cells).  With a scalar lam the
+    leading nlam axis is dropped."""
     x = _check_x(x)
     d = x.numel()
-    F = torch.full((int(s) + 1, d), float("nan"), dtype=torch.float64, device=x.device)
-    K = torch.full((int(s) + 1, d), -1, dtype=torch.int32, device=x.device)
-    out = (ctypes.c_double * 5)()
-    st = lib().ecasq_dp_trace(_ptr(x), _DTYPES[x.dtype], d, int(s), float(lam), _stream(stream),
-                              _ptr(F), _ptr(K), out)
+    scalar = not hasattr(lam, "__len__")
+    lams = [float(lam)] if scalar else [float(v) for v in lam]
+    n = len(lams)
+    shape = (n, int(s) + 1, d)
+    F = torch.full(shape, float("nan"), dtype=torch.float64, device=x.device)
+    K = torch.full(shape, -1, dtype=torch.int32, device=x.device)
+    M = torch.full(shape, float("nan"), dtype=torch.float64, device=x.device) if accumulators else None
+    Ph = torch.full(shape, float("nan"), dtype=torch.float64, device=x.device) if accumulators else None
+    la = (ctypes.c_double * n)(*lams)
+    out = (ctypes.c_double * (5 * n))()
+    st = lib().ecasq_dp_trace(_ptr(x), _DTYPES[x.dtype], d, int(s), n, la, _stream(stream),
+                              _ptr(F), _ptr(K), _ptr(M), _ptr(Ph), out)
     _raise(st)
-    return F, K, tuple(out)
+    res = [tuple(out[5 * m:5 * m + 5]) for m in range(n)]
+    if scalar:
+        return F[0], K[0], (M[0] if M is not None else None), (Ph[0] if Ph is not None else None), res[0]
+    return F, K, M, Ph, res
 
 
 def ecasq_timing_enable(on=True):

@@ -361,6 +361,41 @@ def test_search_matches_dense_lambda_grid():
         assert found[0] == found[1]
 
 
+def test_dp_columns_match_full_layers():
+    """The sampled-column recomputation (used to check full-size GPU layers)
+    equals the full forward DP layer by layer, and its accumulators at the last
+    column equal the MSE and H(I,B) the DP reports for its chosen layer."""
+    rng = np.random.default_rng(17)
+    x = rng.standard_normal(400).astype(np.float32)
+    s, lam = 9, 0.03
+    H = pipeline.prepare(x)
+    p = H.p
+    lamp = lam * H.s2tot
+    r = pipeline.dp_forward(H, s, lamp, backpointers=True, dump=True)
+    F2, K2, M, Ph = pipeline.dp_columns(H, 2, lamp, cols=np.arange(1, p))
+    np.testing.assert_array_equal(F2, r["F"][2, 1:p])
+    Mfull = np.zeros(p)
+    Pfull = np.zeros(p)
+    Mfull[1:], Pfull[1:] = M, Ph
+    Ffull = r["F"][2].copy()
+    accs = {2: (Mfull.copy(), Pfull.copy())}
+    for i in range(3, s + 1):
+        cols = np.arange(i - 1, p)
+        F, K, M, Ph = pipeline.dp_columns(H, i, lamp, Ffull, Mfull, Pfull, cols)
+        np.testing.assert_array_equal(F, r["F"][i, i - 1:p])
+        np.testing.assert_array_equal(K, r["bp"][i, i - 1:p])
+        Ffull = r["F"][i].copy()
+        Mfull = np.zeros(p)
+        Pfull = np.zeros(p)
+        Mfull[i - 1:], Pfull[i - 1:] = M, Ph
+        accs[i] = (Mfull.copy(), Pfull.copy())
+    t = r["t"]
+    assert accs[t][0][p - 1] == r["mse"] and accs[t][1][p - 1] == r["phi"]
+    # the accumulators equal the interval sums along the traced-back chain
+    m = pipeline.chain_metrics(H, r["chain_bp"], lam)
+    assert abs(accs[t][0][p - 1] - m["mse"]) <= 1e-12 * m["mse"]
+
+
 def test_hirschberg_matches_backpointers_at_scale():
     """Hirschberg recovery (Sec. 5) equals the stored-argmin traceback and its
     recomputed cost equals the DP optimum."""
