@@ -2,18 +2,21 @@
 """Throughput of the ECASQ hot path on one MI355X.
 
 One step = the whole path on one synthetic vector already resident in HBM:
-sort + histogram + exact prefix sums, the lambda search (passes of 8
-multipliers, each pass one sweep of dp_APX solving all 8), Hirschberg
-recovery, three-colour refinement (5 rounds at most) and the final Philox
-stochastic rounding with its empirical entropy.
+sort + histogram + exact prefix sums, the lambda search (one full dp_APX solve
+per query), codebook recovery, three-colour refinement (5 rounds at most) and
+the final Philox stochastic rounding with its empirical entropy.  By default
+the library's own defaults run: DP schedule 1 (the column-block sweep, every
+layer updated from each cell, codebook from the argmin traceback) with the
+sequential chord search; --dp-schedule 0 runs the layer-by-layer O(d) path
+with the search in passes of 8 multipliers and Hirschberg recovery.
 
 Default workload (weights_256k): fp32, d = 2^18, 0.9 Normal(0, 0.01) +
 0.1 Laplace(0, 0.1), s = 32, budget 2.0 bits/entry, seed 0.
 
 Printed (one JSON line): DP cell-updates/s counted as s*d^2/2 per DP solve
-(the nominal unit; one solve per multiplier), the roofline of the DP layer
-kernel of the search passes measured with HIP events on its own stream, and
-the CPU oracle timed on a bounded sample.
+(the nominal unit; one solve per multiplier), the roofline of the dominant DP
+kernel measured with HIP events on its own stream, and the CPU oracle timed
+on a bounded sample.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME]
 """
@@ -47,13 +50,18 @@ def flops_per_cell(nlam):
 TRAFFIC_BYTES_PER_LAUNCH = 2.494e9
 TRAFFIC_SOURCES_SHA = "f3a631b21f5b78fb"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
+# the same, averaged over the k_sweep_step launches of the default workload
+# (profiles/k_sweep_step_weights_256k.md)
+SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 9.898e7
+SWEEP_TRAFFIC_SHA = "e39e1c1a98e7e2c0"
+SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 
 
-def kernel_sources_sha():
+def kernel_sources_sha(files=None):
     import hashlib
     h = hashlib.sha256()
     here = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_18147_amd", "csrc")
-    for f in KERNEL_SOURCES:
+    for f in files or KERNEL_SOURCES:
         with open(os.path.join(here, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -61,6 +69,37 @@ def kernel_sources_sha():
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
+
+
+def sweep_roofline(p, s, ms, solves, cells):
+    """Roofline of DP schedule 1: all k_sweep_step launches of one solve timed
+    as one unit.  Algorithmic flops per solve: the 45 shared flops of every
+    (k, j) pair, 3 per (k, j, layer) cell of layers 3..I, and 48 per column of
+    layer 2."""
+    I = min(s, p)
+    pairs = p * (p - 1) / 2.0
+    layer_cells = sum((p - i + 1) * (p - i + 2) / 2.0 for i in range(3, I + 1))
+    flops = FLOPS_SHARED * pairs + FLOPS_PER_LAMBDA * layer_cells + 48.0 * (p - 1)
+    per_ms = ms / max(solves, 1)
+    achieved = flops / (per_ms * 1e-3) / 1e12 if ms > 0 else 0.0
+    steps = (p + 63) // 64
+    return {
+        "bound": "alu",
+        "kernel": "k_sweep_step (fp64 VALU); one DP solve = %d launches" % steps,
+        "achieved": achieved,
+        "peak": FP64_VECTOR_PEAK_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
+        "traffic": (SWEEP_TRAFFIC_BYTES_PER_LAUNCH
+                    if kernel_sources_sha(SWEEP_SOURCES) == SWEEP_TRAFFIC_SHA else None),
+        "traffic_unit": "bytes/launch",
+        "flops_per_solve": flops,
+        "avg_launch_ms": per_ms / steps,
+        "launches": solves * steps,
+        "ms_per_solve": per_ms,
+        "solves": solves,
+        "cells_per_s": cells / (ms * 1e-3) if ms > 0 else None,
+    }
 
 
 def cpu_baseline(x, s, lam, sample_d):
@@ -127,6 +166,9 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=32768)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-batched", action="store_true")
+    ap.add_argument("--dp-schedule", type=int, default=None, choices=(0, 1),
+                    help="0: layer by layer (passes of 8, Hirschberg); 1: column-block sweep\n"
+                         "(default: the library's defaults)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run one plain device copy of 2^28 bytes (the reference kernel\n"
                          "that scales rocprofv3 FETCH_SIZE / WRITE_SIZE readings) and exit")
@@ -161,8 +203,16 @@ def main():
     xd = torch.from_numpy(x).to("cuda")
     torch.cuda.synchronize()
 
+    if args.dp_schedule == 0:
+        opts = ecasq.ecasq_default_options(dp_schedule=0, search_width=8)
+    elif args.dp_schedule == 1:
+        opts = ecasq.ecasq_default_options(dp_schedule=1, search_width=1)
+    else:
+        opts = ecasq.ecasq_default_options()
+    sweep = opts.dp_schedule == 1
+
     def step():
-        cb, rk, info = ecasq.ecasq_solve(xd, s, b)
+        cb, rk, info = ecasq.ecasq_solve(xd, s, b, options=opts)
         sym, ent, hist = ecasq.ecasq_quantize(xd, cb, args.seed)
         return info, ent
 
@@ -174,7 +224,7 @@ def main():
             f"{info['dp_solves']} DP solves, t={info['t']}")
 
     ecasq.ecasq_timing_enable(True)
-    for v in (ecasq.TIMING_SINGLE, ecasq.TIMING_PASS):
+    for v in (ecasq.TIMING_SINGLE, ecasq.TIMING_PASS, ecasq.TIMING_SWEEP):
         ecasq.ecasq_timing_read(v, reset=True)
     infos = []
     torch.cuda.synchronize()
@@ -188,15 +238,36 @@ def main():
     elapsed = time.perf_counter() - t_start
     ms, launches, cells = ecasq.ecasq_timing_read(ecasq.TIMING_PASS)
     ms1, launches1, cells1 = ecasq.ecasq_timing_read(ecasq.TIMING_SINGLE)
+    msw, nsw, cellsw = ecasq.ecasq_timing_read(ecasq.TIMING_SWEEP)
     ecasq.ecasq_timing_enable(False)
 
     nominal = sum(inf["dp_solves"] * s * d * d / 2.0 for inf, _ in infos)
     exact = sum(inf["cells"] for inf, _ in infos)
     value = nominal / elapsed
-    avg_ms = ms / max(launches, 1)
-    fpc = flops_per_cell(LAMBDAS_PER_PASS)
-    achieved = fpc * (cells / max(launches, 1)) / (avg_ms * 1e-3) / 1e12 if ms > 0 else 0.0
     info, ent = infos[-1]
+    p = info["p"]
+    if sweep:
+        roofline = sweep_roofline(p, s, msw, nsw, cellsw)
+    else:
+        avg_ms = ms / max(launches, 1)
+        fpc = flops_per_cell(LAMBDAS_PER_PASS)
+        achieved = fpc * (cells / max(launches, 1)) / (avg_ms * 1e-3) / 1e12 if ms > 0 else 0.0
+        roofline = {
+            "bound": "alu",
+            "kernel": "k_dp_layer, 8 multipliers per launch (fp64 VALU)",
+            "achieved": achieved,
+            "peak": FP64_VECTOR_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
+            "traffic": (TRAFFIC_BYTES_PER_LAUNCH if kernel_sources_sha() == TRAFFIC_SOURCES_SHA
+                        else None),
+            "traffic_unit": "bytes/launch",
+            "flops_per_cell": fpc,
+            "avg_launch_ms": avg_ms,
+            "launches": launches,
+            "cells_per_s": cells / (ms * 1e-3) if ms > 0 else None,
+            "lambda_cells_per_s": LAMBDAS_PER_PASS * cells / (ms * 1e-3) if ms > 0 else None,
+        }
     out = {
         "metric": "DP cell-updates/s (s*d^2/2 per solve)",
         "value": value,
@@ -212,24 +283,11 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": args.workload, "d": d, "s": s, "budget_bits": b, "seed": args.seed,
-            "refine_rounds": 5, "recovery": "hirschberg", "input_dtype": "f32",
+            "refine_rounds": 5, "input_dtype": "f32", "dp_schedule": opts.dp_schedule,
+            "search_width": opts.search_width,
+            "recovery": "argmin traceback" if sweep else "hirschberg",
         },
-        "roofline": {
-            "bound": "alu",
-            "kernel": "k_dp_layer, 8 multipliers per launch (fp64 VALU)",
-            "achieved": achieved,
-            "peak": FP64_VECTOR_PEAK_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
-            "traffic": (TRAFFIC_BYTES_PER_LAUNCH if kernel_sources_sha() == TRAFFIC_SOURCES_SHA
-                        else None),
-            "traffic_unit": "bytes/launch",
-            "flops_per_cell": fpc,
-            "avg_launch_ms": avg_ms,
-            "launches": launches,
-            "cells_per_s": cells / (ms * 1e-3) if ms > 0 else None,
-            "lambda_cells_per_s": LAMBDAS_PER_PASS * cells / (ms * 1e-3) if ms > 0 else None,
-        },
+        "roofline": roofline,
         "single_multiplier_layers": {
             "launches": launches1, "ms": ms1,
             "cells_per_s": cells1 / (ms1 * 1e-3) if ms1 > 0 else None,

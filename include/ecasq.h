@@ -59,9 +59,12 @@ typedef struct {
     int32_t refine_rounds;     /* Sec. 6 rounds, upper bound (default 5; 0 = off) */
     int32_t refine_exhaustive; /* 0: binary search of Sec. 6 (default); 1: full scan */
     int32_t exact_s;           /* 0: at most s values (default); 1: exactly min(s, p) */
-    int32_t max_search_passes; /* lambda-search passes of up to 8 solves (default 32) */
+    int32_t max_search_passes; /* lambda-search passes (default 32) */
     int32_t recovery;          /* 0: Hirschberg, O(d) space (default); 1: stored argmins */
-    int32_t search_width;      /* multipliers per search pass: 8 (default) or 1 */
+    int32_t search_width;      /* multipliers per search pass: 1 (default) or 8 */
+    int32_t dp_schedule;       /* 1: column-block sweep over all layers at once, O(s d)
+                                  space (default); 0: layer by layer, O(d) space (see
+                                  ecasq_solve_ex) */
 } ecasq_options;
 
 typedef struct {
@@ -115,7 +118,19 @@ ecasq_status ecasq_solve(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
                          int32_t *codebook_rank, ecasq_info *info);
 
 /* ecasq_solve with options and an optional caller workspace (device memory of
- * at least ecasq_workspace_size(d, s, 0) bytes; NULL = allocate internally). */
+ * at least ecasq_workspace_size(d, s, flags) bytes with flags = 1 if
+ * opts->recovery == 1, plus 2 if opts->dp_schedule == 1; NULL = allocate
+ * internally).
+ *
+ * DP schedules (both compute eq. apx_base / apx_rec / apx_final with the same
+ * values and argmins bit for bit):
+ *   0  layer by layer with two rolling layers of O(p) memory, as Sec. 5 states
+ *      it; the codebook is recovered by Hirschberg's method (recovery 0) or
+ *      from stored argmins (recovery 1);
+ *   1  one sweep over column blocks in which the interval cost and entropy
+ *      term of each cell serve every layer; keeps F and the argmins of all
+ *      layers (12 (s+1) d bytes) and takes the codebook from the argmin
+ *      traceback of the solve it was found in (recovery is ignored). */
 ecasq_status ecasq_solve_ex(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
                             double bits_per_entry, const ecasq_options *opts, void *stream,
                             double *codebook, int32_t *codebook_rank, ecasq_info *info,
@@ -160,7 +175,8 @@ ecasq_status ecasq_solve_batched(const void *x, ecasq_dtype dt, int64_t n, int64
                                  ecasq_info *infos_dev);
 
 /* Bytes of device workspace a single-vector solve of d entries with at most s
- * values needs (flags reserved, pass 0). */
+ * values needs; flags: 1 = stored argmins (recovery 1 of schedule 0),
+ * 2 = the tables of schedule 1 (0 when d < 1, s < 2 or flags outside 0..3). */
 size_t ecasq_workspace_size(int64_t d, int32_t s, int32_t flags);
 
 /* Static string for a status code. */
@@ -176,20 +192,22 @@ const char *ecasq_status_string(ecasq_status st);
  *
  * ecasq_dp_trace: forward DP solves of dp_APX (eq. apx_base, apx_rec,
  * apx_final) on the histogram of x at nlam multipliers lambdas[] (host array,
- * vNMSE units, nlam = 1 or 8; with 8 they run as one search pass does).  For
+ * vNMSE units, nlam = 1 or 8; with 8 and schedule 0 they run as one search
+ * pass does), by DP schedule `schedule` (0 or 1, as in ecasq_options).  For
  * multiplier m and every layer i in [2, min(s,p)] it records, in row
  * (m * (s+1) + i) of device arrays of nlam * (s+1) rows of d entries: F_i[j]
  * (F, fp64), the argmin k*_i[j] (kstar, int32), and the MSE and H(I,B)
- * accumulated along the argmins (M and Ph, fp64; each may be NULL).  Entries
- * outside a layer's valid columns are left untouched.  out (host, 5 * nlam):
- * per multiplier J (MSE units), MSE, H(I,B) of the minimising path, i*, cells.
+ * accumulated along the argmins (M and Ph, fp64; both NULL or both given).
+ * Entries outside a layer's valid columns are unspecified.  out (host,
+ * 5 * nlam): per multiplier J (MSE units), MSE, H(I,B) of the minimising
+ * path, i*, cells.
  */
 ecasq_status ecasq_histogram(const void *x, ecasq_dtype dt, int64_t d, void *stream, double *v,
                              double *N, double *S, double *S2, int64_t *p_out);
 
 ecasq_status ecasq_dp_trace(const void *x, ecasq_dtype dt, int64_t d, int32_t s, int32_t nlam,
-                            const double *lambdas, void *stream, double *F, int32_t *kstar,
-                            double *M, double *Ph, double *out);
+                            const double *lambdas, int32_t schedule, void *stream, double *F,
+                            int32_t *kstar, double *M, double *Ph, double *out);
 
 /*
  * Kernel timing for measurement tools.  While enabled (process-wide), every
@@ -197,7 +215,9 @@ ecasq_status ecasq_dp_trace(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
  * stream it runs on; the elapsed times are read when the solve synchronizes.
  * Launches are kept apart by variant: 0 = one multiplier per launch (fixed
  * lambda, width-1 search, recovery half-DPs), 1 = the 8 multipliers of a
- * search pass.  ecasq_timing_read returns, for one variant, the summed
+ * search pass, 2 = a whole solve of DP schedule 1 (all its launches, from
+ * the table fill to eq. apx_final, timed as one unit; cells counted as for
+ * schedule 0).  ecasq_timing_read returns, for one variant, the summed
  * milliseconds, the number of timed launches and the (column, predecessor)
  * cells those launches evaluated, each cell for every multiplier of its
  * launch (host pointers, any may be NULL); reset != 0 clears that variant's

@@ -239,14 +239,15 @@ def solve(x, s, b, refine_rounds=5, exhaustive=False, exact_s=False, max_passes=
     return r
 
 
-def solve_lagrangian(x, s, lam, refine_rounds=0, exhaustive=False, exact_s=False):
+def solve_lagrangian(x, s, lam, refine_rounds=0, exhaustive=False, exact_s=False,
+                     recovery="hirschberg"):
     """Fixed-multiplier mode: min vNMSE + lambda H(I,B), then refinement on
     vNMSE + lambda H(Xhat) without a budget guard."""
     H = prepare(x)
     if H.p == 1:
         return _finish(H, np.zeros(1, dtype=np.int32), lam, 0, 0, 0, 0)
     r = dp_forward(H, s, lam * H.s2tot, exact_s)
-    chain, hcells = _recover(H, r["t"], lam)
+    chain, hcells = _recover(H, r["t"], lam, recovery, s, exact_s)
     rounds = 0
     if refine_rounds > 0 and len(chain) >= 3:
         chain, rounds, _ = refine(H, chain, lam * H.s2tot, math.inf, False, refine_rounds,

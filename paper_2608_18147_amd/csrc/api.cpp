@@ -37,12 +37,17 @@ namespace {
 
 struct Layout {
     size_t v, N, S, S2, F0, F1, M0, M1, P0, P1, pval, pidx, last, res, mres, small, chain, kstar,
-        prep;
+        prep, swF, swK, swchain;
     int64_t pstride;  // partial entries per multiplier
     size_t total;
 };
 
-Layout layout(int64_t d, int32_t s, bool kstar) {
+// Workspace flags: stored argmins of every layer (recovery 1 of the
+// layer-by-layer schedule), and the sweep schedule's tables.
+constexpr int32_t kWsArgmins = 1;
+constexpr int32_t kWsSweep = 2;
+
+Layout layout(int64_t d, int32_t s, int32_t flags) {
     Layout L;
     size_t o = 0;
     auto take = [&](size_t bytes) {
@@ -55,24 +60,30 @@ Layout layout(int64_t d, int32_t s, bool kstar) {
     L.N = take(nd);
     L.S = take(nd);
     L.S2 = take(nd);
-    // layer buffers: kMaxLambdas rows of d per array (one per multiplier of a pass)
-    const size_t ndm = nd * kMaxLambdas;
+    const bool sweep = (flags & kWsSweep) != 0;
+    // layer-by-layer buffers: kMaxLambdas rows of d per array (one per
+    // multiplier of a pass); the sweep keeps whole tables instead
+    const size_t ndm = sweep ? 0 : nd * kMaxLambdas;
     L.F0 = take(ndm);
     L.F1 = take(ndm);
     L.M0 = take(ndm);
     L.M1 = take(ndm);
     L.P0 = take(ndm);
     L.P1 = take(ndm);
-    L.pstride = dp_partial_entries(d);
+    L.pstride = sweep ? 0 : dp_partial_entries(d);
     const size_t np = (size_t)L.pstride * kMaxLambdas;
     L.pval = take(sizeof(double) * np);
     L.pidx = take(sizeof(int32_t) * np);
+    L.swF = take(sweep ? sizeof(double) * (size_t)(s + 1) * (size_t)d : 0);
+    L.swK = take(sweep ? sizeof(int32_t) * (size_t)(s + 1) * (size_t)d : 0);
+    L.swchain = take(sizeof(int32_t) * 256);
     L.last = take(sizeof(double) * 3 * (size_t)(s + 1) * kMaxLambdas);
     L.res = take(sizeof(double) * 4 * kMaxLambdas);
     L.mres = take(sizeof(double) * 8);
     L.small = take(sizeof(int64_t) * 8);
     L.chain = take(sizeof(int32_t) * (size_t)(s + 8));
-    L.kstar = kstar ? take(sizeof(int32_t) * (size_t)(s + 1) * (size_t)d) : 0;
+    L.kstar = (flags & kWsArgmins) && !sweep ? take(sizeof(int32_t) * (size_t)(s + 1) * (size_t)d)
+                                              : 0;
     L.prep = take(prep_scratch_bytes(d));
     L.total = o;
     return L;
@@ -81,6 +92,7 @@ Layout layout(int64_t d, int32_t s, bool kstar) {
 struct Point {
     double lam, H, M;
     int32_t t;
+    std::vector<int32_t> chain;  // the solve's codebook (sweep schedule only)
 };
 
 struct Ctx {
@@ -95,6 +107,7 @@ struct Ctx {
     int64_t cells;
     int32_t solves;
     bool own;
+    bool sweep;  // dp_APX by the column-block sweep (else layer by layer)
 
     template <class T>
     T* at(size_t off) const {
@@ -108,12 +121,13 @@ ecasq_status check_x(const void* x, int dt, int64_t d) {
     return ECASQ_OK;
 }
 
-ecasq_status ctx_open(Ctx& c, int64_t d, int32_t s, bool kstar, void* stream, void* ws,
+ecasq_status ctx_open(Ctx& c, int64_t d, int32_t s, int32_t flags, void* stream, void* ws,
                       size_t ws_bytes) {
     c.st = static_cast<hipStream_t>(stream);
     c.d = d;
     c.s = s;
-    c.L = layout(d, s, kstar);
+    c.sweep = (flags & kWsSweep) != 0;
+    c.L = layout(d, s, flags);
     c.cells = 0;
     c.solves = 0;
     c.own = ws == nullptr;
@@ -178,12 +192,78 @@ struct Dumps {
     int64_t stride = 0;
 };
 
+int64_t dp_cells(int64_t p, int32_t imax) {
+    int64_t n = p - 1;
+    for (int32_t i = 3; i <= imax; i++) n += tri_cells(p - i + 1);
+    return n;
+}
+
+// One dp_APX solve at lam by the column-block sweep: the result, the chain of
+// its codebook, and optionally the tables as dumps (row m of a pass).
+ecasq_status sweep_solve(Ctx& c, double lam, int32_t exact_s, Point& out, double* J4,
+                         const Dumps* dump, int32_t m) {
+    const int64_t p = c.p;
+    const int32_t imax = (int32_t)std::min<int64_t>(c.s, p);
+    SweepSolve S;
+    S.H = c.H;
+    S.F = c.at<double>(c.L.swF);
+    S.K = c.at<int32_t>(c.L.swK);
+    S.ld = c.d;
+    S.I = imax;
+    S.lamp = lam * c.s2tot;
+    double* res = c.at<double>(c.L.res);
+    int32_t* ch = c.at<int32_t>(c.L.swchain);
+    timing_begin(2, dp_cells(p, imax), c.st);
+    HIP_TRY(launch_sweep(S, exact_s, res, ch, c.st));
+    timing_end(c.st);
+    if (dump) {
+        const int32_t ls = c.s + 1;
+        const int64_t ds = dump->stride;
+        const size_t rows = (size_t)(imax - 1) * (size_t)c.d;
+        if (ds != c.d) return ECASQ_EINVAL;
+        if (dump->F)
+            HIP_TRY(hipMemcpyAsync(dump->F + ((int64_t)m * ls + 2) * ds, S.F + 2 * c.d,
+                                   sizeof(double) * rows, hipMemcpyDeviceToDevice, c.st));
+        if (dump->K)
+            HIP_TRY(hipMemcpyAsync(dump->K + ((int64_t)m * ls + 2) * ds, S.K + 2 * c.d,
+                                   sizeof(int32_t) * rows, hipMemcpyDeviceToDevice, c.st));
+        if (dump->M && dump->P)
+            HIP_TRY(launch_sweep_accumulators(S, dump->M + (int64_t)m * ls * ds,
+                                              dump->P + (int64_t)m * ls * ds, c.st));
+    }
+    double r[4];
+    HIP_TRY(hipMemcpyAsync(r, res, sizeof r, hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    const int32_t t = (int32_t)r[3];
+    if (t < 2 || t > imax) return ECASQ_EHIP;
+    out.chain.assign(t, 0);
+    HIP_TRY(hipMemcpyAsync(out.chain.data(), ch, sizeof(int32_t) * t, hipMemcpyDeviceToHost,
+                           c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    timing_flush();
+    out.lam = lam;
+    out.H = r[2];
+    out.M = r[1] / c.s2tot;
+    out.t = t;
+    if (J4) std::memcpy(J4, r, sizeof r);
+    c.cells += dp_cells(p, imax);
+    c.solves++;
+    return ECASQ_OK;
+}
+
 // Full dp_APX solves at nlam multipliers lams[] (vNMSE units) in one sweep
-// over the layers (nlam must be 1 or kMaxLambdas).  J_out (optional): the raw
-// (J, MSE, H(I,B), t) of every multiplier.
+// over the layers (nlam must be 1 or kMaxLambdas; the column-block sweep
+// solves them one after the other).  J_out (optional): the raw (J, MSE,
+// H(I,B), t) of every multiplier.
 ecasq_status dp_solve(Ctx& c, const double* lams, int32_t nlam, int32_t exact_s, Point* out,
                       double* J_out, const Dumps* dump) {
     if (nlam != 1 && nlam != kMaxLambdas) return ECASQ_EINVAL;
+    if (c.sweep) {
+        for (int32_t m = 0; m < nlam; m++)
+            ECASQ_TRY(sweep_solve(c, lams[m], exact_s, out[m], J_out ? J_out + 4 * m : nullptr,
+                                  dump, m));
+        return ECASQ_OK;
+    }
     const int64_t p = c.p;
     const int32_t imax = (int32_t)std::min<int64_t>(c.s, p);
     const int32_t ls = c.s + 1;
@@ -546,22 +626,34 @@ ecasq_status finish(Ctx& c, std::vector<int32_t>& chain, double lam, double b, b
     return status;
 }
 
+int32_t ws_flags(const ecasq_options& o) {
+    return (o.recovery == 1 ? kWsArgmins : 0) | (o.dp_schedule == 1 ? kWsSweep : 0);
+}
+
 ecasq_options defaults() {
     ecasq_options o;
     o.refine_rounds = 5;
     o.refine_exhaustive = 0;
     o.exact_s = 0;
     o.max_search_passes = 32;
-    o.search_width = kMaxLambdas;
+    o.search_width = 1;
+    o.dp_schedule = 1;
     o.recovery = 0;
     return o;
+}
+
+bool options_ok(const ecasq_options& o) {
+    return o.refine_rounds >= 0 && o.refine_exhaustive >= 0 && o.refine_exhaustive <= 1 &&
+           o.exact_s >= 0 && o.exact_s <= 1 && o.max_search_passes >= 1 && o.recovery >= 0 &&
+           o.recovery <= 1 && (o.search_width == 1 || o.search_width == kMaxLambdas) &&
+           o.dp_schedule >= 0 && o.dp_schedule <= 1;
 }
 
 ecasq_status solve_budget(const void* x, int dt, int64_t d, int32_t s, double b,
                           const ecasq_options& o, void* stream, double* codebook, int32_t* rank,
                           ecasq_info* info, void* ws, size_t wsb) {
     Ctx c;
-    ECASQ_TRY(ctx_open(c, d, s, o.recovery == 1, stream, ws, wsb));
+    ECASQ_TRY(ctx_open(c, d, s, ws_flags(o), stream, ws, wsb));
     struct Closer {
         Ctx& c;
         ~Closer() { ctx_close(c); }
@@ -579,7 +671,10 @@ ecasq_status solve_budget(const void* x, int dt, int64_t d, int32_t s, double b,
         status = R.status;
         lam = R.lam_final;
         passes = R.passes;
-        ECASQ_TRY(recover(c, R.B.t, R.B.lam, o.exact_s, o.recovery, chain));
+        if (!R.B.chain.empty())
+            chain = R.B.chain;
+        else
+            ECASQ_TRY(recover(c, R.B.t, R.B.lam, o.exact_s, o.recovery, chain));
     }
     ecasq_status st = finish(c, chain, lam, b, true, o, codebook, rank, info, status, passes);
     if (c.p == 2 && info && info->entropy_surrogate > b) {
@@ -598,8 +693,8 @@ void ecasq_default_options(ecasq_options* opts) {
 }
 
 size_t ecasq_workspace_size(int64_t d, int32_t s, int32_t flags) {
-    if (d < 1 || s < 2) return 0;
-    return layout(d, s, (flags & 1) != 0).total;
+    if (d < 1 || s < 2 || flags < 0 || flags > 3) return 0;
+    return layout(d, s, flags).total;
 }
 
 const char* ecasq_status_string(ecasq_status st) {
@@ -623,9 +718,7 @@ ecasq_status ecasq_solve_ex(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
     if (s < 2 || s > 255 || !codebook) return ECASQ_EINVAL;
     if (!(bits_per_entry >= 0.0)) return ECASQ_EINVAL;  // also rejects NaN
     const ecasq_options o = opts ? *opts : defaults();
-    if (o.refine_rounds < 0 || o.max_search_passes < 1 || o.recovery < 0 || o.recovery > 1 ||
-        (o.search_width != 1 && o.search_width != kMaxLambdas))
-        return ECASQ_EINVAL;
+    if (!options_ok(o)) return ECASQ_EINVAL;
     return solve_budget(x, dt, d, s, bits_per_entry, o, stream, codebook, codebook_rank, info,
                         workspace, workspace_bytes);
 }
@@ -644,9 +737,9 @@ ecasq_status ecasq_solve_lagrangian(const void* x, ecasq_dtype dt, int64_t d, in
     if (s < 2 || s > 255 || !codebook || !(lambda >= 0.0) || !std::isfinite(lambda))
         return ECASQ_EINVAL;
     const ecasq_options o = opts ? *opts : defaults();
-    if (o.refine_rounds < 0 || o.recovery < 0 || o.recovery > 1) return ECASQ_EINVAL;
+    if (!options_ok(o)) return ECASQ_EINVAL;
     Ctx c;
-    ECASQ_TRY(ctx_open(c, d, s, o.recovery == 1, stream, nullptr, 0));
+    ECASQ_TRY(ctx_open(c, d, s, ws_flags(o), stream, nullptr, 0));
     struct Closer {
         Ctx& c;
         ~Closer() { ctx_close(c); }
@@ -658,7 +751,10 @@ ecasq_status ecasq_solve_lagrangian(const void* x, ecasq_dtype dt, int64_t d, in
     } else {
         Point P;
         ECASQ_TRY(dp_solve1(c, lambda, o.exact_s, P));
-        ECASQ_TRY(recover(c, P.t, lambda, o.exact_s, o.recovery, chain));
+        if (!P.chain.empty())
+            chain = P.chain;
+        else
+            ECASQ_TRY(recover(c, P.t, lambda, o.exact_s, o.recovery, chain));
     }
     return finish(c, chain, lambda, HUGE_VAL, false, o, codebook, codebook_rank, info, ECASQ_OK,
                   0);
@@ -688,7 +784,7 @@ ecasq_status ecasq_histogram(const void* x, ecasq_dtype dt, int64_t d, void* str
     ECASQ_TRY(check_x(x, dt, d));
     if (!v || !N || !S || !S2 || !p_out) return ECASQ_EINVAL;
     Ctx c;
-    ECASQ_TRY(ctx_open(c, d, 2, false, stream, nullptr, 0));
+    ECASQ_TRY(ctx_open(c, d, 2, 0, stream, nullptr, 0));
     struct Closer {
         Ctx& c;
         ~Closer() { ctx_close(c); }
@@ -705,15 +801,16 @@ ecasq_status ecasq_histogram(const void* x, ecasq_dtype dt, int64_t d, void* str
 }
 
 ecasq_status ecasq_dp_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s, int32_t nlam,
-                            const double* lambdas, void* stream, double* F, int32_t* kstar,
-                            double* M, double* Ph, double* out) {
+                            const double* lambdas, int32_t schedule, void* stream, double* F,
+                            int32_t* kstar, double* M, double* Ph, double* out) {
     ECASQ_TRY(check_x(x, dt, d));
     if (s < 2 || s > 255 || !F || !kstar || !out || !lambdas) return ECASQ_EINVAL;
     if (nlam != 1 && nlam != kMaxLambdas) return ECASQ_EINVAL;
+    if (schedule < 0 || schedule > 1 || ((M == nullptr) != (Ph == nullptr))) return ECASQ_EINVAL;
     for (int32_t m = 0; m < nlam; m++)
         if (!(lambdas[m] >= 0.0) || !std::isfinite(lambdas[m])) return ECASQ_EINVAL;
     Ctx c;
-    ECASQ_TRY(ctx_open(c, d, s, false, stream, nullptr, 0));
+    ECASQ_TRY(ctx_open(c, d, s, schedule == 1 ? kWsSweep : 0, stream, nullptr, 0));
     struct Closer {
         Ctx& c;
         ~Closer() { ctx_close(c); }

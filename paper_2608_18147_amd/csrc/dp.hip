@@ -440,7 +440,8 @@ struct TimingTotals {
 bool g_timing = false;
 std::vector<TimedLaunch> g_pending;
 std::vector<hipEvent_t> g_pool;
-TimingTotals g_tot[2];
+TimingTotals g_tot[3];
+TimedLaunch g_open{nullptr, nullptr, 0, 0};
 
 hipEvent_t take_event() {
     if (!g_pool.empty()) {
@@ -470,9 +471,24 @@ void timing_flush() {
     g_pending.clear();
 }
 
+void timing_begin(int variant, int64_t cells, hipStream_t st) {
+    g_open = TimedLaunch{nullptr, nullptr, cells, variant};
+    if (!g_timing) return;
+    g_open.a = take_event();
+    g_open.b = take_event();
+    if (g_open.a && g_open.b) (void)hipEventRecord(g_open.a, st);
+}
+
+void timing_end(hipStream_t st) {
+    if (!g_timing || !g_open.a || !g_open.b) return;
+    (void)hipEventRecord(g_open.b, st);
+    g_pending.push_back(g_open);
+    g_open = TimedLaunch{nullptr, nullptr, 0, 0};
+}
+
 void timing_read(int variant, double* ms, int64_t* launches, int64_t* cells, bool reset) {
     timing_flush();
-    if (variant < 0 || variant > 1) {
+    if (variant < 0 || variant > 2) {
         if (ms) *ms = 0.0;
         if (launches) *launches = 0;
         if (cells) *cells = 0;

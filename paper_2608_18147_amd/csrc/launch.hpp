@@ -72,6 +72,9 @@ int64_t dp_partial_entries(int64_t p);
 void timing_enable(bool on);
 void timing_flush();
 void timing_read(int variant, double* ms, int64_t* launches, int64_t* cells, bool reset);
+// bracket a span of launches on st as one timed unit of `variant` (2: a sweep solve)
+void timing_begin(int variant, int64_t cells, hipStream_t st);
+void timing_end(hipStream_t st);
 hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st);
 hipError_t launch_dp_init_fwd(const Hist& H, int64_t lo, int64_t jl, int64_t jh,
                               const DpInit& I, hipStream_t st);
@@ -82,6 +85,25 @@ hipError_t launch_dp_final(const double* last, int32_t stride, int32_t imax, int
                            int32_t nlam, double* out, hipStream_t st);
 hipError_t launch_split(const double* Fw, const double* Bw, int64_t ml, int64_t mh,
                         int64_t* m_out, hipStream_t st);
+
+// ---- sweep.hip ----
+// One dp_APX solve as a sweep over column blocks: F and the argmins of every
+// layer in tables of I+1 rows of ld entries (rows 2..I used).
+struct SweepSolve {
+    Hist H;
+    double* F;
+    int32_t* K;
+    int64_t ld;    // >= p
+    int32_t I;     // last layer, min(s, p), 2..255
+    double lamp;   // lambda' in MSE units
+};
+size_t sweep_table_bytes(int64_t d, int32_t s);
+// The sweep, then eq. apx_final: out (device, 4 doubles) = J, MSE, H(I,B), i*;
+// chain (device, optional, >= i* int32): the argmin chain u_0 = 0 .. u_{i*-1} = p-1.
+hipError_t launch_sweep(const SweepSolve& S, int32_t exact_s, double* out, int32_t* chain,
+                        hipStream_t st);
+// MSE / H(I,B) accumulators of every layer into M, Ph (same layout as F).
+hipError_t launch_sweep_accumulators(const SweepSolve& S, double* M, double* Ph, hipStream_t st);
 
 // ---- post.hip ----
 hipError_t launch_refine(const Hist& H, int32_t t, int32_t* u, double lamp, double b,

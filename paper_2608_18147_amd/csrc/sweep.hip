@@ -1,0 +1,451 @@
+// dp_APX (Sec. 5, eq. apx_base / apx_rec / apx_final) for one multiplier as a
+// sweep over column blocks that updates every layer from each cell.
+//
+// The interval cost C[k,j] and the entropy term Phi[k,j] do not depend on the
+// layer i, but the layer-by-layer schedule recomputes them for every layer.
+// Here the (k, j) triangle is swept once: with F_i[k] final for all layers i
+// and all k of the blocks before column block J, one evaluation of C and Phi
+// serves the candidates F_{i-1}[k] + C + lambda' Phi of every layer.  The
+// price is O(s p) memory (F and the argmins of every layer: 12 (s+1) p bytes,
+// 0.1 GB at p = 2^18, s = 32) instead of O(p) rolling buffers; the values and
+// argmins are the same bit for bit (same candidate arithmetic, lowest k on
+// ties).  With every argmin kept, the codebook is a traceback, and the path's
+// MSE and H(I,B) are summed along it in path order (the same additions the
+// layer-by-layer accumulators perform).
+//
+// Step t of the sweep (blocks of 64 columns, one per wavefront) is one launch
+// of k_sweep_step:
+//   workgroup 0    block t: the contribution of block t-1, then the
+//                  triangle inside block t layer after layer (a layer needs
+//                  the previous layer's values of the same block), which
+//                  makes block t final;
+//   the others     blocks J > t: the contribution of block t-1 (final since
+//                  step t-1) to their running minima, kept in F and K.
+// Blocks are visited in increasing order and predecessors in increasing k,
+// so strict '<' keeps the lowest argmin.
+#include "device.hpp"
+#include "launch.hpp"
+
+namespace ecasq {
+
+namespace {
+
+constexpr int kSB = 64;        // columns per block (one wavefront)
+constexpr int kTileWaves = 4;  // wavefronts per workgroup
+// below this many (column block, layer group) tiles a step splits layers
+// over the wavefronts of a workgroup (2 waves per SIMD of 256 CUs)
+#ifndef ECASQ_SWEEP_SPLIT_BELOW
+#define ECASQ_SWEEP_SPLIT_BELOW 2048
+#endif
+constexpr int64_t kSplitBelow = ECASQ_SWEEP_SPLIT_BELOW;
+// widest layer group (register arrays of that many layers per lane)
+#ifndef ECASQ_SWEEP_LG_MAX
+#define ECASQ_SWEEP_LG_MAX 32
+#endif
+
+struct SweepArgs {
+    Hist H;
+    double* F;    // [I+1][ld]: rows 2..I; running minima until a block is final
+    int32_t* K;   // argmins, same layout
+    int64_t ld;
+    int32_t I;    // last layer, min(s, p)
+    double lamp;  // lambda' (MSE units)
+    int64_t nblk;
+};
+
+// Running-minimum update for a predecessor below every column (unmasked):
+// strict '<' keeps the lowest k; min() differs from the select only in the
+// sign of an exact zero.
+__device__ __forceinline__ void take_min(double cand, int32_t k, double& best, int32_t& bk) {
+    bk = cand < best ? k : bk;
+    best = __builtin_fmin(best, cand);
+}
+
+// Stage predecessor block [k0, k0+64): v, N, S, S2 and F_{i-1} for the LG
+// layers i0..i0+LG-1 (+inf past I).  All threads of the workgroup take part.
+template <int LG>
+__device__ __forceinline__ void stage_block(const SweepArgs& a, int64_t k0, int32_t i0, double* sv,
+                                            double* sN, double* sS, double* sS2,
+                                            double (*sF)[LG]) {
+    // block [k0, k0+64) lies below a later block, so k0 + 63 < p
+    for (int x = threadIdx.x; x < kSB; x += blockDim.x) {
+        const int64_t k = k0 + x;
+        sv[x] = a.H.v[k];
+        sN[x] = a.H.N[k];
+        sS[x] = a.H.S[k];
+        sS2[x] = a.H.S2[k];
+    }
+    for (int x = threadIdx.x; x < kSB * LG; x += blockDim.x) {
+        const int kk = x % kSB, l = x / kSB;
+        const int32_t i = i0 + l;
+        sF[kk][l] = i <= a.I ? a.F[(int64_t)(i - 1) * a.ld + k0 + kk] : __builtin_huge_val();
+    }
+}
+
+// Rows 2..I of F := +inf, K := -1 (nothing seen yet; also the value of every
+// entry outside a layer's valid columns, which makes such predecessors lose).
+__global__ __launch_bounds__(256) void k_sweep_fill(SweepArgs a) {
+    const int64_t n = (int64_t)(a.I - 1) * a.ld;
+    for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n;
+         x += (int64_t)gridDim.x * blockDim.x) {
+        a.F[2 * a.ld + x] = __builtin_huge_val();
+        a.K[2 * a.ld + x] = -1;
+    }
+}
+
+// Shared memory of one step workgroup.
+template <int LG>
+struct StepSmem {
+    double2 tab[kLog2Size];
+    double sv[kSB], sN[kSB], sS[kSB], sS2[kSB];  // predecessor block t-1
+    double sF[kSB][LG];                           // its F_{i-1} for one layer group
+    double dv[kSB], dN[kSB], dS[kSB], dS2[kSB];   // block t (diagonal role)
+    double pF[kSB];                               // previous layer of block t
+    double partV[kTileWaves][kSB];                // per-wave partial minima
+    int32_t partK[kTileWaves][kSB];
+};
+
+// Running minima of LW layers i0.. of column jj (rows past I: +inf / -1).
+template <int LW>
+__device__ __forceinline__ void load_running(const SweepArgs& a, int64_t jj, int32_t i0,
+                                             double (&best)[LW], int32_t (&bk)[LW]) {
+#pragma unroll
+    for (int l = 0; l < LW; l++) {
+        const int32_t i = i0 + l;
+        const bool ok = i <= a.I;
+        best[l] = ok ? a.F[(int64_t)i * a.ld + jj] : __builtin_huge_val();
+        bk[l] = ok ? a.K[(int64_t)i * a.ld + jj] : -1;
+    }
+}
+
+template <int LW>
+__device__ __forceinline__ void store_running(const SweepArgs& a, int64_t j, int32_t i0,
+                                              const double (&best)[LW], const int32_t (&bk)[LW]) {
+    if (j >= a.H.p) return;
+#pragma unroll
+    for (int l = 0; l < LW; l++) {
+        const int32_t i = i0 + l;
+        if (i <= a.I) {
+            a.F[(int64_t)i * a.ld + j] = best[l];
+            a.K[(int64_t)i * a.ld + j] = bk[l];
+        }
+    }
+}
+
+// The 64 staged predecessors against column (cv, cN, cS, cS2) for LW layers
+// whose F_{i-1} sit in sF columns lofs..lofs+LW-1.
+template <int LG, int LW>
+__device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int64_t k0, int lofs, double cv,
+                                           double cN, double cS, double cS2, double dd,
+                                           double lamp, double (&best)[LW],
+                                           int32_t (&bk)[LW]) {
+    for (int kk = 0; kk < kSB; kk++) {
+        double C, P;
+        cell_terms(sm.sv[kk], sm.sN[kk], sm.sS[kk], sm.sS2[kk], cv, cN, cS, cS2, dd, false, 0.0,
+                   sm.tab, C, P);
+        const int32_t k = (int32_t)(k0 + kk);
+#pragma unroll
+        for (int l = 0; l < LW; l++)
+            take_min(__builtin_fma(-lamp, P, sm.sF[kk][lofs + l] + C), k, best[l], bk[l]);
+    }
+}
+
+// Stage predecessor block [k0, k0+64) with F_{i-1} of layers i0..i0+LG-1.
+template <int LG>
+__device__ __forceinline__ void stage_pred(const SweepArgs& a, int64_t k0, int32_t i0,
+                                           StepSmem<LG>& sm) {
+    stage_block<LG>(a, k0, i0, sm.sv, sm.sN, sm.sS, sm.sS2, sm.sF);
+}
+
+// Tile role: column blocks J > t take predecessor block t-1 for one layer
+// group.  split = 0: one column block per wavefront, all LG layers; split = 1:
+// one column block per workgroup, LG/4 layers per wavefront (more waves, for
+// the late steps that have few blocks left).
+template <int LG>
+__device__ void tile_role(const SweepArgs& a, int64_t t, int32_t split, int64_t wg, int32_t g,
+                          StepSmem<LG>& sm) {
+    constexpr int LW = LG / kTileWaves;
+    const int32_t i0 = 3 + g * LG;
+    const int64_t k0 = (t - 1) * kSB;
+    stage_pred<LG>(a, k0, i0, sm);
+    __syncthreads();
+    const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
+    const int64_t J = split ? t + 1 + wg : t + 1 + wg * kTileWaves + wave;
+    if (J >= a.nblk) return;
+    const int64_t j = J * kSB + lane;
+    const int64_t jj = j < a.H.p ? j : a.H.p - 1;
+    const double cv = a.H.v[jj], cN = a.H.N[jj], cS = a.H.S[jj], cS2 = a.H.S2[jj];
+    if (split) {
+        double best[LW];
+        int32_t bk[LW];
+        const int32_t iw = i0 + wave * LW;
+        load_running<LW>(a, jj, iw, best, bk);
+        accumulate<LG, LW>(sm, k0, wave * LW, cv, cN, cS, cS2, a.H.dd, a.lamp, best, bk);
+        store_running<LW>(a, j, iw, best, bk);
+    } else {
+        double best[LG];
+        int32_t bk[LG];
+        load_running<LG>(a, jj, i0, best, bk);
+        accumulate<LG, LG>(sm, k0, 0, cv, cN, cS, cS2, a.H.dd, a.lamp, best, bk);
+        store_running<LG>(a, j, i0, best, bk);
+    }
+}
+
+// Diagonal role (workgroup 0): block t becomes final.  For every layer group:
+// predecessor block t-1 (LG/4 layers per wavefront), then the group's layers
+// inside the block in order; each wavefront holds C and Phi of 16 of the
+// block's predecessors in registers, the four partial minima meet in LDS and
+// the wavefront that holds the layer's running minimum merges them in
+// increasing k (running minimum first: its k lie in earlier blocks).
+template <int LG>
+__device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
+    constexpr int LW = LG / kTileWaves;
+    constexpr int KW = kSB / kTileWaves;  // predecessors of the block per wavefront
+    const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
+    const int64_t p = a.H.p;
+    const int64_t j0 = t * kSB;
+    const int64_t j = j0 + lane;
+    const int64_t jj = j < p ? j : p - 1;
+    const bool valid = j < p;
+    const double lamp = a.lamp, dd = a.H.dd;
+    for (int x = threadIdx.x; x < kSB; x += blockDim.x) {
+        const int64_t k = j0 + x < p ? j0 + x : p - 1;
+        sm.dv[x] = a.H.v[k];
+        sm.dN[x] = a.H.N[k];
+        sm.dS[x] = a.H.S[k];
+        sm.dS2[x] = a.H.S2[k];
+    }
+    __syncthreads();
+    const int c = (int)(jj - j0);
+    const double cv = sm.dv[c], cN = sm.dN[c], cS = sm.dS[c], cS2 = sm.dS2[c];
+    // C and Phi of (k, j) for this wavefront's 16 predecessors k < j
+    double cC[KW], cP[KW];
+#pragma unroll
+    for (int q = 0; q < KW; q++) {
+        const int kk = wave * KW + q;
+        cC[q] = 0.0;
+        cP[q] = 0.0;
+        if (j0 + kk < jj)
+            cell_terms(sm.dv[kk], sm.dN[kk], sm.dS[kk], sm.dS2[kk], cv, cN, cS, cS2, dd, false,
+                       0.0, sm.tab, cC[q], cP[q]);
+    }
+    // layer 2 (eq. apx_base): the first interval (v_0, v_j]
+    if (wave == 0) {
+        double f = __builtin_huge_val();
+        if (valid && j >= 1) {
+            double C, P;
+            cell_at(a.H, 0, j, sm.tab, C, P);
+            f = __builtin_fma(-lamp, P, 0.0 + C);
+            a.F[2 * a.ld + j] = f;
+            a.K[2 * a.ld + j] = 0;
+        }
+        sm.pF[lane] = f;
+    }
+    for (int32_t i0 = 3; i0 <= a.I; i0 += LG) {
+        const int32_t iw = i0 + wave * LW;
+        double best[LW];
+        int32_t bk[LW];
+        load_running<LW>(a, jj, iw, best, bk);
+        __syncthreads();  // previous group's use of sF / pF is over
+        if (t >= 1) {
+            const int64_t k0 = (t - 1) * kSB;
+            stage_pred<LG>(a, k0, i0, sm);
+            __syncthreads();
+            accumulate<LG, LW>(sm, k0, wave * LW, cv, cN, cS, cS2, dd, lamp, best, bk);
+        }
+#pragma unroll
+        for (int l = 0; l < LG; l++) {
+            const int32_t i = i0 + l;
+            if (i > a.I) break;
+            double pv = __builtin_huge_val();
+            int32_t pk = -1;
+#pragma unroll
+            for (int q = 0; q < KW; q++) {
+                const int kk = wave * KW + q;
+                const int64_t k = j0 + kk;
+                const double cand = __builtin_fma(-lamp, cP[q], sm.pF[kk] + cC[q]);
+                const bool lt = k < j && cand < pv;
+                pk = lt ? (int32_t)k : pk;
+                pv = lt ? cand : pv;
+            }
+            sm.partV[wave][lane] = pv;
+            sm.partK[wave][lane] = pk;
+            __syncthreads();
+            if (wave == l / LW) {
+                double b = best[l % LW];
+                int32_t kb = bk[l % LW];
+#pragma unroll
+                for (int w = 0; w < kTileWaves; w++) {
+                    const double v = sm.partV[w][lane];
+                    const int32_t kv = sm.partK[w][lane];
+                    kb = v < b ? kv : kb;
+                    b = v < b ? v : b;
+                }
+                if (valid) {
+                    a.F[(int64_t)i * a.ld + j] = b;
+                    a.K[(int64_t)i * a.ld + j] = kb;
+                }
+                sm.pF[lane] = valid ? b : __builtin_huge_val();
+            }
+            __syncthreads();
+        }
+    }
+}
+
+// Step t of the sweep: workgroup 0 makes block t final, the others add
+// predecessor block t-1 to the blocks after it (tile WG index = g * nx + wg).
+template <int LG>
+__global__ __launch_bounds__(kSB* kTileWaves) void k_sweep_step(SweepArgs a, int64_t t,
+                                                              int32_t split, int64_t nx) {
+    __shared__ StepSmem<LG> sm;
+    load_log2_table(sm.tab);
+    __syncthreads();
+    if (blockIdx.x == 0) {
+        // the diagonal block is the step's critical path: let its waves issue
+        // ahead of tile waves that share its SIMDs
+        __builtin_amdgcn_s_setprio(3);
+        diag_role<LG>(a, t, sm);
+    } else {
+        const int64_t x = (int64_t)blockIdx.x - 1;
+        tile_role<LG>(a, t, split, x % nx, (int32_t)(x / nx), sm);
+    }
+}
+
+// eq. apx_final on the finished tables, the chain of the chosen layer traced
+// back through the argmins, and its MSE and H(I,B) summed in path order.
+// One wavefront.  out: J, MSE, H(I,B), i*.
+__global__ __launch_bounds__(kSB) void k_sweep_final(SweepArgs a, int32_t exact_s, double* out,
+                                                     int32_t* chain_out) {
+    __shared__ double2 tab[kLog2Size];
+    __shared__ int32_t u[256];
+    __shared__ double cC[256], cP[256];
+    __shared__ int32_t s_istar;
+    load_log2_table(tab);
+    const int lane = threadIdx.x;
+    const int64_t p = a.H.p;
+    if (lane == 0) {
+        int32_t bi = 2;
+        double bj = a.F[2 * a.ld + p - 1];
+        for (int32_t i = 3; i <= a.I; i++) {
+            const double f = a.F[(int64_t)i * a.ld + p - 1];
+            if (exact_s ? (i == a.I) : (f < bj)) {
+                bj = f;
+                bi = i;
+            }
+        }
+        u[bi - 1] = (int32_t)(p - 1);
+        for (int32_t i = bi; i >= 3; i--) u[i - 2] = a.K[(int64_t)i * a.ld + u[i - 1]];
+        u[0] = 0;
+        s_istar = bi;
+        out[0] = bj;
+    }
+    __syncthreads();
+    const int32_t n = s_istar;
+    for (int r = lane; r + 1 < n; r += kSB) cell_at(a.H, u[r], u[r + 1], tab, cC[r], cP[r]);
+    __syncthreads();
+    if (lane == 0) {
+        double mse = 0.0, ph = 0.0;
+        for (int r = 0; r + 1 < n; r++) {
+            mse = mse + cC[r];
+            ph = ph - cP[r];
+        }
+        out[1] = mse;
+        out[2] = ph;
+        out[3] = (double)n;
+    }
+    if (chain_out)
+        for (int r = lane; r < n; r += kSB) chain_out[r] = u[r];
+}
+
+// Accumulators of layer i for every valid column (inspection only):
+// M_i[j] = M_{i-1}[k*] + C[k*, j], Ph_i[j] = Ph_{i-1}[k*] - P[k*, j] with the
+// layer-2 start 0 + C[0, j], 0 - P[0, j], as the layer-by-layer DP forms them.
+__global__ __launch_bounds__(256) void k_sweep_acc(SweepArgs a, int32_t i, double* M, double* Ph) {
+    __shared__ double2 tab[kLog2Size];
+    load_log2_table(tab);
+    __syncthreads();
+    const int64_t j = (int64_t)(i - 1) + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= a.H.p) return;
+    const int32_t bk = a.K[(int64_t)i * a.ld + j];
+    if (bk < 0) return;
+    double C, P;
+    cell_at(a.H, bk, j, tab, C, P);
+    const double m0 = i == 2 ? 0.0 : M[(int64_t)(i - 1) * a.ld + bk];
+    const double p0 = i == 2 ? 0.0 : Ph[(int64_t)(i - 1) * a.ld + bk];
+    M[(int64_t)i * a.ld + j] = m0 + C;
+    Ph[(int64_t)i * a.ld + j] = p0 - P;
+}
+
+SweepArgs make_args(const SweepSolve& S) {
+    SweepArgs a;
+    a.H = S.H;
+    a.F = S.F;
+    a.K = S.K;
+    a.ld = S.ld;
+    a.I = S.I;
+    a.lamp = S.lamp;
+    a.nblk = (S.H.p + kSB - 1) / kSB;
+    return a;
+}
+
+template <int LG>
+hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
+    const int32_t ngroups = (a.I - 2 + LG - 1) / LG;
+    {
+        const int64_t n = (int64_t)(a.I - 1) * a.ld;
+        int64_t g = (n + 255) / 256;
+        if (g > 4096) g = 4096;
+        k_sweep_fill<<<(unsigned)g, 256, 0, st>>>(a);
+    }
+    for (int64_t t = 0; t < a.nblk; t++) {
+        const int64_t ntiles = (t >= 1 && ngroups > 0) ? a.nblk - t - 1 : 0;
+        // whole-group wavefronts while they give at least two per SIMD,
+        // else one column block per workgroup with the layers split
+        const int32_t split = ntiles * ngroups < kSplitBelow ? 1 : 0;
+        const int64_t nx = split ? ntiles : (ntiles + kTileWaves - 1) / kTileWaves;
+        k_sweep_step<LG><<<(unsigned)(1 + nx * ngroups), kSB * kTileWaves, 0, st>>>(
+            a, t, split, nx > 0 ? nx : 1);
+    }
+    return hipGetLastError();
+}
+
+bool sweep_ok(const SweepSolve& S) {
+    return S.I >= 2 && S.I <= 255 && S.H.p >= 2 && S.ld >= S.H.p && S.F && S.K;
+}
+
+}  // namespace
+
+size_t sweep_table_bytes(int64_t d, int32_t s) {
+    // F (fp64) and K (int32), rows 0..s of d entries each
+    return (size_t)(s + 1) * (size_t)d * (sizeof(double) + sizeof(int32_t));
+}
+
+hipError_t launch_sweep(const SweepSolve& S, int32_t exact_s, double* out, int32_t* chain,
+                        hipStream_t st) {
+    if (!sweep_ok(S) || !out) return hipErrorInvalidValue;
+    const SweepArgs a = make_args(S);
+    const int32_t L = a.I - 2;  // recursive layers 3..I
+    hipError_t e;
+    if (L <= 8)
+        e = sweep_launch<8>(a, st);
+    else if (L <= 16 || ECASQ_SWEEP_LG_MAX == 16)
+        e = sweep_launch<16>(a, st);
+    else
+        e = sweep_launch<32>(a, st);
+    if (e != hipSuccess) return e;
+    k_sweep_final<<<1, kSB, 0, st>>>(a, exact_s, out, chain);
+    return hipGetLastError();
+}
+
+hipError_t launch_sweep_accumulators(const SweepSolve& S, double* M, double* Ph, hipStream_t st) {
+    if (!sweep_ok(S) || !M || !Ph) return hipErrorInvalidValue;
+    const SweepArgs a = make_args(S);
+    for (int32_t i = 2; i <= a.I; i++) {
+        const int64_t n = a.H.p - (i - 1);
+        if (n <= 0) break;
+        k_sweep_acc<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(a, i, M, Ph);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace ecasq

@@ -32,6 +32,7 @@ class ecasq_options(ctypes.Structure):
         ("max_search_passes", ctypes.c_int32),
         ("recovery", ctypes.c_int32),
         ("search_width", ctypes.c_int32),
+        ("dp_schedule", ctypes.c_int32),
     ]
 
 
@@ -99,7 +100,8 @@ def lib():
     L.ecasq_status_string.argtypes = [i32]
     L.ecasq_status_string.restype = ctypes.c_char_p
     L.ecasq_histogram.argtypes = [vp, i32, i64, vp, vp, vp, vp, vp, P(i64)]
-    L.ecasq_dp_trace.argtypes = [vp, i32, i64, i32, i32, P(dbl), vp, vp, vp, vp, vp, P(dbl)]
+    L.ecasq_dp_trace.argtypes = [vp, i32, i64, i32, i32, P(dbl), i32, vp, vp, vp, vp, vp,
+                                 P(dbl)]
     L.ecasq_timing_enable.argtypes = [i32]
     L.ecasq_timing_enable.restype = None
     L.ecasq_timing_read.argtypes = [i32, P(dbl), P(i64), P(i64), i32]
@@ -242,7 +244,7 @@ def ecasq_histogram(x, stream=None):
     return tuple(b[: p.value] for b in bufs)
 
 
-def ecasq_dp_trace(x, s, lam, stream=None, accumulators=False):
+def ecasq_dp_trace(x, s, lam, stream=None, accumulators=False, schedule=0):
     """All layers of forward solves at one multiplier (lam a number) or at the
     8 multipliers of a search pass (lam a sequence of 8).  Returns F
     [nlam, s+1, d] fp64 (NaN where unset), kstar [nlam, s+1, d] int32 (-1
@@ -261,8 +263,8 @@ def ecasq_dp_trace(x, s, lam, stream=None, accumulators=False):
     Ph = torch.full(shape, float("nan"), dtype=torch.float64, device=x.device) if accumulators else None
     la = (ctypes.c_double * n)(*lams)
     out = (ctypes.c_double * (5 * n))()
-    st = lib().ecasq_dp_trace(_ptr(x), _DTYPES[x.dtype], d, int(s), n, la, _stream(stream),
-                              _ptr(F), _ptr(K), _ptr(M), _ptr(Ph), out)
+    st = lib().ecasq_dp_trace(_ptr(x), _DTYPES[x.dtype], d, int(s), n, la, int(schedule),
+                              _stream(stream), _ptr(F), _ptr(K), _ptr(M), _ptr(Ph), out)
     _raise(st)
     res = [tuple(out[5 * m:5 * m + 5]) for m in range(n)]
     if scalar:
@@ -276,6 +278,7 @@ def ecasq_timing_enable(on=True):
 
 TIMING_SINGLE = 0  # one multiplier per DP layer launch
 TIMING_PASS = 1    # the 8 multipliers of a search pass per launch
+TIMING_SWEEP = 2   # one whole solve of DP schedule 1
 
 
 def ecasq_timing_read(variant=TIMING_PASS, reset=False):

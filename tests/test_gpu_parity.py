@@ -21,6 +21,13 @@ pytestmark = pytest.mark.gpu
 
 REL = 1e-9
 
+# DP schedule 0 (layer by layer, O(d) space) with the search in passes of 8 and
+# Hirschberg recovery: the oracle's defaults.  The library's defaults are
+# schedule 1 (the column-block sweep) with the sequential search, whose
+# codebooks come from the argmin traceback.
+LAYERS = dict(dp_schedule=0, search_width=8)
+DEFAULT_ORACLE = dict(width=1, recovery="backpointers")
+
 
 def _say(*a):
     print("[case]", *a, flush=True)
@@ -110,13 +117,14 @@ def _dp_input(name, d):
     return (rng.integers(-40, 40, d) * 0.25).astype(np.float32)
 
 
+@pytest.mark.parametrize("schedule", [0, 1], ids=["layers", "sweep"])
 @pytest.mark.parametrize("name,d,s,lam", DP_CASES, ids=[c[0] for c in DP_CASES])
-def test_dp_layers_bit_exact(name, d, s, lam):
+def test_dp_layers_bit_exact(name, d, s, lam, schedule):
     x = _dp_input(name, d)
-    _say("dp_trace", name, d, s, lam)
-    F, K, _, _, out = ecasq.ecasq_dp_trace(_dev(x), s, lam)
-    F = F.cpu().numpy()
-    K = K.cpu().numpy()
+    _say("dp_trace", name, d, s, lam, "schedule", schedule)
+    F, K, M, Ph, out = ecasq.ecasq_dp_trace(_dev(x), s, lam, accumulators=True,
+                                            schedule=schedule)
+    F, K, M, Ph = (a.cpu().numpy() for a in (F, K, M, Ph))
     H = pipeline.prepare(x)
     p = H.p
     r = pipeline.dp_forward(H, s, lam * H.s2tot, backpointers=True, dump=True)
@@ -125,6 +133,7 @@ def test_dp_layers_bit_exact(name, d, s, lam):
         lo = i - 1
         np.testing.assert_array_equal(F[i, lo:p], r["F"][i, lo:p], err_msg=f"layer {i}")
         np.testing.assert_array_equal(K[i, lo:p], r["bp"][i, lo:p], err_msg=f"argmin layer {i}")
+        _check_accumulators(H, i, lam * H.s2tot, F, K, M, Ph, np.arange(lo, p))
     assert out[0] == r["J"] and out[1] == r["mse"] and out[2] == r["phi"]
     assert int(out[3]) == r["t"] and int(out[4]) == r["cells"]
 
@@ -185,6 +194,27 @@ def _sample_cols(rng, lo, p, n):
     extra = [lo, lo + 1, p - 2, p - 1, 255, 256, 511, 512, 513, p // 2]
     c = set(int(v) for v in rng.integers(lo, p, n)) | {v for v in extra if lo <= v < p}
     return np.array(sorted(c), dtype=np.int64)
+
+
+@pytest.mark.parametrize("workload,s,lam", [("weights_256k", 32, 0.1), ("student_t_1m", 64, 0.05)],
+                         ids=["weights_256k_s32", "student_t_1m_s64"])
+def test_full_size_sweep_sampled(workload, s, lam):
+    """Full-size inputs, DP schedule 1 (the column-block sweep) at one
+    multiplier: every layer checked bit for bit at sampled columns against the
+    oracle's recomputation from the GPU's previous layer."""
+    x = inputs.make(workload, seed=0)
+    _say("full-size sweep trace", workload, x.size, s, lam)
+    F, K, M, Ph, out = ecasq.ecasq_dp_trace(_dev(x), s, lam, accumulators=True, schedule=1)
+    F, K, M, Ph = (a.cpu().numpy() for a in (F, K, M, Ph))
+    _say("oracle prepare")
+    H = pipeline.prepare(x)
+    p = H.p
+    imax = min(s, p)
+    rng = np.random.default_rng(321)
+    for i in range(2, imax + 1):
+        cols = _sample_cols(rng, i - 1, p, 8)
+        _check_accumulators(H, i, lam * H.s2tot, F, K, M, Ph, cols)
+    _check_final(out, F, M, Ph, imax, p)
 
 
 @pytest.mark.parametrize("workload,s", [("weights_256k", 32), ("student_t_1m", 4)],
@@ -278,11 +308,60 @@ def test_solve_parity(case):
     name, wl, d, s, b, R, exh = case
     x = inputs.make(wl, seed=11, d=d)
     _say("solve", name, x.size, s, b, R, exh)
-    opts = ecasq.ecasq_default_options(refine_rounds=R, refine_exhaustive=exh)
+    opts = ecasq.ecasq_default_options(refine_rounds=R, refine_exhaustive=exh, **LAYERS)
     g = ecasq.ecasq_solve(_dev(x), s, b, options=opts)
     o = pipeline.solve(x, s, b, refine_rounds=R, exhaustive=bool(exh))
     _compare(g, o)
     assert g[2]["entropy"] <= b + 1e-12 or g[2]["status"] != 0
+
+
+SWEEP_CASES = [
+    ("normal_1k_w1", "normal_1k", None, 16, 2.0, 5, 1),
+    ("normal_1k_w8", "normal_1k", None, 16, 2.0, 0, 8),
+    ("lognormal_2k_b1.5_w1", "lognormal_16k", 2048, 32, 1.5, 5, 1),
+    ("weights_4k_b2_w1", "weights_256k", 4096, 16, 2.0, 5, 1),
+    ("student_2k_b0.7_w1", "student_t_1m", 2048, 16, 0.7, 5, 1),
+    ("normal_1k_b9_w1", "normal_1k", None, 16, 9.0, 5, 1),
+    ("normal_300_s200_w1", "normal_1k", 300, 200, 3.0, 3, 1),
+]
+
+
+@pytest.mark.parametrize("case", SWEEP_CASES, ids=[c[0] for c in SWEEP_CASES])
+def test_solve_parity_sweep(case):
+    """DP schedule 1: the codebook is the argmin traceback of the solve it was
+    found in, so the oracle recovers by backpointers."""
+    name, wl, d, s, b, R, w = case
+    x = inputs.make(wl, seed=11, d=d)
+    _say("solve sweep", name, x.size, s, b, R, w)
+    opts = ecasq.ecasq_default_options(refine_rounds=R, search_width=w, dp_schedule=1)
+    g = ecasq.ecasq_solve(_dev(x), s, b, options=opts)
+    o = pipeline.solve(x, s, b, refine_rounds=R, width=w, recovery="backpointers")
+    _compare(g, o)
+
+
+def test_lagrangian_and_degenerate_sweep():
+    x = inputs.lognormal_signed(1500, 21)
+    opts = ecasq.ecasq_default_options(refine_rounds=5, dp_schedule=1)
+    _say("lagrangian sweep")
+    g = ecasq.ecasq_solve_lagrangian(_dev(x), 20, 0.05, options=opts)
+    o = pipeline.solve_lagrangian(x, 20, 0.05, refine_rounds=5, recovery="backpointers")
+    _compare(g, o)
+    opts = ecasq.ecasq_default_options(dp_schedule=1, search_width=1)
+    cases = [
+        ("d1", np.array([3.0], dtype=np.float32), 4, 1.0),
+        ("all_equal", np.full(100, -7.0, dtype=np.float32), 4, 1.0),
+        ("two_values", np.array([1, 2, 1, 2, 2], dtype=np.float32), 4, 2.0),
+        ("two_values_infeasible", np.array([1, 2, 1, 2, 2], dtype=np.float32), 4, 0.5),
+        ("s_ge_p", np.arange(6, dtype=np.float32), 16, 8.0),
+        ("p_65", inputs.normal(65, 3), 5, 1.5),
+        ("low_budget_infeasible", inputs.normal(500, 2), 8, 0.05),
+        ("low_budget_feasible", inputs.normal(500, 2), 8, 0.6),
+    ]
+    for name, xx, s, b in cases:
+        _say("degenerate sweep", name)
+        g = ecasq.ecasq_solve(_dev(xx), s, b, options=opts)
+        o = pipeline.solve(xx, s, b, width=1, recovery="backpointers")
+        _compare(g, o)
 
 
 @pytest.mark.parametrize("name,d,s,b", [("lognormal_3k_b2", 3000, 24, 2.0),
@@ -291,7 +370,7 @@ def test_solve_parity_width1(name, d, s, b):
     """The sequential chord search (one multiplier per pass)."""
     x = inputs.lognormal_signed(d, 5)
     _say("solve width 1", name)
-    opts = ecasq.ecasq_default_options(search_width=1)
+    opts = ecasq.ecasq_default_options(search_width=1, dp_schedule=0)
     g = ecasq.ecasq_solve(_dev(x), s, b, options=opts)
     o = pipeline.solve(x, s, b, width=1)
     _compare(g, o)
@@ -301,7 +380,7 @@ def test_solve_parity_width1(name, d, s, b):
 def test_solve_lagrangian_parity(lam, R, exh):
     x = inputs.lognormal_signed(1500, 21)
     _say("lagrangian", lam, R, exh)
-    opts = ecasq.ecasq_default_options(refine_rounds=R, refine_exhaustive=exh)
+    opts = ecasq.ecasq_default_options(refine_rounds=R, refine_exhaustive=exh, dp_schedule=0)
     g = ecasq.ecasq_solve_lagrangian(_dev(x), 20, lam, options=opts)
     o = pipeline.solve_lagrangian(x, 20, lam, refine_rounds=R, exhaustive=bool(exh))
     _compare(g, o)
@@ -310,21 +389,25 @@ def test_solve_lagrangian_parity(lam, R, exh):
 def test_backpointer_recovery_matches_hirschberg():
     x = inputs.normal(2500, 31)
     _say("recovery modes")
-    a = ecasq.ecasq_solve(_dev(x), 24, 2.5, options=ecasq.ecasq_default_options(recovery=0))
-    b = ecasq.ecasq_solve(_dev(x), 24, 2.5, options=ecasq.ecasq_default_options(recovery=1))
+    a = ecasq.ecasq_solve(_dev(x), 24, 2.5, options=ecasq.ecasq_default_options(recovery=0,
+                                                                                **LAYERS))
+    b = ecasq.ecasq_solve(_dev(x), 24, 2.5, options=ecasq.ecasq_default_options(recovery=1,
+                                                                                **LAYERS))
+    c = ecasq.ecasq_solve(_dev(x), 24, 2.5)
     np.testing.assert_array_equal(a[1].cpu().numpy(), b[1].cpu().numpy())
+    np.testing.assert_array_equal(a[1].cpu().numpy(), c[1].cpu().numpy())
 
 
 def test_fp16_and_bf16_inputs():
     rows = inputs.make("kv_rows")[:4].reshape(-1)
     _say("fp16 solve")
     g = ecasq.ecasq_solve(_dev(rows), 16, 3.0)
-    o = pipeline.solve(rows.astype(np.float32), 16, 3.0)
+    o = pipeline.solve(rows.astype(np.float32), 16, 3.0, **DEFAULT_ORACLE)
     _compare(g, o)
     xb = torch.from_numpy(inputs.normal(700, 4)).to(torch.bfloat16)
     _say("bf16 solve")
     g = ecasq.ecasq_solve(xb.to("cuda"), 12, 2.0)
-    o = pipeline.solve(xb.to(torch.float32).numpy(), 12, 2.0)
+    o = pipeline.solve(xb.to(torch.float32).numpy(), 12, 2.0, **DEFAULT_ORACLE)
     _compare(g, o)
 
 
@@ -345,7 +428,7 @@ def test_degenerate_inputs():
     ]
     for name, x, s, b in cases:
         _say("degenerate", name)
-        g = ecasq.ecasq_solve(_dev(x), s, b)
+        g = ecasq.ecasq_solve(_dev(x), s, b, options=ecasq.ecasq_default_options(**LAYERS))
         o = pipeline.solve(x, s, b)
         _compare(g, o)
 
@@ -391,7 +474,7 @@ def test_quantize_solution_end_to_end():
     _say("solve + quantize")
     cb, rk, info = ecasq.ecasq_solve(_dev(x), 16, 2.0)
     sym, ent, hist = ecasq.ecasq_quantize(_dev(x), cb, 5)
-    o = pipeline.solve(x, 16, 2.0)
+    o = pipeline.solve(x, 16, 2.0, **DEFAULT_ORACLE)
     s_o, h_o, e_o = pipeline.quantize(x, o.codebook, 5)
     np.testing.assert_array_equal(sym.cpu().numpy(), s_o)
     assert _close(float(ent), e_o, 1e-12)
