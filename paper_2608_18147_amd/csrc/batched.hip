@@ -109,6 +109,153 @@ __device__ __forceinline__ Hist row_hist(const Row& R) {
     return H;
 }
 
+// eq. apx_final on R.last[2..imax] (lowest i, or imax for exactly min(s, p)
+// values), the chain traced back through argmin buffer `buf`, and its MSE and
+// H(I,B) summed in path order (the same additions as accumulating them along
+// the argmins).
+__device__ Pt row_final(Row& R, double lam, int imax, int exact_s, int buf) {
+    const int p = R.p, lane = R.lane, dp = R.dpad;
+    const int16_t* bp = R.bp[buf];
+    const Hist H = row_hist(R);
+    if (lane == 0) {
+        int bi = 2;
+        double bj = R.last[2];
+        for (int i = 3; i <= imax; i++) {
+            const double f = R.last[i];
+            if (exact_s ? (i == imax) : (f < bj)) {
+                bj = f;
+                bi = i;
+            }
+        }
+        int32_t* u = R.nu;  // scratch chain
+        u[bi - 1] = p - 1;
+        for (int i = bi; i >= 3; i--) u[i - 2] = bp[i * dp + u[i - 1]];
+        u[0] = 0;
+        double mse = 0.0, ph = 0.0;
+        for (int r = 0; r + 1 < bi; r++) {
+            double C, P;
+            cell_at(H, u[r], u[r + 1], R.tab, C, P);
+            mse = mse + C;
+            ph = ph - P;
+        }
+        R.misc[0] = mse;
+        R.misc[1] = ph;
+        R.misc[2] = (double)bi;
+    }
+    wave_sync();
+    Pt out;
+    out.lam = lam;
+    out.M = R.misc[0] / R.s2tot;
+    out.H = R.misc[1];
+    out.t = (int)R.misc[2];
+    out.buf = buf;
+    R.solves++;
+    wave_sync();
+    return out;
+}
+
+__device__ __forceinline__ double readlane_d(double x, int l) {
+    const int lo = __builtin_amdgcn_readlane(__double2loint(x), l);
+    const int hi = __builtin_amdgcn_readlane(__double2hiint(x), l);
+    return __hiloint2double(hi, lo);
+}
+
+// The same solve as a sweep over predecessors k = 0..p-2 in increasing order
+// that updates every layer of every later column from each cell, so C and Phi
+// of a cell are evaluated once instead of once per layer.  Column k is final
+// when the sweep reaches it (all its predecessors are behind); its layer
+// values are broadcast from the lane that holds them.  LG >= imax - 2 layers
+// of CMAX columns per lane live in registers.
+template <int CMAX, int LG>
+__device__ Pt row_sweep(Row& R, double lam, int exact_s, int buf) {
+    const double lamp = lam * R.s2tot;
+    const int p = R.p, lane = R.lane, dp = R.dpad;
+    const int imax = R.s < p ? R.s : p;
+    int16_t* bp = R.bp[buf];
+    const Hist H = row_hist(R);
+    double cv[CMAX], cN[CMAX], cS[CMAX], cS2[CMAX], f2[CMAX];
+    double best[CMAX][LG];
+    int32_t bk[CMAX][LG];
+#pragma unroll
+    for (int c = 0; c < CMAX; c++) {
+        const int j = c * kWave + lane;
+        const int jj = j < p ? j : p - 1;
+        cv[c] = R.v[jj];
+        cN[c] = R.N[jj];
+        cS[c] = R.S[jj];
+        cS2[c] = R.S2[jj];
+        // layer 2 (eq. apx_base); +inf where j = 0 has no interval
+        f2[c] = __builtin_huge_val();
+        if (j >= 1 && j < p) {
+            double C, P;
+            cell_at(H, 0, j, R.tab, C, P);
+            f2[c] = __builtin_fma(-lamp, P, 0.0 + C);
+            bp[2 * dp + j] = 0;
+        }
+#pragma unroll
+        for (int l = 0; l < LG; l++) {
+            best[c][l] = __builtin_huge_val();
+            bk[c][l] = -1;
+        }
+    }
+    const double dd = R.dd;
+#pragma unroll
+    for (int ck = 0; ck < CMAX; ck++) {
+        if (ck * kWave > p - 2) break;
+        for (int kk = 0; kk < kWave; kk++) {
+            const int k = ck * kWave + kk;
+            if (k > p - 2) break;
+            // F_{i-1}[k] of every layer i = 3 + l, from the lane of column k
+            double Fk[LG];
+            Fk[0] = readlane_d(f2[ck], kk);
+#pragma unroll
+            for (int l = 1; l < LG; l++) Fk[l] = readlane_d(best[ck][l - 1], kk);
+            const double pv = R.v[k], pN = R.N[k], pS = R.S[k], pS2 = R.S2[k];
+#pragma unroll
+            for (int c = ck; c < CMAX; c++) {
+                if (c * kWave + kWave - 1 <= k) continue;  // whole segment at or below k
+                const int j = c * kWave + lane;
+                double C, P;
+                cell_terms(pv, pN, pS, pS2, cv[c], cN[c], cS[c], cS2[c], dd, false, 0.0, R.tab,
+                           C, P);
+                const bool ok = j > k;
+#pragma unroll
+                for (int l = 0; l < LG; l++) {
+                    const double cand = __builtin_fma(-lamp, P, Fk[l] + C);
+                    const bool lt = ok && cand < best[c][l];
+                    bk[c][l] = lt ? k : bk[c][l];
+                    best[c][l] = lt ? cand : best[c][l];
+                }
+            }
+        }
+    }
+    // argmins of every layer, and F_i[p-1] for eq. apx_final
+    const int cl = (p - 1) / kWave, ll = (p - 1) % kWave;
+#pragma unroll
+    for (int c = 0; c < CMAX; c++) {
+        const int j = c * kWave + lane;
+#pragma unroll
+        for (int l = 0; l < LG; l++) {
+            const int i = 3 + l;
+            if (i <= imax && j < p) bp[i * dp + j] = (int16_t)bk[c][l];
+        }
+        if (c == cl) {
+            const double l2 = readlane_d(f2[c], ll);
+            if (lane == 0) R.last[2] = l2;
+#pragma unroll
+            for (int l = 0; l < LG; l++) {
+                const double v = readlane_d(best[c][l], ll);
+                if (lane == 0 && 3 + l <= imax) R.last[3 + l] = v;
+            }
+        }
+    }
+    int64_t cells = p - 1;
+    for (int i = 3; i <= imax; i++) cells += (int64_t)(p - i + 1) * (p - i + 2) / 2;
+    R.cells += cells;
+    wave_sync();
+    return row_final(R, lam, imax, exact_s, buf);
+}
+
 // One dp_APX solve at lambda (vNMSE units) into argmin buffer `buf`; returns
 // the lowest i minimising F_i[p-1] and, along its path, MSE and H(I,B) summed
 // in path order (the same additions as accumulating them along the argmins).
@@ -180,42 +327,7 @@ __device__ Pt row_solve(Row& R, double lam, int exact_s, int buf) {
         Fp = Fc;
         Fc = t;
     }
-    // eq. apx_final, then the path's MSE and H(I,B) in path order
-    if (lane == 0) {
-        int bi = 2;
-        double bj = R.last[2];
-        for (int i = 3; i <= imax; i++) {
-            const double f = R.last[i];
-            if (exact_s ? (i == imax) : (f < bj)) {
-                bj = f;
-                bi = i;
-            }
-        }
-        int32_t* u = R.nu;  // scratch chain
-        u[bi - 1] = p - 1;
-        for (int i = bi; i >= 3; i--) u[i - 2] = bp[i * dp + u[i - 1]];
-        u[0] = 0;
-        double mse = 0.0, ph = 0.0;
-        for (int r = 0; r + 1 < bi; r++) {
-            double C, P;
-            cell_at(H, u[r], u[r + 1], R.tab, C, P);
-            mse = mse + C;
-            ph = ph - P;
-        }
-        R.misc[0] = mse;
-        R.misc[1] = ph;
-        R.misc[2] = (double)bi;
-    }
-    wave_sync();
-    Pt out;
-    out.lam = lam;
-    out.M = R.misc[0] / R.s2tot;
-    out.H = R.misc[1];
-    out.t = (int)R.misc[2];
-    out.buf = buf;
-    R.solves++;
-    wave_sync();
-    return out;
+    return row_final(R, lam, imax, exact_s, buf);
 }
 
 // Sec. 6 refinement of the chain in R.chain (t values), one wavefront.
@@ -307,7 +419,17 @@ __device__ __forceinline__ uint32_t load_bits(const void* x, int64_t i) {
     return ((uint32_t)reinterpret_cast<const uint16_t*>(x)[i]) << 16;
 }
 
-template <int DT, int CMAX>
+// LG > 0: DP solves by row_sweep with LG layers in registers; LG = 0: by
+// row_solve, layer by layer.
+template <int CMAX, int LG>
+__device__ __forceinline__ Pt solve_row(Row& R, double lam, int exact_s, int buf) {
+    if constexpr (LG > 0)
+        return row_sweep<CMAX, LG>(R, lam, exact_s, buf);
+    else
+        return row_solve<CMAX>(R, lam, exact_s, buf);
+}
+
+template <int DT, int CMAX, int LG>
 __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
     extern __shared__ __align__(16) char smem[];
     double2* tab = reinterpret_cast<double2*>(smem);
@@ -427,7 +549,7 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
             }
             if (q.H < Lo.H) Lo = q;
         };
-        Lo = row_solve<CMAX>(R, 0.0, A.exact_s, 0);
+        Lo = solve_row<CMAX, LG>(R, 0.0, A.exact_s, 0);
         add(Lo);
         int npass = 1;
         for (;;) {
@@ -455,7 +577,7 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
                     lamF = Bp.lam;
                     break;
                 }
-                add(row_solve<CMAX>(R, 0x1p40, A.exact_s, 1));
+                add(solve_row<CMAX, LG>(R, 0x1p40, A.exact_s, 1));
                 tried40 = true;
                 npass++;
                 continue;
@@ -463,7 +585,7 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
             const double lc = (Bp.M - Ap.M) / (Ap.H - Bp.H);
             lamF = closed ? lc : Bp.lam;
             if (!(lc > 0.0) || npass >= A.max_passes) break;
-            const Pt Cp = row_solve<CMAX>(R, lc, A.exact_s, Bp.buf == 0 ? 1 : 0);
+            const Pt Cp = solve_row<CMAX, LG>(R, lc, A.exact_s, Bp.buf == 0 ? 1 : 0);
             npass++;
             if ((Cp.H == Ap.H && Cp.M == Ap.M) || (Cp.H == Bp.H && Cp.M == Bp.M)) {
                 lamF = lc;
@@ -533,19 +655,32 @@ template <int DT>
 hipError_t launch_dt(const BatchArgs& A, int cmax, unsigned grid, unsigned threads, size_t lds,
                      hipStream_t st) {
     hipError_t e = hipSuccess;
-#define ECASQ_LAUNCH(C)                                                                     \
+#define ECASQ_LAUNCH(C, G)                                                                  \
     do {                                                                                     \
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_batched<DT, C>),           \
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_batched<DT, C, G>),        \
                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);      \
         if (e != hipSuccess) return e;                                                       \
-        k_batched<DT, C><<<grid, threads, lds, st>>>(A);                                     \
+        k_batched<DT, C, G><<<grid, threads, lds, st>>>(A);                                  \
+        return hipGetLastError();                                                            \
     } while (0)
-    if (cmax <= 1) ECASQ_LAUNCH(1);
-    else if (cmax <= 2) ECASQ_LAUNCH(2);
-    else if (cmax <= 4) ECASQ_LAUNCH(4);
-    else ECASQ_LAUNCH(8);
+    // the sweep while CMAX x LG register states per lane stay within 32
+    const int L = (A.s < A.dpad ? A.s : A.dpad) - 2;  // recursive layers, at most
+    if (cmax <= 1) {
+        if (L <= 8) ECASQ_LAUNCH(1, 8);
+        if (L <= 16) ECASQ_LAUNCH(1, 16);
+        ECASQ_LAUNCH(1, 32);
+    }
+    if (cmax <= 2) {
+        if (L <= 8) ECASQ_LAUNCH(2, 8);
+        if (L <= 16) ECASQ_LAUNCH(2, 16);
+        ECASQ_LAUNCH(2, 0);
+    }
+    if (cmax <= 4) {
+        if (L <= 8) ECASQ_LAUNCH(4, 8);
+        ECASQ_LAUNCH(4, 0);
+    }
+    ECASQ_LAUNCH(8, 0);
 #undef ECASQ_LAUNCH
-    return hipGetLastError();
 }
 
 }  // namespace

@@ -139,14 +139,34 @@ __device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int64_t k0, i
                                            double cN, double cS, double cS2, double dd,
                                            double lamp, double (&best)[LW],
                                            int32_t (&bk)[LW]) {
-    for (int kk = 0; kk < kSB; kk++) {
-        double C, P;
+    if constexpr (LW > 8) {
+        // many layers per predecessor: enough independent work per iteration
+        for (int kk = 0; kk < kSB; kk++) {
+            double C, P;
+            cell_terms(sm.sv[kk], sm.sN[kk], sm.sS[kk], sm.sS2[kk], cv, cN, cS, cS2, dd, false,
+                       0.0, sm.tab, C, P);
+            const int32_t k = (int32_t)(k0 + kk);
+#pragma unroll
+            for (int l = 0; l < LW; l++)
+                take_min(__builtin_fma(-lamp, P, sm.sF[kk][lofs + l] + C), k, best[l], bk[l]);
+        }
+    } else {
+    // few layers: two predecessors per iteration, whose C and Phi are
+    // independent chains the scheduler can interleave; updates keep k order
+    for (int kk = 0; kk < kSB; kk += 2) {
+        double C0, P0, C1, P1;
         cell_terms(sm.sv[kk], sm.sN[kk], sm.sS[kk], sm.sS2[kk], cv, cN, cS, cS2, dd, false, 0.0,
-                   sm.tab, C, P);
+                   sm.tab, C0, P0);
+        cell_terms(sm.sv[kk + 1], sm.sN[kk + 1], sm.sS[kk + 1], sm.sS2[kk + 1], cv, cN, cS, cS2,
+                   dd, false, 0.0, sm.tab, C1, P1);
         const int32_t k = (int32_t)(k0 + kk);
 #pragma unroll
-        for (int l = 0; l < LW; l++)
-            take_min(__builtin_fma(-lamp, P, sm.sF[kk][lofs + l] + C), k, best[l], bk[l]);
+        for (int l = 0; l < LW; l++) {
+            take_min(__builtin_fma(-lamp, P0, sm.sF[kk][lofs + l] + C0), k, best[l], bk[l]);
+            take_min(__builtin_fma(-lamp, P1, sm.sF[kk + 1][lofs + l] + C1), k + 1, best[l],
+                     bk[l]);
+        }
+    }
     }
 }
 
@@ -253,34 +273,58 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
             __syncthreads();
             accumulate<LG, LW>(sm, k0, wave * LW, cv, cN, cS, cS2, dd, lamp, best, bk);
         }
+        // layer l = ow * LW + q of the group: held by wavefront ow at q
+#pragma unroll 1
+        for (int ow = 0; ow < kTileWaves; ow++) {
 #pragma unroll
-        for (int l = 0; l < LG; l++) {
-            const int32_t i = i0 + l;
+        for (int q8 = 0; q8 < LW; q8++) {
+            const int32_t i = i0 + ow * LW + q8;
             if (i > a.I) break;
-            double pv = __builtin_huge_val();
-            int32_t pk = -1;
+            // this wavefront's 16 candidates as 4 running minima over
+            // consecutive k (short dependency chains), then combined as a
+            // tree whose left operand always holds the lower k
+            double cv4[4];
+            int32_t ck4[4];
 #pragma unroll
-            for (int q = 0; q < KW; q++) {
-                const int kk = wave * KW + q;
-                const int64_t k = j0 + kk;
-                const double cand = __builtin_fma(-lamp, cP[q], sm.pF[kk] + cC[q]);
-                const bool lt = k < j && cand < pv;
-                pk = lt ? (int32_t)k : pk;
-                pv = lt ? cand : pv;
-            }
-            sm.partV[wave][lane] = pv;
-            sm.partK[wave][lane] = pk;
-            __syncthreads();
-            if (wave == l / LW) {
-                double b = best[l % LW];
-                int32_t kb = bk[l % LW];
+            for (int c = 0; c < 4; c++) {
+                cv4[c] = __builtin_huge_val();
+                ck4[c] = -1;
 #pragma unroll
-                for (int w = 0; w < kTileWaves; w++) {
-                    const double v = sm.partV[w][lane];
-                    const int32_t kv = sm.partK[w][lane];
-                    kb = v < b ? kv : kb;
-                    b = v < b ? v : b;
+                for (int q = 4 * c; q < 4 * c + 4; q++) {
+                    const int kk = wave * KW + q;
+                    const int64_t k = j0 + kk;
+                    const double cand = __builtin_fma(-lamp, cP[q], sm.pF[kk] + cC[q]);
+                    const bool lt = k < j && cand < cv4[c];
+                    ck4[c] = lt ? (int32_t)k : ck4[c];
+                    cv4[c] = lt ? cand : cv4[c];
                 }
+            }
+            const bool ra = cv4[1] < cv4[0], rb = cv4[3] < cv4[2];
+            const double va = ra ? cv4[1] : cv4[0], vb = rb ? cv4[3] : cv4[2];
+            const int32_t ka = ra ? ck4[1] : ck4[0], kb4 = rb ? ck4[3] : ck4[2];
+            const bool rab = vb < va;
+            const double cv16[1] = {rab ? vb : va};
+            const int32_t ck16[1] = {rab ? kb4 : ka};
+            sm.partV[wave][lane] = cv16[0];
+            sm.partK[wave][lane] = ck16[0];
+            __syncthreads();
+            if (wave == ow) {
+                // partials of waves 0,1 and 2,3, then the two, then after the
+                // running minimum (whose k lie in earlier blocks)
+                const double v0 = sm.partV[0][lane], v1 = sm.partV[1][lane];
+                const double v2 = sm.partV[2][lane], v3 = sm.partV[3][lane];
+                const int32_t k0_ = sm.partK[0][lane], k1_ = sm.partK[1][lane];
+                const int32_t k2_ = sm.partK[2][lane], k3_ = sm.partK[3][lane];
+                const bool r01 = v1 < v0, r23 = v3 < v2;
+                const double v01 = r01 ? v1 : v0, v23 = r23 ? v3 : v2;
+                const int32_t k01 = r01 ? k1_ : k0_, k23 = r23 ? k3_ : k2_;
+                const bool r = v23 < v01;
+                const double v = r ? v23 : v01;
+                const int32_t kv = r ? k23 : k01;
+                double b = best[q8];
+                int32_t kb = bk[q8];
+                kb = v < b ? kv : kb;
+                b = v < b ? v : b;
                 if (valid) {
                     a.F[(int64_t)i * a.ld + j] = b;
                     a.K[(int64_t)i * a.ld + j] = kb;
@@ -288,6 +332,7 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
                 sm.pF[lane] = valid ? b : __builtin_huge_val();
             }
             __syncthreads();
+        }
         }
     }
 }
