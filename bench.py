@@ -161,7 +161,12 @@ def main():
     ap.add_argument("--steps", type=int, default=2)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="weights_256k")
-    ap.add_argument("--budget", type=float, default=None)
+    ap.add_argument("--budget", type=float, default=None,
+                    help="one budget (default: the workload's first; with --all-budgets\n"
+                         "every budget of the workload is solved per step with shared solves)")
+    ap.add_argument("--all-budgets", action="store_true")
+    ap.add_argument("--progress", action="store_true",
+                    help="print a line per DP solve (stderr)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-sample", type=int, default=32768)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -211,11 +216,28 @@ def main():
         opts = ecasq.ecasq_default_options()
     sweep = opts.dp_schedule == 1
 
-    def step():
-        cb, rk, info = ecasq.ecasq_solve(xd, s, b, options=opts)
-        sym, ent, hist = ecasq.ecasq_quantize(xd, cb, args.seed)
-        return info, ent
+    budgets = list(w["budgets"]) if args.all_budgets else [b]
 
+    def step():
+        if len(budgets) == 1:
+            cb, rk, info = ecasq.ecasq_solve(xd, s, b, options=opts)
+            sym, ent, hist = ecasq.ecasq_quantize(xd, cb, args.seed)
+            return info, ent
+        res = ecasq.ecasq_solve_budgets(xd, s, budgets, options=opts)
+        agg = dict(res[-1][2])
+        agg["dp_solves"] = sum(r[2]["dp_solves"] for r in res)
+        agg["cells"] = sum(r[2]["cells"] for r in res)
+        agg["search_passes"] = sum(r[2]["search_passes"] for r in res)
+        agg["per_budget"] = []
+        for bb, (cb, rk, info) in zip(budgets, res):
+            sym, ent, hist = ecasq.ecasq_quantize(xd, cb, args.seed)
+            agg["per_budget"].append({"budget": bb, "t": info["t"], "vnmse": info["vnmse"],
+                                      "entropy": info["entropy"], "dp_solves": info["dp_solves"],
+                                      "empirical_entropy": float(ent)})
+        return agg, ent
+
+    # long steps (the 2^20 budget sweep) print a line per DP solve
+    ecasq.ecasq_timing_enable(args.progress, verbose=args.progress)
     for i in range(args.warmup):
         t0 = time.perf_counter()
         info, ent = step()
@@ -223,7 +245,7 @@ def main():
         log(f"warmup {i + 1}/{args.warmup}: {time.perf_counter() - t0:.2f} s, "
             f"{info['dp_solves']} DP solves, t={info['t']}")
 
-    ecasq.ecasq_timing_enable(True)
+    ecasq.ecasq_timing_enable(True, verbose=args.progress)
     for v in (ecasq.TIMING_SINGLE, ecasq.TIMING_PASS, ecasq.TIMING_SWEEP):
         ecasq.ecasq_timing_read(v, reset=True)
     infos = []
@@ -282,7 +304,8 @@ def main():
         "dtype": "f64",
         "data": "synthetic",
         "config": {
-            "workload": args.workload, "d": d, "s": s, "budget_bits": b, "seed": args.seed,
+            "workload": args.workload, "d": d, "s": s,
+            "budget_bits": budgets if len(budgets) > 1 else b, "seed": args.seed,
             "refine_rounds": 5, "input_dtype": "f32", "dp_schedule": opts.dp_schedule,
             "search_width": opts.search_width,
             "recovery": "argmin traceback" if sweep else "hirschberg",
@@ -296,6 +319,7 @@ def main():
         },
         "exact_cells_per_s": exact / elapsed,
         "dp_solves_per_step": info["dp_solves"],
+        **({"per_budget": info["per_budget"]} if "per_budget" in info else {}),
         "search_passes_per_step": info["search_passes"],
         "solution": {
             "t": info["t"], "p": info["p"], "lambda": info["lambda"], "vnmse": info["vnmse"],

@@ -136,6 +136,23 @@ ecasq_status ecasq_solve_ex(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
                             double *codebook, int32_t *codebook_rank, ecasq_info *info,
                             void *workspace, size_t workspace_bytes);
 
+/*
+ * Budget mode for nb budgets on one input, in the given order (as
+ * ecasq_solve_ex for each).  The histogram is built once and the searches share
+ * their DP solves: every solved multiplier's point (H(I,B), vNMSE and, under
+ * schedule 1, its codebook) joins a cache that later searches start from, and a
+ * multiplier already solved is not solved again.  Each search still returns
+ * the lowest-vNMSE supported point with H(I,B) <= b.  budgets: host, nb >= 1
+ * values.  codebooks: device, nb x s fp64 (row k holds infos[k].t values);
+ * codebook_ranks: device, nb x s int32, may be NULL; infos: host, nb entries,
+ * may be NULL (dp_solves, cells and search_passes count budget k's own new
+ * solves).  Returns ECASQ_EINFEASIBLE if any budget is infeasible (every row is
+ * still written); argument errors as ecasq_solve_ex.
+ */
+ecasq_status ecasq_solve_budgets(const void *x, ecasq_dtype dt, int64_t d, int32_t s, int32_t nb,
+                                 const double *budgets, const ecasq_options *opts, void *stream,
+                                 double *codebooks, int32_t *codebook_ranks, ecasq_info *infos);
+
 /* Fixed-multiplier mode: minimise vNMSE + lambda H(I,B) (lambda in vNMSE units,
  * Sec. 3), then refine vNMSE + lambda H(Xhat) without a budget guard. */
 ecasq_status ecasq_solve_lagrangian(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
@@ -221,7 +238,8 @@ ecasq_status ecasq_dp_trace(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
  * milliseconds, the number of timed launches and the (column, predecessor)
  * cells those launches evaluated, each cell for every multiplier of its
  * launch (host pointers, any may be NULL); reset != 0 clears that variant's
- * totals.  Not thread-safe.
+ * totals.  on = 2 also prints one line per DP solve to stderr (multiplier,
+ * H(I,B), vNMSE, values, elapsed time), for long runs.  Not thread-safe.
  */
 void ecasq_timing_enable(int32_t on);
 void ecasq_timing_read(int32_t variant, double *layer_ms, int64_t *layer_launches,

@@ -584,9 +584,15 @@ int orc_refine(const double *v, const double *N, const double *S, const double *
  *
  * Width 1 is the plain sequential chord search.  Returns B, the multiplier at
  * which B was found (used to recover it) and the final chord slope lc (the
- * multiplier of the refinement step).  A point's lambda is the multiplier of
- * its first query.
+ * multiplier of the refinement step).  A query whose lambda equals that of a
+ * point already solved reuses the point (no solve); a point's lambda is the
+ * multiplier of its first query.
  *
+ * cache (optional): points solved before, 4 doubles each (lambda, H(I,B),
+ * vNMSE, t), *ncache of them; they join the point set from the start (grid
+ * multipliers among them are not solved again), and the points this search
+ * solves are appended (up to cap).  Searches for several budgets on one input
+ * share their solves this way.
  * traj (optional, 4 doubles per solve): lambda, H(I,B), vNMSE, t.
  * out: lambda_B, H_B, M_B, t_B, solves, cells, status (0 ok, -3 infeasible),
  *      lambda_final, passes
@@ -601,7 +607,8 @@ typedef struct {
 
 int orc_search(const double *v, const double *N, const double *S, const double *S2, int64_t p,
                int64_t d, int32_t s, double b, int32_t exact_s, int32_t max_passes, int32_t width,
-               double *traj, int32_t traj_cap, double *out)
+               double *cache, int32_t *ncache, int32_t cache_cap, double *traj, int32_t traj_cap,
+               double *out)
 {
     if (width != 1 && width != SEARCH_M) return -1;
     hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
@@ -610,6 +617,14 @@ int orc_search(const double *v, const double *N, const double *S, const double *
     double cells = 0;
     point_t *pts = malloc(sizeof(point_t) * MAX_PTS);
     int32_t npts = 0;
+    if (cache && ncache) {
+        for (int32_t x = 0; x < *ncache && npts < MAX_PTS; x++) {
+            pts[npts].lam = cache[4 * x]; pts[npts].H = cache[4 * x + 1];
+            pts[npts].M = cache[4 * x + 2]; pts[npts].t = (int32_t)cache[4 * x + 3];
+            npts++;
+        }
+    }
+    int32_t ncached = npts;
     if (p <= 2) {
         /* every value is used; nothing to search */
         out[0] = 0.0; out[1] = 0.0; out[2] = 0.0; out[3] = (double)p; out[4] = 0; out[5] = 0;
@@ -624,26 +639,39 @@ int orc_search(const double *v, const double *N, const double *S, const double *
         free(pts);
         return 0;
     }
-    /* evaluate one multiplier (a full DP solve) */
+    /* evaluate one multiplier: reuse a solved point of the same lambda, else a
+       full DP solve */
 #define EVAL(lam_)                                                                            \
     do {                                                                                      \
         double l_ = (lam_);                                                                   \
-        orc_dp_forward(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, r, NULL, NULL, NULL);     \
-        if (npts < MAX_PTS) {                                                                 \
-            pts[npts].lam = l_; pts[npts].H = r[2]; pts[npts].M = r[1] / H.s2tot;            \
-            pts[npts].t = (int32_t)r[3]; npts++;                                               \
+        int hit_ = 0;                                                                         \
+        for (int x_ = 0; x_ < npts; x_++) if (pts[x_].lam == l_) { hit_ = 1; break; }          \
+        if (!hit_) {                                                                          \
+            orc_dp_forward(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, r, NULL, NULL, NULL); \
+            if (npts < MAX_PTS) {                                                             \
+                pts[npts].lam = l_; pts[npts].H = r[2]; pts[npts].M = r[1] / H.s2tot;        \
+                pts[npts].t = (int32_t)r[3]; npts++;                                           \
+            }                                                                                 \
+            cells += r[4];                                                                    \
+            if (traj && nsol < traj_cap) {                                                    \
+                traj[4 * nsol] = l_; traj[4 * nsol + 1] = r[2];                               \
+                traj[4 * nsol + 2] = r[1] / H.s2tot; traj[4 * nsol + 3] = r[3];               \
+            }                                                                                 \
+            nsol++;                                                                           \
         }                                                                                     \
-        cells += r[4];                                                                        \
-        if (traj && nsol < traj_cap) {                                                        \
-            traj[4 * nsol] = l_; traj[4 * nsol + 1] = r[2]; traj[4 * nsol + 2] = r[1] / H.s2tot; \
-            traj[4 * nsol + 3] = r[3];                                                        \
-        }                                                                                     \
-        nsol++;                                                                               \
+    } while (0)
+/* the point of a query (after EVAL) */
+#define POINT_OF(lam_, dst_)                                                                  \
+    do {                                                                                      \
+        for (int x_ = 0; x_ < npts; x_++) if (pts[x_].lam == (lam_)) { dst_ = pts[x_]; break; } \
     } while (0)
 
     static const double grid[SEARCH_M] = {0.0, 1e-4, 1e-3, 1e-2, 1e-1, 1.0, 10.0, 100.0};
-    for (int g = 0; g < width; g++) EVAL(grid[g]);
-    npass = 1;
+    {
+        int32_t before = nsol;
+        for (int g = 0; g < width; g++) EVAL(grid[g]);
+        npass = nsol > before ? 1 : 0;
+    }
     int32_t status = 0;
     point_t A, B;
     double lam_final = 0.0;
@@ -699,17 +727,25 @@ int orc_search(const double *v, const double *N, const double *S, const double *
                 q[g] = A.lam + ((B.lam - A.lam) * (double)g) / 8.0;
             }
         }
-        int first = npts;
         for (int g = 0; g < width; g++) EVAL(q[g]);
         npass++;
-        point_t Cq = pts[first];
+        point_t Cq = pts[0];
+        POINT_OF(q[0], Cq);
         if ((Cq.H == A.H && Cq.M == A.M) || (Cq.H == B.H && Cq.M == B.M)) {
             lam_final = lc;
             break;
         }
     }
 #undef EVAL
+#undef POINT_OF
     (void)have_B;
+    if (cache && ncache) {
+        for (int32_t x = ncached; x < npts && *ncache < cache_cap; x++) {
+            double *c = cache + 4 * (*ncache);
+            c[0] = pts[x].lam; c[1] = pts[x].H; c[2] = pts[x].M; c[3] = (double)pts[x].t;
+            (*ncache)++;
+        }
+    }
     out[0] = B.lam; out[1] = B.H; out[2] = B.M; out[3] = B.t; out[4] = nsol; out[5] = cells;
     out[6] = status; out[7] = lam_final; out[8] = npass;
     free(pts);

@@ -161,13 +161,28 @@ def refine(H, chain, lamp, b=math.inf, budget=False, rounds=5, exhaustive=False)
     return u, int(n), int(moves.value)
 
 
-def search(H, s, b, exact_s=False, max_passes=32, width=8):
-    """Budget search on lambda in passes of `width` (8 or 1) multipliers."""
+class LambdaCache:
+    """Points (lambda, H(I,B), vNMSE, t) solved on one input, shared by the
+    searches for several budgets."""
+
+    def __init__(self, cap=4096):
+        self.pts = np.zeros(4 * cap)
+        self.n = np.zeros(1, dtype=np.int32)
+        self.cap = cap
+
+
+def search(H, s, b, exact_s=False, max_passes=32, width=8, cache=None):
+    """Budget search on lambda in passes of `width` (8 or 1) multipliers; with
+    a LambdaCache, points solved by earlier searches are reused."""
     out = np.zeros(9)
     cap = 1024
     traj = np.zeros(4 * cap)
-    rc = native.lib().orc_search(*H.args(), s, b, int(exact_s), max_passes, width,
-                                 native.dptr(traj), cap, native.dptr(out))
+    if cache is not None:
+        cptr, nptr, ccap = native.dptr(cache.pts), native.iptr(cache.n), cache.cap
+    else:
+        cptr, nptr, ccap = None, None, 0
+    rc = native.lib().orc_search(*H.args(), s, b, int(exact_s), max_passes, width, cptr, nptr,
+                                 ccap, native.dptr(traj), cap, native.dptr(out))
     if rc != 0:
         raise ValueError("search width must be 1 or 8")
     n = int(out[4])
@@ -237,6 +252,28 @@ def solve(x, s, b, refine_rounds=5, exhaustive=False, exact_s=False, max_passes=
                 sr["traj"])
     r.passes = sr["passes"]
     return r
+
+
+def solve_budgets(x, s, budgets, refine_rounds=5, exhaustive=False, exact_s=False,
+                  max_passes=32, recovery="hirschberg", width=8):
+    """Budget mode for several budgets on one input, in the given order, the
+    searches sharing one LambdaCache.  Per budget as solve(); dp_solves and
+    cells count the solves that budget's search ran."""
+    H = prepare(x)
+    cache = LambdaCache()
+    res = []
+    for b in budgets:
+        sr = search(H, s, b, exact_s, max_passes, width, cache)
+        chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s)
+        lam = sr["lam_final"]
+        rounds = 0
+        if refine_rounds > 0 and math.isfinite(lam) and len(chain) >= 3:
+            chain, rounds, _ = refine(H, chain, lam * H.s2tot, b, True, refine_rounds, exhaustive)
+        r = _finish(H, chain, lam, sr["solves"], rounds, sr["cells"] + hcells, sr["status"],
+                    sr["traj"])
+        r.passes = sr["passes"]
+        res.append(r)
+    return res
 
 
 def solve_lagrangian(x, s, lam, refine_rounds=0, exhaustive=False, exact_s=False,

@@ -12,7 +12,9 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
+#include <cstdio>
 #include <cstring>
 #include <vector>
 
@@ -258,10 +260,23 @@ ecasq_status sweep_solve(Ctx& c, double lam, int32_t exact_s, Point& out, double
 ecasq_status dp_solve(Ctx& c, const double* lams, int32_t nlam, int32_t exact_s, Point* out,
                       double* J_out, const Dumps* dump) {
     if (nlam != 1 && nlam != kMaxLambdas) return ECASQ_EINVAL;
+    const auto t0 = std::chrono::steady_clock::now();
+    auto progress = [&](const Point* pts, int32_t n) {
+        if (!timing_verbose()) return;
+        const double ms =
+            std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t0)
+                .count();
+        for (int32_t m = 0; m < n; m++)
+            std::fprintf(stderr, "[ecasq] solve %d: lambda=%.6g H(I,B)=%.6f vNMSE=%.6g t=%d (%.1f ms)\n",
+                         c.solves - n + m + 1, pts[m].lam, pts[m].H, pts[m].M, pts[m].t, ms);
+        std::fflush(stderr);
+    };
     if (c.sweep) {
-        for (int32_t m = 0; m < nlam; m++)
+        for (int32_t m = 0; m < nlam; m++) {
             ECASQ_TRY(sweep_solve(c, lams[m], exact_s, out[m], J_out ? J_out + 4 * m : nullptr,
                                   dump, m));
+            progress(out + m, 1);
+        }
         return ECASQ_OK;
     }
     const int64_t p = c.p;
@@ -356,6 +371,7 @@ ecasq_status dp_solve(Ctx& c, const double* lams, int32_t nlam, int32_t exact_s,
     }
     if (J_out) std::memcpy(J_out, r, sizeof(double) * 4 * nlam);
     c.solves += nlam;
+    progress(out, nlam);
     return ECASQ_OK;
 }
 
@@ -375,16 +391,59 @@ struct SearchResult {
 // The budget search on lambda in passes of kMaxLambdas multipliers (the
 // schedule is stated in include/ecasq.h).  A point's lambda is that of its
 // first query; among points of equal lambda the first one wins.
+// Solve the multipliers of one pass that no point of `pts` already has (the
+// first occurrence of a repeated multiplier counts), appending the new points
+// to pts in query order; returns how many were solved.  Under the layer
+// schedule a partial pass of 2..7 is padded to 8 with repeats of its last
+// multiplier, and the padding is not counted.
+ecasq_status eval_pass(Ctx& c, const double* q, int32_t n, int32_t exact_s,
+                       std::vector<Point>& pts, int32_t& solved) {
+    double todo[kMaxLambdas];
+    int32_t m = 0;
+    for (int32_t g = 0; g < n; g++) {
+        bool seen = false;
+        for (const Point& x : pts)
+            if (x.lam == q[g]) seen = true;
+        for (int32_t h = 0; h < m; h++)
+            if (todo[h] == q[g]) seen = true;
+        if (!seen) todo[m++] = q[g];
+    }
+    solved = m;
+    if (m == 0) return ECASQ_OK;
+    Point out[kMaxLambdas];
+    if (c.sweep || m == 1) {
+        for (int32_t g = 0; g < m; g++) ECASQ_TRY(dp_solve(c, todo + g, 1, exact_s, out + g, nullptr, nullptr));
+    } else {
+        for (int32_t g = m; g < kMaxLambdas; g++) todo[g] = todo[m - 1];
+        const int64_t cells0 = c.cells;
+        const int32_t solves0 = c.solves;
+        ECASQ_TRY(dp_solve(c, todo, kMaxLambdas, exact_s, out, nullptr, nullptr));
+        c.cells = cells0 + (c.cells - cells0) / kMaxLambdas * m;
+        c.solves = solves0 + m;
+    }
+    pts.insert(pts.end(), out, out + m);
+    return ECASQ_OK;
+}
+
+const Point* point_at(const std::vector<Point>& pts, double lam) {
+    for (const Point& x : pts)
+        if (x.lam == lam) return &x;
+    return nullptr;
+}
+
+// cache (optional): points solved by earlier searches on the same input; they
+// join the point set from the start, and this search's new points are added.
 ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32_t width,
-                    SearchResult& R) {
+                    SearchResult& R, std::vector<Point>* cache = nullptr) {
     static const double kGrid[kMaxLambdas] = {0.0, 1e-4, 1e-3, 1e-2, 1e-1, 1.0, 10.0, 100.0};
     static const double kMul[kMaxLambdas - 1] = {0.25, 0.5, 0.75, 1.5, 2.0, 3.0, 4.0};
     if (width != 1 && width != kMaxLambdas) return ECASQ_EINVAL;
     std::vector<Point> pts;
-    Point q[kMaxLambdas];
-    ECASQ_TRY(dp_solve(c, kGrid, width, exact_s, q, nullptr, nullptr));
-    pts.insert(pts.end(), q, q + width);
-    int32_t npass = 1;
+    if (cache) pts = *cache;
+    const size_t ncached = pts.size();
+    int32_t solved = 0;
+    ECASQ_TRY(eval_pass(c, kGrid, width, exact_s, pts, solved));
+    int32_t npass = solved > 0 ? 1 : 0;
     R.status = ECASQ_OK;
     R.lam_final = 0.0;
     Point A, B;
@@ -442,9 +501,8 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
                 R.lam_final = B.lam;
                 break;
             }
-            Point big;
-            ECASQ_TRY(dp_solve1(c, 0x1p40, exact_s, big));
-            pts.push_back(big);
+            const double big = 0x1p40;
+            ECASQ_TRY(eval_pass(c, &big, 1, exact_s, pts, solved));
             npass++;
             continue;
         }
@@ -455,11 +513,9 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
         ql[0] = lc;
         for (int g = 1; g < width; g++)
             ql[g] = closed ? lc * kMul[g - 1] : A.lam + ((B.lam - A.lam) * (double)g) / 8.0;
-        const size_t first = pts.size();
-        ECASQ_TRY(dp_solve(c, ql, width, exact_s, q, nullptr, nullptr));
-        pts.insert(pts.end(), q, q + width);
+        ECASQ_TRY(eval_pass(c, ql, width, exact_s, pts, solved));
         npass++;
-        const Point& C = pts[first];
+        const Point C = *point_at(pts, lc);
         if ((C.H == A.H && C.M == A.M) || (C.H == B.H && C.M == B.M)) {
             R.lam_final = lc;
             break;
@@ -467,6 +523,7 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
     }
     R.B = B;
     R.passes = npass;
+    if (cache) cache->insert(cache->end(), pts.begin() + ncached, pts.end());
     return ECASQ_OK;
 }
 
@@ -684,6 +741,56 @@ ecasq_status solve_budget(const void* x, int dt, int64_t d, int32_t s, double b,
     return st;
 }
 
+ecasq_status solve_budgets(const void* x, int dt, int64_t d, int32_t s, int32_t nb,
+                           const double* budgets, const ecasq_options& o, void* stream,
+                           double* codebooks, int32_t* ranks, ecasq_info* infos) {
+    Ctx c;
+    ECASQ_TRY(ctx_open(c, d, s, ws_flags(o), stream, nullptr, 0));
+    struct Closer {
+        Ctx& c;
+        ~Closer() { ctx_close(c); }
+    } closer{c};
+    ECASQ_TRY(ctx_prep(c, x, dt));
+    std::vector<Point> cache;
+    ecasq_status worst = ECASQ_OK;
+    for (int32_t k = 0; k < nb; k++) {
+        const double b = budgets[k];
+        c.cells = 0;
+        c.solves = 0;
+        std::vector<int32_t> chain;
+        ecasq_status status = ECASQ_OK;
+        double lam = 0.0;
+        int32_t passes = 0;
+        if (c.p <= 2) {
+            for (int64_t q = 0; q < c.p; q++) chain.push_back((int32_t)q);
+        } else {
+            SearchResult R;
+            ECASQ_TRY(search(c, b, o.exact_s, o.max_search_passes, o.search_width, R, &cache));
+            status = R.status;
+            lam = R.lam_final;
+            passes = R.passes;
+            if (!R.B.chain.empty())
+                chain = R.B.chain;
+            else
+                ECASQ_TRY(recover(c, R.B.t, R.B.lam, o.exact_s, o.recovery, chain));
+        }
+        ecasq_info* info = infos ? infos + k : nullptr;
+        ecasq_info local;
+        if (!info) info = &local;
+        ecasq_status st = finish(c, chain, lam, b, true, o, codebooks + (int64_t)k * s,
+                                 ranks ? ranks + (int64_t)k * s : nullptr, info, status, passes);
+        if (c.p == 2 && info->entropy_surrogate > b) {
+            info->status = ECASQ_EINFEASIBLE;
+            st = ECASQ_EINFEASIBLE;
+        }
+        if (st == ECASQ_EINFEASIBLE)
+            worst = ECASQ_EINFEASIBLE;
+        else if (st != ECASQ_OK)
+            return st;
+    }
+    return worst;
+}
+
 }  // namespace
 
 extern "C" {
@@ -728,6 +835,18 @@ ecasq_status ecasq_solve(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
                          int32_t* codebook_rank, ecasq_info* info) {
     return ecasq_solve_ex(x, dt, d, s, bits_per_entry, nullptr, stream, codebook, codebook_rank,
                           info, nullptr, 0);
+}
+
+ecasq_status ecasq_solve_budgets(const void* x, ecasq_dtype dt, int64_t d, int32_t s, int32_t nb,
+                                 const double* budgets, const ecasq_options* opts, void* stream,
+                                 double* codebooks, int32_t* codebook_ranks, ecasq_info* infos) {
+    ECASQ_TRY(check_x(x, dt, d));
+    if (s < 2 || s > 255 || !codebooks || nb < 1 || !budgets) return ECASQ_EINVAL;
+    for (int32_t k = 0; k < nb; k++)
+        if (!(budgets[k] >= 0.0)) return ECASQ_EINVAL;  // also rejects NaN
+    const ecasq_options o = opts ? *opts : defaults();
+    if (!options_ok(o)) return ECASQ_EINVAL;
+    return solve_budgets(x, dt, d, s, nb, budgets, o, stream, codebooks, codebook_ranks, infos);
 }
 
 ecasq_status ecasq_solve_lagrangian(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
@@ -835,7 +954,7 @@ ecasq_status ecasq_dp_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
     return ECASQ_OK;
 }
 
-void ecasq_timing_enable(int32_t on) { timing_enable(on != 0); }
+void ecasq_timing_enable(int32_t on) { timing_enable(on == 2 ? 2 : (on != 0 ? 1 : 0)); }
 
 void ecasq_timing_read(int32_t variant, double* layer_ms, int64_t* layer_launches,
                        int64_t* layer_cells, int32_t reset) {

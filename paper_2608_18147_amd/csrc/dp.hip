@@ -438,6 +438,7 @@ struct TimingTotals {
     int64_t launches = 0, cells = 0;
 };
 bool g_timing = false;
+bool g_verbose = false;
 std::vector<TimedLaunch> g_pending;
 std::vector<hipEvent_t> g_pool;
 TimingTotals g_tot[3];
@@ -455,7 +456,12 @@ hipEvent_t take_event() {
 }
 }  // namespace
 
-void timing_enable(bool on) { g_timing = on; }
+void timing_enable(int mode) {
+    g_timing = mode != 0;
+    g_verbose = mode == 2;
+}
+
+bool timing_verbose() { return g_verbose; }
 
 void timing_flush() {
     for (auto& t : g_pending) {

@@ -69,7 +69,8 @@ struct DpInit {
     int32_t last_stride;
 };
 int64_t dp_partial_entries(int64_t p);
-void timing_enable(bool on);
+void timing_enable(int mode);  // 0 off, 1 timing, 2 timing + a stderr line per DP solve
+bool timing_verbose();
 void timing_flush();
 void timing_read(int variant, double* ms, int64_t* launches, int64_t* cells, bool reset);
 // bracket a span of launches on st as one timed unit of `variant` (2: a sweep solve)

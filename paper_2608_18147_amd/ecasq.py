@@ -71,6 +71,7 @@ EXPORTS = (
     "ecasq_default_options", "ecasq_solve", "ecasq_solve_ex", "ecasq_solve_lagrangian",
     "ecasq_quantize", "ecasq_solve_batched", "ecasq_workspace_size", "ecasq_status_string",
     "ecasq_histogram", "ecasq_dp_trace", "ecasq_timing_enable", "ecasq_timing_read",
+    "ecasq_solve_budgets",
 )
 
 
@@ -92,6 +93,8 @@ def lib():
                                  P(ecasq_info), vp, ctypes.c_size_t]
     L.ecasq_solve_lagrangian.argtypes = [vp, i32, i64, i32, dbl, P(ecasq_options), vp, vp, vp,
                                          P(ecasq_info)]
+    L.ecasq_solve_budgets.argtypes = [vp, i32, i64, i32, i32, P(dbl), P(ecasq_options), vp, vp,
+                                      vp, P(ecasq_info)]
     L.ecasq_quantize.argtypes = [vp, i32, i64, vp, i32, ctypes.c_uint64, vp, vp, vp, vp]
     L.ecasq_solve_batched.argtypes = [vp, i32, i64, i64, i32, dbl, P(ecasq_options), vp, vp,
                                       vp, vp]
@@ -107,7 +110,8 @@ def lib():
     L.ecasq_timing_read.argtypes = [i32, P(dbl), P(i64), P(i64), i32]
     L.ecasq_timing_read.restype = None
     for name in ("ecasq_solve", "ecasq_solve_ex", "ecasq_solve_lagrangian", "ecasq_quantize",
-                 "ecasq_solve_batched", "ecasq_histogram", "ecasq_dp_trace"):
+                 "ecasq_solve_batched", "ecasq_histogram", "ecasq_dp_trace",
+                 "ecasq_solve_budgets"):
         getattr(L, name).restype = i32
     _lib = L
     return L
@@ -175,6 +179,22 @@ def ecasq_solve(x, s, bits_per_entry, options=None, stream=None, workspace=None)
 
 
 ecasq_solve_ex = ecasq_solve
+
+
+def ecasq_solve_budgets(x, s, budgets, options=None, stream=None):
+    """Several budgets on one input with shared DP solves.  Returns a list of
+    (codebook fp64 [t], rank int32 [t], info dict), one per budget."""
+    x = _check_x(x)
+    nb = len(budgets)
+    cb = torch.empty((nb, int(s)), dtype=torch.float64, device=x.device)
+    rk = torch.empty((nb, int(s)), dtype=torch.int32, device=x.device)
+    infos = (ecasq_info * nb)()
+    o = options if options is not None else ecasq_default_options()
+    bs = (ctypes.c_double * nb)(*[float(b) for b in budgets])
+    st = lib().ecasq_solve_budgets(_ptr(x), _DTYPES[x.dtype], x.numel(), int(s), nb, bs,
+                                   ctypes.byref(o), _stream(stream), _ptr(cb), _ptr(rk), infos)
+    _raise(st, (ECASQ_OK, ECASQ_EINFEASIBLE))
+    return [(cb[k, :infos[k].t], rk[k, :infos[k].t], infos[k].as_dict()) for k in range(nb)]
 
 
 def ecasq_solve_lagrangian(x, s, lam, options=None, stream=None):
@@ -272,8 +292,8 @@ def ecasq_dp_trace(x, s, lam, stream=None, accumulators=False, schedule=0):
     return F, K, M, Ph, res
 
 
-def ecasq_timing_enable(on=True):
-    lib().ecasq_timing_enable(1 if on else 0)
+def ecasq_timing_enable(on=True, verbose=False):
+    lib().ecasq_timing_enable((2 if verbose else 1) if on else 0)
 
 
 TIMING_SINGLE = 0  # one multiplier per DP layer launch

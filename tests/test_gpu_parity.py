@@ -364,6 +364,25 @@ def test_lagrangian_and_degenerate_sweep():
         _compare(g, o)
 
 
+@pytest.mark.parametrize("schedule", [1, 0], ids=["sweep_w1", "layers_w8"])
+def test_solve_budgets_shared_cache(schedule):
+    """Several budgets on one input sharing DP solves (the budget sweep of the
+    2^20 workload, at a size the oracle runs in seconds)."""
+    x = inputs.student_t(3000, 6)
+    budgets = (1.0, 2.0, 3.0, 4.0)
+    _say("budget sweep", schedule)
+    if schedule == 1:
+        opts = ecasq.ecasq_default_options(refine_rounds=3)
+        orc = dict(width=1, recovery="backpointers")
+    else:
+        opts = ecasq.ecasq_default_options(refine_rounds=3, **LAYERS)
+        orc = dict(width=8, recovery="hirschberg")
+    g = ecasq.ecasq_solve_budgets(_dev(x), 16, budgets, options=opts)
+    o = pipeline.solve_budgets(x, 16, budgets, refine_rounds=3, **orc)
+    for gk, ok in zip(g, o):
+        _compare(gk, ok)
+
+
 @pytest.mark.parametrize("name,d,s,b", [("lognormal_3k_b2", 3000, 24, 2.0),
                                          ("lognormal_3k_b0.6", 3000, 12, 0.6)])
 def test_solve_parity_width1(name, d, s, b):

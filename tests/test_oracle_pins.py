@@ -361,6 +361,28 @@ def test_search_matches_dense_lambda_grid():
         assert found[0] == found[1]
 
 
+def test_budget_sweep_shares_solves():
+    """Several budgets on one input with a shared lambda cache: each budget's
+    codebook and metrics equal those of its own search (the search ends at the
+    same hull vertex however it starts), with fewer DP solves in total."""
+    x = inputs_student(1000, 4)
+    budgets = (1.0, 2.0, 3.0, 4.0)
+    for width in (1, 8):
+        shared = pipeline.solve_budgets(x, 12, budgets, refine_rounds=2, width=width)
+        alone = [pipeline.solve(x, 12, b, refine_rounds=2, width=width) for b in budgets]
+        for r, a in zip(shared, alone):
+            assert r.t == a.t and list(r.rank) == list(a.rank)
+            assert r.lam == a.lam and r.status == a.status
+            for k in ("mse", "entropy", "entropy_surrogate", "objective"):
+                assert getattr(r, k) == getattr(a, k)
+        assert sum(r.dp_solves for r in shared) < sum(a.dp_solves for a in alone)
+
+
+def inputs_student(d, seed):
+    rng = np.random.default_rng(seed)
+    return rng.standard_t(3, d).astype(np.float32)
+
+
 def test_dp_columns_match_full_layers():
     """The sampled-column recomputation (used to check full-size GPU layers)
     equals the full forward DP layer by layer, and its accumulators at the last
