@@ -108,6 +108,10 @@ void ecasq_default_options(ecasq_options *opts);
  *   pass is the chord slope lc = (M_B - M_A) / (H_A - H_B) followed, when
  *   w = 8, by A + (B - A) g / 8 for g = 1..7 (lc times 1/4, 1/2, 3/4, 3/2, 2,
  *   3, 4 when B is the two-value codebook);
+ *   with w = 1 the pass queries, instead of lc, the slope at H = b of the
+ *   curve through A and B on which log(vNMSE) is linear in H, while it lies
+ *   strictly between the two multipliers and such queries keep finding new
+ *   points;
  *   the search ends when the solve at lc returns A or B again, or after
  *   max_search_passes passes.
  * The codebook is B, recovered at the multiplier it was found at; the
@@ -178,8 +182,9 @@ ecasq_status ecasq_quantize(const void *x, ecasq_dtype dt, int64_t d, const doub
  * Many independent short vectors in one launch (one wavefront per row, several
  * rows per workgroup): x is n rows of d entries, row-major.  Each row is
  * solved as ecasq_solve_ex would with opts->recovery = 1 and
- * opts->search_width = 1 (argmins kept in LDS; both fields of opts are
- * ignored).  codebooks: device, n x s fp64 (row
+ * opts->search_width = 1, except that the search is the plain chord search
+ * (no query aimed at H = b: it runs on the device, whose log and exp are not
+ * those of the host) (argmins kept in LDS; those fields of opts are ignored).  codebooks: device, n x s fp64 (row
  * r's t_out[r] values first, the rest untouched); t_out: device, n int32
  * (0 for a row holding NaN/Inf); infos_dev: device, n ecasq_info, may be NULL
  * (per-row status: ECASQ_OK, ECASQ_EINFEASIBLE or ECASQ_ENONFINITE).

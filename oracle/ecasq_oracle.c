@@ -579,6 +579,12 @@ int orc_refine(const double *v, const double *N, const double *S, const double *
  *     next pass: lc and width-1 more multipliers, la + (lb - la) g / 8 for
  *     g = 1..7 (or lc times 1/4, 1/2, 3/4, 3/2, 2, 3, 4 when B is the
  *     two-value codebook);
+ *     width 1 with aim != 0 queries, instead of lc, the slope at H = b of the
+ *     curve through A and B on which log(vNMSE) is linear in H:
+ *       rho = (log M_B - log M_A) / (H_B - H_A),  M_b = M_A exp(rho (b - H_A)),
+ *       lq = -rho M_b,
+ *     when it lies strictly between la and lb and the previous such query found
+ *     a new point; otherwise it queries lc;
  *   stop when the answer at lc is A or B again (H and M bit for bit): no DP
  *   solution lies below the chord, A and B are adjacent supported points.
  *
@@ -607,8 +613,8 @@ typedef struct {
 
 int orc_search(const double *v, const double *N, const double *S, const double *S2, int64_t p,
                int64_t d, int32_t s, double b, int32_t exact_s, int32_t max_passes, int32_t width,
-               double *cache, int32_t *ncache, int32_t cache_cap, double *traj, int32_t traj_cap,
-               double *out)
+               int32_t aim, double *cache, int32_t *ncache, int32_t cache_cap, double *traj,
+               int32_t traj_cap, double *out)
 {
     if (width != 1 && width != SEARCH_M) return -1;
     hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
@@ -675,7 +681,7 @@ int orc_search(const double *v, const double *N, const double *S, const double *
     int32_t status = 0;
     point_t A, B;
     double lam_final = 0.0;
-    int have_B = 0, closed = 0;
+    int have_B = 0, closed = 0, force_chord = 0;
     for (;;) {
         /* A: infeasible point of largest lambda; B: feasible point of smallest
            lambda (first occurrence wins among equal lambdas) */
@@ -719,6 +725,19 @@ int orc_search(const double *v, const double *N, const double *S, const double *
         if (!(lc > 0.0) || npass >= max_passes) break;
         double q[SEARCH_M];
         q[0] = lc;
+        /* width 1: aim at H = b first (the tangent slope at b of the curve
+           through A and B on which log M is linear in H) while that finds new
+           points; the chord query certifies the end */
+        int model = 0;
+        if (width == 1 && aim && !force_chord && A.M > 0.0 && B.M > 0.0) {
+            double rho = (log(B.M) - log(A.M)) / (B.H - A.H);
+            double mb = A.M * exp(rho * (b - A.H));
+            double lq = -rho * mb;
+            if (isfinite(lq) && lq > A.lam && lq < B.lam) {
+                q[0] = lq;
+                model = 1;
+            }
+        }
         for (int g = 1; g < width; g++) {
             if (closed) {
                 static const double mul[SEARCH_M - 1] = {0.25, 0.5, 0.75, 1.5, 2.0, 3.0, 4.0};
@@ -732,8 +751,13 @@ int orc_search(const double *v, const double *N, const double *S, const double *
         point_t Cq = pts[0];
         POINT_OF(q[0], Cq);
         if ((Cq.H == A.H && Cq.M == A.M) || (Cq.H == B.H && Cq.M == B.M)) {
-            lam_final = lc;
-            break;
+            if (!model) {
+                lam_final = lc;
+                break;
+            }
+            force_chord = 1; /* the aimed query found nothing new */
+        } else {
+            force_chord = 0;
         }
     }
 #undef EVAL

@@ -171,9 +171,11 @@ class LambdaCache:
         self.cap = cap
 
 
-def search(H, s, b, exact_s=False, max_passes=32, width=8, cache=None):
+def search(H, s, b, exact_s=False, max_passes=32, width=8, cache=None, aim=True):
     """Budget search on lambda in passes of `width` (8 or 1) multipliers; with
-    a LambdaCache, points solved by earlier searches are reused."""
+    a LambdaCache, points solved by earlier searches are reused.  aim: width-1
+    queries aimed at H = b before the certifying chord query (the batched row
+    solver runs the plain chord search: aim=False)."""
     out = np.zeros(9)
     cap = 1024
     traj = np.zeros(4 * cap)
@@ -181,8 +183,8 @@ def search(H, s, b, exact_s=False, max_passes=32, width=8, cache=None):
         cptr, nptr, ccap = native.dptr(cache.pts), native.iptr(cache.n), cache.cap
     else:
         cptr, nptr, ccap = None, None, 0
-    rc = native.lib().orc_search(*H.args(), s, b, int(exact_s), max_passes, width, cptr, nptr,
-                                 ccap, native.dptr(traj), cap, native.dptr(out))
+    rc = native.lib().orc_search(*H.args(), s, b, int(exact_s), max_passes, width, int(aim),
+                                 cptr, nptr, ccap, native.dptr(traj), cap, native.dptr(out))
     if rc != 0:
         raise ValueError("search width must be 1 or 8")
     n = int(out[4])
@@ -237,12 +239,12 @@ def _recover(H, t, lam, recovery="hirschberg", s=None, exact_s=False):
 
 
 def solve(x, s, b, refine_rounds=5, exhaustive=False, exact_s=False, max_passes=32,
-          recovery="hirschberg", width=8):
+          recovery="hirschberg", width=8, aim=True):
     """Budget mode: the lowest-MSE supported solution with H(I,B) <= b
     (recovered at the multiplier it was found at), then refinement at the
     final chord slope with the budget guard on H(Xhat)."""
     H = prepare(x)
-    sr = search(H, s, b, exact_s, max_passes, width)
+    sr = search(H, s, b, exact_s, max_passes, width, aim=aim)
     chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s)
     lam = sr["lam_final"]
     rounds = 0

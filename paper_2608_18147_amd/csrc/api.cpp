@@ -449,6 +449,7 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
     Point A, B;
     Point two;
     bool have_two = false;
+    bool force_chord = false;
     for (;;) {
         int ia = -1, ib = -1;
         for (int x = 0; x < (int)pts.size(); x++) {
@@ -511,14 +512,31 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
         if (!(lc > 0.0) || npass >= max_passes) break;
         double ql[kMaxLambdas];
         ql[0] = lc;
+        // width 1: the slope at H = b of the curve through A and B with log M
+        // linear in H, while such queries find new points; the chord certifies
+        bool model = false;
+        if (width == 1 && !force_chord && A.M > 0.0 && B.M > 0.0) {
+            const double rho = (std::log(B.M) - std::log(A.M)) / (B.H - A.H);
+            const double mb = A.M * std::exp(rho * (b - A.H));
+            const double lq = -rho * mb;
+            if (std::isfinite(lq) && lq > A.lam && lq < B.lam) {
+                ql[0] = lq;
+                model = true;
+            }
+        }
         for (int g = 1; g < width; g++)
             ql[g] = closed ? lc * kMul[g - 1] : A.lam + ((B.lam - A.lam) * (double)g) / 8.0;
         ECASQ_TRY(eval_pass(c, ql, width, exact_s, pts, solved));
         npass++;
-        const Point C = *point_at(pts, lc);
+        const Point C = *point_at(pts, ql[0]);
         if ((C.H == A.H && C.M == A.M) || (C.H == B.H && C.M == B.M)) {
-            R.lam_final = lc;
-            break;
+            if (!model) {
+                R.lam_final = lc;
+                break;
+            }
+            force_chord = true;  // the aimed query found nothing new
+        } else {
+            force_chord = false;
         }
     }
     R.B = B;

@@ -526,7 +526,7 @@ def test_batched_rows_parity(R, exh):
     infos = ecasq.infos_to_dicts(infos)
     for r in range(rows.shape[0]):
         o = pipeline.solve(rows[r].astype(np.float32), 16, 3.0, refine_rounds=R,
-                           exhaustive=bool(exh), recovery="backpointers", width=1)
+                           exhaustive=bool(exh), recovery="backpointers", width=1, aim=False)
         _compare_row(cbs[r], int(tt[r]), infos[r], o, 16)
 
 
@@ -547,7 +547,7 @@ def test_batched_shapes_and_edge_rows():
         cbs, tt = cbs.cpu().numpy(), tt.cpu().numpy()
         infos = ecasq.infos_to_dicts(infos)
         for r in range(xb.shape[0]):
-            o = pipeline.solve(xb[r], s, b, recovery="backpointers", width=1)
+            o = pipeline.solve(xb[r], s, b, recovery="backpointers", width=1, aim=False)
             _compare_row(cbs[r], int(tt[r]), infos[r], o, s)
 
 
@@ -559,7 +559,7 @@ def test_batched_nonfinite_row_is_flagged():
     infos = ecasq.infos_to_dicts(infos)
     assert infos[1]["status"] == ecasq.ECASQ_ENONFINITE and int(tt[1]) == 0
     for r in (0, 2):
-        o = pipeline.solve(x[r], 8, 2.0, recovery="backpointers", width=1)
+        o = pipeline.solve(x[r], 8, 2.0, recovery="backpointers", width=1, aim=False)
         _compare_row(cbs[r].cpu().numpy(), int(tt[r]), infos[r], o, 8)
 
 
@@ -579,5 +579,5 @@ def test_batched_full_kv_workload_sampled():
         assert np.all(np.diff(cbs[r, :t]) > 0)
         assert infos[r]["status"] == 0 and infos[r]["entropy"] <= 3.0 + 1e-12
     for r in np.random.default_rng(0).choice(rows.shape[0], 64, replace=False):
-        o = pipeline.solve(r32[r], 16, 3.0, recovery="backpointers", width=1)
+        o = pipeline.solve(r32[r], 16, 3.0, recovery="backpointers", width=1, aim=False)
         _compare_row(cbs[r], int(tt[r]), infos[r], o, 16)
