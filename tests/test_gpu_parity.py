@@ -364,6 +364,37 @@ def test_lagrangian_and_degenerate_sweep():
         _compare(g, o)
 
 
+def test_sweep_options_and_edges():
+    """DP schedule 1 with exactly s values, s = 2 (layer 2 only), s >= p,
+    half-precision inputs, exhaustive refinement and the recovery option (which
+    the sweep ignores)."""
+    x = inputs.lognormal_signed(1800, 13)
+    cases = [
+        ("exact_s", x, 12, 2.0, dict(exact_s=1), dict(exact_s=True)),
+        ("s2", x, 2, 1.0, {}, {}),
+        ("s3", x, 3, 1.5, {}, {}),
+        ("s_ge_p", inputs.normal(40, 2), 64, 3.0, {}, {}),
+        ("exhaustive", x, 16, 2.5, dict(refine_exhaustive=1), dict(exhaustive=True)),
+        ("recovery_ignored", x, 16, 2.5, dict(recovery=1), {}),
+    ]
+    for name, xx, s_, b, gopt, oopt in cases:
+        _say("sweep edge", name)
+        opts = ecasq.ecasq_default_options(**gopt)
+        g = ecasq.ecasq_solve(_dev(xx), s_, b, options=opts)
+        o = pipeline.solve(xx, s_, b, **DEFAULT_ORACLE, **oopt)
+        _compare(g, o)
+    rows = inputs.make("kv_rows")[:6].reshape(-1)
+    _say("sweep fp16")
+    g = ecasq.ecasq_solve(_dev(rows), 16, 3.0)
+    o = pipeline.solve(rows.astype(np.float32), 16, 3.0, **DEFAULT_ORACLE)
+    _compare(g, o)
+    xb = torch.from_numpy(inputs.normal(900, 5)).to(torch.bfloat16)
+    _say("sweep bf16")
+    g = ecasq.ecasq_solve(xb.to("cuda"), 12, 2.0)
+    o = pipeline.solve(xb.to(torch.float32).numpy(), 12, 2.0, **DEFAULT_ORACLE)
+    _compare(g, o)
+
+
 @pytest.mark.parametrize("schedule", [1, 0], ids=["sweep_w1", "layers_w8"])
 def test_solve_budgets_shared_cache(schedule):
     """Several budgets on one input sharing DP solves (the budget sweep of the
