@@ -52,8 +52,8 @@ TRAFFIC_SOURCES_SHA = "f3a631b21f5b78fb"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
-SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 9.898e7
-SWEEP_TRAFFIC_SHA = "e39e1c1a98e7e2c0"
+SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 9.902e7
+SWEEP_TRAFFIC_SHA = "8c7a9db356a3e3ae"
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 
 

@@ -109,6 +109,12 @@ __device__ __forceinline__ Hist row_hist(const Row& R) {
     return H;
 }
 
+__device__ __forceinline__ double uniform_d(double x) {
+    const int lo = __builtin_amdgcn_readfirstlane(__double2loint(x));
+    const int hi = __builtin_amdgcn_readfirstlane(__double2hiint(x));
+    return __hiloint2double(hi, lo);
+}
+
 // eq. apx_final on R.last[2..imax] (lowest i, or imax for exactly min(s, p)
 // values), the chain traced back through argmin buffer `buf`, and its MSE and
 // H(I,B) summed in path order (the same additions as accumulating them along
@@ -143,11 +149,12 @@ __device__ Pt row_final(Row& R, double lam, int imax, int exact_s, int buf) {
         R.misc[2] = (double)bi;
     }
     wave_sync();
+    // the point is the same for every lane: keep it in scalar registers
     Pt out;
     out.lam = lam;
-    out.M = R.misc[0] / R.s2tot;
-    out.H = R.misc[1];
-    out.t = (int)R.misc[2];
+    out.M = uniform_d(R.misc[0]) / R.s2tot;
+    out.H = uniform_d(R.misc[1]);
+    out.t = (int)uniform_d(R.misc[2]);
     out.buf = buf;
     R.solves++;
     wave_sync();
@@ -630,23 +637,23 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
         }
         A.t_out[row] = t;
         if (A.infos) {
-            ecasq_info inf;
-            inf.t = t;
-            inf.p = nonfinite ? 0 : p;
-            inf.lambda = lamF;
-            inf.mse = mse;
-            inf.vnmse = vn;
-            inf.entropy = ho;
-            inf.entropy_surrogate = hs;
+            // field by field (no stack copy of the struct)
+            ecasq_info* inf = A.infos + row;
+            inf->t = t;
+            inf->p = nonfinite ? 0 : p;
+            inf->lambda = lamF;
+            inf->mse = mse;
+            inf->vnmse = vn;
+            inf->entropy = ho;
+            inf->entropy_surrogate = hs;
             const double lr = __builtin_isfinite(lamF) ? lamF : 0.0;
-            inf.objective = __builtin_fma(lr, ho, vn);
-            inf.rate_total = ho + (32.0 * (double)t) / R.dd;
-            inf.dp_solves = R.solves;
-            inf.refine_rounds_run = rounds_run;
-            inf.cells = R.cells;
-            inf.status = status;
-            inf.search_passes = passes;
-            A.infos[row] = inf;
+            inf->objective = __builtin_fma(lr, ho, vn);
+            inf->rate_total = ho + (32.0 * (double)t) / R.dd;
+            inf->dp_solves = R.solves;
+            inf->refine_rounds_run = rounds_run;
+            inf->cells = R.cells;
+            inf->status = status;
+            inf->search_passes = passes;
         }
     }
 }
