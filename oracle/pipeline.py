@@ -83,10 +83,66 @@ class Hist:
                 native.dptr(self.S2), self.p, self.d)
 
 
-def prepare(x):
+def uniform_alphabet(v, m):
+    """m permissible values evenly spaced over [min X, max X] (App. D with
+    P != X; App. F.7 'uniform min-max grid'): p_0 = min X, p_{m-1} = max X,
+    p_k = min X + k * ((max X - min X) / (m - 1)) in between, each operation
+    rounded to nearest; values that round onto their predecessor are dropped."""
+    lo, hi = float(v[0]), float(v[-1])
+    if len(v) == 1:
+        return np.array([lo])
+    step = (hi - lo) / float(m - 1)
+    P = [lo]
+    for k in range(1, m - 1):
+        q = lo + float(k) * step
+        if q > P[-1] and q < hi:
+            P.append(q)
+    P.append(hi)
+    return np.array(P)
+
+
+def quantile_alphabet(v, c, m):
+    """m permissible values at the ranks floor(k (d - 1) / (m - 1)) of the
+    sorted input (a quantile grid drawn from X, App. F.7), repeats dropped; the
+    first and last are min X and max X."""
+    d = int(np.sum(c))
+    cum = np.cumsum(c)
+    P = []
+    for k in range(m):
+        r = (k * (d - 1)) // (m - 1) if m > 1 else 0
+        i = int(np.searchsorted(cum, r, side="right"))  # first i with cum[i] > r
+        if not P or v[i] > P[-1]:
+            P.append(float(v[i]))
+    return np.array(P)
+
+
+def on_alphabet(v, c, N, S, S2, P):
+    """Prefix quantities of X at the permissible values: N(p), S(p), S2(p) are
+    the count, sum and sum of squares of the entries <= p (App. D), taken from
+    the exact prefix sums at the last input value <= p."""
+    idx = np.searchsorted(v, P, side="right") - 1
+    Nn = np.empty(len(P)); Sn = np.empty(len(P)); S2n = np.empty(len(P))
+    cn = np.empty(len(P), dtype=np.int64)
+    prev = 0
+    for k, i in enumerate(idx):
+        Nn[k], Sn[k], S2n[k] = N[i], S[i], S2[i]
+        cn[k] = int(N[i]) - prev
+        prev = int(N[i])
+    return cn, Nn, Sn, S2n
+
+
+def prepare(x, alphabet=None):
+    """Histogram with exact prefix sums over the permissible values: the
+    distinct input values (P = X), or a grid ('uniform', m) / ('quantile', m)."""
     v, c = histogram(x)
     N, S, S2 = exact_prefix(v, c)
-    return Hist(np.ascontiguousarray(v), c, N, S, S2, int(np.asarray(x).size))
+    d = int(np.asarray(x).size)
+    if alphabet is not None:
+        kind, m = alphabet
+        P = uniform_alphabet(v, m) if kind == "uniform" else quantile_alphabet(v, c, m)
+        c, N, S, S2 = on_alphabet(v, c, N, S, S2, P)
+        v = P
+    return Hist(np.ascontiguousarray(v), c, N, S, S2, d)
 
 
 def interval(H, a, b):
@@ -239,11 +295,11 @@ def _recover(H, t, lam, recovery="hirschberg", s=None, exact_s=False):
 
 
 def solve(x, s, b, refine_rounds=5, exhaustive=False, exact_s=False, max_passes=32,
-          recovery="hirschberg", width=8, aim=True):
+          recovery="hirschberg", width=8, aim=True, alphabet=None):
     """Budget mode: the lowest-MSE supported solution with H(I,B) <= b
     (recovered at the multiplier it was found at), then refinement at the
     final chord slope with the budget guard on H(Xhat)."""
-    H = prepare(x)
+    H = prepare(x, alphabet)
     sr = search(H, s, b, exact_s, max_passes, width, aim=aim)
     chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s)
     lam = sr["lam_final"]
@@ -257,15 +313,15 @@ def solve(x, s, b, refine_rounds=5, exhaustive=False, exact_s=False, max_passes=
 
 
 def solve_budgets(x, s, budgets, refine_rounds=5, exhaustive=False, exact_s=False,
-                  max_passes=32, recovery="hirschberg", width=8):
+                  max_passes=32, recovery="hirschberg", width=8, aim=True, alphabet=None):
     """Budget mode for several budgets on one input, in the given order, the
     searches sharing one LambdaCache.  Per budget as solve(); dp_solves and
     cells count the solves that budget's search ran."""
-    H = prepare(x)
+    H = prepare(x, alphabet)
     cache = LambdaCache()
     res = []
     for b in budgets:
-        sr = search(H, s, b, exact_s, max_passes, width, cache)
+        sr = search(H, s, b, exact_s, max_passes, width, cache, aim)
         chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s)
         lam = sr["lam_final"]
         rounds = 0
@@ -279,10 +335,10 @@ def solve_budgets(x, s, budgets, refine_rounds=5, exhaustive=False, exact_s=Fals
 
 
 def solve_lagrangian(x, s, lam, refine_rounds=0, exhaustive=False, exact_s=False,
-                     recovery="hirschberg"):
+                     recovery="hirschberg", alphabet=None):
     """Fixed-multiplier mode: min vNMSE + lambda H(I,B), then refinement on
     vNMSE + lambda H(Xhat) without a budget guard."""
-    H = prepare(x)
+    H = prepare(x, alphabet)
     if H.p == 1:
         return _finish(H, np.zeros(1, dtype=np.int32), lam, 0, 0, 0, 0)
     r = dp_forward(H, s, lam * H.s2tot, exact_s)

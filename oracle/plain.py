@@ -10,7 +10,8 @@ closed forms) from outside:
   * expected frequencies f_q and H(Xhat)            (Sec. 1 and Sec. 3)
   * the surrogate H(I,B) with its interval index I  (Sec. 5, incl. its footnote
     on x = q_1)
-  * brute force over every spanning Q drawn from the input values
+  * brute force over every spanning Q drawn from the input values or from a
+    permissible set P (App. D)
   * the classic ASQ DP, eq. (1)                     (Sec. 2)
   * the optimal DP over (l, j) states               (Sec. 4, App. D with L = {0},
                                                     R = {p-1})
@@ -114,10 +115,17 @@ def objective(x, Q, lam, which="out"):
     return float(vnmse(x, Q)) + lam * H
 
 
-def spanning_codebooks(x, s):
-    """Every Q drawn from the distinct input values with |Q| <= s that spans X
-    (contains min and max; P = X, Sec. 2 and Sec. 4)."""
-    v = sorted(set(float(a) for a in np.asarray(x, dtype=np.float64).ravel()))
+def spanning_codebooks(x, s, P=None):
+    """Every Q drawn from the permissible values P (default: the distinct input
+    values, P = X) with |Q| <= s that spans X: here P's first and last values
+    are min X and max X, which every Q then contains (Sec. 2 and Sec. 4;
+    App. D with L = {first}, R = {last})."""
+    if P is None:
+        v = sorted(set(float(a) for a in np.asarray(x, dtype=np.float64).ravel()))
+    else:
+        v = sorted(set(float(a) for a in P))
+        xf = np.asarray(x, dtype=np.float64)
+        assert v[0] == xf.min() and v[-1] == xf.max()
     if len(v) == 1:
         yield (v[0],)
         return
@@ -127,10 +135,11 @@ def spanning_codebooks(x, s):
             yield (v[0],) + comb + (v[-1],)
 
 
-def brute_force(x, s, lam, which="sur"):
-    """min over spanning Q of vNMSE + lambda * H.  Returns (J, Q)."""
+def brute_force(x, s, lam, which="sur", P=None):
+    """min over spanning Q (drawn from P, default X) of vNMSE + lambda * H.
+    Returns (J, Q)."""
     best = None
-    for Q in spanning_codebooks(x, s):
+    for Q in spanning_codebooks(x, s, P):
         J = objective(x, Q, lam, which)
         if best is None or J < best[0]:
             best = (J, Q)

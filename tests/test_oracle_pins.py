@@ -256,6 +256,59 @@ def test_apx_dp_equals_brute_force():
         assert abs(r["phi"] - m["entropy_surrogate"]) <= 1e-12
 
 
+def test_apx_dp_on_permissible_grids_equals_brute_force():
+    """App. D with P != X: on a uniform grid over [min X, max X] and on a
+    quantile grid, the DP over the grid's prefix quantities minimises
+    vNMSE + lambda H(I,B) over every spanning Q drawn from the grid."""
+    for x, s, lam in _tiny_inputs(60, 21):
+        for alphabet in (("uniform", 7), ("uniform", 3), ("quantile", 5)):
+            H = pipeline.prepare(x, alphabet)
+            if H.p < 2:
+                continue
+            assert H.v[0] == float(np.min(x)) and H.v[-1] == float(np.max(x))
+            assert np.all(np.diff(H.v) > 0)
+            r = pipeline.dp_forward(H, s, lam * H.s2tot, backpointers=True)
+            Jb, _ = plain.brute_force(x, s, lam, "sur", P=list(H.v))
+            assert abs(r["J"] / H.s2tot - Jb) <= 1e-12 * max(1.0, Jb), alphabet
+            m = pipeline.chain_metrics(H, r["chain_bp"], lam)
+            assert abs(m["vnmse"] + lam * m["entropy_surrogate"] - Jb) <= 1e-12 * max(1.0, Jb)
+            # expected output frequencies from the grid's prefix quantities
+            Q = [float(H.v[k]) for k in r["chain_bp"]]
+            assert abs(m["entropy"] - plain.entropy_out(x, Q)) <= 1e-12
+
+
+def test_permissible_grids():
+    """Grid construction: endpoints min X and max X, strictly increasing, the
+    uniform grid's interior points min X + k step, the quantile grid drawn from
+    X at ranks floor(k (d - 1) / (m - 1)); prefix counts and sums at the grid
+    points equal the plain counts and sums of the entries <= p."""
+    rng = np.random.default_rng(22)
+    x = np.round(rng.standard_normal(500) * 4).astype(np.float32) / np.float32(4)
+    xs = np.sort(x.astype(np.float64))
+    Hu = pipeline.prepare(x, ("uniform", 11))
+    step = (xs[-1] - xs[0]) / 10.0
+    assert list(Hu.v) == [xs[0]] + [xs[0] + k * step for k in range(1, 10)] + [xs[-1]]
+    Hq = pipeline.prepare(x, ("quantile", 9))
+    want = []
+    for k in range(9):
+        q = xs[(k * 499) // 8]
+        if not want or q > want[-1]:
+            want.append(q)
+    assert list(Hq.v) == want
+    for H in (Hu, Hq):
+        for k, pk in enumerate(H.v):
+            sel = xs[xs <= pk]
+            assert H.N[k] == len(sel)
+            assert abs(H.S[k] - math.fsum(sel)) <= 1e-12 * max(1.0, abs(math.fsum(sel)))
+            assert abs(H.S2[k] - math.fsum(sel * sel)) <= 1e-12 * math.fsum(sel * sel)
+    # a grid finer than the data's spacing (fp64 has 29 more bits than the
+    # fp32 data, so its points stay distinct)
+    y = np.array([1.0, 1.0 + 2.0 ** -23], dtype=np.float32)
+    Hy = pipeline.prepare(y, ("uniform", 1000))
+    assert len(Hy.v) == 1000 and np.all(np.diff(Hy.v) > 0) and Hy.v[-1] == np.float64(y[1])
+    assert list(Hy.N) == [1.0] * 999 + [2.0]
+
+
 def test_optimal_dp_equals_brute_force_and_sandwich():
     """Sec. 4 optimal DP = brute-force min of vNMSE + lambda H(Xhat); and
     J_opt <= J_apx <= J_opt + lambda (from H(Xhat) <= H(I,B) <= H(Xhat)+1)."""
