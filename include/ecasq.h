@@ -65,6 +65,11 @@ typedef struct {
     int32_t dp_schedule;       /* 1: column-block sweep over all layers at once, O(s d)
                                   space (default); 0: layer by layer, O(d) space (see
                                   ecasq_solve_ex) */
+    int32_t alphabet;          /* permissible values P (App. D): 0 the distinct input
+                                  values, P = X (default); 1 a uniform grid of
+                                  alphabet_size points over [min X, max X]; 2 the input
+                                  values at alphabet_size evenly spaced ranks */
+    int32_t alphabet_size;     /* grid points m, 2 <= m <= d (alphabet 1 and 2) */
 } ecasq_options;
 
 typedef struct {
@@ -126,6 +131,15 @@ ecasq_status ecasq_solve(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
  * opts->recovery == 1, plus 2 if opts->dp_schedule == 1; NULL = allocate
  * internally).
  *
+ * Permissible alphabets (App. D with P != X): with opts->alphabet = 1 the
+ * candidate values are p_0 = min X, p_k = min X + k ((max X - min X) / (m - 1))
+ * (each operation rounded to nearest) for 0 < k < m-1, p_{m-1} = max X; with
+ * opts->alphabet = 2 they are the input values at ranks floor(k (d-1) / (m-1))
+ * of the sorted input; points equal to their predecessor (or, uniform, not
+ * below max X) are dropped.  The interval quantities come from the input's
+ * prefix count, sum and sum of squares at the grid points, so the DP costs
+ * O(s p^2) in the grid size p <= m; codebook_rank indexes the grid.
+ *
  * DP schedules (both compute eq. apx_base / apx_rec / apx_final with the same
  * values and argmins bit for bit):
  *   0  layer by layer with two rolling layers of O(p) memory, as Sec. 5 states
@@ -182,7 +196,8 @@ ecasq_status ecasq_quantize(const void *x, ecasq_dtype dt, int64_t d, const doub
  * Many independent short vectors in one launch (one wavefront per row, several
  * rows per workgroup): x is n rows of d entries, row-major.  Each row is
  * solved as ecasq_solve_ex would with opts->recovery = 1 and
- * opts->search_width = 1, except that the search is the plain chord search
+ * opts->search_width = 1 and opts->alphabet = 0, except that the search is
+ * the plain chord search
  * (no query aimed at H = b: it runs on the device, whose log and exp are not
  * those of the host) (argmins kept in LDS; those fields of opts are ignored).  codebooks: device, n x s fp64 (row
  * r's t_out[r] values first, the rest untouched); t_out: device, n int32
@@ -198,7 +213,8 @@ ecasq_status ecasq_solve_batched(const void *x, ecasq_dtype dt, int64_t n, int64
 
 /* Bytes of device workspace a single-vector solve of d entries with at most s
  * values needs; flags: 1 = stored argmins (recovery 1 of schedule 0),
- * 2 = the tables of schedule 1 (0 when d < 1, s < 2 or flags outside 0..3). */
+ * 2 = the tables of schedule 1, 4 = a permissible grid (alphabet 1 or 2)
+ * (0 when d < 1, s < 2 or flags outside 0..7). */
 size_t ecasq_workspace_size(int64_t d, int32_t s, int32_t flags);
 
 /* Static string for a status code. */

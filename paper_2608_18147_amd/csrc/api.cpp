@@ -38,8 +38,8 @@ namespace {
     } while (0)
 
 struct Layout {
-    size_t v, N, S, S2, F0, F1, M0, M1, P0, P1, pval, pidx, last, res, mres, small, chain, kstar,
-        prep, swF, swK, swchain;
+    size_t v, N, S, S2, gv, gN, gS, gS2, F0, F1, M0, M1, P0, P1, pval, pidx, last, res, mres,
+        small, chain, kstar, prep, swF, swK, swchain;
     int64_t pstride;  // partial entries per multiplier
     size_t total;
 };
@@ -48,6 +48,7 @@ struct Layout {
 // layer-by-layer schedule), and the sweep schedule's tables.
 constexpr int32_t kWsArgmins = 1;
 constexpr int32_t kWsSweep = 2;
+constexpr int32_t kWsAlphabet = 4;  // a permissible grid next to the input's histogram
 
 Layout layout(int64_t d, int32_t s, int32_t flags) {
     Layout L;
@@ -62,6 +63,11 @@ Layout layout(int64_t d, int32_t s, int32_t flags) {
     L.N = take(nd);
     L.S = take(nd);
     L.S2 = take(nd);
+    const size_t ng = (flags & kWsAlphabet) ? nd : 0;
+    L.gv = take(ng);
+    L.gN = take(ng);
+    L.gS = take(ng);
+    L.gS2 = take(ng);
     const bool sweep = (flags & kWsSweep) != 0;
     // layer-by-layer buffers: kMaxLambdas rows of d per array (one per
     // multiplier of a pass); the sweep keeps whole tables instead
@@ -152,8 +158,10 @@ void ctx_close(Ctx& c) {
     c.base = nullptr;
 }
 
-// Sort, histogram, exact prefix sums; reads p, N[0] and ||X||^2 back.
-ecasq_status ctx_prep(Ctx& c, const void* x, int dt) {
+// Sort, histogram, exact prefix sums; reads p, N[0] and ||X||^2 back.  With a
+// permissible grid (alphabet 1 uniform, 2 quantile, of m points), the DP's
+// candidates become the grid and p its size (App. D).
+ecasq_status ctx_prep(Ctx& c, const void* x, int dt, int32_t alphabet = 0, int64_t m = 0) {
     int64_t* small = c.at<int64_t>(c.L.small);
     uint32_t* flags = reinterpret_cast<uint32_t*>(small + 1);
     HIP_TRY(hipMemsetAsync(small, 0, sizeof(int64_t) * 8, c.st));
@@ -165,16 +173,31 @@ ecasq_status ctx_prep(Ctx& c, const void* x, int dt) {
     HIP_TRY(hipStreamSynchronize(c.st));
     if ((uint32_t)hs[1] & 1u) return ECASQ_ENONFINITE;
     c.p = hs[0];
-    double c0 = 0, s2 = 0;
-    HIP_TRY(hipMemcpyAsync(&c0, c.at<double>(c.L.N), sizeof(double), hipMemcpyDeviceToHost, c.st));
-    HIP_TRY(hipMemcpyAsync(&s2, c.at<double>(c.L.S2) + (c.p - 1), sizeof(double),
-                           hipMemcpyDeviceToHost, c.st));
-    HIP_TRY(hipStreamSynchronize(c.st));
-    c.s2tot = s2;
     c.H.v = c.at<double>(c.L.v);
     c.H.N = c.at<double>(c.L.N);
     c.H.S = c.at<double>(c.L.S);
     c.H.S2 = c.at<double>(c.L.S2);
+    double s2 = 0;
+    HIP_TRY(hipMemcpyAsync(&s2, c.H.S2 + (c.p - 1), sizeof(double), hipMemcpyDeviceToHost, c.st));
+    if (alphabet != 0 && c.p >= 2) {
+        int64_t* count = small + 5;
+        HIP_TRY(launch_alphabet(alphabet, m, c.d, c.H.v, c.H.N, c.H.S, c.H.S2, c.p,
+                                c.at<double>(c.L.gv), c.at<double>(c.L.gN), c.at<double>(c.L.gS),
+                                c.at<double>(c.L.gS2), count, c.st));
+        int64_t np = 0;
+        HIP_TRY(hipMemcpyAsync(&np, count, sizeof np, hipMemcpyDeviceToHost, c.st));
+        HIP_TRY(hipStreamSynchronize(c.st));
+        if (np < 2 || np > m) return ECASQ_EHIP;
+        c.p = np;
+        c.H.v = c.at<double>(c.L.gv);
+        c.H.N = c.at<double>(c.L.gN);
+        c.H.S = c.at<double>(c.L.gS);
+        c.H.S2 = c.at<double>(c.L.gS2);
+    }
+    double c0 = 0;
+    HIP_TRY(hipMemcpyAsync(&c0, c.H.N, sizeof(double), hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    c.s2tot = s2;
     c.H.p = c.p;
     c.H.dd = (double)c.d;
     c.H.c0 = c0;
@@ -702,7 +725,8 @@ ecasq_status finish(Ctx& c, std::vector<int32_t>& chain, double lam, double b, b
 }
 
 int32_t ws_flags(const ecasq_options& o) {
-    return (o.recovery == 1 ? kWsArgmins : 0) | (o.dp_schedule == 1 ? kWsSweep : 0);
+    return (o.recovery == 1 ? kWsArgmins : 0) | (o.dp_schedule == 1 ? kWsSweep : 0) |
+           (o.alphabet != 0 ? kWsAlphabet : 0);
 }
 
 ecasq_options defaults() {
@@ -713,6 +737,8 @@ ecasq_options defaults() {
     o.max_search_passes = 32;
     o.search_width = 1;
     o.dp_schedule = 1;
+    o.alphabet = 0;
+    o.alphabet_size = 0;
     o.recovery = 0;
     return o;
 }
@@ -721,7 +747,12 @@ bool options_ok(const ecasq_options& o) {
     return o.refine_rounds >= 0 && o.refine_exhaustive >= 0 && o.refine_exhaustive <= 1 &&
            o.exact_s >= 0 && o.exact_s <= 1 && o.max_search_passes >= 1 && o.recovery >= 0 &&
            o.recovery <= 1 && (o.search_width == 1 || o.search_width == kMaxLambdas) &&
-           o.dp_schedule >= 0 && o.dp_schedule <= 1;
+           o.dp_schedule >= 0 && o.dp_schedule <= 1 && o.alphabet >= 0 && o.alphabet <= 2;
+}
+
+// the grid size of a permissible alphabet must lie in [2, d]
+bool alphabet_ok(const ecasq_options& o, int64_t d) {
+    return o.alphabet == 0 || (o.alphabet_size >= 2 && o.alphabet_size <= d);
 }
 
 ecasq_status solve_budget(const void* x, int dt, int64_t d, int32_t s, double b,
@@ -733,7 +764,7 @@ ecasq_status solve_budget(const void* x, int dt, int64_t d, int32_t s, double b,
         Ctx& c;
         ~Closer() { ctx_close(c); }
     } closer{c};
-    ECASQ_TRY(ctx_prep(c, x, dt));
+    ECASQ_TRY(ctx_prep(c, x, dt, o.alphabet, o.alphabet_size));
     std::vector<int32_t> chain;
     ecasq_status status = ECASQ_OK;
     double lam = 0.0;
@@ -768,7 +799,7 @@ ecasq_status solve_budgets(const void* x, int dt, int64_t d, int32_t s, int32_t 
         Ctx& c;
         ~Closer() { ctx_close(c); }
     } closer{c};
-    ECASQ_TRY(ctx_prep(c, x, dt));
+    ECASQ_TRY(ctx_prep(c, x, dt, o.alphabet, o.alphabet_size));
     std::vector<Point> cache;
     ecasq_status worst = ECASQ_OK;
     for (int32_t k = 0; k < nb; k++) {
@@ -818,7 +849,7 @@ void ecasq_default_options(ecasq_options* opts) {
 }
 
 size_t ecasq_workspace_size(int64_t d, int32_t s, int32_t flags) {
-    if (d < 1 || s < 2 || flags < 0 || flags > 3) return 0;
+    if (d < 1 || s < 2 || flags < 0 || flags > 7) return 0;
     return layout(d, s, flags).total;
 }
 
@@ -843,7 +874,7 @@ ecasq_status ecasq_solve_ex(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
     if (s < 2 || s > 255 || !codebook) return ECASQ_EINVAL;
     if (!(bits_per_entry >= 0.0)) return ECASQ_EINVAL;  // also rejects NaN
     const ecasq_options o = opts ? *opts : defaults();
-    if (!options_ok(o)) return ECASQ_EINVAL;
+    if (!options_ok(o) || !alphabet_ok(o, d)) return ECASQ_EINVAL;
     return solve_budget(x, dt, d, s, bits_per_entry, o, stream, codebook, codebook_rank, info,
                         workspace, workspace_bytes);
 }
@@ -863,7 +894,7 @@ ecasq_status ecasq_solve_budgets(const void* x, ecasq_dtype dt, int64_t d, int32
     for (int32_t k = 0; k < nb; k++)
         if (!(budgets[k] >= 0.0)) return ECASQ_EINVAL;  // also rejects NaN
     const ecasq_options o = opts ? *opts : defaults();
-    if (!options_ok(o)) return ECASQ_EINVAL;
+    if (!options_ok(o) || !alphabet_ok(o, d)) return ECASQ_EINVAL;
     return solve_budgets(x, dt, d, s, nb, budgets, o, stream, codebooks, codebook_ranks, infos);
 }
 
@@ -874,14 +905,14 @@ ecasq_status ecasq_solve_lagrangian(const void* x, ecasq_dtype dt, int64_t d, in
     if (s < 2 || s > 255 || !codebook || !(lambda >= 0.0) || !std::isfinite(lambda))
         return ECASQ_EINVAL;
     const ecasq_options o = opts ? *opts : defaults();
-    if (!options_ok(o)) return ECASQ_EINVAL;
+    if (!options_ok(o) || !alphabet_ok(o, d)) return ECASQ_EINVAL;
     Ctx c;
     ECASQ_TRY(ctx_open(c, d, s, ws_flags(o), stream, nullptr, 0));
     struct Closer {
         Ctx& c;
         ~Closer() { ctx_close(c); }
     } closer{c};
-    ECASQ_TRY(ctx_prep(c, x, dt));
+    ECASQ_TRY(ctx_prep(c, x, dt, o.alphabet, o.alphabet_size));
     std::vector<int32_t> chain;
     if (c.p == 1) {
         chain.assign(1, 0);

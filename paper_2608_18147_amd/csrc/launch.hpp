@@ -29,6 +29,14 @@ size_t prep_scratch_bytes(int64_t d);
 hipError_t launch_prep(const void* x, int dt, int64_t d, void* scratch, hipStream_t st, double* v,
                        double* N, double* S, double* S2, int64_t* p_dev, uint32_t* flags_dev);
 
+// ---- alphabet.hip ----
+// kind 1: uniform grid of m points over [v[0], v[px-1]]; kind 2: the input
+// values at ranks floor(k (d-1) / (m-1)); repeats dropped.  Writes the grid and
+// the prefix sums at its points; *count = grid size.  2 <= m <= d, px >= 2.
+hipError_t launch_alphabet(int32_t kind, int64_t m, int64_t d, const double* v, const double* N,
+                           const double* S, const double* S2, int64_t px, double* gv, double* gN,
+                           double* gS, double* gS2, int64_t* count, hipStream_t st);
+
 // ---- dp.hip ----
 // One DP layer for nlam multipliers (1 or kMaxLambdas); every per-multiplier
 // array below holds nlam valid entries.

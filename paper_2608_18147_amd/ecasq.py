@@ -33,6 +33,8 @@ class ecasq_options(ctypes.Structure):
         ("recovery", ctypes.c_int32),
         ("search_width", ctypes.c_int32),
         ("dp_schedule", ctypes.c_int32),
+        ("alphabet", ctypes.c_int32),
+        ("alphabet_size", ctypes.c_int32),
     ]
 
 

@@ -31,7 +31,8 @@ def test_status_strings_and_defaults():
     assert "NaN" in ecasq.ecasq_status_string(-2)
     o = ecasq.ecasq_default_options()
     assert (o.refine_rounds, o.refine_exhaustive, o.exact_s, o.max_search_passes, o.recovery,
-            o.search_width, o.dp_schedule) == (5, 0, 0, 32, 0, 1, 1)
+            o.search_width, o.dp_schedule, o.alphabet, o.alphabet_size) == \
+        (5, 0, 0, 32, 0, 1, 1, 0, 0)
 
 
 def test_workspace_size_is_linear_in_d():

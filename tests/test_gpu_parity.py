@@ -395,6 +395,66 @@ def test_sweep_options_and_edges():
     _compare(g, o)
 
 
+ALPHABET_CASES = [
+    ("uniform_64", "lognormal_16k", 2048, 16, 2.0, ("uniform", 64)),
+    ("uniform_2", "normal_1k", None, 16, 2.0, ("uniform", 2)),
+    ("uniform_1000_fine", "rounded", 1024, 12, 2.5, ("uniform", 1000)),
+    ("quantile_200", "student_t_1m", 2048, 16, 1.5, ("quantile", 200)),
+    ("quantile_dups", "rounded", 4096, 16, 2.0, ("quantile", 3000)),
+    ("quantile_d", "normal_1k", 700, 10, 2.0, ("quantile", 700)),
+    ("uniform_1500", "weights_256k", 4096, 24, 3.0, ("uniform", 1500)),
+]
+
+
+@pytest.mark.parametrize("schedule", [1, 0], ids=["sweep_w1", "layers_w8"])
+@pytest.mark.parametrize("case", ALPHABET_CASES, ids=[c[0] for c in ALPHABET_CASES])
+def test_permissible_alphabet_parity(case, schedule):
+    """App. D with P != X: the DP over a uniform or quantile grid; a fine
+    uniform grid over few values, a quantile grid over repeated values (points
+    merge) and m = d."""
+    name, wl, d, s, b, alpha = case
+    if wl == "rounded":  # a few dozen distinct values, many repeats
+        x = np.round(inputs.normal(d, 5) * 8.0) / 8.0
+    else:
+        x = inputs.make(wl, seed=5, d=d)
+    kind = 1 if alpha[0] == "uniform" else 2
+    _say("alphabet", name, schedule, x.size, s, b, alpha)
+    extra = dict(dp_schedule=1, search_width=1) if schedule == 1 else LAYERS
+    orc = DEFAULT_ORACLE if schedule == 1 else {}
+    opts = ecasq.ecasq_default_options(alphabet=kind, alphabet_size=alpha[1], **extra)
+    g = ecasq.ecasq_solve(_dev(x), s, b, options=opts)
+    o = pipeline.solve(x, s, b, alphabet=alpha, **orc)
+    _compare(g, o)
+    assert g[2]["p"] <= alpha[1]
+
+
+def test_permissible_alphabet_lagrangian_budgets_and_errors():
+    x = inputs.lognormal_signed(1500, 4)
+    for kind, alpha in ((1, ("uniform", 300)), (2, ("quantile", 250))):
+        _say("alphabet lagrangian", alpha)
+        opts = ecasq.ecasq_default_options(refine_rounds=5, alphabet=kind, alphabet_size=alpha[1])
+        g = ecasq.ecasq_solve_lagrangian(_dev(x), 12, 0.05, options=opts)
+        o = pipeline.solve_lagrangian(x, 12, 0.05, refine_rounds=5, recovery="backpointers",
+                                      alphabet=alpha)
+        _compare(g, o)
+        _say("alphabet budgets", alpha)
+        opts = ecasq.ecasq_default_options(refine_rounds=3, alphabet=kind, alphabet_size=alpha[1])
+        gs = ecasq.ecasq_solve_budgets(_dev(x), 12, (1.0, 2.5), options=opts)
+        os_ = pipeline.solve_budgets(x, 12, (1.0, 2.5), refine_rounds=3, width=1,
+                                     recovery="backpointers", aim=True, alphabet=alpha)
+        for gg, oo in zip(gs, os_):
+            _compare(gg, oo)
+    for m in (1, x.size + 1):
+        opts = ecasq.ecasq_default_options(alphabet=1, alphabet_size=m)
+        with pytest.raises(ecasq.EcasqError):
+            ecasq.ecasq_solve(_dev(x), 12, 2.0, options=opts)
+    # a constant input: the grid collapses to the single value
+    xc = np.full(500, 0.25, dtype=np.float32)
+    opts = ecasq.ecasq_default_options(alphabet=2, alphabet_size=17)
+    g = ecasq.ecasq_solve(_dev(xc), 8, 2.0, options=opts)
+    _compare(g, pipeline.solve(xc, 8, 2.0, alphabet=("quantile", 17), **DEFAULT_ORACLE))
+
+
 @pytest.mark.parametrize("schedule", [1, 0], ids=["sweep_w1", "layers_w8"])
 def test_solve_budgets_shared_cache(schedule):
     """Several budgets on one input sharing DP solves (the budget sweep of the
