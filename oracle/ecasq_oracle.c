@@ -775,3 +775,141 @@ int orc_search(const double *v, const double *N, const double *S, const double *
     free(pts);
     return 0;
 }
+
+/* ------------------------------------------------------------------------- */
+/* Optimal lambda-ECASQ (Sec. 4; App. D for the closed forms).                */
+/*
+ * State (i, l, j): the best cost of the values up to v_l using i-1 codebook
+ * values that end at v_l, plus the MSE of (v_l, v_j] with v_l and v_j
+ * adjacent in the codebook.  The expected frequency of v_l is then known:
+ * U[k,l] + D[l,j], with k the codebook value before v_l.
+ *
+ *   layer 2 (l = 0):  dp(2,0,j) = C[0,j] + lambda' h(n_0/d + D[0,j]/d)
+ *   layer i >= 3:     dp(i,l,j) = C[l,j] + min_k dp(i-1,k,l) + lambda' h(U[k,l]/d + D[l,j]/d)
+ *                     k = 0 for i = 3, i-3 <= k < l for i >= 4, l in [i-2, p-2]
+ *   answer:           min over i <= min(s,p) (i = min(s,p) with exact_s), then
+ *                     over l, of dp(i,l,p-1) + lambda' h(U[l,p-1]/d)
+ *
+ * Every minimum takes the lowest index among ties (i, then l, then k).
+ * Canonical arithmetic: U/d and D/d in the DP's g form (yu, yd of the apx
+ * cell), e(y) = m log2c(m) with m = max(y, 0) (so lambda' h = -lambda' e):
+ *   layer 2:  fma(-lambda', e(yd(0,j) + c0/d), C[0,j])
+ *   T(k)   =  fma(-lambda', e(yu(k,l) + yd(l,j)), dp(i-1,k,l))
+ *   dp     =  C[l,j] + min_k T(k)
+ *   final  =  fma(-lambda', e(yu(l,p-1)), dp(i,l,p-1))
+ * The minimum is over every admissible k (the definition; the SMAWK
+ * acceleration of Sec. 4.1 finds the same minimiser when the matrix is Monge).
+ */
+
+/* yu = U[a,b]/d and yd = D[a,b]/d of (v_a, v_b] in the g form, and C[a,b]. */
+static void interval_y(const hist_t *H, int64_t a, int64_t b, double *C, double *yu, double *yd)
+{
+    double va = H->v[a], vb = H->v[b];
+    double n = H->N[b] - H->N[a];
+    double sa = H->S[b] - H->S[a];
+    double s2 = H->S2[b] - H->S2[a];
+    double w = vb - va;
+    double tu = fma(-va, n, sa);
+    double td = fma(vb, n, -sa);
+    *C = fma(vb, tu, fma(va, sa, -s2));
+    double g = 1.0 / (w * H->dd);
+    *yu = tu * g;
+    *yd = td * g;
+}
+
+static double elog(double y)
+{
+    double m = fmax(y, 0.0);
+    return m * log2c(m);
+}
+
+/* out: J' = MSE + lambda' H(Xhat) of the optimum (lambda' units), t, cells
+ * (admissible (k, l, j) triples plus layer-2 and final entries).
+ * chain (capacity s): the codebook's value indices.  Kdump (optional):
+ * (min(s,p)+1) x p x p int32 argmins, -1 where undefined.  Fdump (optional):
+ * the same shape of dp values (+inf where undefined). */
+int orc_opt_dp(const double *v, const double *N, const double *S, const double *S2, int64_t p,
+               int64_t d, int32_t s, int32_t exact_s, double lamp, int32_t *chain, double *out,
+               int32_t *Kdump, double *Fdump)
+{
+    hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
+    if (p == 1) {
+        chain[0] = 0;
+        out[0] = 0.0; out[1] = 1; out[2] = 0;
+        return 0;
+    }
+    int64_t imax = s < p ? s : p;
+    size_t pp = (size_t)p * (size_t)p;
+    double *prev = malloc(sizeof(double) * pp);
+    double *cur = malloc(sizeof(double) * pp);
+    int32_t *K = malloc(sizeof(int32_t) * pp * (size_t)(imax + 1));
+    if (!prev || !cur || !K) { free(prev); free(cur); free(K); return -4; }
+    for (size_t q = 0; q < pp * (size_t)(imax + 1); q++) K[q] = -1;
+    int64_t cells = 0;
+    double best = INFINITY;
+    int64_t bi = -1, bl = -1;
+    for (size_t q = 0; q < pp; q++) cur[q] = INFINITY;
+    for (int64_t j = 1; j < p; j++) {
+        double C, yu, yd;
+        interval_y(&H, 0, j, &C, &yu, &yd);
+        cur[j] = fma(-lamp, elog(yd + H.c0d), C);
+        cells++;
+    }
+    for (int64_t i = 2; i <= imax; i++) {
+        if (i >= 3) {
+            double *t = prev; prev = cur; cur = t;
+            for (size_t q = 0; q < pp; q++) cur[q] = INFINITY;
+            /* the rows l are independent given layer i-1 */
+#pragma omp parallel for schedule(dynamic, 4) reduction(+ : cells)
+            for (int64_t l = i - 2; l <= p - 2; l++) {
+                int64_t klo = i == 3 ? 0 : i - 3;
+                int64_t khi = i == 3 ? 0 : l - 1;
+                double *yuk = malloc(sizeof(double) * (size_t)(khi + 1));
+                for (int64_t k = klo; k <= khi; k++) {
+                    double Ck, ydk;
+                    interval_y(&H, k, l, &Ck, &yuk[k], &ydk);
+                }
+                for (int64_t j = l + 1; j < p; j++) {
+                    double C, yu, yd;
+                    interval_y(&H, l, j, &C, &yu, &yd);
+                    double bt = INFINITY;
+                    int32_t kb = -1;
+                    for (int64_t k = klo; k <= khi; k++) {
+                        double T = fma(-lamp, elog(yuk[k] + yd), prev[k * p + l]);
+                        if (T < bt) { bt = T; kb = (int32_t)k; }
+                        cells++;
+                    }
+                    cur[l * p + j] = C + bt;
+                    K[(size_t)i * pp + (size_t)(l * p + j)] = kb;
+                }
+                free(yuk);
+            }
+        }
+        if (Fdump) memcpy(Fdump + (size_t)i * pp, cur, sizeof(double) * pp);
+        if (exact_s && i != imax) continue;
+        int64_t lo = i == 2 ? 0 : i - 2, hi = i == 2 ? 0 : p - 2;
+        for (int64_t l = lo; l <= hi; l++) {
+            double C, yu, yd;
+            interval_y(&H, l, p - 1, &C, &yu, &yd);
+            double f = fma(-lamp, elog(yu), cur[l * p + p - 1]);
+            cells++;
+            if (f < best) { best = f; bi = i; bl = l; }
+        }
+    }
+    int32_t t = (int32_t)bi;
+    chain[t - 1] = (int32_t)(p - 1);
+    chain[t - 2] = (int32_t)bl;
+    int64_t l = bl, j = p - 1;
+    for (int64_t i = bi; i >= 3; i--) {
+        int32_t k = K[(size_t)i * pp + (size_t)(l * p + j)];
+        chain[i - 3] = k;
+        j = l;
+        l = k;
+    }
+    if (Kdump) memcpy(Kdump, K, sizeof(int32_t) * pp * (size_t)(imax + 1));
+    out[0] = best;
+    out[1] = t;
+    out[2] = (double)cells;
+    free(prev); free(cur); free(K);
+    return 0;
+}

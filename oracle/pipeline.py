@@ -268,6 +268,7 @@ class Result:
     status: int
     traj: np.ndarray = field(default=None)
     passes: int = 0
+    dp_value: float = None   # the optimal DP's own value (lambda' units)
 
 
 def _finish(H, chain, lam, solves, rounds, cells, status, traj=None):
@@ -348,6 +349,38 @@ def solve_lagrangian(x, s, lam, refine_rounds=0, exhaustive=False, exact_s=False
         chain, rounds, _ = refine(H, chain, lam * H.s2tot, math.inf, False, refine_rounds,
                                   exhaustive)
     return _finish(H, chain, lam, 1, rounds, r["cells"] + hcells, 0)
+
+
+def opt_dp(H, s, lamp, exact_s=False, dump=False):
+    """Optimal lambda-ECASQ over states (i, l, j) (Sec. 4), every admissible
+    predecessor scanned.  Returns dict(J = MSE + lambda' H(Xhat) of the optimum,
+    t, chain, cells[, K, F per layer])."""
+    L = native.lib()
+    out = np.zeros(3)
+    chain = np.zeros(max(s, 1), dtype=np.int32)
+    imax = min(s, H.p)
+    K = np.zeros((imax + 1) * H.p * H.p, dtype=np.int32) if dump else None
+    F = np.zeros((imax + 1) * H.p * H.p) if dump else None
+    rc = L.orc_opt_dp(*H.args(), s, int(exact_s), lamp, native.iptr(chain), native.dptr(out),
+                      native.iptr(K) if dump else None, native.dptr(F) if dump else None)
+    assert rc == 0
+    t = int(out[1])
+    r = dict(J=out[0], t=t, chain=chain[:t].copy(), cells=int(out[2]))
+    if dump:
+        r["K"] = K.reshape(imax + 1, H.p, H.p)
+        r["F"] = F.reshape(imax + 1, H.p, H.p)
+    return r
+
+
+def solve_optimal(x, s, lam, exact_s=False, alphabet=None):
+    """Optimal lambda-ECASQ at a fixed multiplier (vNMSE units): the codebook
+    minimising vNMSE + lambda H(Xhat) with at most s values (exactly s with
+    exact_s) drawn from the permissible values (Sec. 4; App. D)."""
+    H = prepare(x, alphabet)
+    r = opt_dp(H, s, lam * H.s2tot, exact_s)
+    res = _finish(H, r["chain"], lam, 1, 0, r["cells"], 0)
+    res.dp_value = r["J"]
+    return res
 
 
 def uniforms(n, seed):

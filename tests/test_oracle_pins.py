@@ -321,6 +321,91 @@ def test_optimal_dp_equals_brute_force_and_sandwich():
         assert Jbo <= Ja + 1e-12 and Ja <= Jbo + lam + 1e-12
 
 
+def test_native_optimal_dp_equals_brute_force():
+    """The C optimal DP (Sec. 4, states (i, l, j), the full minimum over k):
+    its optimum equals the brute-force minimum of vNMSE + lambda H(Xhat) over
+    every spanning codebook, its own value matches its codebook's objective, and
+    the independent per-entry implementation agrees; exactly s values with
+    exact_s; on permissible grids (App. D) the minimum over grid codebooks."""
+    for x, s, lam in _tiny_inputs(120, 31):
+        H = pipeline.prepare(x)
+        r = pipeline.solve_optimal(x, s, lam)
+        Jb, Qb = plain.brute_force(x, s, lam, "out")
+        assert abs(r.objective - Jb) <= 1e-12 * max(1.0, Jb), (x, s, lam)
+        assert abs(r.dp_value / H.s2tot - r.objective) <= 1e-12 * max(1.0, Jb)
+        Jo, Qo = plain.optimal_dp(x, s, lam)
+        assert abs(Jo - Jb) <= 1e-12 * max(1.0, Jb)
+        assert r.t <= s and r.codebook[0] == H.v[0] and r.codebook[-1] == H.v[-1]
+        if s <= H.p:
+            re = pipeline.solve_optimal(x, s, lam, exact_s=True)
+            cands = [Q for Q in plain.spanning_codebooks(x, s) if len(Q) == s]
+            Je = min(plain.objective(x, Q, lam, "out") for Q in cands)
+            assert re.t == s and abs(re.objective - Je) <= 1e-12 * max(1.0, Je)
+    for x, s, lam in _tiny_inputs(40, 32):
+        for alpha in (("uniform", 9), ("quantile", 4)):
+            H = pipeline.prepare(x, alpha)
+            r = pipeline.solve_optimal(x, s, lam, alphabet=alpha)
+            Jb, _ = plain.brute_force(x, s, lam, "out", P=list(H.v))
+            assert abs(r.objective - Jb) <= 1e-12 * max(1.0, Jb), (x, s, lam, alpha)
+
+
+def test_optimal_dp_special_cases():
+    """lambda = 0 is ASQ (Sec. 3: the minimum MSE with at most s values, the
+    textbook DP eq. (1)); a prohibitive lambda keeps two values; p = 1 and
+    p = 2."""
+    rng = np.random.default_rng(33)
+    for _ in range(10):
+        x = rng.standard_normal(int(rng.integers(20, 60))).astype(np.float32)
+        s = int(rng.integers(2, 8))
+        H = pipeline.prepare(x)
+        r = pipeline.solve_optimal(x, s, 0.0)
+        a = float(plain.asq_dp(x, s))
+        assert abs(r.mse - a) <= 1e-12 * max(1.0, a)
+        assert pipeline.solve_optimal(x, s, 1e6).t == 2
+    r = pipeline.solve_optimal(np.full(7, 2.5, dtype=np.float32), 4, 0.1)
+    assert r.t == 1 and r.mse == 0.0
+    x2 = np.array([1, 1, 3], dtype=np.float32)
+    r = pipeline.solve_optimal(x2, 4, 0.1)
+    assert r.t == 2 and r.mse == 0.0 and list(r.codebook) == [1.0, 3.0]
+
+
+def test_optimal_argmins_monotone_lemma_quadrangle():
+    """Lemma quadrangleM (Sec. 4.1): for fixed i and l the matrix of
+    T(k, j) is Monge with its columns reversed, so the lowest minimiser k*(j)
+    does not increase with j.  Checked on every (i, l) of random inputs: where
+    k*(j+1) > k*(j), the two candidates must tie to rounding."""
+    rng = np.random.default_rng(34)
+    viol = checked = 0
+    for trial in range(6):
+        d = int(rng.integers(40, 90))
+        x = (rng.standard_normal(d) * (1 + 3 * (trial % 2))).astype(np.float32)
+        H = pipeline.prepare(x)
+        s = 7
+        lam = float(10 ** rng.uniform(-3, 0))
+        lamp = lam * H.s2tot
+        r = pipeline.opt_dp(H, s, lamp, dump=True)
+        K, F = r["K"], r["F"]
+        p = H.p
+
+        def T(i, k, l, j):  # the candidate in plain float arithmetic
+            U = pipeline.interval(H, k, l)[1]
+            D = pipeline.interval(H, l, j)[2]
+            return F[i - 1, k, l] + lamp * plain.h((U + D) / H.d)
+
+        for i in range(4, min(s, p) + 1):
+            for l in range(i - 2, p - 1):
+                ks = K[i, l, l + 1:p]
+                checked += len(ks)
+                for jj in range(len(ks) - 1):
+                    if ks[jj + 1] > ks[jj]:
+                        viol += 1
+                        j = l + 1 + jj
+                        # the minimiser at j + 1 and the monotone one tie to rounding
+                        a, b = T(i, ks[jj + 1], l, j + 1), T(i, ks[jj], l, j + 1)
+                        assert abs(a - b) <= 1e-12 * max(1.0, abs(a)), (trial, i, l, j)
+    assert checked > 20000 and viol <= 3, (checked, viol)
+
+
 def test_entropy_sandwich_per_codebook():
     """eq. apx_entropy_sandwich: H(Xhat) <= H(I,B) <= H(Xhat) + 1 for every Q."""
     rng = np.random.default_rng(7)
