@@ -155,6 +155,34 @@ def batched_rate(torch, ecasq, inputs, reps=3):
     }
 
 
+def alphabet_rate(torch, ecasq, xd, s, b, opts, full_info, grids=(("uniform", 4096),
+                                                                   ("quantile", 4096))):
+    """The same solve on permissible grids of m points (App. D with P != X):
+    time per solve step and the objective against the solve over all distinct
+    values (full_info)."""
+    res = []
+    for kind, m in grids:
+        o = ecasq.ecasq_options()
+        ctypes_copy = {f: getattr(opts, f) for f, _ in opts._fields_}
+        for f, v in ctypes_copy.items():
+            setattr(o, f, v)
+        o.alphabet = 1 if kind == "uniform" else 2
+        o.alphabet_size = m
+        ecasq.ecasq_solve(xd, s, b, options=o)  # warm-up
+        torch.cuda.synchronize()
+        reps = 3
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            cb, rk, info = ecasq.ecasq_solve(xd, s, b, options=o)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) / reps * 1e3
+        res.append({"grid": kind, "m": m, "p": info["p"], "ms_per_solve_step": ms,
+                    "dp_solves": info["dp_solves"], "t": info["t"], "vnmse": info["vnmse"],
+                    "entropy": info["entropy"], "objective": info["objective"],
+                    "vnmse_vs_all_values": info["vnmse"] / full_info["vnmse"]})
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -171,6 +199,8 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=32768)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-batched", action="store_true")
+    ap.add_argument("--no-alphabet", action="store_true",
+                    help="skip the permissible-grid solves (uniform / quantile, 4096 points)")
     ap.add_argument("--dp-schedule", type=int, default=None, choices=(0, 1),
                     help="0: layer by layer (passes of 8, Hirschberg); 1: column-block sweep\n"
                          "(default: the library's defaults)")
@@ -327,6 +357,10 @@ def main():
             "empirical_entropy": float(ent), "refine_rounds_run": info["refine_rounds_run"],
         },
     }
+    if not args.no_alphabet and len(budgets) == 1:
+        out["alphabet"] = alphabet_rate(torch, ecasq, xd, s, b, opts, info)
+        for r in out["alphabet"]:
+            r["speedup"] = out["ms_per_step"] / r["ms_per_solve_step"]
     if not args.no_batched:
         out["batched"] = batched_rate(torch, ecasq, inputs)
     if not args.no_cpu_baseline:
