@@ -70,6 +70,8 @@ typedef struct {
                                   alphabet_size points over [min X, max X]; 2 the input
                                   values at alphabet_size evenly spaced ranks */
     int32_t alphabet_size;     /* grid points m, 2 <= m <= d (alphabet 1 and 2) */
+    int32_t optimal_scan;      /* ecasq_solve_optimal: 0 monotone brackets (Sec. 4.1,
+                                  default), 1 every predecessor */
 } ecasq_options;
 
 typedef struct {
@@ -179,6 +181,39 @@ ecasq_status ecasq_solve_lagrangian(const void *x, ecasq_dtype dt, int64_t d, in
                                     ecasq_info *info);
 
 /*
+ * Optimal lambda-ECASQ (Sec. 4): the codebook of at most s values (exactly
+ * min(s, p) with opts->exact_s) drawn from the permissible values (the
+ * distinct input values, or opts->alphabet's grid, App. D) that minimises
+ * vNMSE + lambda H(Xhat) exactly, H(Xhat) the entropy of the expected output
+ * frequencies; lambda >= 0 in vNMSE units (lambda' = RN(lambda ||X||^2)).
+ *
+ * The DP runs over states (i, l, j): dp(i,l,j) is the least cost of the values
+ * up to v_l with i-1 codebook values ending at v_l plus the MSE of (v_l, v_j],
+ *   dp(2,0,j) = C[0,j] + lambda' h((n_0 + D[0,j]) / d),
+ *   dp(i,l,j) = C[l,j] + min_k dp(i-1,k,l) + lambda' h((U[k,l] + D[l,j]) / d),
+ * answer min over (i, l) of dp(i,l,p-1) + lambda' h(U[l,p-1] / d); lowest
+ * index on ties (i, then l, then k).  U/d, D/d and h are evaluated as the
+ * approximate DP's cell does (g form, table log2).  One launch per layer, one
+ * workgroup per row l; opts->optimal_scan = 0 restricts each column's scan over
+ * k to the bracket between the minimisers of the ends of its 64-column segment
+ * (the argmin does not increase with j, Lemma quadrangleM: the SMAWK
+ * acceleration of Sec. 4.1), 1 scans every k (O(s p^3)).  Where rounding breaks
+ * that order between two candidates equal to within rounding, the bracket can
+ * return a codebook whose objective exceeds the minimum by a rounding error.
+ *
+ * Memory: every layer's argmins are kept (no Hirschberg pass): about
+ * 24 p^2 + 2 (min(s,p) - 2) p^2 bytes (4 per argmin when p > 32768), allocated
+ * on the stream for the call; p <= 65536 (ECASQ_ENOMEM above, or when the
+ * allocation fails).  info: dp_solves = 1, cells = the full DP's (k, l, j)
+ * candidates plus its layer-2 and final entries, refine_rounds_run = 0 (the
+ * refinement options are ignored), objective = vNMSE + lambda H(Xhat) of the
+ * codebook.  Errors as ecasq_solve_lagrangian.
+ */
+ecasq_status ecasq_solve_optimal(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
+                                 double lambda, const ecasq_options *opts, void *stream,
+                                 double *codebook, int32_t *codebook_rank, ecasq_info *info);
+
+/*
  * Final stochastic rounding (Sec. 2): symbol i in [0, t) for every entry of x
  * in its original order.  The bracket is q_r < x <= q_{r+1} (x <= q_0 gives
  * r = 0; x > q_{t-1} is clamped to t-1); the entry rounds up iff
@@ -248,6 +283,20 @@ ecasq_status ecasq_dp_trace(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
                             int32_t *kstar, double *M, double *Ph, double *out);
 
 /*
+ * ecasq_opt_trace: the optimal DP of ecasq_solve_optimal with every layer
+ * recorded.  F (device fp64) and K (device int32), capacity entries each, at
+ * least (min(s,p)+1) p^2 (ECASQ_EINVAL otherwise, checked once p is known):
+ * F[i][j][l] = dp(i,l,j) for the layer's valid (l, j) (layers 2..min(s,p)),
+ * K[i][l][j] = the minimising k (layers 3..min(s,p)); other entries
+ * unspecified.  chain (host, s int32): the codebook's value indices.  out
+ * (host, 4 doubles): the optimum's DP value MSE + lambda' H(Xhat) (MSE units),
+ * t, p, cells.  p = 1 records nothing.
+ */
+ecasq_status ecasq_opt_trace(const void *x, ecasq_dtype dt, int64_t d, int32_t s, double lambda,
+                             const ecasq_options *opts, void *stream, int64_t capacity,
+                             double *F, int32_t *K, int32_t *chain, double *out);
+
+/*
  * Kernel timing for measurement tools.  While enabled (process-wide), every
  * launch of the DP layer kernel is bracketed by two HIP events recorded on the
  * stream it runs on; the elapsed times are read when the solve synchronizes.
@@ -255,7 +304,8 @@ ecasq_status ecasq_dp_trace(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
  * lambda, width-1 search, recovery half-DPs), 1 = the 8 multipliers of a
  * search pass, 2 = a whole solve of DP schedule 1 (all its launches, from
  * the table fill to eq. apx_final, timed as one unit; cells counted as for
- * schedule 0).  ecasq_timing_read returns, for one variant, the summed
+ * schedule 0), 3 = one layer of the optimal DP (cells = its (k, l, j)
+ * candidates).  ecasq_timing_read returns, for one variant, the summed
  * milliseconds, the number of timed launches and the (column, predecessor)
  * cells those launches evaluated, each cell for every multiplier of its
  * launch (host pointers, any may be NULL); reset != 0 clears that variant's

@@ -739,6 +739,7 @@ ecasq_options defaults() {
     o.dp_schedule = 1;
     o.alphabet = 0;
     o.alphabet_size = 0;
+    o.optimal_scan = 0;
     o.recovery = 0;
     return o;
 }
@@ -747,7 +748,8 @@ bool options_ok(const ecasq_options& o) {
     return o.refine_rounds >= 0 && o.refine_exhaustive >= 0 && o.refine_exhaustive <= 1 &&
            o.exact_s >= 0 && o.exact_s <= 1 && o.max_search_passes >= 1 && o.recovery >= 0 &&
            o.recovery <= 1 && (o.search_width == 1 || o.search_width == kMaxLambdas) &&
-           o.dp_schedule >= 0 && o.dp_schedule <= 1 && o.alphabet >= 0 && o.alphabet <= 2;
+           o.dp_schedule >= 0 && o.dp_schedule <= 1 && o.alphabet >= 0 && o.alphabet <= 2 &&
+           o.optimal_scan >= 0 && o.optimal_scan <= 1;
 }
 
 // the grid size of a permissible alphabet must lie in [2, d]
@@ -926,6 +928,98 @@ ecasq_status ecasq_solve_lagrangian(const void* x, ecasq_dtype dt, int64_t d, in
     }
     return finish(c, chain, lambda, HUGE_VAL, false, o, codebook, codebook_rank, info, ECASQ_OK,
                   0);
+}
+
+namespace {
+
+// Optimal lambda-ECASQ at lamp: the codebook (value indices) and the DP's own
+// value.  Ftrace / Ktrace: every layer, for the inspection entry point.
+ecasq_status opt_solve(Ctx& c, double lam, const ecasq_options& o, std::vector<int32_t>& chain,
+                       double* J, double* Ftrace, int32_t* Ktrace) {
+    if (c.p == 1) {
+        chain.assign(1, 0);
+        *J = 0.0;
+        return ECASQ_OK;
+    }
+    if (c.p > kOptMaxP) return ECASQ_ENOMEM;
+    const int32_t imax = (int32_t)std::min<int64_t>(c.s, c.p);
+    const size_t bytes = opt_workspace_bytes(c.p, imax, Ktrace != nullptr);
+    void* mem = nullptr;
+    if (hipMallocAsync(&mem, bytes, c.st) != hipSuccess) return ECASQ_ENOMEM;
+    int32_t* ch = c.at<int32_t>(c.L.chain);
+    double* res = c.at<double>(c.L.mres);
+    const hipError_t e = launch_opt(c.H, imax, o.exact_s, lam * c.s2tot, o.optimal_scan,
+                                    static_cast<char*>(mem), ch, res, Ftrace, Ktrace, c.st);
+    double r[2] = {0.0, 0.0};
+    hipError_t e2 = hipSuccess;
+    if (e == hipSuccess) e2 = hipMemcpyAsync(r, res, sizeof r, hipMemcpyDeviceToHost, c.st);
+    (void)hipFreeAsync(mem, c.st);
+    HIP_TRY(hipStreamSynchronize(c.st));
+    HIP_TRY(e);
+    HIP_TRY(e2);
+    const int32_t t = (int32_t)r[1];
+    if (t < 2 || t > imax) return ECASQ_EHIP;
+    chain.resize(t);
+    HIP_TRY(hipMemcpy(chain.data(), ch, sizeof(int32_t) * t, hipMemcpyDeviceToHost));
+    *J = r[0];
+    c.cells += opt_cells(c.p, imax, o.exact_s);
+    c.solves += 1;
+    return ECASQ_OK;
+}
+
+}  // namespace
+
+ecasq_status ecasq_solve_optimal(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
+                                 double lambda, const ecasq_options* opts, void* stream,
+                                 double* codebook, int32_t* codebook_rank, ecasq_info* info) {
+    ECASQ_TRY(check_x(x, dt, d));
+    if (s < 2 || s > 255 || !codebook || !(lambda >= 0.0) || !std::isfinite(lambda))
+        return ECASQ_EINVAL;
+    const ecasq_options o = opts ? *opts : defaults();
+    if (!options_ok(o) || !alphabet_ok(o, d)) return ECASQ_EINVAL;
+    Ctx c;
+    ECASQ_TRY(ctx_open(c, d, s, o.alphabet != 0 ? kWsAlphabet : 0, stream, nullptr, 0));
+    struct Closer {
+        Ctx& c;
+        ~Closer() { ctx_close(c); }
+    } closer{c};
+    ECASQ_TRY(ctx_prep(c, x, dt, o.alphabet, o.alphabet_size));
+    std::vector<int32_t> chain;
+    double J = 0.0;
+    ECASQ_TRY(opt_solve(c, lambda, o, chain, &J, nullptr, nullptr));
+    ecasq_options fo = o;
+    fo.refine_rounds = 0;  // the optimum leaves nothing to refine
+    return finish(c, chain, lambda, HUGE_VAL, false, fo, codebook, codebook_rank, info, ECASQ_OK,
+                  0);
+}
+
+ecasq_status ecasq_opt_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s, double lambda,
+                             const ecasq_options* opts, void* stream, int64_t capacity,
+                             double* F, int32_t* K, int32_t* chain, double* out) {
+    ECASQ_TRY(check_x(x, dt, d));
+    if (s < 2 || s > 255 || !F || !K || !chain || !out || !(lambda >= 0.0) ||
+        !std::isfinite(lambda))
+        return ECASQ_EINVAL;
+    const ecasq_options o = opts ? *opts : defaults();
+    if (!options_ok(o) || !alphabet_ok(o, d)) return ECASQ_EINVAL;
+    Ctx c;
+    ECASQ_TRY(ctx_open(c, d, s, o.alphabet != 0 ? kWsAlphabet : 0, stream, nullptr, 0));
+    struct Closer {
+        Ctx& c;
+        ~Closer() { ctx_close(c); }
+    } closer{c};
+    ECASQ_TRY(ctx_prep(c, x, dt, o.alphabet, o.alphabet_size));
+    const int64_t imax = std::min<int64_t>(s, c.p);
+    if (c.p > 1 && (imax + 1) * c.p * c.p > capacity) return ECASQ_EINVAL;
+    std::vector<int32_t> ch;
+    double J = 0.0;
+    ECASQ_TRY(opt_solve(c, lambda, o, ch, &J, c.p > 1 ? F : nullptr, c.p > 1 ? K : nullptr));
+    std::memcpy(chain, ch.data(), sizeof(int32_t) * ch.size());
+    out[0] = J;
+    out[1] = (double)ch.size();
+    out[2] = (double)c.p;
+    out[3] = (double)c.cells;
+    return ECASQ_OK;
 }
 
 ecasq_status ecasq_quantize(const void* x, ecasq_dtype dt, int64_t d, const double* codebook,

@@ -441,7 +441,7 @@ bool g_timing = false;
 bool g_verbose = false;
 std::vector<TimedLaunch> g_pending;
 std::vector<hipEvent_t> g_pool;
-TimingTotals g_tot[3];
+TimingTotals g_tot[4];
 TimedLaunch g_open{nullptr, nullptr, 0, 0};
 
 hipEvent_t take_event() {
@@ -462,6 +462,8 @@ void timing_enable(int mode) {
 }
 
 bool timing_verbose() { return g_verbose; }
+
+bool timing_active() { return g_timing; }
 
 void timing_flush() {
     for (auto& t : g_pending) {
@@ -494,7 +496,7 @@ void timing_end(hipStream_t st) {
 
 void timing_read(int variant, double* ms, int64_t* launches, int64_t* cells, bool reset) {
     timing_flush();
-    if (variant < 0 || variant > 2) {
+    if (variant < 0 || variant > 3) {
         if (ms) *ms = 0.0;
         if (launches) *launches = 0;
         if (cells) *cells = 0;

@@ -37,6 +37,23 @@ hipError_t launch_alphabet(int32_t kind, int64_t m, int64_t d, const double* v, 
                            const double* S, const double* S2, int64_t px, double* gv, double* gN,
                            double* gS, double* gS2, int64_t* count, hipStream_t st);
 
+// ---- opt.hip ----
+// Optimal lambda-ECASQ (Sec. 4): p x p layers, so p is bounded.
+constexpr int64_t kOptMaxP = (int64_t)1 << 16;
+// device bytes of the optimal DP's tables for p values and layers 2..imax
+// (trace: argmins kept as int32 for launch_opt's Ktrace)
+size_t opt_workspace_bytes(int64_t p, int32_t imax, bool trace);
+// (k, l, j) candidates, layer-2 entries and final entries of the full DP
+int64_t opt_cells(int64_t p, int32_t imax, int32_t exact_s);
+// mem: opt_workspace_bytes(p, imax, Ktrace != null) bytes; chain (>= imax
+// int32) and res (J' = MSE + lambda' H(Xhat) of the optimum, t) are device
+// memory.  full: scan every predecessor (else monotone brackets).  Ftrace /
+// Ktrace (optional, (imax+1) p^2 each) receive every layer's values, [i][j][l],
+// and argmins of layers >= 3, [i][l][j].
+hipError_t launch_opt(const Hist& H, int32_t imax, int32_t exact_s, double lamp, int32_t full,
+                      char* mem, int32_t* chain, double* res, double* Ftrace, int32_t* Ktrace,
+                      hipStream_t st);
+
 // ---- dp.hip ----
 // One DP layer for nlam multipliers (1 or kMaxLambdas); every per-multiplier
 // array below holds nlam valid entries.
@@ -81,9 +98,12 @@ void timing_enable(int mode);  // 0 off, 1 timing, 2 timing + a stderr line per 
 bool timing_verbose();
 void timing_flush();
 void timing_read(int variant, double* ms, int64_t* launches, int64_t* cells, bool reset);
-// bracket a span of launches on st as one timed unit of `variant` (2: a sweep solve)
+// bracket a span of launches on st as one timed unit of `variant` (2: a sweep
+// solve, 3: a layer of the optimal DP)
 void timing_begin(int variant, int64_t cells, hipStream_t st);
 void timing_end(hipStream_t st);
+bool timing_active();
+constexpr int kTimingOpt = 3;
 hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st);
 hipError_t launch_dp_init_fwd(const Hist& H, int64_t lo, int64_t jl, int64_t jh,
                               const DpInit& I, hipStream_t st);

@@ -35,6 +35,7 @@ class ecasq_options(ctypes.Structure):
         ("dp_schedule", ctypes.c_int32),
         ("alphabet", ctypes.c_int32),
         ("alphabet_size", ctypes.c_int32),
+        ("optimal_scan", ctypes.c_int32),
     ]
 
 
@@ -73,7 +74,7 @@ EXPORTS = (
     "ecasq_default_options", "ecasq_solve", "ecasq_solve_ex", "ecasq_solve_lagrangian",
     "ecasq_quantize", "ecasq_solve_batched", "ecasq_workspace_size", "ecasq_status_string",
     "ecasq_histogram", "ecasq_dp_trace", "ecasq_timing_enable", "ecasq_timing_read",
-    "ecasq_solve_budgets",
+    "ecasq_solve_budgets", "ecasq_solve_optimal", "ecasq_opt_trace",
 )
 
 
@@ -98,6 +99,10 @@ def lib():
     L.ecasq_solve_budgets.argtypes = [vp, i32, i64, i32, i32, P(dbl), P(ecasq_options), vp, vp,
                                       vp, P(ecasq_info)]
     L.ecasq_quantize.argtypes = [vp, i32, i64, vp, i32, ctypes.c_uint64, vp, vp, vp, vp]
+    L.ecasq_solve_optimal.argtypes = [vp, i32, i64, i32, dbl, P(ecasq_options), vp, vp, vp,
+                                      P(ecasq_info)]
+    L.ecasq_opt_trace.argtypes = [vp, i32, i64, i32, dbl, P(ecasq_options), vp, i64, vp, vp,
+                                  P(i32), P(dbl)]
     L.ecasq_solve_batched.argtypes = [vp, i32, i64, i64, i32, dbl, P(ecasq_options), vp, vp,
                                       vp, vp]
     L.ecasq_workspace_size.argtypes = [i64, i32, i32]
@@ -113,7 +118,7 @@ def lib():
     L.ecasq_timing_read.restype = None
     for name in ("ecasq_solve", "ecasq_solve_ex", "ecasq_solve_lagrangian", "ecasq_quantize",
                  "ecasq_solve_batched", "ecasq_histogram", "ecasq_dp_trace",
-                 "ecasq_solve_budgets"):
+                 "ecasq_solve_budgets", "ecasq_solve_optimal", "ecasq_opt_trace"):
         getattr(L, name).restype = i32
     _lib = L
     return L
@@ -214,6 +219,46 @@ def ecasq_solve_lagrangian(x, s, lam, options=None, stream=None):
     return cb[:t], rk[:t], info.as_dict()
 
 
+def ecasq_solve_optimal(x, s, lam, options=None, stream=None):
+    """Optimal lambda-ECASQ (Sec. 4) at lam (vNMSE units).  Returns (codebook,
+    rank, info dict)."""
+    x = _check_x(x)
+    cb = torch.empty(int(s), dtype=torch.float64, device=x.device)
+    rk = torch.empty(int(s), dtype=torch.int32, device=x.device)
+    info = ecasq_info()
+    o = options if options is not None else ecasq_default_options()
+    st = lib().ecasq_solve_optimal(_ptr(x), _DTYPES[x.dtype], x.numel(), int(s), float(lam),
+                                   ctypes.byref(o), _stream(stream), _ptr(cb), _ptr(rk),
+                                   ctypes.byref(info))
+    _raise(st)
+    t = info.t
+    return cb[:t], rk[:t], info.as_dict()
+
+
+def ecasq_opt_trace(x, s, lam, p, options=None, stream=None):
+    """Every layer of the optimal DP for an input with p permissible values.
+    Returns (F [imax+1, p, p] with F[i, j, l] = dp(i, l, j), K [imax+1, p, p]
+    with K[i, l, j] the minimising k, chain list, DP value, cells); entries
+    outside a layer's valid (l, j) are unspecified."""
+    x = _check_x(x)
+    imax = min(int(s), int(p))
+    cap = (imax + 1) * p * p
+    F = torch.empty(cap, dtype=torch.float64, device=x.device)
+    K = torch.empty(cap, dtype=torch.int32, device=x.device)
+    chain = (ctypes.c_int32 * int(s))()
+    out = (ctypes.c_double * 4)()
+    o = options if options is not None else ecasq_default_options()
+    st = lib().ecasq_opt_trace(_ptr(x), _DTYPES[x.dtype], x.numel(), int(s), float(lam),
+                               ctypes.byref(o), _stream(stream), cap, _ptr(F), _ptr(K), chain,
+                               out)
+    _raise(st)
+    if int(out[2]) != p:
+        raise ValueError(f"input has {int(out[2])} permissible values, not {p}")
+    t = int(out[1])
+    return (F.view(imax + 1, p, p), K.view(imax + 1, p, p), list(chain[:t]), out[0],
+            int(out[3]))
+
+
 def ecasq_quantize(x, codebook, seed, stream=None):
     """Returns (symbols uint8 [d], empirical entropy (0-d fp64 tensor), hist int64 [t])."""
     x = _check_x(x)
@@ -301,6 +346,7 @@ def ecasq_timing_enable(on=True, verbose=False):
 TIMING_SINGLE = 0  # one multiplier per DP layer launch
 TIMING_PASS = 1    # the 8 multipliers of a search pass per launch
 TIMING_SWEEP = 2   # one whole solve of DP schedule 1
+TIMING_OPT = 3     # one layer of the optimal DP
 
 
 def ecasq_timing_read(variant=TIMING_PASS, reset=False):
