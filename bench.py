@@ -183,6 +183,45 @@ def alphabet_rate(torch, ecasq, xd, s, b, opts, full_info, grids=(("uniform", 40
     return res
 
 
+OPT_FLOPS_PER_CANDIDATE = 17  # y = yu + yd; m log2c(m) (13 + 1); the candidate's fma (2)
+
+
+def optimal_rate(torch, ecasq, inputs, reps=3):
+    """Optimal lambda-ECASQ (Sec. 4) on the weight-like 2^18 vector in bf16
+    (a few thousand permissible values), s = 64, lambda = 0.1: time per solve
+    with the monotone-bracket scan and with the full scan, and the full scan's
+    layer kernel against the FP64 vector peak."""
+    x = torch.from_numpy(inputs.make("weights_256k", seed=0)).to(torch.bfloat16).to("cuda")
+    s, lam = 64, 0.1
+    out = {"workload": "weights_256k as bf16", "s": s, "lambda": lam}
+    for name, scan in (("monotone", 0), ("full", 1)):
+        o = ecasq.ecasq_default_options(optimal_scan=scan)
+        ecasq.ecasq_solve_optimal(x, s, lam, options=o)  # warm-up
+        torch.cuda.synchronize()
+        ecasq.ecasq_timing_enable(True)
+        ecasq.ecasq_timing_read(ecasq.TIMING_OPT, reset=True)
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            cb, rk, info = ecasq.ecasq_solve_optimal(x, s, lam, options=o)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) / reps * 1e3
+        kms, launches, cands = ecasq.ecasq_timing_read(ecasq.TIMING_OPT)
+        ecasq.ecasq_timing_enable(False)
+        r = {"ms_per_solve": ms, "p": info["p"], "t": info["t"], "objective": info["objective"],
+             "vnmse": info["vnmse"], "entropy": info["entropy"],
+             "layer_ms_per_solve": kms / reps, "layer_launches": launches // reps}
+        if scan == 1 and kms > 0:
+            achieved = OPT_FLOPS_PER_CANDIDATE * cands / (kms * 1e-3) / 1e12
+            r["roofline"] = {"bound": "alu", "kernel": "k_opt_layer<full> (fp64 VALU)",
+                             "achieved": achieved, "peak": FP64_VECTOR_PEAK_TFLOPS,
+                             "unit": "TFLOP/s", "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
+                             "candidates_per_s": cands / (kms * 1e-3),
+                             "avg_launch_ms": kms / max(launches, 1)}
+        out[name] = r
+    out["speedup_monotone"] = out["full"]["ms_per_solve"] / out["monotone"]["ms_per_solve"]
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -199,6 +238,10 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=32768)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-batched", action="store_true")
+    ap.add_argument("--no-optimal", action="store_true",
+                    help="skip the optimal-DP solves (bf16 weights, s = 64, lambda = 0.1)")
+    ap.add_argument("--optimal-only", action="store_true",
+                    help="only run the optimal-DP measurement and print it")
     ap.add_argument("--no-alphabet", action="store_true",
                     help="skip the permissible-grid solves (uniform / quantile, 4096 points)")
     ap.add_argument("--dp-schedule", type=int, default=None, choices=(0, 1),
@@ -228,6 +271,10 @@ def main():
     import torch
 
     from paper_2608_18147_amd import ecasq, inputs
+
+    if args.optimal_only:
+        print(json.dumps(optimal_rate(torch, ecasq, inputs)), flush=True)
+        return
 
     w = inputs.WORKLOADS[args.workload]
     if "rows" in w:
@@ -361,6 +408,8 @@ def main():
         out["alphabet"] = alphabet_rate(torch, ecasq, xd, s, b, opts, info)
         for r in out["alphabet"]:
             r["speedup"] = out["ms_per_step"] / r["ms_per_solve_step"]
+    if not args.no_optimal:
+        out["optimal"] = optimal_rate(torch, ecasq, inputs)
     if not args.no_batched:
         out["batched"] = batched_rate(torch, ecasq, inputs)
     if not args.no_cpu_baseline:

@@ -487,16 +487,17 @@ def test_search_matches_dense_lambda_grid():
     for b in (1.3, 1.8, 2.2, 2.9):
         best = min(m for hh, m in pts if hh <= b)
         found = []
-        for width in (1, 8):
-            sr = pipeline.search(H, s, b, width=width)
+        for width, aim in ((1, True), (1, False), (8, True)):
+            sr = pipeline.search(H, s, b, width=width, aim=aim)
             assert sr["status"] == 0 and sr["H"] <= b
             assert sr["M"] <= best * (1 + 1e-12)
             # A and B adjacent on the lower hull: the final slope lies between
             # the multipliers A and B were found at
             assert sr["lam_final"] <= sr["lam"] or sr["lam"] == 0.0
             found.append((sr["H"], sr["M"], sr["t"]))
-        # both schedules end at the same supported point
-        assert found[0] == found[1]
+        # every schedule (aimed or plain sequential, passes of 8) ends at the
+        # same supported point
+        assert found[0] == found[1] == found[2]
 
 
 def test_budget_sweep_shares_solves():
