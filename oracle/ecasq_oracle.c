@@ -611,12 +611,31 @@ typedef struct {
     int32_t t;
 } point_t;
 
+int orc_opt_dp(const double *v, const double *N, const double *S, const double *S2, int64_t p,
+               int64_t d, int32_t s, int32_t exact_s, double lamp, int32_t *chain, double *out,
+               int32_t *Kdump, double *Fdump);
+
+/* One point of the search on the optimal DP (Sec. 4): r[1] = MSE and
+ * r[2] = H(Xhat) of the optimal codebook at lamp (from its chain, as the
+ * metrics sum them), r[3] = t, r[4] = cells. */
+static void opt_point(const double *v, const double *N, const double *S, const double *S2,
+                      int64_t p, int64_t d, int32_t s, int32_t exact_s, double lamp, double *r)
+{
+    int32_t *chain = malloc(sizeof(int32_t) * (size_t)(s > 2 ? s : 2));
+    double o[3], m[6];
+    orc_opt_dp(v, N, S, S2, p, d, s, exact_s, lamp, chain, o, NULL, NULL);
+    orc_chain_metrics(v, N, S, S2, p, d, (int32_t)o[1], chain, 0.0, m);
+    r[0] = o[0]; r[1] = m[0]; r[2] = m[2]; r[3] = o[1]; r[4] = o[2];
+    free(chain);
+}
+
 int orc_search(const double *v, const double *N, const double *S, const double *S2, int64_t p,
                int64_t d, int32_t s, double b, int32_t exact_s, int32_t max_passes, int32_t width,
-               int32_t aim, double *cache, int32_t *ncache, int32_t cache_cap, double *traj,
-               int32_t traj_cap, double *out)
+               int32_t aim, int32_t dp_kind, double *cache, int32_t *ncache, int32_t cache_cap,
+               double *traj, int32_t traj_cap, double *out)
 {
     if (width != 1 && width != SEARCH_M) return -1;
+    if (dp_kind == 1 && width != 1) return -1;
     hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
     double r[5];
     int32_t nsol = 0, npass = 0;
@@ -635,11 +654,18 @@ int orc_search(const double *v, const double *N, const double *S, const double *
         /* every value is used; nothing to search */
         out[0] = 0.0; out[1] = 0.0; out[2] = 0.0; out[3] = (double)p; out[4] = 0; out[5] = 0;
         out[6] = 0; out[7] = 0.0; out[8] = 0;
+        out[9] = out[10] = out[11] = out[12] = NAN;
         if (p == 2) {
             double C, P;
             cell_terms(&H, 0, 1, &C, &P);
             out[1] = 0.0 - P;
             out[2] = (0.0 + C) / H.s2tot;
+            if (dp_kind == 1) {
+                int32_t two[2] = {0, 1};
+                double m[6];
+                orc_chain_metrics(v, N, S, S2, p, d, 2, two, 0.0, m);
+                out[1] = m[2];
+            }
             if (out[1] > b) out[6] = -3;
         }
         free(pts);
@@ -653,7 +679,10 @@ int orc_search(const double *v, const double *N, const double *S, const double *
         int hit_ = 0;                                                                         \
         for (int x_ = 0; x_ < npts; x_++) if (pts[x_].lam == l_) { hit_ = 1; break; }          \
         if (!hit_) {                                                                          \
-            orc_dp_forward(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, r, NULL, NULL, NULL); \
+            if (dp_kind == 1)                                                                 \
+                opt_point(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, r);                    \
+            else                                                                              \
+                orc_dp_forward(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, r, NULL, NULL, NULL); \
             if (npts < MAX_PTS) {                                                             \
                 pts[npts].lam = l_; pts[npts].H = r[2]; pts[npts].M = r[1] / H.s2tot;        \
                 pts[npts].t = (int32_t)r[3]; npts++;                                           \
@@ -681,7 +710,7 @@ int orc_search(const double *v, const double *N, const double *S, const double *
     int32_t status = 0;
     point_t A, B;
     double lam_final = 0.0;
-    int have_B = 0, closed = 0, force_chord = 0;
+    int have_A = 0, have_B = 0, closed = 0, force_chord = 0;
     for (;;) {
         /* A: infeasible point of largest lambda; B: feasible point of smallest
            lambda (first occurrence wins among equal lambdas) */
@@ -694,16 +723,23 @@ int orc_search(const double *v, const double *N, const double *S, const double *
             }
         }
         if (ia < 0) { /* lambda = 0 is feasible */
-            B = pts[ib]; have_B = 1; lam_final = B.lam;
+            B = pts[ib]; have_B = 1; have_A = 0; lam_final = B.lam;
             break;
         }
         A = pts[ia];
+        have_A = 1;
         if (ib >= 0) {
             B = pts[ib]; closed = 0;
         } else if (b >= 1.0) {
             double C, P;
             cell_terms(&H, 0, p - 1, &C, &P);
             B.lam = INFINITY; B.H = 0.0 - P; B.M = (0.0 + C) / H.s2tot; B.t = 2; closed = 1;
+            if (dp_kind == 1) { /* H(Xhat) of {v_0, v_{p-1}} */
+                int32_t two[2] = {0, (int32_t)(p - 1)};
+                double m[6];
+                orc_chain_metrics(v, N, S, S2, p, d, 2, two, 0.0, m);
+                B.H = m[2];
+            }
         } else {
             /* no feasible point yet: try the largest multiplier once */
             int tried = 0;
@@ -712,7 +748,7 @@ int orc_search(const double *v, const double *N, const double *S, const double *
                 /* infeasible budget: return the lowest-entropy point found */
                 int ih = 0;
                 for (int x = 1; x < npts; x++) if (pts[x].H < pts[ih].H) ih = x;
-                B = pts[ih]; have_B = 1; status = -3; lam_final = B.lam;
+                B = pts[ih]; have_B = 1; have_A = 0; status = -3; lam_final = B.lam;
                 break;
             }
             EVAL(0x1p40);
@@ -772,6 +808,9 @@ int orc_search(const double *v, const double *N, const double *S, const double *
     }
     out[0] = B.lam; out[1] = B.H; out[2] = B.M; out[3] = B.t; out[4] = nsol; out[5] = cells;
     out[6] = status; out[7] = lam_final; out[8] = npass;
+    /* A: the infeasible point the final chord starts from (NaN if none) */
+    out[9] = have_A ? A.lam : NAN; out[10] = have_A ? A.H : NAN;
+    out[11] = have_A ? A.M : NAN; out[12] = have_A ? (double)A.t : NAN;
     free(pts);
     return 0;
 }

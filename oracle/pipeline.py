@@ -227,12 +227,15 @@ class LambdaCache:
         self.cap = cap
 
 
-def search(H, s, b, exact_s=False, max_passes=32, width=8, cache=None, aim=True):
+def search(H, s, b, exact_s=False, max_passes=32, width=8, cache=None, aim=True, dp="approx"):
     """Budget search on lambda in passes of `width` (8 or 1) multipliers; with
     a LambdaCache, points solved by earlier searches are reused.  aim: width-1
     queries aimed at H = b before the certifying chord query (the batched row
-    solver runs the plain chord search: aim=False)."""
-    out = np.zeros(9)
+    solver runs the plain chord search: aim=False).  dp: 'approx' searches the
+    approximate DP's (H(I,B), vNMSE) points, 'optimal' the optimal DP's
+    (H(Xhat), vNMSE) points (width 1).  Also returns A, the infeasible point
+    the final chord starts from (lamA etc. NaN when there is none)."""
+    out = np.zeros(13)
     cap = 1024
     traj = np.zeros(4 * cap)
     if cache is not None:
@@ -240,13 +243,15 @@ def search(H, s, b, exact_s=False, max_passes=32, width=8, cache=None, aim=True)
     else:
         cptr, nptr, ccap = None, None, 0
     rc = native.lib().orc_search(*H.args(), s, b, int(exact_s), max_passes, width, int(aim),
-                                 cptr, nptr, ccap, native.dptr(traj), cap, native.dptr(out))
+                                 1 if dp == "optimal" else 0, cptr, nptr, ccap,
+                                 native.dptr(traj), cap, native.dptr(out))
     if rc != 0:
         raise ValueError("search width must be 1 or 8")
     n = int(out[4])
     return dict(lam=out[0], H=out[1], M=out[2], t=int(out[3]), solves=n, cells=int(out[5]),
                 status=int(out[6]), lam_final=out[7], passes=int(out[8]),
-                traj=traj[: 4 * min(n, cap)].reshape(-1, 4))
+                traj=traj[: 4 * min(n, cap)].reshape(-1, 4), lamA=out[9], HA=out[10],
+                MA=out[11], tA=-1 if math.isnan(out[12]) else int(out[12]))
 
 
 @dataclass
@@ -280,14 +285,19 @@ def _finish(H, chain, lam, solves, rounds, cells, status, traj=None):
                   cells=cells, status=status, traj=traj)
 
 
-def _recover(H, t, lam, recovery="hirschberg", s=None, exact_s=False):
+def _recover(H, t, lam, recovery="hirschberg", s=None, exact_s=False, dp="approx"):
     """Codebook (unique indices) with t values at lambda (vNMSE units): by
     Hirschberg (Sec. 5), or by a traceback through the argmins of a solve at
-    the same multiplier ('backpointers')."""
+    the same multiplier ('backpointers'); the optimal DP's own traceback for
+    dp='optimal'."""
     if H.p == 1:
         return np.zeros(1, dtype=np.int32), 0
     if t == 2 or not math.isfinite(lam):
         return np.array([0, H.p - 1], dtype=np.int32), 0
+    if dp == "optimal":
+        r = opt_dp(H, s, lam * H.s2tot, exact_s)
+        assert r["t"] == t
+        return r["chain"], 0
     if recovery == "backpointers":
         r = dp_forward(H, s, lam * H.s2tot, exact_s, backpointers=True)
         assert r["t"] == t
@@ -296,13 +306,17 @@ def _recover(H, t, lam, recovery="hirschberg", s=None, exact_s=False):
 
 
 def solve(x, s, b, refine_rounds=5, exhaustive=False, exact_s=False, max_passes=32,
-          recovery="hirschberg", width=8, aim=True, alphabet=None):
+          recovery="hirschberg", width=8, aim=True, alphabet=None, dp="approx"):
     """Budget mode: the lowest-MSE supported solution with H(I,B) <= b
     (recovered at the multiplier it was found at), then refinement at the
-    final chord slope with the budget guard on H(Xhat)."""
+    final chord slope with the budget guard on H(Xhat).  dp='optimal': the
+    lowest-MSE supported solution of the optimal DP with H(Xhat) <= b (width
+    1, no refinement)."""
     H = prepare(x, alphabet)
-    sr = search(H, s, b, exact_s, max_passes, width, aim=aim)
-    chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s)
+    if dp == "optimal":
+        width, refine_rounds = 1, 0
+    sr = search(H, s, b, exact_s, max_passes, width, aim=aim, dp=dp)
+    chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s, dp)
     lam = sr["lam_final"]
     rounds = 0
     if refine_rounds > 0 and math.isfinite(lam) and len(chain) >= 3:
@@ -314,16 +328,19 @@ def solve(x, s, b, refine_rounds=5, exhaustive=False, exact_s=False, max_passes=
 
 
 def solve_budgets(x, s, budgets, refine_rounds=5, exhaustive=False, exact_s=False,
-                  max_passes=32, recovery="hirschberg", width=8, aim=True, alphabet=None):
+                  max_passes=32, recovery="hirschberg", width=8, aim=True, alphabet=None,
+                  dp="approx"):
     """Budget mode for several budgets on one input, in the given order, the
     searches sharing one LambdaCache.  Per budget as solve(); dp_solves and
     cells count the solves that budget's search ran."""
     H = prepare(x, alphabet)
+    if dp == "optimal":
+        width, refine_rounds = 1, 0
     cache = LambdaCache()
     res = []
     for b in budgets:
-        sr = search(H, s, b, exact_s, max_passes, width, cache, aim)
-        chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s)
+        sr = search(H, s, b, exact_s, max_passes, width, cache, aim, dp)
+        chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s, dp)
         lam = sr["lam_final"]
         rounds = 0
         if refine_rounds > 0 and math.isfinite(lam) and len(chain) >= 3:
@@ -383,16 +400,52 @@ def solve_optimal(x, s, lam, exact_s=False, alphabet=None):
     return res
 
 
-def uniforms(n, seed):
-    """u_i in [0,1): 53 bits of Philox4x32-10(counter=(i_lo, i_hi, 0, 0),
-    key=(seed_lo, seed_hi)), words 0 and 1."""
+def solve_timeshare(x, s, b, exact_s=False, max_passes=32, recovery="backpointers", width=1,
+                    aim=True, alphabet=None, dp="approx"):
+    """Two-way time-sharing (Sec. 7, App. E): the search's final pair, B (the
+    best supported point with H <= b, 'minus') and A (the supported point the
+    final chord starts from, H > b, 'plus'), and the share alpha of entries
+    quantized with A such that alpha H_A + (1 - alpha) H_B = b, H being the
+    search's entropy (H(I,B) for the approximate DP, H(Xhat) for the optimal
+    DP).  Without such a pair (lambda = 0 feasible, an infeasible budget,
+    p <= 2) alpha = 0 and both quantizers are B.  No refinement.
+    Returns dict(minus, plus (Results), alpha, H_mix, M_mix, status, solves,
+    cells)."""
+    H = prepare(x, alphabet)
+    if dp == "optimal":
+        width = 1
+    sr = search(H, s, b, exact_s, max_passes, width, aim=aim, dp=dp)
+    cm, c1 = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s, dp)
+    alpha = 0.0
+    cp, c2 = cm, 0
+    lam_p = sr["lam"]
+    if sr["status"] == 0 and sr["tA"] > 0 and H.p > 2:
+        alpha = (b - sr["H"]) / (sr["HA"] - sr["H"])
+        cp, c2 = _recover(H, sr["tA"], sr["lamA"], recovery, s, exact_s, dp)
+        lam_p = sr["lamA"]
+    cells = sr["cells"] + c1 + c2
+    minus = _finish(H, cm, sr["lam"], sr["solves"], 0, cells, sr["status"])
+    plus = _finish(H, cp, lam_p, sr["solves"], 0, cells, sr["status"])
+    minus.passes = plus.passes = sr["passes"]
+    HA = sr["HA"] if alpha > 0.0 else sr["H"]
+    MA = sr["MA"] if alpha > 0.0 else sr["M"]
+    return dict(minus=minus, plus=plus, alpha=alpha, H_mix=alpha * HA + (1.0 - alpha) * sr["H"],
+                M_mix=alpha * MA + (1.0 - alpha) * sr["M"], status=sr["status"],
+                solves=sr["solves"], cells=cells, HA=HA, HB=sr["H"], MA=MA, MB=sr["M"])
+
+
+def uniforms(n, seed, stream=0):
+    """u_i in [0,1): 53 bits of Philox4x32-10(counter=(i_lo, i_hi, stream, 0),
+    key=(seed_lo, seed_hi)), words 0 and 1.  Stream 0 drives the rounding,
+    stream 1 the time-sharing partition."""
     i = np.arange(n, dtype=np.uint64)
     c0 = (i & np.uint64(0xFFFFFFFF)).astype(np.uint64)
     c1 = (i >> np.uint64(32)).astype(np.uint64)
     z = np.zeros(n, dtype=np.uint64)
+    c2 = np.full(n, stream, dtype=np.uint64)
     k0 = np.full(n, seed & 0xFFFFFFFF, dtype=np.uint64)
     k1 = np.full(n, (seed >> 32) & 0xFFFFFFFF, dtype=np.uint64)
-    w0, w1, _, _ = philox4x32_10(c0, c1, z, z, k0, k1)
+    w0, w1, _, _ = philox4x32_10(c0, c1, c2, z, k0, k1)
     bits = ((w1 << np.uint64(32)) | w0) >> np.uint64(11)
     return bits.astype(np.float64) * 2.0 ** -53
 
@@ -419,3 +472,47 @@ def quantize(x, codebook, seed):
             y = nq / n
             ent -= y * math.log2(y)
     return sym, hist, ent
+
+
+def _plugin_entropy(sym, t):
+    n = len(sym)
+    hist = np.bincount(sym, minlength=t).astype(np.int64)
+    ent = 0.0
+    for nq in hist:
+        if nq > 0:
+            y = nq / n
+            ent -= y * math.log2(y)
+    return hist, ent
+
+
+def quantize_timeshare(x, cb_minus, cb_plus, alpha, seed):
+    """Time-shared final rounding (Sec. 7): entry i uses cb_plus iff its
+    partition uniform (Philox stream 1) is below alpha, else cb_minus, and is
+    then rounded as quantize() rounds it (stream 0), its symbol indexing its
+    own codebook.  The two parts are entropy-coded separately: the entropy is
+    (n_minus H_minus + n_plus H_plus) / d with each part's plug-in entropy.
+    Returns (symbols, part (1 = plus), hist (minus counts then plus counts),
+    entropy)."""
+    xf = np.asarray(x).astype(np.float64).ravel() + 0.0
+    n = len(xf)
+    part = (uniforms(n, seed, 1) < alpha).astype(np.uint8)
+    sym = np.zeros(n, dtype=np.uint8)
+    u = uniforms(n, seed, 0)
+    ent = 0.0
+    hists = []
+    for which, q in ((0, cb_minus), (1, cb_plus)):
+        q = np.asarray(q, dtype=np.float64)
+        t = len(q)
+        sel = part == which
+        if t == 1:
+            sy = np.zeros(int(sel.sum()), dtype=np.uint8)
+        else:
+            xs = xf[sel]
+            r = np.clip(np.searchsorted(q, xs, side="left") - 1, 0, t - 2)
+            pu = (xs - q[r]) / (q[r + 1] - q[r])
+            sy = (r + (u[sel] < pu)).astype(np.uint8)
+        sym[sel] = sy
+        hist, e = _plugin_entropy(sy, t) if len(sy) else (np.zeros(t, dtype=np.int64), 0.0)
+        hists.append(hist)
+        ent += len(sy) * e
+    return sym, part, np.concatenate(hists), ent / n

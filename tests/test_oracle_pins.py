@@ -406,6 +406,110 @@ def test_optimal_argmins_monotone_lemma_quadrangle():
     assert checked > 20000 and viol <= 3, (checked, viol)
 
 
+def _lower_hull_at(points, b):
+    """min M over mixtures of (H, M) points with H <= b: the lower convex
+    envelope up to the lowest-M point, flat after it."""
+    mstar = min(m for _, m in points)
+    hstar = min(h for h, m in points if m == mstar)
+    if b >= hstar:
+        return mstar
+    pts = sorted(set(pt for pt in points if pt[0] <= hstar))
+    hull = []
+    for pt in pts:
+        while len(hull) >= 2:
+            (x1, y1), (x2, y2) = hull[-2], hull[-1]
+            if (x2 - x1) * (pt[1] - y1) - (y2 - y1) * (pt[0] - x1) <= 0:
+                hull.pop()
+            else:
+                break
+        hull.append(pt)
+    if b >= hull[-1][0]:
+        return min(y for _, y in hull)
+    for (x1, y1), (x2, y2) in zip(hull, hull[1:]):
+        if x1 <= b <= x2:
+            return y1 + (y2 - y1) * (b - x1) / (x2 - x1)
+    return math.inf
+
+
+def test_timesharing_reaches_the_convex_frontier():
+    """Sec. 7 / App. E: the two-way time-share of the search's final pair has
+    rate b and the vNMSE of the lower convex envelope of every spanning
+    codebook's (H, vNMSE) at b, so no single codebook with H <= b does
+    better; with the optimal DP the entropy is H(Xhat) (the paper's optimality
+    for every b), with the approximate DP it is H(I,B)."""
+    checked = mixed = 0
+    for x, s, _ in _tiny_inputs(40, 41):
+        if len(set(x.tolist())) < 4:
+            continue
+        for dp, which in (("optimal", "out"), ("approx", "sur")):
+            pts = []
+            for Q in plain.spanning_codebooks(x, s):
+                Hq = (plain.entropy_out(x, Q) if which == "out"
+                      else plain.entropy_surrogate(x, Q))
+                pts.append((float(Hq), float(plain.vnmse(x, Q))))
+            hmin, hmax = min(p[0] for p in pts), max(p[0] for p in pts)
+            for frac in (0.2, 0.45, 0.7, 0.9):
+                b = hmin + frac * (hmax - hmin)
+                if b < 1.0 and hmin > b:
+                    continue
+                r = pipeline.solve_timeshare(x, s, b, dp=dp)
+                if r["status"] != 0:
+                    continue
+                hull = _lower_hull_at(pts, b)
+                assert r["M_mix"] <= hull + 1e-12, (x, s, b, dp)
+                assert hull <= r["M_mix"] + 1e-12, (x, s, b, dp)
+                single = min(m for hq, m in pts if hq <= b + 1e-12)
+                assert r["M_mix"] <= single + 1e-12
+                if r["alpha"] > 0.0:
+                    mixed += 1
+                    assert abs(r["H_mix"] - b) <= 1e-12
+                    assert 0.0 < r["alpha"] < 1.0 and r["HB"] <= b < r["HA"]
+                    # the pair is the codebooks' own (H, vNMSE)
+                    pl, mi = r["plus"], r["minus"]
+                    Hp = pl.entropy if dp == "optimal" else pl.entropy_surrogate
+                    Hm = mi.entropy if dp == "optimal" else mi.entropy_surrogate
+                    assert abs(Hp - r["HA"]) <= 1e-12 and abs(Hm - r["HB"]) <= 1e-12
+                    assert abs(pl.vnmse - r["MA"]) <= 1e-12 and abs(mi.vnmse - r["MB"]) <= 1e-12
+                checked += 1
+    assert checked > 100 and mixed > 40, (checked, mixed)
+
+
+def test_timeshared_rounding():
+    """Time-shared rounding: alpha = 0 and alpha = 1 reduce to the plain
+    rounding with one codebook; the share of entries on the second codebook
+    is alpha (binomial); every entry stays unbiased; the entropy is the
+    size-weighted plug-in entropy of the two parts."""
+    rng = np.random.default_rng(42)
+    x = rng.standard_normal(20000).astype(np.float32)
+    lo, hi = float(x.min()), float(x.max())
+    cm = np.array([lo, -0.5, 0.7, hi])
+    cp = np.array([lo, -1.0, 0.0, 1.0, hi])
+    sym0, _, _ = pipeline.quantize(x, cm, 7)[:3]
+    s0, part0, h0, e0 = pipeline.quantize_timeshare(x, cm, cp, 0.0, 7)
+    assert not part0.any() and np.array_equal(s0, sym0)
+    assert abs(e0 - pipeline.quantize(x, cm, 7)[2]) <= 1e-15
+    s1, part1, _, _ = pipeline.quantize_timeshare(x, cm, cp, 1.0, 7)
+    assert part1.all() and np.array_equal(s1, pipeline.quantize(x, cp, 7)[0])
+    alpha = 0.37
+    s, part, hist, ent = pipeline.quantize_timeshare(x, cm, cp, alpha, 9)
+    n = len(x)
+    z = (part.sum() - alpha * n) / math.sqrt(n * alpha * (1 - alpha))
+    assert abs(z) < 5
+    assert hist.sum() == n and hist[:4].sum() == n - part.sum()
+    e_m = pipeline._plugin_entropy(s[part == 0], 4)[1]
+    e_p = pipeline._plugin_entropy(s[part == 1], 5)[1]
+    assert abs(ent - ((n - part.sum()) * e_m + part.sum() * e_p) / n) <= 1e-12
+    # unbiased: the mean reconstruction over seeds tends to x
+    xs = x[:200]
+    acc = np.zeros(len(xs))
+    seeds = 300
+    for sd in range(seeds):
+        sy, pt, _, _ = pipeline.quantize_timeshare(xs, cm, cp, alpha, 1000 + sd)
+        acc += np.where(pt == 1, cp[np.minimum(sy, 4)], cm[np.minimum(sy, 3)])
+    err = acc / seeds - xs.astype(np.float64)
+    assert abs(err.mean()) < 0.02 and np.abs(err).max() < 0.35
+
+
 def test_entropy_sandwich_per_codebook():
     """eq. apx_entropy_sandwich: H(Xhat) <= H(I,B) <= H(Xhat) + 1 for every Q."""
     rng = np.random.default_rng(7)
