@@ -70,8 +70,12 @@ typedef struct {
                                   alphabet_size points over [min X, max X]; 2 the input
                                   values at alphabet_size evenly spaced ranks */
     int32_t alphabet_size;     /* grid points m, 2 <= m <= d (alphabet 1 and 2) */
-    int32_t optimal_scan;      /* ecasq_solve_optimal: 0 monotone brackets (Sec. 4.1,
-                                  default), 1 every predecessor */
+    int32_t optimal_scan;      /* optimal DP: 0 monotone brackets (Sec. 4.1, default),
+                                  1 every predecessor */
+    int32_t dp_objective;      /* budget modes: 0 the search runs on dp_APX and its
+                                  H(I,B) (default); 1 on the optimal DP of
+                                  ecasq_solve_optimal and H(Xhat) (search_width and
+                                  the refinement are then ignored) */
 } ecasq_options;
 
 typedef struct {
@@ -212,6 +216,48 @@ ecasq_status ecasq_solve_lagrangian(const void *x, ecasq_dtype dt, int64_t d, in
 ecasq_status ecasq_solve_optimal(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
                                  double lambda, const ecasq_options *opts, void *stream,
                                  double *codebook, int32_t *codebook_rank, ecasq_info *info);
+
+/*
+ * Two-way time-sharing (Sec. 7, App. E): the lambda search for b ends at two
+ * adjacent supported points, B with H <= b (the codebook ecasq_solve returns
+ * before refinement) and A with H > b (the point the final chord starts
+ * from); quantizing a share alpha = (b - H_B) / (H_A - H_B) of the entries
+ * with A and the rest with B has rate exactly b and the vNMSE of the
+ * convexified frontier at b, alpha vNMSE_A + (1 - alpha) vNMSE_B.  H is the
+ * search's entropy: H(I,B) with opts->dp_objective = 0, H(Xhat) with 1 (then
+ * the time-share is optimal for every b).  Without such a pair (lambda = 0
+ * feasible, an infeasible budget, p <= 2) alpha = 0 and both rows hold B.
+ * No refinement (the points of the frontier are used as they are).
+ *
+ * codebooks: device, 2 x s fp64: row 0 = B ("minus", t = infos[0].t values),
+ * row 1 = A ("plus"); codebook_ranks: device, 2 x s int32, may be NULL;
+ * alpha: host, the share of entries quantized with row 1; infos: host, 2
+ * entries (each quantizer's own metrics; lambda = the multiplier it was found
+ * at; dp_solves, cells, search_passes of the search), may be NULL.  Returns
+ * ECASQ_EINFEASIBLE for an infeasible budget; errors as ecasq_solve_ex.
+ */
+ecasq_status ecasq_solve_timeshare(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
+                                   double bits_per_entry, const ecasq_options *opts,
+                                   void *stream, double *codebooks, int32_t *codebook_ranks,
+                                   double *alpha, ecasq_info *infos);
+
+/*
+ * Time-shared final rounding (Sec. 7): entry i uses codebook1 iff the 53-bit
+ * uniform of Philox4x32-10 with counter (i mod 2^32, i / 2^32, 1, 0) and key
+ * (seed mod 2^32, seed / 2^32) is below alpha (shared randomness: a decoder
+ * with the seed knows the partition), else codebook0, and is then rounded
+ * exactly as ecasq_quantize rounds (counter word 2 = 0), its symbol indexing
+ * its own codebook.  part: device, d bytes (1 = codebook1), may be NULL.
+ * The two parts are entropy-coded separately: *empirical_entropy (device) =
+ * (n_0 H_0 + n_1 H_1) / d with each part's plug-in entropy over its own
+ * entries; hist: device, t0 + t1 int64 counts (codebook0's first), may be NULL.
+ * 0 <= alpha <= 1; 1 <= t0, t1 <= 256.
+ */
+ecasq_status ecasq_quantize_timeshare(const void *x, ecasq_dtype dt, int64_t d,
+                                      const double *codebook0, int32_t t0,
+                                      const double *codebook1, int32_t t1, double alpha,
+                                      uint64_t seed, void *stream, uint8_t *symbols,
+                                      uint8_t *part, double *empirical_entropy, int64_t *hist);
 
 /*
  * Final stochastic rounding (Sec. 2): symbol i in [0, t) for every entry of x

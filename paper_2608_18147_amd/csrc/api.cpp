@@ -116,6 +116,8 @@ struct Ctx {
     int32_t solves;
     bool own;
     bool sweep;  // dp_APX by the column-block sweep (else layer by layer)
+    int32_t objective = 0;  // search points: 0 dp_APX (H(I,B)), 1 the optimal DP (H(Xhat))
+    int32_t opt_full = 0;   // optimal DP: scan every predecessor
 
     template <class T>
     T* at(size_t off) const {
@@ -402,10 +404,75 @@ ecasq_status dp_solve1(Ctx& c, double lam, int32_t exact_s, Point& out) {
     return dp_solve(c, &lam, 1, exact_s, &out, nullptr, nullptr);
 }
 
-// Result of the budget search: B (the codebook to recover), the multiplier of
-// the refinement step and the number of passes.
+
+// Optimal lambda-ECASQ at lamp: the codebook (value indices) and the DP's own
+// value.  Ftrace / Ktrace: every layer, for the inspection entry point.
+ecasq_status opt_solve(Ctx& c, double lam, int32_t exact_s, std::vector<int32_t>& chain,
+                       double* J, double* Ftrace, int32_t* Ktrace) {
+    if (c.p == 1) {
+        chain.assign(1, 0);
+        *J = 0.0;
+        return ECASQ_OK;
+    }
+    if (c.p > kOptMaxP) return ECASQ_ENOMEM;
+    const int32_t imax = (int32_t)std::min<int64_t>(c.s, c.p);
+    const size_t bytes = opt_workspace_bytes(c.p, imax, Ktrace != nullptr);
+    void* mem = nullptr;
+    if (hipMallocAsync(&mem, bytes, c.st) != hipSuccess) return ECASQ_ENOMEM;
+    int32_t* ch = c.at<int32_t>(c.L.chain);
+    double* res = c.at<double>(c.L.mres);
+    const hipError_t e = launch_opt(c.H, imax, exact_s, lam * c.s2tot, c.opt_full,
+                                    static_cast<char*>(mem), ch, res, Ftrace, Ktrace, c.st);
+    double r[2] = {0.0, 0.0};
+    hipError_t e2 = hipSuccess;
+    if (e == hipSuccess) e2 = hipMemcpyAsync(r, res, sizeof r, hipMemcpyDeviceToHost, c.st);
+    (void)hipFreeAsync(mem, c.st);
+    HIP_TRY(hipStreamSynchronize(c.st));
+    HIP_TRY(e);
+    HIP_TRY(e2);
+    const int32_t t = (int32_t)r[1];
+    if (t < 2 || t > imax) return ECASQ_EHIP;
+    chain.resize(t);
+    HIP_TRY(hipMemcpy(chain.data(), ch, sizeof(int32_t) * t, hipMemcpyDeviceToHost));
+    *J = r[0];
+    c.cells += opt_cells(c.p, imax, exact_s);
+    c.solves += 1;
+    return ECASQ_OK;
+}
+
+
+// A search point of the optimal DP: its codebook's H(Xhat) and vNMSE, summed
+// over the chain by the metrics kernel.
+ecasq_status opt_point(Ctx& c, double lam, int32_t exact_s, Point& out) {
+    std::vector<int32_t> chain;
+    double J = 0.0;
+    ECASQ_TRY(opt_solve(c, lam, exact_s, chain, &J, nullptr, nullptr));
+    int32_t* ch = c.at<int32_t>(c.L.chain);
+    double* mres = c.at<double>(c.L.mres);
+    HIP_TRY(hipMemcpyAsync(ch, chain.data(), sizeof(int32_t) * chain.size(),
+                           hipMemcpyHostToDevice, c.st));
+    HIP_TRY(launch_metrics(c.H, (int32_t)chain.size(), ch, 0.0, c.s2tot, mres, c.st));
+    double m[6];
+    HIP_TRY(hipMemcpyAsync(m, mres, sizeof m, hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    out.lam = lam;
+    out.H = m[2];
+    out.M = m[0] / c.s2tot;
+    out.t = (int32_t)chain.size();
+    out.chain = chain;
+    if (timing_verbose())
+        std::fprintf(stderr, "[ecasq] optimal solve lambda=%.6g H(Xhat)=%.6f vNMSE=%.6g t=%d\n",
+                     lam, out.H, out.M, out.t);
+    return ECASQ_OK;
+}
+
+// Result of the budget search: B (the codebook to recover), A (the infeasible
+// point the final chord starts from, if any), the multiplier of the
+// refinement step and the number of passes.
 struct SearchResult {
     Point B;
+    Point A;
+    bool have_A = false;
     double lam_final;
     int32_t passes;
     ecasq_status status;
@@ -434,7 +501,9 @@ ecasq_status eval_pass(Ctx& c, const double* q, int32_t n, int32_t exact_s,
     solved = m;
     if (m == 0) return ECASQ_OK;
     Point out[kMaxLambdas];
-    if (c.sweep || m == 1) {
+    if (c.objective == 1) {
+        for (int32_t g = 0; g < m; g++) ECASQ_TRY(opt_point(c, todo[g], exact_s, out[g]));
+    } else if (c.sweep || m == 1) {
         for (int32_t g = 0; g < m; g++) ECASQ_TRY(dp_solve(c, todo + g, 1, exact_s, out + g, nullptr, nullptr));
     } else {
         for (int32_t g = m; g < kMaxLambdas; g++) todo[g] = todo[m - 1];
@@ -461,6 +530,7 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
     static const double kGrid[kMaxLambdas] = {0.0, 1e-4, 1e-3, 1e-2, 1e-1, 1.0, 10.0, 100.0};
     static const double kMul[kMaxLambdas - 1] = {0.25, 0.5, 0.75, 1.5, 2.0, 3.0, 4.0};
     if (width != 1 && width != kMaxLambdas) return ECASQ_EINVAL;
+    if (c.objective == 1) width = 1;
     std::vector<Point> pts;
     if (cache) pts = *cache;
     const size_t ncached = pts.size();
@@ -471,7 +541,7 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
     R.lam_final = 0.0;
     Point A, B;
     Point two;
-    bool have_two = false;
+    bool have_two = false, have_A = false;
     bool force_chord = false;
     for (;;) {
         int ia = -1, ib = -1;
@@ -484,10 +554,12 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
         }
         if (ia < 0) {  // lambda = 0 is feasible
             B = pts[ib];
+            have_A = false;
             R.lam_final = B.lam;
             break;
         }
         A = pts[ia];
+        have_A = true;
         bool closed = false;
         if (ib >= 0) {
             B = pts[ib];
@@ -503,7 +575,7 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
                 HIP_TRY(hipMemcpyAsync(m, mres, sizeof m, hipMemcpyDeviceToHost, c.st));
                 HIP_TRY(hipStreamSynchronize(c.st));
                 two.lam = HUGE_VAL;
-                two.H = m[3];
+                two.H = c.objective == 1 ? m[2] : m[3];
                 two.M = (0.0 + m[0]) / c.s2tot;
                 two.t = 2;
                 have_two = true;
@@ -521,6 +593,7 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
                 for (int x = 1; x < (int)pts.size(); x++)
                     if (pts[x].H < pts[ih].H) ih = x;
                 B = pts[ih];
+                have_A = false;
                 R.status = ECASQ_EINFEASIBLE;
                 R.lam_final = B.lam;
                 break;
@@ -563,6 +636,8 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
         }
     }
     R.B = B;
+    R.A = A;
+    R.have_A = have_A;
     R.passes = npass;
     if (cache) cache->insert(cache->end(), pts.begin() + ncached, pts.end());
     return ECASQ_OK;
@@ -740,6 +815,7 @@ ecasq_options defaults() {
     o.alphabet = 0;
     o.alphabet_size = 0;
     o.optimal_scan = 0;
+    o.dp_objective = 0;
     o.recovery = 0;
     return o;
 }
@@ -749,7 +825,8 @@ bool options_ok(const ecasq_options& o) {
            o.exact_s >= 0 && o.exact_s <= 1 && o.max_search_passes >= 1 && o.recovery >= 0 &&
            o.recovery <= 1 && (o.search_width == 1 || o.search_width == kMaxLambdas) &&
            o.dp_schedule >= 0 && o.dp_schedule <= 1 && o.alphabet >= 0 && o.alphabet <= 2 &&
-           o.optimal_scan >= 0 && o.optimal_scan <= 1;
+           o.optimal_scan >= 0 && o.optimal_scan <= 1 && o.dp_objective >= 0 &&
+           o.dp_objective <= 1;
 }
 
 // the grid size of a permissible alphabet must lie in [2, d]
@@ -767,6 +844,8 @@ ecasq_status solve_budget(const void* x, int dt, int64_t d, int32_t s, double b,
         ~Closer() { ctx_close(c); }
     } closer{c};
     ECASQ_TRY(ctx_prep(c, x, dt, o.alphabet, o.alphabet_size));
+    c.objective = o.dp_objective;
+    c.opt_full = o.optimal_scan;
     std::vector<int32_t> chain;
     ecasq_status status = ECASQ_OK;
     double lam = 0.0;
@@ -784,8 +863,12 @@ ecasq_status solve_budget(const void* x, int dt, int64_t d, int32_t s, double b,
         else
             ECASQ_TRY(recover(c, R.B.t, R.B.lam, o.exact_s, o.recovery, chain));
     }
-    ecasq_status st = finish(c, chain, lam, b, true, o, codebook, rank, info, status, passes);
-    if (c.p == 2 && info && info->entropy_surrogate > b) {
+    ecasq_options fo = o;
+    if (o.dp_objective == 1) fo.refine_rounds = 0;  // the optimal DP's point as it is
+    ecasq_info local;
+    if (!info) info = &local;
+    ecasq_status st = finish(c, chain, lam, b, true, fo, codebook, rank, info, status, passes);
+    if (c.p == 2 && (o.dp_objective == 1 ? info->entropy : info->entropy_surrogate) > b) {
         info->status = ECASQ_EINFEASIBLE;
         st = ECASQ_EINFEASIBLE;
     }
@@ -802,6 +885,10 @@ ecasq_status solve_budgets(const void* x, int dt, int64_t d, int32_t s, int32_t 
         ~Closer() { ctx_close(c); }
     } closer{c};
     ECASQ_TRY(ctx_prep(c, x, dt, o.alphabet, o.alphabet_size));
+    c.objective = o.dp_objective;
+    c.opt_full = o.optimal_scan;
+    ecasq_options fo = o;
+    if (o.dp_objective == 1) fo.refine_rounds = 0;
     std::vector<Point> cache;
     ecasq_status worst = ECASQ_OK;
     for (int32_t k = 0; k < nb; k++) {
@@ -828,9 +915,9 @@ ecasq_status solve_budgets(const void* x, int dt, int64_t d, int32_t s, int32_t 
         ecasq_info* info = infos ? infos + k : nullptr;
         ecasq_info local;
         if (!info) info = &local;
-        ecasq_status st = finish(c, chain, lam, b, true, o, codebooks + (int64_t)k * s,
+        ecasq_status st = finish(c, chain, lam, b, true, fo, codebooks + (int64_t)k * s,
                                  ranks ? ranks + (int64_t)k * s : nullptr, info, status, passes);
-        if (c.p == 2 && info->entropy_surrogate > b) {
+        if (c.p == 2 && (o.dp_objective == 1 ? info->entropy : info->entropy_surrogate) > b) {
             info->status = ECASQ_EINFEASIBLE;
             st = ECASQ_EINFEASIBLE;
         }
@@ -840,6 +927,64 @@ ecasq_status solve_budgets(const void* x, int dt, int64_t d, int32_t s, int32_t 
             return st;
     }
     return worst;
+}
+
+// Two-way time-sharing (Sec. 7): the search's final pair B (H <= b) and A
+// (H > b) and the share alpha of entries on A with alpha H_A + (1-alpha) H_B = b.
+ecasq_status solve_timeshare(const void* x, int dt, int64_t d, int32_t s, double b,
+                             const ecasq_options& o, void* stream, double* codebooks,
+                             int32_t* ranks, double* alpha_out, ecasq_info* infos) {
+    Ctx c;
+    ECASQ_TRY(ctx_open(c, d, s, ws_flags(o), stream, nullptr, 0));
+    struct Closer {
+        Ctx& c;
+        ~Closer() { ctx_close(c); }
+    } closer{c};
+    ECASQ_TRY(ctx_prep(c, x, dt, o.alphabet, o.alphabet_size));
+    c.objective = o.dp_objective;
+    c.opt_full = o.optimal_scan;
+    std::vector<int32_t> cm, cp;
+    ecasq_status status = ECASQ_OK;
+    double alpha = 0.0, lam_m = 0.0, lam_p = 0.0;
+    int32_t passes = 0;
+    if (c.p <= 2) {
+        for (int64_t k = 0; k < c.p; k++) cm.push_back((int32_t)k);
+        cp = cm;
+    } else {
+        SearchResult R;
+        ECASQ_TRY(search(c, b, o.exact_s, o.max_search_passes, o.search_width, R));
+        status = R.status;
+        passes = R.passes;
+        lam_m = lam_p = R.B.lam;
+        if (!R.B.chain.empty())
+            cm = R.B.chain;
+        else
+            ECASQ_TRY(recover(c, R.B.t, R.B.lam, o.exact_s, o.recovery, cm));
+        cp = cm;
+        if (status == ECASQ_OK && R.have_A) {
+            alpha = (b - R.B.H) / (R.A.H - R.B.H);
+            lam_p = R.A.lam;
+            if (!R.A.chain.empty())
+                cp = R.A.chain;
+            else
+                ECASQ_TRY(recover(c, R.A.t, R.A.lam, o.exact_s, o.recovery, cp));
+        }
+    }
+    ecasq_options fo = o;
+    fo.refine_rounds = 0;  // the supported points themselves
+    ecasq_info local[2];
+    ecasq_info* inf = infos ? infos : local;
+    // finish returns the status it is given; only other codes are errors
+    ecasq_status e = finish(c, cm, lam_m, b, true, fo, codebooks, ranks, inf, status, passes);
+    if (e != status) return e;
+    e = finish(c, cp, lam_p, b, true, fo, codebooks + s, ranks ? ranks + s : nullptr, inf + 1,
+               status, passes);
+    if (e != status) return e;
+    if (c.p == 2 && (o.dp_objective == 1 ? inf[0].entropy : inf[0].entropy_surrogate) > b)
+        status = ECASQ_EINFEASIBLE;
+    inf[0].status = inf[1].status = status;
+    if (alpha_out) *alpha_out = alpha;
+    return status;
 }
 
 }  // namespace
@@ -930,44 +1075,6 @@ ecasq_status ecasq_solve_lagrangian(const void* x, ecasq_dtype dt, int64_t d, in
                   0);
 }
 
-namespace {
-
-// Optimal lambda-ECASQ at lamp: the codebook (value indices) and the DP's own
-// value.  Ftrace / Ktrace: every layer, for the inspection entry point.
-ecasq_status opt_solve(Ctx& c, double lam, const ecasq_options& o, std::vector<int32_t>& chain,
-                       double* J, double* Ftrace, int32_t* Ktrace) {
-    if (c.p == 1) {
-        chain.assign(1, 0);
-        *J = 0.0;
-        return ECASQ_OK;
-    }
-    if (c.p > kOptMaxP) return ECASQ_ENOMEM;
-    const int32_t imax = (int32_t)std::min<int64_t>(c.s, c.p);
-    const size_t bytes = opt_workspace_bytes(c.p, imax, Ktrace != nullptr);
-    void* mem = nullptr;
-    if (hipMallocAsync(&mem, bytes, c.st) != hipSuccess) return ECASQ_ENOMEM;
-    int32_t* ch = c.at<int32_t>(c.L.chain);
-    double* res = c.at<double>(c.L.mres);
-    const hipError_t e = launch_opt(c.H, imax, o.exact_s, lam * c.s2tot, o.optimal_scan,
-                                    static_cast<char*>(mem), ch, res, Ftrace, Ktrace, c.st);
-    double r[2] = {0.0, 0.0};
-    hipError_t e2 = hipSuccess;
-    if (e == hipSuccess) e2 = hipMemcpyAsync(r, res, sizeof r, hipMemcpyDeviceToHost, c.st);
-    (void)hipFreeAsync(mem, c.st);
-    HIP_TRY(hipStreamSynchronize(c.st));
-    HIP_TRY(e);
-    HIP_TRY(e2);
-    const int32_t t = (int32_t)r[1];
-    if (t < 2 || t > imax) return ECASQ_EHIP;
-    chain.resize(t);
-    HIP_TRY(hipMemcpy(chain.data(), ch, sizeof(int32_t) * t, hipMemcpyDeviceToHost));
-    *J = r[0];
-    c.cells += opt_cells(c.p, imax, o.exact_s);
-    c.solves += 1;
-    return ECASQ_OK;
-}
-
-}  // namespace
 
 ecasq_status ecasq_solve_optimal(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
                                  double lambda, const ecasq_options* opts, void* stream,
@@ -984,9 +1091,10 @@ ecasq_status ecasq_solve_optimal(const void* x, ecasq_dtype dt, int64_t d, int32
         ~Closer() { ctx_close(c); }
     } closer{c};
     ECASQ_TRY(ctx_prep(c, x, dt, o.alphabet, o.alphabet_size));
+    c.opt_full = o.optimal_scan;
     std::vector<int32_t> chain;
     double J = 0.0;
-    ECASQ_TRY(opt_solve(c, lambda, o, chain, &J, nullptr, nullptr));
+    ECASQ_TRY(opt_solve(c, lambda, o.exact_s, chain, &J, nullptr, nullptr));
     ecasq_options fo = o;
     fo.refine_rounds = 0;  // the optimum leaves nothing to refine
     return finish(c, chain, lambda, HUGE_VAL, false, fo, codebook, codebook_rank, info, ECASQ_OK,
@@ -1011,15 +1119,52 @@ ecasq_status ecasq_opt_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s
     ECASQ_TRY(ctx_prep(c, x, dt, o.alphabet, o.alphabet_size));
     const int64_t imax = std::min<int64_t>(s, c.p);
     if (c.p > 1 && (imax + 1) * c.p * c.p > capacity) return ECASQ_EINVAL;
+    c.opt_full = o.optimal_scan;
     std::vector<int32_t> ch;
     double J = 0.0;
-    ECASQ_TRY(opt_solve(c, lambda, o, ch, &J, c.p > 1 ? F : nullptr, c.p > 1 ? K : nullptr));
+    ECASQ_TRY(opt_solve(c, lambda, o.exact_s, ch, &J, c.p > 1 ? F : nullptr,
+                        c.p > 1 ? K : nullptr));
     std::memcpy(chain, ch.data(), sizeof(int32_t) * ch.size());
     out[0] = J;
     out[1] = (double)ch.size();
     out[2] = (double)c.p;
     out[3] = (double)c.cells;
     return ECASQ_OK;
+}
+
+ecasq_status ecasq_solve_timeshare(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
+                                   double bits_per_entry, const ecasq_options* opts, void* stream,
+                                   double* codebooks, int32_t* codebook_ranks, double* alpha,
+                                   ecasq_info* infos) {
+    ECASQ_TRY(check_x(x, dt, d));
+    if (s < 2 || s > 255 || !codebooks || !alpha || !(bits_per_entry >= 0.0)) return ECASQ_EINVAL;
+    const ecasq_options o = opts ? *opts : defaults();
+    if (!options_ok(o) || !alphabet_ok(o, d)) return ECASQ_EINVAL;
+    return solve_timeshare(x, dt, d, s, bits_per_entry, o, stream, codebooks, codebook_ranks,
+                           alpha, infos);
+}
+
+ecasq_status ecasq_quantize_timeshare(const void* x, ecasq_dtype dt, int64_t d,
+                                      const double* codebook0, int32_t t0,
+                                      const double* codebook1, int32_t t1, double alpha,
+                                      uint64_t seed, void* stream, uint8_t* symbols,
+                                      uint8_t* part, double* empirical_entropy, int64_t* hist) {
+    ECASQ_TRY(check_x(x, dt, d));
+    if (!codebook0 || !codebook1 || t0 < 1 || t0 > 256 || t1 < 1 || t1 > 256 || !symbols ||
+        !empirical_entropy || !(alpha >= 0.0 && alpha <= 1.0))
+        return ECASQ_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    void* h = nullptr;
+    const size_t hb = sizeof(unsigned long long) * 512;
+    if (hipMallocAsync(&h, hb, st) != hipSuccess) return ECASQ_ENOMEM;
+    unsigned long long* hh = static_cast<unsigned long long*>(h);
+    ecasq_status rc = ECASQ_OK;
+    if (hipMemsetAsync(hh, 0, hb, st) != hipSuccess ||
+        launch_quantize_ts(x, dt, d, codebook0, t0, codebook1, t1, alpha, seed, symbols, part,
+                           hh, empirical_entropy, hist, st) != hipSuccess)
+        rc = ECASQ_EHIP;
+    if (hipFreeAsync(h, st) != hipSuccess) rc = ECASQ_EHIP;
+    return rc;
 }
 
 ecasq_status ecasq_quantize(const void* x, ecasq_dtype dt, int64_t d, const double* codebook,

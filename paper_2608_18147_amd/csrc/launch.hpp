@@ -147,6 +147,12 @@ hipError_t launch_quantize(const void* x, int dt, int64_t d, const double* codeb
                            hipStream_t st);
 hipError_t launch_entropy(const unsigned long long* hist, int32_t t, int64_t d, double* ent,
                           int64_t* hist_out, hipStream_t st);
+// time-shared rounding with two codebooks (t0, t1 <= 256) and the entropy of
+// its two parts; hist (device, t0 + t1 counters) must start at zero
+hipError_t launch_quantize_ts(const void* x, int dt, int64_t d, const double* cb0, int32_t t0,
+                              const double* cb1, int32_t t1, double alpha, uint64_t seed,
+                              uint8_t* symbols, uint8_t* part, unsigned long long* hist,
+                              double* ent, int64_t* hist_out, hipStream_t st);
 
 // ---- batched.hip ----
 hipError_t launch_batched(const void* x, int dt, int64_t n, int32_t d, int32_t s, double b,

@@ -226,6 +226,87 @@ __global__ __launch_bounds__(256) void k_quantize(const void* __restrict__ x, in
         if (lh[r]) atomicAdd(&hist[r], (unsigned long long)lh[r]);
 }
 
+// Time-shared rounding (Sec. 7): entry i takes the second codebook iff the
+// 53-bit uniform of Philox counter (i_lo, i_hi, 1, 0) is below alpha, and is
+// then rounded with its codebook exactly as k_quantize rounds (counter
+// (i_lo, i_hi, 0, 0)).  hist: the first codebook's t0 counts, then the
+// second's t1; part[i] = 1 for the second.
+template <int DT>
+__global__ __launch_bounds__(256) void k_quantize_ts(
+    const void* __restrict__ x, int64_t d, const double* __restrict__ cb0, int32_t t0,
+    const double* __restrict__ cb1, int32_t t1, double alpha, uint32_t k0, uint32_t k1,
+    uint8_t* __restrict__ symbols, uint8_t* __restrict__ part,
+    unsigned long long* __restrict__ hist) {
+    __shared__ double q[2][kMaxT];
+    __shared__ unsigned int lh[2][kMaxT];
+    for (int r = threadIdx.x; r < kMaxT; r += blockDim.x) {
+        q[0][r] = r < t0 ? cb0[r] : 0.0;
+        q[1][r] = r < t1 ? cb1[r] : 0.0;
+        lh[0][r] = 0u;
+        lh[1][r] = 0u;
+    }
+    __syncthreads();
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < d;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        uint32_t c[4] = {(uint32_t)i, (uint32_t)((uint64_t)i >> 32), 1u, 0u};
+        philox4x32_10(c, k0, k1);
+        const uint64_t pbits = ((((uint64_t)c[1]) << 32) | c[0]) >> 11;
+        const int w = ((double)pbits * 0x1p-53) < alpha ? 1 : 0;
+        const int32_t t = w ? t1 : t0;
+        const double* qq = q[w];
+        uint32_t sym = 0;
+        if (t > 1) {
+            const double xv = load_x<DT>(x, i);
+            int lo = 0, hi = t - 2;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (qq[mid] < xv) lo = mid;
+                else hi = mid - 1;
+            }
+            const double pu = (xv - qq[lo]) / (qq[lo + 1] - qq[lo]);
+            uint32_t e[4] = {(uint32_t)i, (uint32_t)((uint64_t)i >> 32), 0u, 0u};
+            philox4x32_10(e, k0, k1);
+            const uint64_t bits = ((((uint64_t)e[1]) << 32) | e[0]) >> 11;
+            const double uu = (double)bits * 0x1p-53;
+            sym = (uint32_t)lo + (uu < pu ? 1u : 0u);
+        }
+        symbols[i] = (uint8_t)sym;
+        if (part) part[i] = (uint8_t)w;
+        atomicAdd(&lh[w][sym], 1u);
+    }
+    __syncthreads();
+    for (int r = threadIdx.x; r < t0; r += blockDim.x)
+        if (lh[0][r]) atomicAdd(&hist[r], (unsigned long long)lh[0][r]);
+    for (int r = threadIdx.x; r < t1; r += blockDim.x)
+        if (lh[1][r]) atomicAdd(&hist[t0 + r], (unsigned long long)lh[1][r]);
+}
+
+// Entropy of a time-shared rounding: each part's plug-in entropy over its own
+// entries, weighted by its size: (n_0 H_0 + n_1 H_1) / d.
+__global__ void k_entropy_ts(const unsigned long long* __restrict__ hist, int32_t t0, int32_t t1,
+                             int64_t d, double* __restrict__ ent, int64_t* __restrict__ hist_out) {
+    __shared__ double2 tab[kLog2Size];
+    load_log2_table(tab);
+    __syncthreads();
+    if (threadIdx.x != 0) return;
+    double total = 0.0;
+    int32_t base = 0;
+    for (int w = 0; w < 2; w++) {
+        const int32_t t = w ? t1 : t0;
+        unsigned long long n = 0;
+        for (int32_t r = 0; r < t; r++) n += hist[base + r];
+        double H = 0.0;
+        for (int32_t r = 0; r < t; r++) {
+            const unsigned long long c = hist[base + r];
+            if (hist_out) hist_out[base + r] = (int64_t)c;
+            if (c) H = H + hfun((double)c / (double)n, tab);
+        }
+        if (n) total = total + (double)n * H;
+        base += t;
+    }
+    *ent = total / (double)d;
+}
+
 __global__ void k_entropy(const unsigned long long* __restrict__ hist, int32_t t, int64_t d,
                           double* __restrict__ ent, int64_t* __restrict__ hist_out) {
     __shared__ double2 tab[kLog2Size];
@@ -285,6 +366,27 @@ hipError_t launch_quantize(const void* x, int dt, int64_t d, const double* codeb
 hipError_t launch_entropy(const unsigned long long* hist, int32_t t, int64_t d, double* ent,
                           int64_t* hist_out, hipStream_t st) {
     k_entropy<<<1, 64, 0, st>>>(hist, t, d, ent, hist_out);
+    return hipGetLastError();
+}
+
+hipError_t launch_quantize_ts(const void* x, int dt, int64_t d, const double* cb0, int32_t t0,
+                              const double* cb1, int32_t t1, double alpha, uint64_t seed,
+                              uint8_t* symbols, uint8_t* part, unsigned long long* hist,
+                              double* ent, int64_t* hist_out, hipStream_t st) {
+    int64_t g = (d + 255) / 256;
+    if (g > 4096) g = 4096;
+    if (g < 1) g = 1;
+    const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+    if (dt == 0)
+        k_quantize_ts<0><<<(unsigned)g, 256, 0, st>>>(x, d, cb0, t0, cb1, t1, alpha, k0, k1,
+                                                      symbols, part, hist);
+    else if (dt == 1)
+        k_quantize_ts<1><<<(unsigned)g, 256, 0, st>>>(x, d, cb0, t0, cb1, t1, alpha, k0, k1,
+                                                      symbols, part, hist);
+    else
+        k_quantize_ts<2><<<(unsigned)g, 256, 0, st>>>(x, d, cb0, t0, cb1, t1, alpha, k0, k1,
+                                                      symbols, part, hist);
+    k_entropy_ts<<<1, 64, 0, st>>>(hist, t0, t1, d, ent, hist_out);
     return hipGetLastError();
 }
 

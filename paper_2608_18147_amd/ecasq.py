@@ -36,6 +36,7 @@ class ecasq_options(ctypes.Structure):
         ("alphabet", ctypes.c_int32),
         ("alphabet_size", ctypes.c_int32),
         ("optimal_scan", ctypes.c_int32),
+        ("dp_objective", ctypes.c_int32),
     ]
 
 
@@ -75,6 +76,7 @@ EXPORTS = (
     "ecasq_quantize", "ecasq_solve_batched", "ecasq_workspace_size", "ecasq_status_string",
     "ecasq_histogram", "ecasq_dp_trace", "ecasq_timing_enable", "ecasq_timing_read",
     "ecasq_solve_budgets", "ecasq_solve_optimal", "ecasq_opt_trace",
+    "ecasq_solve_timeshare", "ecasq_quantize_timeshare",
 )
 
 
@@ -103,6 +105,10 @@ def lib():
                                       P(ecasq_info)]
     L.ecasq_opt_trace.argtypes = [vp, i32, i64, i32, dbl, P(ecasq_options), vp, i64, vp, vp,
                                   P(i32), P(dbl)]
+    L.ecasq_solve_timeshare.argtypes = [vp, i32, i64, i32, dbl, P(ecasq_options), vp, vp, vp,
+                                        P(dbl), P(ecasq_info)]
+    L.ecasq_quantize_timeshare.argtypes = [vp, i32, i64, vp, i32, vp, i32, dbl,
+                                           ctypes.c_uint64, vp, vp, vp, vp, vp]
     L.ecasq_solve_batched.argtypes = [vp, i32, i64, i64, i32, dbl, P(ecasq_options), vp, vp,
                                       vp, vp]
     L.ecasq_workspace_size.argtypes = [i64, i32, i32]
@@ -118,7 +124,8 @@ def lib():
     L.ecasq_timing_read.restype = None
     for name in ("ecasq_solve", "ecasq_solve_ex", "ecasq_solve_lagrangian", "ecasq_quantize",
                  "ecasq_solve_batched", "ecasq_histogram", "ecasq_dp_trace",
-                 "ecasq_solve_budgets", "ecasq_solve_optimal", "ecasq_opt_trace"):
+                 "ecasq_solve_budgets", "ecasq_solve_optimal", "ecasq_opt_trace",
+                 "ecasq_solve_timeshare", "ecasq_quantize_timeshare"):
         getattr(L, name).restype = i32
     _lib = L
     return L
@@ -257,6 +264,44 @@ def ecasq_opt_trace(x, s, lam, p, options=None, stream=None):
     t = int(out[1])
     return (F.view(imax + 1, p, p), K.view(imax + 1, p, p), list(chain[:t]), out[0],
             int(out[3]))
+
+
+def ecasq_solve_timeshare(x, s, bits_per_entry, options=None, stream=None):
+    """Two-way time-sharing (Sec. 7).  Returns (minus, plus, alpha): minus
+    and plus are (codebook, rank, info dict) of B (H <= b) and A (H > b);
+    alpha is the share of entries quantized with plus."""
+    x = _check_x(x)
+    cb = torch.empty((2, int(s)), dtype=torch.float64, device=x.device)
+    rk = torch.empty((2, int(s)), dtype=torch.int32, device=x.device)
+    infos = (ecasq_info * 2)()
+    alpha = ctypes.c_double(0.0)
+    o = options if options is not None else ecasq_default_options()
+    st = lib().ecasq_solve_timeshare(_ptr(x), _DTYPES[x.dtype], x.numel(), int(s),
+                                     float(bits_per_entry), ctypes.byref(o), _stream(stream),
+                                     _ptr(cb), _ptr(rk), ctypes.byref(alpha), infos)
+    _raise(st, (ECASQ_OK, ECASQ_EINFEASIBLE))
+    out = [(cb[k, :infos[k].t], rk[k, :infos[k].t], infos[k].as_dict()) for k in range(2)]
+    return out[0], out[1], alpha.value
+
+
+def ecasq_quantize_timeshare(x, codebook0, codebook1, alpha, seed, stream=None):
+    """Returns (symbols uint8 [d], part uint8 [d] (1 = codebook1), entropy
+    (0-d fp64 tensor), hist int64 [t0 + t1])."""
+    x = _check_x(x)
+    c0 = codebook0.to(device=x.device, dtype=torch.float64).contiguous()
+    c1 = codebook1.to(device=x.device, dtype=torch.float64).contiguous()
+    t0, t1 = c0.numel(), c1.numel()
+    sym = torch.empty(x.numel(), dtype=torch.uint8, device=x.device)
+    part = torch.empty(x.numel(), dtype=torch.uint8, device=x.device)
+    ent = torch.empty((), dtype=torch.float64, device=x.device)
+    hist = torch.empty(t0 + t1, dtype=torch.int64, device=x.device)
+    st = lib().ecasq_quantize_timeshare(_ptr(x), _DTYPES[x.dtype], x.numel(), _ptr(c0), t0,
+                                        _ptr(c1), t1, float(alpha),
+                                        ctypes.c_uint64(int(seed) & (2 ** 64 - 1)),
+                                        _stream(stream), _ptr(sym), _ptr(part), _ptr(ent),
+                                        _ptr(hist))
+    _raise(st)
+    return sym, part, ent, hist
 
 
 def ecasq_quantize(x, codebook, seed, stream=None):
