@@ -73,9 +73,12 @@ typedef struct {
     int32_t optimal_scan;      /* optimal DP: 0 monotone brackets (Sec. 4.1, default),
                                   1 every predecessor */
     int32_t dp_objective;      /* budget modes: 0 the search runs on dp_APX and its
-                                  H(I,B) (default); 1 on the optimal DP of
-                                  ecasq_solve_optimal and H(Xhat) (search_width and
-                                  the refinement are then ignored) */
+                                  H(I,B), then refines (default); 1 on the optimal DP
+                                  of ecasq_solve_optimal and H(Xhat); 2 on dp_APX's
+                                  codebooks refined at each query's multiplier and
+                                  their H(Xhat), returning the feasible one of lowest
+                                  vNMSE (1, 2: search_width is 1; no refinement after
+                                  the search) */
 } ecasq_options;
 
 typedef struct {

@@ -629,13 +629,36 @@ static void opt_point(const double *v, const double *N, const double *S, const d
     free(chain);
 }
 
+/* One point of the refinement-aware search: the approximate DP's codebook at
+ * lamp (the traceback of its argmins), refined at lamp without a budget guard
+ * (Sec. 6), scored by its own MSE (r[1]) and H(Xhat) (r[2]); r[3] = t,
+ * r[4] = the DP's cells. */
+static void refined_point(const double *v, const double *N, const double *S, const double *S2,
+                          int64_t p, int64_t d, int32_t s, int32_t exact_s, double lamp,
+                          int32_t rounds, int32_t exhaustive, double *r)
+{
+    double o[5], m[6];
+    int32_t *bp = malloc(sizeof(int32_t) * (size_t)(s + 1) * (size_t)p);
+    int32_t *chain = malloc(sizeof(int32_t) * (size_t)(s > 2 ? s : 2));
+    orc_dp_forward(v, N, S, S2, p, d, s, exact_s, lamp, o, bp, NULL, NULL);
+    int32_t t = (int32_t)o[3];
+    orc_traceback(bp, p, t, chain);
+    if (t >= 3 && rounds > 0)
+        orc_refine(v, N, S, S2, p, d, t, chain, lamp, INFINITY, 0, rounds, exhaustive, NULL);
+    orc_chain_metrics(v, N, S, S2, p, d, t, chain, 0.0, m);
+    r[0] = 0.0; r[1] = m[0]; r[2] = m[2]; r[3] = t; r[4] = o[4];
+    free(bp);
+    free(chain);
+}
+
 int orc_search(const double *v, const double *N, const double *S, const double *S2, int64_t p,
                int64_t d, int32_t s, double b, int32_t exact_s, int32_t max_passes, int32_t width,
-               int32_t aim, int32_t dp_kind, double *cache, int32_t *ncache, int32_t cache_cap,
-               double *traj, int32_t traj_cap, double *out)
+               int32_t aim, int32_t dp_kind, int32_t refine_rounds, int32_t refine_exhaustive,
+               double *cache, int32_t *ncache, int32_t cache_cap, double *traj,
+               int32_t traj_cap, double *out)
 {
     if (width != 1 && width != SEARCH_M) return -1;
-    if (dp_kind == 1 && width != 1) return -1;
+    if (dp_kind != 0 && width != 1) return -1;
     hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
     double r[5];
     int32_t nsol = 0, npass = 0;
@@ -660,7 +683,7 @@ int orc_search(const double *v, const double *N, const double *S, const double *
             cell_terms(&H, 0, 1, &C, &P);
             out[1] = 0.0 - P;
             out[2] = (0.0 + C) / H.s2tot;
-            if (dp_kind == 1) {
+            if (dp_kind != 0) {
                 int32_t two[2] = {0, 1};
                 double m[6];
                 orc_chain_metrics(v, N, S, S2, p, d, 2, two, 0.0, m);
@@ -681,6 +704,9 @@ int orc_search(const double *v, const double *N, const double *S, const double *
         if (!hit_) {                                                                          \
             if (dp_kind == 1)                                                                 \
                 opt_point(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, r);                    \
+            else if (dp_kind == 2)                                                            \
+                refined_point(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, refine_rounds,     \
+                              refine_exhaustive, r);                                          \
             else                                                                              \
                 orc_dp_forward(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, r, NULL, NULL, NULL); \
             if (npts < MAX_PTS) {                                                             \
@@ -734,7 +760,7 @@ int orc_search(const double *v, const double *N, const double *S, const double *
             double C, P;
             cell_terms(&H, 0, p - 1, &C, &P);
             B.lam = INFINITY; B.H = 0.0 - P; B.M = (0.0 + C) / H.s2tot; B.t = 2; closed = 1;
-            if (dp_kind == 1) { /* H(Xhat) of {v_0, v_{p-1}} */
+            if (dp_kind != 0) { /* H(Xhat) of {v_0, v_{p-1}} */
                 int32_t two[2] = {0, (int32_t)(p - 1)};
                 double m[6];
                 orc_chain_metrics(v, N, S, S2, p, d, 2, two, 0.0, m);
@@ -808,6 +834,16 @@ int orc_search(const double *v, const double *N, const double *S, const double *
     }
     out[0] = B.lam; out[1] = B.H; out[2] = B.M; out[3] = B.t; out[4] = nsol; out[5] = cells;
     out[6] = status; out[7] = lam_final; out[8] = npass;
+    /* refined points need not lie on a convex curve: the answer is the
+       feasible point of lowest vNMSE found (the first among equals) */
+    if (dp_kind == 2 && status == 0) {
+        int ib = -1;
+        for (int x = 0; x < npts; x++)
+            if (pts[x].H <= b && (ib < 0 || pts[x].M < pts[ib].M)) ib = x;
+        if (ib >= 0) {
+            out[0] = pts[ib].lam; out[1] = pts[ib].H; out[2] = pts[ib].M; out[3] = pts[ib].t;
+        }
+    }
     /* A: the infeasible point the final chord starts from (NaN if none) */
     out[9] = have_A ? A.lam : NAN; out[10] = have_A ? A.H : NAN;
     out[11] = have_A ? A.M : NAN; out[12] = have_A ? (double)A.t : NAN;

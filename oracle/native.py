@@ -58,7 +58,8 @@ def lib():
     L.orc_chain_metrics.argtypes = hist + [i32, ip, d, dp]
     L.orc_opt_dp.argtypes = hist + [i32, i32, d, ip, dp, ip, dp]
     L.orc_refine.argtypes = hist + [i32, ip, d, d, i32, i32, i32, ip]
-    L.orc_search.argtypes = hist + [i32, d, i32, i32, i32, i32, i32, dp, ip, i32, dp, i32, dp]
+    L.orc_search.argtypes = hist + [i32, d, i32, i32, i32, i32, i32, i32, i32, dp, ip, i32, dp,
+                                    i32, dp]
     L.orc_interval.argtypes = hist + [i64, i64, dp]
     L.orc_dp_columns.argtypes = hist + [i32, d, dp, dp, dp, i64, i64p, dp, ip, dp, dp]
     L.orc_dp_columns.restype = None

@@ -227,14 +227,18 @@ class LambdaCache:
         self.cap = cap
 
 
-def search(H, s, b, exact_s=False, max_passes=32, width=8, cache=None, aim=True, dp="approx"):
+def search(H, s, b, exact_s=False, max_passes=32, width=8, cache=None, aim=True, dp="approx",
+           refine_rounds=5, exhaustive=False):
     """Budget search on lambda in passes of `width` (8 or 1) multipliers; with
     a LambdaCache, points solved by earlier searches are reused.  aim: width-1
     queries aimed at H = b before the certifying chord query (the batched row
     solver runs the plain chord search: aim=False).  dp: 'approx' searches the
     approximate DP's (H(I,B), vNMSE) points, 'optimal' the optimal DP's
-    (H(Xhat), vNMSE) points (width 1).  Also returns A, the infeasible point
-    the final chord starts from (lamA etc. NaN when there is none)."""
+    (H(Xhat), vNMSE) points (width 1), 'refined' the points (H(Xhat), vNMSE)
+    of the approximate DP's codebooks after refinement at their multiplier
+    (width 1; the answer is the feasible point of lowest vNMSE found).  Also
+    returns A, the infeasible point the final chord starts from (lamA etc.
+    NaN when there is none)."""
     out = np.zeros(13)
     cap = 1024
     traj = np.zeros(4 * cap)
@@ -242,8 +246,9 @@ def search(H, s, b, exact_s=False, max_passes=32, width=8, cache=None, aim=True,
         cptr, nptr, ccap = native.dptr(cache.pts), native.iptr(cache.n), cache.cap
     else:
         cptr, nptr, ccap = None, None, 0
+    kind = {"approx": 0, "optimal": 1, "refined": 2}[dp]
     rc = native.lib().orc_search(*H.args(), s, b, int(exact_s), max_passes, width, int(aim),
-                                 1 if dp == "optimal" else 0, cptr, nptr, ccap,
+                                 kind, refine_rounds, int(exhaustive), cptr, nptr, ccap,
                                  native.dptr(traj), cap, native.dptr(out))
     if rc != 0:
         raise ValueError("search width must be 1 or 8")
@@ -285,7 +290,8 @@ def _finish(H, chain, lam, solves, rounds, cells, status, traj=None):
                   cells=cells, status=status, traj=traj)
 
 
-def _recover(H, t, lam, recovery="hirschberg", s=None, exact_s=False, dp="approx"):
+def _recover(H, t, lam, recovery="hirschberg", s=None, exact_s=False, dp="approx",
+             refine_rounds=5, exhaustive=False):
     """Codebook (unique indices) with t values at lambda (vNMSE units): by
     Hirschberg (Sec. 5), or by a traceback through the argmins of a solve at
     the same multiplier ('backpointers'); the optimal DP's own traceback for
@@ -298,6 +304,14 @@ def _recover(H, t, lam, recovery="hirschberg", s=None, exact_s=False, dp="approx
         r = opt_dp(H, s, lam * H.s2tot, exact_s)
         assert r["t"] == t
         return r["chain"], 0
+    if dp == "refined":
+        r = dp_forward(H, s, lam * H.s2tot, exact_s, backpointers=True)
+        assert r["t"] == t
+        chain = r["chain_bp"]
+        if refine_rounds > 0 and len(chain) >= 3:
+            chain, _, _ = refine(H, chain, lam * H.s2tot, math.inf, False, refine_rounds,
+                                 exhaustive)
+        return chain, 0
     if recovery == "backpointers":
         r = dp_forward(H, s, lam * H.s2tot, exact_s, backpointers=True)
         assert r["t"] == t
@@ -313,10 +327,12 @@ def solve(x, s, b, refine_rounds=5, exhaustive=False, exact_s=False, max_passes=
     lowest-MSE supported solution of the optimal DP with H(Xhat) <= b (width
     1, no refinement)."""
     H = prepare(x, alphabet)
-    if dp == "optimal":
+    rr = refine_rounds
+    if dp != "approx":
         width, refine_rounds = 1, 0
-    sr = search(H, s, b, exact_s, max_passes, width, aim=aim, dp=dp)
-    chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s, dp)
+    sr = search(H, s, b, exact_s, max_passes, width, aim=aim, dp=dp, refine_rounds=rr,
+                exhaustive=exhaustive)
+    chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s, dp, rr, exhaustive)
     lam = sr["lam_final"]
     rounds = 0
     if refine_rounds > 0 and math.isfinite(lam) and len(chain) >= 3:
@@ -334,13 +350,14 @@ def solve_budgets(x, s, budgets, refine_rounds=5, exhaustive=False, exact_s=Fals
     searches sharing one LambdaCache.  Per budget as solve(); dp_solves and
     cells count the solves that budget's search ran."""
     H = prepare(x, alphabet)
-    if dp == "optimal":
+    rr = refine_rounds
+    if dp != "approx":
         width, refine_rounds = 1, 0
     cache = LambdaCache()
     res = []
     for b in budgets:
-        sr = search(H, s, b, exact_s, max_passes, width, cache, aim, dp)
-        chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s, dp)
+        sr = search(H, s, b, exact_s, max_passes, width, cache, aim, dp, rr, exhaustive)
+        chain, hcells = _recover(H, sr["t"], sr["lam"], recovery, s, exact_s, dp, rr, exhaustive)
         lam = sr["lam_final"]
         rounds = 0
         if refine_rounds > 0 and math.isfinite(lam) and len(chain) >= 3:

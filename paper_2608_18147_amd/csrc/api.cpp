@@ -116,8 +116,11 @@ struct Ctx {
     int32_t solves;
     bool own;
     bool sweep;  // dp_APX by the column-block sweep (else layer by layer)
-    int32_t objective = 0;  // search points: 0 dp_APX (H(I,B)), 1 the optimal DP (H(Xhat))
+    // search points: 0 dp_APX (H(I,B)), 1 the optimal DP (H(Xhat)), 2 dp_APX's
+    // codebook refined at the query's multiplier (H(Xhat))
+    int32_t objective = 0;
     int32_t opt_full = 0;   // optimal DP: scan every predecessor
+    int32_t refine_rounds = 0, refine_exhaustive = 0, recovery = 0;
 
     template <class T>
     T* at(size_t off) const {
@@ -466,6 +469,40 @@ ecasq_status opt_point(Ctx& c, double lam, int32_t exact_s, Point& out) {
     return ECASQ_OK;
 }
 
+ecasq_status recover(Ctx& c, int32_t t, double lam, int32_t exact_s, int32_t mode,
+                     std::vector<int32_t>& chain);
+
+// A point of the refinement-aware search: dp_APX's codebook at lambda (the
+// argmin traceback of the solve), refined at lambda without a budget guard
+// (Sec. 6), scored by its own H(Xhat) and vNMSE.
+ecasq_status refined_point(Ctx& c, double lam, int32_t exact_s, Point& out) {
+    Point P;
+    ECASQ_TRY(dp_solve(c, &lam, 1, exact_s, &P, nullptr, nullptr));
+    std::vector<int32_t> chain = P.chain;
+    if (chain.empty()) ECASQ_TRY(recover(c, P.t, lam, exact_s, c.recovery, chain));
+    const int32_t t = (int32_t)chain.size();
+    int32_t* ch = c.at<int32_t>(c.L.chain);
+    int32_t* stats = ch + c.s + 2;
+    double* mres = c.at<double>(c.L.mres);
+    HIP_TRY(hipMemcpyAsync(ch, chain.data(), sizeof(int32_t) * t, hipMemcpyHostToDevice, c.st));
+    if (t >= 3 && c.refine_rounds > 0) {
+        HIP_TRY(hipMemsetAsync(stats, 0, sizeof(int32_t) * 2, c.st));
+        HIP_TRY(launch_refine(c.H, t, ch, lam * c.s2tot, HUGE_VAL, 0, c.refine_rounds,
+                              c.refine_exhaustive, stats, c.st));
+    }
+    HIP_TRY(launch_metrics(c.H, t, ch, 0.0, c.s2tot, mres, c.st));
+    double m[6];
+    HIP_TRY(hipMemcpyAsync(chain.data(), ch, sizeof(int32_t) * t, hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipMemcpyAsync(m, mres, sizeof m, hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    out.lam = lam;
+    out.H = m[2];
+    out.M = m[0] / c.s2tot;
+    out.t = t;
+    out.chain = chain;
+    return ECASQ_OK;
+}
+
 // Result of the budget search: B (the codebook to recover), A (the infeasible
 // point the final chord starts from, if any), the multiplier of the
 // refinement step and the number of passes.
@@ -503,6 +540,8 @@ ecasq_status eval_pass(Ctx& c, const double* q, int32_t n, int32_t exact_s,
     Point out[kMaxLambdas];
     if (c.objective == 1) {
         for (int32_t g = 0; g < m; g++) ECASQ_TRY(opt_point(c, todo[g], exact_s, out[g]));
+    } else if (c.objective == 2) {
+        for (int32_t g = 0; g < m; g++) ECASQ_TRY(refined_point(c, todo[g], exact_s, out[g]));
     } else if (c.sweep || m == 1) {
         for (int32_t g = 0; g < m; g++) ECASQ_TRY(dp_solve(c, todo + g, 1, exact_s, out + g, nullptr, nullptr));
     } else {
@@ -530,7 +569,7 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
     static const double kGrid[kMaxLambdas] = {0.0, 1e-4, 1e-3, 1e-2, 1e-1, 1.0, 10.0, 100.0};
     static const double kMul[kMaxLambdas - 1] = {0.25, 0.5, 0.75, 1.5, 2.0, 3.0, 4.0};
     if (width != 1 && width != kMaxLambdas) return ECASQ_EINVAL;
-    if (c.objective == 1) width = 1;
+    if (c.objective != 0) width = 1;
     std::vector<Point> pts;
     if (cache) pts = *cache;
     const size_t ncached = pts.size();
@@ -575,7 +614,7 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
                 HIP_TRY(hipMemcpyAsync(m, mres, sizeof m, hipMemcpyDeviceToHost, c.st));
                 HIP_TRY(hipStreamSynchronize(c.st));
                 two.lam = HUGE_VAL;
-                two.H = c.objective == 1 ? m[2] : m[3];
+                two.H = c.objective != 0 ? m[2] : m[3];
                 two.M = (0.0 + m[0]) / c.s2tot;
                 two.t = 2;
                 have_two = true;
@@ -634,6 +673,14 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
         } else {
             force_chord = false;
         }
+    }
+    // refined points need not lie on a convex curve: the answer is the
+    // feasible point of lowest vNMSE found (the first among equals)
+    if (c.objective == 2 && R.status == ECASQ_OK) {
+        int ib = -1;
+        for (int x = 0; x < (int)pts.size(); x++)
+            if (pts[x].H <= b && (ib < 0 || pts[x].M < pts[ib].M)) ib = x;
+        if (ib >= 0) B = pts[ib];
     }
     R.B = B;
     R.A = A;
@@ -826,7 +873,7 @@ bool options_ok(const ecasq_options& o) {
            o.recovery <= 1 && (o.search_width == 1 || o.search_width == kMaxLambdas) &&
            o.dp_schedule >= 0 && o.dp_schedule <= 1 && o.alphabet >= 0 && o.alphabet <= 2 &&
            o.optimal_scan >= 0 && o.optimal_scan <= 1 && o.dp_objective >= 0 &&
-           o.dp_objective <= 1;
+           o.dp_objective <= 2;
 }
 
 // the grid size of a permissible alphabet must lie in [2, d]
@@ -846,6 +893,9 @@ ecasq_status solve_budget(const void* x, int dt, int64_t d, int32_t s, double b,
     ECASQ_TRY(ctx_prep(c, x, dt, o.alphabet, o.alphabet_size));
     c.objective = o.dp_objective;
     c.opt_full = o.optimal_scan;
+    c.refine_rounds = o.refine_rounds;
+    c.refine_exhaustive = o.refine_exhaustive;
+    c.recovery = o.recovery;
     std::vector<int32_t> chain;
     ecasq_status status = ECASQ_OK;
     double lam = 0.0;
@@ -864,11 +914,11 @@ ecasq_status solve_budget(const void* x, int dt, int64_t d, int32_t s, double b,
             ECASQ_TRY(recover(c, R.B.t, R.B.lam, o.exact_s, o.recovery, chain));
     }
     ecasq_options fo = o;
-    if (o.dp_objective == 1) fo.refine_rounds = 0;  // the optimal DP's point as it is
+    if (o.dp_objective != 0) fo.refine_rounds = 0;  // the point as the search scored it
     ecasq_info local;
     if (!info) info = &local;
     ecasq_status st = finish(c, chain, lam, b, true, fo, codebook, rank, info, status, passes);
-    if (c.p == 2 && (o.dp_objective == 1 ? info->entropy : info->entropy_surrogate) > b) {
+    if (c.p == 2 && (o.dp_objective != 0 ? info->entropy : info->entropy_surrogate) > b) {
         info->status = ECASQ_EINFEASIBLE;
         st = ECASQ_EINFEASIBLE;
     }
@@ -887,8 +937,11 @@ ecasq_status solve_budgets(const void* x, int dt, int64_t d, int32_t s, int32_t 
     ECASQ_TRY(ctx_prep(c, x, dt, o.alphabet, o.alphabet_size));
     c.objective = o.dp_objective;
     c.opt_full = o.optimal_scan;
+    c.refine_rounds = o.refine_rounds;
+    c.refine_exhaustive = o.refine_exhaustive;
+    c.recovery = o.recovery;
     ecasq_options fo = o;
-    if (o.dp_objective == 1) fo.refine_rounds = 0;
+    if (o.dp_objective != 0) fo.refine_rounds = 0;
     std::vector<Point> cache;
     ecasq_status worst = ECASQ_OK;
     for (int32_t k = 0; k < nb; k++) {
@@ -917,7 +970,7 @@ ecasq_status solve_budgets(const void* x, int dt, int64_t d, int32_t s, int32_t 
         if (!info) info = &local;
         ecasq_status st = finish(c, chain, lam, b, true, fo, codebooks + (int64_t)k * s,
                                  ranks ? ranks + (int64_t)k * s : nullptr, info, status, passes);
-        if (c.p == 2 && (o.dp_objective == 1 ? info->entropy : info->entropy_surrogate) > b) {
+        if (c.p == 2 && (o.dp_objective != 0 ? info->entropy : info->entropy_surrogate) > b) {
             info->status = ECASQ_EINFEASIBLE;
             st = ECASQ_EINFEASIBLE;
         }
@@ -943,6 +996,9 @@ ecasq_status solve_timeshare(const void* x, int dt, int64_t d, int32_t s, double
     ECASQ_TRY(ctx_prep(c, x, dt, o.alphabet, o.alphabet_size));
     c.objective = o.dp_objective;
     c.opt_full = o.optimal_scan;
+    c.refine_rounds = o.refine_rounds;
+    c.refine_exhaustive = o.refine_exhaustive;
+    c.recovery = o.recovery;
     std::vector<int32_t> cm, cp;
     ecasq_status status = ECASQ_OK;
     double alpha = 0.0, lam_m = 0.0, lam_p = 0.0;
@@ -980,7 +1036,7 @@ ecasq_status solve_timeshare(const void* x, int dt, int64_t d, int32_t s, double
     e = finish(c, cp, lam_p, b, true, fo, codebooks + s, ranks ? ranks + s : nullptr, inf + 1,
                status, passes);
     if (e != status) return e;
-    if (c.p == 2 && (o.dp_objective == 1 ? inf[0].entropy : inf[0].entropy_surrogate) > b)
+    if (c.p == 2 && (o.dp_objective != 0 ? inf[0].entropy : inf[0].entropy_surrogate) > b)
         status = ECASQ_EINFEASIBLE;
     inf[0].status = inf[1].status = status;
     if (alpha_out) *alpha_out = alpha;

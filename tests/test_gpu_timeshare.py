@@ -159,3 +159,41 @@ def test_timeshare_full_size_weights():
     share = float(part.sum()) / n
     assert abs(share - alpha) <= 5 * math.sqrt(max(alpha * (1 - alpha), 1e-12) / n) + 1e-12
     assert int(hist.sum()) == n
+
+
+REFINED_CASES = OPT_BUDGET_CASES + [
+    ("weights_2k_b2", lambda: inputs.make("weights_256k", seed=11, d=2048), 16, 2.0, {}),
+    ("student_2k_b1.5", lambda: inputs.make("student_t_1m", seed=11, d=2048), 16, 1.5, {}),
+    ("lognormal_2k_b2.5_exh", lambda: inputs.make("lognormal_16k", seed=11, d=2048), 32, 2.5,
+     dict(refine_exhaustive=1)),
+]
+
+
+@pytest.mark.parametrize("case", REFINED_CASES, ids=[c[0] for c in REFINED_CASES])
+def test_refinement_aware_search_parity(case):
+    """Budget search on the refined codebooks' true H(Xhat) (dp_objective 2):
+    every point is dp_APX's traceback refined at its multiplier; the answer is
+    the feasible point of lowest vNMSE."""
+    name, mk, s, b, o = case
+    x = mk()
+    _say("refined search", name, x.size, s, b)
+    r = pipeline.solve(x, s, b, exact_s=bool(o.get("exact_s", 0)), dp="refined",
+                       recovery="backpointers", width=1, alphabet=_alpha(o),
+                       exhaustive=bool(o.get("refine_exhaustive", 0)))
+    opts = ecasq.ecasq_default_options(dp_objective=2, **o)
+    g = ecasq.ecasq_solve(_dev(x), s, b, options=opts)
+    _compare(g, r)
+    if r.status == 0:
+        assert g[2]["entropy"] <= b
+
+
+def test_refinement_aware_budget_sweep():
+    x = inputs.student_t(3000, 44)
+    budgets = (1.0, 2.0, 3.0)
+    _say("refined budget sweep")
+    rs = pipeline.solve_budgets(x, 16, budgets, refine_rounds=5, recovery="backpointers",
+                                width=1, dp="refined")
+    gs = ecasq.ecasq_solve_budgets(_dev(x), 16, budgets,
+                                   options=ecasq.ecasq_default_options(dp_objective=2))
+    for g, r in zip(gs, rs):
+        _compare(g, r)

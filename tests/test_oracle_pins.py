@@ -474,6 +474,41 @@ def test_timesharing_reaches_the_convex_frontier():
     assert checked > 100 and mixed > 40, (checked, mixed)
 
 
+def test_refinement_aware_search():
+    """Search on the true H(Xhat) of refined codebooks: the answer is
+    feasible (H(Xhat) <= b, recomputed exactly), no better than the brute-force
+    optimum under the same budget, the lowest-vNMSE feasible point among the
+    search's solves, and each solve's point is the refined codebook's own
+    (H(Xhat), vNMSE)."""
+    n = 0
+    for x, s, _ in _tiny_inputs(60, 43):
+        if len(set(x.tolist())) < 4:
+            continue
+        H = pipeline.prepare(x)
+        for b in (1.1, 1.5, 2.0):
+            r = pipeline.solve(x, s, b, dp="refined", recovery="backpointers", width=1)
+            if r.status != 0:
+                continue
+            Hout = float(plain.entropy_out(x, list(r.codebook)))
+            assert Hout <= b + 1e-12 and abs(Hout - r.entropy) <= 1e-12
+            m_opt, _ = plain.brute_force_budget(x, s, b, "out")
+            assert float(m_opt) / float(plain.norm2(x)) <= r.vnmse * (1 + 1e-12) + 1e-15
+            sr = pipeline.search(H, s, b, width=1, dp="refined")
+            feas = [row for row in sr["traj"] if row[1] <= b]
+            if feas:
+                assert min(row[2] for row in feas) == r.vnmse or abs(
+                    min(row[2] for row in feas) - r.vnmse) <= 1e-15
+            for lam, hh, mm, t in sr["traj"][:3]:
+                rr = pipeline.dp_forward(H, s, lam * H.s2tot, backpointers=True)
+                ch = rr["chain_bp"]
+                if len(ch) >= 3:
+                    ch, _, _ = pipeline.refine(H, ch, lam * H.s2tot)
+                m = pipeline.chain_metrics(H, ch, 0.0)
+                assert m["entropy"] == hh and m["mse"] / H.s2tot == mm and len(ch) == t
+            n += 1
+    assert n > 60, n
+
+
 def test_timeshared_rounding():
     """Time-shared rounding: alpha = 0 and alpha = 1 reduce to the plain
     rounding with one codebook; the share of entries on the second codebook
