@@ -263,6 +263,32 @@ ecasq_status ecasq_quantize_timeshare(const void *x, ecasq_dtype dt, int64_t d,
                                       uint8_t *part, double *empirical_entropy, int64_t *hist);
 
 /*
+ * Entropy coding of symbols in [0, t) with rANS (Duda, arXiv:1311.2540), so
+ * that the payload App. F.1 charges at H(Xhat) bits per entry, with a 16-bit
+ * descriptor per codebook value, exists as bytes.  Frequencies
+ * f_q = max(1, floor(n_q 2^16 / d)) of the symbol counts n_q, made to sum to
+ * 2^16 (a surplus to the largest f, lowest q among ties; a deficit one unit at
+ * a time from the largest f > 1); 32-bit state in [2^23, 2^31), bytes out;
+ * segments of 4096 symbols coded independently (one lane each).  Stream:
+ * t little-endian u16 (f_q - 1), then one little-endian u32 per segment (the
+ * end of its bytes from the payload start), then the payload; a segment
+ * starts with its final encoder state, big-endian.
+ *
+ * ecasq_encode_bound: the largest stream for d symbols over t values
+ * (2 t + 8 ceil(d / 4096) + 2 d bytes; 0 for d outside [1, 2^28] or t outside
+ * [1, 256]).  ecasq_encode: symbols and out are device memory, capacity >=
+ * the bound; *out_bytes (host) = the stream's length.  ECASQ_EINVAL if a
+ * symbol is >= t.  ecasq_decode: in (device, in_bytes) -> d symbols (device);
+ * ECASQ_EINVAL for a malformed stream (a segment that overruns its bytes or
+ * does not end in the initial state).  Both return after the stream work.
+ */
+size_t ecasq_encode_bound(int64_t d, int32_t t);
+ecasq_status ecasq_encode(const uint8_t *symbols, int64_t d, int32_t t, void *stream,
+                          uint8_t *out, size_t capacity, int64_t *out_bytes);
+ecasq_status ecasq_decode(const uint8_t *in, int64_t in_bytes, int64_t d, int32_t t,
+                          void *stream, uint8_t *symbols);
+
+/*
  * Final stochastic rounding (Sec. 2): symbol i in [0, t) for every entry of x
  * in its original order.  The bracket is q_r < x <= q_{r+1} (x <= q_0 gives
  * r = 0; x > q_{t-1} is clamped to t-1); the entry rounds up iff

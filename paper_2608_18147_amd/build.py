@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libecasq.so")
 SOURCES = ["prep.hip", "alphabet.hip", "dp.hip", "sweep.hip", "opt.hip", "post.hip",
-           "batched.hip", "api.cpp"]
+           "rans.hip", "batched.hip", "api.cpp"]
 ARCH = os.environ.get("ECASQ_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -1223,6 +1223,60 @@ ecasq_status ecasq_quantize_timeshare(const void* x, ecasq_dtype dt, int64_t d,
     return rc;
 }
 
+size_t ecasq_encode_bound(int64_t d, int32_t t) {
+    if (d < 1 || d > ((int64_t)1 << 28) || t < 1 || t > 256) return 0;
+    return rans_bound(d, t);
+}
+
+ecasq_status ecasq_encode(const uint8_t* symbols, int64_t d, int32_t t, void* stream,
+                          uint8_t* out, size_t capacity, int64_t* out_bytes) {
+    if (!symbols || !out || !out_bytes || d < 1 || d > ((int64_t)1 << 28) || t < 1 || t > 256)
+        return ECASQ_EINVAL;
+    if (capacity < rans_bound(d, t)) return ECASQ_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const size_t sb = rans_scratch_bytes(d);
+    void* mem = nullptr;
+    if (hipMallocAsync(&mem, sb + 512, st) != hipSuccess) return ECASQ_ENOMEM;
+    char* base = static_cast<char*>(mem);
+    auto* bad = reinterpret_cast<unsigned int*>(base + sb);
+    auto* total = reinterpret_cast<unsigned long long*>(base + sb + 256);
+    unsigned long long tot = 0;
+    unsigned int nbad = 0;
+    ecasq_status rc = ECASQ_OK;
+    if (hipMemsetAsync(bad, 0, sizeof(unsigned int), st) != hipSuccess ||
+        launch_rans_encode(symbols, d, t, out, base, total, bad, st) != hipSuccess ||
+        hipMemcpyAsync(&tot, total, sizeof tot, hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipMemcpyAsync(&nbad, bad, sizeof nbad, hipMemcpyDeviceToHost, st) != hipSuccess)
+        rc = ECASQ_EHIP;
+    if (hipFreeAsync(mem, st) != hipSuccess) rc = ECASQ_EHIP;
+    if (hipStreamSynchronize(st) != hipSuccess) rc = ECASQ_EHIP;
+    if (rc != ECASQ_OK) return rc;
+    if (nbad) return ECASQ_EINVAL;
+    *out_bytes = 2 * (int64_t)t + 4 * rans_segments(d) + (int64_t)tot;
+    return ECASQ_OK;
+}
+
+ecasq_status ecasq_decode(const uint8_t* in, int64_t in_bytes, int64_t d, int32_t t, void* stream,
+                          uint8_t* symbols) {
+    if (!in || !symbols || d < 1 || d > ((int64_t)1 << 28) || t < 1 || t > 256)
+        return ECASQ_EINVAL;
+    if (in_bytes < 2 * (int64_t)t + 4 * rans_segments(d)) return ECASQ_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    void* mem = nullptr;
+    if (hipMallocAsync(&mem, 256, st) != hipSuccess) return ECASQ_ENOMEM;
+    auto* bad = static_cast<unsigned int*>(mem);
+    unsigned int nbad = 0;
+    ecasq_status rc = ECASQ_OK;
+    if (hipMemsetAsync(bad, 0, sizeof(unsigned int), st) != hipSuccess ||
+        launch_rans_decode(in, in_bytes, d, t, symbols, bad, st) != hipSuccess ||
+        hipMemcpyAsync(&nbad, bad, sizeof nbad, hipMemcpyDeviceToHost, st) != hipSuccess)
+        rc = ECASQ_EHIP;
+    if (hipFreeAsync(mem, st) != hipSuccess) rc = ECASQ_EHIP;
+    if (hipStreamSynchronize(st) != hipSuccess) rc = ECASQ_EHIP;
+    if (rc != ECASQ_OK) return rc;
+    return nbad ? ECASQ_EINVAL : ECASQ_OK;
+}
+
 ecasq_status ecasq_quantize(const void* x, ecasq_dtype dt, int64_t d, const double* codebook,
                             int32_t t, uint64_t seed, void* stream, uint8_t* symbols,
                             double* empirical_entropy, int64_t* hist) {

@@ -54,6 +54,19 @@ hipError_t launch_opt(const Hist& H, int32_t imax, int32_t exact_s, double lamp,
                       char* mem, int32_t* chain, double* res, double* Ftrace, int32_t* Ktrace,
                       hipStream_t st);
 
+// ---- rans.hip ----
+int64_t rans_segments(int64_t d);
+size_t rans_bound(int64_t d, int32_t t);      // largest coded stream, bytes
+size_t rans_scratch_bytes(int64_t d);
+// out: at least rans_bound(d, t) bytes; *total_out (device) = payload bytes;
+// *bad (device, zeroed by the caller) counts symbols >= t
+hipError_t launch_rans_encode(const uint8_t* sym, int64_t d, int32_t t, uint8_t* out,
+                              char* scratch, unsigned long long* total_out, unsigned int* bad,
+                              hipStream_t st);
+// *bad (device, zeroed by the caller) counts malformed segments
+hipError_t launch_rans_decode(const uint8_t* in, int64_t nin, int64_t d, int32_t t, uint8_t* sym,
+                              unsigned int* bad, hipStream_t st);
+
 // ---- dp.hip ----
 // One DP layer for nlam multipliers (1 or kMaxLambdas); every per-multiplier
 // array below holds nlam valid entries.

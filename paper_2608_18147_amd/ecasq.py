@@ -76,7 +76,8 @@ EXPORTS = (
     "ecasq_quantize", "ecasq_solve_batched", "ecasq_workspace_size", "ecasq_status_string",
     "ecasq_histogram", "ecasq_dp_trace", "ecasq_timing_enable", "ecasq_timing_read",
     "ecasq_solve_budgets", "ecasq_solve_optimal", "ecasq_opt_trace",
-    "ecasq_solve_timeshare", "ecasq_quantize_timeshare",
+    "ecasq_solve_timeshare", "ecasq_quantize_timeshare", "ecasq_encode_bound", "ecasq_encode",
+    "ecasq_decode",
 )
 
 
@@ -109,6 +110,10 @@ def lib():
                                         P(dbl), P(ecasq_info)]
     L.ecasq_quantize_timeshare.argtypes = [vp, i32, i64, vp, i32, vp, i32, dbl,
                                            ctypes.c_uint64, vp, vp, vp, vp, vp]
+    L.ecasq_encode_bound.argtypes = [i64, i32]
+    L.ecasq_encode_bound.restype = ctypes.c_size_t
+    L.ecasq_encode.argtypes = [vp, i64, i32, vp, vp, ctypes.c_size_t, P(i64)]
+    L.ecasq_decode.argtypes = [vp, i64, i64, i32, vp, vp]
     L.ecasq_solve_batched.argtypes = [vp, i32, i64, i64, i32, dbl, P(ecasq_options), vp, vp,
                                       vp, vp]
     L.ecasq_workspace_size.argtypes = [i64, i32, i32]
@@ -125,7 +130,8 @@ def lib():
     for name in ("ecasq_solve", "ecasq_solve_ex", "ecasq_solve_lagrangian", "ecasq_quantize",
                  "ecasq_solve_batched", "ecasq_histogram", "ecasq_dp_trace",
                  "ecasq_solve_budgets", "ecasq_solve_optimal", "ecasq_opt_trace",
-                 "ecasq_solve_timeshare", "ecasq_quantize_timeshare"):
+                 "ecasq_solve_timeshare", "ecasq_quantize_timeshare", "ecasq_encode",
+                 "ecasq_decode"):
         getattr(L, name).restype = i32
     _lib = L
     return L
@@ -302,6 +308,33 @@ def ecasq_quantize_timeshare(x, codebook0, codebook1, alpha, seed, stream=None):
                                         _ptr(hist))
     _raise(st)
     return sym, part, ent, hist
+
+
+def ecasq_encode(symbols, t, stream=None):
+    """rANS-code uint8 symbols (device) over t values.  Returns the stream as
+    a uint8 device tensor."""
+    if not isinstance(symbols, torch.Tensor) or not symbols.is_cuda or symbols.dtype != torch.uint8:
+        raise TypeError("symbols must be a uint8 CUDA (HIP) tensor")
+    sym = symbols.contiguous()
+    d = sym.numel()
+    cap = lib().ecasq_encode_bound(d, int(t))
+    if cap == 0:
+        raise ValueError("d or t out of range")
+    out = torch.empty(cap, dtype=torch.uint8, device=sym.device)
+    n = ctypes.c_int64(0)
+    st = lib().ecasq_encode(_ptr(sym), d, int(t), _stream(stream), _ptr(out), cap,
+                            ctypes.byref(n))
+    _raise(st)
+    return out[: n.value]
+
+
+def ecasq_decode(data, d, t, stream=None):
+    """Decode a stream of ecasq_encode back to d uint8 symbols (device)."""
+    data = data.contiguous()
+    sym = torch.empty(int(d), dtype=torch.uint8, device=data.device)
+    st = lib().ecasq_decode(_ptr(data), data.numel(), int(d), int(t), _stream(stream), _ptr(sym))
+    _raise(st)
+    return sym
 
 
 def ecasq_quantize(x, codebook, seed, stream=None):
