@@ -222,6 +222,45 @@ def optimal_rate(torch, ecasq, inputs, reps=3):
     return out
 
 
+def coding_rate(torch, ecasq, sym, t, info, reps=5):
+    """rANS coding of the final symbols: coded bits per entry (payload,
+    16-bit frequency descriptors, segment table, and a 16-bit value per
+    codebook entry as App. F.1 charges) against H(Xhat) + 32 t / d, and the
+    encode / decode times."""
+    d = sym.numel()
+    data = ecasq.ecasq_encode(sym, t)
+    back = ecasq.ecasq_decode(data, d, t)
+    assert torch.equal(back, sym)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        data = ecasq.ecasq_encode(sym, t)
+    torch.cuda.synchronize()
+    enc_ms = (time.perf_counter() - t0) / reps * 1e3
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        back = ecasq.ecasq_decode(data, d, t)
+    torch.cuda.synchronize()
+    dec_ms = (time.perf_counter() - t0) / reps * 1e3
+    return {"t": t, "d": d, "stream_bytes": int(data.numel()),
+            "coded_bits_per_entry": (8.0 * data.numel() + 16.0 * t) / d,
+            "ideal_rate_total": info["rate_total"], "entropy": info["entropy"],
+            "encode_ms": enc_ms, "decode_ms": dec_ms}
+
+
+def refined_search_rate(torch, ecasq, xd, s, b):
+    """The refinement-aware search (dp_objective 2) on the same input and
+    budget: time per solve step and the codebook's quality."""
+    o = ecasq.ecasq_default_options(dp_objective=2)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    cb, rk, info = ecasq.ecasq_solve(xd, s, b, options=o)
+    torch.cuda.synchronize()
+    return {"ms_per_solve_step": (time.perf_counter() - t0) * 1e3, "dp_solves": info["dp_solves"],
+            "t": info["t"], "vnmse": info["vnmse"], "entropy": info["entropy"],
+            "entropy_surrogate": info["entropy_surrogate"], "objective": info["objective"]}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -242,6 +281,9 @@ def main():
                     help="skip the optimal-DP solves (bf16 weights, s = 64, lambda = 0.1)")
     ap.add_argument("--optimal-only", action="store_true",
                     help="only run the optimal-DP measurement and print it")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the side measurements (grids, optimal DP, refinement-aware\n"
+                         "search, entropy coding, batched rows)")
     ap.add_argument("--no-alphabet", action="store_true",
                     help="skip the permissible-grid solves (uniform / quantile, 4096 points)")
     ap.add_argument("--dp-schedule", type=int, default=None, choices=(0, 1),
@@ -295,10 +337,13 @@ def main():
 
     budgets = list(w["budgets"]) if args.all_budgets else [b]
 
+    last = {}
+
     def step():
         if len(budgets) == 1:
             cb, rk, info = ecasq.ecasq_solve(xd, s, b, options=opts)
             sym, ent, hist = ecasq.ecasq_quantize(xd, cb, args.seed)
+            last["sym"], last["t"] = sym, info["t"]
             return info, ent
         res = ecasq.ecasq_solve_budgets(xd, s, budgets, options=opts)
         agg = dict(res[-1][2])
@@ -404,6 +449,13 @@ def main():
             "empirical_entropy": float(ent), "refine_rounds_run": info["refine_rounds_run"],
         },
     }
+    if args.no_extras:
+        args.no_alphabet = args.no_optimal = args.no_batched = True
+    if not args.no_extras and len(budgets) == 1:
+        out["entropy_coding"] = coding_rate(torch, ecasq, last["sym"], last["t"], info)
+        r = refined_search_rate(torch, ecasq, xd, s, b)
+        r["vnmse_vs_default"] = r["vnmse"] / info["vnmse"]
+        out["refined_search"] = r
     if not args.no_alphabet and len(budgets) == 1:
         out["alphabet"] = alphabet_rate(torch, ecasq, xd, s, b, opts, info)
         for r in out["alphabet"]:
