@@ -52,8 +52,8 @@ TRAFFIC_SOURCES_SHA = "f3a631b21f5b78fb"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
-SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 9.902e7
-SWEEP_TRAFFIC_SHA = "8c7a9db356a3e3ae"
+SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 6.752e7
+SWEEP_TRAFFIC_SHA = "a6e9d1f53623ecbc"
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 
 

@@ -348,7 +348,9 @@ const char *ecasq_status_string(ecasq_status st);
  * accumulated along the argmins (M and Ph, fp64; both NULL or both given).
  * Entries outside a layer's valid columns are unspecified.  out (host,
  * 5 * nlam): per multiplier J (MSE units), MSE, H(I,B) of the minimising
- * path, i*, cells.
+ * path, i*, cells.  Schedule 1 keeps values only and recomputes the argmins
+ * for the dump (an O(s p^2) pass); with kstar, M and Ph all NULL it returns
+ * the values alone.
  */
 ecasq_status ecasq_histogram(const void *x, ecasq_dtype dt, int64_t d, void *stream, double *v,
                              double *N, double *S, double *S2, int64_t *p_out);

@@ -84,7 +84,7 @@ Layout layout(int64_t d, int32_t s, int32_t flags) {
     L.pidx = take(sizeof(int32_t) * np);
     L.swF = take(sweep ? sizeof(double) * (size_t)(s + 1) * (size_t)d : 0);
     L.swK = take(sweep ? sizeof(int32_t) * (size_t)(s + 1) * (size_t)d : 0);
-    L.swchain = take(sizeof(int32_t) * 256);
+    L.swchain = take(sizeof(int32_t) * 528);  // chain, then the traceback state
     L.last = take(sizeof(double) * 3 * (size_t)(s + 1) * kMaxLambdas);
     L.res = take(sizeof(double) * 4 * kMaxLambdas);
     L.mres = take(sizeof(double) * 8);
@@ -238,6 +238,7 @@ ecasq_status sweep_solve(Ctx& c, double lam, int32_t exact_s, Point& out, double
     S.H = c.H;
     S.F = c.at<double>(c.L.swF);
     S.K = c.at<int32_t>(c.L.swK);
+    S.st = c.at<int32_t>(c.L.swchain) + 256;
     S.ld = c.d;
     S.I = imax;
     S.lamp = lam * c.s2tot;
@@ -254,6 +255,7 @@ ecasq_status sweep_solve(Ctx& c, double lam, int32_t exact_s, Point& out, double
         if (dump->F)
             HIP_TRY(hipMemcpyAsync(dump->F + ((int64_t)m * ls + 2) * ds, S.F + 2 * c.d,
                                    sizeof(double) * rows, hipMemcpyDeviceToDevice, c.st));
+        if (dump->K || (dump->M && dump->P)) HIP_TRY(launch_sweep_argmins(S, c.st));
         if (dump->K)
             HIP_TRY(hipMemcpyAsync(dump->K + ((int64_t)m * ls + 2) * ds, S.K + 2 * c.d,
                                    sizeof(int32_t) * rows, hipMemcpyDeviceToDevice, c.st));
@@ -1321,9 +1323,11 @@ ecasq_status ecasq_dp_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
                             const double* lambdas, int32_t schedule, void* stream, double* F,
                             int32_t* kstar, double* M, double* Ph, double* out) {
     ECASQ_TRY(check_x(x, dt, d));
-    if (s < 2 || s > 255 || !F || !kstar || !out || !lambdas) return ECASQ_EINVAL;
+    if (s < 2 || s > 255 || !F || !out || !lambdas) return ECASQ_EINVAL;
     if (nlam != 1 && nlam != kMaxLambdas) return ECASQ_EINVAL;
     if (schedule < 0 || schedule > 1 || ((M == nullptr) != (Ph == nullptr))) return ECASQ_EINVAL;
+    // argmins may be left out under schedule 1 (values only), not with accumulators
+    if (!kstar && (schedule == 0 || M)) return ECASQ_EINVAL;
     for (int32_t m = 0; m < nlam; m++)
         if (!(lambdas[m] >= 0.0) || !std::isfinite(lambdas[m])) return ECASQ_EINVAL;
     Ctx c;

@@ -134,17 +134,22 @@ hipError_t launch_split(const double* Fw, const double* Bw, int64_t ml, int64_t 
 struct SweepSolve {
     Hist H;
     double* F;
-    int32_t* K;
+    int32_t* K;    // argmins on request (launch_sweep_argmins); traceback scratch
+    int32_t* st;   // traceback state, 264 int32
     int64_t ld;    // >= p
     int32_t I;     // last layer, min(s, p), 2..255
     double lamp;   // lambda' in MSE units
 };
 size_t sweep_table_bytes(int64_t d, int32_t s);
-// The sweep, then eq. apx_final: out (device, 4 doubles) = J, MSE, H(I,B), i*;
-// chain (device, optional, >= i* int32): the argmin chain u_0 = 0 .. u_{i*-1} = p-1.
+// The sweep, then eq. apx_final and the traceback (argmins recomputed along
+// the chain): out (device, 4 doubles) = J, MSE, H(I,B), i*; chain (device,
+// optional, >= i* int32): u_0 = 0 .. u_{i*-1} = p-1.
 hipError_t launch_sweep(const SweepSolve& S, int32_t exact_s, double* out, int32_t* chain,
                         hipStream_t st);
-// MSE / H(I,B) accumulators of every layer into M, Ph (same layout as F).
+// The argmin of every layer and valid column into K (after launch_sweep).
+hipError_t launch_sweep_argmins(const SweepSolve& S, hipStream_t st);
+// MSE / H(I,B) accumulators of every layer into M, Ph (same layout as F);
+// needs the argmins in K.
 hipError_t launch_sweep_accumulators(const SweepSolve& S, double* M, double* Ph, hipStream_t st);
 
 // ---- post.hip ----

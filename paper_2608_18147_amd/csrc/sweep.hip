@@ -6,12 +6,19 @@
 // Here the (k, j) triangle is swept once: with F_i[k] final for all layers i
 // and all k of the blocks before column block J, one evaluation of C and Phi
 // serves the candidates F_{i-1}[k] + C + lambda' Phi of every layer.  The
-// price is O(s p) memory (F and the argmins of every layer: 12 (s+1) p bytes,
-// 0.1 GB at p = 2^18, s = 32) instead of O(p) rolling buffers; the values and
-// argmins are the same bit for bit (same candidate arithmetic, lowest k on
-// ties).  With every argmin kept, the codebook is a traceback, and the path's
-// MSE and H(I,B) are summed along it in path order (the same additions the
-// layer-by-layer accumulators perform).
+// price is O(s p) memory (F of every layer: 8 (s+1) p bytes, 0.07 GB at
+// p = 2^18, s = 32) instead of O(p) rolling buffers; the values are the same
+// bit for bit (same candidate arithmetic; the minimum of a set does not depend
+// on the order, up to the sign of an exact zero).
+//
+// The sweep keeps values only: a layer's update per cell is an add, an fma
+// and a min.  With every F_{i-1} kept, the argmin of any (i, j) is recomputed
+// when needed: the traceback of the chosen layer asks for one column per
+// layer (t columns of at most p candidates each, a few hundred microseconds,
+// against O(s p^2) for tracking the argmin of every cell), taking the lowest k
+// among equal candidates exactly as the DP's strict '<' in increasing k does.
+// The path's MSE and H(I,B) are then summed along it in path order (the same
+// additions the layer-by-layer accumulators perform).
 //
 // Step t of the sweep (blocks of 64 columns, one per wavefront) is one launch
 // of k_sweep_step:
@@ -20,9 +27,7 @@
 //                  the previous layer's values of the same block), which
 //                  makes block t final;
 //   the others     blocks J > t: the contribution of block t-1 (final since
-//                  step t-1) to their running minima, kept in F and K.
-// Blocks are visited in increasing order and predecessors in increasing k,
-// so strict '<' keeps the lowest argmin.
+//                  step t-1) to their running minima, kept in F.
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -42,24 +47,26 @@ constexpr int64_t kSplitBelow = ECASQ_SWEEP_SPLIT_BELOW;
 #ifndef ECASQ_SWEEP_LG_MAX
 #define ECASQ_SWEEP_LG_MAX 32
 #endif
+// wavefronts per SIMD the step kernel's registers are sized for (0: the
+// compiler's choice)
+#ifndef ECASQ_SWEEP_WAVES
+#define ECASQ_SWEEP_WAVES 0
+#endif
+#if ECASQ_SWEEP_WAVES > 0
+#define ECASQ_STEP_ATTR __attribute__((amdgpu_waves_per_eu(ECASQ_SWEEP_WAVES)))
+#else
+#define ECASQ_STEP_ATTR
+#endif
 
 struct SweepArgs {
     Hist H;
     double* F;    // [I+1][ld]: rows 2..I; running minima until a block is final
-    int32_t* K;   // argmins, same layout
+    int32_t* K;   // argmins recomputed for inspection (same layout), and scratch
     int64_t ld;
     int32_t I;    // last layer, min(s, p)
     double lamp;  // lambda' (MSE units)
     int64_t nblk;
 };
-
-// Running-minimum update for a predecessor below every column (unmasked):
-// strict '<' keeps the lowest k; min() differs from the select only in the
-// sign of an exact zero.
-__device__ __forceinline__ void take_min(double cand, int32_t k, double& best, int32_t& bk) {
-    bk = cand < best ? k : bk;
-    best = __builtin_fmin(best, cand);
-}
 
 // Stage predecessor block [k0, k0+64): v, N, S, S2 and F_{i-1} for the LG
 // layers i0..i0+LG-1 (+inf past I).  All threads of the workgroup take part.
@@ -82,15 +89,13 @@ __device__ __forceinline__ void stage_block(const SweepArgs& a, int64_t k0, int3
     }
 }
 
-// Rows 2..I of F := +inf, K := -1 (nothing seen yet; also the value of every
-// entry outside a layer's valid columns, which makes such predecessors lose).
+// Rows 2..I of F := +inf (nothing seen yet; also the value of every entry
+// outside a layer's valid columns, which makes such predecessors lose).
 __global__ __launch_bounds__(256) void k_sweep_fill(SweepArgs a) {
     const int64_t n = (int64_t)(a.I - 1) * a.ld;
     for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n;
-         x += (int64_t)gridDim.x * blockDim.x) {
+         x += (int64_t)gridDim.x * blockDim.x)
         a.F[2 * a.ld + x] = __builtin_huge_val();
-        a.K[2 * a.ld + x] = -1;
-    }
 }
 
 // Shared memory of one step workgroup.
@@ -102,69 +107,61 @@ struct StepSmem {
     double dv[kSB], dN[kSB], dS[kSB], dS2[kSB];   // block t (diagonal role)
     double pF[kSB];                               // previous layer of block t
     double partV[kTileWaves][kSB];                // per-wave partial minima
-    int32_t partK[kTileWaves][kSB];
 };
 
-// Running minima of LW layers i0.. of column jj (rows past I: +inf / -1).
+// Running minima of LW layers i0.. of column jj (rows past I: +inf).
 template <int LW>
 __device__ __forceinline__ void load_running(const SweepArgs& a, int64_t jj, int32_t i0,
-                                             double (&best)[LW], int32_t (&bk)[LW]) {
+                                             double (&best)[LW]) {
 #pragma unroll
     for (int l = 0; l < LW; l++) {
         const int32_t i = i0 + l;
-        const bool ok = i <= a.I;
-        best[l] = ok ? a.F[(int64_t)i * a.ld + jj] : __builtin_huge_val();
-        bk[l] = ok ? a.K[(int64_t)i * a.ld + jj] : -1;
+        best[l] = i <= a.I ? a.F[(int64_t)i * a.ld + jj] : __builtin_huge_val();
     }
 }
 
 template <int LW>
 __device__ __forceinline__ void store_running(const SweepArgs& a, int64_t j, int32_t i0,
-                                              const double (&best)[LW], const int32_t (&bk)[LW]) {
+                                              const double (&best)[LW]) {
     if (j >= a.H.p) return;
 #pragma unroll
     for (int l = 0; l < LW; l++) {
         const int32_t i = i0 + l;
-        if (i <= a.I) {
-            a.F[(int64_t)i * a.ld + j] = best[l];
-            a.K[(int64_t)i * a.ld + j] = bk[l];
-        }
+        if (i <= a.I) a.F[(int64_t)i * a.ld + j] = best[l];
     }
 }
 
 // The 64 staged predecessors against column (cv, cN, cS, cS2) for LW layers
 // whose F_{i-1} sit in sF columns lofs..lofs+LW-1.
 template <int LG, int LW>
-__device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int64_t k0, int lofs, double cv,
-                                           double cN, double cS, double cS2, double dd,
-                                           double lamp, double (&best)[LW],
-                                           int32_t (&bk)[LW]) {
+__device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int lofs, double cv, double cN,
+                                           double cS, double cS2, double dd, double lamp,
+                                           double (&best)[LW]) {
     if constexpr (LW > 8) {
         // many layers per predecessor: enough independent work per iteration
         for (int kk = 0; kk < kSB; kk++) {
             double C, P;
             cell_terms(sm.sv[kk], sm.sN[kk], sm.sS[kk], sm.sS2[kk], cv, cN, cS, cS2, dd, false,
                        0.0, sm.tab, C, P);
-            const int32_t k = (int32_t)(k0 + kk);
 #pragma unroll
             for (int l = 0; l < LW; l++)
-                take_min(__builtin_fma(-lamp, P, sm.sF[kk][lofs + l] + C), k, best[l], bk[l]);
+                best[l] = __builtin_fmin(best[l],
+                                         __builtin_fma(-lamp, P, sm.sF[kk][lofs + l] + C));
         }
     } else {
     // few layers: two predecessors per iteration, whose C and Phi are
-    // independent chains the scheduler can interleave; updates keep k order
+    // independent chains the scheduler can interleave
     for (int kk = 0; kk < kSB; kk += 2) {
         double C0, P0, C1, P1;
         cell_terms(sm.sv[kk], sm.sN[kk], sm.sS[kk], sm.sS2[kk], cv, cN, cS, cS2, dd, false, 0.0,
                    sm.tab, C0, P0);
         cell_terms(sm.sv[kk + 1], sm.sN[kk + 1], sm.sS[kk + 1], sm.sS2[kk + 1], cv, cN, cS, cS2,
                    dd, false, 0.0, sm.tab, C1, P1);
-        const int32_t k = (int32_t)(k0 + kk);
 #pragma unroll
         for (int l = 0; l < LW; l++) {
-            take_min(__builtin_fma(-lamp, P0, sm.sF[kk][lofs + l] + C0), k, best[l], bk[l]);
-            take_min(__builtin_fma(-lamp, P1, sm.sF[kk + 1][lofs + l] + C1), k + 1, best[l],
-                     bk[l]);
+            best[l] = __builtin_fmin(best[l], __builtin_fma(-lamp, P0, sm.sF[kk][lofs + l] + C0));
+            best[l] =
+                __builtin_fmin(best[l], __builtin_fma(-lamp, P1, sm.sF[kk + 1][lofs + l] + C1));
         }
     }
     }
@@ -197,17 +194,15 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int32_t split, int64_t 
     const double cv = a.H.v[jj], cN = a.H.N[jj], cS = a.H.S[jj], cS2 = a.H.S2[jj];
     if (split) {
         double best[LW];
-        int32_t bk[LW];
         const int32_t iw = i0 + wave * LW;
-        load_running<LW>(a, jj, iw, best, bk);
-        accumulate<LG, LW>(sm, k0, wave * LW, cv, cN, cS, cS2, a.H.dd, a.lamp, best, bk);
-        store_running<LW>(a, j, iw, best, bk);
+        load_running<LW>(a, jj, iw, best);
+        accumulate<LG, LW>(sm, wave * LW, cv, cN, cS, cS2, a.H.dd, a.lamp, best);
+        store_running<LW>(a, j, iw, best);
     } else {
         double best[LG];
-        int32_t bk[LG];
-        load_running<LG>(a, jj, i0, best, bk);
-        accumulate<LG, LG>(sm, k0, 0, cv, cN, cS, cS2, a.H.dd, a.lamp, best, bk);
-        store_running<LG>(a, j, i0, best, bk);
+        load_running<LG>(a, jj, i0, best);
+        accumulate<LG, LG>(sm, 0, cv, cN, cS, cS2, a.H.dd, a.lamp, best);
+        store_running<LG>(a, j, i0, best);
     }
 }
 
@@ -215,8 +210,7 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int32_t split, int64_t 
 // predecessor block t-1 (LG/4 layers per wavefront), then the group's layers
 // inside the block in order; each wavefront holds C and Phi of 16 of the
 // block's predecessors in registers, the four partial minima meet in LDS and
-// the wavefront that holds the layer's running minimum merges them in
-// increasing k (running minimum first: its k lie in earlier blocks).
+// the wavefront that holds the layer's running minimum merges them.
 template <int LG>
 __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
     constexpr int LW = LG / kTileWaves;
@@ -238,12 +232,13 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
     __syncthreads();
     const int c = (int)(jj - j0);
     const double cv = sm.dv[c], cN = sm.dN[c], cS = sm.dS[c], cS2 = sm.dS2[c];
-    // C and Phi of (k, j) for this wavefront's 16 predecessors k < j
+    // C and Phi of (k, j) for this wavefront's 16 predecessors k < j; the
+    // others get Phi = 0 and C = +inf, so their candidates are +inf
     double cC[KW], cP[KW];
 #pragma unroll
     for (int q = 0; q < KW; q++) {
         const int kk = wave * KW + q;
-        cC[q] = 0.0;
+        cC[q] = __builtin_huge_val();
         cP[q] = 0.0;
         if (j0 + kk < jj)
             cell_terms(sm.dv[kk], sm.dN[kk], sm.dS[kk], sm.dS2[kk], cv, cN, cS, cS2, dd, false,
@@ -257,21 +252,19 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
             cell_at(a.H, 0, j, sm.tab, C, P);
             f = __builtin_fma(-lamp, P, 0.0 + C);
             a.F[2 * a.ld + j] = f;
-            a.K[2 * a.ld + j] = 0;
         }
         sm.pF[lane] = f;
     }
     for (int32_t i0 = 3; i0 <= a.I; i0 += LG) {
         const int32_t iw = i0 + wave * LW;
         double best[LW];
-        int32_t bk[LW];
-        load_running<LW>(a, jj, iw, best, bk);
+        load_running<LW>(a, jj, iw, best);
         __syncthreads();  // previous group's use of sF / pF is over
         if (t >= 1) {
             const int64_t k0 = (t - 1) * kSB;
             stage_pred<LG>(a, k0, i0, sm);
             __syncthreads();
-            accumulate<LG, LW>(sm, k0, wave * LW, cv, cN, cS, cS2, dd, lamp, best, bk);
+            accumulate<LG, LW>(sm, wave * LW, cv, cN, cS, cS2, dd, lamp, best);
         }
         // layer l = ow * LW + q of the group: held by wavefront ow at q
 #pragma unroll 1
@@ -280,55 +273,28 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
         for (int q8 = 0; q8 < LW; q8++) {
             const int32_t i = i0 + ow * LW + q8;
             if (i > a.I) break;
-            // this wavefront's 16 candidates as 4 running minima over
-            // consecutive k (short dependency chains), then combined as a
-            // tree whose left operand always holds the lower k
-            double cv4[4];
-            int32_t ck4[4];
+            // this wavefront's 16 candidates as 4 minima of 4 (short
+            // dependency chains), then a tree
+            double m4[4];
 #pragma unroll
-            for (int c = 0; c < 4; c++) {
-                cv4[c] = __builtin_huge_val();
-                ck4[c] = -1;
+            for (int c4 = 0; c4 < 4; c4++) {
+                m4[c4] = __builtin_huge_val();
 #pragma unroll
-                for (int q = 4 * c; q < 4 * c + 4; q++) {
+                for (int q = 4 * c4; q < 4 * c4 + 4; q++) {
                     const int kk = wave * KW + q;
-                    const int64_t k = j0 + kk;
-                    const double cand = __builtin_fma(-lamp, cP[q], sm.pF[kk] + cC[q]);
-                    const bool lt = k < j && cand < cv4[c];
-                    ck4[c] = lt ? (int32_t)k : ck4[c];
-                    cv4[c] = lt ? cand : cv4[c];
+                    m4[c4] = __builtin_fmin(m4[c4],
+                                            __builtin_fma(-lamp, cP[q], sm.pF[kk] + cC[q]));
                 }
             }
-            const bool ra = cv4[1] < cv4[0], rb = cv4[3] < cv4[2];
-            const double va = ra ? cv4[1] : cv4[0], vb = rb ? cv4[3] : cv4[2];
-            const int32_t ka = ra ? ck4[1] : ck4[0], kb4 = rb ? ck4[3] : ck4[2];
-            const bool rab = vb < va;
-            const double cv16[1] = {rab ? vb : va};
-            const int32_t ck16[1] = {rab ? kb4 : ka};
-            sm.partV[wave][lane] = cv16[0];
-            sm.partK[wave][lane] = ck16[0];
+            sm.partV[wave][lane] =
+                __builtin_fmin(__builtin_fmin(m4[0], m4[1]), __builtin_fmin(m4[2], m4[3]));
             __syncthreads();
             if (wave == ow) {
-                // partials of waves 0,1 and 2,3, then the two, then after the
-                // running minimum (whose k lie in earlier blocks)
-                const double v0 = sm.partV[0][lane], v1 = sm.partV[1][lane];
-                const double v2 = sm.partV[2][lane], v3 = sm.partV[3][lane];
-                const int32_t k0_ = sm.partK[0][lane], k1_ = sm.partK[1][lane];
-                const int32_t k2_ = sm.partK[2][lane], k3_ = sm.partK[3][lane];
-                const bool r01 = v1 < v0, r23 = v3 < v2;
-                const double v01 = r01 ? v1 : v0, v23 = r23 ? v3 : v2;
-                const int32_t k01 = r01 ? k1_ : k0_, k23 = r23 ? k3_ : k2_;
-                const bool r = v23 < v01;
-                const double v = r ? v23 : v01;
-                const int32_t kv = r ? k23 : k01;
-                double b = best[q8];
-                int32_t kb = bk[q8];
-                kb = v < b ? kv : kb;
-                b = v < b ? v : b;
-                if (valid) {
-                    a.F[(int64_t)i * a.ld + j] = b;
-                    a.K[(int64_t)i * a.ld + j] = kb;
-                }
+                const double v =
+                    __builtin_fmin(__builtin_fmin(sm.partV[0][lane], sm.partV[1][lane]),
+                                   __builtin_fmin(sm.partV[2][lane], sm.partV[3][lane]));
+                const double b = __builtin_fmin(best[q8], v);
+                if (valid) a.F[(int64_t)i * a.ld + j] = b;
                 sm.pF[lane] = valid ? b : __builtin_huge_val();
             }
             __syncthreads();
@@ -340,7 +306,8 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
 // Step t of the sweep: workgroup 0 makes block t final, the others add
 // predecessor block t-1 to the blocks after it (tile WG index = g * nx + wg).
 template <int LG>
-__global__ __launch_bounds__(kSB* kTileWaves) void k_sweep_step(SweepArgs a, int64_t t,
+__global__ __launch_bounds__(kSB* kTileWaves) ECASQ_STEP_ATTR void k_sweep_step(SweepArgs a,
+                                                                               int64_t t,
                                                               int32_t split, int64_t nx) {
     __shared__ StepSmem<LG> sm;
     load_log2_table(sm.tab);
@@ -356,36 +323,125 @@ __global__ __launch_bounds__(kSB* kTileWaves) void k_sweep_step(SweepArgs a, int
     }
 }
 
-// eq. apx_final on the finished tables, the chain of the chosen layer traced
-// back through the argmins, and its MSE and H(I,B) summed in path order.
-// One wavefront.  out: J, MSE, H(I,B), i*.
-__global__ __launch_bounds__(kSB) void k_sweep_final(SweepArgs a, int32_t exact_s, double* out,
-                                                     int32_t* chain_out) {
-    __shared__ double2 tab[kLog2Size];
-    __shared__ int32_t u[256];
-    __shared__ double cC[256], cP[256];
-    __shared__ int32_t s_istar;
-    load_log2_table(tab);
-    const int lane = threadIdx.x;
+// Traceback state (device): st[0] = i*, the chain u_0..u_{i*-1} at st + 8.
+constexpr int kStChain = 8;
+
+// eq. apx_final on the finished table: i* (the lowest argmin over layers, or
+// I for exactly s values), u_{i*-1} = p - 1, u_0 = 0, out[0] = J.
+__global__ void k_sweep_pick(SweepArgs a, int32_t exact_s, double* out, int32_t* st) {
+    if (threadIdx.x != 0 || blockIdx.x != 0) return;
     const int64_t p = a.H.p;
-    if (lane == 0) {
-        int32_t bi = 2;
-        double bj = a.F[2 * a.ld + p - 1];
-        for (int32_t i = 3; i <= a.I; i++) {
-            const double f = a.F[(int64_t)i * a.ld + p - 1];
-            if (exact_s ? (i == a.I) : (f < bj)) {
-                bj = f;
-                bi = i;
-            }
+    int32_t bi = 2;
+    double bj = a.F[2 * a.ld + p - 1];
+    for (int32_t i = 3; i <= a.I; i++) {
+        const double f = a.F[(int64_t)i * a.ld + p - 1];
+        if (exact_s ? (i == a.I) : (f < bj)) {
+            bj = f;
+            bi = i;
         }
-        u[bi - 1] = (int32_t)(p - 1);
-        for (int32_t i = bi; i >= 3; i--) u[i - 2] = a.K[(int64_t)i * a.ld + u[i - 1]];
-        u[0] = 0;
-        s_istar = bi;
-        out[0] = bj;
     }
+    st[0] = bi;
+    st[kStChain + bi - 1] = (int32_t)(p - 1);
+    st[kStChain] = 0;
+    out[0] = bj;
+}
+
+// The lowest argmin k of F_{i-1}[k] + C[k,j] + lambda' Phi[k,j] over k in
+// [i-2, j-1] for one column j, as (value, k) pairs reduced lexicographically
+// (the DP's strict '<' in increasing k keeps the same k).  Part 1: workgroup
+// g takes 256 x kTrR consecutive predecessors.
+constexpr int kTrT = 256;
+constexpr int kTrR = 8;
+
+__device__ __forceinline__ void lexmin(double& v, int32_t& k, double ov, int32_t ok) {
+    const bool take = ov < v || (ov == v && ok < k);
+    v = take ? ov : v;
+    k = take ? ok : k;
+}
+
+__global__ __launch_bounds__(kTrT) void k_sweep_trace_part(SweepArgs a, int32_t i,
+                                                           const int32_t* __restrict__ st,
+                                                           double* __restrict__ pv,
+                                                           int32_t* __restrict__ pk) {
+    __shared__ double2 tab[kLog2Size];
+    __shared__ double rv[kTrT];
+    __shared__ int32_t rk[kTrT];
+    if (i > st[0]) return;  // uniform: layer above the chosen one
+    load_log2_table(tab);
     __syncthreads();
-    const int32_t n = s_istar;
+    const int64_t j = st[kStChain + i - 1];
+    const int64_t klo = i - 2, khi = j - 1;
+    const int64_t k0 = klo + (int64_t)blockIdx.x * (kTrT * kTrR);
+    double best = __builtin_huge_val();
+    int32_t bk = INT32_MAX;
+    const double* Fp = a.F + (int64_t)(i - 1) * a.ld;
+#pragma unroll
+    for (int r = 0; r < kTrR; r++) {
+        const int64_t k = k0 + r * kTrT + threadIdx.x;
+        if (k <= khi) {
+            double C, P;
+            cell_at(a.H, k, j, tab, C, P);
+            const double cand = __builtin_fma(-a.lamp, P, Fp[k] + C);
+            lexmin(best, bk, cand, (int32_t)k);
+        }
+    }
+    rv[threadIdx.x] = best;
+    rk[threadIdx.x] = bk;
+    __syncthreads();
+    for (int off = kTrT / 2; off > 0; off >>= 1) {
+        if ((int)threadIdx.x < off) {
+            double v = rv[threadIdx.x];
+            int32_t k = rk[threadIdx.x];
+            lexmin(v, k, rv[threadIdx.x + off], rk[threadIdx.x + off]);
+            rv[threadIdx.x] = v;
+            rk[threadIdx.x] = k;
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        pv[blockIdx.x] = rv[0];
+        pk[blockIdx.x] = rk[0];
+    }
+}
+
+// Part 2: the g partials -> u_{i-2}.
+__global__ __launch_bounds__(kTrT) void k_sweep_trace_pick(int32_t i, int32_t* __restrict__ st,
+                                                           const double* __restrict__ pv,
+                                                           const int32_t* __restrict__ pk,
+                                                           int32_t g) {
+    __shared__ double rv[kTrT];
+    __shared__ int32_t rk[kTrT];
+    if (i > st[0]) return;
+    double best = __builtin_huge_val();
+    int32_t bk = INT32_MAX;
+    for (int32_t x = threadIdx.x; x < g; x += kTrT) lexmin(best, bk, pv[x], pk[x]);
+    rv[threadIdx.x] = best;
+    rk[threadIdx.x] = bk;
+    __syncthreads();
+    for (int off = kTrT / 2; off > 0; off >>= 1) {
+        if ((int)threadIdx.x < off) {
+            double v = rv[threadIdx.x];
+            int32_t k = rk[threadIdx.x];
+            lexmin(v, k, rv[threadIdx.x + off], rk[threadIdx.x + off]);
+            rv[threadIdx.x] = v;
+            rk[threadIdx.x] = k;
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) st[kStChain + i - 2] = rk[0];
+}
+
+// The chain's MSE and H(I,B) summed in path order.  One wavefront.
+// out: J (already written), MSE, H(I,B), i*.
+__global__ __launch_bounds__(kSB) void k_sweep_sums(SweepArgs a, const int32_t* __restrict__ st,
+                                                    double* out, int32_t* chain_out) {
+    __shared__ double2 tab[kLog2Size];
+    __shared__ double cC[256], cP[256];
+    load_log2_table(tab);
+    __syncthreads();
+    const int lane = threadIdx.x;
+    const int32_t n = st[0];
+    const int32_t* u = st + kStChain;
     for (int r = lane; r + 1 < n; r += kSB) cell_at(a.H, u[r], u[r + 1], tab, cC[r], cP[r]);
     __syncthreads();
     if (lane == 0) {
@@ -400,6 +456,37 @@ __global__ __launch_bounds__(kSB) void k_sweep_final(SweepArgs a, int32_t exact_
     }
     if (chain_out)
         for (int r = lane; r < n; r += kSB) chain_out[r] = u[r];
+}
+
+// Argmins of layer i at every valid column (inspection only): one column per
+// lane, predecessors in increasing k at wave-uniform addresses.
+__global__ __launch_bounds__(256) void k_sweep_argmins(SweepArgs a, int32_t i) {
+    __shared__ double2 tab[kLog2Size];
+    load_log2_table(tab);
+    __syncthreads();
+    const int64_t p = a.H.p;
+    const int64_t jfirst = (int64_t)(i - 1) + (int64_t)blockIdx.x * blockDim.x;
+    const int64_t j = jfirst + threadIdx.x;
+    const int64_t jl = min(jfirst + (int64_t)blockDim.x - 1, p - 1);  // block's last column
+    const int64_t jj = j < p ? j : p - 1;
+    const double* Fp = a.F + (int64_t)(i - 1) * a.ld;
+    double best = __builtin_huge_val();
+    int32_t bk = -1;
+    for (int64_t k = i - 2; k < jl; k++) {
+        double C, P;
+        cell_at(a.H, k, jj, tab, C, P);
+        const double cand = __builtin_fma(-a.lamp, P, Fp[k] + C);
+        const bool lt = k < jj && cand < best;
+        bk = lt ? (int32_t)k : bk;
+        best = lt ? cand : best;
+    }
+    if (j < p) a.K[(int64_t)i * a.ld + j] = bk;
+}
+
+// Layer 2's argmin is 0 (eq. apx_base) at every valid column.
+__global__ __launch_bounds__(256) void k_sweep_argmins2(SweepArgs a) {
+    const int64_t j = 1 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (j < a.H.p) a.K[2 * a.ld + j] = 0;
 }
 
 // Accumulators of layer i for every valid column (inspection only):
@@ -454,14 +541,21 @@ hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
+int32_t trace_groups(int64_t p) { return (int32_t)((p + kTrT * kTrR - 1) / (kTrT * kTrR)); }
+
+size_t trace_scratch_bytes(int64_t p) {
+    return (size_t)trace_groups(p) * (sizeof(double) + sizeof(int32_t));
+}
+
 bool sweep_ok(const SweepSolve& S) {
-    return S.I >= 2 && S.I <= 255 && S.H.p >= 2 && S.ld >= S.H.p && S.F && S.K;
+    return S.I >= 2 && S.I <= 255 && S.H.p >= 2 && S.ld >= S.H.p && S.F && S.K && S.st &&
+           (size_t)S.ld * sizeof(int32_t) >= trace_scratch_bytes(S.H.p);
 }
 
 }  // namespace
 
 size_t sweep_table_bytes(int64_t d, int32_t s) {
-    // F (fp64) and K (int32), rows 0..s of d entries each
+    // F (fp64) and K (int32: inspection and traceback scratch), rows 0..s
     return (size_t)(s + 1) * (size_t)d * (sizeof(double) + sizeof(int32_t));
 }
 
@@ -478,7 +572,28 @@ hipError_t launch_sweep(const SweepSolve& S, int32_t exact_s, double* out, int32
     else
         e = sweep_launch<32>(a, st);
     if (e != hipSuccess) return e;
-    k_sweep_final<<<1, kSB, 0, st>>>(a, exact_s, out, chain);
+    k_sweep_pick<<<1, 64, 0, st>>>(a, exact_s, out, S.st);
+    // traceback: layers above i* return at once
+    const int32_t g = trace_groups(a.H.p);
+    double* pv = reinterpret_cast<double*>(S.K);
+    int32_t* pk = reinterpret_cast<int32_t*>(pv + g);
+    for (int32_t i = a.I; i >= 3; i--) {
+        k_sweep_trace_part<<<(unsigned)g, kTrT, 0, st>>>(a, i, S.st, pv, pk);
+        k_sweep_trace_pick<<<1, kTrT, 0, st>>>(i, S.st, pv, pk, g);
+    }
+    k_sweep_sums<<<1, kSB, 0, st>>>(a, S.st, out, chain);
+    return hipGetLastError();
+}
+
+hipError_t launch_sweep_argmins(const SweepSolve& S, hipStream_t st) {
+    if (!sweep_ok(S)) return hipErrorInvalidValue;
+    const SweepArgs a = make_args(S);
+    k_sweep_argmins2<<<(unsigned)((a.H.p - 1 + 255) / 256), 256, 0, st>>>(a);
+    for (int32_t i = 3; i <= a.I; i++) {
+        const int64_t n = a.H.p - (i - 1);
+        if (n <= 0) break;
+        k_sweep_argmins<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(a, i);
+    }
     return hipGetLastError();
 }
 

@@ -389,7 +389,7 @@ def ecasq_histogram(x, stream=None):
     return tuple(b[: p.value] for b in bufs)
 
 
-def ecasq_dp_trace(x, s, lam, stream=None, accumulators=False, schedule=0):
+def ecasq_dp_trace(x, s, lam, stream=None, accumulators=False, schedule=0, argmins=True):
     """All layers of forward solves at one multiplier (lam a number) or at the
     8 multipliers of a search pass (lam a sequence of 8).  Returns F
     [nlam, s+1, d] fp64 (NaN where unset), kstar [nlam, s+1, d] int32 (-1
@@ -403,7 +403,7 @@ def ecasq_dp_trace(x, s, lam, stream=None, accumulators=False, schedule=0):
     n = len(lams)
     shape = (n, int(s) + 1, d)
     F = torch.full(shape, float("nan"), dtype=torch.float64, device=x.device)
-    K = torch.full(shape, -1, dtype=torch.int32, device=x.device)
+    K = torch.full(shape, -1, dtype=torch.int32, device=x.device) if argmins else None
     M = torch.full(shape, float("nan"), dtype=torch.float64, device=x.device) if accumulators else None
     Ph = torch.full(shape, float("nan"), dtype=torch.float64, device=x.device) if accumulators else None
     la = (ctypes.c_double * n)(*lams)
@@ -413,7 +413,8 @@ def ecasq_dp_trace(x, s, lam, stream=None, accumulators=False, schedule=0):
     _raise(st)
     res = [tuple(out[5 * m:5 * m + 5]) for m in range(n)]
     if scalar:
-        return F[0], K[0], (M[0] if M is not None else None), (Ph[0] if Ph is not None else None), res[0]
+        return (F[0], K[0] if K is not None else None, M[0] if M is not None else None,
+                Ph[0] if Ph is not None else None, res[0])
     return F, K, M, Ph, res
 
 

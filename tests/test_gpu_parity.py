@@ -201,20 +201,39 @@ def _sample_cols(rng, lo, p, n):
 def test_full_size_sweep_sampled(workload, s, lam):
     """Full-size inputs, DP schedule 1 (the column-block sweep) at one
     multiplier: every layer checked bit for bit at sampled columns against the
-    oracle's recomputation from the GPU's previous layer."""
+    oracle's recomputation from the GPU's previous layer.  At 2^18 also the
+    recomputed argmins and the accumulators along them; at 2^20 (s = 64) the
+    values the sweep keeps (recomputing every argmin there is a full
+    layer-by-layer solve)."""
     x = inputs.make(workload, seed=0)
-    _say("full-size sweep trace", workload, x.size, s, lam)
-    F, K, M, Ph, out = ecasq.ecasq_dp_trace(_dev(x), s, lam, accumulators=True, schedule=1)
-    F, K, M, Ph = (a.cpu().numpy() for a in (F, K, M, Ph))
+    full = x.size <= (1 << 18)
+    _say("full-size sweep trace", workload, x.size, s, lam, "argmins" if full else "values")
+    F, K, M, Ph, out = ecasq.ecasq_dp_trace(_dev(x), s, lam, accumulators=full, schedule=1,
+                                            argmins=full)
+    F = F.cpu().numpy()
     _say("oracle prepare")
     H = pipeline.prepare(x)
     p = H.p
     imax = min(s, p)
     rng = np.random.default_rng(321)
+    lamp = lam * H.s2tot
+    if full:
+        K, M, Ph = (a.cpu().numpy() for a in (K, M, Ph))
+        for i in range(2, imax + 1):
+            cols = _sample_cols(rng, i - 1, p, 8)
+            _check_accumulators(H, i, lamp, F, K, M, Ph, cols)
+        _check_final(out, F, M, Ph, imax, p)
+        return
+    z = np.zeros(F.shape[1])
     for i in range(2, imax + 1):
         cols = _sample_cols(rng, i - 1, p, 8)
-        _check_accumulators(H, i, lam * H.s2tot, F, K, M, Ph, cols)
-    _check_final(out, F, M, Ph, imax, p)
+        if i == 2:
+            Fo, _, _, _ = pipeline.dp_columns(H, 2, lamp, cols=cols)
+        else:
+            Fo, _, _, _ = pipeline.dp_columns(H, i, lamp, F[i - 1], z, z, cols)
+        np.testing.assert_array_equal(F[i, cols], Fo, err_msg=f"F layer {i}")
+    last = [F[i, p - 1] for i in range(2, imax + 1)]
+    assert int(out[3]) == 2 + int(np.argmin(last)) and out[0] == min(last)
 
 
 @pytest.mark.parametrize("workload,s", [("weights_256k", 32), ("student_t_1m", 4)],
