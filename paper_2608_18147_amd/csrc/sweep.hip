@@ -38,9 +38,10 @@ namespace {
 constexpr int kSB = 64;        // columns per block (one wavefront)
 constexpr int kTileWaves = 4;  // wavefronts per workgroup
 // below this many (column block, layer group) tiles a step splits layers
-// over the wavefronts of a workgroup (2 waves per SIMD of 256 CUs)
+// over the wavefronts of a workgroup (fewer tiles than SIMDs: splitting buys
+// wavefronts at the price of evaluating C and Phi once per wavefront)
 #ifndef ECASQ_SWEEP_SPLIT_BELOW
-#define ECASQ_SWEEP_SPLIT_BELOW 2048
+#define ECASQ_SWEEP_SPLIT_BELOW 512
 #endif
 constexpr int64_t kSplitBelow = ECASQ_SWEEP_SPLIT_BELOW;
 // widest layer group (register arrays of that many layers per lane)
@@ -48,9 +49,15 @@ constexpr int64_t kSplitBelow = ECASQ_SWEEP_SPLIT_BELOW;
 #define ECASQ_SWEEP_LG_MAX 32
 #endif
 // wavefronts per SIMD the step kernel's registers are sized for (0: the
-// compiler's choice)
+// compiler's choice).  4 (128 VGPRs) lets the early steps' ~4000 tile
+// wavefronts run in one round; it costs a few spilled registers.
 #ifndef ECASQ_SWEEP_WAVES
-#define ECASQ_SWEEP_WAVES 0
+#define ECASQ_SWEEP_WAVES 4
+#endif
+// layer counts per wavefront up to which predecessors are taken in pairs
+// (two independent C / Phi chains per iteration; also fewer registers)
+#ifndef ECASQ_SWEEP_PAIR_MAX
+#define ECASQ_SWEEP_PAIR_MAX 32
 #endif
 #if ECASQ_SWEEP_WAVES > 0
 #define ECASQ_STEP_ATTR __attribute__((amdgpu_waves_per_eu(ECASQ_SWEEP_WAVES)))
@@ -137,7 +144,7 @@ template <int LG, int LW>
 __device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int lofs, double cv, double cN,
                                            double cS, double cS2, double dd, double lamp,
                                            double (&best)[LW]) {
-    if constexpr (LW > 8) {
+    if constexpr (LW > ECASQ_SWEEP_PAIR_MAX) {
         // many layers per predecessor: enough independent work per iteration
         for (int kk = 0; kk < kSB; kk++) {
             double C, P;
