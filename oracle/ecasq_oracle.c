@@ -29,7 +29,8 @@
  *     g = 1/(w*d)   yu = tu*g   yd = td*g  (+ c0/d if a == 0, first interval)
  *     mu = max(yu,0)   md = max(yd,0)
  *     P = fma(mu, log2c(mu), md*log2c(md))                      (P = -Phi)
- *     cand = fma(-lambda', P, F_prev + C)
+ *     Q    = fma(-lambda', P, C)                                  (the cell's cost)
+ *     cand = F_prev + Q
  *   refinement / output-entropy (inv form):
  *     U = tu*(1/w)   D = td*(1/w)   h(f) = -(m*log2c(m)), m = max(f/d, 0)
  *   log2c: table-driven, see log2c() below.
@@ -230,7 +231,7 @@ int orc_dp_forward(const double *v, const double *N, const double *S, const doub
             for (int64_t k = klo; k < j; k++) {
                 double C, P;
                 cell_terms(&H, k, j, &C, &P);
-                double cand = fma(-lamp, P, F0[k] + C);
+                double cand = F0[k] + fma(-lamp, P, C);
                 if (cand < best) { best = cand; bk = k; }
             }
             F1[j] = best;
@@ -289,7 +290,7 @@ void orc_dp_columns(const double *v, const double *N, const double *S, const dou
         int64_t bk = -1;
         for (int64_t k = layer - 2; k < j; k++) {
             cell_terms(&H, k, j, &C, &P);
-            double cand = fma(-lamp, P, Fprev[k] + C);
+            double cand = Fprev[k] + fma(-lamp, P, C);
             if (cand < best) { best = cand; bk = k; }
         }
         F[x] = best;
@@ -341,7 +342,7 @@ static void hb_forward(const hist_t *H, double lamp, int64_t lo, int64_t hi, int
             for (int64_t k = kl; k <= ke; k++) {
                 double C, P;
                 cell_terms(H, k, j, &C, &P);
-                double cand = fma(-lamp, P, F[k - lo] + C);
+                double cand = F[k - lo] + fma(-lamp, P, C);
                 if (cand < best) best = cand;
             }
             G[j - lo] = best;
@@ -370,7 +371,7 @@ static void hb_backward(const hist_t *H, double lamp, int64_t lo, int64_t hi, in
             for (int64_t k = ks; k <= kh; k++) {
                 double C, P;
                 cell_terms(H, j, k, &C, &P);
-                double cand = fma(-lamp, P, B[k - lo] + C);
+                double cand = B[k - lo] + fma(-lamp, P, C);
                 if (cand < best) best = cand;
             }
             G[j - lo] = best;

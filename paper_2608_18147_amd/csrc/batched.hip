@@ -225,10 +225,11 @@ __device__ Pt row_sweep(Row& R, double lam, int exact_s, int buf) {
                 double C, P;
                 cell_terms(pv, pN, pS, pS2, cv[c], cN[c], cS[c], cS2[c], dd, false, 0.0, R.tab,
                            C, P);
+                const double Q = __builtin_fma(-lamp, P, C);
                 const bool ok = j > k;
 #pragma unroll
                 for (int l = 0; l < LG; l++) {
-                    const double cand = __builtin_fma(-lamp, P, Fk[l] + C);
+                    const double cand = Fk[l] + Q;
                     const bool lt = ok && cand < best[c][l];
                     bk[c][l] = lt ? k : bk[c][l];
                     best[c][l] = lt ? cand : best[c][l];
@@ -313,7 +314,7 @@ __device__ Pt row_solve(Row& R, double lam, int exact_s, int buf) {
                 double C, P;
                 cell_terms(pv, pN, pS, pS2, cv[c], cN[c], cS[c], cS2[c], R.dd, false, 0.0, R.tab,
                            C, P);
-                const double cand = __builtin_fma(-lamp, P, pF + C);
+                const double cand = pF + __builtin_fma(-lamp, P, C);
                 const bool lt = (j > k) && (j < p) && cand < best[c];
                 bk[c] = lt ? k : bk[c];
                 best[c] = lt ? cand : best[c];

@@ -13,7 +13,7 @@
 //     g = 1/(w*d)  yu = tu*g  yd = td*g (+ c0/d for the first interval)
 //     mu = max(yu,0)  md = max(yd,0)
 //     P = fma(mu, log2c(mu), md*log2c(md))                    (P = -Phi)
-//   DP candidate (eq. apx_rec):  fma(-lambda', P, F_prev + C)
+//   DP candidate (eq. apx_rec):  F_prev + Q,  Q = fma(-lambda', P, C)
 //   refinement / output entropy (Sec. 6):
 //     U = tu*(1/w)  D = td*(1/w)   h(f) = -(m*log2c(m)),  m = max(f/d, 0)
 #pragma once

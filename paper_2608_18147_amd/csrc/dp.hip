@@ -122,7 +122,7 @@ __device__ __forceinline__ void tile_pass(const double* sv, const double* sN, co
             const bool ok = !MASKED || (BWD ? (k > col[r]) : (k < col[r]));
 #pragma unroll
             for (int m = 0; m < ML; m++)
-                take<MASKED>(__builtin_fma(-lam[m], P, pF[m] + C), (int32_t)k, ok, best[r][m],
+                take<MASKED>(pF[m] + __builtin_fma(-lam[m], P, C), (int32_t)k, ok, best[r][m],
                              bk[r][m]);
         }
     }
@@ -190,7 +190,7 @@ __global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a, const double* 
                 else
                     cell_terms(pv, pN, pS, pS2, cv[r], cN[r], cS[r], cS2[r], dd, false, 0.0, tab,
                                C, P);
-                take<false>(__builtin_fma(-lam[0], P, pF + C), (int32_t)k, true, best[r][0],
+                take<false>(pF + __builtin_fma(-lam[0], P, C), (int32_t)k, true, best[r][0],
                             bk[r][0]);
             }
         }
@@ -208,7 +208,7 @@ __global__ __launch_bounds__(kBlock) void k_dp_layer(LayerArgs a, const double* 
                 else
                     cell_terms(pv, pN, pS, pS2, cv[r], cN[r], cS[r], cS2[r], dd, false, 0.0, tab,
                                C, P);
-                take<true>(__builtin_fma(-lam[0], P, pF + C), (int32_t)k,
+                take<true>(pF + __builtin_fma(-lam[0], P, C), (int32_t)k,
                            BWD ? (k > col[r]) : (k < col[r]), best[r][0], bk[r][0]);
             }
         }

@@ -150,10 +150,9 @@ __device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int lofs, dou
             double C, P;
             cell_terms(sm.sv[kk], sm.sN[kk], sm.sS[kk], sm.sS2[kk], cv, cN, cS, cS2, dd, false,
                        0.0, sm.tab, C, P);
+            const double Q = __builtin_fma(-lamp, P, C);
 #pragma unroll
-            for (int l = 0; l < LW; l++)
-                best[l] = __builtin_fmin(best[l],
-                                         __builtin_fma(-lamp, P, sm.sF[kk][lofs + l] + C));
+            for (int l = 0; l < LW; l++) best[l] = __builtin_fmin(best[l], sm.sF[kk][lofs + l] + Q);
         }
     } else {
     // few layers: two predecessors per iteration, whose C and Phi are
@@ -164,11 +163,11 @@ __device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int lofs, dou
                    sm.tab, C0, P0);
         cell_terms(sm.sv[kk + 1], sm.sN[kk + 1], sm.sS[kk + 1], sm.sS2[kk + 1], cv, cN, cS, cS2,
                    dd, false, 0.0, sm.tab, C1, P1);
+        const double Q0 = __builtin_fma(-lamp, P0, C0), Q1 = __builtin_fma(-lamp, P1, C1);
 #pragma unroll
         for (int l = 0; l < LW; l++) {
-            best[l] = __builtin_fmin(best[l], __builtin_fma(-lamp, P0, sm.sF[kk][lofs + l] + C0));
-            best[l] =
-                __builtin_fmin(best[l], __builtin_fma(-lamp, P1, sm.sF[kk + 1][lofs + l] + C1));
+            best[l] = __builtin_fmin(best[l], sm.sF[kk][lofs + l] + Q0);
+            best[l] = __builtin_fmin(best[l], sm.sF[kk + 1][lofs + l] + Q1);
         }
     }
     }
@@ -239,17 +238,19 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
     __syncthreads();
     const int c = (int)(jj - j0);
     const double cv = sm.dv[c], cN = sm.dN[c], cS = sm.dS[c], cS2 = sm.dS2[c];
-    // C and Phi of (k, j) for this wavefront's 16 predecessors k < j; the
-    // others get Phi = 0 and C = +inf, so their candidates are +inf
-    double cC[KW], cP[KW];
+    // the cost Q = C - lambda' Phi of (k, j) for this wavefront's 16
+    // predecessors k < j; the others get +inf, so their candidates are +inf
+    double cQ[KW];
 #pragma unroll
     for (int q = 0; q < KW; q++) {
         const int kk = wave * KW + q;
-        cC[q] = __builtin_huge_val();
-        cP[q] = 0.0;
-        if (j0 + kk < jj)
+        cQ[q] = __builtin_huge_val();
+        if (j0 + kk < jj) {
+            double C, P;
             cell_terms(sm.dv[kk], sm.dN[kk], sm.dS[kk], sm.dS2[kk], cv, cN, cS, cS2, dd, false,
-                       0.0, sm.tab, cC[q], cP[q]);
+                       0.0, sm.tab, C, P);
+            cQ[q] = __builtin_fma(-lamp, P, C);
+        }
     }
     // layer 2 (eq. apx_base): the first interval (v_0, v_j]
     if (wave == 0) {
@@ -289,8 +290,7 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
 #pragma unroll
                 for (int q = 4 * c4; q < 4 * c4 + 4; q++) {
                     const int kk = wave * KW + q;
-                    m4[c4] = __builtin_fmin(m4[c4],
-                                            __builtin_fma(-lamp, cP[q], sm.pF[kk] + cC[q]));
+                    m4[c4] = __builtin_fmin(m4[c4], sm.pF[kk] + cQ[q]);
                 }
             }
             sm.partV[wave][lane] =
@@ -388,7 +388,7 @@ __global__ __launch_bounds__(kTrT) void k_sweep_trace_part(SweepArgs a, int32_t 
         if (k <= khi) {
             double C, P;
             cell_at(a.H, k, j, tab, C, P);
-            const double cand = __builtin_fma(-a.lamp, P, Fp[k] + C);
+            const double cand = Fp[k] + __builtin_fma(-a.lamp, P, C);
             lexmin(best, bk, cand, (int32_t)k);
         }
     }
@@ -482,7 +482,7 @@ __global__ __launch_bounds__(256) void k_sweep_argmins(SweepArgs a, int32_t i) {
     for (int64_t k = i - 2; k < jl; k++) {
         double C, P;
         cell_at(a.H, k, jj, tab, C, P);
-        const double cand = __builtin_fma(-a.lamp, P, Fp[k] + C);
+        const double cand = Fp[k] + __builtin_fma(-a.lamp, P, C);
         const bool lt = k < jj && cand < best;
         bk = lt ? (int32_t)k : bk;
         best = lt ? cand : best;
