@@ -27,19 +27,28 @@ import sys
 import time
 
 # Algorithmic fp64 operations per DP cell in the canonical cell arithmetic.
-# Shared by every multiplier of a launch (45): 4 range differences, 2 fma (tu,
-# td), 2 fma (C), w*d, one IEEE division (counted as 1), 2 products (yu, yd),
-# two log2 evaluations of 13 flops each (fma for r, 4 Horner fma, 1 add, 1
-# final fma), 1 mul + 1 fma for the entropy term.  Per multiplier (3): 1 add +
-# 1 fma for the candidate.  fma counts 2.
-FLOPS_SHARED = 45
-FLOPS_PER_LAMBDA = 3
+# The DP is a min-plus recurrence bound by FP64 VALU issue, and its
+# operations are not all flops (the min, the max of h, the compare), so the
+# roofline counts algorithmic FP64 lane operations (add, mul, fma, min, max,
+# compare, a division and a log2 each count 1) against the chip's FP64 lane
+# issue rate: 256 CUs x 64 FP64 lanes x 2.4 GHz = 39.32 Tops/s (the rate at
+# which the 78.6 TFLOP/s FMA peak is reached, an FMA counting 2 flops there).
+# Per (k, j) pair, shared by every layer and multiplier (18): 4 range
+# differences, tu, td, 2 for C, w*d, the division, yu, yd, 2 max, 2 log2,
+# the mul and fma of Phi.  Per multiplier: the cost Q = fma(-lambda', P, C)
+# (1); per (k, j, layer) cell: F_prev + Q and the min (2).
+OPS_PAIR = 18
+OPS_Q = 1
+OPS_CELL = 2
 LAMBDAS_PER_PASS = 8
+ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 FP64_VECTOR_PEAK_TFLOPS = 78.6
 
 
 def flops_per_cell(nlam):
-    return FLOPS_SHARED + FLOPS_PER_LAMBDA * nlam
+    """Algorithmic ops of one (k, j) cell of the layer kernel with nlam
+    multipliers per launch."""
+    return OPS_PAIR + (OPS_Q + OPS_CELL) * nlam
 
 
 # HBM bytes per launch of the pass kernel (k_dp_layer, 8 multipliers) from
@@ -73,27 +82,27 @@ def log(*a):
 
 def sweep_roofline(p, s, ms, solves, cells):
     """Roofline of DP schedule 1: all k_sweep_step launches of one solve timed
-    as one unit.  Algorithmic flops per solve: the 45 shared flops of every
-    (k, j) pair, 3 per (k, j, layer) cell of layers 3..I, and 48 per column of
-    layer 2."""
+    as one unit.  Algorithmic ops per solve: 19 per (k, j) pair (its C, Phi
+    and cost Q, shared by all layers), 2 per (k, j, layer) cell of layers
+    3..I, and 20 per column of layer 2."""
     I = min(s, p)
     pairs = p * (p - 1) / 2.0
     layer_cells = sum((p - i + 1) * (p - i + 2) / 2.0 for i in range(3, I + 1))
-    flops = FLOPS_SHARED * pairs + FLOPS_PER_LAMBDA * layer_cells + 48.0 * (p - 1)
+    ops = (OPS_PAIR + OPS_Q) * pairs + OPS_CELL * layer_cells + 20.0 * (p - 1)
     per_ms = ms / max(solves, 1)
-    achieved = flops / (per_ms * 1e-3) / 1e12 if ms > 0 else 0.0
+    achieved = ops / (per_ms * 1e-3) / 1e12 if ms > 0 else 0.0
     steps = (p + 63) // 64
     return {
         "bound": "alu",
         "kernel": "k_sweep_step (fp64 VALU); one DP solve = %d launches" % steps,
         "achieved": achieved,
-        "peak": FP64_VECTOR_PEAK_TFLOPS,
-        "unit": "TFLOP/s",
-        "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
+        "peak": ALU_PEAK_TOPS,
+        "unit": "TOP/s (fp64 lane ops)",
+        "frac": achieved / ALU_PEAK_TOPS,
         "traffic": (SWEEP_TRAFFIC_BYTES_PER_LAUNCH
                     if kernel_sources_sha(SWEEP_SOURCES) == SWEEP_TRAFFIC_SHA else None),
         "traffic_unit": "bytes/launch",
-        "flops_per_solve": flops,
+        "ops_per_solve": ops,
         "avg_launch_ms": per_ms / steps,
         "launches": solves * steps,
         "ms_per_solve": per_ms,
@@ -183,7 +192,8 @@ def alphabet_rate(torch, ecasq, xd, s, b, opts, full_info, grids=(("uniform", 40
     return res
 
 
-OPT_FLOPS_PER_CANDIDATE = 17  # y = yu + yd; m log2c(m) (13 + 1); the candidate's fma (2)
+# y = yu + yd, max, log2, the mul m log2(m), the candidate's fma, the min
+OPT_OPS_PER_CANDIDATE = 6
 
 
 def optimal_rate(torch, ecasq, inputs, reps=3):
@@ -211,10 +221,10 @@ def optimal_rate(torch, ecasq, inputs, reps=3):
              "vnmse": info["vnmse"], "entropy": info["entropy"],
              "layer_ms_per_solve": kms / reps, "layer_launches": launches // reps}
         if scan == 1 and kms > 0:
-            achieved = OPT_FLOPS_PER_CANDIDATE * cands / (kms * 1e-3) / 1e12
+            achieved = OPT_OPS_PER_CANDIDATE * cands / (kms * 1e-3) / 1e12
             r["roofline"] = {"bound": "alu", "kernel": "k_opt_layer<full> (fp64 VALU)",
-                             "achieved": achieved, "peak": FP64_VECTOR_PEAK_TFLOPS,
-                             "unit": "TFLOP/s", "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
+                             "achieved": achieved, "peak": ALU_PEAK_TOPS,
+                             "unit": "TOP/s (fp64 lane ops)", "frac": achieved / ALU_PEAK_TOPS,
                              "candidates_per_s": cands / (kms * 1e-3),
                              "avg_launch_ms": kms / max(launches, 1)}
         out[name] = r
@@ -400,13 +410,13 @@ def main():
             "bound": "alu",
             "kernel": "k_dp_layer, 8 multipliers per launch (fp64 VALU)",
             "achieved": achieved,
-            "peak": FP64_VECTOR_PEAK_TFLOPS,
-            "unit": "TFLOP/s",
-            "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
+            "peak": ALU_PEAK_TOPS,
+            "unit": "TOP/s (fp64 lane ops)",
+            "frac": achieved / ALU_PEAK_TOPS,
             "traffic": (TRAFFIC_BYTES_PER_LAUNCH if kernel_sources_sha() == TRAFFIC_SOURCES_SHA
                         else None),
             "traffic_unit": "bytes/launch",
-            "flops_per_cell": fpc,
+            "ops_per_cell": fpc,
             "avg_launch_ms": avg_ms,
             "launches": launches,
             "cells_per_s": cells / (ms * 1e-3) if ms > 0 else None,
@@ -436,7 +446,7 @@ def main():
         "single_multiplier_layers": {
             "launches": launches1, "ms": ms1,
             "cells_per_s": cells1 / (ms1 * 1e-3) if ms1 > 0 else None,
-            "achieved_tflops": (flops_per_cell(1) * cells1 / (ms1 * 1e-3) / 1e12
+            "achieved_tops": (flops_per_cell(1) * cells1 / (ms1 * 1e-3) / 1e12
                                 if ms1 > 0 else None),
         },
         "exact_cells_per_s": exact / elapsed,
