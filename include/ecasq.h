@@ -309,7 +309,8 @@ ecasq_status ecasq_quantize(const void *x, ecasq_dtype dt, int64_t d, const doub
  * opts->search_width = 1 and opts->alphabet = 0, except that the search is
  * the plain chord search
  * (no query aimed at H = b: it runs on the device, whose log and exp are not
- * those of the host) (argmins kept in LDS; those fields of opts are ignored).  codebooks: device, n x s fp64 (row
+ * those of the host) and the codebook is the argmin traceback of the solve
+ * it was found in (those fields of opts are ignored).  codebooks: device, n x s fp64 (row
  * r's t_out[r] values first, the rest untouched); t_out: device, n int32
  * (0 for a row holding NaN/Inf); infos_dev: device, n ecasq_info, may be NULL
  * (per-row status: ECASQ_OK, ECASQ_EINFEASIBLE or ECASQ_ENONFINITE).

@@ -30,7 +30,7 @@ FLAGS = [
 # that are finite or +inf, never NaN; without the no-NaN promise the compiler
 # quiets every loop-carried operand of fmin (one extra fp64 max per layer and
 # predecessor, about a fifth of the kernel's instructions).
-EXTRA_FLAGS = {"sweep.hip": ["-fno-honor-nans"]}
+EXTRA_FLAGS = {"sweep.hip": ["-fno-honor-nans"], "batched.hip": ["-fno-honor-nans"]}
 
 
 def _table():

@@ -5,10 +5,12 @@
 //
 // Per row the steps are those of the single-vector path (Sec. 2 histogram,
 // App. D prefix sums, Sec. 5 eq. apx_base/apx_rec/apx_final, Sec. 3/Sec. 5
-// lambda search, Sec. 6 refinement).  Recovery keeps the argmins of every
-// layer (s x p int16 in LDS, two buffers so that the best feasible solve's
-// argmins survive the later queries) and traces them back: at these sizes the
-// O(s p) table is a few KB and Hirschberg's O(p) bound buys nothing.
+// lambda search, Sec. 6 refinement).  Every solve traces its chain back at
+// once and keeps it with the solve (two buffers, so that the best feasible
+// solve's chain survives the later queries): the sweep over predecessors
+// keeps layer values only and recomputes each argmin along the chain; the
+// layer-by-layer solver (long rows) keeps the argmins of every layer (s x p
+// int16 in LDS).  At these sizes Hirschberg's O(p) bound buys nothing.
 //
 // Columns sit in lanes (column j = 64c + lane, c < CMAX); the predecessor k is
 // uniform and read from LDS as a broadcast.  Column segments entirely at or
@@ -115,38 +117,26 @@ __device__ __forceinline__ double uniform_d(double x) {
     return __hiloint2double(hi, lo);
 }
 
-// eq. apx_final on R.last[2..imax] (lowest i, or imax for exactly min(s, p)
-// values), the chain traced back through argmin buffer `buf`, and its MSE and
-// H(I,B) summed in path order (the same additions as accumulating them along
-// the argmins).
-__device__ Pt row_final(Row& R, double lam, int imax, int exact_s, int buf) {
-    const int p = R.p, lane = R.lane, dp = R.dpad;
-    const int16_t* bp = R.bp[buf];
+// The solve's point from its chain u_0 .. u_{n-1} in R.nu: MSE and H(I,B)
+// summed in path order (the same additions as accumulating them along the
+// argmins); the chain is kept in the first entries of argmin buffer `buf`
+// (rows 0 and 1 of the table are never layers).
+__device__ Pt row_chain_point(Row& R, double lam, int n, int buf) {
+    const int lane = R.lane;
     const Hist H = row_hist(R);
     if (lane == 0) {
-        int bi = 2;
-        double bj = R.last[2];
-        for (int i = 3; i <= imax; i++) {
-            const double f = R.last[i];
-            if (exact_s ? (i == imax) : (f < bj)) {
-                bj = f;
-                bi = i;
-            }
-        }
-        int32_t* u = R.nu;  // scratch chain
-        u[bi - 1] = p - 1;
-        for (int i = bi; i >= 3; i--) u[i - 2] = bp[i * dp + u[i - 1]];
-        u[0] = 0;
+        const int32_t* u = R.nu;
         double mse = 0.0, ph = 0.0;
-        for (int r = 0; r + 1 < bi; r++) {
+        for (int r = 0; r + 1 < n; r++) {
             double C, P;
             cell_at(H, u[r], u[r + 1], R.tab, C, P);
             mse = mse + C;
             ph = ph - P;
         }
+        for (int r = 0; r < n; r++) R.bp[buf][r] = (int16_t)u[r];
         R.misc[0] = mse;
         R.misc[1] = ph;
-        R.misc[2] = (double)bi;
+        R.misc[2] = (double)n;
     }
     wave_sync();
     // the point is the same for every lane: keep it in scalar registers
@@ -161,6 +151,39 @@ __device__ Pt row_final(Row& R, double lam, int imax, int exact_s, int buf) {
     return out;
 }
 
+// eq. apx_final on R.last[2..imax]: the lowest i minimising F_i[p-1], or imax
+// for exactly min(s, p) values.
+__device__ __forceinline__ int row_istar(const Row& R, int imax, int exact_s) {
+    int bi = 2;
+    double bj = R.last[2];
+    for (int i = 3; i <= imax; i++) {
+        const double f = R.last[i];
+        if (exact_s ? (i == imax) : (f < bj)) {
+            bj = f;
+            bi = i;
+        }
+    }
+    return bi;
+}
+
+// eq. apx_final and the chain traced back through argmin buffer `buf`.
+__device__ Pt row_final(Row& R, double lam, int imax, int exact_s, int buf) {
+    const int p = R.p, lane = R.lane, dp = R.dpad;
+    const int16_t* bp = R.bp[buf];
+    if (lane == 0) {
+        const int bi = row_istar(R, imax, exact_s);
+        int32_t* u = R.nu;
+        u[bi - 1] = p - 1;
+        for (int i = bi; i >= 3; i--) u[i - 2] = bp[i * dp + u[i - 1]];
+        u[0] = 0;
+        R.misc[2] = (double)bi;
+    }
+    wave_sync();
+    const int n = (int)uniform_d(R.misc[2]);
+    wave_sync();
+    return row_chain_point(R, lam, n, buf);
+}
+
 __device__ __forceinline__ double readlane_d(double x, int l) {
     const int lo = __builtin_amdgcn_readlane(__double2loint(x), l);
     const int hi = __builtin_amdgcn_readlane(__double2hiint(x), l);
@@ -172,17 +195,18 @@ __device__ __forceinline__ double readlane_d(double x, int l) {
 // of a cell are evaluated once instead of once per layer.  Column k is final
 // when the sweep reaches it (all its predecessors are behind); its layer
 // values are broadcast from the lane that holds them.  LG >= imax - 2 layers
-// of CMAX columns per lane live in registers.
+// of CMAX columns per lane live in registers, values only: the chain of the
+// chosen layer is traced back afterwards, each argmin recomputed for its one
+// column from the layer values the lanes still hold (lowest k among equal
+// candidates, as the DP's strict '<' in increasing k).
 template <int CMAX, int LG>
 __device__ Pt row_sweep(Row& R, double lam, int exact_s, int buf) {
     const double lamp = lam * R.s2tot;
-    const int p = R.p, lane = R.lane, dp = R.dpad;
+    const int p = R.p, lane = R.lane;
     const int imax = R.s < p ? R.s : p;
-    int16_t* bp = R.bp[buf];
     const Hist H = row_hist(R);
     double cv[CMAX], cN[CMAX], cS[CMAX], cS2[CMAX], f2[CMAX];
     double best[CMAX][LG];
-    int32_t bk[CMAX][LG];
 #pragma unroll
     for (int c = 0; c < CMAX; c++) {
         const int j = c * kWave + lane;
@@ -197,13 +221,9 @@ __device__ Pt row_sweep(Row& R, double lam, int exact_s, int buf) {
             double C, P;
             cell_at(H, 0, j, R.tab, C, P);
             f2[c] = __builtin_fma(-lamp, P, 0.0 + C);
-            bp[2 * dp + j] = 0;
         }
 #pragma unroll
-        for (int l = 0; l < LG; l++) {
-            best[c][l] = __builtin_huge_val();
-            bk[c][l] = -1;
-        }
+        for (int l = 0; l < LG; l++) best[c][l] = __builtin_huge_val();
     }
     const double dd = R.dd;
 #pragma unroll
@@ -225,28 +245,17 @@ __device__ Pt row_sweep(Row& R, double lam, int exact_s, int buf) {
                 double C, P;
                 cell_terms(pv, pN, pS, pS2, cv[c], cN[c], cS[c], cS2[c], dd, false, 0.0, R.tab,
                            C, P);
-                const double Q = __builtin_fma(-lamp, P, C);
-                const bool ok = j > k;
+                // columns at or below k take nothing from it
+                const double Q = j > k ? __builtin_fma(-lamp, P, C) : __builtin_huge_val();
 #pragma unroll
-                for (int l = 0; l < LG; l++) {
-                    const double cand = Fk[l] + Q;
-                    const bool lt = ok && cand < best[c][l];
-                    bk[c][l] = lt ? k : bk[c][l];
-                    best[c][l] = lt ? cand : best[c][l];
-                }
+                for (int l = 0; l < LG; l++) best[c][l] = __builtin_fmin(best[c][l], Fk[l] + Q);
             }
         }
     }
-    // argmins of every layer, and F_i[p-1] for eq. apx_final
+    // F_i[p-1] of every layer for eq. apx_final
     const int cl = (p - 1) / kWave, ll = (p - 1) % kWave;
 #pragma unroll
     for (int c = 0; c < CMAX; c++) {
-        const int j = c * kWave + lane;
-#pragma unroll
-        for (int l = 0; l < LG; l++) {
-            const int i = 3 + l;
-            if (i <= imax && j < p) bp[i * dp + j] = (int16_t)bk[c][l];
-        }
         if (c == cl) {
             const double l2 = readlane_d(f2[c], ll);
             if (lane == 0) R.last[2] = l2;
@@ -257,11 +266,55 @@ __device__ Pt row_sweep(Row& R, double lam, int exact_s, int buf) {
             }
         }
     }
+    wave_sync();
+    const int bi = row_istar(R, imax, exact_s);
+    // traceback: layer i's argmin at the chain's column j from F_{i-1} (layer
+    // i-1 = 3 + l held in best[.][l], layer 2 in f2), one (value, k) pair per
+    // lane and column segment, then a butterfly over the wavefront
+    int jc = p - 1;
+    if (lane == 0) {
+        R.nu[bi - 1] = p - 1;
+        R.nu[0] = 0;
+    }
+#pragma unroll
+    for (int l = LG - 1; l >= -1; l--) {
+        const int i = l + 4;
+        if (i > bi) continue;
+        double bv = __builtin_huge_val();
+        int bk = 0x7fffffff;
+        const double jv = R.v[jc], jN = R.N[jc], jS = R.S[jc], jS2 = R.S2[jc];
+#pragma unroll
+        for (int c = 0; c < CMAX; c++) {
+            const int k = c * kWave + lane;
+            if (k >= i - 2 && k < jc) {
+                double C, P;
+                cell_terms(R.v[k], R.N[k], R.S[k], R.S2[k], jv, jN, jS, jS2, dd, false, 0.0,
+                           R.tab, C, P);
+                const double F = l >= 0 ? best[c][l >= 0 ? l : 0] : f2[c];
+                const double cand = F + __builtin_fma(-lamp, P, C);
+                if (cand < bv) {
+                    bv = cand;
+                    bk = k;
+                }
+            }
+        }
+#pragma unroll
+        for (int off = kWave / 2; off > 0; off >>= 1) {
+            const double ov = __shfl_xor(bv, off);
+            const int ok = __shfl_xor(bk, off);
+            if (ov < bv || (ov == bv && ok < bk)) {
+                bv = ov;
+                bk = ok;
+            }
+        }
+        jc = __builtin_amdgcn_readfirstlane(bk);
+        if (lane == 0) R.nu[i - 2] = jc;
+    }
     int64_t cells = p - 1;
     for (int i = 3; i <= imax; i++) cells += (int64_t)(p - i + 1) * (p - i + 2) / 2;
     R.cells += cells;
     wave_sync();
-    return row_final(R, lam, imax, exact_s, buf);
+    return row_chain_point(R, lam, bi, buf);
 }
 
 // One dp_APX solve at lambda (vNMSE units) into argmin buffer `buf`; returns
@@ -608,10 +661,8 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
                 R.chain[0] = 0;
                 R.chain[1] = p - 1;
             } else {
-                const int16_t* bp = R.bp[Bp.buf];
-                R.chain[t - 1] = p - 1;
-                for (int i = t; i >= 3; i--) R.chain[i - 2] = bp[i * dpad + R.chain[i - 1]];
-                R.chain[0] = 0;
+                const int16_t* kept = R.bp[Bp.buf];
+                for (int r = 0; r < t; r++) R.chain[r] = kept[r];
             }
         }
         wave_sync();
