@@ -358,6 +358,52 @@ def test_solve_parity_sweep(case):
     _compare(g, o)
 
 
+def _tie_inputs():
+    """Inputs whose DP candidates tie exactly: evenly spaced integer values
+    with equal counts (the interval costs depend only on the gaps, so many
+    predecessors give the same candidate), and a symmetric two-cluster set."""
+    rng = np.random.default_rng(77)
+    even = np.repeat(np.arange(40, dtype=np.float32), 25)
+    rng.shuffle(even)
+    sym = np.concatenate([-np.arange(1, 31, dtype=np.float32), np.arange(1, 31, dtype=np.float32),
+                          np.zeros(7, dtype=np.float32)])
+    return [("even_grid", even), ("symmetric", sym)]
+
+
+@pytest.mark.parametrize("name,x", _tie_inputs(), ids=[c[0] for c in _tie_inputs()])
+def test_sweep_and_batched_ties(name, x):
+    """Exact ties among DP candidates: the sweep's traceback (argmins
+    recomputed from the kept values) and the batched rows' register traceback
+    take the lowest k, as the oracle's backpointers do; every layer's argmins
+    of the sweep equal the oracle's."""
+    _say("ties", name, x.size)
+    for s_, b, lam in ((8, 2.0, 0.05), (16, 3.0, 0.0), (5, 1.5, 0.3)):
+        opts = ecasq.ecasq_default_options(refine_rounds=0, dp_schedule=1)
+        g = ecasq.ecasq_solve(_dev(x), s_, b, options=opts)
+        o = pipeline.solve(x, s_, b, refine_rounds=0, width=1, recovery="backpointers")
+        _compare(g, o)
+        gl = ecasq.ecasq_solve_lagrangian(_dev(x), s_, lam, options=opts)
+        ol = pipeline.solve_lagrangian(x, s_, lam, recovery="backpointers")
+        _compare(gl, ol)
+        F, K, M, Ph, out = ecasq.ecasq_dp_trace(_dev(x), s_, lam, schedule=1)
+        H = pipeline.prepare(x)
+        r = pipeline.dp_forward(H, s_, lam * H.s2tot, backpointers=True, dump=True)
+        K = K.cpu().numpy()
+        for i in range(3, min(s_, H.p) + 1):
+            np.testing.assert_array_equal(K[i, i - 1:H.p], r["bp"][i, i - 1:H.p],
+                                          err_msg=f"{name} s={s_} layer {i}")
+    if x.size <= 512:
+        rows = np.stack([x, x[::-1].copy()]).astype(np.float32)
+        cbs, tt, infos = ecasq.ecasq_solve_batched(_dev(rows), 16, 2.0,
+                                                   options=ecasq.ecasq_default_options(
+                                                       refine_rounds=0))
+        for rr in range(2):
+            o = pipeline.solve(rows[rr], 16, 2.0, refine_rounds=0, width=1, aim=False,
+                               recovery="backpointers")
+            assert int(tt[rr]) == o.t
+            np.testing.assert_array_equal(cbs[rr, :o.t].cpu().numpy(), o.codebook)
+
+
 def test_lagrangian_and_degenerate_sweep():
     x = inputs.lognormal_signed(1500, 21)
     opts = ecasq.ecasq_default_options(refine_rounds=5, dp_schedule=1)
