@@ -28,13 +28,15 @@
 //   monotone brackets (the SMAWK acceleration of Sec. 4.1): for fixed i and l
 //   the matrix T(k, j) with its columns reversed is Monge (Lemma
 //   quadrangleM), so the lowest minimiser k*(j) does not increase with j.
-//   The columns are cut into segments of 64 (one wavefront); k* of every
-//   segment end is found by a full scan split over the four wavefronts, and a
-//   segment's columns then scan only [k*(its end), k*(the previous end)].
-//   The work per row drops from (l - k_lo) (p - l) to about 2 (l - k_lo)
-//   wavefront-steps.  Where rounding breaks the monotone order of two
-//   near-equal candidates, the bracket can miss a minimiser that is better by
-//   a rounding error only.
+//   The columns are cut into segments of 64 (one wavefront).  k* of the
+//   segment ends is found coarse to fine, each end scanning the bracket
+//   left by the ends resolved before it (one wavefront per end, its lanes
+//   splitting k); a segment's columns then scan only [k*(its end), k*(the
+//   previous end)].  With n_seg = (p - 1 - l) / 64 segments the work per
+//   row drops from n_seg (l - k_lo) wavefront-steps to about
+//   (1 + log2(n_seg) / 64) (l - k_lo) + a few steps per end.  Where
+//   rounding breaks the monotone order of two near-equal candidates, a
+//   bracket can miss a minimiser that is better by a rounding error only.
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -110,6 +112,37 @@ __device__ __forceinline__ void scan(const double* __restrict__ A, const double*
     }
 }
 
+// Candidates k = k0, k0 + 64, ... <= k1 (one lane's share of a wavefront's
+// scan), strict '<' keeping the lowest k of this lane.
+__device__ __forceinline__ void scan_strided(const double* __restrict__ A,
+                                             const double* __restrict__ Y, int64_t k0,
+                                             int64_t k1, double yd, double lamp,
+                                             const double2* __restrict__ tab, double& best,
+                                             int32_t& kb) {
+    int64_t k = k0;
+    for (; k + 3 * kSeg <= k1; k += 4 * kSeg) {
+        double a4[4], y4[4];
+#pragma unroll
+        for (int u = 0; u < 4; u++) {
+            a4[u] = A[k + u * kSeg];
+            y4[u] = Y[k + u * kSeg];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; u++) {
+            const double T = __builtin_fma(-lamp, elog(y4[u] + yd, tab), a4[u]);
+            const bool lt = T < best;
+            kb = lt ? (int32_t)(k + u * kSeg) : kb;
+            best = lt ? T : best;
+        }
+    }
+    for (; k <= k1; k += kSeg) {
+        const double T = __builtin_fma(-lamp, elog(Y[k] + yd, tab), A[k]);
+        const bool lt = T < best;
+        kb = lt ? (int32_t)k : kb;
+        best = lt ? T : best;
+    }
+}
+
 __device__ __forceinline__ void emit(const OptLayerArgs& a, int64_t l, int64_t j, double C,
                                      double yu, double best, int32_t kb,
                                      const double2* __restrict__ tab) {
@@ -151,9 +184,7 @@ __global__ __launch_bounds__(kOT) void k_opt_layer2(Hist H, double* __restrict__
 template <bool FULL>
 __global__ __launch_bounds__(kOT) void k_opt_layer(OptLayerArgs a) {
     __shared__ double2 tab[kLog2Size];
-    __shared__ double mb[4][kSeg];
-    __shared__ int32_t mk[4][kSeg];
-    __shared__ int32_t kst[FULL ? 1 : kMaxSeg];
+    __shared__ int32_t kst[FULL ? 1 : kMaxSeg + 1];
     const int tid = threadIdx.x, lane = tid & (kSeg - 1), w = tid >> 6;
     const int64_t p = a.p;
     const int64_t l = p - 2 - (int64_t)blockIdx.x;  // heaviest rows first
@@ -177,43 +208,48 @@ __global__ __launch_bounds__(kOT) void k_opt_layer(OptLayerArgs a) {
         return;
     }
     const int64_t nseg = (p - 1 - l + kSeg - 1) / kSeg;
-    const int64_t kq = (khi - klo + 1 + 3) / 4;
-    // k* at the segment ends e_q = min(l + 64 (q+1), p-1), the scan split over
-    // the four wavefronts in increasing k and merged in that order
-    for (int64_t g0 = 0; g0 < nseg; g0 += kSeg) {
-        const int64_t q = g0 + lane;
-        const bool ok = q < nseg;
-        const int64_t e = ok ? min(l + kSeg * (q + 1), p - 1) : p - 1;
-        double C, yu, yd;
-        interval_y(a.H, l, e, C, yu, yd);
-        double best = HUGE_VAL;
-        int32_t kb = -1;
-        const int64_t k0 = klo + w * kq;
-        const int64_t k1 = min(k0 + kq - 1, khi);
-        scan(A, Y, k0, k1, yd, a.lamp, tab, best, kb);
-        mb[w][lane] = best;
-        mk[w][lane] = kb;
-        __syncthreads();
-        if (w == 0 && ok) {
-            double b = mb[0][lane];
-            int32_t k = mk[0][lane];
+    // k* at the segment ends e_q = min(l + 64 (q+1), p-1), kept as kst[q+1]
+    // with kst[0] = k_hi.  They do not increase with q, so they are resolved
+    // coarse to fine: at stride S the ends r = S, 3S, 5S, ... (r = q+1) scan
+    // only [k*(r+S), k*(r-S)] (k_lo past the last end), both resolved at a
+    // coarser stride.  One wavefront per end (the stride's ends dealt to the
+    // four in turn): its lanes split k and a butterfly over (T, k) keeps the
+    // lowest k of the minimum, as a scan in increasing k with strict '<' does.
+    int64_t S = 1;
+    while (S <= nseg) S <<= 1;
+    if (tid == 0) kst[0] = (int32_t)khi;
+    __syncthreads();
+    for (S >>= 1; S >= 1; S >>= 1) {
+        const int64_t nends = (nseg / S + 1) / 2;  // odd multiples of S up to nseg
+        for (int64_t m = w; m < nends; m += 4) {
+            const int64_t r = (2 * m + 1) * S;
+            const int64_t kB = kst[r - S];
+            const int64_t kA = r + S <= nseg ? (int64_t)kst[r + S] : klo;
+            const int64_t e = min(l + kSeg * r, p - 1);
+            double C, yu, yd;
+            interval_y(a.H, l, e, C, yu, yd);
+            double best = HUGE_VAL;
+            int32_t kb = -1;
+            scan_strided(A, Y, kA + lane, kB, yd, a.lamp, tab, best, kb);
 #pragma unroll
-            for (int u = 1; u < 4; u++) {
-                if (mb[u][lane] < b) {
-                    b = mb[u][lane];
-                    k = mk[u][lane];
+            for (int off = kSeg / 2; off > 0; off >>= 1) {
+                const double ob = __shfl_xor(best, off);
+                const int32_t okb = __shfl_xor(kb, off);
+                if (ob < best || (ob == best && okb < kb)) {
+                    best = ob;
+                    kb = okb;
                 }
             }
-            kst[q] = k;
+            // no finite candidate (not reached for finite inputs): keep the
+            // bracket's low end so later brackets stay inside [k_lo, k_hi]
+            if (lane == 0) kst[r] = kb < 0 ? (int32_t)kA : kb;
         }
         __syncthreads();
     }
     // each segment's columns scan between the minimisers of its end and of
     // the previous segment's end
     for (int64_t q = w; q < nseg; q += 4) {
-        const int64_t kA = kst[q];
-        const int64_t kB = q == 0 ? khi : kst[q - 1];
-        const int64_t k0 = min(kA, kB), k1 = max(kA, kB);
+        const int64_t k0 = kst[q + 1], k1 = kst[q];
         const int64_t j = l + 1 + kSeg * q + lane;
         const bool ok = j < p;
         double C = 0.0, yu = 0.0, yd = 0.0;
