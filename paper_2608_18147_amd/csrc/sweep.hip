@@ -181,10 +181,11 @@ __device__ __forceinline__ void stage_pred(const SweepArgs& a, int64_t k0, int32
 }
 
 // Tile role: column blocks J > t take predecessor block t-1 for one layer
-// group.  split = 0: one column block per wavefront, all LG layers; split = 1:
-// one column block per workgroup, LG/4 layers per wavefront (more waves, for
-// the late steps that have few blocks left).
-template <int LG>
+// group.  split = 0: one column block per wavefront, the group's first NL
+// layers (NL < LG only where the layers past them exceed I); split = 1: one
+// column block per workgroup, LG/4 layers per wavefront (more waves, for the
+// late steps that have few blocks left).
+template <int LG, int NL>
 __device__ void tile_role(const SweepArgs& a, int64_t t, int32_t split, int64_t wg, int32_t g,
                           StepSmem<LG>& sm) {
     constexpr int LW = LG / kTileWaves;
@@ -205,10 +206,10 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int32_t split, int64_t 
         accumulate<LG, LW>(sm, wave * LW, cv, cN, cS, cS2, a.H.dd, a.lamp, best);
         store_running<LW>(a, j, iw, best);
     } else {
-        double best[LG];
-        load_running<LG>(a, jj, i0, best);
-        accumulate<LG, LG>(sm, 0, cv, cN, cS, cS2, a.H.dd, a.lamp, best);
-        store_running<LG>(a, j, i0, best);
+        double best[NL];
+        load_running<NL>(a, jj, i0, best);
+        accumulate<LG, NL>(sm, 0, cv, cN, cS, cS2, a.H.dd, a.lamp, best);
+        store_running<NL>(a, j, i0, best);
     }
 }
 
@@ -312,7 +313,7 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
 
 // Step t of the sweep: workgroup 0 makes block t final, the others add
 // predecessor block t-1 to the blocks after it (tile WG index = g * nx + wg).
-template <int LG>
+template <int LG, int NL>
 __global__ __launch_bounds__(kSB* kTileWaves) ECASQ_STEP_ATTR void k_sweep_step(SweepArgs a,
                                                                                int64_t t,
                                                               int32_t split, int64_t nx) {
@@ -326,7 +327,7 @@ __global__ __launch_bounds__(kSB* kTileWaves) ECASQ_STEP_ATTR void k_sweep_step(
         diag_role<LG>(a, t, sm);
     } else {
         const int64_t x = (int64_t)blockIdx.x - 1;
-        tile_role<LG>(a, t, split, x % nx, (int32_t)(x / nx), sm);
+        tile_role<LG, NL>(a, t, split, x % nx, (int32_t)(x / nx), sm);
     }
 }
 
@@ -527,7 +528,7 @@ SweepArgs make_args(const SweepSolve& S) {
     return a;
 }
 
-template <int LG>
+template <int LG, int NL = LG>
 hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
     const int32_t ngroups = (a.I - 2 + LG - 1) / LG;
     {
@@ -542,7 +543,7 @@ hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
         // else one column block per workgroup with the layers split
         const int32_t split = ntiles * ngroups < kSplitBelow ? 1 : 0;
         const int64_t nx = split ? ntiles : (ntiles + kTileWaves - 1) / kTileWaves;
-        k_sweep_step<LG><<<(unsigned)(1 + nx * ngroups), kSB * kTileWaves, 0, st>>>(
+        k_sweep_step<LG, NL><<<(unsigned)(1 + nx * ngroups), kSB * kTileWaves, 0, st>>>(
             a, t, split, nx > 0 ? nx : 1);
     }
     return hipGetLastError();
@@ -576,6 +577,8 @@ hipError_t launch_sweep(const SweepSolve& S, int32_t exact_s, double* out, int32
         e = sweep_launch<8>(a, st);
     else if (L <= 16 || ECASQ_SWEEP_LG_MAX == 16)
         e = sweep_launch<16>(a, st);
+    else if (L == 30)  // s = 32: one group without its two layers past I
+        e = sweep_launch<32, 30>(a, st);
     else
         e = sweep_launch<32>(a, st);
     if (e != hipSuccess) return e;
