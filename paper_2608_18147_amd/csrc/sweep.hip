@@ -37,13 +37,17 @@ namespace {
 
 constexpr int kSB = 64;        // columns per block (one wavefront)
 constexpr int kTileWaves = 4;  // wavefronts per workgroup
-// below this many (column block, layer group) tiles a step splits layers
-// over the wavefronts of a workgroup (fewer tiles than SIMDs: splitting buys
-// wavefronts at the price of evaluating C and Phi once per wavefront)
-#ifndef ECASQ_SWEEP_SPLIT_BELOW
-#define ECASQ_SWEEP_SPLIT_BELOW 512
+// Wavefronts per column block in the tile role (the block's 64 predecessors
+// split between them; their partial minima meet in LDS): 4 below
+// ECASQ_SWEEP_SP4_BELOW (column block, layer group) tiles, 2 below
+// ECASQ_SWEEP_SP2_BELOW, else 1.  More wavefronts per tile fill the SIMDs of
+// the late steps, which have few blocks left, without recomputing C and Phi.
+#ifndef ECASQ_SWEEP_SP4_BELOW
+#define ECASQ_SWEEP_SP4_BELOW 1024
 #endif
-constexpr int64_t kSplitBelow = ECASQ_SWEEP_SPLIT_BELOW;
+#ifndef ECASQ_SWEEP_SP2_BELOW
+#define ECASQ_SWEEP_SP2_BELOW 1536
+#endif
 // widest layer group (register arrays of that many layers per lane)
 #ifndef ECASQ_SWEEP_LG_MAX
 #define ECASQ_SWEEP_LG_MAX 32
@@ -138,15 +142,15 @@ __device__ __forceinline__ void store_running(const SweepArgs& a, int64_t j, int
     }
 }
 
-// The 64 staged predecessors against column (cv, cN, cS, cS2) for LW layers
-// whose F_{i-1} sit in sF columns lofs..lofs+LW-1.
+// Staged predecessors kb..ke-1 (ke - kb even) against column (cv, cN, cS,
+// cS2) for LW layers whose F_{i-1} sit in sF columns lofs..lofs+LW-1.
 template <int LG, int LW>
-__device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int lofs, double cv, double cN,
-                                           double cS, double cS2, double dd, double lamp,
-                                           double (&best)[LW]) {
+__device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int lofs, int kb, int ke,
+                                           double cv, double cN, double cS, double cS2, double dd,
+                                           double lamp, double (&best)[LW]) {
     if constexpr (LW > ECASQ_SWEEP_PAIR_MAX) {
         // many layers per predecessor: enough independent work per iteration
-        for (int kk = 0; kk < kSB; kk++) {
+        for (int kk = kb; kk < ke; kk++) {
             double C, P;
             cell_terms(sm.sv[kk], sm.sN[kk], sm.sS[kk], sm.sS2[kk], cv, cN, cS, cS2, dd, false,
                        0.0, sm.tab, C, P);
@@ -157,7 +161,7 @@ __device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int lofs, dou
     } else {
     // few layers: two predecessors per iteration, whose C and Phi are
     // independent chains the scheduler can interleave
-    for (int kk = 0; kk < kSB; kk += 2) {
+    for (int kk = kb; kk < ke; kk += 2) {
         double C0, P0, C1, P1;
         cell_terms(sm.sv[kk], sm.sN[kk], sm.sS[kk], sm.sS2[kk], cv, cN, cS, cS2, dd, false, 0.0,
                    sm.tab, C0, P0);
@@ -181,47 +185,76 @@ __device__ __forceinline__ void stage_pred(const SweepArgs& a, int64_t k0, int32
 }
 
 // Tile role: column blocks J > t take predecessor block t-1 for one layer
-// group.  split = 0: one column block per wavefront, the group's first NL
-// layers (NL < LG only where the layers past them exceed I); split = 1: one
-// column block per workgroup, LG/4 layers per wavefront (more waves, for the
-// late steps that have few blocks left).
-template <int LG, int NL>
-__device__ void tile_role(const SweepArgs& a, int64_t t, int32_t split, int64_t wg, int32_t g,
-                          StepSmem<LG>& sm) {
-    constexpr int LW = LG / kTileWaves;
+// group (its first NL layers; NL < LG only where the layers past them exceed
+// I).  SP wavefronts per column block, each taking 64/SP of the
+// predecessors; with SP > 1 their partial minima meet in LDS (the staging
+// buffer, free once every wavefront is done with it), LG/4 layers at a time,
+// and one wavefront per chunk merges them into the running minima in F.
+template <int LG, int NL, int SP>
+__device__ void tile_role(const SweepArgs& a, int64_t t, int64_t wg, int32_t g, StepSmem<LG>& sm) {
+    constexpr int KP = kSB / SP;
     const int32_t i0 = 3 + g * LG;
     const int64_t k0 = (t - 1) * kSB;
+    const int64_t p = a.H.p;
     stage_pred<LG>(a, k0, i0, sm);
     __syncthreads();
     const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
-    const int64_t J = split ? t + 1 + wg : t + 1 + wg * kTileWaves + wave;
-    if (J >= a.nblk) return;
+    const int part = wave % SP;
+    const int64_t J = t + 1 + wg * (kTileWaves / SP) + wave / SP;
+    const bool live = J < a.nblk;  // the same for the SP wavefronts of a column block
+    if (SP == 1 && !live) return;  // (no barrier follows for SP = 1)
     const int64_t j = J * kSB + lane;
-    const int64_t jj = j < a.H.p ? j : a.H.p - 1;
+    const int64_t jj = live && j < p ? j : p - 1;
     const double cv = a.H.v[jj], cN = a.H.N[jj], cS = a.H.S[jj], cS2 = a.H.S2[jj];
-    if (split) {
-        double best[LW];
-        const int32_t iw = i0 + wave * LW;
-        load_running<LW>(a, jj, iw, best);
-        accumulate<LG, LW>(sm, wave * LW, cv, cN, cS, cS2, a.H.dd, a.lamp, best);
-        store_running<LW>(a, j, iw, best);
-    } else {
-        double best[NL];
+    double best[NL];
+    if constexpr (SP == 1) {
         load_running<NL>(a, jj, i0, best);
-        accumulate<LG, NL>(sm, 0, cv, cN, cS, cS2, a.H.dd, a.lamp, best);
+    } else {
+#pragma unroll
+        for (int l = 0; l < NL; l++) best[l] = __builtin_huge_val();
+    }
+    accumulate<LG, NL>(sm, 0, part * KP, part * KP + KP, cv, cN, cS, cS2, a.H.dd, a.lamp, best);
+    if constexpr (SP == 1) {
         store_running<NL>(a, j, i0, best);
+    } else {
+        constexpr int CH = LG / kTileWaves;  // 4 x CH rows of 64 fit the staging buffer
+        double (*xb)[kSB] = reinterpret_cast<double (*)[kSB]>(&sm.sF[0][0]);
+        const int lead = wave - part;
+        __syncthreads();  // the staging buffer is free
+#pragma unroll
+        for (int c0 = 0; c0 < NL; c0 += CH) {
+            const int c = c0 / CH;
+#pragma unroll
+            for (int l = c0; l < c0 + CH && l < NL; l++) xb[wave * CH + l - c0][lane] = best[l];
+            __syncthreads();
+            if (live && part == c % SP) {
+#pragma unroll
+                for (int l = c0; l < c0 + CH && l < NL; l++) {
+                    const int32_t i = i0 + l;
+                    if (i > a.I) break;
+                    double v = a.F[(int64_t)i * a.ld + jj];
+#pragma unroll
+                    for (int u = 0; u < SP; u++) v = __builtin_fmin(v, xb[(lead + u) * CH + l - c0][lane]);
+                    if (j < p) a.F[(int64_t)i * a.ld + j] = v;
+                }
+            }
+            __syncthreads();
+        }
     }
 }
 
 // Diagonal role (workgroup 0): block t becomes final.  For every layer group:
-// predecessor block t-1 (LG/4 layers per wavefront), then the group's layers
-// inside the block in order; each wavefront holds C and Phi of 16 of the
-// block's predecessors in registers, the four partial minima meet in LDS and
-// the wavefront that holds the layer's running minimum merges them.
-template <int LG>
+// predecessor block t-1, each wavefront taking 16 of its predecessors for
+// all the group's layers, the four partial minima merged in LDS by the
+// wavefront that holds a layer (layers ow*LG/4.. of the group on wavefront
+// ow, with their running minima); then the group's layers inside the block in
+// order: each wavefront holds the cost Q of 16 of the block's predecessors in
+// registers, the four partial minima meet in LDS and the wavefront that holds
+// the layer merges them.
+template <int LG, int NL>
 __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
     constexpr int LW = LG / kTileWaves;
-    constexpr int KW = kSB / kTileWaves;  // predecessors of the block per wavefront
+    constexpr int KW = kSB / kTileWaves;  // predecessors of a block per wavefront
     const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
     const int64_t p = a.H.p;
     const int64_t j0 = t * kSB;
@@ -239,20 +272,6 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
     __syncthreads();
     const int c = (int)(jj - j0);
     const double cv = sm.dv[c], cN = sm.dN[c], cS = sm.dS[c], cS2 = sm.dS2[c];
-    // the cost Q = C - lambda' Phi of (k, j) for this wavefront's 16
-    // predecessors k < j; the others get +inf, so their candidates are +inf
-    double cQ[KW];
-#pragma unroll
-    for (int q = 0; q < KW; q++) {
-        const int kk = wave * KW + q;
-        cQ[q] = __builtin_huge_val();
-        if (j0 + kk < jj) {
-            double C, P;
-            cell_terms(sm.dv[kk], sm.dN[kk], sm.dS[kk], sm.dS2[kk], cv, cN, cS, cS2, dd, false,
-                       0.0, sm.tab, C, P);
-            cQ[q] = __builtin_fma(-lamp, P, C);
-        }
-    }
     // layer 2 (eq. apx_base): the first interval (v_0, v_j]
     if (wave == 0) {
         double f = __builtin_huge_val();
@@ -270,10 +289,45 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
         load_running<LW>(a, jj, iw, best);
         __syncthreads();  // previous group's use of sF / pF is over
         if (t >= 1) {
-            const int64_t k0 = (t - 1) * kSB;
-            stage_pred<LG>(a, k0, i0, sm);
+            stage_pred<LG>(a, (t - 1) * kSB, i0, sm);
             __syncthreads();
-            accumulate<LG, LW>(sm, wave * LW, cv, cN, cS, cS2, dd, lamp, best);
+            double pa[NL];
+#pragma unroll
+            for (int l = 0; l < NL; l++) pa[l] = __builtin_huge_val();
+            accumulate<LG, NL>(sm, 0, wave * KW, wave * KW + KW, cv, cN, cS, cS2, dd, lamp, pa);
+            __syncthreads();  // the staging buffer is free: 4 x LW rows of 64
+            double (*xb)[kSB] = reinterpret_cast<double (*)[kSB]>(&sm.sF[0][0]);
+#pragma unroll
+            for (int ow = 0; ow < kTileWaves; ow++) {
+                if (ow * LW >= NL) break;
+#pragma unroll
+                for (int q = 0; q < LW && ow * LW + q < NL; q++) xb[wave * LW + q][lane] = pa[ow * LW + q];
+                __syncthreads();
+                if (wave == ow) {
+#pragma unroll
+                    for (int q = 0; q < LW && ow * LW + q < NL; q++)
+                        best[q] = __builtin_fmin(
+                            best[q], __builtin_fmin(__builtin_fmin(xb[q][lane], xb[LW + q][lane]),
+                                                    __builtin_fmin(xb[2 * LW + q][lane],
+                                                                   xb[3 * LW + q][lane])));
+                }
+                __syncthreads();
+            }
+        }
+        // the cost Q = C - lambda' Phi of (k, j) for this wavefront's 16
+        // predecessors k < j of the block; the others get +inf, so their
+        // candidates are +inf
+        double cQ[KW];
+#pragma unroll
+        for (int q = 0; q < KW; q++) {
+            const int kk = wave * KW + q;
+            cQ[q] = __builtin_huge_val();
+            if (j0 + kk < jj) {
+                double C, P;
+                cell_terms(sm.dv[kk], sm.dN[kk], sm.dS[kk], sm.dS2[kk], cv, cN, cS, cS2, dd,
+                           false, 0.0, sm.tab, C, P);
+                cQ[q] = __builtin_fma(-lamp, P, C);
+            }
         }
         // layer l = ow * LW + q of the group: held by wavefront ow at q
 #pragma unroll 1
@@ -316,7 +370,8 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
 template <int LG, int NL>
 __global__ __launch_bounds__(kSB* kTileWaves) ECASQ_STEP_ATTR void k_sweep_step(SweepArgs a,
                                                                                int64_t t,
-                                                              int32_t split, int64_t nx) {
+                                                                               int32_t sp,
+                                                                               int64_t nx) {
     __shared__ StepSmem<LG> sm;
     load_log2_table(sm.tab);
     __syncthreads();
@@ -324,10 +379,17 @@ __global__ __launch_bounds__(kSB* kTileWaves) ECASQ_STEP_ATTR void k_sweep_step(
         // the diagonal block is the step's critical path: let its waves issue
         // ahead of tile waves that share its SIMDs
         __builtin_amdgcn_s_setprio(3);
-        diag_role<LG>(a, t, sm);
+        diag_role<LG, NL>(a, t, sm);
     } else {
         const int64_t x = (int64_t)blockIdx.x - 1;
-        tile_role<LG, NL>(a, t, split, x % nx, (int32_t)(x / nx), sm);
+        const int64_t wg = x % nx;
+        const int32_t g = (int32_t)(x / nx);
+        if (sp == 4)
+            tile_role<LG, NL, 4>(a, t, wg, g, sm);
+        else if (sp == 2)
+            tile_role<LG, NL, 2>(a, t, wg, g, sm);
+        else
+            tile_role<LG, NL, 1>(a, t, wg, g, sm);
     }
 }
 
@@ -539,12 +601,12 @@ hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
     }
     for (int64_t t = 0; t < a.nblk; t++) {
         const int64_t ntiles = (t >= 1 && ngroups > 0) ? a.nblk - t - 1 : 0;
-        // whole-group wavefronts while they give at least two per SIMD,
-        // else one column block per workgroup with the layers split
-        const int32_t split = ntiles * ngroups < kSplitBelow ? 1 : 0;
-        const int64_t nx = split ? ntiles : (ntiles + kTileWaves - 1) / kTileWaves;
+        const int64_t tiles = ntiles * ngroups;
+        const int32_t sp = tiles < ECASQ_SWEEP_SP4_BELOW ? 4 : tiles < ECASQ_SWEEP_SP2_BELOW ? 2 : 1;
+        const int64_t per = kTileWaves / sp;  // column blocks per workgroup
+        const int64_t nx = (ntiles + per - 1) / per;
         k_sweep_step<LG, NL><<<(unsigned)(1 + nx * ngroups), kSB * kTileWaves, 0, st>>>(
-            a, t, split, nx > 0 ? nx : 1);
+            a, t, sp, nx > 0 ? nx : 1);
     }
     return hipGetLastError();
 }
