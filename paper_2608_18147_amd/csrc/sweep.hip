@@ -196,23 +196,26 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int64_t wg, int32_t g, 
     const int32_t i0 = 3 + g * LG;
     const int64_t k0 = (t - 1) * kSB;
     const int64_t p = a.H.p;
-    stage_pred<LG>(a, k0, i0, sm);
-    __syncthreads();
     const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
     const int part = wave % SP;
     const int64_t J = t + 1 + wg * (kTileWaves / SP) + wave / SP;
     const bool live = J < a.nblk;  // the same for the SP wavefronts of a column block
-    if (SP == 1 && !live) return;  // (no barrier follows for SP = 1)
     const int64_t j = J * kSB + lane;
     const int64_t jj = live && j < p ? j : p - 1;
+    // this column's values and running minima first: their latency overlaps
+    // the table and staging loads
     const double cv = a.H.v[jj], cN = a.H.N[jj], cS = a.H.S[jj], cS2 = a.H.S2[jj];
     double best[NL];
     if constexpr (SP == 1) {
-        load_running<NL>(a, jj, i0, best);
+        if (live) load_running<NL>(a, jj, i0, best);
     } else {
 #pragma unroll
         for (int l = 0; l < NL; l++) best[l] = __builtin_huge_val();
     }
+    load_log2_table(sm.tab);
+    stage_pred<LG>(a, k0, i0, sm);
+    __syncthreads();
+    if (SP == 1 && !live) return;  // (no barrier follows for SP = 1)
     accumulate<LG, NL>(sm, 0, part * KP, part * KP + KP, cv, cN, cS, cS2, a.H.dd, a.lamp, best);
     if constexpr (SP == 1) {
         store_running<NL>(a, j, i0, best);
@@ -262,6 +265,7 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
     const int64_t jj = j < p ? j : p - 1;
     const bool valid = j < p;
     const double lamp = a.lamp, dd = a.H.dd;
+    load_log2_table(sm.tab);
     for (int x = threadIdx.x; x < kSB; x += blockDim.x) {
         const int64_t k = j0 + x < p ? j0 + x : p - 1;
         sm.dv[x] = a.H.v[k];
@@ -373,8 +377,7 @@ __global__ __launch_bounds__(kSB* kTileWaves) ECASQ_STEP_ATTR void k_sweep_step(
                                                                                int32_t sp,
                                                                                int64_t nx) {
     __shared__ StepSmem<LG> sm;
-    load_log2_table(sm.tab);
-    __syncthreads();
+    // each role loads the log2 table with its first staging (one barrier)
     if (blockIdx.x == 0) {
         // the diagonal block is the step's critical path: let its waves issue
         // ahead of tile waves that share its SIMDs
