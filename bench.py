@@ -61,8 +61,8 @@ TRAFFIC_SOURCES_SHA = "f3a631b21f5b78fb"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
-SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 6.749e7
-SWEEP_TRAFFIC_SHA = "294d9c7c89771c89"
+SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 6.751e7
+SWEEP_TRAFFIC_SHA = "5e747c6953b5998d"
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 
 
