@@ -64,6 +64,8 @@ KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 6.751e7
 SWEEP_TRAFFIC_SHA = "5e747c6953b5998d"
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
+# the (workload, s) both traffic figures were measured on; null for others
+TRAFFIC_WORKLOAD = ("weights_256k", 32)
 
 
 def kernel_sources_sha(files=None):
@@ -80,7 +82,7 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def sweep_roofline(p, s, ms, solves, cells):
+def sweep_roofline(p, s, ms, solves, cells, measured=True):
     """Roofline of DP schedule 1: all k_sweep_step launches of one solve timed
     as one unit.  Algorithmic ops per solve: 19 per (k, j) pair (its C, Phi
     and cost Q, shared by all layers), 2 per (k, j, layer) cell of layers
@@ -100,7 +102,8 @@ def sweep_roofline(p, s, ms, solves, cells):
         "unit": "TOP/s (fp64 lane ops)",
         "frac": achieved / ALU_PEAK_TOPS,
         "traffic": (SWEEP_TRAFFIC_BYTES_PER_LAUNCH
-                    if kernel_sources_sha(SWEEP_SOURCES) == SWEEP_TRAFFIC_SHA else None),
+                    if measured and kernel_sources_sha(SWEEP_SOURCES) == SWEEP_TRAFFIC_SHA
+                    else None),
         "traffic_unit": "bytes/launch",
         "ops_per_solve": ops,
         "avg_launch_ms": per_ms / steps,
@@ -400,8 +403,9 @@ def main():
     value = nominal / elapsed
     info, ent = infos[-1]
     p = info["p"]
+    measured = (args.workload, s) == TRAFFIC_WORKLOAD
     if sweep:
-        roofline = sweep_roofline(p, s, msw, nsw, cellsw)
+        roofline = sweep_roofline(p, s, msw, nsw, cellsw, measured)
     else:
         avg_ms = ms / max(launches, 1)
         fpc = flops_per_cell(LAMBDAS_PER_PASS)
@@ -413,8 +417,8 @@ def main():
             "peak": ALU_PEAK_TOPS,
             "unit": "TOP/s (fp64 lane ops)",
             "frac": achieved / ALU_PEAK_TOPS,
-            "traffic": (TRAFFIC_BYTES_PER_LAUNCH if kernel_sources_sha() == TRAFFIC_SOURCES_SHA
-                        else None),
+            "traffic": (TRAFFIC_BYTES_PER_LAUNCH
+                        if measured and kernel_sources_sha() == TRAFFIC_SOURCES_SHA else None),
             "traffic_unit": "bytes/launch",
             "ops_per_cell": fpc,
             "avg_launch_ms": avg_ms,
