@@ -189,7 +189,8 @@ __device__ __forceinline__ void stage_pred(const SweepArgs& a, int64_t k0, int32
 // I).  SP wavefronts per column block, each taking 64/SP of the
 // predecessors; with SP > 1 their partial minima meet in LDS (the staging
 // buffer, free once every wavefront is done with it), LG/4 layers at a time,
-// and one wavefront per chunk merges them into the running minima in F.
+// and the wavefront that merges a chunk (its partial started from the
+// chunk's running minima) writes the result to F.
 template <int LG, int NL, int SP>
 __device__ void tile_role(const SweepArgs& a, int64_t t, int64_t wg, int32_t g, StepSmem<LG>& sm) {
     constexpr int KP = kSB / SP;
@@ -205,12 +206,18 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int64_t wg, int32_t g, 
     // this column's values and running minima first: their latency overlaps
     // the table and staging loads
     const double cv = a.H.v[jj], cN = a.H.N[jj], cS = a.H.S[jj], cS2 = a.H.S2[jj];
+    constexpr int CH = LG / kTileWaves;  // layers per merge chunk (SP > 1)
     double best[NL];
     if constexpr (SP == 1) {
         if (live) load_running<NL>(a, jj, i0, best);
     } else {
+        // the wavefront that merges a chunk starts from its running minima
 #pragma unroll
-        for (int l = 0; l < NL; l++) best[l] = __builtin_huge_val();
+        for (int l = 0; l < NL; l++) {
+            const int32_t i = i0 + l;
+            best[l] = (live && part == (l / CH) % SP && i <= a.I) ? a.F[(int64_t)i * a.ld + jj]
+                                                                 : __builtin_huge_val();
+        }
     }
     load_log2_table(sm.tab);
     stage_pred<LG>(a, k0, i0, sm);
@@ -220,7 +227,7 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int64_t wg, int32_t g, 
     if constexpr (SP == 1) {
         store_running<NL>(a, j, i0, best);
     } else {
-        constexpr int CH = LG / kTileWaves;  // 4 x CH rows of 64 fit the staging buffer
+        // 4 x CH rows of 64 fit the staging buffer
         double (*xb)[kSB] = reinterpret_cast<double (*)[kSB]>(&sm.sF[0][0]);
         const int lead = wave - part;
         __syncthreads();  // the staging buffer is free
@@ -235,9 +242,9 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int64_t wg, int32_t g, 
                 for (int l = c0; l < c0 + CH && l < NL; l++) {
                     const int32_t i = i0 + l;
                     if (i > a.I) break;
-                    double v = a.F[(int64_t)i * a.ld + jj];
+                    double v = xb[lead * CH + l - c0][lane];
 #pragma unroll
-                    for (int u = 0; u < SP; u++) v = __builtin_fmin(v, xb[(lead + u) * CH + l - c0][lane]);
+                    for (int u = 1; u < SP; u++) v = __builtin_fmin(v, xb[(lead + u) * CH + l - c0][lane]);
                     if (j < p) a.F[(int64_t)i * a.ld + j] = v;
                 }
             }
