@@ -20,14 +20,16 @@
 // The path's MSE and H(I,B) are then summed along it in path order (the same
 // additions the layer-by-layer accumulators perform).
 //
-// Step t of the sweep (blocks of 64 columns, one per wavefront) is one launch
-// of k_sweep_step:
-//   workgroup 0    block t: the contribution of block t-1, then the
-//                  triangle inside block t layer after layer (a layer needs
-//                  the previous layer's values of the same block), which
-//                  makes block t final;
-//   the others     blocks J > t: the contribution of block t-1 (final since
-//                  step t-1) to their running minima, kept in F.
+// A step of the sweep (blocks of 64 columns, one per wavefront) is one launch
+// of k_sweep_step that makes blocks t..t+nb-1 final (nb = 2 in the early
+// steps, where the tiles fill the GPU, else 1), with blocks kp0..t-1 made
+// final by the step before:
+//   workgroup 0    blocks t..t+nb-1 in order: the contribution of the
+//                  final blocks not yet added to the block, then the
+//                  triangle inside it layer after layer (a layer needs the
+//                  previous layer's values of the same block);
+//   the others     blocks J >= t+nb: the contribution of blocks kp0..t-1 to
+//                  their running minima, kept in F.
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -44,6 +46,11 @@ constexpr int kTileWaves = 4;  // wavefronts per workgroup
 // the late steps, which have few blocks left, without recomputing C and Phi.
 #ifndef ECASQ_SWEEP_SP4_BELOW
 #define ECASQ_SWEEP_SP4_BELOW 1024
+#endif
+// (column block, layer group) tiles from which a step makes two diagonal
+// blocks final (a launch's fixed cost is then shared by two blocks)
+#ifndef ECASQ_SWEEP_PAIR_ABOVE
+#define ECASQ_SWEEP_PAIR_ABOVE 2048
 #endif
 #ifndef ECASQ_SWEEP_SP2_BELOW
 #define ECASQ_SWEEP_SP2_BELOW 1536
@@ -184,22 +191,22 @@ __device__ __forceinline__ void stage_pred(const SweepArgs& a, int64_t k0, int32
     stage_block<LG>(a, k0, i0, sm.sv, sm.sN, sm.sS, sm.sS2, sm.sF);
 }
 
-// Tile role: column blocks J > t take predecessor block t-1 for one layer
-// group (its first NL layers; NL < LG only where the layers past them exceed
-// I).  SP wavefronts per column block, each taking 64/SP of the
+// Tile role: column blocks J >= t + nb take the predecessor blocks kp0..t-1
+// (made final by the last step) for one layer group (its first NL layers;
+// NL < LG only where the layers past them exceed I).  SP wavefronts per column block, each taking 64/SP of the
 // predecessors; with SP > 1 their partial minima meet in LDS (the staging
 // buffer, free once every wavefront is done with it), LG/4 layers at a time,
 // and the wavefront that merges a chunk (its partial started from the
 // chunk's running minima) writes the result to F.
-template <int LG, int NL, int SP>
-__device__ void tile_role(const SweepArgs& a, int64_t t, int64_t wg, int32_t g, StepSmem<LG>& sm) {
+template <int LG, int NL, int SP, int MP>
+__device__ void tile_role(const SweepArgs& a, int64_t t, int32_t nb, int64_t kp0, int64_t wg,
+                          int32_t g, StepSmem<LG>& sm) {
     constexpr int KP = kSB / SP;
     const int32_t i0 = 3 + g * LG;
-    const int64_t k0 = (t - 1) * kSB;
     const int64_t p = a.H.p;
     const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
     const int part = wave % SP;
-    const int64_t J = t + 1 + wg * (kTileWaves / SP) + wave / SP;
+    const int64_t J = t + nb + wg * (kTileWaves / SP) + wave / SP;
     const bool live = J < a.nblk;  // the same for the SP wavefronts of a column block
     const int64_t j = J * kSB + lane;
     const int64_t jj = live && j < p ? j : p - 1;
@@ -220,10 +227,27 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int64_t wg, int32_t g, 
         }
     }
     load_log2_table(sm.tab);
-    stage_pred<LG>(a, k0, i0, sm);
-    __syncthreads();
-    if (SP == 1 && !live) return;  // (no barrier follows for SP = 1)
-    accumulate<LG, NL>(sm, 0, part * KP, part * KP + KP, cv, cN, cS, cS2, a.H.dd, a.lamp, best);
+    // predecessor blocks kp0..t-1 (at most MP; tiles run only when there is
+    // one), one staged at a time
+    if constexpr (MP == 1) {
+        stage_pred<LG>(a, (t - 1) * kSB, i0, sm);
+        __syncthreads();
+        if (SP == 1 && !live) return;  // (no barrier follows for SP = 1)
+        accumulate<LG, NL>(sm, 0, part * KP, part * KP + KP, cv, cN, cS, cS2, a.H.dd, a.lamp,
+                           best);
+    } else {
+        const int np = (int)min<int64_t>(t - kp0, MP);
+        for (int u = 0; u < np; u++) {
+            const int64_t pb = t - np + u;
+            if (u > 0) __syncthreads();  // every wavefront is done with the last block
+            stage_pred<LG>(a, pb * kSB, i0, sm);
+            __syncthreads();
+            if (live)
+                accumulate<LG, NL>(sm, 0, part * KP, part * KP + KP, cv, cN, cS, cS2, a.H.dd,
+                                   a.lamp, best);
+        }
+        if (SP == 1 && !live) return;  // (no barrier follows for SP = 1)
+    }
     if constexpr (SP == 1) {
         store_running<NL>(a, j, i0, best);
     } else {
@@ -253,16 +277,19 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int64_t wg, int32_t g, 
     }
 }
 
-// Diagonal role (workgroup 0): block t becomes final.  For every layer group:
-// predecessor block t-1, each wavefront taking 16 of its predecessors for
-// all the group's layers, the four partial minima merged in LDS by the
-// wavefront that holds a layer (layers ow*LG/4.. of the group on wavefront
-// ow, with their running minima); then the group's layers inside the block in
-// order: each wavefront holds the cost Q of 16 of the block's predecessors in
-// registers, the four partial minima meet in LDS and the wavefront that holds
-// the layer merges them.
-template <int LG, int NL>
-__device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
+// Diagonal role (workgroup 0): blocks t..t+nb-1 become final, in order.  For
+// block b and every layer group: the predecessor blocks kp0..b-1 not yet
+// added to it (those the last step made final, and block t when b = t+1),
+// each wavefront taking 16 predecessors of each for all the group's layers,
+// the four partial minima merged in LDS by the wavefront that holds a layer
+// (layers ow*LG/4.. of the group on wavefront ow, with their running
+// minima); then the group's layers inside the block in order: each wavefront
+// holds the cost Q of 16 of the block's predecessors in registers, the four
+// partial minima meet in LDS and the wavefront that holds the layer merges
+// them.  A block's final values are read back from F for the next block
+// after the workgroup barrier that orders them.
+template <int LG, int NL, int MP>
+__device__ void diag_block(const SweepArgs& a, int64_t t, int64_t kp0, StepSmem<LG>& sm) {
     constexpr int LW = LG / kTileWaves;
     constexpr int KW = kSB / kTileWaves;  // predecessors of a block per wavefront
     const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
@@ -272,7 +299,6 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
     const int64_t jj = j < p ? j : p - 1;
     const bool valid = j < p;
     const double lamp = a.lamp, dd = a.H.dd;
-    load_log2_table(sm.tab);
     for (int x = threadIdx.x; x < kSB; x += blockDim.x) {
         const int64_t k = j0 + x < p ? j0 + x : p - 1;
         sm.dv[x] = a.H.v[k];
@@ -299,8 +325,11 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
         double best[LW];
         load_running<LW>(a, jj, iw, best);
         __syncthreads();  // previous group's use of sF / pF is over
-        if (t >= 1) {
-            stage_pred<LG>(a, (t - 1) * kSB, i0, sm);
+        // each final block not yet added (at most MP): a partial per
+        // wavefront, merged into the layers' holders before the next block
+        // is staged
+        auto add_block = [&](int64_t pb) {
+            stage_pred<LG>(a, pb * kSB, i0, sm);
             __syncthreads();
             double pa[NL];
 #pragma unroll
@@ -323,6 +352,15 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
                                                                    xb[3 * LW + q][lane])));
                 }
                 __syncthreads();
+            }
+        };
+        if constexpr (MP == 1) {
+            if (kp0 < t) add_block(t - 1);
+        } else {
+            const int np = (int)min<int64_t>(t - kp0, MP);
+            for (int u = 0; u < np; u++) {
+                if (u > 0) __syncthreads();  // the last merge is done with the buffer
+                add_block(t - np + u);
             }
         }
         // the cost Q = C - lambda' Phi of (k, j) for this wavefront's 16
@@ -376,30 +414,42 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, StepSmem<LG>& sm) {
     }
 }
 
-// Step t of the sweep: workgroup 0 makes block t final, the others add
-// predecessor block t-1 to the blocks after it (tile WG index = g * nx + wg).
-template <int LG, int NL>
-__global__ __launch_bounds__(kSB* kTileWaves) ECASQ_STEP_ATTR void k_sweep_step(SweepArgs a,
-                                                                               int64_t t,
-                                                                               int32_t sp,
-                                                                               int64_t nx) {
+template <int LG, int NL, int MP, int NB>
+__device__ void diag_role(const SweepArgs& a, int64_t t, int64_t kp0, StepSmem<LG>& sm) {
+    load_log2_table(sm.tab);
+    diag_block<LG, NL, MP>(a, t, kp0, sm);
+    if constexpr (NB == 2) {
+        if (t + 1 < a.nblk) {
+            __syncthreads();  // the first block's use of LDS is over
+            diag_block<LG, NL, MP + 1>(a, t + 1, kp0, sm);
+        }
+    }
+}
+
+// One step of the sweep: workgroup 0 makes blocks t..t+nb-1 final, the others
+// add predecessor blocks kp0..t-1 to the blocks after them (tile WG index =
+// g * nx + wg).
+template <int LG, int NL, int MP, int NB>
+__global__ __launch_bounds__(kSB* kTileWaves) ECASQ_STEP_ATTR void k_sweep_step(
+    SweepArgs a, int64_t t, int64_t kp0, int32_t sp, int64_t nx) {
+    constexpr int32_t nb = NB;
     __shared__ StepSmem<LG> sm;
     // each role loads the log2 table with its first staging (one barrier)
     if (blockIdx.x == 0) {
         // the diagonal block is the step's critical path: let its waves issue
         // ahead of tile waves that share its SIMDs
         __builtin_amdgcn_s_setprio(3);
-        diag_role<LG, NL>(a, t, sm);
+        diag_role<LG, NL, MP, NB>(a, t, kp0, sm);
     } else {
         const int64_t x = (int64_t)blockIdx.x - 1;
         const int64_t wg = x % nx;
         const int32_t g = (int32_t)(x / nx);
         if (sp == 4)
-            tile_role<LG, NL, 4>(a, t, wg, g, sm);
+            tile_role<LG, NL, 4, MP>(a, t, nb, kp0, wg, g, sm);
         else if (sp == 2)
-            tile_role<LG, NL, 2>(a, t, wg, g, sm);
+            tile_role<LG, NL, 2, MP>(a, t, nb, kp0, wg, g, sm);
         else
-            tile_role<LG, NL, 1>(a, t, wg, g, sm);
+            tile_role<LG, NL, 1, MP>(a, t, nb, kp0, wg, g, sm);
     }
 }
 
@@ -609,14 +659,31 @@ hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
         if (g > 4096) g = 4096;
         k_sweep_fill<<<(unsigned)g, 256, 0, st>>>(a);
     }
-    for (int64_t t = 0; t < a.nblk; t++) {
-        const int64_t ntiles = (t >= 1 && ngroups > 0) ? a.nblk - t - 1 : 0;
+    // blocks kp0..t-1 are final and not yet added to the blocks after them;
+    // a step makes nb more final (two while the tiles keep at least
+    // ECASQ_SWEEP_PAIR_ABOVE wavefronts busy: half the launches and half the
+    // running-minima traffic, for a diagonal chain twice as long)
+    int64_t kp0 = 0;
+    for (int64_t t = 0; t < a.nblk;) {
+        const int64_t after1 = a.nblk - t - 1;
+        const int32_t nb = after1 * ngroups >= ECASQ_SWEEP_PAIR_ABOVE ? 2 : 1;
+        const int64_t ntiles = (kp0 < t && ngroups > 0) ? a.nblk - t - nb : 0;
         const int64_t tiles = ntiles * ngroups;
         const int32_t sp = tiles < ECASQ_SWEEP_SP4_BELOW ? 4 : tiles < ECASQ_SWEEP_SP2_BELOW ? 2 : 1;
         const int64_t per = kTileWaves / sp;  // column blocks per workgroup
         const int64_t nx = (ntiles + per - 1) / per;
-        k_sweep_step<LG, NL><<<(unsigned)(1 + nx * ngroups), kSB * kTileWaves, 0, st>>>(
-            a, t, sp, nx > 0 ? nx : 1);
+        const dim3 grid((unsigned)(1 + nx * ngroups)), block(kSB * kTileWaves);
+        const int64_t nxa = nx > 0 ? nx : 1;
+        // instantiations by (most final blocks to add, blocks made final):
+        // the paired steps, the step after them, and the single steps
+        if (nb == 2)
+            k_sweep_step<LG, NL, 2, 2><<<grid, block, 0, st>>>(a, t, kp0, sp, nxa);
+        else if (t - kp0 == 2)
+            k_sweep_step<LG, NL, 2, 1><<<grid, block, 0, st>>>(a, t, kp0, sp, nxa);
+        else
+            k_sweep_step<LG, NL, 1, 1><<<grid, block, 0, st>>>(a, t, kp0, sp, nxa);
+        kp0 = t;
+        t += nb;
     }
     return hipGetLastError();
 }

@@ -196,15 +196,18 @@ def _sample_cols(rng, lo, p, n):
     return np.array(sorted(c), dtype=np.int64)
 
 
-@pytest.mark.parametrize("workload,s,lam", [("weights_256k", 32, 0.1), ("student_t_1m", 64, 0.05)],
-                         ids=["weights_256k_s32", "student_t_1m_s64"])
+@pytest.mark.parametrize("workload,s,lam", [("weights_256k", 32, 0.1), ("student_t_1m", 64, 0.05),
+                                             ("weights_256k", 16, 0.1)],
+                         ids=["weights_256k_s32", "student_t_1m_s64", "weights_256k_s16"])
 def test_full_size_sweep_sampled(workload, s, lam):
     """Full-size inputs, DP schedule 1 (the column-block sweep) at one
     multiplier: every layer checked bit for bit at sampled columns against the
     oracle's recomputation from the GPU's previous layer.  At 2^18 also the
     recomputed argmins and the accumulators along them; at 2^20 (s = 64) the
     values the sweep keeps (recomputing every argmin there is a full
-    layer-by-layer solve)."""
+    layer-by-layer solve).  These sizes run the early steps that make two
+    diagonal blocks final per launch, with one (s = 16, 32) and two (s = 64)
+    layer groups."""
     x = inputs.make(workload, seed=0)
     full = x.size <= (1 << 18)
     _say("full-size sweep trace", workload, x.size, s, lam, "argmins" if full else "values")
