@@ -61,8 +61,8 @@ TRAFFIC_SOURCES_SHA = "f3a631b21f5b78fb"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
-SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 6.751e7
-SWEEP_TRAFFIC_SHA = "5e747c6953b5998d"
+SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 5.644e7
+SWEEP_TRAFFIC_SHA = "7be7fb4921e4e671"
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the (workload, s) both traffic figures were measured on; null for others
 TRAFFIC_WORKLOAD = ("weights_256k", 32)
@@ -82,6 +82,26 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+# steps from which k_sweep_step makes two diagonal blocks final per launch:
+# while at least this many (column block, layer group) tiles follow
+SWEEP_PAIR_ABOVE = 2048
+
+
+def sweep_launches(p, s):
+    """k_sweep_step launches of one sweep solve (the library's step schedule:
+    blocks of 64 columns, two per launch while the tiles that follow number
+    at least SWEEP_PAIR_ABOVE)."""
+    nblk = (p + 63) // 64
+    layers = min(s, p) - 2
+    lg = 8 if layers <= 8 else 16 if layers <= 16 else 32
+    groups = max(1, (layers + lg - 1) // lg)
+    t = n = 0
+    while t < nblk:
+        t += 2 if (nblk - t - 1) * groups >= SWEEP_PAIR_ABOVE else 1
+        n += 1
+    return n
+
+
 def sweep_roofline(p, s, ms, solves, cells, measured=True):
     """Roofline of DP schedule 1: all k_sweep_step launches of one solve timed
     as one unit.  Algorithmic ops per solve: 19 per (k, j) pair (its C, Phi
@@ -93,7 +113,7 @@ def sweep_roofline(p, s, ms, solves, cells, measured=True):
     ops = (OPS_PAIR + OPS_Q) * pairs + OPS_CELL * layer_cells + 20.0 * (p - 1)
     per_ms = ms / max(solves, 1)
     achieved = ops / (per_ms * 1e-3) / 1e12 if ms > 0 else 0.0
-    steps = (p + 63) // 64
+    steps = sweep_launches(p, s)
     return {
         "bound": "alu",
         "kernel": "k_sweep_step (fp64 VALU); one DP solve = %d launches" % steps,
