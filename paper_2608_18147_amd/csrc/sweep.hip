@@ -47,13 +47,13 @@ constexpr int kTileWaves = 4;  // wavefronts per workgroup
 #ifndef ECASQ_SWEEP_SP4_BELOW
 #define ECASQ_SWEEP_SP4_BELOW 1024
 #endif
+#ifndef ECASQ_SWEEP_SP2_BELOW
+#define ECASQ_SWEEP_SP2_BELOW 1536
+#endif
 // (column block, layer group) tiles from which a step makes two diagonal
 // blocks final (a launch's fixed cost is then shared by two blocks)
 #ifndef ECASQ_SWEEP_PAIR_ABOVE
 #define ECASQ_SWEEP_PAIR_ABOVE 2048
-#endif
-#ifndef ECASQ_SWEEP_SP2_BELOW
-#define ECASQ_SWEEP_SP2_BELOW 1536
 #endif
 // widest layer group (register arrays of that many layers per lane)
 #ifndef ECASQ_SWEEP_LG_MAX
@@ -61,7 +61,8 @@ constexpr int kTileWaves = 4;  // wavefronts per workgroup
 #endif
 // wavefronts per SIMD the step kernel's registers are sized for (0: the
 // compiler's choice).  4 (128 VGPRs) lets the early steps' ~4000 tile
-// wavefronts run in one round; it costs a few spilled registers.
+// wavefronts run in one round; it costs a few spilled registers outside the
+// predecessor loops.
 #ifndef ECASQ_SWEEP_WAVES
 #define ECASQ_SWEEP_WAVES 4
 #endif
@@ -120,7 +121,7 @@ __global__ __launch_bounds__(256) void k_sweep_fill(SweepArgs a) {
 template <int LG>
 struct StepSmem {
     double2 tab[kLog2Size];
-    double sv[kSB], sN[kSB], sS[kSB], sS2[kSB];  // predecessor block t-1
+    double sv[kSB], sN[kSB], sS[kSB], sS2[kSB];  // the staged predecessor block
     double sF[kSB][LG];                           // its F_{i-1} for one layer group
     double dv[kSB], dN[kSB], dS[kSB], dS2[kSB];   // block t (diagonal role)
     double pF[kSB];                               // previous layer of block t
