@@ -255,6 +255,52 @@ def optimal_rate(torch, ecasq, inputs, reps=3):
     return out
 
 
+# the paper's mean runtimes at its runtime setting (its CPU implementation,
+# BF16 inputs, d = 2^18, s = 64, lambda = 0.1): context, not a target
+PAPER_RUNTIME_S = {"approx": 0.26, "refined": 0.33, "optimal": 6.39}
+
+
+def paper_setting_rate(torch, ecasq, inputs, seeds=5):
+    """The paper's runtime setting: d = 2^18 vectors of its four synthetic
+    distributions (Normal, Lognormal, Student-t, sparse outliers) cast to
+    bf16, s = 64, lambda = 0.1, five seeds each.  Time of one whole solve
+    (sort, histogram, DP, recovery, metrics), without refinement, with five
+    refinement rounds, and of the optimal DP (monotone brackets); like the
+    paper, the mean of the four distributions' means."""
+    d, s, lam = 1 << 18, 64, 0.1
+    gens = (("normal", inputs.normal), ("lognormal", inputs.lognormal_signed),
+            ("student_t", inputs.student_t), ("sparse_outlier", inputs.sparse_outlier))
+    opts = {"approx": ecasq.ecasq_default_options(refine_rounds=0),
+            "refined": ecasq.ecasq_default_options(refine_rounds=5),
+            "optimal": ecasq.ecasq_default_options()}
+    per = {v: [] for v in opts}
+    ps = []
+    for _, gen in gens:
+        ms = {v: [] for v in opts}
+        for seed in range(seeds):
+            x = torch.from_numpy(gen(d, seed)).to(torch.bfloat16).to("cuda")
+            for v, o in opts.items():
+                run = ((lambda: ecasq.ecasq_solve_optimal(x, s, lam, options=o)) if v == "optimal"
+                       else (lambda: ecasq.ecasq_solve_lagrangian(x, s, lam, options=o)))
+                run()  # warm-up
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                info = run()[2]
+                torch.cuda.synchronize()
+                ms[v].append((time.perf_counter() - t0) * 1e3)
+            ps.append(info["p"])
+        for v in opts:
+            per[v].append(sum(ms[v]) / len(ms[v]))
+    out = {"workload": "normal, lognormal, student_t, sparse_outlier; d = 2^18 as bf16",
+           "s": s, "lambda": lam, "seeds": seeds, "p_range": [min(ps), max(ps)]}
+    for v in opts:
+        mean = sum(per[v]) / len(per[v])
+        out[v] = {"ms_per_solve": mean, "per_distribution_ms": per[v],
+                  "paper_cpu_s": PAPER_RUNTIME_S[v],
+                  "ratio_to_paper_cpu": PAPER_RUNTIME_S[v] * 1e3 / mean}
+    return out
+
+
 def coding_rate(torch, ecasq, sym, t, info, reps=5):
     """rANS coding of the final symbols: coded bits per entry (payload,
     16-bit frequency descriptors, segment table, and a 16-bit value per
@@ -316,7 +362,7 @@ def main():
                     help="only run the optimal-DP measurement and print it")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the side measurements (grids, optimal DP, refinement-aware\n"
-                         "search, entropy coding, batched rows)")
+                         "search, entropy coding, batched rows, the paper's runtime setting)")
     ap.add_argument("--no-alphabet", action="store_true",
                     help="skip the permissible-grid solves (uniform / quantile, 4096 points)")
     ap.add_argument("--dp-schedule", type=int, default=None, choices=(0, 1),
@@ -496,6 +542,8 @@ def main():
             r["speedup"] = out["ms_per_step"] / r["ms_per_solve_step"]
     if not args.no_optimal:
         out["optimal"] = optimal_rate(torch, ecasq, inputs)
+    if not args.no_extras:
+        out["paper_setting"] = paper_setting_rate(torch, ecasq, inputs)
     if not args.no_batched:
         out["batched"] = batched_rate(torch, ecasq, inputs)
     if not args.no_cpu_baseline:

@@ -50,6 +50,15 @@ def kv_rows(rows=4096, d=128, seed=0, outlier_rate=0.01, outlier=8.0):
     return x.astype(np.float16)
 
 
+def sparse_outlier(d, seed=0, rate=0.01, scale=8.0):
+    """Standard normal entries, a share `rate` of them replaced by +-scale."""
+    g = _rng(seed)
+    x = g.standard_normal(d)
+    hit = g.random(d) < rate
+    sign = g.choice(np.array([-1.0, 1.0]), size=d)
+    return np.where(hit, scale * sign, x).astype(np.float32)
+
+
 def weight_mixture(d=1 << 18, seed=0):
     g = _rng(seed)
     pick = g.random(d) < 0.9
