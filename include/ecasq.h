@@ -155,9 +155,12 @@ ecasq_status ecasq_solve(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
  *      it; the codebook is recovered by Hirschberg's method (recovery 0) or
  *      from stored argmins (recovery 1);
  *   1  one sweep over column blocks in which the interval cost and entropy
- *      term of each cell serve every layer; keeps F and the argmins of all
- *      layers (12 (s+1) d bytes) and takes the codebook from the argmin
- *      traceback of the solve it was found in (recovery is ignored). */
+ *      term of each cell serve every layer; keeps F of all layers and an
+ *      int32 table of the same shape (traceback scratch; every argmin only
+ *      when an inspection call asks for them): 12 (s+1) d bytes.  The
+ *      codebook comes from the argmin traceback of the solve it was found
+ *      in, each argmin recomputed from the kept layers (recovery is
+ *      ignored). */
 ecasq_status ecasq_solve_ex(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
                             double bits_per_entry, const ecasq_options *opts, void *stream,
                             double *codebook, int32_t *codebook_rank, ecasq_info *info,
