@@ -301,6 +301,37 @@ def paper_setting_rate(torch, ecasq, inputs, seeds=5):
     return out
 
 
+def rounding_rate(torch, ecasq, d=1 << 26, t=32, reps=5):
+    """The final stochastic rounding (k_quantize: 4 B in, 1 B out per entry)
+    and its time-shared form (k_quantize_ts: 4 B in, 1 + 1 B out) on 2^26
+    standard normal fp32 entries with t = 32 evenly spaced values over
+    [min, max] (alpha = 0.4 and a second codebook of 31 for the time-shared
+    form), timed with HIP events on the stream the library launches on,
+    against the 8 TB/s HBM peak."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0)
+    x = torch.randn(d, generator=g, device="cuda", dtype=torch.float32)
+    lo, hi = float(x.min()), float(x.max())
+    c0 = torch.linspace(lo, hi, t, dtype=torch.float64, device="cuda")
+    c1 = torch.linspace(lo, hi, t - 1, dtype=torch.float64, device="cuda")
+    out = {"d": d, "t": t}
+    for name, run, per in (
+            ("quantize", lambda: ecasq.ecasq_quantize(x, c0, 7), 5),
+            ("quantize_timeshare", lambda: ecasq.ecasq_quantize_timeshare(x, c0, c1, 0.4, 7), 6)):
+        run()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            run()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / reps
+        gbs = per * d / (ms * 1e-3) / 1e9
+        out[name] = {"ms": ms, "bytes_per_entry": per, "achieved_GBs": gbs, "frac_of_8TBs": gbs / 8000.0}
+    return out
+
+
 def coding_rate(torch, ecasq, sym, t, info, reps=5):
     """rANS coding of the final symbols: coded bits per entry (payload,
     16-bit frequency descriptors, segment table, and a 16-bit value per
@@ -362,7 +393,8 @@ def main():
                     help="only run the optimal-DP measurement and print it")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the side measurements (grids, optimal DP, refinement-aware\n"
-                         "search, entropy coding, batched rows, the paper's runtime setting)")
+                         "search, entropy coding, batched rows, the paper's runtime setting,\n"
+                         "the stochastic rounding at 2^26 entries)")
     ap.add_argument("--no-alphabet", action="store_true",
                     help="skip the permissible-grid solves (uniform / quantile, 4096 points)")
     ap.add_argument("--dp-schedule", type=int, default=None, choices=(0, 1),
@@ -544,6 +576,7 @@ def main():
         out["optimal"] = optimal_rate(torch, ecasq, inputs)
     if not args.no_extras:
         out["paper_setting"] = paper_setting_rate(torch, ecasq, inputs)
+        out["rounding"] = rounding_rate(torch, ecasq)
     if not args.no_batched:
         out["batched"] = batched_rate(torch, ecasq, inputs)
     if not args.no_cpu_baseline:
