@@ -62,7 +62,7 @@ KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
 SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 5.644e7
-SWEEP_TRAFFIC_SHA = "0da7f4789ccc6a28"
+SWEEP_TRAFFIC_SHA = "9e10ed7cd0226d9d"
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the (workload, s) both traffic figures were measured on; null for others
 TRAFFIC_WORKLOAD = ("weights_256k", 32)

@@ -11,8 +11,9 @@
 // bit for bit (same candidate arithmetic; the minimum of a set does not depend
 // on the order, up to the sign of an exact zero).
 //
-// The sweep keeps values only: a layer's update per cell is an add, an fma
-// and a min.  With every F_{i-1} kept, the argmin of any (i, j) is recomputed
+// The sweep keeps values only: a layer's update per cell is an add and a min
+// (the pair's cost Q = C - lambda' Phi is formed once for all layers).  With
+// every F_{i-1} kept, the argmin of any (i, j) is recomputed
 // when needed: the traceback of the chosen layer asks for one column per
 // layer (t columns of at most p candidates each, a few hundred microseconds,
 // against O(s p^2) for tracking the argmin of every cell), taking the lowest k
