@@ -44,7 +44,15 @@ namespace ecasq {
 
 namespace {
 
-constexpr int kOT = 256;   // threads per workgroup (4 wavefronts)
+constexpr int kOT = 256;   // threads per workgroup of the table kernels
+// wavefronts per row of the layer kernel: 4 for the full scan; 2 for the
+// monotone brackets (rows with few segments leave fewer of them idle, and
+// more rows share a CU)
+#ifndef ECASQ_OPT_ROW_WAVES
+#define ECASQ_OPT_ROW_WAVES 2
+#endif
+template <bool FULL>
+constexpr int row_waves() { return FULL ? 4 : ECASQ_OPT_ROW_WAVES; }
 constexpr int kSeg = 64;   // columns per segment (one wavefront)
 constexpr int kMaxSeg = (int)(kOptMaxP / kSeg) + 1;
 
@@ -182,7 +190,9 @@ __global__ __launch_bounds__(kOT) void k_opt_layer2(Hist H, double* __restrict__
 }
 
 template <bool FULL>
-__global__ __launch_bounds__(kOT) void k_opt_layer(OptLayerArgs a) {
+__global__ __launch_bounds__(row_waves<FULL>() * 64) void k_opt_layer(OptLayerArgs a) {
+    constexpr int kRW = row_waves<FULL>();
+    constexpr int kRT = kRW * 64;  // threads of the row's workgroup
     __shared__ double2 tab[kLog2Size];
     __shared__ int32_t kst[FULL ? 1 : kMaxSeg + 1];
     const int tid = threadIdx.x, lane = tid & (kSeg - 1), w = tid >> 6;
@@ -195,7 +205,7 @@ __global__ __launch_bounds__(kOT) void k_opt_layer(OptLayerArgs a) {
     const double* A = a.Dp + l * p;
     const double* Y = a.YU + l * p;
     if (FULL) {
-        for (int64_t j0 = l + 1; j0 < p; j0 += kOT) {
+        for (int64_t j0 = l + 1; j0 < p; j0 += kRT) {
             const int64_t j = j0 + tid;
             const bool ok = j < p;
             double C = 0.0, yu = 0.0, yd = 0.0;
@@ -221,7 +231,7 @@ __global__ __launch_bounds__(kOT) void k_opt_layer(OptLayerArgs a) {
     __syncthreads();
     for (S >>= 1; S >= 1; S >>= 1) {
         const int64_t nends = (nseg / S + 1) / 2;  // odd multiples of S up to nseg
-        for (int64_t m = w; m < nends; m += 4) {
+        for (int64_t m = w; m < nends; m += kRW) {
             const int64_t r = (2 * m + 1) * S;
             const int64_t kB = kst[r - S];
             const int64_t kA = r + S <= nseg ? (int64_t)kst[r + S] : klo;
@@ -248,7 +258,7 @@ __global__ __launch_bounds__(kOT) void k_opt_layer(OptLayerArgs a) {
     }
     // each segment's columns scan between the minimisers of its end and of
     // the previous segment's end
-    for (int64_t q = w; q < nseg; q += 4) {
+    for (int64_t q = w; q < nseg; q += kRW) {
         const int64_t k0 = kst[q + 1], k1 = kst[q];
         const int64_t j = l + 1 + kSeg * q + lane;
         const bool ok = j < p;
@@ -408,9 +418,9 @@ hipError_t launch_opt(const Hist& H, int32_t imax, int32_t exact_s, double lamp,
         }
         timing_begin(kTimingOpt, cells, st);
         if (full)
-            k_opt_layer<true><<<dim3(rows), dim3(kOT), 0, st>>>(a);
+            k_opt_layer<true><<<dim3(rows), dim3(row_waves<true>() * 64), 0, st>>>(a);
         else
-            k_opt_layer<false><<<dim3(rows), dim3(kOT), 0, st>>>(a);
+            k_opt_layer<false><<<dim3(rows), dim3(row_waves<false>() * 64), 0, st>>>(a);
         timing_end(st);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
