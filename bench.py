@@ -61,8 +61,8 @@ TRAFFIC_SOURCES_SHA = "f3a631b21f5b78fb"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
-SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 5.644e7
-SWEEP_TRAFFIC_SHA = "9e10ed7cd0226d9d"
+SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 5.649e7
+SWEEP_TRAFFIC_SHA = "51fc2b933e658483"
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the (workload, s) both traffic figures were measured on; null for others
 TRAFFIC_WORKLOAD = ("weights_256k", 32)

@@ -39,7 +39,7 @@ namespace {
 
 struct Layout {
     size_t v, N, S, S2, gv, gN, gS, gS2, F0, F1, M0, M1, P0, P1, pval, pidx, last, res, mres,
-        small, chain, kstar, prep, swF, swK, swchain;
+        small, chain, kstar, prep, swF, swQ, swK, swchain;
     int64_t pstride;  // partial entries per multiplier
     size_t total;
 };
@@ -83,6 +83,7 @@ Layout layout(int64_t d, int32_t s, int32_t flags) {
     L.pval = take(sizeof(double) * np);
     L.pidx = take(sizeof(int32_t) * np);
     L.swF = take(sweep ? sizeof(double) * (size_t)(s + 1) * (size_t)d : 0);
+    L.swQ = take(sweep ? sweep_cost_bytes() : 0);
     L.swK = take(sweep ? sizeof(int32_t) * (size_t)(s + 1) * (size_t)d : 0);
     L.swchain = take(sizeof(int32_t) * 528);  // chain, then the traceback state
     L.last = take(sizeof(double) * 3 * (size_t)(s + 1) * kMaxLambdas);
@@ -237,6 +238,7 @@ ecasq_status sweep_solve(Ctx& c, double lam, int32_t exact_s, Point& out, double
     SweepSolve S;
     S.H = c.H;
     S.F = c.at<double>(c.L.swF);
+    S.Q = c.at<double>(c.L.swQ);
     S.K = c.at<int32_t>(c.L.swK);
     S.st = c.at<int32_t>(c.L.swchain) + 256;
     S.ld = c.d;

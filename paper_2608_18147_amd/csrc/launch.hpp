@@ -134,6 +134,7 @@ hipError_t launch_split(const double* Fw, const double* Bw, int64_t ml, int64_t 
 struct SweepSolve {
     Hist H;
     double* F;
+    double* Q;     // sweep_cost_bytes(): the next diagonal block's costs
     int32_t* K;    // argmins on request (launch_sweep_argmins); traceback scratch
     int32_t* st;   // traceback state, 264 int32
     int64_t ld;    // >= p
@@ -141,6 +142,7 @@ struct SweepSolve {
     double lamp;   // lambda' in MSE units
 };
 size_t sweep_table_bytes(int64_t d, int32_t s);
+size_t sweep_cost_bytes();
 // The sweep, then eq. apx_final and the traceback (argmins recomputed along
 // the chain): out (device, 4 doubles) = J, MSE, H(I,B), i*; chain (device,
 // optional, >= i* int32): u_0 = 0 .. u_{i*-1} = p-1.

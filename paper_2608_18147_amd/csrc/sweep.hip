@@ -56,6 +56,10 @@ constexpr int kTileWaves = 4;  // wavefronts per workgroup
 #ifndef ECASQ_SWEEP_PAIR_ABOVE
 #define ECASQ_SWEEP_PAIR_ABOVE 2048
 #endif
+// form workgroup 0's costs one launch ahead in the late single-block steps
+#ifndef ECASQ_SWEEP_PREP_COSTS
+#define ECASQ_SWEEP_PREP_COSTS 1
+#endif
 // widest layer group (register arrays of that many layers per lane)
 #ifndef ECASQ_SWEEP_LG_MAX
 #define ECASQ_SWEEP_LG_MAX 32
@@ -78,9 +82,17 @@ constexpr int kTileWaves = 4;  // wavefronts per workgroup
 #define ECASQ_STEP_ATTR
 #endif
 
+// Costs Q = C - lambda' Phi of workgroup 0's predecessors, formed one launch
+// ahead in the late single-block steps (they do not depend on F): for block
+// b, at parity b & 1, QP[k][c] of predecessor 64 (b-1) + k and QD[k][c] of
+// predecessor 64 b + k (+inf unless 64 b + k < the column), against column
+// 64 b + c (the last column in place of columns past p - 1).
+constexpr int64_t kQTab = (int64_t)kSB * kSB;
+
 struct SweepArgs {
     Hist H;
     double* F;    // [I+1][ld]: rows 2..I; running minima until a block is final
+    double* Q;    // [2][2][64][64]: QP, QD of the next diagonal block
     int32_t* K;   // argmins recomputed for inspection (same layout), and scratch
     int64_t ld;
     int32_t I;    // last layer, min(s, p)
@@ -183,6 +195,44 @@ __device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int lofs, int
             best[l] = __builtin_fmin(best[l], sm.sF[kk + 1][lofs + l] + Q1);
         }
     }
+    }
+}
+
+// As accumulate, with the costs Q of predecessors kb..ke-1 (ke - kb even)
+// read from Qc[kk * 64] instead of formed here (same update order).
+template <int LG, int LW>
+__device__ __forceinline__ void accumulate_q(const StepSmem<LG>& sm, int kb, int ke,
+                                             const double* __restrict__ Qc, double (&best)[LW]) {
+    for (int kk = kb; kk < ke; kk += 2) {
+        const double Q0 = Qc[kk * kSB], Q1 = Qc[(kk + 1) * kSB];
+#pragma unroll
+        for (int l = 0; l < LW; l++) {
+            best[l] = __builtin_fmin(best[l], sm.sF[kk][l] + Q0);
+            best[l] = __builtin_fmin(best[l], sm.sF[kk + 1][l] + Q1);
+        }
+    }
+}
+
+// QP and QD of block b (see SweepArgs), the workgroup's threads taking the
+// entries in turn; the arguments of cell_terms are those of the tiles and of
+// workgroup 0, so the costs are the same bit for bit.
+__device__ void prep_costs(const SweepArgs& a, int64_t b, const double2* __restrict__ tab) {
+    const int64_t p = a.H.p;
+    double* QP = a.Q + (b & 1) * 2 * kQTab;
+    double* QD = QP + kQTab;
+    for (int e = threadIdx.x; e < 2 * kQTab; e += blockDim.x) {
+        const int which = e / (int)kQTab, k = (e / kSB) % kSB, c = e % kSB;
+        const int64_t j = b * kSB + c;
+        const int64_t jj = j < p ? j : p - 1;
+        const int64_t kg = (b - 1 + which) * kSB + k;
+        double q = __builtin_huge_val();
+        if (which == 0 || kg < jj) {
+            double C, P;
+            cell_terms(a.H.v[kg], a.H.N[kg], a.H.S[kg], a.H.S2[kg], a.H.v[jj], a.H.N[jj],
+                       a.H.S[jj], a.H.S2[jj], a.H.dd, false, 0.0, tab, C, P);
+            q = __builtin_fma(-a.lamp, P, C);
+        }
+        (which == 0 ? QP : QD)[k * kSB + c] = q;
     }
 }
 
@@ -290,7 +340,7 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int32_t nb, int64_t kp0
 // partial minima meet in LDS and the wavefront that holds the layer merges
 // them.  A block's final values are read back from F for the next block
 // after the workgroup barrier that orders them.
-template <int LG, int NL, int MP>
+template <int LG, int NL, int MP, bool PRE = false>
 __device__ void diag_block(const SweepArgs& a, int64_t t, int64_t kp0, StepSmem<LG>& sm) {
     constexpr int LW = LG / kTileWaves;
     constexpr int KW = kSB / kTileWaves;  // predecessors of a block per wavefront
@@ -336,7 +386,12 @@ __device__ void diag_block(const SweepArgs& a, int64_t t, int64_t kp0, StepSmem<
             double pa[NL];
 #pragma unroll
             for (int l = 0; l < NL; l++) pa[l] = __builtin_huge_val();
-            accumulate<LG, NL>(sm, 0, wave * KW, wave * KW + KW, cv, cN, cS, cS2, dd, lamp, pa);
+            if constexpr (PRE)  // block t-1's costs, formed by the last launch
+                accumulate_q<LG, NL>(sm, wave * KW, wave * KW + KW,
+                                     a.Q + (t & 1) * 2 * kQTab + lane, pa);
+            else
+                accumulate<LG, NL>(sm, 0, wave * KW, wave * KW + KW, cv, cN, cS, cS2, dd, lamp,
+                                   pa);
             __syncthreads();  // the staging buffer is free: 4 x LW rows of 64
             double (*xb)[kSB] = reinterpret_cast<double (*)[kSB]>(&sm.sF[0][0]);
 #pragma unroll
@@ -373,7 +428,9 @@ __device__ void diag_block(const SweepArgs& a, int64_t t, int64_t kp0, StepSmem<
         for (int q = 0; q < KW; q++) {
             const int kk = wave * KW + q;
             cQ[q] = __builtin_huge_val();
-            if (j0 + kk < jj) {
+            if constexpr (PRE) {
+                cQ[q] = a.Q[(t & 1) * 2 * kQTab + kQTab + kk * kSB + lane];
+            } else if (j0 + kk < jj) {
                 double C, P;
                 cell_terms(sm.dv[kk], sm.dN[kk], sm.dS[kk], sm.dS2[kk], cv, cN, cS, cS2, dd,
                            false, 0.0, sm.tab, C, P);
@@ -416,10 +473,10 @@ __device__ void diag_block(const SweepArgs& a, int64_t t, int64_t kp0, StepSmem<
     }
 }
 
-template <int LG, int NL, int MP, int NB>
+template <int LG, int NL, int MP, int NB, bool PRE>
 __device__ void diag_role(const SweepArgs& a, int64_t t, int64_t kp0, StepSmem<LG>& sm) {
     load_log2_table(sm.tab);
-    diag_block<LG, NL, MP>(a, t, kp0, sm);
+    diag_block<LG, NL, MP, PRE>(a, t, kp0, sm);
     if constexpr (NB == 2) {
         if (t + 1 < a.nblk) {
             __syncthreads();  // the first block's use of LDS is over
@@ -431,7 +488,9 @@ __device__ void diag_role(const SweepArgs& a, int64_t t, int64_t kp0, StepSmem<L
 // One step of the sweep: workgroup 0 makes blocks t..t+nb-1 final, the others
 // add predecessor blocks kp0..t-1 to the blocks after them (tile WG index =
 // g * nx + wg).
-template <int LG, int NL, int MP, int NB>
+// PRE: workgroup 0 reads block t's costs formed by the last launch; PREP:
+// the last workgroup forms block t+1's (single-block steps only).
+template <int LG, int NL, int MP, int NB, bool PRE = false, bool PREP = false>
 __global__ __launch_bounds__(kSB* kTileWaves) ECASQ_STEP_ATTR void k_sweep_step(
     SweepArgs a, int64_t t, int64_t kp0, int32_t sp, int64_t nx) {
     constexpr int32_t nb = NB;
@@ -441,7 +500,12 @@ __global__ __launch_bounds__(kSB* kTileWaves) ECASQ_STEP_ATTR void k_sweep_step(
         // the diagonal block is the step's critical path: let its waves issue
         // ahead of tile waves that share its SIMDs
         __builtin_amdgcn_s_setprio(3);
-        diag_role<LG, NL, MP, NB>(a, t, kp0, sm);
+        diag_role<LG, NL, MP, NB, PRE>(a, t, kp0, sm);
+    } else if (PREP && blockIdx.x == gridDim.x - 1) {
+        if (t + 1 >= a.nblk) return;
+        load_log2_table(sm.tab);
+        __syncthreads();
+        prep_costs(a, t + 1, sm.tab);
     } else {
         const int64_t x = (int64_t)blockIdx.x - 1;
         const int64_t wg = x % nx;
@@ -644,6 +708,7 @@ SweepArgs make_args(const SweepSolve& S) {
     SweepArgs a;
     a.H = S.H;
     a.F = S.F;
+    a.Q = S.Q;
     a.K = S.K;
     a.ld = S.ld;
     a.I = S.I;
@@ -666,6 +731,7 @@ hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
     // ECASQ_SWEEP_PAIR_ABOVE wavefronts busy: half the launches and half the
     // running-minima traffic, for a diagonal chain twice as long)
     int64_t kp0 = 0;
+    bool prepped = false;  // the last launch formed block t's costs
     for (int64_t t = 0; t < a.nblk;) {
         const int64_t after1 = a.nblk - t - 1;
         const int32_t nb = after1 * ngroups >= ECASQ_SWEEP_PAIR_ABOVE ? 2 : 1;
@@ -676,14 +742,23 @@ hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
         const int64_t nx = (ntiles + per - 1) / per;
         const dim3 grid((unsigned)(1 + nx * ngroups)), block(kSB * kTileWaves);
         const int64_t nxa = nx > 0 ? nx : 1;
+        // the late single-block steps (four wavefronts per tile, workgroup 0
+        // the longest part): one more workgroup forms the next block's costs
+        const bool late = ECASQ_SWEEP_PREP_COSTS && nb == 1 && t - kp0 <= 1 && sp == 4;
+        const dim3 gridp((unsigned)(2 + nx * ngroups));
         // instantiations by (most final blocks to add, blocks made final):
         // the paired steps, the step after them, and the single steps
         if (nb == 2)
             k_sweep_step<LG, NL, 2, 2><<<grid, block, 0, st>>>(a, t, kp0, sp, nxa);
         else if (t - kp0 == 2)
             k_sweep_step<LG, NL, 2, 1><<<grid, block, 0, st>>>(a, t, kp0, sp, nxa);
+        else if (late && prepped)
+            k_sweep_step<LG, NL, 1, 1, true, true><<<gridp, block, 0, st>>>(a, t, kp0, sp, nxa);
+        else if (late)
+            k_sweep_step<LG, NL, 1, 1, false, true><<<gridp, block, 0, st>>>(a, t, kp0, sp, nxa);
         else
             k_sweep_step<LG, NL, 1, 1><<<grid, block, 0, st>>>(a, t, kp0, sp, nxa);
+        prepped = late;
         kp0 = t;
         t += nb;
     }
@@ -697,7 +772,7 @@ size_t trace_scratch_bytes(int64_t p) {
 }
 
 bool sweep_ok(const SweepSolve& S) {
-    return S.I >= 2 && S.I <= 255 && S.H.p >= 2 && S.ld >= S.H.p && S.F && S.K && S.st &&
+    return S.I >= 2 && S.I <= 255 && S.H.p >= 2 && S.ld >= S.H.p && S.F && S.Q && S.K && S.st &&
            (size_t)S.ld * sizeof(int32_t) >= trace_scratch_bytes(S.H.p);
 }
 
@@ -707,6 +782,8 @@ size_t sweep_table_bytes(int64_t d, int32_t s) {
     // F (fp64) and K (int32: inspection and traceback scratch), rows 0..s
     return (size_t)(s + 1) * (size_t)d * (sizeof(double) + sizeof(int32_t));
 }
+
+size_t sweep_cost_bytes() { return 4 * (size_t)kQTab * sizeof(double); }
 
 hipError_t launch_sweep(const SweepSolve& S, int32_t exact_s, double* out, int32_t* chain,
                         hipStream_t st) {
