@@ -503,8 +503,90 @@ static double refine_local(const hist_t *H, int32_t t, const int32_t *u, int32_t
     return fma(lamp, Hl, Cl + Cr);
 }
 
-/* Refines u in place.  Returns the number of rounds run.  In budget mode a
- * colour substep whose result has H(Xhat) > b is undone. */
+/* Exported for the tests that pin it: the local objective of mover r at m. */
+double orc_refine_local(const double *v, const double *N, const double *S, const double *S2,
+                        int64_t p, int64_t d, int32_t t, const int32_t *u, int32_t r, int64_t m,
+                        double lamp)
+{
+    hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
+    return refine_local(&H, t, u, r, m, lamp);
+}
+
+/* The position a mover r (1 <= r <= t-2) searches out in the open range
+ * (u_{r-1}, u_{r+1}) (Sec. 6): the lowest minimiser of the local objective
+ * (exhaustive), or the paper's binary search, which keeps the half whose
+ * forward difference points downhill: lo = L+1, hi = R-1; while lo < hi,
+ * mid = lo + (hi-lo)/2 and lo = mid+1 if L_r(mid+1) < L_r(mid), else hi = mid.
+ * Returns u_r itself when the range holds only u_r. */
+static int64_t refine_search(const hist_t *H, int32_t t, const int32_t *u, int32_t r,
+                             double lamp, int32_t exhaustive)
+{
+    int64_t L = u[r - 1], R = u[r + 1];
+    if (R - L < 3) return u[r];
+    if (exhaustive) {
+        double bv = INFINITY;
+        int64_t m = -1;
+        for (int64_t x = L + 1; x < R; x++) {
+            double val = refine_local(H, t, u, r, x, lamp);
+            if (val < bv) { bv = val; m = x; }
+        }
+        return m;
+    }
+    int64_t lo = L + 1, hi = R - 1;
+    while (lo < hi) {
+        int64_t mid = lo + (hi - lo) / 2;
+        if (refine_local(H, t, u, r, mid + 1, lamp) < refine_local(H, t, u, r, mid, lamp))
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+int64_t orc_refine_search(const double *v, const double *N, const double *S, const double *S2,
+                          int64_t p, int64_t d, int32_t t, const int32_t *u, int32_t r,
+                          double lamp, int32_t exhaustive)
+{
+    hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
+    return refine_search(&H, t, u, r, lamp, exhaustive);
+}
+
+/* One colour substep (Sec. 6): every mover r = c (mod 3), 1 <= r <= t-2,
+ * searched against the chain u as it stands; a mover whose found position
+ * strictly lowers its local objective moves there.  The new chain goes to nu
+ * (u itself is not changed); returns the number of movers that moved.  Movers
+ * of one colour are three apart, so the frequencies each of them changes
+ * (its own and its two neighbours') are disjoint. */
+static int32_t refine_substep(const hist_t *H, int32_t t, const int32_t *u, int32_t c,
+                              double lamp, int32_t exhaustive, int32_t *nu)
+{
+    int32_t moved = 0;
+    memcpy(nu, u, sizeof(int32_t) * t);
+    for (int32_t r = 1; r <= t - 2; r++) {
+        if (r % 3 != c) continue;
+        int64_t m = refine_search(H, t, u, r, lamp, exhaustive);
+        if (m != u[r] &&
+            refine_local(H, t, u, r, m, lamp) < refine_local(H, t, u, r, u[r], lamp)) {
+            nu[r] = (int32_t)m;
+            moved++;
+        }
+    }
+    return moved;
+}
+
+int32_t orc_refine_substep(const double *v, const double *N, const double *S, const double *S2,
+                           int64_t p, int64_t d, int32_t t, const int32_t *u, int32_t c,
+                           double lamp, int32_t exhaustive, int32_t *nu)
+{
+    hist_t H = {v, N, S, S2, p, (double)d, N[0], N[0] / (double)d, S2[p - 1]};
+    if (t < 3) { memcpy(nu, u, sizeof(int32_t) * t); return 0; }
+    return refine_substep(&H, t, u, c, lamp, exhaustive, nu);
+}
+
+/* Refines u in place: rounds of the substeps of colours 0, 1, 2 (Sec. 6),
+ * stopping after a round in which nothing moved or after `rounds` rounds.
+ * In budget mode a substep whose result has H(Xhat) > b is undone.  Returns
+ * the number of rounds run. */
 int orc_refine(const double *v, const double *N, const double *S, const double *S2, int64_t p,
                int64_t d, int32_t t, int32_t *u, double lamp, double b, int32_t budget_mode,
                int32_t rounds, int32_t exhaustive, int32_t *moves_out)
@@ -516,38 +598,7 @@ int orc_refine(const double *v, const double *N, const double *S, const double *
     for (int32_t rd = 0; rd < rounds; rd++) {
         int any = 0;
         for (int32_t c = 0; c < 3; c++) {
-            memcpy(nu, u, sizeof(int32_t) * t);
-            int moved = 0;
-            for (int32_t r = 1; r <= t - 2; r++) {
-                if (r % 3 != c) continue;
-                int64_t L = u[r - 1], R = u[r + 1];
-                if (R - L < 3) continue; /* the open range holds u_r only */
-                int64_t m;
-                if (exhaustive) {
-                    double bv = INFINITY;
-                    m = -1;
-                    for (int64_t x = L + 1; x < R; x++) {
-                        double val = refine_local(&H, t, u, r, x, lamp);
-                        if (val < bv) { bv = val; m = x; }
-                    }
-                } else {
-                    int64_t lo = L + 1, hi = R - 1;
-                    while (lo < hi) {
-                        int64_t mid = lo + (hi - lo) / 2;
-                        if (refine_local(&H, t, u, r, mid + 1, lamp) <
-                            refine_local(&H, t, u, r, mid, lamp))
-                            lo = mid + 1;
-                        else
-                            hi = mid;
-                    }
-                    m = lo;
-                }
-                if (m != u[r] &&
-                    refine_local(&H, t, u, r, m, lamp) < refine_local(&H, t, u, r, u[r], lamp)) {
-                    nu[r] = (int32_t)m;
-                    moved++;
-                }
-            }
+            int32_t moved = refine_substep(&H, t, u, c, lamp, exhaustive, nu);
             if (moved && budget_mode && chain_hout(&H, t, nu) > b)
                 moved = 0;
             if (moved) {

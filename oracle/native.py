@@ -58,6 +58,12 @@ def lib():
     L.orc_chain_metrics.argtypes = hist + [i32, ip, d, dp]
     L.orc_opt_dp.argtypes = hist + [i32, i32, d, ip, dp, ip, dp]
     L.orc_refine.argtypes = hist + [i32, ip, d, d, i32, i32, i32, ip]
+    L.orc_refine_local.argtypes = hist + [i32, ip, i32, i64, d]
+    L.orc_refine_local.restype = d
+    L.orc_refine_search.argtypes = hist + [i32, ip, i32, d, i32]
+    L.orc_refine_search.restype = i64
+    L.orc_refine_substep.argtypes = hist + [i32, ip, i32, d, i32, ip]
+    L.orc_refine_substep.restype = i32
     L.orc_search.argtypes = hist + [i32, d, i32, i32, i32, i32, i32, i32, i32, dp, ip, i32, dp,
                                     i32, dp]
     L.orc_interval.argtypes = hist + [i64, i64, dp]

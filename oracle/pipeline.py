@@ -217,6 +217,28 @@ def refine(H, chain, lamp, b=math.inf, budget=False, rounds=5, exhaustive=False)
     return u, int(n), int(moves.value)
 
 
+def refine_local(H, chain, r, m, lamp):
+    """Local objective of mover r placed at unique index m (Sec. 6)."""
+    u = np.ascontiguousarray(chain, dtype=np.int32)
+    return native.lib().orc_refine_local(*H.args(), len(u), native.iptr(u), r, m, lamp)
+
+
+def refine_search(H, chain, r, lamp, exhaustive=False):
+    """The position mover r's search finds (before the strict-improvement test)."""
+    u = np.ascontiguousarray(chain, dtype=np.int32)
+    return int(native.lib().orc_refine_search(*H.args(), len(u), native.iptr(u), r, lamp,
+                                              int(exhaustive)))
+
+
+def refine_substep(H, chain, colour, lamp, exhaustive=False):
+    """One colour substep without the budget guard: (new chain, movers moved)."""
+    u = np.ascontiguousarray(chain, dtype=np.int32)
+    nu = np.zeros_like(u)
+    n = native.lib().orc_refine_substep(*H.args(), len(u), native.iptr(u), colour, lamp,
+                                        int(exhaustive), native.iptr(nu))
+    return nu, int(n)
+
+
 class LambdaCache:
     """Points (lambda, H(I,B), vNMSE, t) solved on one input, shared by the
     searches for several budgets."""

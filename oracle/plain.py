@@ -261,3 +261,118 @@ def optimal_dp(x, s, lam):
         j, l, i = l, k, i - 1
     idx = sorted(set(idx))
     return J / nx, tuple(vf[k] for k in idx)
+
+
+# --------------------------------------------------------------------------
+# Three-colour refinement (Sec. 6) on the plain objective.
+
+
+def _interval_mse(xs, lo, hi):
+    """Sum over the entries in (lo, hi] of (hi - x)(x - lo), exact."""
+    return sum((hi - xv) * (xv - lo) for xv in xs if lo < xv <= hi)
+
+
+def refine_local(x, Q, r, lam_p):
+    """What moving q_r (0 < r < t-1) changes in MSE + lam' H(Xhat), per entry:
+    the MSE of the entries in (q_{r-1}, q_{r+1}] plus lam' times h(f/d) of the
+    three values whose expected frequencies depend on q_r (q_{r-1}, q_r,
+    q_{r+1}), with f from the per-entry rounding probabilities (Sec. 3).
+    lam' is in MSE units.  Exact (a Fraction) when lam' = 0."""
+    xs = _hist(x)
+    Qs, f = freqs(x, Q)
+    d = len(xs)
+    m = _interval_mse(xs, Qs[r - 1], Qs[r]) + _interval_mse(xs, Qs[r], Qs[r + 1])
+    if lam_p == 0:
+        return m
+    return float(m) + lam_p * ((h(f[r - 1] / d) + h(f[r] / d)) + h(f[r + 1] / d))
+
+
+class NearTie(Exception):
+    """A decision of the plain refinement fell within rounding of a tie."""
+
+
+def _less(a, b, tol):
+    """a < b, raising NearTie when the two are within tol of each other but
+    not exactly equal Fractions (then rounding could decide either way)."""
+    if isinstance(a, Fraction) and isinstance(b, Fraction):
+        return a < b
+    if abs(a - b) <= tol:
+        raise NearTie()
+    return a < b
+
+
+def refine_search(x, v, chain, r, lam_p, exhaustive=False, tol=0.0):
+    """The position (a unique index) mover r's search finds in the open range
+    (u_{r-1}, u_{r+1}) (Sec. 6): the lowest minimiser of refine_local
+    (exhaustive), or the binary search on the sign of its forward difference
+    (lo = L+1, hi = R-1; while lo < hi: mid = lo + (hi-lo)//2, lo = mid+1 if
+    L(mid+1) < L(mid), else hi = mid)."""
+    L, R = chain[r - 1], chain[r + 1]
+    if R - L < 3:
+        return chain[r]
+
+    def val(m):
+        Q = [v[k] for k in chain]
+        Q[r] = v[m]
+        return refine_local(x, Q, r, lam_p)
+
+    if exhaustive:
+        best, bm = None, None
+        for m in range(L + 1, R):
+            cur = val(m)
+            if best is None or _less(cur, best, tol):
+                best, bm = cur, m
+        return bm
+    lo, hi = L + 1, R - 1
+    while lo < hi:
+        mid = lo + (hi - lo) // 2
+        if _less(val(mid + 1), val(mid), tol):
+            lo = mid + 1
+        else:
+            hi = mid
+    return lo
+
+
+def refine(x, v, chain, lam_p, b=math.inf, budget=False, rounds=5, exhaustive=False, tol=0.0):
+    """Sec. 6 on the plain objective: rounds of the colour substeps c = 0, 1, 2;
+    in a substep every mover r = c (mod 3), 1 <= r <= t-2, searched against
+    the chain as it stands, moves to the found position if that strictly lowers
+    refine_local; with the budget guard the substep is undone if the new
+    codebook's H(Xhat) exceeds b.  Stops after a round without a move or after
+    `rounds` rounds.  Returns (chain, rounds run); raises NearTie when a
+    decision is within tol of a tie (or the guard within tol of b)."""
+    u = list(int(a) for a in chain)
+    t = len(u)
+    nrun = 0
+    if t < 3:
+        return u, 0
+    for _ in range(rounds):
+        any_move = False
+        for c in range(3):
+            nu = list(u)
+            moved = 0
+            for r in range(1, t - 1):
+                if r % 3 != c:
+                    continue
+                m = refine_search(x, v, u, r, lam_p, exhaustive, tol)
+                if m == u[r]:
+                    continue
+                Qm = [v[k] for k in u]
+                Qm[r] = v[m]
+                Q0 = [v[k] for k in u]
+                if _less(refine_local(x, Qm, r, lam_p), refine_local(x, Q0, r, lam_p), tol):
+                    nu[r] = m
+                    moved += 1
+            if moved and budget:
+                Hn = entropy_out(x, [v[k] for k in nu])
+                if abs(Hn - b) <= 1e-12:
+                    raise NearTie()
+                if Hn > b:
+                    moved = 0
+            if moved:
+                u = nu
+                any_move = True
+        nrun += 1
+        if not any_move:
+            break
+    return u, nrun
