@@ -306,6 +306,24 @@ ecasq_status ecasq_quantize(const void *x, ecasq_dtype dt, int64_t d, const doub
                             double *empirical_entropy, int64_t *hist);
 
 /*
+ * ecasq_quantize for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same arguments, outputs and errors as ecasq_quantize, bit for bit the
+ * same symbols, counts and entropy, but the symbol counts live in a
+ * file-scope device array of 256 64-bit counters (2 KB per device, held
+ * until the process ends) instead of memory allocated per call; no
+ * hipMalloc, hipFree or memset node is issued (the counts are cleared by a
+ * kernel).  t above 256 is rejected with ECASQ_EINVAL.  Every call on one
+ * device shares that array: calls that overlap on one device (other streams,
+ * other threads) race and must be serialised by the caller.  Returns once
+ * the work is enqueued.
+ */
+ecasq_status ecasq_quantize_noalloc(const void *x, ecasq_dtype dt, int64_t d,
+                                    const double *codebook, int32_t t, uint64_t seed,
+                                    void *stream, uint8_t *symbols, double *empirical_entropy,
+                                    int64_t *hist);
+
+/*
  * Many independent short vectors in one launch (one wavefront per row, several
  * rows per workgroup): x is n rows of d entries, row-major.  Each row is
  * solved as ecasq_solve_ex would with opts->recovery = 1 and

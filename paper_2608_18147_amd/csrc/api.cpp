@@ -1300,6 +1300,21 @@ ecasq_status ecasq_quantize(const void* x, ecasq_dtype dt, int64_t d, const doub
     return rc;
 }
 
+ecasq_status ecasq_quantize_noalloc(const void* x, ecasq_dtype dt, int64_t d,
+                                    const double* codebook, int32_t t, uint64_t seed,
+                                    void* stream, uint8_t* symbols, double* empirical_entropy,
+                                    int64_t* hist) {
+    ECASQ_TRY(check_x(x, dt, d));
+    if (!codebook || t < 1 || t > 256 || !symbols || !empirical_entropy) return ECASQ_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    unsigned long long* hh = nullptr;
+    HIP_TRY(quantize_scratch(&hh));
+    HIP_TRY(launch_zero_counts(hh, t, st));
+    HIP_TRY(launch_quantize(x, dt, d, codebook, t, seed, symbols, hh, st));
+    HIP_TRY(launch_entropy(hh, t, d, empirical_entropy, hist, st));
+    return ECASQ_OK;
+}
+
 ecasq_status ecasq_histogram(const void* x, ecasq_dtype dt, int64_t d, void* stream, double* v,
                              double* N, double* S, double* S2, int64_t* p_out) {
     ECASQ_TRY(check_x(x, dt, d));

@@ -165,6 +165,11 @@ hipError_t launch_gather(const double* v, const int32_t* u, int32_t t, double* c
 hipError_t launch_quantize(const void* x, int dt, int64_t d, const double* codebook, int32_t t,
                            uint64_t seed, uint8_t* symbols, unsigned long long* hist,
                            hipStream_t st);
+// the allocation-free rounding's counts: a file-scope device array of 256
+// entries, its address on the current device (looked up once per device)
+hipError_t quantize_scratch(unsigned long long** out);
+// h[0..n) := 0 by a kernel (no memset node, so the call can be captured)
+hipError_t launch_zero_counts(unsigned long long* h, int32_t n, hipStream_t st);
 hipError_t launch_entropy(const unsigned long long* hist, int32_t t, int64_t d, double* ent,
                           int64_t* hist_out, hipStream_t st);
 // time-shared rounding with two codebooks (t0, t1 <= 256) and the entropy of

@@ -3,6 +3,8 @@
 // a plug-in entropy of the symbol histogram.
 #include <hip/hip_fp16.h>
 
+#include <mutex>
+
 #include "chain.hpp"
 #include "device.hpp"
 #include "launch.hpp"
@@ -327,7 +329,45 @@ __global__ void k_entropy(const unsigned long long* __restrict__ hist, int32_t t
     *ent = H;
 }
 
+// Symbol counts of the allocation-free rounding entry point: one array per
+// device, alive until the process ends, shared by every such call on that
+// device (calls that overlap on one device race on it).
+static __device__ __align__(256) unsigned long long scratch[kMaxT];
+
+__global__ void k_zero_counts(unsigned long long* __restrict__ h, int32_t n) {
+    for (int32_t r = threadIdx.x; r < n; r += blockDim.x) h[r] = 0ull;
+}
+
 }  // namespace
+
+// Device address of `scratch` on the current device, looked up once per
+// device (the host-side name is not a device address).
+hipError_t quantize_scratch(unsigned long long** out) {
+    constexpr int kMaxDev = 64;
+    static std::mutex mu;
+    static unsigned long long* ptr[kMaxDev] = {};
+    static hipError_t err[kMaxDev] = {};
+    static bool done[kMaxDev] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDev) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!done[dev]) {
+        void* p = nullptr;
+        err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        ptr[dev] = static_cast<unsigned long long*>(p);
+        done[dev] = true;
+    }
+    if (err[dev] != hipSuccess) return err[dev];
+    *out = ptr[dev];
+    return hipSuccess;
+}
+
+hipError_t launch_zero_counts(unsigned long long* h, int32_t n, hipStream_t st) {
+    k_zero_counts<<<1, 256, 0, st>>>(h, n);
+    return hipGetLastError();
+}
 
 hipError_t launch_refine(const Hist& H, int32_t t, int32_t* u, double lamp, double b,
                          int32_t budget, int32_t rounds, int32_t exhaustive, int32_t* stats,

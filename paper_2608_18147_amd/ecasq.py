@@ -77,7 +77,7 @@ EXPORTS = (
     "ecasq_histogram", "ecasq_dp_trace", "ecasq_timing_enable", "ecasq_timing_read",
     "ecasq_solve_budgets", "ecasq_solve_optimal", "ecasq_opt_trace",
     "ecasq_solve_timeshare", "ecasq_quantize_timeshare", "ecasq_encode_bound", "ecasq_encode",
-    "ecasq_decode",
+    "ecasq_decode", "ecasq_quantize_noalloc",
 )
 
 
@@ -102,6 +102,7 @@ def lib():
     L.ecasq_solve_budgets.argtypes = [vp, i32, i64, i32, i32, P(dbl), P(ecasq_options), vp, vp,
                                       vp, P(ecasq_info)]
     L.ecasq_quantize.argtypes = [vp, i32, i64, vp, i32, ctypes.c_uint64, vp, vp, vp, vp]
+    L.ecasq_quantize_noalloc.argtypes = [vp, i32, i64, vp, i32, ctypes.c_uint64, vp, vp, vp, vp]
     L.ecasq_solve_optimal.argtypes = [vp, i32, i64, i32, dbl, P(ecasq_options), vp, vp, vp,
                                       P(ecasq_info)]
     L.ecasq_opt_trace.argtypes = [vp, i32, i64, i32, dbl, P(ecasq_options), vp, i64, vp, vp,
@@ -131,7 +132,7 @@ def lib():
                  "ecasq_solve_batched", "ecasq_histogram", "ecasq_dp_trace",
                  "ecasq_solve_budgets", "ecasq_solve_optimal", "ecasq_opt_trace",
                  "ecasq_solve_timeshare", "ecasq_quantize_timeshare", "ecasq_encode",
-                 "ecasq_decode"):
+                 "ecasq_decode", "ecasq_quantize_noalloc"):
         getattr(L, name).restype = i32
     _lib = L
     return L
@@ -350,6 +351,23 @@ def ecasq_quantize(x, codebook, seed, stream=None):
                               _ptr(sym), _ptr(ent), _ptr(hist))
     _raise(st)
     return sym, ent, hist
+
+
+def ecasq_quantize_noalloc(x, codebook, seed, symbols, entropy, hist=None, stream=None):
+    """ecasq_quantize into caller-provided outputs, with no allocation inside
+    the library: symbols uint8 [d], entropy 0-d fp64, hist int64 [t] or None
+    (all on x's device).  codebook must be a contiguous fp64 tensor there."""
+    x = _check_x(x)
+    if (codebook.dtype != torch.float64 or not codebook.is_contiguous()
+            or codebook.device != x.device):
+        raise TypeError("codebook must be a contiguous fp64 tensor on x's device")
+    t = codebook.numel()
+    st = lib().ecasq_quantize_noalloc(_ptr(x), _DTYPES[x.dtype], x.numel(), _ptr(codebook), t,
+                                      ctypes.c_uint64(int(seed) & (2 ** 64 - 1)),
+                                      _stream(stream), _ptr(symbols), _ptr(entropy),
+                                      _ptr(hist) if hist is not None else None)
+    _raise(st)
+    return symbols, entropy, hist
 
 
 def ecasq_solve_batched(x, s, bits_per_entry, options=None, stream=None):
