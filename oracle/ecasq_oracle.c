@@ -91,6 +91,60 @@ static double log2c(double y)
 
 double orc_log2c(double y) { return log2c(y); }
 
+/* Canonical base-2 exponential (Tang 1989, table-driven).  y = k/64 + r with
+ * k = RN(64 y) (64 y is exact) and r = (64 y - k) / 64, exact, |r| <= 1/128;
+ * 2^y = 2^floor(k/64) * T[k mod 64] * 2^r with T[i] = RN(2^(i/64)) and
+ * 2^r - 1 = r * (C1 + C2 r + C3 r^2 + C4 r^3 + C5 r^4), C_k = RN(ln(2)^k / k!)
+ * (the Taylor series of e^(r ln 2), truncation below 2^-60 here).  About one
+ * ulp for |y| < 1000; NaN stays NaN, y <= -1100 gives 0, y >= 1100 gives +inf. */
+static double g_exp2t[64];
+static double g_exp2k[5];
+
+void orc_set_exp2_table(const double *t, const double *c)
+{
+    memcpy(g_exp2t, t, sizeof g_exp2t);
+    memcpy(g_exp2k, c, sizeof g_exp2k);
+}
+
+static double exp2c(double y)
+{
+    if (y != y) return y;
+    if (!(y > -1100.0)) return 0.0;
+    if (!(y < 1100.0)) return INFINITY;
+    double y64 = y * 64.0;
+    double kd = rint(y64);
+    double r = (y64 - kd) * 0x1p-6;
+    int64_t k = (int64_t)kd;
+    int32_t i = (int32_t)(k & 63);
+    int32_t e = (int32_t)((k - i) / 64);
+    double q = g_exp2k[4];
+    q = fma(q, r, g_exp2k[3]);
+    q = fma(q, r, g_exp2k[2]);
+    q = fma(q, r, g_exp2k[1]);
+    q = fma(q, r, g_exp2k[0]);
+    double pm1 = q * r;
+    double m = fma(g_exp2t[i], pm1, g_exp2t[i]);
+    return ldexp(m, e);
+}
+
+double orc_exp2c(double y) { return exp2c(y); }
+
+/* The width-1 search's aimed multiplier (see orc_search): the slope at H = b
+ * of the curve through A and B on which log vNMSE is linear in H, in base 2:
+ *   r2 = (log2 M_B - log2 M_A) / (H_B - H_A),  M_b = M_A 2^(r2 (b - H_A)),
+ *   lq = -(r2 ln 2) M_b. */
+static double aim_query(double b, double HA, double MA, double HB, double MB)
+{
+    double r2 = (log2c(MB) - log2c(MA)) / (HB - HA);
+    double mb = MA * exp2c(r2 * (b - HA));
+    return -(r2 * 0x1.62e42fefa39efp-1) * mb;
+}
+
+double orc_aim_query(double b, double HA, double MA, double HB, double MB)
+{
+    return aim_query(b, HA, MA, HB, MB);
+}
+
 /* h(y) = -y log2 y for y > 0, 0 otherwise (Sec. 4, definition of h). */
 static double hfun(double y)
 {
@@ -633,8 +687,8 @@ int orc_refine(const double *v, const double *N, const double *S, const double *
  *     two-value codebook);
  *     width 1 with aim != 0 queries, instead of lc, the slope at H = b of the
  *     curve through A and B on which log(vNMSE) is linear in H:
- *       rho = (log M_B - log M_A) / (H_B - H_A),  M_b = M_A exp(rho (b - H_A)),
- *       lq = -rho M_b,
+ *       r2 = (log2 M_B - log2 M_A) / (H_B - H_A),  M_b = M_A 2^(r2 (b - H_A)),
+ *       lq = -(r2 ln 2) M_b   (canonical log2c and exp2c, ln 2 rounded),
  *     when it lies strictly between la and lb and the previous such query found
  *     a new point; otherwise it queries lc;
  *   stop when the answer at lc is A or B again (H and M bit for bit): no DP
@@ -652,6 +706,11 @@ int orc_refine(const double *v, const double *N, const double *S, const double *
  * solves are appended (up to cap).  Searches for several budgets on one input
  * share their solves this way.
  * traj (optional, 4 doubles per solve): lambda, H(I,B), vNMSE, t.
+ * replay (optional, nreplay points of 4 doubles as traj): instead of solving,
+ * the n-th solve the search asks for takes the n-th replay point, whose
+ * lambda must equal the query bit for bit; the search then returns -2 at the
+ * first query that differs or runs past the list (a recorded trajectory is
+ * checked against the decisions this search takes on its points).
  * out: lambda_B, H_B, M_B, t_B, solves, cells, status (0 ok, -3 infeasible),
  *      lambda_final, passes
  */
@@ -707,7 +766,7 @@ int orc_search(const double *v, const double *N, const double *S, const double *
                int64_t d, int32_t s, double b, int32_t exact_s, int32_t max_passes, int32_t width,
                int32_t aim, int32_t dp_kind, int32_t refine_rounds, int32_t refine_exhaustive,
                double *cache, int32_t *ncache, int32_t cache_cap, double *traj,
-               int32_t traj_cap, double *out)
+               int32_t traj_cap, const double *replay, int32_t nreplay, double *out)
 {
     if (width != 1 && width != SEARCH_M) return -1;
     if (dp_kind != 0 && width != 1) return -1;
@@ -754,21 +813,30 @@ int orc_search(const double *v, const double *N, const double *S, const double *
         int hit_ = 0;                                                                         \
         for (int x_ = 0; x_ < npts; x_++) if (pts[x_].lam == l_) { hit_ = 1; break; }          \
         if (!hit_) {                                                                          \
-            if (dp_kind == 1)                                                                 \
-                opt_point(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, r);                    \
-            else if (dp_kind == 2)                                                            \
-                refined_point(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, refine_rounds,     \
-                              refine_exhaustive, r);                                          \
-            else                                                                              \
-                orc_dp_forward(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, r, NULL, NULL, NULL); \
+            double M_;                                                                        \
+            if (replay) {                                                                     \
+                if (nsol >= nreplay || replay[4 * nsol] != l_) goto replay_mismatch;          \
+                r[2] = replay[4 * nsol + 1]; M_ = replay[4 * nsol + 2];                       \
+                r[3] = replay[4 * nsol + 3]; r[4] = 0;                                        \
+            } else {                                                                          \
+                if (dp_kind == 1)                                                             \
+                    opt_point(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, r);                \
+                else if (dp_kind == 2)                                                        \
+                    refined_point(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, refine_rounds, \
+                                  refine_exhaustive, r);                                      \
+                else                                                                          \
+                    orc_dp_forward(v, N, S, S2, p, d, s, exact_s, l_ * H.s2tot, r, NULL, NULL, \
+                                   NULL);                                                     \
+                M_ = r[1] / H.s2tot;                                                          \
+            }                                                                                 \
             if (npts < MAX_PTS) {                                                             \
-                pts[npts].lam = l_; pts[npts].H = r[2]; pts[npts].M = r[1] / H.s2tot;        \
+                pts[npts].lam = l_; pts[npts].H = r[2]; pts[npts].M = M_;                     \
                 pts[npts].t = (int32_t)r[3]; npts++;                                           \
             }                                                                                 \
             cells += r[4];                                                                    \
             if (traj && nsol < traj_cap) {                                                    \
                 traj[4 * nsol] = l_; traj[4 * nsol + 1] = r[2];                               \
-                traj[4 * nsol + 2] = r[1] / H.s2tot; traj[4 * nsol + 3] = r[3];               \
+                traj[4 * nsol + 2] = M_; traj[4 * nsol + 3] = r[3];                           \
             }                                                                                 \
             nsol++;                                                                           \
         }                                                                                     \
@@ -844,9 +912,7 @@ int orc_search(const double *v, const double *N, const double *S, const double *
            points; the chord query certifies the end */
         int model = 0;
         if (width == 1 && aim && !force_chord && A.M > 0.0 && B.M > 0.0) {
-            double rho = (log(B.M) - log(A.M)) / (B.H - A.H);
-            double mb = A.M * exp(rho * (b - A.H));
-            double lq = -rho * mb;
+            double lq = aim_query(b, A.H, A.M, B.H, B.M);
             if (isfinite(lq) && lq > A.lam && lq < B.lam) {
                 q[0] = lq;
                 model = 1;
@@ -901,6 +967,10 @@ int orc_search(const double *v, const double *N, const double *S, const double *
     out[11] = have_A ? A.M : NAN; out[12] = have_A ? (double)A.t : NAN;
     free(pts);
     return 0;
+replay_mismatch:
+    out[4] = nsol;
+    free(pts);
+    return -2;
 }
 
 /* ------------------------------------------------------------------------- */

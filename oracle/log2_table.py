@@ -57,3 +57,25 @@ def build_table():
         invc.append(ic)
         lc.append(_round_checked(-mpmath.log(mpmath.mpf(ic), 2)))
     return invc, lc
+
+
+# --------------------------------------------------------------------------
+# Canonical base-2 exponential (used by the budget search's aimed query).
+#
+# exp2c(y) splits y = k/64 + r with k = RN(64 y) and |r| <= 1/128, and forms
+# 2^(k/64) = 2^floor(k/64) * T[k mod 64] with T[i] = RN(2^(i/64)) and
+# 2^r - 1 = r (C1 + C2 r + ... + C5 r^4) with C_k = RN(ln(2)^k / k!) (Tang
+# 1989, table-driven exp).  Both tables here come from mpmath; the GPU library
+# derives its copy with exact integer arithmetic.
+
+EXP2_TABLE_SIZE = 64
+
+
+def build_exp2_table():
+    """Return (T, C): T[i] = RN(2^(i/64)) for i < 64 and C = [C1..C5]."""
+    mpmath.mp.prec = 256
+    T = [_round_checked(mpmath.power(2, mpmath.mpf(i) / EXP2_TABLE_SIZE))
+         for i in range(EXP2_TABLE_SIZE)]
+    ln2 = mpmath.log(2)
+    C = [_round_checked(ln2 ** k / mpmath.factorial(k)) for k in range(1, 6)]
+    return T, C

@@ -65,7 +65,12 @@ def lib():
     L.orc_refine_substep.argtypes = hist + [i32, ip, i32, d, i32, ip]
     L.orc_refine_substep.restype = i32
     L.orc_search.argtypes = hist + [i32, d, i32, i32, i32, i32, i32, i32, i32, dp, ip, i32, dp,
-                                    i32, dp]
+                                    i32, dp, i32, dp]
+    L.orc_exp2c.argtypes = [d]
+    L.orc_exp2c.restype = d
+    L.orc_aim_query.argtypes = [d, d, d, d, d]
+    L.orc_aim_query.restype = d
+    L.orc_set_exp2_table.argtypes = [dp, dp]
     L.orc_interval.argtypes = hist + [i64, i64, dp]
     L.orc_dp_columns.argtypes = hist + [i32, d, dp, dp, dp, i64, i64p, dp, ip, dp, dp]
     L.orc_dp_columns.restype = None
@@ -73,6 +78,11 @@ def lib():
     a = np.asarray(invc, dtype=np.float64)
     b = np.asarray(lc, dtype=np.float64)
     L.orc_set_log2_table(a.ctypes.data_as(dp), b.ctypes.data_as(dp))
+    et, ec = log2_table.build_exp2_table()
+    ea = np.asarray(et, dtype=np.float64)
+    eb = np.asarray(ec, dtype=np.float64)
+    L.orc_set_exp2_table(ea.ctypes.data_as(dp), eb.ctypes.data_as(dp))
+    L._tables = (a, b, ea, eb)
     _lib = L
     return L
 

@@ -239,6 +239,10 @@ def refine_substep(H, chain, colour, lamp, exhaustive=False):
     return nu, int(n)
 
 
+class ReplayMismatch(AssertionError):
+    """The search's queries differ from a recorded trajectory."""
+
+
 class LambdaCache:
     """Points (lambda, H(I,B), vNMSE, t) solved on one input, shared by the
     searches for several budgets."""
@@ -250,7 +254,7 @@ class LambdaCache:
 
 
 def search(H, s, b, exact_s=False, max_passes=32, width=8, cache=None, aim=True, dp="approx",
-           refine_rounds=5, exhaustive=False):
+           refine_rounds=5, exhaustive=False, replay=None):
     """Budget search on lambda in passes of `width` (8 or 1) multipliers; with
     a LambdaCache, points solved by earlier searches are reused.  aim: width-1
     queries aimed at H = b before the certifying chord query (the batched row
@@ -260,7 +264,12 @@ def search(H, s, b, exact_s=False, max_passes=32, width=8, cache=None, aim=True,
     of the approximate DP's codebooks after refinement at their multiplier
     (width 1; the answer is the feasible point of lowest vNMSE found).  Also
     returns A, the infeasible point the final chord starts from (lamA etc.
-    NaN when there is none)."""
+    NaN when there is none).
+
+    replay: a recorded trajectory (rows lambda, H, vNMSE, t) whose points
+    stand in for the solves, in order; raises ReplayMismatch when the search
+    asks for a multiplier other than the next recorded one, or for more
+    solves than were recorded."""
     out = np.zeros(13)
     cap = 1024
     traj = np.zeros(4 * cap)
@@ -269,9 +278,15 @@ def search(H, s, b, exact_s=False, max_passes=32, width=8, cache=None, aim=True,
     else:
         cptr, nptr, ccap = None, None, 0
     kind = {"approx": 0, "optimal": 1, "refined": 2}[dp]
+    rp, nrp = None, 0
+    if replay is not None:
+        rep = np.ascontiguousarray(np.asarray(replay, dtype=np.float64).reshape(-1, 4))
+        rp, nrp = native.dptr(rep), len(rep)
     rc = native.lib().orc_search(*H.args(), s, b, int(exact_s), max_passes, width, int(aim),
                                  kind, refine_rounds, int(exhaustive), cptr, nptr, ccap,
-                                 native.dptr(traj), cap, native.dptr(out))
+                                 native.dptr(traj), cap, rp, nrp, native.dptr(out))
+    if rc == -2:
+        raise ReplayMismatch(f"query {int(out[4])} differs from the recorded trajectory")
     if rc != 0:
         raise ValueError("search width must be 1 or 8")
     n = int(out[4])
