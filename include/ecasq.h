@@ -10,9 +10,16 @@
  * H(Xhat) <= b.  The library solves the Lagrangian surrogate of Sec. 5
  * (vNMSE + lambda * H(I,B), dp_APX, eq. apx_base / apx_rec / apx_final)
  * exactly, searches lambda for the budget (Sec. 3 and Sec. 5), recovers the
- * codebook with Hirschberg's method in O(d) space (Sec. 5), refines it with
- * the three-colour pass of Sec. 6, and rounds the input stochastically
- * (Sec. 2) with Philox4x32-10.
+ * codebook, refines it with the three-colour pass of Sec. 6, and rounds the
+ * input stochastically (Sec. 2) with Philox4x32-10.
+ *
+ * By default (ecasq_options.dp_schedule = 1) each DP solve is one sweep over
+ * column blocks that keeps F of every layer, O(s d) memory (12 (s+1) d bytes),
+ * and the codebook is the argmin traceback of the solve it was found in;
+ * `recovery` is then ignored.  The layer-by-layer schedule (dp_schedule = 0)
+ * keeps two O(d) layers, as Sec. 5 states the method, and recovers the
+ * codebook with Hirschberg's method in O(d) space (recovery = 0) or from
+ * stored argmins (recovery = 1).
  *
  * Conventions for every entry point:
  *   - Array arguments named x, codebook*, symbols, hist, t_out, infos_dev and
@@ -21,8 +28,14 @@
  *     caller memory.
  *   - stream is a hipStream_t passed as void* (NULL = the null stream).  All
  *     device work is ordered on it.  The solve entry points block the calling
- *     thread until their results are in device memory, because the budget
- *     search and the recovery read small results back between steps.
+ *     thread until their results are in device memory.  The budget search
+ *     runs on the device: a one-thread controller kernel picks each next
+ *     multiplier and the DP solves read it from device memory, so under the
+ *     default settings the host reads back only the number of distinct values
+ *     before the search, a done flag between solves and the result at the
+ *     end.  Hirschberg recovery (dp_schedule 0), width-8 passes and the
+ *     optimal / refinement-aware search points (dp_objective 1, 2) still read
+ *     small results back between steps.
  *   - Argument errors are reported before any work is enqueued.  Data errors
  *     (NaN or Inf in x) are detected on the device and returned as
  *     ECASQ_ENONFINITE.
@@ -60,7 +73,9 @@ typedef struct {
     int32_t refine_exhaustive; /* 0: binary search of Sec. 6 (default); 1: full scan */
     int32_t exact_s;           /* 0: at most s values (default); 1: exactly min(s, p) */
     int32_t max_search_passes; /* lambda-search passes (default 32) */
-    int32_t recovery;          /* 0: Hirschberg, O(d) space (default); 1: stored argmins */
+    int32_t recovery;          /* dp_schedule 0 only: 0 Hirschberg, O(d) space (default);
+                                  1 stored argmins.  Ignored by the default sweep
+                                  (dp_schedule 1), which traces its argmins back */
     int32_t search_width;      /* multipliers per search pass: 1 (default) or 8 */
     int32_t dp_schedule;       /* 1: column-block sweep over all layers at once, O(s d)
                                   space (default); 0: layer by layer, O(d) space (see
@@ -123,9 +138,11 @@ void ecasq_default_options(ecasq_options *opts);
  *   w = 8, by A + (B - A) g / 8 for g = 1..7 (lc times 1/4, 1/2, 3/4, 3/2, 2,
  *   3, 4 when B is the two-value codebook);
  *   with w = 1 the pass queries, instead of lc, the slope at H = b of the
- *   curve through A and B on which log(vNMSE) is linear in H, while it lies
- *   strictly between the two multipliers and such queries keep finding new
- *   points;
+ *   curve through A and B on which log(vNMSE) is linear in H,
+ *   lq = -(r2 ln 2) M_A 2^(r2 (b - H_A)) with r2 = (log2 M_B - log2 M_A) /
+ *   (H_B - H_A) (a table-driven log2 and exp2, so that the query is the same
+ *   bit for bit wherever it is computed), while it lies strictly between the
+ *   two multipliers and such queries keep finding new points;
  *   the search ends when the solve at lc returns A or B again, or after
  *   max_search_passes passes.
  * The codebook is B, recovered at the multiplier it was found at; the

@@ -15,7 +15,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libecasq.so")
 SOURCES = ["prep.hip", "alphabet.hip", "dp.hip", "sweep.hip", "opt.hip", "post.hip",
-           "rans.hip", "batched.hip", "api.cpp"]
+           "rans.hip", "batched.hip", "search.hip", "api.cpp"]
 ARCH = os.environ.get("ECASQ_OFFLOAD_ARCH", "gfx950")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -34,11 +34,12 @@ EXTRA_FLAGS = {"sweep.hip": ["-fno-honor-nans"], "batched.hip": ["-fno-honor-nan
 
 
 def _table():
-    out = os.path.join(CSRC, "log2_table.inc")
-    with open(out + ".tmp", "w") as fh:
-        subprocess.run([sys.executable, os.path.join(CSRC, "gen_log2_table.py")], check=True,
-                       stdout=fh)
-    os.replace(out + ".tmp", out)
+    for name in ("log2", "exp2"):
+        out = os.path.join(CSRC, f"{name}_table.inc")
+        with open(out + ".tmp", "w") as fh:
+            subprocess.run([sys.executable, os.path.join(CSRC, f"gen_{name}_table.py")],
+                           check=True, stdout=fh)
+        os.replace(out + ".tmp", out)
 
 
 def _compile(src):

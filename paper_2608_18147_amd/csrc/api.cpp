@@ -15,6 +15,7 @@
 #include <chrono>
 #include <cmath>
 #include <cstdio>
+#include <cstddef>
 #include <cstring>
 #include <vector>
 
@@ -39,7 +40,7 @@ namespace {
 
 struct Layout {
     size_t v, N, S, S2, gv, gN, gS, gS2, F0, F1, M0, M1, P0, P1, pval, pidx, last, res, mres,
-        small, chain, kstar, prep, swF, swQ, swK, swchain;
+        small, chain, kstar, prep, swF, swQ, swK, swchain, sstate, schains, two, cres, cchain;
     int64_t pstride;  // partial entries per multiplier
     size_t total;
 };
@@ -94,12 +95,19 @@ Layout layout(int64_t d, int32_t s, int32_t flags) {
     L.kstar = (flags & kWsArgmins) && !sweep ? take(sizeof(int32_t) * (size_t)(s + 1) * (size_t)d)
                                               : 0;
     L.prep = take(prep_scratch_bytes(d));
+    // the budget search's state, its points' codebooks and commit inputs
+    L.sstate = take(sizeof(SearchState));
+    L.schains = take(sizeof(int32_t) * (size_t)kSearchMaxPts * (size_t)s);
+    L.two = take(sizeof(double) * 8);
+    L.cres = take(sizeof(double) * 4 * kMaxLambdas);
+    L.cchain = take(sizeof(int32_t) * (size_t)(s + 8));
     L.total = o;
     return L;
 }
 
 struct Point {
     double lam, H, M;
+    double mse = 0.0;  // MSE of the point's codebook (points the host scores)
     int32_t t;
     std::vector<int32_t> chain;  // the solve's codebook (sweep schedule only)
 };
@@ -122,6 +130,8 @@ struct Ctx {
     int32_t objective = 0;
     int32_t opt_full = 0;   // optimal DP: scan every predecessor
     int32_t refine_rounds = 0, refine_exhaustive = 0, recovery = 0;
+    SearchPeek* poll = nullptr;  // pinned host memory (device-resident search)
+    hipEvent_t ev[2] = {nullptr, nullptr};
 
     template <class T>
     T* at(size_t off) const {
@@ -157,6 +167,12 @@ ecasq_status ctx_open(Ctx& c, int64_t d, int32_t s, int32_t flags, void* stream,
 }
 
 void ctx_close(Ctx& c) {
+    if (c.poll || c.ev[0] || c.ev[1]) (void)hipStreamSynchronize(c.st);
+    for (auto& e : c.ev)
+        if (e) (void)hipEventDestroy(e);
+    if (c.poll) (void)hipHostFree(c.poll);
+    c.poll = nullptr;
+    c.ev[0] = c.ev[1] = nullptr;
     if (c.own && c.base) {
         (void)hipFreeAsync(c.base, c.st);
         (void)hipStreamSynchronize(c.st);
@@ -229,12 +245,7 @@ int64_t dp_cells(int64_t p, int32_t imax) {
     return n;
 }
 
-// One dp_APX solve at lam by the column-block sweep: the result, the chain of
-// its codebook, and optionally the tables as dumps (row m of a pass).
-ecasq_status sweep_solve(Ctx& c, double lam, int32_t exact_s, Point& out, double* J4,
-                         const Dumps* dump, int32_t m) {
-    const int64_t p = c.p;
-    const int32_t imax = (int32_t)std::min<int64_t>(c.s, p);
+SweepSolve sweep_args(const Ctx& c) {
     SweepSolve S;
     S.H = c.H;
     S.F = c.at<double>(c.L.swF);
@@ -242,7 +253,31 @@ ecasq_status sweep_solve(Ctx& c, double lam, int32_t exact_s, Point& out, double
     S.K = c.at<int32_t>(c.L.swK);
     S.st = c.at<int32_t>(c.L.swchain) + 256;
     S.ld = c.d;
-    S.I = imax;
+    S.I = (int32_t)std::min<int64_t>(c.s, c.p);
+    S.lamp = 0.0;
+    return S;
+}
+
+// Enqueue one dp_APX solve by the sweep whose lambda' and run flag the
+// kernels read from device memory (the device-resident search); the result
+// (J, MSE, H(I,B), t) goes to the res slot and the codebook to the chain slot.
+ecasq_status sweep_enqueue(Ctx& c, const double* lampp, const int32_t* runp, int32_t exact_s) {
+    SweepSolve S = sweep_args(c);
+    S.lampp = lampp;
+    S.runp = runp;
+    timing_begin(2, dp_cells(c.p, S.I), c.st);
+    HIP_TRY(launch_sweep(S, exact_s, c.at<double>(c.L.res), c.at<int32_t>(c.L.swchain), c.st));
+    timing_end(c.st);
+    return ECASQ_OK;
+}
+
+// One dp_APX solve at lam by the column-block sweep: the result, the chain of
+// its codebook, and optionally the tables as dumps (row m of a pass).
+ecasq_status sweep_solve(Ctx& c, double lam, int32_t exact_s, Point& out, double* J4,
+                         const Dumps* dump, int32_t m) {
+    const int64_t p = c.p;
+    const int32_t imax = (int32_t)std::min<int64_t>(c.s, p);
+    SweepSolve S = sweep_args(c);
     S.lamp = lam * c.s2tot;
     double* res = c.at<double>(c.L.res);
     int32_t* ch = c.at<int32_t>(c.L.swchain);
@@ -465,6 +500,7 @@ ecasq_status opt_point(Ctx& c, double lam, int32_t exact_s, Point& out) {
     out.lam = lam;
     out.H = m[2];
     out.M = m[0] / c.s2tot;
+    out.mse = m[0];
     out.t = (int32_t)chain.size();
     out.chain = chain;
     if (timing_verbose())
@@ -502,6 +538,7 @@ ecasq_status refined_point(Ctx& c, double lam, int32_t exact_s, Point& out) {
     out.lam = lam;
     out.H = m[2];
     out.M = m[0] / c.s2tot;
+    out.mse = m[0];
     out.t = t;
     out.chain = chain;
     return ECASQ_OK;
@@ -519,35 +556,134 @@ struct SearchResult {
     ecasq_status status;
 };
 
-// The budget search on lambda in passes of kMaxLambdas multipliers (the
-// schedule is stated in include/ecasq.h).  A point's lambda is that of its
-// first query; among points of equal lambda the first one wins.
-// Solve the multipliers of one pass that no point of `pts` already has (the
-// first occurrence of a repeated multiplier counts), appending the new points
-// to pts in query order; returns how many were solved.  Under the layer
-// schedule a partial pass of 2..7 is padded to 8 with repeats of its last
-// multiplier, and the padding is not counted.
-ecasq_status eval_pass(Ctx& c, const double* q, int32_t n, int32_t exact_s,
-                       std::vector<Point>& pts, int32_t& solved) {
-    double todo[kMaxLambdas];
-    int32_t m = 0;
-    for (int32_t g = 0; g < n; g++) {
-        bool seen = false;
-        for (const Point& x : pts)
-            if (x.lam == q[g]) seen = true;
-        for (int32_t h = 0; h < m; h++)
-            if (todo[h] == q[g]) seen = true;
-        if (!seen) todo[m++] = q[g];
+// Per-context host resources of the device-resident search: a pinned poll
+// block and two events (created on first use, released by ctx_close).
+ecasq_status search_host_init(Ctx& c) {
+    if (c.poll) return ECASQ_OK;
+    void* h = nullptr;
+    HIP_TRY(hipHostMalloc(&h, 2 * sizeof(SearchPeek), hipHostMallocDefault));
+    c.poll = static_cast<SearchPeek*>(h);
+    for (auto& e : c.ev) HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    return ECASQ_OK;
+}
+
+// The search state's fields before its point list, read back in one copy.
+ecasq_status read_state(Ctx& c, SearchState& h) {
+    SearchState* S = c.at<SearchState>(c.L.sstate);
+    HIP_TRY(hipMemcpyAsync(&h, S, offsetof(SearchState, pts), hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    return ECASQ_OK;
+}
+
+Point to_point(const SearchPt& q) {
+    Point P;
+    P.lam = q.lam;
+    P.H = q.H;
+    P.M = q.M;
+    P.t = q.t;
+    return P;
+}
+
+ecasq_status point_chain(Ctx& c, int32_t at, Point& P) {
+    P.chain.assign(P.t, 0);
+    HIP_TRY(hipMemcpyAsync(P.chain.data(), c.at<int32_t>(c.L.schains) + (int64_t)at * c.s,
+                           sizeof(int32_t) * P.t, hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    return ECASQ_OK;
+}
+
+void print_point(int32_t n, const SearchPt& q) {
+    std::fprintf(stderr, "[ecasq] solve %d: lambda=%.6g H=%.6f vNMSE=%.6g t=%d\n", n, q.lam, q.H,
+                 q.M, q.t);
+    std::fflush(stderr);
+}
+
+// The default configuration (dp_APX by the sweep, one multiplier per pass):
+// every solve reads lambda' and a run flag from the search state and is
+// followed by the commit kernel, so the host reads back nothing but the done
+// flag.  For short solves (fewer than kAheadBlocks column blocks) the host
+// keeps one solve queued ahead and polls the done flag of the one before it,
+// so solves run back to back; when the search ends, the queued solve and its
+// commit find run = 0 and return at once.  Long solves are polled one by one
+// (the poll costs nothing next to them, a skipped solve's launches would).
+constexpr int64_t kAheadBlocks = 1024;
+
+ecasq_status search_device_loop(Ctx& c, int32_t exact_s, int32_t max_passes) {
+    ECASQ_TRY(search_host_init(c));
+    SearchState* S = c.at<SearchState>(c.L.sstate);
+    double* res = c.at<double>(c.L.res);
+    int32_t* ch = c.at<int32_t>(c.L.swchain);
+    int32_t* pch = c.at<int32_t>(c.L.schains);
+    // the search may end without a solve (every query cached)
+    HIP_TRY(hipMemcpyAsync(c.poll, &S->peek, sizeof(SearchPeek), hipMemcpyDeviceToHost, c.st));
+    HIP_TRY(hipStreamSynchronize(c.st));
+    if (c.poll[0].done) return ECASQ_OK;
+    const int32_t limit = 2 * max_passes + 8;  // each solve adds a point to a finite search
+    const int32_t ahead = (c.p + 63) / 64 < kAheadBlocks ? 1 : 0;
+    int32_t n = 0;
+    for (;;) {
+        ECASQ_TRY(sweep_enqueue(c, &S->todo_lamp[0], &S->run, exact_s));
+        HIP_TRY(launch_search_commit(S, res, ch, 1, pch, 1, c.st));
+        HIP_TRY(hipMemcpyAsync(c.poll + (n & 1), &S->peek, sizeof(SearchPeek),
+                               hipMemcpyDeviceToHost, c.st));
+        HIP_TRY(hipEventRecord(c.ev[n & 1], c.st));
+        n++;
+        if (n > ahead) {
+            // the solve `ahead` places back and its commit
+            const int32_t k = (n - 1 - ahead) & 1;
+            HIP_TRY(hipEventSynchronize(c.ev[k]));
+            const SearchPeek& pk = c.poll[k];
+            if (timing_verbose()) print_point(pk.nsol, pk.last);
+            if (pk.done) break;  // a queued solve finds run = 0
+        }
+        if (n > limit) return ECASQ_EHIP;
     }
-    solved = m;
-    if (m == 0) return ECASQ_OK;
+    HIP_TRY(hipStreamSynchronize(c.st));
+    if (ahead) timing_discard_last();  // the skipped solve
+    timing_flush();
+    return ECASQ_OK;
+}
+
+// One pass's solves driven from the host (the other configurations): the
+// state's todo list is read back, each multiplier solved as its kind says,
+// and the points committed on the device in query order.
+ecasq_status search_host_pass(Ctx& c, const SearchState& h, int32_t exact_s) {
+    SearchState* S = c.at<SearchState>(c.L.sstate);
+    int32_t* pch = c.at<int32_t>(c.L.schains);
+    double* cres = c.at<double>(c.L.cres);
+    int32_t* cch = c.at<int32_t>(c.L.cchain);
+    const int32_t m = h.ntodo;
+    if (c.objective != 0) {
+        for (int32_t g = 0; g < m; g++) {
+            Point P;
+            if (c.objective == 1)
+                ECASQ_TRY(opt_point(c, h.todo[g], exact_s, P));
+            else
+                ECASQ_TRY(refined_point(c, h.todo[g], exact_s, P));
+            const double r[4] = {0.0, P.mse, P.H, (double)P.t};
+            HIP_TRY(hipMemcpyAsync(cres, r, sizeof r, hipMemcpyHostToDevice, c.st));
+            HIP_TRY(hipMemcpyAsync(cch, P.chain.data(), sizeof(int32_t) * P.t,
+                                   hipMemcpyHostToDevice, c.st));
+            HIP_TRY(launch_search_commit(S, cres, cch, 1, pch, 0, c.st));
+        }
+        return ECASQ_OK;
+    }
+    if (c.sweep) {
+        for (int32_t g = 0; g < m; g++) {
+            Point P;
+            ECASQ_TRY(sweep_solve(c, h.todo[g], exact_s, P, nullptr, nullptr, 0));
+            HIP_TRY(launch_search_commit(S, c.at<double>(c.L.res), c.at<int32_t>(c.L.swchain), 1,
+                                         pch, 0, c.st));
+        }
+        return ECASQ_OK;
+    }
+    // layer by layer: one multiplier, or a pass of kMaxLambdas (padded with
+    // repeats of the last, which are not counted)
+    double todo[kMaxLambdas];
+    for (int32_t g = 0; g < m; g++) todo[g] = h.todo[g];
     Point out[kMaxLambdas];
-    if (c.objective == 1) {
-        for (int32_t g = 0; g < m; g++) ECASQ_TRY(opt_point(c, todo[g], exact_s, out[g]));
-    } else if (c.objective == 2) {
-        for (int32_t g = 0; g < m; g++) ECASQ_TRY(refined_point(c, todo[g], exact_s, out[g]));
-    } else if (c.sweep || m == 1) {
-        for (int32_t g = 0; g < m; g++) ECASQ_TRY(dp_solve(c, todo + g, 1, exact_s, out + g, nullptr, nullptr));
+    if (m == 1) {
+        ECASQ_TRY(dp_solve(c, todo, 1, exact_s, out, nullptr, nullptr));
     } else {
         for (int32_t g = m; g < kMaxLambdas; g++) todo[g] = todo[m - 1];
         const int64_t cells0 = c.cells;
@@ -556,141 +692,66 @@ ecasq_status eval_pass(Ctx& c, const double* q, int32_t n, int32_t exact_s,
         c.cells = cells0 + (c.cells - cells0) / kMaxLambdas * m;
         c.solves = solves0 + m;
     }
-    pts.insert(pts.end(), out, out + m);
+    HIP_TRY(launch_search_commit(S, c.at<double>(c.L.res), nullptr, m, pch, 0, c.st));
     return ECASQ_OK;
 }
 
-const Point* point_at(const std::vector<Point>& pts, double lam) {
-    for (const Point& x : pts)
-        if (x.lam == lam) return &x;
-    return nullptr;
-}
-
-// cache (optional): points solved by earlier searches on the same input; they
-// join the point set from the start, and this search's new points are added.
+// The budget search on lambda (the schedule is stated in include/ecasq.h),
+// run by the device state machine of search.hip.  keep: start from the points
+// earlier searches on this input solved (a budget sweep), reusing any of
+// their multipliers the search queries again.
 ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32_t width,
-                    SearchResult& R, std::vector<Point>* cache = nullptr) {
-    static const double kGrid[kMaxLambdas] = {0.0, 1e-4, 1e-3, 1e-2, 1e-1, 1.0, 10.0, 100.0};
-    static const double kMul[kMaxLambdas - 1] = {0.25, 0.5, 0.75, 1.5, 2.0, 3.0, 4.0};
+                    SearchResult& R, bool keep = false) {
     if (width != 1 && width != kMaxLambdas) return ECASQ_EINVAL;
     if (c.objective != 0) width = 1;
-    std::vector<Point> pts;
-    if (cache) pts = *cache;
-    const size_t ncached = pts.size();
-    int32_t solved = 0;
-    ECASQ_TRY(eval_pass(c, kGrid, width, exact_s, pts, solved));
-    int32_t npass = solved > 0 ? 1 : 0;
-    R.status = ECASQ_OK;
-    R.lam_final = 0.0;
-    Point A, B;
-    Point two;
-    bool have_two = false, have_A = false;
-    bool force_chord = false;
-    for (;;) {
-        int ia = -1, ib = -1;
-        for (int x = 0; x < (int)pts.size(); x++) {
-            if (pts[x].H > b) {
-                if (ia < 0 || pts[x].lam > pts[ia].lam) ia = x;
-            } else {
-                if (ib < 0 || pts[x].lam < pts[ib].lam) ib = x;
-            }
-        }
-        if (ia < 0) {  // lambda = 0 is feasible
-            B = pts[ib];
-            have_A = false;
-            R.lam_final = B.lam;
-            break;
-        }
-        A = pts[ia];
-        have_A = true;
-        bool closed = false;
-        if (ib >= 0) {
-            B = pts[ib];
-        } else if (b >= 1.0) {
-            if (!have_two) {
-                // closed form of the two-value codebook {v_0, v_{p-1}}
-                int32_t ends[2] = {0, (int32_t)(c.p - 1)};
-                int32_t* ch = c.at<int32_t>(c.L.chain);
-                double* mres = c.at<double>(c.L.mres);
-                HIP_TRY(hipMemcpyAsync(ch, ends, sizeof ends, hipMemcpyHostToDevice, c.st));
-                HIP_TRY(launch_metrics(c.H, 2, ch, 0.0, c.s2tot, mres, c.st));
-                double m[6];
-                HIP_TRY(hipMemcpyAsync(m, mres, sizeof m, hipMemcpyDeviceToHost, c.st));
-                HIP_TRY(hipStreamSynchronize(c.st));
-                two.lam = HUGE_VAL;
-                two.H = c.objective != 0 ? m[2] : m[3];
-                two.M = (0.0 + m[0]) / c.s2tot;
-                two.t = 2;
-                have_two = true;
-            }
-            B = two;
-            closed = true;
-        } else {
-            // no feasible point yet: try the largest multiplier once
-            bool tried = false;
-            for (const Point& x : pts)
-                if (x.lam == 0x1p40) tried = true;
-            if (tried || npass >= max_passes) {
-                // infeasible budget: the lowest-entropy point found
-                int ih = 0;
-                for (int x = 1; x < (int)pts.size(); x++)
-                    if (pts[x].H < pts[ih].H) ih = x;
-                B = pts[ih];
-                have_A = false;
-                R.status = ECASQ_EINFEASIBLE;
-                R.lam_final = B.lam;
-                break;
-            }
-            const double big = 0x1p40;
-            ECASQ_TRY(eval_pass(c, &big, 1, exact_s, pts, solved));
-            npass++;
-            continue;
-        }
-        const double lc = (B.M - A.M) / (A.H - B.H);
-        R.lam_final = closed ? lc : B.lam;
-        if (!(lc > 0.0) || npass >= max_passes) break;
-        double ql[kMaxLambdas];
-        ql[0] = lc;
-        // width 1: the slope at H = b of the curve through A and B with log M
-        // linear in H, while such queries find new points; the chord certifies
-        bool model = false;
-        if (width == 1 && !force_chord && A.M > 0.0 && B.M > 0.0) {
-            const double rho = (std::log(B.M) - std::log(A.M)) / (B.H - A.H);
-            const double mb = A.M * std::exp(rho * (b - A.H));
-            const double lq = -rho * mb;
-            if (std::isfinite(lq) && lq > A.lam && lq < B.lam) {
-                ql[0] = lq;
-                model = true;
-            }
-        }
-        for (int g = 1; g < width; g++)
-            ql[g] = closed ? lc * kMul[g - 1] : A.lam + ((B.lam - A.lam) * (double)g) / 8.0;
-        ECASQ_TRY(eval_pass(c, ql, width, exact_s, pts, solved));
-        npass++;
-        const Point C = *point_at(pts, ql[0]);
-        if ((C.H == A.H && C.M == A.M) || (C.H == B.H && C.M == B.M)) {
-            if (!model) {
-                R.lam_final = lc;
-                break;
-            }
-            force_chord = true;  // the aimed query found nothing new
-        } else {
-            force_chord = false;
-        }
+    SearchState* S = c.at<SearchState>(c.L.sstate);
+    // the two-value codebook {v_0, v_{p-1}}: B when no point is feasible
+    {
+        int32_t ends[2] = {0, (int32_t)(c.p - 1)};
+        int32_t* ech = c.at<int32_t>(c.L.cchain);
+        HIP_TRY(hipMemcpyAsync(ech, ends, sizeof ends, hipMemcpyHostToDevice, c.st));
+        HIP_TRY(launch_metrics(c.H, 2, ech, 0.0, c.s2tot, c.at<double>(c.L.two), c.st));
     }
-    // refined points need not lie on a convex curve: the answer is the
-    // feasible point of lowest vNMSE found (the first among equals)
-    if (c.objective == 2 && R.status == ECASQ_OK) {
-        int ib = -1;
-        for (int x = 0; x < (int)pts.size(); x++)
-            if (pts[x].H <= b && (ib < 0 || pts[x].M < pts[ib].M)) ib = x;
-        if (ib >= 0) B = pts[ib];
+    SearchParams P;
+    P.b = b;
+    P.s2tot = c.s2tot;
+    P.max_passes = max_passes;
+    P.width = width;
+    P.aim = 1;
+    P.kind = c.objective;
+    P.has_chain = (c.objective != 0 || c.sweep) ? 1 : 0;
+    P.s = c.s;
+    P.keep_points = keep ? 1 : 0;
+    HIP_TRY(launch_search_begin(S, P, c.at<double>(c.L.two), c.st));
+    const int32_t solves0 = c.solves;
+    SearchState h;
+    if (c.objective == 0 && c.sweep && width == 1) {
+        ECASQ_TRY(search_device_loop(c, exact_s, max_passes));
+        ECASQ_TRY(read_state(c, h));
+        const int32_t imax = (int32_t)std::min<int64_t>(c.s, c.p);
+        c.solves += h.nsol;
+        c.cells += (int64_t)h.nsol * dp_cells(c.p, imax);
+    } else {
+        for (int32_t guard = 0;; guard++) {
+            ECASQ_TRY(read_state(c, h));
+            if (h.done) break;
+            if (guard > 4 * kSearchMaxPts || h.ntodo < 1 || h.ntodo > kMaxLambdas)
+                return ECASQ_EHIP;
+            ECASQ_TRY(search_host_pass(c, h, exact_s));
+        }
+        if (c.solves - solves0 != h.nsol) return ECASQ_EHIP;
     }
-    R.B = B;
-    R.A = A;
-    R.have_A = have_A;
-    R.passes = npass;
-    if (cache) cache->insert(cache->end(), pts.begin() + ncached, pts.end());
+    if (h.status == -5) return ECASQ_EHIP;
+    R.status = h.status == -3 ? ECASQ_EINFEASIBLE : ECASQ_OK;
+    R.lam_final = h.lam_final;
+    R.passes = h.npass;
+    R.B = to_point(h.B);
+    if (h.iB >= 0 && P.has_chain) ECASQ_TRY(point_chain(c, h.iB, R.B));
+    R.have_A = h.have_A != 0;
+    if (R.have_A) {
+        R.A = to_point(h.A);
+        if (P.has_chain) ECASQ_TRY(point_chain(c, h.iA, R.A));
+    }
     return ECASQ_OK;
 }
 
@@ -946,7 +1007,6 @@ ecasq_status solve_budgets(const void* x, int dt, int64_t d, int32_t s, int32_t 
     c.recovery = o.recovery;
     ecasq_options fo = o;
     if (o.dp_objective != 0) fo.refine_rounds = 0;
-    std::vector<Point> cache;
     ecasq_status worst = ECASQ_OK;
     for (int32_t k = 0; k < nb; k++) {
         const double b = budgets[k];
@@ -960,7 +1020,7 @@ ecasq_status solve_budgets(const void* x, int dt, int64_t d, int32_t s, int32_t 
             for (int64_t q = 0; q < c.p; q++) chain.push_back((int32_t)q);
         } else {
             SearchResult R;
-            ECASQ_TRY(search(c, b, o.exact_s, o.max_search_passes, o.search_width, R, &cache));
+            ECASQ_TRY(search(c, b, o.exact_s, o.max_search_passes, o.search_width, R, k > 0));
             status = R.status;
             lam = R.lam_final;
             passes = R.passes;

@@ -20,6 +20,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "exp2_table.inc"
 #include "log2_table.inc"
 
 namespace ecasq {
@@ -55,6 +56,31 @@ __device__ __forceinline__ double log2c(double y, const double2* __restrict__ ta
     q = __builtin_fma(q, r, K * 1.0);
     const double base = t.y - (double)ne;
     return __builtin_fma(r, q, base);
+}
+
+// Table-driven base-2 exponential (Tang 1989 style): y = k/64 + r with
+// k = RN(64 y) (64 y is exact) and r = (64 y - k) / 64 (exact, |r| <= 1/128);
+// 2^y = 2^floor(k/64) * T[k mod 64] * 2^r with T[i] = RN(2^(i/64)) and
+// 2^r - 1 = r (C1 + C2 r + ... + C5 r^4), C_k = RN(ln(2)^k / k!).  About one
+// ulp for |y| < 1000; NaN stays NaN, y <= -1100 gives 0, y >= 1100 gives +inf.
+__device__ __forceinline__ double exp2c(double y) {
+    if (y != y) return y;
+    if (!(y > -1100.0)) return 0.0;
+    if (!(y < 1100.0)) return __builtin_huge_val();
+    const double y64 = y * 64.0;
+    const double kd = __builtin_rint(y64);
+    const double r = (y64 - kd) * 0x1p-6;
+    const int64_t k = (int64_t)kd;
+    const int32_t i = (int32_t)(k & 63);
+    const int32_t e = (int32_t)((k - i) / 64);
+    double q = kExp2Coef[4];
+    q = __builtin_fma(q, r, kExp2Coef[3]);
+    q = __builtin_fma(q, r, kExp2Coef[2]);
+    q = __builtin_fma(q, r, kExp2Coef[1]);
+    q = __builtin_fma(q, r, kExp2Coef[0]);
+    const double pm1 = q * r;
+    const double t = kExp2Table[i];
+    return __builtin_ldexp(__builtin_fma(t, pm1, t), e);
 }
 
 // 1/x rounded to nearest for positive x with |log2 x| < 700: the hardware

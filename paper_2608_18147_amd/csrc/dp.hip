@@ -494,6 +494,15 @@ void timing_end(hipStream_t st) {
     g_open = TimedLaunch{nullptr, nullptr, 0, 0};
 }
 
+void timing_discard_last() {
+    if (g_pending.empty()) return;
+    const TimedLaunch& t = g_pending.back();
+    (void)hipEventSynchronize(t.b);
+    g_pool.push_back(t.a);
+    g_pool.push_back(t.b);
+    g_pending.pop_back();
+}
+
 void timing_read(int variant, double* ms, int64_t* launches, int64_t* cells, bool reset) {
     timing_flush();
     if (variant < 0 || variant > 3) {

@@ -115,6 +115,8 @@ void timing_read(int variant, double* ms, int64_t* launches, int64_t* cells, boo
 // solve, 3: a layer of the optimal DP)
 void timing_begin(int variant, int64_t cells, hipStream_t st);
 void timing_end(hipStream_t st);
+// drop the newest timed unit not yet flushed (a solve that was skipped)
+void timing_discard_last();
 bool timing_active();
 constexpr int kTimingOpt = 3;
 hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st);
@@ -139,7 +141,9 @@ struct SweepSolve {
     int32_t* st;   // traceback state, 264 int32
     int64_t ld;    // >= p
     int32_t I;     // last layer, min(s, p), 2..255
-    double lamp;   // lambda' in MSE units
+    double lamp;   // lambda' in MSE units (when lampp is null)
+    const double* lampp = nullptr;  // device: lambda', read by the kernels
+    const int32_t* runp = nullptr;  // device: 0 = skip the whole solve (null: run)
 };
 size_t sweep_table_bytes(int64_t d, int32_t s);
 size_t sweep_cost_bytes();
@@ -153,6 +157,50 @@ hipError_t launch_sweep_argmins(const SweepSolve& S, hipStream_t st);
 // MSE / H(I,B) accumulators of every layer into M, Ph (same layout as F);
 // needs the argmins in K.
 hipError_t launch_sweep_accumulators(const SweepSolve& S, double* M, double* Ph, hipStream_t st);
+
+// ---- search.hip ----
+// The budget search on lambda (Sec. 3 and Sec. 5), kept in device memory and
+// advanced by one-thread kernels: after each batch of DP solves the commit
+// kernel appends their points and runs the search until it needs more solves
+// (todo[0..ntodo), lambda' in todo_lamp, run = 1) or is done (run = 0).
+constexpr int kSearchMaxPts = 1024;
+struct SearchPt {
+    double lam, H, M;
+    int32_t t, pad;
+};
+struct SearchPeek {
+    int32_t done, nsol;
+    SearchPt last;
+};
+struct SearchState {
+    SearchPeek peek;  // done, nsol and the newest point, for the host's polls
+    double b, s2tot, twoH, twoM;
+    int32_t max_passes, width, aim, kind, has_chain, s;
+    int32_t npts, ncached, nsol, npass, status, done, run;
+    int32_t stage, pass_kind, issued, nq, ntodo, nin, force_chord, model, closed, have_A, iA,
+        iB, nsol0;
+    double lc, lam_final;
+    double q[kMaxLambdas], todo[kMaxLambdas], todo_lamp[kMaxLambdas];
+    SearchPt A, B;
+    SearchPt pts[kSearchMaxPts];
+};
+struct SearchParams {
+    double b, s2tot;
+    int32_t max_passes, width, aim, kind, has_chain, s;
+    int32_t keep_points;  // 1: keep the points of earlier searches on this input
+};
+// Start a search: two (device, metrics of the codebook {v_0, v_{p-1}}: MSE at
+// [0], H(Xhat) at [2], H(I,B) at [3]).
+hipError_t launch_search_begin(SearchState* S, const SearchParams& P, const double* two,
+                               hipStream_t st);
+// Append the m points solved for the next m entries of todo (a pass's solves
+// may come in several commits; the search advances once all are in): res
+// (device) holds 4 doubles per point (J, MSE, H, t); chains (device, stride
+// S->s, may be null) their codebooks, copied into pchains (kSearchMaxPts x s)
+// when S->has_chain.  With gate != 0 the kernel does nothing unless S->run is
+// set (a solve that was skipped because the search had ended).
+hipError_t launch_search_commit(SearchState* S, const double* res, const int32_t* chains,
+                                int32_t m, int32_t* pchains, int32_t gate, hipStream_t st);
 
 // ---- post.hip ----
 hipError_t launch_refine(const Hist& H, int32_t t, int32_t* u, double lamp, double b,

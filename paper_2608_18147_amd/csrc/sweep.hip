@@ -98,7 +98,17 @@ struct SweepArgs {
     int32_t I;    // last layer, min(s, p)
     double lamp;  // lambda' (MSE units)
     int64_t nblk;
+    const double* lampp;  // device lambda' (replaces lamp when set)
+    const int32_t* runp;  // device run flag: 0 skips the solve (null: run)
 };
+
+// Every kernel of a solve starts here: false when the run flag says the
+// solve is skipped, else lambda' taken from device memory when given.
+__device__ __forceinline__ bool sweep_live(SweepArgs& a) {
+    if (a.runp && *a.runp == 0) return false;
+    if (a.lampp) a.lamp = *a.lampp;
+    return true;
+}
 
 // Stage predecessor block [k0, k0+64): v, N, S, S2 and F_{i-1} for the LG
 // layers i0..i0+LG-1 (+inf past I).  All threads of the workgroup take part.
@@ -124,6 +134,7 @@ __device__ __forceinline__ void stage_block(const SweepArgs& a, int64_t k0, int3
 // Rows 2..I of F := +inf (nothing seen yet; also the value of every entry
 // outside a layer's valid columns, which makes such predecessors lose).
 __global__ __launch_bounds__(256) void k_sweep_fill(SweepArgs a) {
+    if (!sweep_live(a)) return;
     const int64_t n = (int64_t)(a.I - 1) * a.ld;
     for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n;
          x += (int64_t)gridDim.x * blockDim.x)
@@ -495,6 +506,7 @@ __global__ __launch_bounds__(kSB* kTileWaves) ECASQ_STEP_ATTR void k_sweep_step(
     SweepArgs a, int64_t t, int64_t kp0, int32_t sp, int64_t nx) {
     constexpr int32_t nb = NB;
     __shared__ StepSmem<LG> sm;
+    if (!sweep_live(a)) return;  // uniform
     // each role loads the log2 table with its first staging (one barrier)
     if (blockIdx.x == 0) {
         // the diagonal block is the step's critical path: let its waves issue
@@ -525,7 +537,7 @@ constexpr int kStChain = 8;
 // eq. apx_final on the finished table: i* (the lowest argmin over layers, or
 // I for exactly s values), u_{i*-1} = p - 1, u_0 = 0, out[0] = J.
 __global__ void k_sweep_pick(SweepArgs a, int32_t exact_s, double* out, int32_t* st) {
-    if (threadIdx.x != 0 || blockIdx.x != 0) return;
+    if (threadIdx.x != 0 || blockIdx.x != 0 || !sweep_live(a)) return;
     const int64_t p = a.H.p;
     int32_t bi = 2;
     double bj = a.F[2 * a.ld + p - 1];
@@ -562,7 +574,7 @@ __global__ __launch_bounds__(kTrT) void k_sweep_trace_part(SweepArgs a, int32_t 
     __shared__ double2 tab[kLog2Size];
     __shared__ double rv[kTrT];
     __shared__ int32_t rk[kTrT];
-    if (i > st[0]) return;  // uniform: layer above the chosen one
+    if (!sweep_live(a) || i > st[0]) return;  // uniform: skipped, or above the chosen layer
     load_log2_table(tab);
     __syncthreads();
     const int64_t j = st[kStChain + i - 1];
@@ -604,10 +616,10 @@ __global__ __launch_bounds__(kTrT) void k_sweep_trace_part(SweepArgs a, int32_t 
 __global__ __launch_bounds__(kTrT) void k_sweep_trace_pick(int32_t i, int32_t* __restrict__ st,
                                                            const double* __restrict__ pv,
                                                            const int32_t* __restrict__ pk,
-                                                           int32_t g) {
+                                                           int32_t g, const int32_t* runp) {
     __shared__ double rv[kTrT];
     __shared__ int32_t rk[kTrT];
-    if (i > st[0]) return;
+    if ((runp && *runp == 0) || i > st[0]) return;
     double best = __builtin_huge_val();
     int32_t bk = INT32_MAX;
     for (int32_t x = threadIdx.x; x < g; x += kTrT) lexmin(best, bk, pv[x], pk[x]);
@@ -633,6 +645,7 @@ __global__ __launch_bounds__(kSB) void k_sweep_sums(SweepArgs a, const int32_t* 
                                                     double* out, int32_t* chain_out) {
     __shared__ double2 tab[kLog2Size];
     __shared__ double cC[256], cP[256];
+    if (!sweep_live(a)) return;
     load_log2_table(tab);
     __syncthreads();
     const int lane = threadIdx.x;
@@ -658,6 +671,7 @@ __global__ __launch_bounds__(kSB) void k_sweep_sums(SweepArgs a, const int32_t* 
 // lane, predecessors in increasing k at wave-uniform addresses.
 __global__ __launch_bounds__(256) void k_sweep_argmins(SweepArgs a, int32_t i) {
     __shared__ double2 tab[kLog2Size];
+    if (!sweep_live(a)) return;
     load_log2_table(tab);
     __syncthreads();
     const int64_t p = a.H.p;
@@ -690,6 +704,7 @@ __global__ __launch_bounds__(256) void k_sweep_argmins2(SweepArgs a) {
 // layer-2 start 0 + C[0, j], 0 - P[0, j], as the layer-by-layer DP forms them.
 __global__ __launch_bounds__(256) void k_sweep_acc(SweepArgs a, int32_t i, double* M, double* Ph) {
     __shared__ double2 tab[kLog2Size];
+    if (!sweep_live(a)) return;
     load_log2_table(tab);
     __syncthreads();
     const int64_t j = (int64_t)(i - 1) + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -714,6 +729,8 @@ SweepArgs make_args(const SweepSolve& S) {
     a.I = S.I;
     a.lamp = S.lamp;
     a.nblk = (S.H.p + kSB - 1) / kSB;
+    a.lampp = S.lampp;
+    a.runp = S.runp;
     return a;
 }
 
@@ -807,7 +824,7 @@ hipError_t launch_sweep(const SweepSolve& S, int32_t exact_s, double* out, int32
     int32_t* pk = reinterpret_cast<int32_t*>(pv + g);
     for (int32_t i = a.I; i >= 3; i--) {
         k_sweep_trace_part<<<(unsigned)g, kTrT, 0, st>>>(a, i, S.st, pv, pk);
-        k_sweep_trace_pick<<<1, kTrT, 0, st>>>(i, S.st, pv, pk, g);
+        k_sweep_trace_pick<<<1, kTrT, 0, st>>>(i, S.st, pv, pk, g, S.runp);
     }
     k_sweep_sums<<<1, kSB, 0, st>>>(a, S.st, out, chain);
     return hipGetLastError();
