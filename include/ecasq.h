@@ -413,6 +413,28 @@ ecasq_status ecasq_opt_trace(const void *x, ecasq_dtype dt, int64_t d, int32_t s
                              double *F, int32_t *K, int32_t *chain, double *out);
 
 /*
+ * Inspection log for the parity tests (process-wide, not thread-safe).
+ * ecasq_inspect_enable(on != 0) clears the log and starts recording; 0 clears
+ * it and stops.  While on, every budget search (ecasq_solve, _ex, _budgets,
+ * _timeshare) appends one point per DP solve it runs, in solve order:
+ * lambda (vNMSE units), H (H(I,B), or H(Xhat) with dp_objective 1 and 2),
+ * vNMSE and t; points a budget sweep's search reuses from earlier budgets
+ * are not repeated.  Every budget result appends the multiplier its codebook
+ * was found at, the multiplier of the refinement (info.lambda) and the
+ * codebook's value indices before and after refinement.
+ * ecasq_inspect_points: copies min(n, cap) points (4 doubles each, host)
+ * and returns n; ecasq_inspect_results: copies min(n, cap) results, lams
+ * (host, 2 doubles each: found-at, refinement multiplier) and chains (host,
+ * 514 int32 each: t_before, the t_before indices in slots 1..256, t_after at
+ * slot 257, the t_after indices from slot 258), and returns n.  With out
+ * NULL (points) or both arrays NULL (results) the call only returns n;
+ * otherwise it clears that part of the log.
+ */
+void ecasq_inspect_enable(int32_t on);
+int32_t ecasq_inspect_points(double *out, int32_t cap);
+int32_t ecasq_inspect_results(double *lams, int32_t *chains, int32_t cap);
+
+/*
  * Kernel timing for measurement tools.  While enabled (process-wide), every
  * launch of the DP layer kernel is bracketed by two HIP events recorded on the
  * stream it runs on; the elapsed times are read when the solve synchronizes.

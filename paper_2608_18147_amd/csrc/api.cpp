@@ -26,6 +26,17 @@ using namespace ecasq;
 
 namespace {
 
+// Inspection log (ecasq_inspect_*): every DP solve's point of the budget
+// searches and every budget result's codebook before and after refinement.
+struct InspectResult {
+    double lam_B, lam_final;
+    std::vector<int32_t> pre, post;
+};
+bool g_inspect = false;
+std::vector<double> g_ins_pts;  // lambda, H, vNMSE, t per solve
+std::vector<InspectResult> g_ins_res;
+double g_ins_lamB = 0.0;  // the multiplier the last search's B was found at
+
 #define HIP_TRY(expr)                               \
     do {                                            \
         hipError_t e_ = (expr);                     \
@@ -742,6 +753,18 @@ ecasq_status search(Ctx& c, double b, int32_t exact_s, int32_t max_passes, int32
         if (c.solves - solves0 != h.nsol) return ECASQ_EHIP;
     }
     if (h.status == -5) return ECASQ_EHIP;
+    if (g_inspect) {
+        const int32_t n0 = h.ncached, n1 = std::min<int32_t>(h.npts, kSearchMaxPts);
+        if (n1 > n0) {
+            std::vector<SearchPt> q((size_t)(n1 - n0));
+            HIP_TRY(hipMemcpyAsync(q.data(), &S->pts[n0], sizeof(SearchPt) * q.size(),
+                                   hipMemcpyDeviceToHost, c.st));
+            HIP_TRY(hipStreamSynchronize(c.st));
+            for (const SearchPt& x : q)
+                g_ins_pts.insert(g_ins_pts.end(), {x.lam, x.H, x.M, (double)x.t});
+        }
+        g_ins_lamB = h.B.lam;
+    }
     R.status = h.status == -3 ? ECASQ_EINFEASIBLE : ECASQ_OK;
     R.lam_final = h.lam_final;
     R.passes = h.npass;
@@ -886,6 +909,17 @@ ecasq_status finish(Ctx& c, std::vector<int32_t>& chain, double lam, double b, b
     double* mres = c.at<double>(c.L.mres);
     HIP_TRY(launch_metrics(c.H, t, ch, lam, c.s2tot, mres, c.st));
     HIP_TRY(launch_gather(c.H.v, ch, t, codebook, rank, c.st));
+    if (g_inspect && budget) {
+        InspectResult r;
+        r.lam_B = g_ins_lamB;
+        r.lam_final = lam;
+        r.pre = chain;
+        r.post.assign(t, 0);
+        HIP_TRY(hipMemcpyAsync(r.post.data(), ch, sizeof(int32_t) * t, hipMemcpyDeviceToHost,
+                               c.st));
+        HIP_TRY(hipStreamSynchronize(c.st));
+        g_ins_res.push_back(std::move(r));
+    }
     double m[6];
     int32_t stt[2];
     HIP_TRY(hipMemcpyAsync(m, mres, sizeof m, hipMemcpyDeviceToHost, c.st));
@@ -1431,6 +1465,41 @@ ecasq_status ecasq_dp_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
         out[5 * m + 4] = per;
     }
     return ECASQ_OK;
+}
+
+void ecasq_inspect_enable(int32_t on) {
+    g_inspect = on != 0;
+    g_ins_pts.clear();
+    g_ins_res.clear();
+}
+
+int32_t ecasq_inspect_points(double* out, int32_t cap) {
+    const int32_t n = (int32_t)(g_ins_pts.size() / 4);
+    if (!out) return n;  // a size query
+    std::memcpy(out, g_ins_pts.data(), sizeof(double) * 4 * (size_t)std::max(0, std::min(n, cap)));
+    g_ins_pts.clear();
+    return n;
+}
+
+int32_t ecasq_inspect_results(double* lams, int32_t* chains, int32_t cap) {
+    const int32_t n = (int32_t)g_ins_res.size();
+    if (!lams && !chains) return n;  // a size query
+    for (int32_t k = 0; k < n && k < cap; k++) {
+        const InspectResult& r = g_ins_res[k];
+        if (lams) {
+            lams[2 * k] = r.lam_B;
+            lams[2 * k + 1] = r.lam_final;
+        }
+        if (chains) {
+            int32_t* row = chains + (int64_t)k * 2 * 257;
+            row[0] = (int32_t)r.pre.size();
+            std::memcpy(row + 1, r.pre.data(), sizeof(int32_t) * r.pre.size());
+            row[257] = (int32_t)r.post.size();
+            std::memcpy(row + 258, r.post.data(), sizeof(int32_t) * r.post.size());
+        }
+    }
+    g_ins_res.clear();
+    return n;
 }
 
 void ecasq_timing_enable(int32_t on) { timing_enable(on == 2 ? 2 : (on != 0 ? 1 : 0)); }

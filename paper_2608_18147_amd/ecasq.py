@@ -8,6 +8,7 @@ there is no fallback.
 import ctypes
 import os
 
+import numpy as np
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -77,7 +78,8 @@ EXPORTS = (
     "ecasq_histogram", "ecasq_dp_trace", "ecasq_timing_enable", "ecasq_timing_read",
     "ecasq_solve_budgets", "ecasq_solve_optimal", "ecasq_opt_trace",
     "ecasq_solve_timeshare", "ecasq_quantize_timeshare", "ecasq_encode_bound", "ecasq_encode",
-    "ecasq_decode", "ecasq_quantize_noalloc",
+    "ecasq_decode", "ecasq_quantize_noalloc", "ecasq_inspect_enable", "ecasq_inspect_points",
+    "ecasq_inspect_results",
 )
 
 
@@ -124,6 +126,12 @@ def lib():
     L.ecasq_histogram.argtypes = [vp, i32, i64, vp, vp, vp, vp, vp, P(i64)]
     L.ecasq_dp_trace.argtypes = [vp, i32, i64, i32, i32, P(dbl), i32, vp, vp, vp, vp, vp,
                                  P(dbl)]
+    L.ecasq_inspect_enable.argtypes = [i32]
+    L.ecasq_inspect_enable.restype = None
+    L.ecasq_inspect_points.argtypes = [vp, i32]
+    L.ecasq_inspect_points.restype = i32
+    L.ecasq_inspect_results.argtypes = [vp, vp, i32]
+    L.ecasq_inspect_results.restype = i32
     L.ecasq_timing_enable.argtypes = [i32]
     L.ecasq_timing_enable.restype = None
     L.ecasq_timing_read.argtypes = [i32, P(dbl), P(i64), P(i64), i32]
@@ -434,6 +442,36 @@ def ecasq_dp_trace(x, s, lam, stream=None, accumulators=False, schedule=0, argmi
         return (F[0], K[0] if K is not None else None, M[0] if M is not None else None,
                 Ph[0] if Ph is not None else None, res[0])
     return F, K, M, Ph, res
+
+
+def ecasq_inspect_enable(on=True):
+    lib().ecasq_inspect_enable(1 if on else 0)
+
+
+def ecasq_inspect_points():
+    """The recorded search points as a float64 array [n, 4]: lambda, H, vNMSE,
+    t (clears them)."""
+    n = lib().ecasq_inspect_points(None, 0)
+    out = np.zeros((max(n, 1), 4))
+    lib().ecasq_inspect_points(out.ctypes.data_as(ctypes.c_void_p), n)
+    return out[:n]
+
+
+def ecasq_inspect_results():
+    """The recorded budget results (clears them): dicts with lam_B (the
+    multiplier the codebook was found at), lam_final (the refinement's), pre
+    and post (value indices before and after refinement)."""
+    n = lib().ecasq_inspect_results(None, None, 0)
+    lams = np.zeros(2 * max(n, 1))
+    ch = np.zeros(514 * max(n, 1), dtype=np.int32)
+    lib().ecasq_inspect_results(lams.ctypes.data_as(ctypes.c_void_p),
+                                ch.ctypes.data_as(ctypes.c_void_p), n)
+    out = []
+    for k in range(n):
+        row = ch[514 * k: 514 * (k + 1)]
+        out.append(dict(lam_B=float(lams[2 * k]), lam_final=float(lams[2 * k + 1]),
+                        pre=row[1: 1 + row[0]].copy(), post=row[258: 258 + row[257]].copy()))
+    return out
 
 
 def ecasq_timing_enable(on=True, verbose=False):
