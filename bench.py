@@ -44,6 +44,19 @@ LAMBDAS_PER_PASS = 8
 ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
 FP64_VECTOR_PEAK_TFLOPS = 78.6
 
+# The roofline fraction proper: algorithmic FP64 flops per second against the
+# published FP64 vector peak (256 CUs x 2.4 GHz x 128 flops per clock per CU).
+# Flops per cell of the method: 23 with an FMA counting 2 (4 range
+# differences, v_a + v_b, the Phi sum, the candidate's add; v_a v_b, g, u,
+# w d and the two products of h; the FMAs of C (2), t_u, t_d and
+# + lambda' Phi), plus the division and the two log2 at 1 flop each: 26.  The
+# sweep forms everything but the candidate's add once per (k, j) pair and
+# adds it once per (k, j, layer) cell: 25 per pair + 1 per cell (min and max
+# count 0); a layer-2 column (its first interval's C and Phi) counts 25.
+FLOPS_PAIR = 25
+FLOPS_CELL = 1
+FLOPS_LAYER2_COL = 25
+
 
 def flops_per_cell(nlam):
     """Algorithmic ops of one (k, j) cell of the layer kernel with nlam
@@ -63,6 +76,10 @@ KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # (profiles/k_sweep_step_weights_256k.md)
 SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 5.649e7
 SWEEP_TRAFFIC_SHA = "51fc2b933e658483"
+# hardware counters of the same profile: SQ_INSTS_VALU_FLOPS_FP64 per solve over
+# the seconds per solve, and the share of VALU issue slots used
+SWEEP_COUNTER_FP64_TFLOPS = 14.9
+SWEEP_COUNTER_VALU_BUSY = 0.49
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the (workload, s) both traffic figures were measured on; null for others
 TRAFFIC_WORKLOAD = ("weights_256k", 32)
@@ -104,28 +121,43 @@ def sweep_launches(p, s):
 
 def sweep_roofline(p, s, ms, solves, cells, measured=True):
     """Roofline of DP schedule 1: all k_sweep_step launches of one solve timed
-    as one unit.  Algorithmic ops per solve: 19 per (k, j) pair (its C, Phi
-    and cost Q, shared by all layers), 2 per (k, j, layer) cell of layers
-    3..I, and 20 per column of layer 2."""
+    as one unit.  achieved = algorithmic FP64 flops per solve (FLOPS_PAIR per
+    (k, j) pair, FLOPS_CELL per (k, j, layer) cell of layers 3..I,
+    FLOPS_LAYER2_COL per layer-2 column) / seconds per solve, against the
+    78.6 TFLOP/s FP64 vector peak.  Also reported, under their own names: the
+    algorithmic FP64 lane operations per second against the lane issue rate
+    (19 per pair with the cost Q, 2 per cell, 20 per layer-2 column; every
+    add, mul, fma, min, max, division and log2 counting 1), and the
+    hardware-counted FP64 rate and VALU busy share of the committed profile
+    (for the kernel sources it was taken on)."""
     I = min(s, p)
     pairs = p * (p - 1) / 2.0
     layer_cells = sum((p - i + 1) * (p - i + 2) / 2.0 for i in range(3, I + 1))
+    flops = FLOPS_PAIR * pairs + FLOPS_CELL * layer_cells + FLOPS_LAYER2_COL * (p - 1)
     ops = (OPS_PAIR + OPS_Q) * pairs + OPS_CELL * layer_cells + 20.0 * (p - 1)
     per_ms = ms / max(solves, 1)
-    achieved = ops / (per_ms * 1e-3) / 1e12 if ms > 0 else 0.0
+    achieved = flops / (per_ms * 1e-3) / 1e12 if ms > 0 else 0.0
+    lane = ops / (per_ms * 1e-3) / 1e12 if ms > 0 else 0.0
     steps = sweep_launches(p, s)
+    current = measured and kernel_sources_sha(SWEEP_SOURCES) == SWEEP_TRAFFIC_SHA
     return {
         "bound": "alu",
         "kernel": "k_sweep_step (fp64 VALU); one DP solve = %d launches" % steps,
         "achieved": achieved,
-        "peak": ALU_PEAK_TOPS,
-        "unit": "TOP/s (fp64 lane ops)",
-        "frac": achieved / ALU_PEAK_TOPS,
-        "traffic": (SWEEP_TRAFFIC_BYTES_PER_LAUNCH
-                    if measured and kernel_sources_sha(SWEEP_SOURCES) == SWEEP_TRAFFIC_SHA
-                    else None),
+        "peak": FP64_VECTOR_PEAK_TFLOPS,
+        "unit": "TFLOP/s",
+        "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
+        "traffic": SWEEP_TRAFFIC_BYTES_PER_LAUNCH if current else None,
         "traffic_unit": "bytes/launch",
-        "ops_per_solve": ops,
+        "flops_per_solve": flops,
+        "flops_accounting": ("%d per (k, j) pair + %d per (k, j, layer) cell + %d per layer-2 "
+                             "column; FMA = 2, division and log2 = 1 each, min/max = 0"
+                             % (FLOPS_PAIR, FLOPS_CELL, FLOPS_LAYER2_COL)),
+        "lane_ops": {"achieved_tops": lane, "peak_tops": ALU_PEAK_TOPS,
+                     "frac": lane / ALU_PEAK_TOPS, "ops_per_solve": ops},
+        "counters": ({"fp64_tflops": SWEEP_COUNTER_FP64_TFLOPS,
+                      "frac_of_fp64_peak": SWEEP_COUNTER_FP64_TFLOPS / FP64_VECTOR_PEAK_TFLOPS,
+                      "valu_busy": SWEEP_COUNTER_VALU_BUSY} if current else None),
         "avg_launch_ms": per_ms / steps,
         "launches": solves * steps,
         "ms_per_solve": per_ms,
@@ -134,30 +166,56 @@ def sweep_roofline(p, s, ms, solves, cells, measured=True):
     }
 
 
-def cpu_baseline(x, s, lam, sample_d):
+def _omp():
+    """The OpenMP runtime the oracle library uses (to set its thread count)."""
+    import ctypes
+    import ctypes.util
+    name = ctypes.util.find_library("gomp") or "libgomp.so.1"
+    return ctypes.CDLL(name)
+
+
+def cpu_baseline(x, s, lam, sample_d, sample_d1=None):
     """The oracle's forward DP on the sample_d smallest entries of the same
-    input (exact cell arithmetic, OpenMP over columns)."""
+    input (exact cell arithmetic, OpenMP over columns) with all threads, and
+    on the sample_d1 smallest with one thread."""
     import numpy as np
 
     from oracle import pipeline
 
-    xs = np.sort(x)[:sample_d]
-    H = pipeline.prepare(xs)
-    t0 = time.perf_counter()
-    r = pipeline.dp_forward(H, s, lam * H.s2tot)
-    dt = time.perf_counter() - t0
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    omp = _omp()
+    threads = int(omp.omp_get_max_threads())
+
+    def run(n):
+        H = pipeline.prepare(np.sort(x)[:n])
+        t0 = time.perf_counter()
+        r = pipeline.dp_forward(H, s, lam * H.s2tot)
+        return r, time.perf_counter() - t0
+
+    r, dt = run(sample_d)
     nominal = s * sample_d * sample_d / 2.0
-    return {
+    out = {
         "value": nominal / dt,
         "unit": "cell-updates/s",
         "cores": threads,
         "kind": "oracle",
         "sample": (f"one forward dp_APX solve (s={s}, lambda={lam}) on the {sample_d} smallest "
-                   f"entries of the same input: {r['cells']} cells evaluated in {dt:.2f} s; "
-                   f"value counts s*d^2/2 with d={sample_d}"),
+                   f"entries of the same input: {r['cells']} cells evaluated in {dt:.2f} s "
+                   f"on {threads} threads; value counts s*d^2/2 with d={sample_d}"),
         "exact_cells_per_s": r["cells"] / dt,
     }
+    n1 = sample_d1 or max(1024, sample_d // 4)
+    omp.omp_set_num_threads(1)
+    try:
+        r1, dt1 = run(n1)
+    finally:
+        omp.omp_set_num_threads(threads)
+    out["one_thread"] = {
+        "value": s * n1 * n1 / 2.0 / dt1, "unit": "cell-updates/s", "cores": 1,
+        "exact_cells_per_s": r1["cells"] / dt1,
+        "sample": (f"the same solve on the {n1} smallest entries, one thread: "
+                   f"{r1['cells']} cells in {dt1:.2f} s"),
+    }
+    return out
 
 
 def batched_rate(torch, ecasq, inputs, reps=3):
@@ -296,8 +354,7 @@ def paper_setting_rate(torch, ecasq, inputs, seeds=5):
     for v in opts:
         mean = sum(per[v]) / len(per[v])
         out[v] = {"ms_per_solve": mean, "per_distribution_ms": per[v],
-                  "paper_cpu_s": PAPER_RUNTIME_S[v],
-                  "ratio_to_paper_cpu": PAPER_RUNTIME_S[v] * 1e3 / mean}
+                  "paper_cpu_s_other_machine": PAPER_RUNTIME_S[v]}
     return out
 
 
