@@ -83,6 +83,18 @@ __device__ __forceinline__ double exp2c(double y) {
     return __builtin_ldexp(__builtin_fma(t, pm1, t), e);
 }
 
+// The budget search's aimed multiplier (one multiplier per pass): the slope
+// at H = b of the curve through the bracketing points A (H_A > b) and B on
+// which log vNMSE is linear in H, in base 2:
+//   r2 = (log2 M_B - log2 M_A) / (H_B - H_A),  M_b = M_A 2^(r2 (b - H_A)),
+//   lq = -(r2 ln 2) M_b.
+__device__ __forceinline__ double aim_query(double b, double HA, double MA, double HB, double MB,
+                                            const double2* __restrict__ tab) {
+    const double r2 = (log2c(MB, tab) - log2c(MA, tab)) / (HB - HA);
+    const double mb = MA * exp2c(r2 * (b - HA));
+    return -(r2 * 0x1.62e42fefa39efp-1) * mb;
+}
+
 // 1/x rounded to nearest for positive x with |log2 x| < 700: the hardware
 // reciprocal refined by two Newton steps and one residual correction.  These
 // are the same operations, in the same order, as the IEEE double division

@@ -38,15 +38,6 @@ __device__ int find_point(const SearchState& S, double lam) {
     return -1;
 }
 
-// The width-1 search's aimed multiplier: with r2 = (log2 M_B - log2 M_A) /
-// (H_B - H_A), M_b = M_A 2^(r2 (b - H_A)) and lq = -(r2 ln 2) M_b.
-__device__ double aim_query(double b, const SearchPt& A, const SearchPt& B,
-                            const double2* __restrict__ tab) {
-    const double r2 = (log2c(B.M, tab) - log2c(A.M, tab)) / (B.H - A.H);
-    const double mb = A.M * exp2c(r2 * (b - A.H));
-    return -(r2 * 0x1.62e42fefa39efp-1) * mb;
-}
-
 // What the host polls between solves: done, solves so far, the last point.
 __device__ void peek(SearchState& S) {
     S.peek.done = S.done;
@@ -185,7 +176,7 @@ __device__ void advance(SearchState& S, const double2* __restrict__ tab) {
         S.q[0] = lc;
         S.model = 0;
         if (S.width == 1 && S.aim && !S.force_chord && S.A.M > 0.0 && S.B.M > 0.0) {
-            const double lq = aim_query(S.b, S.A, S.B, tab);
+            const double lq = aim_query(S.b, S.A.H, S.A.M, S.B.H, S.B.M, tab);
             if (__builtin_isfinite(lq) && lq > S.A.lam && lq < S.B.lam) {
                 S.q[0] = lq;
                 S.model = 1;
