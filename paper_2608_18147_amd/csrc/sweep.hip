@@ -64,6 +64,10 @@ constexpr int kTileWaves = 4;  // wavefronts per workgroup
 #ifndef ECASQ_SWEEP_LG_MAX
 #define ECASQ_SWEEP_LG_MAX 32
 #endif
+// tile workgroups keep their column blocks on one XCD from launch to launch
+#ifndef ECASQ_SWEEP_XCD
+#define ECASQ_SWEEP_XCD 1
+#endif
 // wavefronts per SIMD the step kernel's registers are sized for (0: the
 // compiler's choice).  4 (128 VGPRs) lets the early steps' ~4000 tile
 // wavefronts run in one round; it costs a few spilled registers outside the
@@ -269,8 +273,17 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int32_t nb, int64_t kp0
     const int64_t p = a.H.p;
     const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
     const int part = wave % SP;
-    const int64_t J = t + nb + wg * (kTileWaves / SP) + wave / SP;
-    const bool live = J < a.nblk;  // the same for the SP wavefronts of a column block
+    constexpr int64_t per = kTileWaves / SP;  // column blocks per workgroup
+#if ECASQ_SWEEP_XCD
+    // fixed groups of `per` column blocks, group q on workgroup 1 + q - q0
+    // with q0 a multiple of 8: a group keeps its XCD from launch to launch
+    const int64_t q0 = ((t + nb) / per) & ~(int64_t)7;
+    const int64_t J = (q0 + wg) * per + wave / SP;
+#else
+    const int64_t J = t + nb + wg * per + wave / SP;
+#endif
+    // the same for the SP wavefronts of a column block
+    const bool live = J >= t + nb && J < a.nblk;
     const int64_t j = J * kSB + lane;
     const int64_t jj = live && j < p ? j : p - 1;
     // this column's values and running minima first: their latency overlaps
@@ -756,7 +769,14 @@ hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
         const int64_t tiles = ntiles * ngroups;
         const int32_t sp = tiles < ECASQ_SWEEP_SP4_BELOW ? 4 : tiles < ECASQ_SWEEP_SP2_BELOW ? 2 : 1;
         const int64_t per = kTileWaves / sp;  // column blocks per workgroup
+#if ECASQ_SWEEP_XCD
+        // workgroups of fixed column-block groups (see tile_role), a multiple
+        // of 8 per layer group so that every group keeps its XCD
+        const int64_t q0 = ((t + nb) / per) & ~(int64_t)7;
+        const int64_t nx = ntiles > 0 ? ((a.nblk - 1) / per - q0 + 1 + 7) / 8 * 8 : 0;
+#else
         const int64_t nx = (ntiles + per - 1) / per;
+#endif
         const dim3 grid((unsigned)(1 + nx * ngroups)), block(kSB * kTileWaves);
         const int64_t nxa = nx > 0 ? nx : 1;
         // the late single-block steps (four wavefronts per tile, workgroup 0
