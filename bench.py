@@ -74,12 +74,12 @@ TRAFFIC_SOURCES_SHA = "f3a631b21f5b78fb"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
-SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 5.649e7
-SWEEP_TRAFFIC_SHA = "51fc2b933e658483"
+SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 5.651e7
+SWEEP_TRAFFIC_SHA = "a43c049ba354f64d"
 # hardware counters of the same profile: SQ_INSTS_VALU_FLOPS_FP64 per solve over
 # the seconds per solve, and the share of VALU issue slots used
-SWEEP_COUNTER_FP64_TFLOPS = 14.9
-SWEEP_COUNTER_VALU_BUSY = 0.49
+SWEEP_COUNTER_FP64_TFLOPS = 15.0
+SWEEP_COUNTER_VALU_BUSY = 0.50
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the (workload, s) both traffic figures were measured on; null for others
 TRAFFIC_WORKLOAD = ("weights_256k", 32)
