@@ -99,24 +99,15 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-# steps from which k_sweep_step makes two diagonal blocks final per launch:
-# while at least this many (column block, layer group) tiles follow
-SWEEP_PAIR_ABOVE = 2048
+# diagonal blocks k_sweep_step makes final per launch (the last launch: the rest)
+SWEEP_STEP_BLOCKS = 8
 
 
 def sweep_launches(p, s):
     """k_sweep_step launches of one sweep solve (the library's step schedule:
-    blocks of 64 columns, two per launch while the tiles that follow number
-    at least SWEEP_PAIR_ABOVE)."""
+    blocks of 64 columns, SWEEP_STEP_BLOCKS per launch)."""
     nblk = (p + 63) // 64
-    layers = min(s, p) - 2
-    lg = 8 if layers <= 8 else 16 if layers <= 16 else 32
-    groups = max(1, (layers + lg - 1) // lg)
-    t = n = 0
-    while t < nblk:
-        t += 2 if (nblk - t - 1) * groups >= SWEEP_PAIR_ABOVE else 1
-        n += 1
-    return n
+    return (nblk + SWEEP_STEP_BLOCKS - 1) // SWEEP_STEP_BLOCKS
 
 
 def sweep_roofline(p, s, ms, solves, cells, measured=True):

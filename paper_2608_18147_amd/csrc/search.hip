@@ -254,7 +254,8 @@ __global__ __launch_bounds__(64) void k_search_commit(SearchState* __restrict__ 
         for (int g = 0; g < m; g++) {
             slot[g] = -1;
             slot_t[g] = (int32_t)res[4 * g + 3];
-            if (S.npts < kSearchMaxPts) {
+            if (slot_t[g] < 2) S.status = -5;  // a failed solve ends the search
+            if (S.npts < kSearchMaxPts && slot_t[g] >= 2) {
                 SearchPt& q = S.pts[S.npts];
                 q.lam = S.todo[S.nin + g];
                 q.H = res[4 * g + 2];
@@ -279,7 +280,10 @@ __global__ __launch_bounds__(64) void k_search_commit(SearchState* __restrict__ 
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        if (S.nin >= S.ntodo) advance(S, tab);  // the pass's solves are all in
+        if (S.status == -5)
+            finish(S);
+        else if (S.nin >= S.ntodo)
+            advance(S, tab);  // the pass's solves are all in
         peek(S);
     }
 }

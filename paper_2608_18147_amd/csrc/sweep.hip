@@ -22,15 +22,21 @@
 // additions the layer-by-layer accumulators perform).
 //
 // A step of the sweep (blocks of 64 columns, one per wavefront) is one launch
-// of k_sweep_step that makes blocks t..t+nb-1 final (nb = 2 in the early
-// steps, where the tiles fill the GPU, else 1), with blocks kp0..t-1 made
-// final by the step before:
-//   workgroup 0    blocks t..t+nb-1 in order: the contribution of the
-//                  final blocks not yet added to the block, then the
-//                  triangle inside it layer after layer (a layer needs the
-//                  previous layer's values of the same block);
-//   the others     blocks J >= t+nb: the contribution of blocks kp0..t-1 to
-//                  their running minima, kept in F.
+// of k_sweep_step that makes blocks t..t+nb-1 final (nb = ECASQ_SWEEP_NB but
+// for the last step), with blocks tp..t-1 made final by the step before:
+//   workgroup m    block t+m (m < nb): its costs first, then the final
+//                  blocks not yet added to it (t-1, and t..t+m-1 as the
+//                  workgroups before it publish them), then the triangle
+//                  inside it layer after layer (a layer needs the previous
+//                  layer's values of the same block); then it publishes
+//                  the block (a flag the later workgroups wait for);
+//   the others     blocks J >= t+nb: the contribution of blocks tp..t-1 to
+//                  their running minima, kept in F; the next step's
+//                  diagonal blocks also take t..t+nb-2 as they are
+//                  published, so that its chain starts with one block to add.
+// The fixed cost of a launch (dispatch, staging, the running minima read and
+// written back) is shared by nb blocks, and the chain inside a launch costs
+// one block addition and one triangle per block.
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -46,19 +52,19 @@ constexpr int kTileWaves = 4;  // wavefronts per workgroup
 // ECASQ_SWEEP_SP2_BELOW, else 1.  More wavefronts per tile fill the SIMDs of
 // the late steps, which have few blocks left, without recomputing C and Phi.
 #ifndef ECASQ_SWEEP_SP4_BELOW
-#define ECASQ_SWEEP_SP4_BELOW 1024
+#define ECASQ_SWEEP_SP4_BELOW 1792
 #endif
 #ifndef ECASQ_SWEEP_SP2_BELOW
-#define ECASQ_SWEEP_SP2_BELOW 1536
+#define ECASQ_SWEEP_SP2_BELOW 3584
 #endif
-// (column block, layer group) tiles from which a step makes two diagonal
-// blocks final (a launch's fixed cost is then shared by two blocks)
-#ifndef ECASQ_SWEEP_PAIR_ABOVE
-#define ECASQ_SWEEP_PAIR_ABOVE 2048
+// diagonal blocks a step makes final (one workgroup each, in a chain within
+// the launch; fewer launches share their fixed cost between more blocks)
+#ifndef ECASQ_SWEEP_NB
+#define ECASQ_SWEEP_NB 8
 #endif
-// form workgroup 0's costs one launch ahead in the late single-block steps
-#ifndef ECASQ_SWEEP_PREP_COSTS
-#define ECASQ_SWEEP_PREP_COSTS 1
+// polls of a block's flag before a wait gives up (about a second)
+#ifndef ECASQ_SWEEP_SPIN
+#define ECASQ_SWEEP_SPIN (1u << 21)
 #endif
 // widest layer group (register arrays of that many layers per lane)
 #ifndef ECASQ_SWEEP_LG_MAX
@@ -86,18 +92,23 @@ constexpr int kTileWaves = 4;  // wavefronts per workgroup
 #define ECASQ_STEP_ATTR
 #endif
 
-// Costs Q = C - lambda' Phi of workgroup 0's predecessors, formed one launch
-// ahead in the late single-block steps (they do not depend on F): for block
-// b, at parity b & 1, QP[k][c] of predecessor 64 (b-1) + k and QD[k][c] of
-// predecessor 64 b + k (+inf unless 64 b + k < the column), against column
-// 64 b + c (the last column in place of columns past p - 1).
+// Costs Q = C - lambda' Phi of a diagonal block b, formed by its workgroup
+// before it waits for the block before it (they do not depend on F), in slot
+// m (the workgroup's place in the step's chain): QP[k][c] of predecessor
+// 64 (b-1) + k and QD[k][c] of predecessor 64 b + k (+inf unless 64 b + k <
+// the column), against column 64 b + c (the last column in place of columns
+// past p - 1).
 constexpr int64_t kQTab = (int64_t)kSB * kSB;
+// a diagonal workgroup's slot: QD and the tables of up to ECASQ_SWEEP_NB + 1
+// blocks it adds
+constexpr int64_t kQSlot = (ECASQ_SWEEP_NB + 2) * kQTab;
 
 struct SweepArgs {
     Hist H;
     double* F;    // [I+1][ld]: rows 2..I; running minima until a block is final
-    double* Q;    // [2][2][64][64]: QP, QD of the next diagonal block
+    double* Q;    // [ECASQ_SWEEP_NB][2][64][64]: QP, QD of each diagonal block of a step
     int32_t* K;   // argmins recomputed for inspection (same layout), and scratch
+                  // (during the steps: block flags K[0..nblk), failure word K[nblk])
     int64_t ld;
     int32_t I;    // last layer, min(s, p)
     double lamp;  // lambda' (MSE units)
@@ -137,12 +148,16 @@ __device__ __forceinline__ void stage_block(const SweepArgs& a, int64_t k0, int3
 
 // Rows 2..I of F := +inf (nothing seen yet; also the value of every entry
 // outside a layer's valid columns, which makes such predecessors lose).
+// Also clears the steps' block flags and failure word (K[0..nblk]).
 __global__ __launch_bounds__(256) void k_sweep_fill(SweepArgs a) {
     if (!sweep_live(a)) return;
     const int64_t n = (int64_t)(a.I - 1) * a.ld;
     for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n;
          x += (int64_t)gridDim.x * blockDim.x)
         a.F[2 * a.ld + x] = __builtin_huge_val();
+    for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x <= a.nblk;
+         x += (int64_t)gridDim.x * blockDim.x)
+        a.K[x] = 0;
 }
 
 // Shared memory of one step workgroup.
@@ -228,26 +243,88 @@ __device__ __forceinline__ void accumulate_q(const StepSmem<LG>& sm, int kb, int
     }
 }
 
-// QP and QD of block b (see SweepArgs), the workgroup's threads taking the
-// entries in turn; the arguments of cell_terms are those of the tiles and of
-// workgroup 0, so the costs are the same bit for bit.
-__device__ void prep_costs(const SweepArgs& a, int64_t b, const double2* __restrict__ tab) {
+// Cost tables of a diagonal workgroup: block b's own costs QD[k][c] (pred
+// 64 b + k, +inf unless 64 b + k < the column) and, for each block pb of the
+// n blocks kpd..kpd+n-1 before it that it adds, QB[pb - kpd][k][c] (pred
+// 64 pb + k), against column 64 b + c (the last column in place of columns
+// past p - 1).  A thread keeps its lane's column and takes predecessors
+// wave, wave + 4, ... of each block, staged in LDS.  The arguments of
+// cell_terms are those of the tiles, so the costs are the same bit for bit.
+template <int LG>
+__device__ void form_costs(const SweepArgs& a, int64_t b, int64_t kpd, int32_t n,
+                           double* __restrict__ QD, StepSmem<LG>& sm) {
     const int64_t p = a.H.p;
-    double* QP = a.Q + (b & 1) * 2 * kQTab;
-    double* QD = QP + kQTab;
-    for (int e = threadIdx.x; e < 2 * kQTab; e += blockDim.x) {
-        const int which = e / (int)kQTab, k = (e / kSB) % kSB, c = e % kSB;
-        const int64_t j = b * kSB + c;
-        const int64_t jj = j < p ? j : p - 1;
-        const int64_t kg = (b - 1 + which) * kSB + k;
-        double q = __builtin_huge_val();
-        if (which == 0 || kg < jj) {
-            double C, P;
-            cell_terms(a.H.v[kg], a.H.N[kg], a.H.S[kg], a.H.S2[kg], a.H.v[jj], a.H.N[jj],
-                       a.H.S[jj], a.H.S2[jj], a.H.dd, false, 0.0, tab, C, P);
-            q = __builtin_fma(-a.lamp, P, C);
+    const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
+    const int64_t j = b * kSB + lane;
+    const int64_t jj = j < p ? j : p - 1;
+    const double cv = a.H.v[jj], cN = a.H.N[jj], cS = a.H.S[jj], cS2 = a.H.S2[jj];
+    for (int32_t x = 0; x <= n; x++) {
+        const int64_t k0 = (x == 0 ? b : kpd + x - 1) * kSB;
+        if (x > 0) __syncthreads();  // every thread is done with the last block
+        if (threadIdx.x < kSB) {
+            const int64_t k = k0 + threadIdx.x < p ? k0 + threadIdx.x : p - 1;
+            sm.sv[threadIdx.x] = a.H.v[k];
+            sm.sN[threadIdx.x] = a.H.N[k];
+            sm.sS[threadIdx.x] = a.H.S[k];
+            sm.sS2[threadIdx.x] = a.H.S2[k];
         }
-        (which == 0 ? QP : QD)[k * kSB + c] = q;
+        __syncthreads();
+        double* T = QD + (int64_t)x * kQTab;
+#pragma unroll 4
+        for (int k = wave; k < kSB; k += kTileWaves) {
+            double q = __builtin_huge_val();
+            if (x > 0 || k0 + k < jj) {
+                double C, P;
+                cell_terms(sm.sv[k], sm.sN[k], sm.sS[k], sm.sS2[k], cv, cN, cS, cS2, a.H.dd, false,
+                           0.0, sm.tab, C, P);
+                q = __builtin_fma(-a.lamp, P, C);
+            }
+            T[k * kSB + lane] = q;
+        }
+    }
+}
+
+// Chunk counters of the step's chain: flag[b] counts the chunks of block b
+// that are final (a chunk is the LG/4 layers of a layer group that one
+// wavefront of the diagonal workgroup holds; chunks are final in order, so
+// flag[b] = n means every layer up to the n'th chunk's last); flag[nblk] != 0
+// once a wait has given up.  Both live in K (free during the steps) and are
+// cleared by k_sweep_fill.
+//
+// wait_flag: one thread polls flag[b] until it reaches n (device-scope loads,
+// which see other XCDs' stores), then an acquire fence makes the chunks'
+// values visible to the workgroup, whose threads meet at the barrier.  The
+// wait is bounded: after ECASQ_SWEEP_SPIN polls it marks the solve failed and
+// returns, and every later wait returns at once, so every wavefront ends;
+// k_sweep_pick then reports no codebook.
+__device__ void wait_flag(const SweepArgs& a, int64_t b, int32_t n) {
+    if (threadIdx.x == 0) {
+        int32_t* flag = a.K;
+        for (uint32_t r = 0;; r++) {
+            if (__hip_atomic_load(flag + b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= n)
+                break;
+            if ((r & 63) == 0 &&
+                __hip_atomic_load(flag + a.nblk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+                break;
+            if (r >= ECASQ_SWEEP_SPIN) {
+                __hip_atomic_store(flag + a.nblk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
+            __builtin_amdgcn_s_sleep(1);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
+    __syncthreads();
+}
+
+// flag[b] := n: every wavefront waits for its stores, and after the barrier
+// one thread releases them (device scope) and sets the counter.
+__device__ void publish_flag(const SweepArgs& a, int64_t b, int32_t n) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        __hip_atomic_store(a.K + b, n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
@@ -258,32 +335,30 @@ __device__ __forceinline__ void stage_pred(const SweepArgs& a, int64_t k0, int32
     stage_block<LG>(a, k0, i0, sm.sv, sm.sN, sm.sS, sm.sS2, sm.sF);
 }
 
-// Tile role: column blocks J >= t + nb take the predecessor blocks kp0..t-1
-// (made final by the last step) for one layer group (its first NL layers;
-// NL < LG only where the layers past them exceed I).  SP wavefronts per column block, each taking 64/SP of the
-// predecessors; with SP > 1 their partial minima meet in LDS (the staging
-// buffer, free once every wavefront is done with it), LG/4 layers at a time,
-// and the wavefront that merges a chunk (its partial started from the
-// chunk's running minima) writes the result to F.
-template <int LG, int NL, int SP, int MP>
-__device__ void tile_role(const SweepArgs& a, int64_t t, int32_t nb, int64_t kp0, int64_t wg,
-                          int32_t g, StepSmem<LG>& sm) {
+// Tile role: the column blocks Jw..Jw+per-1 (those in [Jlo, nblk) live) of
+// one layer group (its first NL layers; NL < LG only where the layers past
+// them exceed I) take the final blocks tp..pe-1, waiting for those >= t (made
+// final by this step's chain).  The far tiles (J >= t + nb + nbn) take
+// tp..t-1, made final by the last step; the next step's nbn diagonal blocks,
+// one workgroup each, also take this step's blocks t..t+nb-2 as they are
+// published, so that the next step's chain starts with one block to add.
+// SP wavefronts per column block, each taking 64/SP of the predecessors;
+// with SP > 1 their partial minima meet in LDS (the staging buffer, free once
+// every wavefront is done with it), LG/4 layers at a time, and the wavefront
+// that merges a chunk (its partial started from the chunk's running minima)
+// writes the result to F.
+template <int LG, int NL, int SP>
+__device__ void tile_role(const SweepArgs& a, int64_t t, int64_t tp, int64_t pe, int64_t Jw,
+                          int64_t Jlo, int32_t g, int32_t nch, StepSmem<LG>& sm) {
     constexpr int KP = kSB / SP;
     const int32_t i0 = 3 + g * LG;
     const int64_t p = a.H.p;
     const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
     const int part = wave % SP;
     constexpr int64_t per = kTileWaves / SP;  // column blocks per workgroup
-#if ECASQ_SWEEP_XCD
-    // fixed groups of `per` column blocks, group q on workgroup 1 + q - q0
-    // with q0 a multiple of 8: a group keeps its XCD from launch to launch
-    const int64_t q0 = ((t + nb) / per) & ~(int64_t)7;
-    const int64_t J = (q0 + wg) * per + wave / SP;
-#else
-    const int64_t J = t + nb + wg * per + wave / SP;
-#endif
-    // the same for the SP wavefronts of a column block
-    const bool live = J >= t + nb && J < a.nblk;
+    const int64_t J = Jw + wave / SP;  // the same for the SP wavefronts of a column block
+    const bool live = J >= Jlo && J < a.nblk;
+    if (Jw + per <= Jlo || Jw >= a.nblk || pe <= tp) return;  // uniform: nothing to do
     const int64_t j = J * kSB + lane;
     const int64_t jj = live && j < p ? j : p - 1;
     // this column's values and running minima first: their latency overlaps
@@ -303,29 +378,17 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int32_t nb, int64_t kp0
         }
     }
     load_log2_table(sm.tab);
-    // predecessor blocks kp0..t-1 (at most MP; tiles run only when there is
-    // one), one staged at a time
-    if constexpr (MP == 1) {
-        stage_pred<LG>(a, (t - 1) * kSB, i0, sm);
+    for (int64_t pb = tp; pb < pe; pb++) {
+        if (pb > tp) __syncthreads();  // every wavefront is done with the last block
+        if (pb >= t) wait_flag(a, pb, nch);
+        stage_pred<LG>(a, pb * kSB, i0, sm);
         __syncthreads();
-        if (SP == 1 && !live) return;  // (no barrier follows for SP = 1)
-        accumulate<LG, NL>(sm, 0, part * KP, part * KP + KP, cv, cN, cS, cS2, a.H.dd, a.lamp,
-                           best);
-    } else {
-        const int np = (int)min<int64_t>(t - kp0, MP);
-        for (int u = 0; u < np; u++) {
-            const int64_t pb = t - np + u;
-            if (u > 0) __syncthreads();  // every wavefront is done with the last block
-            stage_pred<LG>(a, pb * kSB, i0, sm);
-            __syncthreads();
-            if (live)
-                accumulate<LG, NL>(sm, 0, part * KP, part * KP + KP, cv, cN, cS, cS2, a.H.dd,
-                                   a.lamp, best);
-        }
-        if (SP == 1 && !live) return;  // (no barrier follows for SP = 1)
+        if (live)
+            accumulate<LG, NL>(sm, 0, part * KP, part * KP + KP, cv, cN, cS, cS2, a.H.dd, a.lamp,
+                               best);
     }
     if constexpr (SP == 1) {
-        store_running<NL>(a, j, i0, best);
+        if (live) store_running<NL>(a, j, i0, best);
     } else {
         // 4 x CH rows of 64 fit the staging buffer
         double (*xb)[kSB] = reinterpret_cast<double (*)[kSB]>(&sm.sF[0][0]);
@@ -353,194 +416,196 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int32_t nb, int64_t kp0
     }
 }
 
-// Diagonal role (workgroup 0): blocks t..t+nb-1 become final, in order.  For
-// block b and every layer group: the predecessor blocks kp0..b-1 not yet
-// added to it (those the last step made final, and block t when b = t+1),
-// each wavefront taking 16 predecessors of each for all the group's layers,
-// the four partial minima merged in LDS by the wavefront that holds a layer
-// (layers ow*LG/4.. of the group on wavefront ow, with their running
-// minima); then the group's layers inside the block in order: each wavefront
-// holds the cost Q of 16 of the block's predecessors in registers, the four
-// partial minima meet in LDS and the wavefront that holds the layer merges
-// them.  A block's final values are read back from F for the next block
-// after the workgroup barrier that orders them.
-template <int LG, int NL, int MP, bool PRE = false>
-__device__ void diag_block(const SweepArgs& a, int64_t t, int64_t kp0, StepSmem<LG>& sm) {
-    constexpr int LW = LG / kTileWaves;
+// Diagonal role: workgroup m of a step makes block b = t + m final, one chunk
+// at a time (chunk c of a layer group: the LW = LG/4 layers that wavefront c
+// holds, with their running minima).  It first forms its cost tables: QD and
+// one per block it adds (t-1, made final by the last step, and t..b-1, made
+// final by this step's workgroups 0..m-1).  Then per chunk: each of those
+// blocks for the chunk's layers, in order, once its chunk is final (waited
+// for): each wavefront takes 16 of its predecessors, and the four partial
+// minima meet in LDS, where the holder merges them into its running minima;
+// then the chunk's layers inside the block in order: each wavefront holds
+// the cost Q of 16 of the block's predecessors in registers, the four
+// partial minima meet in LDS and the holder merges them; then the chunk is
+// published.  So block b's chunk c needs block b-1's chunk c, not all of
+// block b-1.
+template <int LG, int NL>
+__device__ void diag_block(const SweepArgs& a, int64_t t, int32_t m, StepSmem<LG>& sm) {
+    constexpr int LW = LG / kTileWaves;   // layers per chunk
     constexpr int KW = kSB / kTileWaves;  // predecessors of a block per wavefront
+    constexpr int kStage = LG / LW;       // blocks whose chunk rows fit the staging buffer
     const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
     const int64_t p = a.H.p;
-    const int64_t j0 = t * kSB;
-    const int64_t j = j0 + lane;
+    const int64_t b = t + m;
+    const int64_t j = b * kSB + lane;
     const int64_t jj = j < p ? j : p - 1;
     const bool valid = j < p;
-    const double lamp = a.lamp, dd = a.H.dd;
-    for (int x = threadIdx.x; x < kSB; x += blockDim.x) {
-        const int64_t k = j0 + x < p ? j0 + x : p - 1;
-        sm.dv[x] = a.H.v[k];
-        sm.dN[x] = a.H.N[k];
-        sm.dS[x] = a.H.S[k];
-        sm.dS2[x] = a.H.S2[k];
-    }
-    __syncthreads();
-    const int c = (int)(jj - j0);
-    const double cv = sm.dv[c], cN = sm.dN[c], cS = sm.dS[c], cS2 = sm.dS2[c];
+    const int64_t kpd = t > 0 ? t - 1 : 0;  // first block not yet added to b
+    double* QD = a.Q + (int64_t)m * kQSlot;
+    __syncthreads();  // the log2 table
+    if (a.I >= 3) form_costs<LG>(a, b, kpd, (int32_t)(b - kpd), QD, sm);
     // layer 2 (eq. apx_base): the first interval (v_0, v_j]
     if (wave == 0) {
         double f = __builtin_huge_val();
         if (valid && j >= 1) {
             double C, P;
             cell_at(a.H, 0, j, sm.tab, C, P);
-            f = __builtin_fma(-lamp, P, 0.0 + C);
+            f = __builtin_fma(-a.lamp, P, 0.0 + C);
             a.F[2 * a.ld + j] = f;
         }
         sm.pF[lane] = f;
     }
+    __syncthreads();  // the cost tables and layer 2
+    double (*xb)[kSB] = reinterpret_cast<double (*)[kSB]>(&sm.sF[0][0]);
+    int32_t cg = 0;  // chunks published
     for (int32_t i0 = 3; i0 <= a.I; i0 += LG) {
-        const int32_t iw = i0 + wave * LW;
         double best[LW];
-        load_running<LW>(a, jj, iw, best);
-        __syncthreads();  // previous group's use of sF / pF is over
-        // each final block not yet added (at most MP): a partial per
-        // wavefront, merged into the layers' holders before the next block
-        // is staged
-        auto add_block = [&](int64_t pb) {
-            stage_pred<LG>(a, pb * kSB, i0, sm);
-            __syncthreads();
-            double pa[NL];
-#pragma unroll
-            for (int l = 0; l < NL; l++) pa[l] = __builtin_huge_val();
-            if constexpr (PRE)  // block t-1's costs, formed by the last launch
-                accumulate_q<LG, NL>(sm, wave * KW, wave * KW + KW,
-                                     a.Q + (t & 1) * 2 * kQTab + lane, pa);
-            else
-                accumulate<LG, NL>(sm, 0, wave * KW, wave * KW + KW, cv, cN, cS, cS2, dd, lamp,
-                                   pa);
-            __syncthreads();  // the staging buffer is free: 4 x LW rows of 64
-            double (*xb)[kSB] = reinterpret_cast<double (*)[kSB]>(&sm.sF[0][0]);
-#pragma unroll
-            for (int ow = 0; ow < kTileWaves; ow++) {
-                if (ow * LW >= NL) break;
-#pragma unroll
-                for (int q = 0; q < LW && ow * LW + q < NL; q++) xb[wave * LW + q][lane] = pa[ow * LW + q];
-                __syncthreads();
-                if (wave == ow) {
-#pragma unroll
-                    for (int q = 0; q < LW && ow * LW + q < NL; q++)
-                        best[q] = __builtin_fmin(
-                            best[q], __builtin_fmin(__builtin_fmin(xb[q][lane], xb[LW + q][lane]),
-                                                    __builtin_fmin(xb[2 * LW + q][lane],
-                                                                   xb[3 * LW + q][lane])));
-                }
-                __syncthreads();
-            }
-        };
-        if constexpr (MP == 1) {
-            if (kp0 < t) add_block(t - 1);
-        } else {
-            const int np = (int)min<int64_t>(t - kp0, MP);
-            for (int u = 0; u < np; u++) {
-                if (u > 0) __syncthreads();  // the last merge is done with the buffer
-                add_block(t - np + u);
-            }
-        }
-        // the cost Q = C - lambda' Phi of (k, j) for this wavefront's 16
-        // predecessors k < j of the block; the others get +inf, so their
-        // candidates are +inf
-        double cQ[KW];
-#pragma unroll
-        for (int q = 0; q < KW; q++) {
-            const int kk = wave * KW + q;
-            cQ[q] = __builtin_huge_val();
-            if constexpr (PRE) {
-                cQ[q] = a.Q[(t & 1) * 2 * kQTab + kQTab + kk * kSB + lane];
-            } else if (j0 + kk < jj) {
-                double C, P;
-                cell_terms(sm.dv[kk], sm.dN[kk], sm.dS[kk], sm.dS2[kk], cv, cN, cS, cS2, dd,
-                           false, 0.0, sm.tab, C, P);
-                cQ[q] = __builtin_fma(-lamp, P, C);
-            }
-        }
-        // layer l = ow * LW + q of the group: held by wavefront ow at q
+        load_running<LW>(a, jj, i0 + wave * LW, best);
 #pragma unroll 1
-        for (int ow = 0; ow < kTileWaves; ow++) {
+        for (int c = 0; c < kTileWaves; c++) {
+            const int32_t ic = i0 + c * LW;  // the chunk's first layer
+            if (ic > a.I) break;
+            // the blocks not yet added, for the chunk's layers: partial minima
+            // over this wavefront's 16 predecessors of each, merged once
+            double pa[LW];
 #pragma unroll
-        for (int q8 = 0; q8 < LW; q8++) {
-            const int32_t i = i0 + ow * LW + q8;
-            if (i > a.I) break;
-            // this wavefront's 16 candidates as 4 minima of 4 (short
-            // dependency chains), then a tree
-            double m4[4];
-#pragma unroll
-            for (int c4 = 0; c4 < 4; c4++) {
-                m4[c4] = __builtin_huge_val();
-#pragma unroll
-                for (int q = 4 * c4; q < 4 * c4 + 4; q++) {
-                    const int kk = wave * KW + q;
-                    m4[c4] = __builtin_fmin(m4[c4], sm.pF[kk] + cQ[q]);
+            for (int l = 0; l < LW; l++) pa[l] = __builtin_huge_val();
+            // up to kStage blocks u0..u0+n-1 staged together (F_{i-1} for the
+            // chunk's layers), then their candidates
+            auto add_blocks = [&](int64_t u0, int n) {
+                __syncthreads();  // the staging buffer is free
+                for (int x = threadIdx.x; x < kSB * LW * n; x += blockDim.x) {
+                    const int kk = x % kSB, l = (x / kSB) % LW, u = x / (kSB * LW);
+                    const int32_t i = ic + l;
+                    sm.sF[kk][u * LW + l] =
+                        i <= a.I ? a.F[(int64_t)(i - 1) * a.ld + (u0 + u) * kSB + kk]
+                                 : __builtin_huge_val();
                 }
+                __syncthreads();
+                for (int u = 0; u < n; u++) {
+                    const double* Qc = QD + (u0 + u - kpd + 1) * kQTab + lane;
+#pragma unroll
+                    for (int q = 0; q < KW; q += 2) {
+                        const int kk = wave * KW + q;
+                        const double Q0 = Qc[kk * kSB], Q1 = Qc[(kk + 1) * kSB];
+#pragma unroll
+                        for (int l = 0; l < LW; l++) {
+                            pa[l] = __builtin_fmin(pa[l], sm.sF[kk][u * LW + l] + Q0);
+                            pa[l] = __builtin_fmin(pa[l], sm.sF[kk + 1][u * LW + l] + Q1);
+                        }
+                    }
+                }
+            };
+            // blocks kpd..b-2 first (their chunk is final once block b-2's
+            // is), then block b-1, the one the chain waits for
+            if (b - 2 >= t) wait_flag(a, b - 2, cg + 1);
+            for (int64_t u0 = kpd; u0 < b - 1; u0 += kStage)
+                add_blocks(u0, (int)min<int64_t>(kStage, b - 1 - u0));
+            if (b > kpd) {
+                if (b - 1 >= t) wait_flag(a, b - 1, cg + 1);
+                add_blocks(b - 1, 1);
+                __syncthreads();  // the staging buffer is free: 4 x LW rows of 64
+#pragma unroll
+                for (int l = 0; l < LW; l++) xb[wave * LW + l][lane] = pa[l];
+                __syncthreads();
+                if (wave == c) {
+#pragma unroll
+                    for (int l = 0; l < LW; l++)
+                        best[l] = __builtin_fmin(
+                            best[l], __builtin_fmin(__builtin_fmin(xb[l][lane], xb[LW + l][lane]),
+                                                    __builtin_fmin(xb[2 * LW + l][lane],
+                                                                   xb[3 * LW + l][lane])));
+                }
+                __syncthreads();
             }
-            sm.partV[wave][lane] =
-                __builtin_fmin(__builtin_fmin(m4[0], m4[1]), __builtin_fmin(m4[2], m4[3]));
-            __syncthreads();
-            if (wave == ow) {
-                const double v =
-                    __builtin_fmin(__builtin_fmin(sm.partV[0][lane], sm.partV[1][lane]),
-                                   __builtin_fmin(sm.partV[2][lane], sm.partV[3][lane]));
-                const double b = __builtin_fmin(best[q8], v);
-                if (valid) a.F[(int64_t)i * a.ld + j] = b;
-                sm.pF[lane] = valid ? b : __builtin_huge_val();
+            // the chunk's layers inside the block, in order, with the cost of
+            // (k, j) for this wavefront's 16 predecessors k < j of the block
+            // (+inf for the others, so their candidates are +inf)
+            double cQ[KW];
+#pragma unroll
+            for (int q = 0; q < KW; q++) cQ[q] = QD[(wave * KW + q) * kSB + lane];
+#pragma unroll
+            for (int q8 = 0; q8 < LW; q8++) {
+                const int32_t i = ic + q8;
+                if (i > a.I) break;
+                // this wavefront's 16 candidates as 4 minima of 4 (short
+                // dependency chains), then a tree
+                double m4[4];
+#pragma unroll
+                for (int c4 = 0; c4 < 4; c4++) {
+                    m4[c4] = __builtin_huge_val();
+#pragma unroll
+                    for (int q = 4 * c4; q < 4 * c4 + 4; q++)
+                        m4[c4] = __builtin_fmin(m4[c4], sm.pF[wave * KW + q] + cQ[q]);
+                }
+                sm.partV[wave][lane] =
+                    __builtin_fmin(__builtin_fmin(m4[0], m4[1]), __builtin_fmin(m4[2], m4[3]));
+                __syncthreads();
+                if (wave == c) {
+                    const double v =
+                        __builtin_fmin(__builtin_fmin(sm.partV[0][lane], sm.partV[1][lane]),
+                                       __builtin_fmin(sm.partV[2][lane], sm.partV[3][lane]));
+                    const double bv = __builtin_fmin(best[q8], v);
+                    if (valid) a.F[(int64_t)i * a.ld + j] = bv;
+                    sm.pF[lane] = valid ? bv : __builtin_huge_val();
+                }
+                __syncthreads();
             }
-            __syncthreads();
+            cg++;
+            publish_flag(a, b, cg);
         }
-        }
+        if constexpr (NL < LG) break;  // one group holds every layer (I = NL + 2)
     }
 }
 
-template <int LG, int NL, int MP, int NB, bool PRE>
-__device__ void diag_role(const SweepArgs& a, int64_t t, int64_t kp0, StepSmem<LG>& sm) {
-    load_log2_table(sm.tab);
-    diag_block<LG, NL, MP, PRE>(a, t, kp0, sm);
-    if constexpr (NB == 2) {
-        if (t + 1 < a.nblk) {
-            __syncthreads();  // the first block's use of LDS is over
-            diag_block<LG, NL, MP + 1>(a, t + 1, kp0, sm);
-        }
-    }
-}
-
-// One step of the sweep: workgroup 0 makes blocks t..t+nb-1 final, the others
-// add predecessor blocks kp0..t-1 to the blocks after them (tile WG index =
-// g * nx + wg).
-// PRE: workgroup 0 reads block t's costs formed by the last launch; PREP:
-// the last workgroup forms block t+1's (single-block steps only).
-template <int LG, int NL, int MP, int NB, bool PRE = false, bool PREP = false>
+// One step of the sweep: workgroups 0..nb-1 make blocks t..t+nb-1 final (a
+// chain: each waits for the one before); the next nbn x ngroups take this
+// step's final blocks to the next step's diagonal blocks (near tiles: one
+// column block and layer group each, four wavefronts on it); the others
+// (far tiles, WG index g * nx + wg after them) take blocks tp..t-1 to the
+// column blocks after those.
+template <int LG, int NL>
 __global__ __launch_bounds__(kSB* kTileWaves) ECASQ_STEP_ATTR void k_sweep_step(
-    SweepArgs a, int64_t t, int64_t kp0, int32_t sp, int64_t nx) {
-    constexpr int32_t nb = NB;
+    SweepArgs a, int64_t t, int32_t nb, int32_t nbn, int64_t tp, int32_t sp, int64_t nx,
+    int32_t ngroups) {
     __shared__ StepSmem<LG> sm;
     if (!sweep_live(a)) return;  // uniform
-    // each role loads the log2 table with its first staging (one barrier)
-    if (blockIdx.x == 0) {
-        // the diagonal block is the step's critical path: let its waves issue
+    const int64_t J1 = t + nb;   // the first column block after the step's
+    const int64_t Jn = J1 + nbn;  // the first far column block
+    const int64_t nnear = (int64_t)nbn * ngroups;
+    // chunks per block (LG/4 layers each, those that hold a layer <= I)
+    const int32_t nch = (a.I - 2 + LG / kTileWaves - 1) / (LG / kTileWaves);
+    if ((int32_t)blockIdx.x < nb) {
+        // the diagonal chain is the step's critical path: let its waves issue
         // ahead of tile waves that share its SIMDs
         __builtin_amdgcn_s_setprio(3);
-        diag_role<LG, NL, MP, NB, PRE>(a, t, kp0, sm);
-    } else if (PREP && blockIdx.x == gridDim.x - 1) {
-        if (t + 1 >= a.nblk) return;
         load_log2_table(sm.tab);
-        __syncthreads();
-        prep_costs(a, t + 1, sm.tab);
+        diag_block<LG, NL>(a, t, (int32_t)blockIdx.x, sm);
+    } else if ((int64_t)blockIdx.x < nb + nnear) {
+        // the next step's chain waits for these
+        __builtin_amdgcn_s_setprio(2);
+        const int64_t x = (int64_t)blockIdx.x - nb;
+        tile_role<LG, NL, 4>(a, t, tp, t + nb - 1, J1 + x % nbn, J1, (int32_t)(x / nbn), nch,
+                             sm);
     } else {
-        const int64_t x = (int64_t)blockIdx.x - 1;
+        const int64_t x = (int64_t)blockIdx.x - nb - nnear;
         const int64_t wg = x % nx;
         const int32_t g = (int32_t)(x / nx);
+        const int64_t per = kTileWaves / sp;
+#if ECASQ_SWEEP_XCD
+        // fixed groups of `per` column blocks, group q on the q - q0'th far
+        // workgroup, q0 a multiple of 8: a group keeps its XCD from launch to
+        // launch while the diagonal and near workgroups before them are as many
+        const int64_t Jw = (((J1 / per) & ~(int64_t)7) + wg) * per;
+#else
+        const int64_t Jw = Jn + wg * per;
+#endif
         if (sp == 4)
-            tile_role<LG, NL, 4, MP>(a, t, nb, kp0, wg, g, sm);
+            tile_role<LG, NL, 4>(a, t, tp, t, Jw, Jn, g, nch, sm);
         else if (sp == 2)
-            tile_role<LG, NL, 2, MP>(a, t, nb, kp0, wg, g, sm);
+            tile_role<LG, NL, 2>(a, t, tp, t, Jw, Jn, g, nch, sm);
         else
-            tile_role<LG, NL, 1, MP>(a, t, nb, kp0, wg, g, sm);
+            tile_role<LG, NL, 1>(a, t, tp, t, Jw, Jn, g, nch, sm);
     }
 }
 
@@ -549,9 +614,17 @@ constexpr int kStChain = 8;
 
 // eq. apx_final on the finished table: i* (the lowest argmin over layers, or
 // I for exactly s values), u_{i*-1} = p - 1, u_0 = 0, out[0] = J.
+// A solve whose steps gave up a wait (failure word set) reports i* = 0: the
+// traceback kernels then return at once and the result has t = 0, which the
+// callers take as a failed solve.
 __global__ void k_sweep_pick(SweepArgs a, int32_t exact_s, double* out, int32_t* st) {
     if (threadIdx.x != 0 || blockIdx.x != 0 || !sweep_live(a)) return;
     const int64_t p = a.H.p;
+    if (a.K[a.nblk] != 0) {
+        st[0] = 0;
+        out[0] = __builtin_nan("");
+        return;
+    }
     int32_t bi = 2;
     double bj = a.F[2 * a.ld + p - 1];
     for (int32_t i = 3; i <= a.I; i++) {
@@ -747,6 +820,11 @@ SweepArgs make_args(const SweepSolve& S) {
     return a;
 }
 
+// Blocks a step starting at block t makes final.
+int32_t step_blocks(int64_t t, int64_t nblk) {
+    return (int32_t)(nblk - t < ECASQ_SWEEP_NB ? nblk - t : ECASQ_SWEEP_NB);
+}
+
 template <int LG, int NL = LG>
 hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
     const int32_t ngroups = (a.I - 2 + LG - 1) / LG;
@@ -756,16 +834,13 @@ hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
         if (g > 4096) g = 4096;
         k_sweep_fill<<<(unsigned)g, 256, 0, st>>>(a);
     }
-    // blocks kp0..t-1 are final and not yet added to the blocks after them;
-    // a step makes nb more final (two while the tiles keep at least
-    // ECASQ_SWEEP_PAIR_ABOVE wavefronts busy: half the launches and half the
-    // running-minima traffic, for a diagonal chain twice as long)
-    int64_t kp0 = 0;
-    bool prepped = false;  // the last launch formed block t's costs
+    // a step makes blocks t..t+nb-1 final; blocks tp..t-1 (the last step's)
+    // are final and not yet added to the column blocks after t + nb
+    int64_t tp = 0;
     for (int64_t t = 0; t < a.nblk;) {
-        const int64_t after1 = a.nblk - t - 1;
-        const int32_t nb = after1 * ngroups >= ECASQ_SWEEP_PAIR_ABOVE ? 2 : 1;
-        const int64_t ntiles = (kp0 < t && ngroups > 0) ? a.nblk - t - nb : 0;
+        const int32_t nb = step_blocks(t, a.nblk);
+        const int32_t nbn = t + nb < a.nblk ? step_blocks(t + nb, a.nblk) : 0;
+        const int64_t ntiles = ngroups > 0 ? a.nblk - t - nb : 0;
         const int64_t tiles = ntiles * ngroups;
         const int32_t sp = tiles < ECASQ_SWEEP_SP4_BELOW ? 4 : tiles < ECASQ_SWEEP_SP2_BELOW ? 2 : 1;
         const int64_t per = kTileWaves / sp;  // column blocks per workgroup
@@ -777,26 +852,11 @@ hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
 #else
         const int64_t nx = (ntiles + per - 1) / per;
 #endif
-        const dim3 grid((unsigned)(1 + nx * ngroups)), block(kSB * kTileWaves);
-        const int64_t nxa = nx > 0 ? nx : 1;
-        // the late single-block steps (four wavefronts per tile, workgroup 0
-        // the longest part): one more workgroup forms the next block's costs
-        const bool late = ECASQ_SWEEP_PREP_COSTS && nb == 1 && t - kp0 <= 1 && sp == 4;
-        const dim3 gridp((unsigned)(2 + nx * ngroups));
-        // instantiations by (most final blocks to add, blocks made final):
-        // the paired steps, the step after them, and the single steps
-        if (nb == 2)
-            k_sweep_step<LG, NL, 2, 2><<<grid, block, 0, st>>>(a, t, kp0, sp, nxa);
-        else if (t - kp0 == 2)
-            k_sweep_step<LG, NL, 2, 1><<<grid, block, 0, st>>>(a, t, kp0, sp, nxa);
-        else if (late && prepped)
-            k_sweep_step<LG, NL, 1, 1, true, true><<<gridp, block, 0, st>>>(a, t, kp0, sp, nxa);
-        else if (late)
-            k_sweep_step<LG, NL, 1, 1, false, true><<<gridp, block, 0, st>>>(a, t, kp0, sp, nxa);
-        else
-            k_sweep_step<LG, NL, 1, 1><<<grid, block, 0, st>>>(a, t, kp0, sp, nxa);
-        prepped = late;
-        kp0 = t;
+        const int64_t nnear = ngroups > 0 ? (int64_t)nbn * ngroups : 0;
+        const dim3 grid((unsigned)(nb + nnear + nx * ngroups)), block(kSB * kTileWaves);
+        k_sweep_step<LG, NL><<<grid, block, 0, st>>>(a, t, nb, nbn, tp, sp, nx > 0 ? nx : 1,
+                                                      ngroups);
+        tp = t;
         t += nb;
     }
     return hipGetLastError();
@@ -820,7 +880,7 @@ size_t sweep_table_bytes(int64_t d, int32_t s) {
     return (size_t)(s + 1) * (size_t)d * (sizeof(double) + sizeof(int32_t));
 }
 
-size_t sweep_cost_bytes() { return 4 * (size_t)kQTab * sizeof(double); }
+size_t sweep_cost_bytes() { return ECASQ_SWEEP_NB * (size_t)kQSlot * sizeof(double); }
 
 hipError_t launch_sweep(const SweepSolve& S, int32_t exact_s, double* out, int32_t* chain,
                         hipStream_t st) {

@@ -13,15 +13,11 @@ import bench  # noqa: E402
 
 def _schedule(p, s):
     """The step schedule written out: blocks of 64 columns, a step making
-    two blocks final while at least SWEEP_PAIR_ABOVE (column block, layer
-    group) tiles follow its first block, else one."""
+    SWEEP_STEP_BLOCKS blocks final (the last step the rest)."""
     nblk = -(-p // 64)
-    layers = min(s, p) - 2
-    lg = 8 if layers <= 8 else (16 if layers <= 16 else 32)
-    groups = max(1, -(-layers // lg))
     steps, t = [], 0
     while t < nblk:
-        nb = 2 if (nblk - t - 1) * groups >= bench.SWEEP_PAIR_ABOVE else 1
+        nb = min(bench.SWEEP_STEP_BLOCKS, nblk - t)
         steps.append((t, nb))
         t += nb
     return nblk, steps
@@ -34,15 +30,11 @@ def test_sweep_launches_cover_every_block_once(p, s):
     assert bench.sweep_launches(p, s) == len(steps)
     made = [b for t, nb in steps for b in range(t, t + nb)]
     assert made == list(range(nblk))
-    # pairs only in a prefix: the blocks per step never increase
-    nbs = [nb for _, nb in steps]
-    assert nbs == sorted(nbs, reverse=True)
 
 
 def test_default_workload_launch_count():
-    # 4090 blocks: 1021 paired steps while 2048 or more blocks follow, then
-    # one step per block
-    assert bench.sweep_launches(261755, 32) == 1021 + 2048
+    # 4090 blocks of 64 columns, eight per launch
+    assert bench.sweep_launches(261755, 32) == 512
 
 
 def test_bench_refuses_more_than_one_gpu():

@@ -98,6 +98,8 @@ DP_CASES = [
     ("weights_5000", 5000, 6, 1.0),
     ("dups_700", 700, 10, 0.3),
     ("wide_range_2000", 2000, 10, 0.1),  # interval widths from 2^-148 to 2^128
+    ("normal_190_s9", 190, 9, 0.1),      # three column blocks: one sweep step, a short chain
+    ("normal_4500_s64", 4500, 64, 0.02),  # two layer groups, 71 column blocks
 ]
 
 
