@@ -100,7 +100,7 @@ def log(*a):
 
 
 # diagonal blocks k_sweep_step makes final per launch (the last launch: the rest)
-SWEEP_STEP_BLOCKS = 8
+SWEEP_STEP_BLOCKS = 12
 
 
 def sweep_launches(p, s):

@@ -60,7 +60,7 @@ constexpr int kTileWaves = 4;  // wavefronts per workgroup
 // diagonal blocks a step makes final (one workgroup each, in a chain within
 // the launch; fewer launches share their fixed cost between more blocks)
 #ifndef ECASQ_SWEEP_NB
-#define ECASQ_SWEEP_NB 8
+#define ECASQ_SWEEP_NB 12
 #endif
 // polls of a block's flag before a wait gives up (about a second)
 #ifndef ECASQ_SWEEP_SPIN
@@ -92,23 +92,34 @@ constexpr int kTileWaves = 4;  // wavefronts per workgroup
 #define ECASQ_STEP_ATTR
 #endif
 
-// Costs Q = C - lambda' Phi of a diagonal block b, formed by its workgroup
-// before it waits for the block before it (they do not depend on F), in slot
-// m (the workgroup's place in the step's chain): QP[k][c] of predecessor
-// 64 (b-1) + k and QD[k][c] of predecessor 64 b + k (+inf unless 64 b + k <
-// the column), against column 64 b + c (the last column in place of columns
-// past p - 1).
+// Helpers of the step's chain: diagonal block b = t + m takes the blocks
+// tp..b-2 it has not yet added (the last step's blocks and this step's
+// before b-1) from helper workgroups, kHelpBlocks blocks each, which run side
+// by side and leave their partial minima of every layer of block b in a
+// buffer of their own.
+constexpr int kHelpBlocks = 2;
+constexpr int kHelpMax = ECASQ_SWEEP_NB > 1 ? ECASQ_SWEEP_NB - 1 : 1;  // per diagonal block
+
+// Cost tables Q = C - lambda' Phi (they do not depend on F), formed by the
+// workgroups of the chain before they wait for anything and read back into
+// registers once: T[k][c] of predecessor 64 kb + k against column 64 b + c
+// of a diagonal block b (the last column in place of columns past p - 1; for
+// kb = b, +inf unless 64 b + k < the column).  Slot of diagonal workgroup m:
+// blocks b-1 and b; slot of its helper h: the helper's blocks.  Then the
+// helpers' partial minima, kPLayers layers of 64 columns each.
 constexpr int64_t kQTab = (int64_t)kSB * kSB;
-// a diagonal workgroup's slot: QD and the tables of up to ECASQ_SWEEP_NB + 1
-// blocks it adds
-constexpr int64_t kQSlot = (ECASQ_SWEEP_NB + 2) * kQTab;
+constexpr int64_t kQSlot = (int64_t)kHelpBlocks * kQTab;  // two tables per workgroup
+constexpr int64_t kPLayers = 256;                         // layers 3..258 include 3..I
+constexpr int64_t kPartAt = (int64_t)ECASQ_SWEEP_NB * (1 + kHelpMax) * kQSlot;
+constexpr int64_t kQAll = kPartAt + (int64_t)ECASQ_SWEEP_NB * kHelpMax * kPLayers * kSB;
 
 struct SweepArgs {
     Hist H;
     double* F;    // [I+1][ld]: rows 2..I; running minima until a block is final
-    double* Q;    // [ECASQ_SWEEP_NB][2][64][64]: QP, QD of each diagonal block of a step
+    double* Q;    // kQAll doubles: the chain's cost tables
     int32_t* K;   // argmins recomputed for inspection (same layout), and scratch
-                  // (during the steps: block flags K[0..nblk), failure word K[nblk])
+                  // (during the steps: chunk counters of blocks K[0..nblk), the
+                  // failure word K[nblk], the helpers' counters after it)
     int64_t ld;
     int32_t I;    // last layer, min(s, p)
     double lamp;  // lambda' (MSE units)
@@ -126,37 +137,80 @@ __device__ __forceinline__ bool sweep_live(SweepArgs& a) {
 }
 
 // Stage predecessor block [k0, k0+64): v, N, S, S2 and F_{i-1} for the LG
-// layers i0..i0+LG-1 (+inf past I).  All threads of the workgroup take part.
+// layers i0..i0+LG-1 (+inf past I).  All kThreads threads of the workgroup
+// take part; each issues all its loads before it stores any to LDS.
+constexpr int kThreads = kSB * kTileWaves;
 template <int LG>
 __device__ __forceinline__ void stage_block(const SweepArgs& a, int64_t k0, int32_t i0, double* sv,
                                             double* sN, double* sS, double* sS2,
                                             double (*sF)[LG]) {
     // block [k0, k0+64) lies below a later block, so k0 + 63 < p
-    for (int x = threadIdx.x; x < kSB; x += blockDim.x) {
-        const int64_t k = k0 + x;
-        sv[x] = a.H.v[k];
-        sN[x] = a.H.N[k];
-        sS[x] = a.H.S[k];
-        sS2[x] = a.H.S2[k];
-    }
-    for (int x = threadIdx.x; x < kSB * LG; x += blockDim.x) {
+    constexpr int R = kSB * LG / kThreads;  // F values per thread
+    static_assert(R * kThreads == kSB * LG, "a layer group of 64 columns fills the workgroup");
+    double f[R];
+#pragma unroll
+    for (int r = 0; r < R; r++) {
+        const int x = threadIdx.x + r * kThreads;
         const int kk = x % kSB, l = x / kSB;
         const int32_t i = i0 + l;
-        sF[kk][l] = i <= a.I ? a.F[(int64_t)(i - 1) * a.ld + k0 + kk] : __builtin_huge_val();
+        f[r] = i <= a.I ? a.F[(int64_t)(i - 1) * a.ld + k0 + kk] : __builtin_huge_val();
+    }
+    if (threadIdx.x < kSB) {
+        const int64_t k = k0 + threadIdx.x;
+        sv[threadIdx.x] = a.H.v[k];
+        sN[threadIdx.x] = a.H.N[k];
+        sS[threadIdx.x] = a.H.S[k];
+        sS2[threadIdx.x] = a.H.S2[k];
+    }
+#pragma unroll
+    for (int r = 0; r < R; r++) {
+        const int x = threadIdx.x + r * kThreads;
+        sF[x % kSB][x / kSB] = f[r];
+    }
+}
+
+// F_{i-1} of the LW layers ic.. of a chunk for blocks u0..u0+n-1 (n <= NU)
+// into sF[k][u LW + l] (+inf past I); all kThreads threads take part and
+// issue their loads before their stores.
+template <int LG, int LW, int NU>
+__device__ __forceinline__ void stage_chunk(const SweepArgs& a, int64_t u0, int n, int32_t ic,
+                                            double (*sF)[LG]) {
+    constexpr int R = (kSB * LW + kThreads - 1) / kThreads;  // values per thread and block
+    double f[NU][R];
+#pragma unroll
+    for (int u = 0; u < NU; u++) {
+#pragma unroll
+        for (int r = 0; r < R; r++) {
+            const int x = threadIdx.x + r * kThreads;
+            const int32_t i = ic + x / kSB;
+            f[u][r] = u < n && x < kSB * LW && i <= a.I
+                          ? a.F[(int64_t)(i - 1) * a.ld + (u0 + u) * kSB + x % kSB]
+                          : __builtin_huge_val();
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < NU; u++) {
+        if (u < n) {
+#pragma unroll
+            for (int r = 0; r < R; r++) {
+                const int x = threadIdx.x + r * kThreads;
+                if (x < kSB * LW) sF[x % kSB][u * LW + x / kSB] = f[u][r];
+            }
+        }
     }
 }
 
 // Rows 2..I of F := +inf (nothing seen yet; also the value of every entry
 // outside a layer's valid columns, which makes such predecessors lose).
-// Also clears the steps' block flags and failure word (K[0..nblk]).
+// Also clears the steps' counters and failure word (K[0..nblk (1 + kHelpMax)]).
 __global__ __launch_bounds__(256) void k_sweep_fill(SweepArgs a) {
     if (!sweep_live(a)) return;
     const int64_t n = (int64_t)(a.I - 1) * a.ld;
     for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n;
          x += (int64_t)gridDim.x * blockDim.x)
         a.F[2 * a.ld + x] = __builtin_huge_val();
-    for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x <= a.nblk;
-         x += (int64_t)gridDim.x * blockDim.x)
+    for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+         x <= a.nblk * (1 + kHelpMax); x += (int64_t)gridDim.x * blockDim.x)
         a.K[x] = 0;
 }
 
@@ -164,9 +218,10 @@ __global__ __launch_bounds__(256) void k_sweep_fill(SweepArgs a) {
 template <int LG>
 struct StepSmem {
     double2 tab[kLog2Size];
-    double sv[kSB], sN[kSB], sS[kSB], sS2[kSB];  // the staged predecessor block
-    double sF[kSB][LG];                           // its F_{i-1} for one layer group
-    double dv[kSB], dN[kSB], dS[kSB], dS2[kSB];   // block t (diagonal role)
+    // v, N, S, S2 of two blocks: a tile's staged predecessor block in [0],
+    // the chain roles' two blocks in [0] and [1]
+    double hv[2][kSB], hN[2][kSB], hS[2][kSB], hS2[2][kSB];
+    double sF[kSB][LG];  // F_{i-1} of the staged block for one layer group
     double pF[kSB];                               // previous layer of block t
     double partV[kTileWaves][kSB];                // per-wave partial minima
 };
@@ -203,7 +258,7 @@ __device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int lofs, int
         // many layers per predecessor: enough independent work per iteration
         for (int kk = kb; kk < ke; kk++) {
             double C, P;
-            cell_terms(sm.sv[kk], sm.sN[kk], sm.sS[kk], sm.sS2[kk], cv, cN, cS, cS2, dd, false,
+            cell_terms(sm.hv[0][kk], sm.hN[0][kk], sm.hS[0][kk], sm.hS2[0][kk], cv, cN, cS, cS2, dd, false,
                        0.0, sm.tab, C, P);
             const double Q = __builtin_fma(-lamp, P, C);
 #pragma unroll
@@ -214,9 +269,9 @@ __device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int lofs, int
     // independent chains the scheduler can interleave
     for (int kk = kb; kk < ke; kk += 2) {
         double C0, P0, C1, P1;
-        cell_terms(sm.sv[kk], sm.sN[kk], sm.sS[kk], sm.sS2[kk], cv, cN, cS, cS2, dd, false, 0.0,
+        cell_terms(sm.hv[0][kk], sm.hN[0][kk], sm.hS[0][kk], sm.hS2[0][kk], cv, cN, cS, cS2, dd, false, 0.0,
                    sm.tab, C0, P0);
-        cell_terms(sm.sv[kk + 1], sm.sN[kk + 1], sm.sS[kk + 1], sm.sS2[kk + 1], cv, cN, cS, cS2,
+        cell_terms(sm.hv[0][kk + 1], sm.hN[0][kk + 1], sm.hS[0][kk + 1], sm.hS2[0][kk + 1], cv, cN, cS, cS2,
                    dd, false, 0.0, sm.tab, C1, P1);
         const double Q0 = __builtin_fma(-lamp, P0, C0), Q1 = __builtin_fma(-lamp, P1, C1);
 #pragma unroll
@@ -243,45 +298,55 @@ __device__ __forceinline__ void accumulate_q(const StepSmem<LG>& sm, int kb, int
     }
 }
 
-// Cost tables of a diagonal workgroup: block b's own costs QD[k][c] (pred
-// 64 b + k, +inf unless 64 b + k < the column) and, for each block pb of the
-// n blocks kpd..kpd+n-1 before it that it adds, QB[pb - kpd][k][c] (pred
-// 64 pb + k), against column 64 b + c (the last column in place of columns
-// past p - 1).  A thread keeps its lane's column and takes predecessors
-// wave, wave + 4, ... of each block, staged in LDS.  The arguments of
-// cell_terms are those of the tiles, so the costs are the same bit for bit.
-template <int LG>
-__device__ void form_costs(const SweepArgs& a, int64_t b, int64_t kpd, int32_t n,
-                           double* __restrict__ QD, StepSmem<LG>& sm) {
-    const int64_t p = a.H.p;
+// v, N, S, S2 of block kb (indices past p - 1 clamped) into LDS; call from
+// all threads, then __syncthreads().
+__device__ __forceinline__ void stage_hist(const SweepArgs& a, int64_t kb, double* sv, double* sN,
+                                           double* sS, double* sS2) {
+    if (threadIdx.x < kSB) {
+        const int64_t k = kb * kSB + threadIdx.x < a.H.p ? kb * kSB + threadIdx.x : a.H.p - 1;
+        sv[threadIdx.x] = a.H.v[k];
+        sN[threadIdx.x] = a.H.N[k];
+        sS[threadIdx.x] = a.H.S[k];
+        sS2[threadIdx.x] = a.H.S2[k];
+    }
+}
+
+// Cost tables against the columns of block b (cv.. the column of the
+// thread's lane, jj its index): T + x kQTab for x = 0..n-1 holds the table of
+// the predecessor block whose v, N, S, S2 are staged in sv[x].. (block kb0 +
+// x).  A thread takes predecessors wave, wave + 4, ... of each block.  The
+// arguments of cell_terms are those of the tiles, so the costs are the same
+// bit for bit.
+__device__ void form_costs(const SweepArgs& a, int64_t b, int64_t kb0, int n,
+                           const double (*sv)[kSB], const double (*sN)[kSB],
+                           const double (*sS)[kSB], const double (*sS2)[kSB], int64_t jj,
+                           double cv, double cN, double cS, double cS2,
+                           const double2* __restrict__ tab, double* __restrict__ T0) {
     const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
-    const int64_t j = b * kSB + lane;
-    const int64_t jj = j < p ? j : p - 1;
-    const double cv = a.H.v[jj], cN = a.H.N[jj], cS = a.H.S[jj], cS2 = a.H.S2[jj];
-    for (int32_t x = 0; x <= n; x++) {
-        const int64_t k0 = (x == 0 ? b : kpd + x - 1) * kSB;
-        if (x > 0) __syncthreads();  // every thread is done with the last block
-        if (threadIdx.x < kSB) {
-            const int64_t k = k0 + threadIdx.x < p ? k0 + threadIdx.x : p - 1;
-            sm.sv[threadIdx.x] = a.H.v[k];
-            sm.sN[threadIdx.x] = a.H.N[k];
-            sm.sS[threadIdx.x] = a.H.S[k];
-            sm.sS2[threadIdx.x] = a.H.S2[k];
-        }
-        __syncthreads();
-        double* T = QD + (int64_t)x * kQTab;
-#pragma unroll 4
+    for (int x = 0; x < n; x++) {
+        const int64_t kb = kb0 + x;
+        double* T = T0 + (int64_t)x * kQTab;
+#pragma unroll 2
         for (int k = wave; k < kSB; k += kTileWaves) {
             double q = __builtin_huge_val();
-            if (x > 0 || k0 + k < jj) {
+            if (kb < b || kb * kSB + k < jj) {
                 double C, P;
-                cell_terms(sm.sv[k], sm.sN[k], sm.sS[k], sm.sS2[k], cv, cN, cS, cS2, a.H.dd, false,
-                           0.0, sm.tab, C, P);
+                cell_terms(sv[x][k], sN[x][k], sS[x][k], sS2[x][k], cv, cN, cS, cS2, a.H.dd, false,
+                           0.0, tab, C, P);
                 q = __builtin_fma(-a.lamp, P, C);
             }
             T[k * kSB + lane] = q;
         }
     }
+}
+
+// This wavefront's 16 predecessors' costs from table T (this lane's column).
+__device__ __forceinline__ void lane_costs(const double* __restrict__ T,
+                                           double (&Q)[kSB / kTileWaves]) {
+    constexpr int KW = kSB / kTileWaves;
+    const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
+#pragma unroll
+    for (int q = 0; q < KW; q++) Q[q] = T[(wave * KW + q) * kSB + lane];
 }
 
 // Chunk counters of the step's chain: flag[b] counts the chunks of block b
@@ -297,21 +362,35 @@ __device__ void form_costs(const SweepArgs& a, int64_t b, int64_t kpd, int32_t n
 // wait is bounded: after ECASQ_SWEEP_SPIN polls it marks the solve failed and
 // returns, and every later wait returns at once, so every wavefront ends;
 // k_sweep_pick then reports no codebook.
+__device__ __forceinline__ void poll_flag(const SweepArgs& a, int64_t b, int32_t n) {
+    int32_t* flag = a.K;
+    for (uint32_t r = 0;; r++) {
+        if (__hip_atomic_load(flag + b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= n) break;
+        if ((r & 63) == 0 &&
+            __hip_atomic_load(flag + a.nblk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
+            break;
+        if (r >= ECASQ_SWEEP_SPIN) {
+            __hip_atomic_store(flag + a.nblk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
 __device__ void wait_flag(const SweepArgs& a, int64_t b, int32_t n) {
     if (threadIdx.x == 0) {
-        int32_t* flag = a.K;
-        for (uint32_t r = 0;; r++) {
-            if (__hip_atomic_load(flag + b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= n)
-                break;
-            if ((r & 63) == 0 &&
-                __hip_atomic_load(flag + a.nblk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT))
-                break;
-            if (r >= ECASQ_SWEEP_SPIN) {
-                __hip_atomic_store(flag + a.nblk, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                break;
-            }
-            __builtin_amdgcn_s_sleep(1);
-        }
+        poll_flag(a, b, n);
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    }
+    __syncthreads();
+}
+
+// As wait_flag for the counters K[b0] (b0 >= 0) and K[h0..h0+nh), all >= n:
+// one acquire and one barrier.
+__device__ void wait_flags(const SweepArgs& a, int64_t b0, int64_t h0, int nh, int32_t n) {
+    if (threadIdx.x == 0) {
+        if (b0 >= 0) poll_flag(a, b0, n);
+        for (int x = 0; x < nh; x++) poll_flag(a, h0 + x, n);
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
     __syncthreads();
@@ -332,24 +411,20 @@ __device__ void publish_flag(const SweepArgs& a, int64_t b, int32_t n) {
 template <int LG>
 __device__ __forceinline__ void stage_pred(const SweepArgs& a, int64_t k0, int32_t i0,
                                            StepSmem<LG>& sm) {
-    stage_block<LG>(a, k0, i0, sm.sv, sm.sN, sm.sS, sm.sS2, sm.sF);
+    stage_block<LG>(a, k0, i0, sm.hv[0], sm.hN[0], sm.hS[0], sm.hS2[0], sm.sF);
 }
 
 // Tile role: the column blocks Jw..Jw+per-1 (those in [Jlo, nblk) live) of
 // one layer group (its first NL layers; NL < LG only where the layers past
-// them exceed I) take the final blocks tp..pe-1, waiting for those >= t (made
-// final by this step's chain).  The far tiles (J >= t + nb + nbn) take
-// tp..t-1, made final by the last step; the next step's nbn diagonal blocks,
-// one workgroup each, also take this step's blocks t..t+nb-2 as they are
-// published, so that the next step's chain starts with one block to add.
-// SP wavefronts per column block, each taking 64/SP of the predecessors;
-// with SP > 1 their partial minima meet in LDS (the staging buffer, free once
+// them exceed I) take the blocks tp..t-1, made final by the last step.  SP
+// wavefronts per column block, each taking 64/SP of the predecessors; with
+// SP > 1 their partial minima meet in LDS (the staging buffer, free once
 // every wavefront is done with it), LG/4 layers at a time, and the wavefront
 // that merges a chunk (its partial started from the chunk's running minima)
 // writes the result to F.
 template <int LG, int NL, int SP>
-__device__ void tile_role(const SweepArgs& a, int64_t t, int64_t tp, int64_t pe, int64_t Jw,
-                          int64_t Jlo, int32_t g, int32_t nch, StepSmem<LG>& sm) {
+__device__ void tile_role(const SweepArgs& a, int64_t t, int64_t tp, int64_t Jw, int64_t Jlo,
+                          int32_t g, StepSmem<LG>& sm) {
     constexpr int KP = kSB / SP;
     const int32_t i0 = 3 + g * LG;
     const int64_t p = a.H.p;
@@ -358,7 +433,7 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int64_t tp, int64_t pe,
     constexpr int64_t per = kTileWaves / SP;  // column blocks per workgroup
     const int64_t J = Jw + wave / SP;  // the same for the SP wavefronts of a column block
     const bool live = J >= Jlo && J < a.nblk;
-    if (Jw + per <= Jlo || Jw >= a.nblk || pe <= tp) return;  // uniform: nothing to do
+    if (Jw + per <= Jlo || Jw >= a.nblk || t <= tp) return;  // uniform: nothing to do
     const int64_t j = J * kSB + lane;
     const int64_t jj = live && j < p ? j : p - 1;
     // this column's values and running minima first: their latency overlaps
@@ -378,9 +453,8 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int64_t tp, int64_t pe,
         }
     }
     load_log2_table(sm.tab);
-    for (int64_t pb = tp; pb < pe; pb++) {
+    for (int64_t pb = tp; pb < t; pb++) {
         if (pb > tp) __syncthreads();  // every wavefront is done with the last block
-        if (pb >= t) wait_flag(a, pb, nch);
         stage_pred<LG>(a, pb * kSB, i0, sm);
         __syncthreads();
         if (live)
@@ -416,34 +490,143 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int64_t tp, int64_t pe,
     }
 }
 
-// Diagonal role: workgroup m of a step makes block b = t + m final, one chunk
-// at a time (chunk c of a layer group: the LW = LG/4 layers that wavefront c
-// holds, with their running minima).  It first forms its cost tables: QD and
-// one per block it adds (t-1, made final by the last step, and t..b-1, made
-// final by this step's workgroups 0..m-1).  Then per chunk: each of those
-// blocks for the chunk's layers, in order, once its chunk is final (waited
-// for): each wavefront takes 16 of its predecessors, and the four partial
-// minima meet in LDS, where the holder merges them into its running minima;
-// then the chunk's layers inside the block in order: each wavefront holds
-// the cost Q of 16 of the block's predecessors in registers, the four
-// partial minima meet in LDS and the holder merges them; then the chunk is
-// published.  So block b's chunk c needs block b-1's chunk c, not all of
-// block b-1.
+// Index of the chunk counter of helper h of block b in K.
+__device__ __forceinline__ int64_t help_counter(const SweepArgs& a, int64_t b, int h) {
+    return a.nblk + 1 + b * kHelpMax + h;
+}
+
+// Helpers of diagonal block b = t + m: the blocks tp..b-2 not yet added to
+// b, kHelpBlocks per helper.
+__device__ __forceinline__ int helpers_of(int64_t t, int64_t tp, int32_t m) {
+    const int64_t n = t + m - 1 - tp;
+    return n > 0 ? (int)((n + kHelpBlocks - 1) / kHelpBlocks) : 0;
+}
+
+// Partial minima of helper h of diagonal workgroup m: kPLayers rows of 64.
+__device__ __forceinline__ double* help_partials(const SweepArgs& a, int32_t m, int h) {
+    return a.Q + kPartAt + ((int64_t)m * kHelpMax + h) * kPLayers * kSB;
+}
+
+// Helper h of diagonal block b = t + m: blocks u0..u1-1 (u0 = tp +
+// kHelpBlocks h), chunk by chunk as their chunks become final (waited for):
+// each wavefront takes 16 predecessors of each block with their costs in
+// registers, the four partial minima meet in LDS and go to the helper's
+// buffer, one row per layer; then the helper's counter is published.
 template <int LG, int NL>
-__device__ void diag_block(const SweepArgs& a, int64_t t, int32_t m, StepSmem<LG>& sm) {
+__device__ void helper_block(const SweepArgs& a, int64_t t, int64_t tp, int32_t m, int h,
+                             StepSmem<LG>& sm) {
     constexpr int LW = LG / kTileWaves;   // layers per chunk
     constexpr int KW = kSB / kTileWaves;  // predecessors of a block per wavefront
-    constexpr int kStage = LG / LW;       // blocks whose chunk rows fit the staging buffer
+    const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
+    const int64_t p = a.H.p;
+    const int64_t b = t + m;
+    const int64_t u0 = tp + (int64_t)kHelpBlocks * h;
+    const int64_t u1 = min<int64_t>(u0 + kHelpBlocks, b - 1);
+    if (u0 >= u1 || a.I < 3) return;  // uniform: nothing to add
+    const int nu = (int)(u1 - u0);
+    const int64_t jj = min<int64_t>(b * kSB + lane, p - 1);
+    double* T = a.Q + ((int64_t)ECASQ_SWEEP_NB + (int64_t)m * kHelpMax + h) * kQSlot;
+    double* P = help_partials(a, m, h);
+    stage_hist(a, u0, sm.hv[0], sm.hN[0], sm.hS[0], sm.hS2[0]);
+    if (nu > 1) stage_hist(a, u0 + 1, sm.hv[1], sm.hN[1], sm.hS[1], sm.hS2[1]);
+    const double cv = a.H.v[jj], cN = a.H.N[jj], cS = a.H.S[jj], cS2 = a.H.S2[jj];
+    __syncthreads();  // (also the log2 table)
+    form_costs(a, b, u0, nu, sm.hv, sm.hN, sm.hS, sm.hS2, jj, cv, cN, cS, cS2, sm.tab, T);
+    __syncthreads();  // the tables
+    double q0[KW], q1[KW];
+    lane_costs(T, q0);
+    if (nu > 1) lane_costs(T + kQTab, q1);
+    double (*xb)[kSB] = reinterpret_cast<double (*)[kSB]>(&sm.sF[0][0]);
+    int32_t cg = 0;  // chunks published
+    for (int32_t i0 = 3; i0 <= a.I; i0 += LG) {
+#pragma unroll 1
+        for (int c = 0; c < kTileWaves; c++) {
+            const int32_t ic = i0 + c * LW;  // the chunk's first layer
+            if (ic > a.I) break;
+            if (u1 - 1 >= t) wait_flag(a, u1 - 1, cg + 1);
+            __syncthreads();  // the staging buffer is free
+            stage_chunk<LG, LW, kHelpBlocks>(a, u0, nu, ic, sm.sF);
+            __syncthreads();
+            double pa[LW];
+#pragma unroll
+            for (int l = 0; l < LW; l++) pa[l] = __builtin_huge_val();
+#pragma unroll
+            for (int q = 0; q < KW; q++) {
+                const int kk = wave * KW + q;
+#pragma unroll
+                for (int l = 0; l < LW; l++) pa[l] = __builtin_fmin(pa[l], sm.sF[kk][l] + q0[q]);
+            }
+            if (nu > 1) {
+#pragma unroll
+                for (int q = 0; q < KW; q++) {
+                    const int kk = wave * KW + q;
+#pragma unroll
+                    for (int l = 0; l < LW; l++)
+                        pa[l] = __builtin_fmin(pa[l], sm.sF[kk][LW + l] + q1[q]);
+                }
+            }
+            __syncthreads();  // the staging buffer is free: 4 x LW rows of 64
+#pragma unroll
+            for (int l = 0; l < LW; l++) xb[wave * LW + l][lane] = pa[l];
+            __syncthreads();
+            for (int x = threadIdx.x; x < LW * kSB; x += blockDim.x) {
+                const int l = x / kSB, c2 = x % kSB;
+                P[(int64_t)(ic - 3 + l) * kSB + c2] =
+                    __builtin_fmin(__builtin_fmin(xb[l][c2], xb[LW + l][c2]),
+                                   __builtin_fmin(xb[2 * LW + l][c2], xb[3 * LW + l][c2]));
+            }
+            cg++;
+            publish_flag(a, help_counter(a, b, h), cg);
+        }
+        if constexpr (NL < LG) break;  // one group holds every layer (I = NL + 2)
+    }
+}
+
+// Diagonal role: workgroup m of a step makes block b = t + m final, one chunk
+// at a time (chunk c of a layer group: the LW = LG/4 layers that wavefront c
+// holds, with their running minima).  It first forms the cost tables of
+// block b-1 and of b itself and keeps its 16 predecessors' costs of both in
+// registers.  Then per chunk: once that chunk of block b-1 is final and the
+// helper has folded the blocks before b-1 into b's running minima (both
+// waited for), the holder reads the running minima of the chunk's layers,
+// and block b-1's contribution (each wavefront takes 16 of its
+// predecessors) is merged into them in LDS; then the chunk's layers inside the
+// block in order: each wavefront holds the cost Q of 16 of the block's
+// predecessors in registers, the four partial minima meet in LDS and the
+// holder merges them; then the chunk is published.  So block b's chunk c
+// needs block b-1's chunk c, not all of block b-1.
+template <int LG, int NL>
+__device__ void diag_block(const SweepArgs& a, int64_t t, int64_t tp, int32_t m,
+                           StepSmem<LG>& sm) {
+    constexpr int LW = LG / kTileWaves;   // layers per chunk
+    constexpr int KW = kSB / kTileWaves;  // predecessors of a block per wavefront
     const int wave = threadIdx.x / kSB, lane = threadIdx.x % kSB;
     const int64_t p = a.H.p;
     const int64_t b = t + m;
     const int64_t j = b * kSB + lane;
     const int64_t jj = j < p ? j : p - 1;
     const bool valid = j < p;
-    const int64_t kpd = t > 0 ? t - 1 : 0;  // first block not yet added to b
-    double* QD = a.Q + (int64_t)m * kQSlot;
-    __syncthreads();  // the log2 table
-    if (a.I >= 3) form_costs<LG>(a, b, kpd, (int32_t)(b - kpd), QD, sm);
+    const int64_t kpd = tp;                 // first block not yet added to b
+    const int nh = helpers_of(t, tp, m);    // blocks kpd..b-2 come from the helpers
+    // the tables of the costs of (k, j) for block b-1's predecessors k and
+    // block b's own (+inf unless k < j), the same for every chunk
+    double* T = a.Q + (int64_t)m * kQSlot;  // block b-1's table, then b's own
+    const int64_t kb0 = b >= 1 ? b - 1 : b;
+    stage_hist(a, kb0, sm.hv[0], sm.hN[0], sm.hS[0], sm.hS2[0]);
+    if (b >= 1) stage_hist(a, b, sm.hv[1], sm.hN[1], sm.hS[1], sm.hS2[1]);
+    __syncthreads();  // (also the log2 table)
+    const int cc = (int)(jj - b * kSB);
+    {
+        const int o = b >= 1 ? 1 : 0;  // block b's place
+        const double cv = sm.hv[o][cc], cN = sm.hN[o][cc], cS = sm.hS[o][cc], cS2 = sm.hS2[o][cc];
+        if (a.I >= 3)
+            form_costs(a, b, kb0, b >= 1 ? 2 : 1, sm.hv, sm.hN, sm.hS, sm.hS2, jj, cv, cN, cS,
+                       cS2, sm.tab, b >= 1 ? T : T + kQTab);
+    }
+    __syncthreads();  // the tables
+    double qP[KW], cQ[KW];
+    if (b >= 1) lane_costs(T, qP);
+    lane_costs(T + kQTab, cQ);
     // layer 2 (eq. apx_base): the first interval (v_0, v_j]
     if (wave == 0) {
         double f = __builtin_huge_val();
@@ -455,60 +638,50 @@ __device__ void diag_block(const SweepArgs& a, int64_t t, int32_t m, StepSmem<LG
         }
         sm.pF[lane] = f;
     }
-    __syncthreads();  // the cost tables and layer 2
+    __syncthreads();  // layer 2
     double (*xb)[kSB] = reinterpret_cast<double (*)[kSB]>(&sm.sF[0][0]);
     int32_t cg = 0;  // chunks published
     for (int32_t i0 = 3; i0 <= a.I; i0 += LG) {
-        double best[LW];
-        load_running<LW>(a, jj, i0 + wave * LW, best);
 #pragma unroll 1
-        for (int c = 0; c < kTileWaves; c++) {
-            const int32_t ic = i0 + c * LW;  // the chunk's first layer
+        for (int ch = 0; ch < kTileWaves; ch++) {
+            const int32_t ic = i0 + ch * LW;  // the chunk's first layer
             if (ic > a.I) break;
-            // the blocks not yet added, for the chunk's layers: partial minima
-            // over this wavefront's 16 predecessors of each, merged once
-            double pa[LW];
+            if (b - 1 >= t || nh > 0)
+                wait_flags(a, b - 1 >= t ? b - 1 : -1, help_counter(a, b, 0), nh, cg + 1);
+            // the holder's running minima of the chunk's layers and the
+            // helpers' partial minima
+            double best[LW];
 #pragma unroll
-            for (int l = 0; l < LW; l++) pa[l] = __builtin_huge_val();
-            // up to kStage blocks u0..u0+n-1 staged together (F_{i-1} for the
-            // chunk's layers), then their candidates
-            auto add_blocks = [&](int64_t u0, int n) {
-                __syncthreads();  // the staging buffer is free
-                for (int x = threadIdx.x; x < kSB * LW * n; x += blockDim.x) {
-                    const int kk = x % kSB, l = (x / kSB) % LW, u = x / (kSB * LW);
-                    const int32_t i = ic + l;
-                    sm.sF[kk][u * LW + l] =
-                        i <= a.I ? a.F[(int64_t)(i - 1) * a.ld + (u0 + u) * kSB + kk]
-                                 : __builtin_huge_val();
+            for (int l = 0; l < LW; l++)
+                best[l] = wave == ch && ic + l <= a.I ? a.F[(int64_t)(ic + l) * a.ld + jj]
+                                                     : __builtin_huge_val();
+            if (wave == ch) {
+                for (int h = 0; h < nh; h++) {
+                    const double* P = help_partials(a, m, h) + (int64_t)(ic - 3) * kSB + lane;
+#pragma unroll
+                    for (int l = 0; l < LW; l++) best[l] = __builtin_fmin(best[l], P[l * kSB]);
                 }
-                __syncthreads();
-                for (int u = 0; u < n; u++) {
-                    const double* Qc = QD + (u0 + u - kpd + 1) * kQTab + lane;
-#pragma unroll
-                    for (int q = 0; q < KW; q += 2) {
-                        const int kk = wave * KW + q;
-                        const double Q0 = Qc[kk * kSB], Q1 = Qc[(kk + 1) * kSB];
-#pragma unroll
-                        for (int l = 0; l < LW; l++) {
-                            pa[l] = __builtin_fmin(pa[l], sm.sF[kk][u * LW + l] + Q0);
-                            pa[l] = __builtin_fmin(pa[l], sm.sF[kk + 1][u * LW + l] + Q1);
-                        }
-                    }
-                }
-            };
-            // blocks kpd..b-2 first (their chunk is final once block b-2's
-            // is), then block b-1, the one the chain waits for
-            if (b - 2 >= t) wait_flag(a, b - 2, cg + 1);
-            for (int64_t u0 = kpd; u0 < b - 1; u0 += kStage)
-                add_blocks(u0, (int)min<int64_t>(kStage, b - 1 - u0));
+            }
             if (b > kpd) {
-                if (b - 1 >= t) wait_flag(a, b - 1, cg + 1);
-                add_blocks(b - 1, 1);
+                // block b-1 for the chunk's layers
+                __syncthreads();  // the staging buffer is free
+                stage_chunk<LG, LW, 1>(a, b - 1, 1, ic, sm.sF);
+                __syncthreads();
+                double pa[LW];
+#pragma unroll
+                for (int l = 0; l < LW; l++) pa[l] = __builtin_huge_val();
+#pragma unroll
+                for (int q = 0; q < KW; q++) {
+                    const int kk = wave * KW + q;
+#pragma unroll
+                    for (int l = 0; l < LW; l++)
+                        pa[l] = __builtin_fmin(pa[l], sm.sF[kk][l] + qP[q]);
+                }
                 __syncthreads();  // the staging buffer is free: 4 x LW rows of 64
 #pragma unroll
                 for (int l = 0; l < LW; l++) xb[wave * LW + l][lane] = pa[l];
                 __syncthreads();
-                if (wave == c) {
+                if (wave == ch) {
 #pragma unroll
                     for (int l = 0; l < LW; l++)
                         best[l] = __builtin_fmin(
@@ -518,12 +691,7 @@ __device__ void diag_block(const SweepArgs& a, int64_t t, int32_t m, StepSmem<LG
                 }
                 __syncthreads();
             }
-            // the chunk's layers inside the block, in order, with the cost of
-            // (k, j) for this wavefront's 16 predecessors k < j of the block
-            // (+inf for the others, so their candidates are +inf)
-            double cQ[KW];
-#pragma unroll
-            for (int q = 0; q < KW; q++) cQ[q] = QD[(wave * KW + q) * kSB + lane];
+            // the chunk's layers inside the block, in order
 #pragma unroll
             for (int q8 = 0; q8 < LW; q8++) {
                 const int32_t i = ic + q8;
@@ -541,7 +709,7 @@ __device__ void diag_block(const SweepArgs& a, int64_t t, int32_t m, StepSmem<LG
                 sm.partV[wave][lane] =
                     __builtin_fmin(__builtin_fmin(m4[0], m4[1]), __builtin_fmin(m4[2], m4[3]));
                 __syncthreads();
-                if (wave == c) {
+                if (wave == ch) {
                     const double v =
                         __builtin_fmin(__builtin_fmin(sm.partV[0][lane], sm.partV[1][lane]),
                                        __builtin_fmin(sm.partV[2][lane], sm.partV[3][lane]));
@@ -559,53 +727,47 @@ __device__ void diag_block(const SweepArgs& a, int64_t t, int32_t m, StepSmem<LG
 }
 
 // One step of the sweep: workgroups 0..nb-1 make blocks t..t+nb-1 final (a
-// chain: each waits for the one before); the next nbn x ngroups take this
-// step's final blocks to the next step's diagonal blocks (near tiles: one
-// column block and layer group each, four wavefronts on it); the others
-// (far tiles, WG index g * nx + wg after them) take blocks tp..t-1 to the
-// column blocks after those.
+// chain: each waits for the one before, chunk by chunk), the next nb x
+// kHelpMax are their helpers (helper h of block t + m at nb + m kHelpMax + h),
+// and the others (tiles, WG index g * nx + wg after them) add blocks tp..t-1,
+// the last step's, to the column blocks after this step's.
 template <int LG, int NL>
 __global__ __launch_bounds__(kSB* kTileWaves) ECASQ_STEP_ATTR void k_sweep_step(
-    SweepArgs a, int64_t t, int32_t nb, int32_t nbn, int64_t tp, int32_t sp, int64_t nx,
-    int32_t ngroups) {
+    SweepArgs a, int64_t t, int32_t nb, int64_t tp, int32_t sp, int64_t nx) {
     __shared__ StepSmem<LG> sm;
     if (!sweep_live(a)) return;  // uniform
     const int64_t J1 = t + nb;   // the first column block after the step's
-    const int64_t Jn = J1 + nbn;  // the first far column block
-    const int64_t nnear = (int64_t)nbn * ngroups;
-    // chunks per block (LG/4 layers each, those that hold a layer <= I)
-    const int32_t nch = (a.I - 2 + LG / kTileWaves - 1) / (LG / kTileWaves);
-    if ((int32_t)blockIdx.x < nb) {
+    const int32_t nh = nb * kHelpMax;
+    if ((int32_t)blockIdx.x < nb + nh) {
         // the diagonal chain is the step's critical path: let its waves issue
         // ahead of tile waves that share its SIMDs
         __builtin_amdgcn_s_setprio(3);
         load_log2_table(sm.tab);
-        diag_block<LG, NL>(a, t, (int32_t)blockIdx.x, sm);
-    } else if ((int64_t)blockIdx.x < nb + nnear) {
-        // the next step's chain waits for these
-        __builtin_amdgcn_s_setprio(2);
-        const int64_t x = (int64_t)blockIdx.x - nb;
-        tile_role<LG, NL, 4>(a, t, tp, t + nb - 1, J1 + x % nbn, J1, (int32_t)(x / nbn), nch,
-                             sm);
+        if ((int32_t)blockIdx.x < nb) {
+            diag_block<LG, NL>(a, t, tp, (int32_t)blockIdx.x, sm);
+        } else {
+            const int32_t x = (int32_t)blockIdx.x - nb;
+            helper_block<LG, NL>(a, t, tp, x / kHelpMax, x % kHelpMax, sm);
+        }
     } else {
-        const int64_t x = (int64_t)blockIdx.x - nb - nnear;
+        const int64_t x = (int64_t)blockIdx.x - nb - nh;
         const int64_t wg = x % nx;
         const int32_t g = (int32_t)(x / nx);
         const int64_t per = kTileWaves / sp;
 #if ECASQ_SWEEP_XCD
-        // fixed groups of `per` column blocks, group q on the q - q0'th far
+        // fixed groups of `per` column blocks, group q on the q - q0'th tile
         // workgroup, q0 a multiple of 8: a group keeps its XCD from launch to
-        // launch while the diagonal and near workgroups before them are as many
+        // launch while the chain's workgroups before them are as many
         const int64_t Jw = (((J1 / per) & ~(int64_t)7) + wg) * per;
 #else
-        const int64_t Jw = Jn + wg * per;
+        const int64_t Jw = J1 + wg * per;
 #endif
         if (sp == 4)
-            tile_role<LG, NL, 4>(a, t, tp, t, Jw, Jn, g, nch, sm);
+            tile_role<LG, NL, 4>(a, t, tp, Jw, J1, g, sm);
         else if (sp == 2)
-            tile_role<LG, NL, 2>(a, t, tp, t, Jw, Jn, g, nch, sm);
+            tile_role<LG, NL, 2>(a, t, tp, Jw, J1, g, sm);
         else
-            tile_role<LG, NL, 1>(a, t, tp, t, Jw, Jn, g, nch, sm);
+            tile_role<LG, NL, 1>(a, t, tp, Jw, J1, g, sm);
     }
 }
 
@@ -835,27 +997,25 @@ hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
         k_sweep_fill<<<(unsigned)g, 256, 0, st>>>(a);
     }
     // a step makes blocks t..t+nb-1 final; blocks tp..t-1 (the last step's)
-    // are final and not yet added to the column blocks after t + nb
+    // are final and not yet added to the column blocks after t - 1
     int64_t tp = 0;
     for (int64_t t = 0; t < a.nblk;) {
         const int32_t nb = step_blocks(t, a.nblk);
-        const int32_t nbn = t + nb < a.nblk ? step_blocks(t + nb, a.nblk) : 0;
         const int64_t ntiles = ngroups > 0 ? a.nblk - t - nb : 0;
         const int64_t tiles = ntiles * ngroups;
         const int32_t sp = tiles < ECASQ_SWEEP_SP4_BELOW ? 4 : tiles < ECASQ_SWEEP_SP2_BELOW ? 2 : 1;
         const int64_t per = kTileWaves / sp;  // column blocks per workgroup
 #if ECASQ_SWEEP_XCD
-        // workgroups of fixed column-block groups (see tile_role), a multiple
-        // of 8 per layer group so that every group keeps its XCD
+        // workgroups of fixed column-block groups (see k_sweep_step), a
+        // multiple of 8 per layer group so that every group keeps its XCD
         const int64_t q0 = ((t + nb) / per) & ~(int64_t)7;
-        const int64_t nx = ntiles > 0 ? ((a.nblk - 1) / per - q0 + 1 + 7) / 8 * 8 : 0;
+        const int64_t nx = ntiles > 0 && tp < t ? ((a.nblk - 1) / per - q0 + 1 + 7) / 8 * 8 : 0;
 #else
-        const int64_t nx = (ntiles + per - 1) / per;
+        const int64_t nx = tp < t ? (ntiles + per - 1) / per : 0;
 #endif
-        const int64_t nnear = ngroups > 0 ? (int64_t)nbn * ngroups : 0;
-        const dim3 grid((unsigned)(nb + nnear + nx * ngroups)), block(kSB * kTileWaves);
-        k_sweep_step<LG, NL><<<grid, block, 0, st>>>(a, t, nb, nbn, tp, sp, nx > 0 ? nx : 1,
-                                                      ngroups);
+        const int64_t nh = (int64_t)nb * kHelpMax;
+        const dim3 grid((unsigned)(nb + nh + nx * ngroups)), block(kSB * kTileWaves);
+        k_sweep_step<LG, NL><<<grid, block, 0, st>>>(a, t, nb, tp, sp, nx > 0 ? nx : 1);
         tp = t;
         t += nb;
     }
@@ -880,7 +1040,7 @@ size_t sweep_table_bytes(int64_t d, int32_t s) {
     return (size_t)(s + 1) * (size_t)d * (sizeof(double) + sizeof(int32_t));
 }
 
-size_t sweep_cost_bytes() { return ECASQ_SWEEP_NB * (size_t)kQSlot * sizeof(double); }
+size_t sweep_cost_bytes() { return (size_t)kQAll * sizeof(double); }
 
 hipError_t launch_sweep(const SweepSolve& S, int32_t exact_s, double* out, int32_t* chain,
                         hipStream_t st) {
