@@ -646,10 +646,10 @@ __device__ void diag_block(const SweepArgs& a, int64_t t, int64_t tp, int32_t m,
         for (int ch = 0; ch < kTileWaves; ch++) {
             const int32_t ic = i0 + ch * LW;  // the chunk's first layer
             if (ic > a.I) break;
-            if (b - 1 >= t || nh > 0)
-                wait_flags(a, b - 1 >= t ? b - 1 : -1, help_counter(a, b, 0), nh, cg + 1);
-            // the holder's running minima of the chunk's layers and the
-            // helpers' partial minima
+            // the helpers' partial minima (usually ready before block b-1's
+            // chunk) and the holder's running minima of the chunk's layers,
+            // read while the chain waits for block b-1
+            if (nh > 0) wait_flags(a, -1, help_counter(a, b, 0), nh, cg + 1);
             double best[LW];
 #pragma unroll
             for (int l = 0; l < LW; l++)
@@ -662,6 +662,7 @@ __device__ void diag_block(const SweepArgs& a, int64_t t, int64_t tp, int32_t m,
                     for (int l = 0; l < LW; l++) best[l] = __builtin_fmin(best[l], P[l * kSB]);
                 }
             }
+            if (b - 1 >= t) wait_flag(a, b - 1, cg + 1);
             if (b > kpd) {
                 // block b-1 for the chunk's layers
                 __syncthreads();  // the staging buffer is free
