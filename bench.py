@@ -69,17 +69,17 @@ def flops_per_cell(nlam):
 # (profiles/k_dp_layer_pass8_weights_256k.md), scaled by a plain copy's
 # readings (FETCH x2.0, WRITE x1.0).  Valid only for the kernel sources they
 # were taken on: reported as null once those sources change.
-TRAFFIC_BYTES_PER_LAUNCH = 2.494e9
-TRAFFIC_SOURCES_SHA = "f3a631b21f5b78fb"
+TRAFFIC_BYTES_PER_LAUNCH = 2.489e9
+TRAFFIC_SOURCES_SHA = "6fe1af9a675358b4"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
-SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 5.651e7
-SWEEP_TRAFFIC_SHA = "a43c049ba354f64d"
+SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 1.032e8
+SWEEP_TRAFFIC_SHA = "1fbe9154786e4ecd"
 # hardware counters of the same profile: SQ_INSTS_VALU_FLOPS_FP64 per solve over
 # the seconds per solve, and the share of VALU issue slots used
-SWEEP_COUNTER_FP64_TFLOPS = 15.0
-SWEEP_COUNTER_VALU_BUSY = 0.50
+SWEEP_COUNTER_FP64_TFLOPS = 18.3
+SWEEP_COUNTER_VALU_BUSY = 0.595
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the (workload, s) both traffic figures were measured on; null for others
 TRAFFIC_WORKLOAD = ("weights_256k", 32)
