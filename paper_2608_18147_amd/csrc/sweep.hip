@@ -455,6 +455,17 @@ __device__ void tile_role(const SweepArgs& a, int64_t t, int64_t tp, int64_t Jw,
     load_log2_table(sm.tab);
     for (int64_t pb = tp; pb < t; pb++) {
         if (pb > tp) __syncthreads();  // every wavefront is done with the last block
+        // issue priority 2, 1, 0 over the thirds of the blocks: a SIMD's tile
+        // wavefronts otherwise finish one after another (the oldest is issued
+        // first) and the last runs alone at a fraction of the issue rate; the
+        // chain keeps priority 3
+        const int64_t third = (3 * (pb - tp)) / (t - tp);
+        if (third == 0)
+            __builtin_amdgcn_s_setprio(2);
+        else if (third == 1)
+            __builtin_amdgcn_s_setprio(1);
+        else
+            __builtin_amdgcn_s_setprio(0);
         stage_pred<LG>(a, pb * kSB, i0, sm);
         __syncthreads();
         if (live)
