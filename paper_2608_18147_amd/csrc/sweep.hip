@@ -136,6 +136,11 @@ __device__ __forceinline__ bool sweep_live(SweepArgs& a) {
     return true;
 }
 
+// Row padding of the staging buffer: the staging stores of a wavefront
+// (one row each, the same column) fall in 8 banks instead of one, and rows
+// stay 16-byte aligned for the two-value broadcast reads.
+constexpr int kSFPad = 2;
+
 // Stage predecessor block [k0, k0+64): v, N, S, S2 and F_{i-1} for the LG
 // layers i0..i0+LG-1 (+inf past I).  All kThreads threads of the workgroup
 // take part; each issues all its loads before it stores any to LDS.
@@ -143,7 +148,7 @@ constexpr int kThreads = kSB * kTileWaves;
 template <int LG>
 __device__ __forceinline__ void stage_block(const SweepArgs& a, int64_t k0, int32_t i0, double* sv,
                                             double* sN, double* sS, double* sS2,
-                                            double (*sF)[LG]) {
+                                            double (*sF)[LG + kSFPad]) {
     // block [k0, k0+64) lies below a later block, so k0 + 63 < p
     constexpr int R = kSB * LG / kThreads;  // F values per thread
     static_assert(R * kThreads == kSB * LG, "a layer group of 64 columns fills the workgroup");
@@ -174,7 +179,7 @@ __device__ __forceinline__ void stage_block(const SweepArgs& a, int64_t k0, int3
 // issue their loads before their stores.
 template <int LG, int LW, int NU>
 __device__ __forceinline__ void stage_chunk(const SweepArgs& a, int64_t u0, int n, int32_t ic,
-                                            double (*sF)[LG]) {
+                                            double (*sF)[LG + kSFPad]) {
     constexpr int R = (kSB * LW + kThreads - 1) / kThreads;  // values per thread and block
     double f[NU][R];
 #pragma unroll
@@ -221,7 +226,7 @@ struct StepSmem {
     // v, N, S, S2 of two blocks: a tile's staged predecessor block in [0],
     // the chain roles' two blocks in [0] and [1]
     double hv[2][kSB], hN[2][kSB], hS[2][kSB], hS2[2][kSB];
-    double sF[kSB][LG];  // F_{i-1} of the staged block for one layer group
+    double sF[kSB][LG + kSFPad];  // F_{i-1} of the staged block for one layer group
     double pF[kSB];                               // previous layer of block t
     double partV[kTileWaves][kSB];                // per-wave partial minima
 };
@@ -796,7 +801,7 @@ __global__ void k_sweep_pick(SweepArgs a, int32_t exact_s, double* out, int32_t*
     const int64_t p = a.H.p;
     if (a.K[a.nblk] != 0) {
         st[0] = 0;
-        out[0] = __builtin_nan("");
+        out[0] = __builtin_huge_val();
         return;
     }
     int32_t bi = 2;
