@@ -18,6 +18,8 @@
 // masked lanes.
 #include <hip/hip_fp16.h>
 
+#include <initializer_list>
+
 #include "../../include/ecasq.h"
 #include "chain.hpp"
 #include "device.hpp"
@@ -38,14 +40,17 @@ __device__ __forceinline__ void wave_sync() {
 }
 
 struct RowLayout {
-    uint32_t keys, v, N, S, S2, F0, F1, last, bp0, bp1, chain, nu, misc, total;
+    uint32_t keys, v, N, S, S2, F0, F1, last, bp0, bp1, chain, nu, misc, srch, total;
 };
 
 __host__ __device__ inline uint32_t up16(uint32_t b) { return (b + 15u) & ~15u; }
 
-// LDS bytes of one row: dpad keys, 6 fp64 arrays of dpad, s+1 last-column
-// values, two (s+1) x dpad int16 argmin tables, two int32 chains, scalars.
-__host__ __device__ inline RowLayout row_layout(int dpad, int s) {
+// LDS bytes of one row: dpad keys, 4 fp64 arrays of dpad (v, N, S, S2), s+1
+// last-column values, two int32 chains, scalars and the search state; the
+// layer-by-layer solver (sweep = false) adds two fp64 layer buffers of dpad
+// and two (s+1) x dpad int16 argmin tables, the sweep keeps only a chain of
+// s+1 in each of the two.
+__host__ __device__ inline RowLayout row_layout(int dpad, int s, bool sweep) {
     RowLayout L;
     uint32_t o = 0;
     auto take = [&](uint32_t b) {
@@ -58,14 +63,15 @@ __host__ __device__ inline RowLayout row_layout(int dpad, int s) {
     L.N = take(8u * dpad);
     L.S = take(8u * dpad);
     L.S2 = take(8u * dpad);
-    L.F0 = take(8u * dpad);
-    L.F1 = take(8u * dpad);
+    L.F0 = take(sweep ? 0u : 8u * dpad);
+    L.F1 = take(sweep ? 0u : 8u * dpad);
     L.last = take(8u * (s + 1));
-    L.bp0 = take(2u * (s + 1) * dpad);
-    L.bp1 = take(2u * (s + 1) * dpad);
+    L.bp0 = take(2u * (s + 1) * (sweep ? 1u : (uint32_t)dpad));
+    L.bp1 = take(2u * (s + 1) * (sweep ? 1u : (uint32_t)dpad));
     L.chain = take(4u * (s + 1));
     L.nu = take(4u * (s + 1));
     L.misc = take(64);
+    L.srch = take(256);  // RowSearch
     L.total = o;
     return L;
 }
@@ -97,6 +103,18 @@ struct Pt {
     double lam, H, M;
     int t, buf;  // buf: argmin buffer holding this solve (-1: closed form)
 };
+
+// The budget search of one row, kept in LDS between its solves (written by
+// lane 0): A = infeasible point of largest lambda, B = feasible point of
+// smallest lambda, L = point of lowest H(I,B), P = the pair's feasible end;
+// kind of the query in flight: 0 the first (lambda = 0), 1 the largest
+// multiplier, 2 a chord query.
+struct RowSearch {
+    Pt A, B, L, P;
+    double lam, lc, lamF;
+    int haveA, haveB, tried40, npass, closed, status, kind, done, buf;
+};
+static_assert(sizeof(RowSearch) <= 256, "RowSearch fits its LDS slot");
 
 __device__ __forceinline__ Hist row_hist(const Row& R) {
     Hist H;
@@ -473,6 +491,86 @@ __device__ int row_refine(Row& R, int t, double lamp, double b, int budget, int 
     return nrun;
 }
 
+__device__ __forceinline__ int uniform_i(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// File the point q of the query in flight (lane 0).
+__device__ void row_search_file(RowSearch* Sr, const Pt& q, double b) {
+    auto add = [&](const Pt& x) {
+        if (x.H > b) {
+            if (!Sr->haveA || x.lam > Sr->A.lam) Sr->A = x;
+            Sr->haveA = 1;
+        } else {
+            if (!Sr->haveB || x.lam < Sr->B.lam) Sr->B = x;
+            Sr->haveB = 1;
+        }
+        if (x.H < Sr->L.H) Sr->L = x;
+    };
+    if (Sr->kind == 0) {
+        Sr->L = q;
+        add(q);
+        Sr->npass = 1;
+    } else if (Sr->kind == 1) {
+        add(q);
+        Sr->tried40 = 1;
+        Sr->npass++;
+    } else {
+        Sr->npass++;
+        if ((q.H == Sr->A.H && q.M == Sr->A.M) || (q.H == Sr->P.H && q.M == Sr->P.M)) {
+            Sr->lamF = Sr->lc;
+            Sr->done = 1;
+        } else {
+            add(q);
+        }
+    }
+}
+
+// Decide the next query from the points filed so far, or end the search
+// (lane 0).
+__device__ void row_search_next(RowSearch* Sr, const Row& R, double b, int max_passes,
+                                const double2* __restrict__ tab) {
+    if (!Sr->haveA) {  // lambda = 0 is feasible
+        Sr->P = Sr->B;
+        Sr->lamF = Sr->P.lam;
+        Sr->done = 1;
+        return;
+    }
+    Sr->closed = 0;
+    if (Sr->haveB) {
+        Sr->P = Sr->B;
+    } else if (b >= 1.0) {
+        double C, P;
+        cell_at(row_hist(R), 0, R.p - 1, tab, C, P);
+        Sr->P.lam = __builtin_huge_val();
+        Sr->P.H = 0.0 - P;
+        Sr->P.M = (0.0 + C) / R.s2tot;
+        Sr->P.t = 2;
+        Sr->P.buf = -1;
+        Sr->closed = 1;
+    } else {
+        if (Sr->tried40 || Sr->npass >= max_passes) {
+            Sr->P = Sr->L;  // both solves so far still hold their argmins
+            Sr->status = ECASQ_EINFEASIBLE;
+            Sr->lamF = Sr->P.lam;
+            Sr->done = 1;
+            return;
+        }
+        Sr->kind = 1;
+        Sr->lam = 0x1p40;
+        Sr->buf = 1;
+        return;
+    }
+    const double lc = (Sr->P.M - Sr->A.M) / (Sr->A.H - Sr->P.H);
+    Sr->lc = lc;
+    Sr->lamF = Sr->closed ? lc : Sr->P.lam;
+    if (!(lc > 0.0) || Sr->npass >= max_passes) {
+        Sr->done = 1;
+        return;
+    }
+    Sr->kind = 2;
+    Sr->lam = lc;
+    Sr->buf = Sr->P.buf == 0 ? 1 : 0;
+}
+
 template <int DT>
 __device__ __forceinline__ uint32_t load_bits(const void* x, int64_t i) {
     if (DT == 0) return reinterpret_cast<const uint32_t*>(x)[i];
@@ -500,7 +598,7 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
     const int lane = threadIdx.x % kWave;
     const int64_t row = (int64_t)blockIdx.x * A.rows_per_block + wave;
     if (wave >= A.rows_per_block || row >= A.n) return;
-    const RowLayout L = row_layout(A.dpad, A.s);
+    const RowLayout L = row_layout(A.dpad, A.s, LG > 0);
     char* base = smem + sizeof(double2) * kLog2Size + (size_t)wave * L.total;
     uint32_t* keys = reinterpret_cast<uint32_t*>(base + L.keys);
     Row R;
@@ -597,71 +695,45 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
         // the budget search with one multiplier per pass (the schedule of the
         // single-vector path at width 1): A = infeasible point of largest
         // lambda, B = feasible point of smallest lambda, Lo = lowest H(I,B);
-        // first occurrence wins every tie
-        Pt Ap, Bf, Lo, Bp;
-        bool haveA = false, haveB = false, tried40 = false;
-        auto add = [&](const Pt& q) {
-            if (q.H > b) {
-                if (!haveA || q.lam > Ap.lam) Ap = q;
-                haveA = true;
-            } else {
-                if (!haveB || q.lam < Bf.lam) Bf = q;
-                haveB = true;
-            }
-            if (q.H < Lo.H) Lo = q;
-        };
-        Lo = solve_row<CMAX, LG>(R, 0.0, A.exact_s, 0);
-        add(Lo);
-        int npass = 1;
-        for (;;) {
-            if (!haveA) {  // lambda = 0 is feasible
-                Bp = Bf;
-                lamF = Bp.lam;
-                break;
-            }
-            bool closed = false;
-            if (haveB) {
-                Bp = Bf;
-            } else if (b >= 1.0) {
-                double C, P;
-                cell_at(row_hist(R), 0, p - 1, tab, C, P);
-                Bp.lam = __builtin_huge_val();
-                Bp.H = 0.0 - P;
-                Bp.M = (0.0 + C) / R.s2tot;
-                Bp.t = 2;
-                Bp.buf = -1;
-                closed = true;
-            } else {
-                if (tried40 || npass >= A.max_passes) {
-                    Bp = Lo;  // both solves so far still hold their argmins
-                    status = ECASQ_EINFEASIBLE;
-                    lamF = Bp.lam;
-                    break;
-                }
-                add(solve_row<CMAX, LG>(R, 0x1p40, A.exact_s, 1));
-                tried40 = true;
-                npass++;
-                continue;
-            }
-            const double lc = (Bp.M - Ap.M) / (Ap.H - Bp.H);
-            lamF = closed ? lc : Bp.lam;
-            if (!(lc > 0.0) || npass >= A.max_passes) break;
-            const Pt Cp = solve_row<CMAX, LG>(R, lc, A.exact_s, Bp.buf == 0 ? 1 : 0);
-            npass++;
-            if ((Cp.H == Ap.H && Cp.M == Ap.M) || (Cp.H == Bp.H && Cp.M == Bp.M)) {
-                lamF = lc;
-                break;
-            }
-            add(Cp);
-        }
-        passes = npass;
-        t = Bp.t;
+        // first occurrence wins every tie.  One solve site: lane 0 decides
+        // the next query from the state in LDS, every lane solves it, lane 0
+        // files the point.
+        RowSearch* Sr = reinterpret_cast<RowSearch*>(base + L.srch);
         if (lane == 0) {
-            if (t == 2 || Bp.buf < 0 || !__builtin_isfinite(Bp.lam)) {
+            Sr->haveA = Sr->haveB = Sr->tried40 = 0;
+            Sr->npass = 0;
+            Sr->closed = 0;
+            Sr->status = ECASQ_OK;
+            Sr->done = 0;
+            Sr->lamF = 0.0;
+            Sr->kind = 0;
+            Sr->lam = 0.0;
+            Sr->buf = 0;
+        }
+        wave_sync();
+        for (;;) {
+            if (lane == 0 && Sr->npass > 0) row_search_next(Sr, R, b, A.max_passes, tab);
+            wave_sync();
+            if (uniform_i(Sr->done)) break;
+            const double lam = uniform_d(Sr->lam);
+            const int qb = uniform_i(Sr->buf);
+            const Pt q = solve_row<CMAX, LG>(R, lam, A.exact_s, qb);
+            if (lane == 0) row_search_file(Sr, q, b);
+            wave_sync();
+            if (uniform_i(Sr->done)) break;
+        }
+        status = uniform_i(Sr->status);
+        lamF = uniform_d(Sr->lamF);
+        passes = uniform_i(Sr->npass);
+        t = uniform_i(Sr->P.t);
+        const int pbuf = uniform_i(Sr->P.buf);
+        const double plam = uniform_d(Sr->P.lam);
+        if (lane == 0) {
+            if (t == 2 || pbuf < 0 || !__builtin_isfinite(plam)) {
                 R.chain[0] = 0;
                 R.chain[1] = p - 1;
             } else {
-                const int16_t* kept = R.bp[Bp.buf];
+                const int16_t* kept = R.bp[pbuf];
                 for (int r = 0; r < t; r++) R.chain[r] = kept[r];
             }
         }
@@ -710,9 +782,34 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
     }
 }
 
+// The (CMAX, LG) instantiation of k_batched for rows of dpad padded entries
+// and s values: the sweep while CMAX x LG register states per lane stay
+// within 32 (LG the recursive layers rounded up to 8, 14, 16 or 32), else
+// layer by layer (LG = 0).
+void batched_config(int dpad, int s, int& cmax, int& lg) {
+    const int L = (s < dpad ? s : dpad) - 2;  // recursive layers, at most
+    const int c = dpad / kWave;
+    auto pick = [&](int c0, std::initializer_list<int> lgs) {
+        for (int g : lgs)
+            if (g == 0 || L <= g) {
+                cmax = c0;
+                lg = g;
+                return;
+            }
+    };
+    if (c <= 1)
+        pick(1, {8, 14, 16, 32});
+    else if (c <= 2)
+        pick(2, {8, 14, 16, 0});
+    else if (c <= 4)
+        pick(4, {8, 0});
+    else
+        pick(8, {0});
+}
+
 template <int DT>
-hipError_t launch_dt(const BatchArgs& A, int cmax, unsigned grid, unsigned threads, size_t lds,
-                     hipStream_t st) {
+hipError_t launch_dt(const BatchArgs& A, int cmax, int lg, unsigned grid, unsigned threads,
+                     size_t lds, hipStream_t st) {
     hipError_t e = hipSuccess;
 #define ECASQ_LAUNCH(C, G)                                                                  \
     do {                                                                                     \
@@ -722,20 +819,20 @@ hipError_t launch_dt(const BatchArgs& A, int cmax, unsigned grid, unsigned threa
         k_batched<DT, C, G><<<grid, threads, lds, st>>>(A);                                  \
         return hipGetLastError();                                                            \
     } while (0)
-    // the sweep while CMAX x LG register states per lane stay within 32
-    const int L = (A.s < A.dpad ? A.s : A.dpad) - 2;  // recursive layers, at most
-    if (cmax <= 1) {
-        if (L <= 8) ECASQ_LAUNCH(1, 8);
-        if (L <= 16) ECASQ_LAUNCH(1, 16);
+    if (cmax == 1) {
+        if (lg == 8) ECASQ_LAUNCH(1, 8);
+        if (lg == 14) ECASQ_LAUNCH(1, 14);
+        if (lg == 16) ECASQ_LAUNCH(1, 16);
         ECASQ_LAUNCH(1, 32);
     }
-    if (cmax <= 2) {
-        if (L <= 8) ECASQ_LAUNCH(2, 8);
-        if (L <= 16) ECASQ_LAUNCH(2, 16);
+    if (cmax == 2) {
+        if (lg == 8) ECASQ_LAUNCH(2, 8);
+        if (lg == 14) ECASQ_LAUNCH(2, 14);
+        if (lg == 16) ECASQ_LAUNCH(2, 16);
         ECASQ_LAUNCH(2, 0);
     }
-    if (cmax <= 4) {
-        if (L <= 8) ECASQ_LAUNCH(4, 8);
+    if (cmax == 4) {
+        if (lg == 8) ECASQ_LAUNCH(4, 8);
         ECASQ_LAUNCH(4, 0);
     }
     ECASQ_LAUNCH(8, 0);
@@ -750,7 +847,9 @@ hipError_t launch_batched(const void* x, int dt, int64_t n, int32_t d, int32_t s
                           hipStream_t st) {
     int dpad = kWave;
     while (dpad < d) dpad <<= 1;
-    const RowLayout L = row_layout(dpad, s);
+    int cmax = 0, lg = 0;
+    batched_config(dpad, s, cmax, lg);
+    const RowLayout L = row_layout(dpad, s, lg > 0);
     // rows per workgroup: as many as fit next to the table in 128 KB of LDS
     const size_t table = sizeof(double2) * kLog2Size;
     int rows = (int)((128 * 1024 - table) / L.total);
@@ -774,10 +873,9 @@ hipError_t launch_batched(const void* x, int dt, int64_t n, int32_t d, int32_t s
     const size_t lds = table + (size_t)rows * L.total;
     const unsigned grid = (unsigned)((n + rows - 1) / rows);
     const unsigned threads = (unsigned)(rows * kWave);
-    const int cmax = dpad / kWave;
-    if (dt == 0) return launch_dt<0>(A, cmax, grid, threads, lds, st);
-    if (dt == 1) return launch_dt<1>(A, cmax, grid, threads, lds, st);
-    return launch_dt<2>(A, cmax, grid, threads, lds, st);
+    if (dt == 0) return launch_dt<0>(A, cmax, lg, grid, threads, lds, st);
+    if (dt == 1) return launch_dt<1>(A, cmax, lg, grid, threads, lds, st);
+    return launch_dt<2>(A, cmax, lg, grid, threads, lds, st);
 }
 
 }  // namespace ecasq
