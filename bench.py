@@ -74,12 +74,12 @@ TRAFFIC_SOURCES_SHA = "6fe1af9a675358b4"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
-SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 1.032e8
-SWEEP_TRAFFIC_SHA = "1fbe9154786e4ecd"
+SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 1.056e8
+SWEEP_TRAFFIC_SHA = "bd25d68065edd0b7"
 # hardware counters of the same profile: SQ_INSTS_VALU_FLOPS_FP64 per solve over
 # the seconds per solve, and the share of VALU issue slots used
-SWEEP_COUNTER_FP64_TFLOPS = 18.3
-SWEEP_COUNTER_VALU_BUSY = 0.595
+SWEEP_COUNTER_FP64_TFLOPS = 21.2
+SWEEP_COUNTER_VALU_BUSY = 0.691
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the (workload, s) both traffic figures were measured on; null for others
 TRAFFIC_WORKLOAD = ("weights_256k", 32)
