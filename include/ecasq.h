@@ -444,11 +444,11 @@ int32_t ecasq_inspect_results(double *lams, int32_t *chains, int32_t cap);
  * search pass, 2 = a whole solve of DP schedule 1 (all its launches, from
  * the table fill to eq. apx_final, timed as one unit; cells counted as for
  * schedule 0), 3 = one layer of the optimal DP (cells = its (k, l, j)
- * candidates).  ecasq_timing_read returns, for one variant, the summed
- * milliseconds, the number of timed launches and the (column, predecessor)
- * cells those launches evaluated, each cell for every multiplier of its
- * launch (host pointers, any may be NULL); reset != 0 clears that variant's
- * totals.  on = 2 also prints one line per DP solve to stderr (multiplier,
+ * candidates), 4 = one launch of ecasq_solve_batched (cells not counted).
+ * ecasq_timing_read returns, for one variant, the summed milliseconds, the
+ * number of timed launches and the (column, predecessor) cells those launches
+ * evaluated, each cell for every multiplier of its launch (host pointers, any
+ * may be NULL); reset != 0 clears that variant's totals.  on = 2 also prints one line per DP solve to stderr (multiplier,
  * H(I,B), vNMSE, values, elapsed time), for long runs.  Not thread-safe.
  */
 void ecasq_timing_enable(int32_t on);

@@ -1518,10 +1518,13 @@ ecasq_status ecasq_solve_batched(const void* x, ecasq_dtype dt, int64_t n, int64
     const ecasq_options o = opts ? *opts : defaults();
     if (o.refine_rounds < 0 || o.max_search_passes < 1) return ECASQ_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
+    timing_begin(kTimingBatched, 0, st);
     HIP_TRY(launch_batched(x, dt, n, (int32_t)d, s, bits_per_entry, o.refine_rounds,
                            o.refine_exhaustive, o.exact_s, o.max_search_passes, codebooks, t_out,
                            infos_dev, st));
+    timing_end(st);
     HIP_TRY(hipStreamSynchronize(st));
+    timing_flush();
     return ECASQ_OK;
 }
 

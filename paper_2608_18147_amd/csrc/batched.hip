@@ -90,7 +90,8 @@ struct BatchArgs {
 struct Row {
     const double2* tab;
     double *v, *N, *S, *S2, *F0, *F1, *last;
-    int16_t* bp[2];
+    int16_t *bp0, *bp1;  // the two argmin buffers (selected, never indexed:
+                         // a dynamic index would put the struct in scratch)
     int32_t *chain, *nu;
     double* misc;  // scratch scalars shared by the lanes of the row
     int p, s, dpad, lane;
@@ -98,6 +99,10 @@ struct Row {
     int64_t cells;
     int32_t solves;
 };
+
+__device__ __forceinline__ int16_t* argmin_buf(const Row& R, int buf) {
+    return buf ? R.bp1 : R.bp0;
+}
 
 struct Pt {
     double lam, H, M;
@@ -116,6 +121,22 @@ struct RowSearch {
 };
 static_assert(sizeof(RowSearch) <= 256, "RowSearch fits its LDS slot");
 
+// Values every lane of the wavefront holds alike, moved to scalar registers
+// (the compiler cannot prove LDS loads or the wave index uniform).
+__device__ __forceinline__ int uniform_i(int x) { return __builtin_amdgcn_readfirstlane(x); }
+
+__device__ __forceinline__ double uniform_d(double x) {
+    const int lo = __builtin_amdgcn_readfirstlane(__double2loint(x));
+    const int hi = __builtin_amdgcn_readfirstlane(__double2hiint(x));
+    return __hiloint2double(hi, lo);
+}
+
+__device__ __forceinline__ double readlane_d(double x, int l) {
+    const int lo = __builtin_amdgcn_readlane(__double2loint(x), l);
+    const int hi = __builtin_amdgcn_readlane(__double2hiint(x), l);
+    return __hiloint2double(hi, lo);
+}
+
 __device__ __forceinline__ Hist row_hist(const Row& R) {
     Hist H;
     H.v = R.v;
@@ -129,40 +150,29 @@ __device__ __forceinline__ Hist row_hist(const Row& R) {
     return H;
 }
 
-__device__ __forceinline__ double uniform_d(double x) {
-    const int lo = __builtin_amdgcn_readfirstlane(__double2loint(x));
-    const int hi = __builtin_amdgcn_readfirstlane(__double2hiint(x));
-    return __hiloint2double(hi, lo);
-}
-
 // The solve's point from its chain u_0 .. u_{n-1} in R.nu: MSE and H(I,B)
 // summed in path order (the same additions as accumulating them along the
-// argmins); the chain is kept in the first entries of argmin buffer `buf`
-// (rows 0 and 1 of the table are never layers).
+// argmins); lane r evaluates the interval (u_r, u_{r+1}] (n <= s <= 32) and
+// the sums run over the lanes in order.  The chain is kept in the first entries of argmin
+// buffer `buf` (rows 0 and 1 of the table are never layers).
 __device__ Pt row_chain_point(Row& R, double lam, int n, int buf) {
     const int lane = R.lane;
     const Hist H = row_hist(R);
-    if (lane == 0) {
-        const int32_t* u = R.nu;
-        double mse = 0.0, ph = 0.0;
-        for (int r = 0; r + 1 < n; r++) {
-            double C, P;
-            cell_at(H, u[r], u[r + 1], R.tab, C, P);
-            mse = mse + C;
-            ph = ph - P;
-        }
-        for (int r = 0; r < n; r++) R.bp[buf][r] = (int16_t)u[r];
-        R.misc[0] = mse;
-        R.misc[1] = ph;
-        R.misc[2] = (double)n;
+    const int32_t* u = R.nu;
+    double C = 0.0, P = 0.0;
+    if (lane + 1 < n) cell_at(H, u[lane], u[lane + 1], R.tab, C, P);
+    double mse = 0.0, ph = 0.0;
+    for (int r = 0; r + 1 < n; r++) {
+        mse = mse + readlane_d(C, r);
+        ph = ph - readlane_d(P, r);
     }
-    wave_sync();
-    // the point is the same for every lane: keep it in scalar registers
+    int16_t* keep = argmin_buf(R, buf);
+    if (lane < n) keep[lane] = (int16_t)u[lane];
     Pt out;
     out.lam = lam;
-    out.M = uniform_d(R.misc[0]) / R.s2tot;
-    out.H = uniform_d(R.misc[1]);
-    out.t = (int)uniform_d(R.misc[2]);
+    out.M = uniform_d(mse) / R.s2tot;
+    out.H = uniform_d(ph);
+    out.t = n;
     out.buf = buf;
     R.solves++;
     wave_sync();
@@ -187,7 +197,7 @@ __device__ __forceinline__ int row_istar(const Row& R, int imax, int exact_s) {
 // eq. apx_final and the chain traced back through argmin buffer `buf`.
 __device__ Pt row_final(Row& R, double lam, int imax, int exact_s, int buf) {
     const int p = R.p, lane = R.lane, dp = R.dpad;
-    const int16_t* bp = R.bp[buf];
+    const int16_t* bp = argmin_buf(R, buf);
     if (lane == 0) {
         const int bi = row_istar(R, imax, exact_s);
         int32_t* u = R.nu;
@@ -202,12 +212,6 @@ __device__ Pt row_final(Row& R, double lam, int imax, int exact_s, int buf) {
     return row_chain_point(R, lam, n, buf);
 }
 
-__device__ __forceinline__ double readlane_d(double x, int l) {
-    const int lo = __builtin_amdgcn_readlane(__double2loint(x), l);
-    const int hi = __builtin_amdgcn_readlane(__double2hiint(x), l);
-    return __hiloint2double(hi, lo);
-}
-
 // The same solve as a sweep over predecessors k = 0..p-2 in increasing order
 // that updates every layer of every later column from each cell, so C and Phi
 // of a cell are evaluated once instead of once per layer.  Column k is final
@@ -216,9 +220,11 @@ __device__ __forceinline__ double readlane_d(double x, int l) {
 // of CMAX columns per lane live in registers, values only: the chain of the
 // chosen layer is traced back afterwards, each argmin recomputed for its one
 // column from the layer values the lanes still hold (lowest k among equal
-// candidates, as the DP's strict '<' in increasing k).
+// candidates, as the DP's strict '<' in increasing k).  At lambda = 0 every
+// candidate is F + C (cell_c), a uniform branch per cell.
 template <int CMAX, int LG>
 __device__ Pt row_sweep(Row& R, double lam, int exact_s, int buf) {
+    const bool zl = lam == 0.0;
     const double lamp = lam * R.s2tot;
     const int p = R.p, lane = R.lane;
     const int imax = R.s < p ? R.s : p;
@@ -257,14 +263,19 @@ __device__ Pt row_sweep(Row& R, double lam, int exact_s, int buf) {
             for (int l = 1; l < LG; l++) Fk[l] = readlane_d(best[ck][l - 1], kk);
             const double pv = R.v[k], pN = R.N[k], pS = R.S[k], pS2 = R.S2[k];
 #pragma unroll
-            for (int c = ck; c < CMAX; c++) {
-                if (c * kWave + kWave - 1 <= k) continue;  // whole segment at or below k
+            for (int c = ck; c < CMAX; c++) {  // (segment ck at kk = 63 takes nothing)
                 const int j = c * kWave + lane;
-                double C, P;
-                cell_terms(pv, pN, pS, pS2, cv[c], cN[c], cS[c], cS2[c], dd, false, 0.0, R.tab,
-                           C, P);
+                double Q;
+                if (zl) {
+                    Q = cell_c(pv, pN, pS, pS2, cv[c], cN[c], cS[c], cS2[c]);
+                } else {
+                    double C, P;
+                    cell_terms(pv, pN, pS, pS2, cv[c], cN[c], cS[c], cS2[c], dd, false, 0.0,
+                               R.tab, C, P);
+                    Q = __builtin_fma(-lamp, P, C);
+                }
                 // columns at or below k take nothing from it
-                const double Q = j > k ? __builtin_fma(-lamp, P, C) : __builtin_huge_val();
+                Q = j > k ? Q : __builtin_huge_val();
 #pragma unroll
                 for (int l = 0; l < LG; l++) best[c][l] = __builtin_fmin(best[c][l], Fk[l] + Q);
             }
@@ -285,7 +296,7 @@ __device__ Pt row_sweep(Row& R, double lam, int exact_s, int buf) {
         }
     }
     wave_sync();
-    const int bi = row_istar(R, imax, exact_s);
+    const int bi = uniform_i(row_istar(R, imax, exact_s));
     // traceback: layer i's argmin at the chain's column j from F_{i-1} (layer
     // i-1 = 3 + l held in best[.][l], layer 2 in f2), one (value, k) pair per
     // lane and column segment, then a butterfly over the wavefront
@@ -305,11 +316,17 @@ __device__ Pt row_sweep(Row& R, double lam, int exact_s, int buf) {
         for (int c = 0; c < CMAX; c++) {
             const int k = c * kWave + lane;
             if (k >= i - 2 && k < jc) {
-                double C, P;
-                cell_terms(R.v[k], R.N[k], R.S[k], R.S2[k], jv, jN, jS, jS2, dd, false, 0.0,
-                           R.tab, C, P);
+                double Q;
+                if (zl) {
+                    Q = cell_c(R.v[k], R.N[k], R.S[k], R.S2[k], jv, jN, jS, jS2);
+                } else {
+                    double C, P;
+                    cell_terms(R.v[k], R.N[k], R.S[k], R.S2[k], jv, jN, jS, jS2, dd, false, 0.0,
+                               R.tab, C, P);
+                    Q = __builtin_fma(-lamp, P, C);
+                }
                 const double F = l >= 0 ? best[c][l >= 0 ? l : 0] : f2[c];
-                const double cand = F + __builtin_fma(-lamp, P, C);
+                const double cand = F + Q;
                 if (cand < bv) {
                     bv = cand;
                     bk = k;
@@ -343,7 +360,7 @@ __device__ Pt row_solve(Row& R, double lam, int exact_s, int buf) {
     const double lamp = lam * R.s2tot;
     const int p = R.p, lane = R.lane, dp = R.dpad;
     const int imax = R.s < p ? R.s : p;
-    int16_t* bp = R.bp[buf];
+    int16_t* bp = argmin_buf(R, buf);
     const Hist H = row_hist(R);
     for (int j = 1 + lane; j < p; j += kWave) {
         double C, P;
@@ -491,8 +508,6 @@ __device__ int row_refine(Row& R, int t, double lamp, double b, int budget, int 
     return nrun;
 }
 
-__device__ __forceinline__ int uniform_i(int x) { return __builtin_amdgcn_readfirstlane(x); }
-
 // File the point q of the query in flight (lane 0).
 __device__ void row_search_file(RowSearch* Sr, const Pt& q, double b) {
     auto add = [&](const Pt& x) {
@@ -571,6 +586,74 @@ __device__ void row_search_next(RowSearch* Sr, const Row& R, double b, int max_p
     Sr->buf = Sr->P.buf == 0 ? 1 : 0;
 }
 
+// The unique values of the sorted keys with their counts and exact prefix
+// sums (Sec. 2 histogram, App. D prefix sums), one wavefront: lane l takes the
+// entries [l E, (l+1) E) in order; its wide sums are combined by an exclusive
+// scan over the wavefront (Hillis-Steele, a limb-wise carry add per step),
+// then each lane walks its entries from the sum of those before it and writes
+// every last occurrence of a value at its rank among the unique values, the
+// sums rounded once.  Returns p.
+__device__ int row_histogram(Row& R, const uint32_t* keys, int d, int E) {
+    const int lane = R.lane;
+    const int i0 = lane * E;
+    uint64_t s[kSL] = {0}, q[kS2L] = {0};
+    int nlast = 0;
+    for (int e = 0; e < E; e++) {
+        const int i = i0 + e;
+        if (i < d) {
+            const uint32_t k = keys[i];
+            accumulate(s, q, term_of(key_bits(k)));
+            nlast += (i == d - 1 || keys[i + 1] != k) ? 1 : 0;
+        }
+    }
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        uint64_t ts[kSL], tq[kS2L];
+#pragma unroll
+        for (int l = 0; l < kSL; l++) ts[l] = __shfl_up(s[l], off);
+#pragma unroll
+        for (int l = 0; l < kS2L; l++) tq[l] = __shfl_up(q[l], off);
+        const int tn = __shfl_up(nlast, off);
+        if (lane >= off) {
+            wide_add_full<kSL>(s, ts);
+            wide_add_full<kS2L>(q, tq);
+            nlast += tn;
+        }
+    }
+    // inclusive -> exclusive: the sums of the lanes before this one (every
+    // lane takes part in the shuffle: a lane reading from an inactive one
+    // would not see its value)
+#pragma unroll
+    for (int l = 0; l < kSL; l++) {
+        const uint64_t t = __shfl_up(s[l], 1);
+        s[l] = lane ? t : 0ull;
+    }
+#pragma unroll
+    for (int l = 0; l < kS2L; l++) {
+        const uint64_t t = __shfl_up(q[l], 1);
+        q[l] = lane ? t : 0ull;
+    }
+    const int p = __builtin_amdgcn_readlane(nlast, kWave - 1);
+    int u = __shfl_up(nlast, 1);
+    if (lane == 0) u = 0;
+    for (int e = 0; e < E; e++) {
+        const int i = i0 + e;
+        if (i < d) {
+            const uint32_t k = keys[i];
+            const uint32_t bits = key_bits(k);
+            accumulate(s, q, term_of(bits));
+            if (i == d - 1 || keys[i + 1] != k) {
+                R.v[u] = (double)__uint_as_float(bits);
+                R.N[u] = (double)(i + 1);
+                R.S[u] = wide_to_double<kSL>(s, true, -149);
+                R.S2[u] = wide_to_double<kS2L>(q, false, -298);
+                u++;
+            }
+        }
+    }
+    return p;
+}
+
 template <int DT>
 __device__ __forceinline__ uint32_t load_bits(const void* x, int64_t i) {
     if (DT == 0) return reinterpret_cast<const uint32_t*>(x)[i];
@@ -588,18 +671,29 @@ __device__ __forceinline__ Pt solve_row(Row& R, double lam, int exact_s, int buf
         return row_solve<CMAX>(R, lam, exact_s, buf);
 }
 
+// Wavefronts per SIMD the register allocation must allow: four for the
+// register sweeps of up to 28 layer-column states per lane (a workgroup of
+// four rows then takes under a quarter of a CU's LDS), the compiler's choice
+// otherwise.
+template <int CMAX, int LG>
+constexpr int batched_min_waves() {
+    return (LG > 0 && CMAX * LG <= 28) ? 4 : 1;
+}
+
 template <int DT, int CMAX, int LG>
-__global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
+__global__ __launch_bounds__(256, (batched_min_waves<CMAX, LG>())) void k_batched(BatchArgs A) {
+    // the table at a fixed LDS address (a static array) so that the lookups
+    // fold it into their offsets; the rows in the dynamic part after it
+    __shared__ double2 tab[kLog2Size];
     extern __shared__ __align__(16) char smem[];
-    double2* tab = reinterpret_cast<double2*>(smem);
     load_log2_table(tab);
     __syncthreads();  // the only block-wide barrier: rows diverge from here on
-    const int wave = threadIdx.x / kWave;
+    const int wave = uniform_i(threadIdx.x / kWave);
     const int lane = threadIdx.x % kWave;
     const int64_t row = (int64_t)blockIdx.x * A.rows_per_block + wave;
     if (wave >= A.rows_per_block || row >= A.n) return;
     const RowLayout L = row_layout(A.dpad, A.s, LG > 0);
-    char* base = smem + sizeof(double2) * kLog2Size + (size_t)wave * L.total;
+    char* base = smem + (size_t)wave * L.total;
     uint32_t* keys = reinterpret_cast<uint32_t*>(base + L.keys);
     Row R;
     R.tab = tab;
@@ -610,8 +704,8 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
     R.F0 = reinterpret_cast<double*>(base + L.F0);
     R.F1 = reinterpret_cast<double*>(base + L.F1);
     R.last = reinterpret_cast<double*>(base + L.last);
-    R.bp[0] = reinterpret_cast<int16_t*>(base + L.bp0);
-    R.bp[1] = reinterpret_cast<int16_t*>(base + L.bp1);
+    R.bp0 = reinterpret_cast<int16_t*>(base + L.bp0);
+    R.bp1 = reinterpret_cast<int16_t*>(base + L.bp1);
     R.chain = reinterpret_cast<int32_t*>(base + L.chain);
     R.nu = reinterpret_cast<int32_t*>(base + L.nu);
     R.misc = reinterpret_cast<double*>(base + L.misc);
@@ -652,30 +746,12 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
             wave_sync();
         }
     }
-    // histogram + exact prefix sums (one lane; at most 512 entries)
-    if (lane == 0) {
-        uint64_t s[kSL] = {0}, q[kS2L] = {0};
-        int u = 0;
-        for (int i = 0; i < d; i++) {
-            const uint32_t k = keys[i];
-            const uint32_t bits = key_bits(k);
-            accumulate(s, q, term_of(bits));
-            if (i == d - 1 || keys[i + 1] != k) {
-                R.v[u] = (double)__uint_as_float(bits);
-                R.N[u] = (double)(i + 1);
-                R.S[u] = wide_to_double<kSL>(s, true, -149);
-                R.S2[u] = wide_to_double<kS2L>(q, false, -298);
-                u++;
-            }
-        }
-        R.misc[4] = (double)u;
-    }
+    R.p = uniform_i(row_histogram(R, keys, d, dpad / kWave));
     wave_sync();
-    R.p = (int)R.misc[4];
     R.dd = (double)d;
-    R.c0 = R.N[0];
+    R.c0 = uniform_d(R.N[0]);
     R.c0d = R.c0 / R.dd;
-    R.s2tot = R.S2[R.p - 1];
+    R.s2tot = uniform_d(R.S2[R.p - 1]);
     const int p = R.p;
     const double b = A.b;
 
@@ -733,7 +809,7 @@ __global__ __launch_bounds__(256) void k_batched(BatchArgs A) {
                 R.chain[0] = 0;
                 R.chain[1] = p - 1;
             } else {
-                const int16_t* kept = R.bp[pbuf];
+                const int16_t* kept = argmin_buf(R, pbuf);
                 for (int r = 0; r < t; r++) R.chain[r] = kept[r];
             }
         }
@@ -870,7 +946,7 @@ hipError_t launch_batched(const void* x, int dt, int64_t n, int32_t d, int32_t s
     A.codebooks = codebooks;
     A.t_out = t_out;
     A.infos = static_cast<ecasq_info*>(infos);
-    const size_t lds = table + (size_t)rows * L.total;
+    const size_t lds = (size_t)rows * L.total;  // the table is static
     const unsigned grid = (unsigned)((n + rows - 1) / rows);
     const unsigned threads = (unsigned)(rows * kWave);
     if (dt == 0) return launch_dt<0>(A, cmax, lg, grid, threads, lds, st);

@@ -138,6 +138,19 @@ __device__ __forceinline__ void cell_terms(double va, double Na, double Sa, doub
     P = __builtin_fma(mu, log2c(mu, tab), md * log2c(md, tab));
 }
 
+// C alone, by the operations cell_terms uses for it.  At lambda' = 0 the DP
+// candidate fma(-lambda', P, C) is C bit for bit: the product is a zero (P is
+// finite), and C is never -0 (v_b is never -0 and t_u > 0 when v_b = 0), so
+// a solve at lambda = 0 needs no entropy terms.
+__device__ __forceinline__ double cell_c(double va, double Na, double Sa, double S2a, double vb,
+                                         double Nb, double Sb, double S2b) {
+    const double n = Nb - Na;
+    const double sa = Sb - Sa;
+    const double s2 = S2b - S2a;
+    const double tu = __builtin_fma(-va, n, sa);
+    return __builtin_fma(vb, tu, __builtin_fma(va, sa, -s2));
+}
+
 // U and D of (v_a, v_b] in the refinement (inv) form.
 __device__ __forceinline__ void interval_ud(double va, double Na, double Sa, double vb, double Nb,
                                             double Sb, double& U, double& D) {

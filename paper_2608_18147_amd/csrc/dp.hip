@@ -441,7 +441,7 @@ bool g_timing = false;
 bool g_verbose = false;
 std::vector<TimedLaunch> g_pending;
 std::vector<hipEvent_t> g_pool;
-TimingTotals g_tot[4];
+TimingTotals g_tot[kTimingVariants];
 TimedLaunch g_open{nullptr, nullptr, 0, 0};
 
 hipEvent_t take_event() {
@@ -505,7 +505,7 @@ void timing_discard_last() {
 
 void timing_read(int variant, double* ms, int64_t* launches, int64_t* cells, bool reset) {
     timing_flush();
-    if (variant < 0 || variant > 3) {
+    if (variant < 0 || variant >= kTimingVariants) {
         if (ms) *ms = 0.0;
         if (launches) *launches = 0;
         if (cells) *cells = 0;

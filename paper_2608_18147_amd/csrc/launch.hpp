@@ -112,13 +112,15 @@ bool timing_verbose();
 void timing_flush();
 void timing_read(int variant, double* ms, int64_t* launches, int64_t* cells, bool reset);
 // bracket a span of launches on st as one timed unit of `variant` (2: a sweep
-// solve, 3: a layer of the optimal DP)
+// solve, 3: a layer of the optimal DP, 4: a batched launch)
 void timing_begin(int variant, int64_t cells, hipStream_t st);
 void timing_end(hipStream_t st);
 // drop the newest timed unit not yet flushed (a solve that was skipped)
 void timing_discard_last();
 bool timing_active();
 constexpr int kTimingOpt = 3;
+constexpr int kTimingBatched = 4;
+constexpr int kTimingVariants = 5;
 hipError_t launch_dp_layer(const DpLayer& L, hipStream_t st);
 hipError_t launch_dp_init_fwd(const Hist& H, int64_t lo, int64_t jl, int64_t jh,
                               const DpInit& I, hipStream_t st);

@@ -482,6 +482,7 @@ TIMING_SINGLE = 0  # one multiplier per DP layer launch
 TIMING_PASS = 1    # the 8 multipliers of a search pass per launch
 TIMING_SWEEP = 2   # one whole solve of DP schedule 1
 TIMING_OPT = 3     # one layer of the optimal DP
+TIMING_BATCHED = 4  # one launch of ecasq_solve_batched
 
 
 def ecasq_timing_read(variant=TIMING_PASS, reset=False):
