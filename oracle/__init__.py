@@ -12,7 +12,9 @@ Modules:
   philox     Philox4x32-10 in numpy
   log2_table correctly rounded table of the canonical log2 (mpmath)
 
-Parity status per function is recorded in the header of each module; the
-refinement heuristic is "parity unpinned" beyond the invariants its tests
-check (objective never increases; the three colour classes are separable).
+Every function is pinned to something other than itself (closed forms, brute
+force, the paper's worked examples, per-entry definitions in plain.py);
+tests/test_oracle_*.py hold the pins.  The refinement is the paper's
+heuristic procedure: what it computes is pinned step by step against the
+per-entry objective (tests/test_oracle_refine_pins.py).
 """
