@@ -265,12 +265,13 @@ ecasq_status ecasq_solve_timeshare(const void *x, ecasq_dtype dt, int64_t d, int
                                    double *alpha, ecasq_info *infos);
 
 /*
- * Time-shared final rounding (Sec. 7): entry i uses codebook1 iff the 53-bit
- * uniform of Philox4x32-10 with counter (i mod 2^32, i / 2^32, 1, 0) and key
- * (seed mod 2^32, seed / 2^32) is below alpha (shared randomness: a decoder
- * with the seed knows the partition), else codebook0, and is then rounded
- * exactly as ecasq_quantize rounds (counter word 2 = 0), its symbol indexing
- * its own codebook.  part: device, d bytes (1 = codebook1), may be NULL.
+ * Time-shared final rounding (Sec. 7): entry i uses codebook1 iff its 53-bit
+ * uniform from Philox4x32-10 with counter (j mod 2^32, j / 2^32, 1, 0), j =
+ * i / 2, and key (seed mod 2^32, seed / 2^32) is below alpha (words 0 and 1
+ * for even i, 2 and 3 for odd i, as in ecasq_quantize; shared randomness: a
+ * decoder with the seed knows the partition), else codebook0, and is then
+ * rounded exactly as ecasq_quantize rounds (counter word 2 = 0), its symbol
+ * indexing its own codebook.  part: device, d bytes (1 = codebook1), may be NULL.
  * The two parts are entropy-coded separately: *empirical_entropy (device) =
  * (n_0 H_0 + n_1 H_1) / d with each part's plug-in entropy over its own
  * entries; hist: device, t0 + t1 int64 counts (codebook0's first), may be NULL.
@@ -312,8 +313,11 @@ ecasq_status ecasq_decode(const uint8_t *in, int64_t in_bytes, int64_t d, int32_
  * Final stochastic rounding (Sec. 2): symbol i in [0, t) for every entry of x
  * in its original order.  The bracket is q_r < x <= q_{r+1} (x <= q_0 gives
  * r = 0; x > q_{t-1} is clamped to t-1); the entry rounds up iff
- * u < (x - q_r) / (q_{r+1} - q_r), where u is 53 bits of Philox4x32-10 with
- * counter (i mod 2^32, i / 2^32, 0, 0) and key (seed mod 2^32, seed / 2^32).
+ * u < (x - q_r) / (q_{r+1} - q_r) (IEEE fp64), where u = bits 2^-53 and bits
+ * = (w_hi 2^32 + w_lo) >> 11 for the output words of Philox4x32-10 with
+ * counter (j mod 2^32, j / 2^32, 0, 0), j = i / 2, and key (seed mod 2^32,
+ * seed / 2^32): words 0 (lo) and 1 (hi) for even i, 2 and 3 for odd i (one
+ * generator call serves two entries).
  * codebook: device, t ascending fp64 values, 1 <= t <= 256.  symbols: device,
  * d bytes.  empirical_entropy: device scalar, plug-in entropy of the symbol
  * histogram in bits/entry.  hist: device, t int64 counts, may be NULL.

@@ -190,92 +190,149 @@ __device__ __forceinline__ double load_x(const void* x, int64_t i) {
     return (double)__uint_as_float(bits);
 }
 
+// The rounding's codebook in LDS: the values q_0 .. q_{t-1}; in s, the
+// search's copy, q_0 .. q_{t-2} followed by +inf (so the search needs no
+// bound: no x is below +inf, and a bracket never starts at q_{t-1}); each
+// interval's width D_r = q_{r+1} - q_r and, where 1/D_r is a normal number,
+// R_r = RN(1/D_r) (NaN otherwise, which sends every entry of that interval to
+// the exact division).
+struct RoundBook {
+    double q[kMaxT], s[2 * kMaxT], D[kMaxT], R[kMaxT];
+};
+
+__device__ __forceinline__ void load_book(RoundBook& B, const double* __restrict__ cb, int32_t t) {
+    for (int r = threadIdx.x; r < kMaxT; r += blockDim.x) B.q[r] = r < t ? cb[r] : 0.0;
+    for (int r = threadIdx.x; r < 2 * kMaxT; r += blockDim.x)
+        B.s[r] = r <= t - 2 ? cb[r] : __builtin_huge_val();
+    __syncthreads();
+    for (int r = threadIdx.x; r + 1 < t; r += blockDim.x) {
+        const double D = B.q[r + 1] - B.q[r];
+        B.D[r] = D;
+        B.R[r] = (D >= 0x1p-1000 && D <= 0x1p+1000) ? 1.0 / D : __builtin_nan("");
+    }
+}
+
+__device__ __forceinline__ int32_t search_step(int32_t t) {
+    return t >= 3 ? (int32_t)(1u << (31 - __builtin_clz((uint32_t)(t - 2)))) : 0;
+}
+
+// Symbol of x under the codebook (t >= 2) and the 53-bit uniform u: the
+// bracket r (the largest r <= t-2 with q_r < x, else 0, by a search over
+// powers of two from the largest power h <= t-2: indices up to 2h - 1 <
+// 2 kMaxT), then up iff u < RN((x - q_r) / D_r).  The quotient is
+// first taken as RN(N R_r) (N = x - q_r): within 0.4 2^-50 of the exact RN
+// quotient, relative, for quotients in [2^-900, 2^900], so u below or above
+// it by more than 2^-50 (relative) decides the comparison, and N = +-0 means
+// a quotient of +-0, which u never is below.  Only u inside that band, or a
+// quotient outside that range (NaN included), takes the IEEE division.
+__device__ __forceinline__ uint32_t round_one(const RoundBook& B, int32_t h,
+                                              double xv, double u) {
+    int32_t lo = 0;
+    for (int32_t step = h; step > 0; step >>= 1) {
+        const int32_t m = lo + step;
+        lo = B.s[m] < xv ? m : lo;
+    }
+    const double N = xv - B.q[lo];
+    const double qa = N * B.R[lo];
+    const double aq = __builtin_fabs(qa);
+    const double m = aq * 0x1p-50;
+    bool up = u < qa - m;  // false when N = +-0 (qa is then +-0 or NaN)
+    const bool sure = N == 0.0 || (aq >= 0x1p-900 && aq <= 0x1p+900 && (up || u > qa + m));
+    if (!sure) up = u < N / B.D[lo];
+    return (uint32_t)lo + (up ? 1u : 0u);
+}
+
+__device__ __forceinline__ double uniform53(uint32_t lo, uint32_t hi) {
+    const uint64_t bits = ((((uint64_t)hi) << 32) | lo) >> 11;
+    return (double)bits * 0x1p-53;
+}
+
+// Final stochastic rounding (Sec. 2), two entries per thread: entries 2j and
+// 2j+1 take words (0, 1) and (2, 3) of Philox4x32-10 at counter (j_lo, j_hi,
+// 0, 0) with key (k0, k1).  Symbol counts gather in LDS per workgroup.
 template <int DT>
 __global__ __launch_bounds__(256) void k_quantize(const void* __restrict__ x, int64_t d,
                                                   const double* __restrict__ cb, int32_t t,
                                                   uint32_t k0, uint32_t k1,
                                                   uint8_t* __restrict__ symbols,
                                                   unsigned long long* __restrict__ hist) {
-    __shared__ double q[kMaxT];
+    __shared__ RoundBook B;
     __shared__ unsigned int lh[kMaxT];
-    for (int r = threadIdx.x; r < kMaxT; r += blockDim.x) {
-        q[r] = r < t ? cb[r] : 0.0;
-        lh[r] = 0u;
-    }
+    for (int r = threadIdx.x; r < kMaxT; r += blockDim.x) lh[r] = 0u;
+    load_book(B, cb, t);
     __syncthreads();
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < d;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        uint32_t sym = 0;
+    const int32_t h = search_step(t);
+    const int64_t npair = (d + 1) / 2;
+    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < npair;
+         j += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i0 = 2 * j;
+        const bool two = i0 + 1 < d;
+        uint32_t s0 = 0, s1 = 0;
         if (t > 1) {
-            const double xv = load_x<DT>(x, i);
-            int lo = 0, hi = t - 2;
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (q[mid] < xv) lo = mid;
-                else hi = mid - 1;
-            }
-            const double pu = (xv - q[lo]) / (q[lo + 1] - q[lo]);
-            uint32_t c[4] = {(uint32_t)i, (uint32_t)((uint64_t)i >> 32), 0u, 0u};
+            const double x0 = load_x<DT>(x, i0);
+            const double x1 = two ? load_x<DT>(x, i0 + 1) : 0.0;
+            uint32_t c[4] = {(uint32_t)j, (uint32_t)((uint64_t)j >> 32), 0u, 0u};
             philox4x32_10(c, k0, k1);
-            const uint64_t bits = ((((uint64_t)c[1]) << 32) | c[0]) >> 11;
-            const double uu = (double)bits * 0x1p-53;
-            sym = (uint32_t)lo + (uu < pu ? 1u : 0u);
+            s0 = round_one(B, h, x0, uniform53(c[0], c[1]));
+            s1 = round_one(B, h, x1, uniform53(c[2], c[3]));
         }
-        symbols[i] = (uint8_t)sym;
-        atomicAdd(&lh[sym], 1u);
+        symbols[i0] = (uint8_t)s0;
+        atomicAdd(&lh[s0], 1u);
+        if (two) {
+            symbols[i0 + 1] = (uint8_t)s1;
+            atomicAdd(&lh[s1], 1u);
+        }
     }
     __syncthreads();
     for (int r = threadIdx.x; r < t; r += blockDim.x)
         if (lh[r]) atomicAdd(&hist[r], (unsigned long long)lh[r]);
 }
 
-// Time-shared rounding (Sec. 7): entry i takes the second codebook iff the
-// 53-bit uniform of Philox counter (i_lo, i_hi, 1, 0) is below alpha, and is
-// then rounded with its codebook exactly as k_quantize rounds (counter
-// (i_lo, i_hi, 0, 0)).  hist: the first codebook's t0 counts, then the
-// second's t1; part[i] = 1 for the second.
+// Time-shared rounding (Sec. 7): entry i takes the second codebook iff its
+// partition uniform, from Philox counter (j_lo, j_hi, 1, 0) with j = i / 2
+// (words (0, 1) for even i, (2, 3) for odd), is below alpha, and is then
+// rounded with its codebook exactly as k_quantize rounds it (counter (j_lo,
+// j_hi, 0, 0)).  hist: the first codebook's t0 counts, then the second's t1;
+// part[i] = 1 for the second.
 template <int DT>
 __global__ __launch_bounds__(256) void k_quantize_ts(
     const void* __restrict__ x, int64_t d, const double* __restrict__ cb0, int32_t t0,
     const double* __restrict__ cb1, int32_t t1, double alpha, uint32_t k0, uint32_t k1,
     uint8_t* __restrict__ symbols, uint8_t* __restrict__ part,
     unsigned long long* __restrict__ hist) {
-    __shared__ double q[2][kMaxT];
+    __shared__ RoundBook B[2];
     __shared__ unsigned int lh[2][kMaxT];
     for (int r = threadIdx.x; r < kMaxT; r += blockDim.x) {
-        q[0][r] = r < t0 ? cb0[r] : 0.0;
-        q[1][r] = r < t1 ? cb1[r] : 0.0;
         lh[0][r] = 0u;
         lh[1][r] = 0u;
     }
+    load_book(B[0], cb0, t0);
+    load_book(B[1], cb1, t1);
     __syncthreads();
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < d;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        uint32_t c[4] = {(uint32_t)i, (uint32_t)((uint64_t)i >> 32), 1u, 0u};
+    const int32_t h0 = search_step(t0), h1 = search_step(t1);
+    const int64_t npair = (d + 1) / 2;
+    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < npair;
+         j += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t i0 = 2 * j;
+        const bool two = i0 + 1 < d;
+        uint32_t w[4] = {(uint32_t)j, (uint32_t)((uint64_t)j >> 32), 1u, 0u};
+        philox4x32_10(w, k0, k1);
+        uint32_t c[4] = {(uint32_t)j, (uint32_t)((uint64_t)j >> 32), 0u, 0u};
         philox4x32_10(c, k0, k1);
-        const uint64_t pbits = ((((uint64_t)c[1]) << 32) | c[0]) >> 11;
-        const int w = ((double)pbits * 0x1p-53) < alpha ? 1 : 0;
-        const int32_t t = w ? t1 : t0;
-        const double* qq = q[w];
-        uint32_t sym = 0;
-        if (t > 1) {
-            const double xv = load_x<DT>(x, i);
-            int lo = 0, hi = t - 2;
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (qq[mid] < xv) lo = mid;
-                else hi = mid - 1;
-            }
-            const double pu = (xv - qq[lo]) / (qq[lo + 1] - qq[lo]);
-            uint32_t e[4] = {(uint32_t)i, (uint32_t)((uint64_t)i >> 32), 0u, 0u};
-            philox4x32_10(e, k0, k1);
-            const uint64_t bits = ((((uint64_t)e[1]) << 32) | e[0]) >> 11;
-            const double uu = (double)bits * 0x1p-53;
-            sym = (uint32_t)lo + (uu < pu ? 1u : 0u);
+#pragma unroll
+        for (int e = 0; e < 2; e++) {
+            const int64_t i = i0 + e;
+            if (e == 1 && !two) break;
+            const int pw = uniform53(w[2 * e], w[2 * e + 1]) < alpha ? 1 : 0;
+            const int32_t t = pw ? t1 : t0;
+            uint32_t sym = 0;
+            if (t > 1)
+                sym = round_one(B[pw], pw ? h1 : h0, load_x<DT>(x, i),
+                                uniform53(c[2 * e], c[2 * e + 1]));
+            symbols[i] = (uint8_t)sym;
+            if (part) part[i] = (uint8_t)pw;
+            atomicAdd(&lh[pw][sym], 1u);
         }
-        symbols[i] = (uint8_t)sym;
-        if (part) part[i] = (uint8_t)w;
-        atomicAdd(&lh[w][sym], 1u);
     }
     __syncthreads();
     for (int r = threadIdx.x; r < t0; r += blockDim.x)
@@ -391,7 +448,7 @@ hipError_t launch_gather(const double* v, const int32_t* u, int32_t t, double* c
 hipError_t launch_quantize(const void* x, int dt, int64_t d, const double* codebook, int32_t t,
                            uint64_t seed, uint8_t* symbols, unsigned long long* hist,
                            hipStream_t st) {
-    int64_t g = (d + 255) / 256;
+    int64_t g = ((d + 1) / 2 + 255) / 256;  // a thread per pair of entries
     if (g > 4096) g = 4096;
     if (g < 1) g = 1;
     const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
@@ -414,7 +471,7 @@ hipError_t launch_quantize_ts(const void* x, int dt, int64_t d, const double* cb
                               const double* cb1, int32_t t1, double alpha, uint64_t seed,
                               uint8_t* symbols, uint8_t* part, unsigned long long* hist,
                               double* ent, int64_t* hist_out, hipStream_t st) {
-    int64_t g = (d + 255) / 256;
+    int64_t g = ((d + 1) / 2 + 255) / 256;  // a thread per pair of entries
     if (g > 4096) g = 4096;
     if (g < 1) g = 1;
     const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);

@@ -787,6 +787,35 @@ def test_uniforms_are_uniform():
     assert chi2 < 100  # 49 dof, p ~ 1e-5
 
 
+def test_uniforms_stream_layout():
+    """Entries 2j and 2j+1 take words (0, 1) and (2, 3) of the generator at
+    counter (j, 0, stream, 0); an odd count ends on an even entry."""
+    seed = 0x1234_5678_9ABC_DEF0
+    for stream in (0, 1):
+        u = pipeline.uniforms(7, seed, stream)
+        assert len(u) == 7
+        for j in range(4):
+            a = [np.array([v], dtype=np.uint64) for v in (j, 0, stream, 0)]
+            w = [int(g[0]) for g in philox4x32_10(*a, np.array([seed & 0xFFFFFFFF], dtype=np.uint64),
+                                                  np.array([seed >> 32], dtype=np.uint64))]
+            for e in range(2):
+                if 2 * j + e < 7:
+                    bits = ((w[2 * e + 1] << 32) | w[2 * e]) >> 11
+                    assert u[2 * j + e] == bits * 2.0 ** -53
+
+
+def test_uniform_pairs_are_independent():
+    """The two entries that share a generator call are jointly uniform: a
+    10 x 10 chi-square on (u_2j, u_2j+1), and the two streams against each
+    other."""
+    n = 400000
+    for a, b in ((pipeline.uniforms(n, 99)[0::2], pipeline.uniforms(n, 99)[1::2]),
+                 (pipeline.uniforms(n, 99, 0), pipeline.uniforms(n, 99, 1))):
+        h, _, _ = np.histogram2d(a, b, bins=10, range=[[0, 1], [0, 1]])
+        e = len(a) / 100.0
+        assert ((h - e) ** 2 / e).sum() < 160  # 99 dof, p ~ 1e-4
+
+
 def test_quantize_is_unbiased():
     """E[xhat] = x for SQ (Sec. 2): mean over K seeds within 5 sigma per entry,
     and the empirical MSE matches sum (b-x)(x-a)."""
