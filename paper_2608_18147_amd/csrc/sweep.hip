@@ -904,6 +904,59 @@ __global__ __launch_bounds__(kTrT) void k_sweep_trace_pick(int32_t i, int32_t* _
     if (threadIdx.x == 0) st[kStChain + i - 2] = rk[0];
 }
 
+// The whole traceback in one workgroup, for small p: layer by layer from i*
+// down to 3, the lowest argmin of the chain column's candidates (the same
+// (value, k) pairs as the two kernels above, reduced lexicographically: a
+// butterfly per wavefront, then across the wavefronts in LDS), the next
+// column kept in LDS.  One launch instead of two per layer.
+constexpr int kTrOneT = 1024;
+constexpr int64_t kTrOneMaxP = 16384;  // at most 16 candidates per thread
+
+__global__ __launch_bounds__(kTrOneT) void k_sweep_trace_one(SweepArgs a, int32_t* __restrict__ st) {
+    __shared__ double2 tab[kLog2Size];
+    __shared__ double rv[kTrOneT / kSB];
+    __shared__ int32_t rk[kTrOneT / kSB];
+    __shared__ int32_t jn;
+    if (!sweep_live(a)) return;  // uniform
+    const int32_t n = st[0];
+    if (n < 3) return;  // uniform: no interior value, or a failed solve (0)
+    load_log2_table(tab);
+    if (threadIdx.x == 0) jn = st[kStChain + n - 1];
+    __syncthreads();
+    const int lane = threadIdx.x % kSB, wave = threadIdx.x / kSB;
+    for (int32_t i = n; i >= 3; i--) {
+        const int64_t j = jn;
+        const double* Fp = a.F + (int64_t)(i - 1) * a.ld;
+        double best = __builtin_huge_val();
+        int32_t bk = INT32_MAX;
+        for (int64_t k = (i - 2) + (int64_t)threadIdx.x; k < j; k += kTrOneT) {
+            double C, P;
+            cell_at(a.H, k, j, tab, C, P);
+            lexmin(best, bk, Fp[k] + __builtin_fma(-a.lamp, P, C), (int32_t)k);
+        }
+#pragma unroll
+        for (int off = kSB / 2; off > 0; off >>= 1)
+            lexmin(best, bk, __shfl_xor(best, off), __shfl_xor(bk, off));
+        if (lane == 0) {
+            rv[wave] = best;
+            rk[wave] = bk;
+        }
+        __syncthreads();
+        if (wave == 0) {
+            best = lane < kTrOneT / kSB ? rv[lane] : __builtin_huge_val();
+            bk = lane < kTrOneT / kSB ? rk[lane] : INT32_MAX;
+#pragma unroll
+            for (int off = kSB / 2; off > 0; off >>= 1)
+                lexmin(best, bk, __shfl_xor(best, off), __shfl_xor(bk, off));
+            if (lane == 0) {
+                st[kStChain + i - 2] = bk;
+                jn = bk;
+            }
+        }
+        __syncthreads();
+    }
+}
+
 // The chain's MSE and H(I,B) summed in path order.  One wavefront.
 // out: J (already written), MSE, H(I,B), i*.
 __global__ __launch_bounds__(kSB) void k_sweep_sums(SweepArgs a, const int32_t* __restrict__ st,
@@ -1075,13 +1128,17 @@ hipError_t launch_sweep(const SweepSolve& S, int32_t exact_s, double* out, int32
         e = sweep_launch<32>(a, st);
     if (e != hipSuccess) return e;
     k_sweep_pick<<<1, 64, 0, st>>>(a, exact_s, out, S.st);
-    // traceback: layers above i* return at once
-    const int32_t g = trace_groups(a.H.p);
-    double* pv = reinterpret_cast<double*>(S.K);
-    int32_t* pk = reinterpret_cast<int32_t*>(pv + g);
-    for (int32_t i = a.I; i >= 3; i--) {
-        k_sweep_trace_part<<<(unsigned)g, kTrT, 0, st>>>(a, i, S.st, pv, pk);
-        k_sweep_trace_pick<<<1, kTrT, 0, st>>>(i, S.st, pv, pk, g, S.runp);
+    // traceback: layers above i* return at once; small p in one launch
+    if (a.H.p <= kTrOneMaxP) {
+        k_sweep_trace_one<<<1, kTrOneT, 0, st>>>(a, S.st);
+    } else {
+        const int32_t g = trace_groups(a.H.p);
+        double* pv = reinterpret_cast<double*>(S.K);
+        int32_t* pk = reinterpret_cast<int32_t*>(pv + g);
+        for (int32_t i = a.I; i >= 3; i--) {
+            k_sweep_trace_part<<<(unsigned)g, kTrT, 0, st>>>(a, i, S.st, pv, pk);
+            k_sweep_trace_pick<<<1, kTrT, 0, st>>>(i, S.st, pv, pk, g, S.runp);
+        }
     }
     k_sweep_sums<<<1, kSB, 0, st>>>(a, S.st, out, chain);
     return hipGetLastError();
