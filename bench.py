@@ -75,11 +75,11 @@ KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
 SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 1.056e8
-SWEEP_TRAFFIC_SHA = "0f426c17a12c3ca7"
+SWEEP_TRAFFIC_SHA = "00e8daa2b39458ea"
 # hardware counters of the same profile: SQ_INSTS_VALU_FLOPS_FP64 per solve over
 # the seconds per solve, and the share of VALU issue slots used
-SWEEP_COUNTER_FP64_TFLOPS = 21.0
-SWEEP_COUNTER_VALU_BUSY = 0.686
+SWEEP_COUNTER_FP64_TFLOPS = 21.1
+SWEEP_COUNTER_VALU_BUSY = 0.689
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the (workload, s) both traffic figures were measured on; null for others
 TRAFFIC_WORKLOAD = ("weights_256k", 32)

@@ -649,6 +649,46 @@ def test_quantize_bit_exact(seed):
     assert _close(float(ent), e_o, 1e-12)
 
 
+def _near_tie_rounding_case(seed, e, n=64):
+    """Entry e of an n-entry vector whose rounding probability x_e / D equals
+    its own uniform u_e to within an ulp or two: the codebook is {0, D} with
+    D = RN(a / u_e) and x_e = a, a power of two that keeps D below 4, so the
+    quotient RN(a / D) lands next to u_e, inside the 2^-50 band where the
+    kernel must fall back to the exact division.  The other entries are
+    spread over [0, D]."""
+    u = pipeline.uniforms(n, seed)
+    m = 0
+    while 2.0 ** -m / u[e] >= 3.5:
+        m += 1
+    a = 2.0 ** -m
+    D = a / u[e]
+    x = (np.random.default_rng(seed + e).random(n) * D).astype(np.float32)
+    x[e] = np.float32(a)
+    return x, np.array([0.0, D]), u[e]
+
+
+@pytest.mark.parametrize("seed", [3, 2 ** 33 + 1])
+def test_quantize_near_ties_take_the_exact_division(seed):
+    """Entries where u and the rounding probability differ by an ulp or two:
+    symbols equal to the oracle's plain-division symbols.  Each such entry is
+    undecided by the reciprocal estimate (checked here in numpy with the
+    kernel's own bound), so the fallback is what decides it; both outcomes
+    occur."""
+    outcomes = set()
+    for e in range(0, 64, 3):
+        x, q, ue = _near_tie_rounding_case(seed, e)
+        a = float(x[e])
+        qa = a * (1.0 / q[1])
+        assert abs(ue - qa) <= abs(qa) * 2.0 ** -50
+        _say("quantize near tie", seed, e)
+        sym, ent, hist = ecasq.ecasq_quantize(_dev(x), torch.from_numpy(q), seed)
+        s_o, h_o, e_o = pipeline.quantize(x, q, seed)
+        np.testing.assert_array_equal(sym.cpu().numpy(), s_o)
+        np.testing.assert_array_equal(hist.cpu().numpy(), h_o)
+        outcomes.add(int(s_o[e]))
+    assert outcomes == {0, 1}
+
+
 def test_quantize_solution_end_to_end():
     x = inputs.normal(4096, 12)
     _say("solve + quantize")
