@@ -341,49 +341,71 @@ __global__ __launch_bounds__(256) void k_quantize_ts(
         if (lh[1][r]) atomicAdd(&hist[t0 + r], (unsigned long long)lh[1][r]);
 }
 
+// Sum over a 256-thread workgroup (a butterfly per wavefront, then the four
+// wavefront sums in order); every thread gets the total.
+__device__ __forceinline__ double block_sum(double v, double* red) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    __syncthreads();  // red is free
+    if (threadIdx.x % 64 == 0) red[threadIdx.x / 64] = v;
+    __syncthreads();
+    return ((red[0] + red[1]) + red[2]) + red[3];
+}
+
+// Plug-in entropy of one symbol histogram (t <= 256 counts, one per thread):
+// H = sum of h(n_r / n) over the nonzero counts, n = the counts' total
+// (d for the plain rounding, the part's size for a time-shared part).
+__device__ __forceinline__ double plugin_entropy(const unsigned long long* __restrict__ hist,
+                                                 int32_t t, double n, int64_t* hist_out,
+                                                 const double2* __restrict__ tab, double* red) {
+    const int r = threadIdx.x;
+    double h = 0.0;
+    if (r < t) {
+        const unsigned long long c = hist[r];
+        if (hist_out) hist_out[r] = (int64_t)c;
+        if (c) h = hfun((double)c / n, tab);
+    }
+    return block_sum(h, red);
+}
+
 // Entropy of a time-shared rounding: each part's plug-in entropy over its own
 // entries, weighted by its size: (n_0 H_0 + n_1 H_1) / d.
-__global__ void k_entropy_ts(const unsigned long long* __restrict__ hist, int32_t t0, int32_t t1,
-                             int64_t d, double* __restrict__ ent, int64_t* __restrict__ hist_out) {
+__global__ __launch_bounds__(256) void k_entropy_ts(const unsigned long long* __restrict__ hist,
+                                                    int32_t t0, int32_t t1, int64_t d,
+                                                    double* __restrict__ ent,
+                                                    int64_t* __restrict__ hist_out) {
     __shared__ double2 tab[kLog2Size];
+    __shared__ double red[4];
     load_log2_table(tab);
     __syncthreads();
-    if (threadIdx.x != 0) return;
     double total = 0.0;
     int32_t base = 0;
     for (int w = 0; w < 2; w++) {
         const int32_t t = w ? t1 : t0;
-        unsigned long long n = 0;
-        for (int32_t r = 0; r < t; r++) n += hist[base + r];
-        double H = 0.0;
-        for (int32_t r = 0; r < t; r++) {
-            const unsigned long long c = hist[base + r];
-            if (hist_out) hist_out[base + r] = (int64_t)c;
-            if (c) H = H + hfun((double)c / (double)n, tab);
+        const int r = threadIdx.x;
+        const double nr = r < t ? (double)hist[base + r] : 0.0;  // counts < 2^53: exact
+        const double n = block_sum(nr, red);
+        if (n > 0.0) {
+            const double H = plugin_entropy(hist + base, t, n, hist_out ? hist_out + base : nullptr,
+                                            tab, red);
+            total = total + n * H;
+        } else if (hist_out && r < t) {
+            hist_out[base + r] = 0;
         }
-        if (n) total = total + (double)n * H;
         base += t;
     }
-    *ent = total / (double)d;
+    if (threadIdx.x == 0) *ent = total / (double)d;
 }
 
-__global__ void k_entropy(const unsigned long long* __restrict__ hist, int32_t t, int64_t d,
-                          double* __restrict__ ent, int64_t* __restrict__ hist_out) {
+__global__ __launch_bounds__(256) void k_entropy(const unsigned long long* __restrict__ hist,
+                                                 int32_t t, int64_t d, double* __restrict__ ent,
+                                                 int64_t* __restrict__ hist_out) {
     __shared__ double2 tab[kLog2Size];
+    __shared__ double red[4];
     load_log2_table(tab);
     __syncthreads();
-    if (threadIdx.x != 0) return;
-    double H = 0.0;
-    const double dd = (double)d;
-    for (int32_t r = 0; r < t; r++) {
-        const unsigned long long n = hist[r];
-        if (hist_out) hist_out[r] = (int64_t)n;
-        if (n) {
-            const double y = (double)n / dd;
-            H = H + hfun(y, tab);
-        }
-    }
-    *ent = H;
+    const double H = plugin_entropy(hist, t, (double)d, hist_out, tab, red);
+    if (threadIdx.x == 0) *ent = H;
 }
 
 // Symbol counts of the allocation-free rounding entry point: one array per
@@ -463,7 +485,7 @@ hipError_t launch_quantize(const void* x, int dt, int64_t d, const double* codeb
 
 hipError_t launch_entropy(const unsigned long long* hist, int32_t t, int64_t d, double* ent,
                           int64_t* hist_out, hipStream_t st) {
-    k_entropy<<<1, 64, 0, st>>>(hist, t, d, ent, hist_out);
+    k_entropy<<<1, 256, 0, st>>>(hist, t, d, ent, hist_out);
     return hipGetLastError();
 }
 
@@ -484,7 +506,7 @@ hipError_t launch_quantize_ts(const void* x, int dt, int64_t d, const double* cb
     else
         k_quantize_ts<2><<<(unsigned)g, 256, 0, st>>>(x, d, cb0, t0, cb1, t1, alpha, k0, k1,
                                                       symbols, part, hist);
-    k_entropy_ts<<<1, 64, 0, st>>>(hist, t0, t1, d, ent, hist_out);
+    k_entropy_ts<<<1, 256, 0, st>>>(hist, t0, t1, d, ent, hist_out);
     return hipGetLastError();
 }
 
