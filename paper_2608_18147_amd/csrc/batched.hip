@@ -153,8 +153,9 @@ __device__ __forceinline__ Hist row_hist(const Row& R) {
 // The solve's point from its chain u_0 .. u_{n-1} in R.nu: MSE and H(I,B)
 // summed in path order (the same additions as accumulating them along the
 // argmins); lane r evaluates the interval (u_r, u_{r+1}] (n <= s <= 32) and
-// the sums run over the lanes in order.  The chain is kept in the first entries of argmin
-// buffer `buf` (rows 0 and 1 of the table are never layers).
+// the sums run over the lanes in order.  The chain is kept in the first
+// entries of argmin buffer `buf` (rows 0 and 1 of the table are never
+// layers).
 __device__ Pt row_chain_point(Row& R, double lam, int n, int buf) {
     const int lane = R.lane;
     const Hist H = row_hist(R);
