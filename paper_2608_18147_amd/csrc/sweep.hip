@@ -254,7 +254,9 @@ __device__ __forceinline__ void store_running(const SweepArgs& a, int64_t j, int
 }
 
 // Staged predecessors kb..ke-1 (ke - kb even) against column (cv, cN, cS,
-// cS2) for LW layers whose F_{i-1} sit in sF columns lofs..lofs+LW-1.
+// cS2) for LW layers whose F_{i-1} sit in sF columns lofs..lofs+LW-1.  At
+// lambda' = 0 the cost is C alone (cell_c: the same value as the fma with
+// a zero multiplier), without the entropy terms.
 template <int LG, int LW>
 __device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int lofs, int kb, int ke,
                                            double cv, double cN, double cS, double cS2, double dd,
@@ -273,12 +275,20 @@ __device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int lofs, int
     // few layers: two predecessors per iteration, whose C and Phi are
     // independent chains the scheduler can interleave
     for (int kk = kb; kk < ke; kk += 2) {
-        double C0, P0, C1, P1;
-        cell_terms(sm.hv[0][kk], sm.hN[0][kk], sm.hS[0][kk], sm.hS2[0][kk], cv, cN, cS, cS2, dd, false, 0.0,
-                   sm.tab, C0, P0);
-        cell_terms(sm.hv[0][kk + 1], sm.hN[0][kk + 1], sm.hS[0][kk + 1], sm.hS2[0][kk + 1], cv, cN, cS, cS2,
-                   dd, false, 0.0, sm.tab, C1, P1);
-        const double Q0 = __builtin_fma(-lamp, P0, C0), Q1 = __builtin_fma(-lamp, P1, C1);
+        double Q0, Q1;
+        if (lamp == 0.0) {  // uniform
+            Q0 = cell_c(sm.hv[0][kk], sm.hN[0][kk], sm.hS[0][kk], sm.hS2[0][kk], cv, cN, cS, cS2);
+            Q1 = cell_c(sm.hv[0][kk + 1], sm.hN[0][kk + 1], sm.hS[0][kk + 1], sm.hS2[0][kk + 1], cv,
+                        cN, cS, cS2);
+        } else {
+            double C0, P0, C1, P1;
+            cell_terms(sm.hv[0][kk], sm.hN[0][kk], sm.hS[0][kk], sm.hS2[0][kk], cv, cN, cS, cS2,
+                       dd, false, 0.0, sm.tab, C0, P0);
+            cell_terms(sm.hv[0][kk + 1], sm.hN[0][kk + 1], sm.hS[0][kk + 1], sm.hS2[0][kk + 1], cv,
+                       cN, cS, cS2, dd, false, 0.0, sm.tab, C1, P1);
+            Q0 = __builtin_fma(-lamp, P0, C0);
+            Q1 = __builtin_fma(-lamp, P1, C1);
+        }
 #pragma unroll
         for (int l = 0; l < LW; l++) {
             best[l] = __builtin_fmin(best[l], sm.sF[kk][lofs + l] + Q0);
@@ -335,10 +345,14 @@ __device__ void form_costs(const SweepArgs& a, int64_t b, int64_t kb0, int n,
         for (int k = wave; k < kSB; k += kTileWaves) {
             double q = __builtin_huge_val();
             if (kb < b || kb * kSB + k < jj) {
-                double C, P;
-                cell_terms(sv[x][k], sN[x][k], sS[x][k], sS2[x][k], cv, cN, cS, cS2, a.H.dd, false,
-                           0.0, tab, C, P);
-                q = __builtin_fma(-a.lamp, P, C);
+                if (a.lamp == 0.0) {  // C alone (cell_c), as in the tiles
+                    q = cell_c(sv[x][k], sN[x][k], sS[x][k], sS2[x][k], cv, cN, cS, cS2);
+                } else {
+                    double C, P;
+                    cell_terms(sv[x][k], sN[x][k], sS[x][k], sS2[x][k], cv, cN, cS, cS2, a.H.dd,
+                               false, 0.0, tab, C, P);
+                    q = __builtin_fma(-a.lamp, P, C);
+                }
             }
             T[k * kSB + lane] = q;
         }
