@@ -172,9 +172,10 @@ ecasq_status ecasq_solve(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
  *      it; the codebook is recovered by Hirschberg's method (recovery 0) or
  *      from stored argmins (recovery 1);
  *   1  one sweep over column blocks in which the interval cost and entropy
- *      term of each cell serve every layer; keeps F of all layers and an
- *      int32 table of the same shape (traceback scratch; every argmin only
- *      when an inspection call asks for them): 12 (s+1) d bytes.  The
+ *      term of each cell serve every layer; keeps F of all layers, 8 (s+1) d
+ *      bytes, and about 0.8 d bytes of step counters and traceback scratch
+ *      (an int32 argmin table of F's shape only when an inspection call asks
+ *      for argmins or accumulators).  The
  *      codebook comes from the argmin traceback of the solve it was found
  *      in, each argmin recomputed from the kept layers (recovery is
  *      ignored). */

@@ -53,6 +53,7 @@ struct Layout {
     size_t v, N, S, S2, gv, gN, gS, gS2, F0, F1, M0, M1, P0, P1, pval, pidx, last, res, mres,
         small, chain, kstar, prep, swF, swQ, swK, swchain, sstate, schains, two, cres, cchain;
     int64_t pstride;  // partial entries per multiplier
+    size_t swKbytes;  // bytes at swK
     size_t total;
 };
 
@@ -61,6 +62,10 @@ struct Layout {
 constexpr int32_t kWsArgmins = 1;
 constexpr int32_t kWsSweep = 2;
 constexpr int32_t kWsAlphabet = 4;  // a permissible grid next to the input's histogram
+// (internal) schedule 1 with the argmin table of every layer, for the
+// inspection call's argmin and accumulator dumps; without it K holds only
+// the steps' counters and the traceback's partials
+constexpr int32_t kWsSweepArgmins = 8;
 
 Layout layout(int64_t d, int32_t s, int32_t flags) {
     Layout L;
@@ -96,7 +101,10 @@ Layout layout(int64_t d, int32_t s, int32_t flags) {
     L.pidx = take(sizeof(int32_t) * np);
     L.swF = take(sweep ? sizeof(double) * (size_t)(s + 1) * (size_t)d : 0);
     L.swQ = take(sweep ? sweep_cost_bytes() : 0);
-    L.swK = take(sweep ? sizeof(int32_t) * (size_t)(s + 1) * (size_t)d : 0);
+    L.swKbytes = !sweep ? 0
+                 : (flags & kWsSweepArgmins) ? sizeof(int32_t) * (size_t)(s + 1) * (size_t)d
+                                             : sweep_scratch_bytes(d);
+    L.swK = take(L.swKbytes);
     L.swchain = take(sizeof(int32_t) * 528);  // chain, then the traceback state
     L.last = take(sizeof(double) * 3 * (size_t)(s + 1) * kMaxLambdas);
     L.res = take(sizeof(double) * 4 * kMaxLambdas);
@@ -262,6 +270,7 @@ SweepSolve sweep_args(const Ctx& c) {
     S.F = c.at<double>(c.L.swF);
     S.Q = c.at<double>(c.L.swQ);
     S.K = c.at<int32_t>(c.L.swK);
+    S.kbytes = c.L.swKbytes;
     S.st = c.at<int32_t>(c.L.swchain) + 256;
     S.ld = c.d;
     S.I = (int32_t)std::min<int64_t>(c.s, c.p);
@@ -1442,7 +1451,8 @@ ecasq_status ecasq_dp_trace(const void* x, ecasq_dtype dt, int64_t d, int32_t s,
     for (int32_t m = 0; m < nlam; m++)
         if (!(lambdas[m] >= 0.0) || !std::isfinite(lambdas[m])) return ECASQ_EINVAL;
     Ctx c;
-    ECASQ_TRY(ctx_open(c, d, s, schedule == 1 ? kWsSweep : 0, stream, nullptr, 0));
+    const int32_t flags = schedule == 1 ? (kWsSweep | (kstar || M ? kWsSweepArgmins : 0)) : 0;
+    ECASQ_TRY(ctx_open(c, d, s, flags, stream, nullptr, 0));
     struct Closer {
         Ctx& c;
         ~Closer() { ctx_close(c); }

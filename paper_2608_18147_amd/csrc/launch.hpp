@@ -139,7 +139,9 @@ struct SweepSolve {
     Hist H;
     double* F;
     double* Q;     // sweep_cost_bytes(): the next diagonal block's costs
-    int32_t* K;    // argmins on request (launch_sweep_argmins); traceback scratch
+    int32_t* K;    // step counters and traceback scratch; the argmins on request
+                   // (launch_sweep_argmins), when it holds (I + 1) x ld int32
+    size_t kbytes = 0;  // bytes at K
     int32_t* st;   // traceback state, 264 int32
     int64_t ld;    // >= p
     int32_t I;     // last layer, min(s, p), 2..255
@@ -148,6 +150,9 @@ struct SweepSolve {
     const int32_t* runp = nullptr;  // device: 0 = skip the whole solve (null: run)
 };
 size_t sweep_table_bytes(int64_t d, int32_t s);
+// Bytes of K that a solve needs for p <= d: the steps' counters and the
+// traceback's partials (the argmin table is (s + 1) d int32 on top).
+size_t sweep_scratch_bytes(int64_t d);
 size_t sweep_cost_bytes();
 // The sweep, then eq. apx_final and the traceback (argmins recomputed along
 // the chain): out (device, 4 doubles) = J, MSE, H(I,B), i*; chain (device,

@@ -1112,9 +1112,21 @@ size_t trace_scratch_bytes(int64_t p) {
     return (size_t)trace_groups(p) * (sizeof(double) + sizeof(int32_t));
 }
 
+// The counters of the steps: a chunk counter per block, the failure word,
+// kHelpMax helper counters per block.
+size_t counter_bytes(int64_t p) {
+    const int64_t nblk = (p + kSB - 1) / kSB;
+    return sizeof(int32_t) * (size_t)(nblk * (1 + kHelpMax) + 1);
+}
+
 bool sweep_ok(const SweepSolve& S) {
     return S.I >= 2 && S.I <= 255 && S.H.p >= 2 && S.ld >= S.H.p && S.F && S.Q && S.K && S.st &&
-           (size_t)S.ld * sizeof(int32_t) >= trace_scratch_bytes(S.H.p);
+           S.kbytes >= counter_bytes(S.H.p) && S.kbytes >= trace_scratch_bytes(S.H.p);
+}
+
+// K holds the argmin table of layers 0..I.
+bool sweep_argmins_ok(const SweepSolve& S) {
+    return sweep_ok(S) && S.kbytes >= sizeof(int32_t) * (size_t)(S.I + 1) * (size_t)S.ld;
 }
 
 }  // namespace
@@ -1122,6 +1134,11 @@ bool sweep_ok(const SweepSolve& S) {
 size_t sweep_table_bytes(int64_t d, int32_t s) {
     // F (fp64) and K (int32: inspection and traceback scratch), rows 0..s
     return (size_t)(s + 1) * (size_t)d * (sizeof(double) + sizeof(int32_t));
+}
+
+size_t sweep_scratch_bytes(int64_t d) {
+    const size_t a = counter_bytes(d), b = trace_scratch_bytes(d);
+    return a > b ? a : b;
 }
 
 size_t sweep_cost_bytes() { return (size_t)kQAll * sizeof(double); }
@@ -1159,7 +1176,7 @@ hipError_t launch_sweep(const SweepSolve& S, int32_t exact_s, double* out, int32
 }
 
 hipError_t launch_sweep_argmins(const SweepSolve& S, hipStream_t st) {
-    if (!sweep_ok(S)) return hipErrorInvalidValue;
+    if (!sweep_argmins_ok(S)) return hipErrorInvalidValue;
     const SweepArgs a = make_args(S);
     k_sweep_argmins2<<<(unsigned)((a.H.p - 1 + 255) / 256), 256, 0, st>>>(a);
     for (int32_t i = 3; i <= a.I; i++) {
@@ -1171,7 +1188,7 @@ hipError_t launch_sweep_argmins(const SweepSolve& S, hipStream_t st) {
 }
 
 hipError_t launch_sweep_accumulators(const SweepSolve& S, double* M, double* Ph, hipStream_t st) {
-    if (!sweep_ok(S) || !M || !Ph) return hipErrorInvalidValue;
+    if (!sweep_argmins_ok(S) || !M || !Ph) return hipErrorInvalidValue;
     const SweepArgs a = make_args(S);
     for (int32_t i = 2; i <= a.I; i++) {
         const int64_t n = a.H.p - (i - 1);
