@@ -74,12 +74,12 @@ TRAFFIC_SOURCES_SHA = "8106750032cad4c6"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
-SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 1.079e8
-SWEEP_TRAFFIC_SHA = "3976004e5fe53788"
+SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 1.082e8
+SWEEP_TRAFFIC_SHA = "a7ca1f641bb12390"
 # hardware counters of the same profile: SQ_INSTS_VALU_FLOPS_FP64 per solve over
 # the seconds per solve, and the share of VALU issue slots used
-SWEEP_COUNTER_FP64_TFLOPS = 20.3
-SWEEP_COUNTER_VALU_BUSY = 0.675
+SWEEP_COUNTER_FP64_TFLOPS = 20.1
+SWEEP_COUNTER_VALU_BUSY = 0.667
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the (workload, s) both traffic figures were measured on; null for others
 TRAFFIC_WORKLOAD = ("weights_256k", 32)
