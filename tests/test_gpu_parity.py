@@ -752,6 +752,44 @@ def test_batched_shapes_and_edge_rows():
             _compare_row(cbs[r], int(tt[r]), infos[r], o, s)
 
 
+def _wide_range_rows(rng, n, d):
+    """Rows whose values span the whole fp32 range with both signs:
+    subnormals, values near 2^-126 and 2^127 and ordinary ones, so that the
+    exact prefix sums carry and borrow across every limb of the wide
+    accumulators."""
+    e = rng.integers(-149, 127, size=(n, d))
+    m = rng.random((n, d)) + 1.0
+    x = (np.where(rng.random((n, d)) < 0.5, -1.0, 1.0) * m * np.exp2(e.astype(np.float64)))
+    x = x.astype(np.float32)
+    x[:, 0] = np.float32(2.0 ** -149)        # the smallest subnormal
+    x[:, 1] = -np.float32(3.0 * 2.0 ** -140)  # a negative subnormal
+    x[:, 2] = np.float32(3.0e38)
+    x[:, 3] = np.float32(-3.0e38)
+    return x
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_batched_wide_range_rows(dt):
+    """Exact prefix sums of rows spanning the fp32 exponent range (the
+    wavefront scan of the wide sums), fp32 and bf16 storage: the oracle's
+    solve row by row."""
+    rng = np.random.default_rng(45)
+    x = _wide_range_rows(rng, 6, 128)
+    xt = torch.from_numpy(x)
+    if dt == "bf16":
+        xt = xt.to(torch.bfloat16)
+    xs = xt.float().numpy()  # the values the library sees
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    _say("batched wide range", dt)
+    cbs, tt, infos = ecasq.ecasq_solve_batched(xt.to("cuda"), 12, 2.5)
+    cbs, tt = cbs.cpu().numpy(), tt.cpu().numpy()
+    infos = ecasq.infos_to_dicts(infos)
+    for r in range(xs.shape[0]):
+        o = pipeline.solve(xs[r], 12, 2.5, recovery="backpointers", width=1, aim=False)
+        _compare_row(cbs[r], int(tt[r]), infos[r], o, 12)
+
+
 def test_batched_nonfinite_row_is_flagged():
     x = np.random.default_rng(2).standard_normal((3, 64)).astype(np.float32)
     x[1, 7] = np.inf
