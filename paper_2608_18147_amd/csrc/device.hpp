@@ -40,22 +40,39 @@ constexpr int kLog2Size = 1 << kLog2Bits;
 // -e = u >> 20 (arithmetic) in one subtraction and, in bits 10..19, the
 // complement 1023 - i of the table index, so the LDS copy of the table is
 // stored in reverse; e + lc is formed as lc - (double)(-e), the same IEEE sum.
-__device__ __forceinline__ double log2c(double y, const double2* __restrict__ tab) {
+// log2c in two parts, for callers that issue several table reads before
+// using any: the reduction and the table index, then the series.
+struct Log2Arg {
+    double z;   // ldexp(y, -e)
+    int32_t ne; // -e
+    uint32_t ir; // mirrored table index
+};
+
+__device__ __forceinline__ Log2Arg log2c_arg(double y) {
     const uint32_t hi = (uint32_t)__double2hiint(y);
     const int32_t u = (int32_t)((ECASQ_LOG2_OFF_HI + 0xFFFFFu) - hi);
-    const int32_t ne = u >> 20;  // -e
-    const uint32_t ir = ((uint32_t)u >> (20 - kLog2Bits)) & (kLog2Size - 1);  // mirrored i
-    const double z = __builtin_ldexp(y, ne);
-    const double2 t = tab[ir];
-    const double r = __builtin_fma(z, t.x, -1.0);
+    Log2Arg r;
+    r.ne = u >> 20;  // -e
+    r.ir = ((uint32_t)u >> (20 - kLog2Bits)) & (kLog2Size - 1);
+    r.z = __builtin_ldexp(y, r.ne);
+    return r;
+}
+
+__device__ __forceinline__ double log2c_fin(const Log2Arg& a, double2 t) {
+    const double r = __builtin_fma(a.z, t.x, -1.0);
     constexpr double K = 0x1.71547652b82fep+0;
     double q = K * (1.0 / 5.0);
     q = __builtin_fma(q, r, K * -0.25);
     q = __builtin_fma(q, r, K * (1.0 / 3.0));
     q = __builtin_fma(q, r, K * -0.5);
     q = __builtin_fma(q, r, K * 1.0);
-    const double base = t.y - (double)ne;
+    const double base = t.y - (double)a.ne;
     return __builtin_fma(r, q, base);
+}
+
+__device__ __forceinline__ double log2c(double y, const double2* __restrict__ tab) {
+    const Log2Arg a = log2c_arg(y);
+    return log2c_fin(a, tab[a.ir]);
 }
 
 // Table-driven base-2 exponential (Tang 1989 style): y = k/64 + r with
@@ -116,11 +133,11 @@ __device__ __forceinline__ double hfun(double y, const double2* __restrict__ tab
     return -(m * log2c(m, tab));
 }
 
-// C and P (= -Phi, or -Phi^first when `first`) of the interval (v_a, v_b].
-__device__ __forceinline__ void cell_terms(double va, double Na, double Sa, double S2a, double vb,
-                                           double Nb, double Sb, double S2b, double dd, bool first,
-                                           double c0d, const double2* __restrict__ tab, double& C,
-                                           double& P) {
+// C and the clamped scaled frequencies mu = max(yu, 0), md = max(yd, 0) of
+// the interval (v_a, v_b]: everything of cell_terms before the logarithms.
+__device__ __forceinline__ void cell_pre(double va, double Na, double Sa, double S2a, double vb,
+                                         double Nb, double Sb, double S2b, double dd, bool first,
+                                         double c0d, double& C, double& mu, double& md) {
     const double n = Nb - Na;
     const double sa = Sb - Sa;
     const double s2 = S2b - S2a;
@@ -133,8 +150,17 @@ __device__ __forceinline__ void cell_terms(double va, double Na, double Sa, doub
     const double yu = tu * g;
     double yd = td * g;
     if (first) yd = yd + c0d;
-    const double mu = __builtin_fmax(yu, 0.0);
-    const double md = __builtin_fmax(yd, 0.0);
+    mu = __builtin_fmax(yu, 0.0);
+    md = __builtin_fmax(yd, 0.0);
+}
+
+// C and P (= -Phi, or -Phi^first when `first`) of the interval (v_a, v_b].
+__device__ __forceinline__ void cell_terms(double va, double Na, double Sa, double S2a, double vb,
+                                           double Nb, double Sb, double S2b, double dd, bool first,
+                                           double c0d, const double2* __restrict__ tab, double& C,
+                                           double& P) {
+    double mu, md;
+    cell_pre(va, Na, Sa, S2a, vb, Nb, Sb, S2b, dd, first, c0d, C, mu, md);
     P = __builtin_fma(mu, log2c(mu, tab), md * log2c(md, tab));
 }
 

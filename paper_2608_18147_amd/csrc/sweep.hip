@@ -37,6 +37,8 @@
 // The fixed cost of a launch (dispatch, staging, the running minima read and
 // written back) is shared by nb blocks, and the chain inside a launch costs
 // one block addition and one triangle per block.
+#include <stddef.h>
+
 #include "device.hpp"
 #include "launch.hpp"
 
@@ -85,6 +87,16 @@ constexpr int kTileWaves = 4;  // wavefronts per workgroup
 // (two independent C / Phi chains per iteration; also fewer registers)
 #ifndef ECASQ_SWEEP_PAIR_MAX
 #define ECASQ_SWEEP_PAIR_MAX 32
+#endif
+// LDS read pairs the tile loop keeps in flight ahead of their use (0: the
+// scheduler's own order)
+#ifndef ECASQ_SWEEP_AHEAD
+#define ECASQ_SWEEP_AHEAD 2
+#endif
+// the tile loop issues the four log2 table reads of a predecessor pair
+// before it uses any
+#ifndef ECASQ_SWEEP_LOG_BATCH
+#define ECASQ_SWEEP_LOG_BATCH 1
 #endif
 #if ECASQ_SWEEP_WAVES > 0
 #define ECASQ_STEP_ATTR __attribute__((amdgpu_waves_per_eu(ECASQ_SWEEP_WAVES)))
@@ -230,6 +242,10 @@ struct StepSmem {
     double pF[kSB];                               // previous layer of block t
     double partV[kTileWaves][kSB];                // per-wave partial minima
 };
+// the staging rows are read two layers at a time (16-byte LDS reads)
+static_assert(offsetof(StepSmem<8>, sF) % 16 == 0 && offsetof(StepSmem<16>, sF) % 16 == 0 &&
+                  offsetof(StepSmem<32>, sF) % 16 == 0 && (8 + kSFPad) % 2 == 0,
+              "staging rows 16-byte aligned");
 
 // Running minima of LW layers i0.. of column jj (rows past I: +inf).
 template <int LW>
@@ -250,6 +266,41 @@ __device__ __forceinline__ void store_running(const SweepArgs& a, int64_t j, int
     for (int l = 0; l < LW; l++) {
         const int32_t i = i0 + l;
         if (i <= a.I) a.F[(int64_t)i * a.ld + j] = best[l];
+    }
+}
+
+// best[l] = min(best[l], F0[l] + Q0, F1[l] + Q1) for the LW layers of two
+// staged rows (16-byte aligned), read two layers at a time.  Scheduling
+// barriers keep ECASQ_SWEEP_AHEAD read pairs in flight ahead of the adds and
+// minima that use them, so that the LDS latency overlaps arithmetic instead
+// of stalling the wavefront once per read (left alone, the scheduler waits
+// for each read right after issuing it, for want of registers).
+template <int LW>
+__device__ __forceinline__ void add_min_rows(const double* F0, const double* F1, double Q0,
+                                             double Q1, double (&best)[LW]) {
+    static_assert(LW % 2 == 0, "layers in pairs");
+    constexpr int H = LW / 2;
+    constexpr int D = ECASQ_SWEEP_AHEAD < H ? ECASQ_SWEEP_AHEAD : H;
+    const double2* r0 = reinterpret_cast<const double2*>(F0);
+    const double2* r1 = reinterpret_cast<const double2*>(F1);
+    double2 a[H], b[H];
+#pragma unroll
+    for (int h = 0; h < D; h++) {
+        a[h] = r0[h];
+        b[h] = r1[h];
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int h = 0; h < H; h++) {
+        if (h + D < H) {
+            a[h + D] = r0[h + D];
+            b[h + D] = r1[h + D];
+        }
+        best[2 * h] = __builtin_fmin(best[2 * h], a[h].x + Q0);
+        best[2 * h] = __builtin_fmin(best[2 * h], b[h].x + Q1);
+        best[2 * h + 1] = __builtin_fmin(best[2 * h + 1], a[h].y + Q0);
+        best[2 * h + 1] = __builtin_fmin(best[2 * h + 1], b[h].y + Q1);
+        __builtin_amdgcn_sched_barrier(0);
     }
 }
 
@@ -275,25 +326,45 @@ __device__ __forceinline__ void accumulate(const StepSmem<LG>& sm, int lofs, int
     // few layers: two predecessors per iteration, whose C and Phi are
     // independent chains the scheduler can interleave
     for (int kk = kb; kk < ke; kk += 2) {
+        const double v0 = sm.hv[0][kk], N0 = sm.hN[0][kk], S0 = sm.hS[0][kk],
+                     S20 = sm.hS2[0][kk];
+        const double v1 = sm.hv[0][kk + 1], N1 = sm.hN[0][kk + 1], S1 = sm.hS[0][kk + 1],
+                     S21 = sm.hS2[0][kk + 1];
         double Q0, Q1;
         if (lamp == 0.0) {  // uniform
-            Q0 = cell_c(sm.hv[0][kk], sm.hN[0][kk], sm.hS[0][kk], sm.hS2[0][kk], cv, cN, cS, cS2);
-            Q1 = cell_c(sm.hv[0][kk + 1], sm.hN[0][kk + 1], sm.hS[0][kk + 1], sm.hS2[0][kk + 1], cv,
-                        cN, cS, cS2);
+            Q0 = cell_c(v0, N0, S0, S20, cv, cN, cS, cS2);
+            Q1 = cell_c(v1, N1, S1, S21, cv, cN, cS, cS2);
         } else {
+#if ECASQ_SWEEP_LOG_BATCH
+            // cell_terms of both predecessors, the four table reads issued
+            // together before any is used
+            double C0, mu0, md0, C1, mu1, md1;
+            cell_pre(v0, N0, S0, S20, cv, cN, cS, cS2, dd, false, 0.0, C0, mu0, md0);
+            cell_pre(v1, N1, S1, S21, cv, cN, cS, cS2, dd, false, 0.0, C1, mu1, md1);
+            const Log2Arg u0 = log2c_arg(mu0), d0 = log2c_arg(md0);
+            const Log2Arg u1 = log2c_arg(mu1), d1 = log2c_arg(md1);
+            const double2 tu0 = sm.tab[u0.ir], td0 = sm.tab[d0.ir];
+            const double2 tu1 = sm.tab[u1.ir], td1 = sm.tab[d1.ir];
+            __builtin_amdgcn_sched_barrier(0);
+            const double P0 = __builtin_fma(mu0, log2c_fin(u0, tu0), md0 * log2c_fin(d0, td0));
+            const double P1 = __builtin_fma(mu1, log2c_fin(u1, tu1), md1 * log2c_fin(d1, td1));
+#else
             double C0, P0, C1, P1;
-            cell_terms(sm.hv[0][kk], sm.hN[0][kk], sm.hS[0][kk], sm.hS2[0][kk], cv, cN, cS, cS2,
-                       dd, false, 0.0, sm.tab, C0, P0);
-            cell_terms(sm.hv[0][kk + 1], sm.hN[0][kk + 1], sm.hS[0][kk + 1], sm.hS2[0][kk + 1], cv,
-                       cN, cS, cS2, dd, false, 0.0, sm.tab, C1, P1);
+            cell_terms(v0, N0, S0, S20, cv, cN, cS, cS2, dd, false, 0.0, sm.tab, C0, P0);
+            cell_terms(v1, N1, S1, S21, cv, cN, cS, cS2, dd, false, 0.0, sm.tab, C1, P1);
+#endif
             Q0 = __builtin_fma(-lamp, P0, C0);
             Q1 = __builtin_fma(-lamp, P1, C1);
         }
+#if ECASQ_SWEEP_AHEAD > 0
+        add_min_rows<LW>(&sm.sF[kk][lofs], &sm.sF[kk + 1][lofs], Q0, Q1, best);
+#else
 #pragma unroll
         for (int l = 0; l < LW; l++) {
             best[l] = __builtin_fmin(best[l], sm.sF[kk][lofs + l] + Q0);
             best[l] = __builtin_fmin(best[l], sm.sF[kk + 1][lofs + l] + Q1);
         }
+#endif
     }
     }
 }
