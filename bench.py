@@ -69,17 +69,17 @@ def flops_per_cell(nlam):
 # (profiles/k_dp_layer_pass8_weights_256k.md), scaled by a plain copy's
 # readings (FETCH x2.0, WRITE x1.0).  Valid only for the kernel sources they
 # were taken on: reported as null once those sources change.
-TRAFFIC_BYTES_PER_LAUNCH = 2.486e9
-TRAFFIC_SOURCES_SHA = "8106750032cad4c6"
+TRAFFIC_BYTES_PER_LAUNCH = 2.489e9
+TRAFFIC_SOURCES_SHA = "4d97e06384505869"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
-SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 1.082e8
-SWEEP_TRAFFIC_SHA = "a7ca1f641bb12390"
+SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 1.259e8
+SWEEP_TRAFFIC_SHA = "9a3c1f70f2ecd550"
 # hardware counters of the same profile: SQ_INSTS_VALU_FLOPS_FP64 per solve over
 # the seconds per solve, and the share of VALU issue slots used
-SWEEP_COUNTER_FP64_TFLOPS = 20.1
-SWEEP_COUNTER_VALU_BUSY = 0.667
+SWEEP_COUNTER_FP64_TFLOPS = 22.6
+SWEEP_COUNTER_VALU_BUSY = 0.757
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the (workload, s) both traffic figures were measured on; null for others
 TRAFFIC_WORKLOAD = ("weights_256k", 32)

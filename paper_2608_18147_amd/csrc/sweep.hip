@@ -164,13 +164,18 @@ __device__ __forceinline__ void stage_block(const SweepArgs& a, int64_t k0, int3
     // block [k0, k0+64) lies below a later block, so k0 + 63 < p
     constexpr int R = kSB * LG / kThreads;  // F values per thread
     static_assert(R * kThreads == kSB * LG, "a layer group of 64 columns fills the workgroup");
+    // the row stride as a value the compiler cannot carry across calls: the
+    // R row addresses are formed here (a few integer operations) instead of
+    // being kept for the whole tile loop in registers it does not have
+    int64_t ld = a.ld;
+    asm volatile("" : "+s"(ld));
     double f[R];
 #pragma unroll
     for (int r = 0; r < R; r++) {
         const int x = threadIdx.x + r * kThreads;
         const int kk = x % kSB, l = x / kSB;
         const int32_t i = i0 + l;
-        f[r] = i <= a.I ? a.F[(int64_t)(i - 1) * a.ld + k0 + kk] : __builtin_huge_val();
+        f[r] = i <= a.I ? a.F[(int64_t)(i - 1) * ld + k0 + kk] : __builtin_huge_val();
     }
     if (threadIdx.x < kSB) {
         const int64_t k = k0 + threadIdx.x;
