@@ -263,22 +263,45 @@ __device__ Pt row_sweep(Row& R, double lam, int exact_s, int buf) {
 #pragma unroll
             for (int l = 1; l < LG; l++) Fk[l] = readlane_d(best[ck][l - 1], kk);
             const double pv = R.v[k], pN = R.N[k], pS = R.S[k], pS2 = R.S2[k];
+            // the costs of (k, j) for this lane's columns from segment ck on
+            // (segment ck at kk = 63 takes nothing); with entropy terms, every
+            // column's log2 table reads are issued before any is used
+            double Q[CMAX];
+            if (zl) {
 #pragma unroll
-            for (int c = ck; c < CMAX; c++) {  // (segment ck at kk = 63 takes nothing)
-                const int j = c * kWave + lane;
-                double Q;
-                if (zl) {
-                    Q = cell_c(pv, pN, pS, pS2, cv[c], cN[c], cS[c], cS2[c]);
-                } else {
-                    double C, P;
-                    cell_terms(pv, pN, pS, pS2, cv[c], cN[c], cS[c], cS2[c], dd, false, 0.0,
-                               R.tab, C, P);
-                    Q = __builtin_fma(-lamp, P, C);
+                for (int c = ck; c < CMAX; c++)
+                    Q[c] = cell_c(pv, pN, pS, pS2, cv[c], cN[c], cS[c], cS2[c]);
+            } else {
+                double C[CMAX], mu[CMAX], md[CMAX];
+                Log2Arg au[CMAX], ad[CMAX];
+                double2 tu[CMAX], td[CMAX];
+#pragma unroll
+                for (int c = ck; c < CMAX; c++) {
+                    cell_pre(pv, pN, pS, pS2, cv[c], cN[c], cS[c], cS2[c], dd, false, 0.0, C[c],
+                             mu[c], md[c]);
+                    au[c] = log2c_arg(mu[c]);
+                    ad[c] = log2c_arg(md[c]);
                 }
-                // columns at or below k take nothing from it
-                Q = j > k ? Q : __builtin_huge_val();
 #pragma unroll
-                for (int l = 0; l < LG; l++) best[c][l] = __builtin_fmin(best[c][l], Fk[l] + Q);
+                for (int c = ck; c < CMAX; c++) {
+                    tu[c] = R.tab[au[c].ir];
+                    td[c] = R.tab[ad[c].ir];
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int c = ck; c < CMAX; c++) {
+                    const double P = __builtin_fma(mu[c], log2c_fin(au[c], tu[c]),
+                                                   md[c] * log2c_fin(ad[c], td[c]));
+                    Q[c] = __builtin_fma(-lamp, P, C[c]);
+                }
+            }
+#pragma unroll
+            for (int c = ck; c < CMAX; c++) {
+                const int j = c * kWave + lane;
+                // columns at or below k take nothing from it
+                const double q = j > k ? Q[c] : __builtin_huge_val();
+#pragma unroll
+                for (int l = 0; l < LG; l++) best[c][l] = __builtin_fmin(best[c][l], Fk[l] + q);
             }
         }
     }
