@@ -56,6 +56,16 @@ FP64_VECTOR_PEAK_TFLOPS = 78.6
 FLOPS_PAIR = 25
 FLOPS_CELL = 1
 FLOPS_LAYER2_COL = 25
+# the + lambda' Phi FMA inside FLOPS_PAIR: the layer kernel forms it once per
+# multiplier, so a (k, j) cell of its launch over nlam multipliers counts
+# FLOPS_PAIR - FLOPS_Q + (FLOPS_Q + FLOPS_CELL) nlam (47 for 8)
+FLOPS_Q = 2
+
+
+def layer_flops_per_cell(nlam):
+    """Algorithmic FP64 flops of one (k, j) cell of the layer kernel with
+    nlam multipliers per launch."""
+    return FLOPS_PAIR - FLOPS_Q + (FLOPS_Q + FLOPS_CELL) * nlam
 
 
 def flops_per_cell(nlam):
@@ -276,6 +286,8 @@ def alphabet_rate(torch, ecasq, xd, s, b, opts, full_info, grids=(("uniform", 40
 
 # y = yu + yd, max, log2, the mul m log2(m), the candidate's fma, the min
 OPT_OPS_PER_CANDIDATE = 6
+# the same as flops: the add, the log2 (1), the mul, the fma (2); max and min 0
+OPT_FLOPS_PER_CANDIDATE = 5
 
 
 def optimal_rate(torch, ecasq, inputs, reps=3):
@@ -303,11 +315,17 @@ def optimal_rate(torch, ecasq, inputs, reps=3):
              "vnmse": info["vnmse"], "entropy": info["entropy"],
              "layer_ms_per_solve": kms / reps, "layer_launches": launches // reps}
         if scan == 1 and kms > 0:
-            achieved = OPT_OPS_PER_CANDIDATE * cands / (kms * 1e-3) / 1e12
+            rate = cands / (kms * 1e-3)
+            achieved = OPT_FLOPS_PER_CANDIDATE * rate / 1e12
+            tops = OPT_OPS_PER_CANDIDATE * rate / 1e12
             r["roofline"] = {"bound": "alu", "kernel": "k_opt_layer<full> (fp64 VALU)",
-                             "achieved": achieved, "peak": ALU_PEAK_TOPS,
-                             "unit": "TOP/s (fp64 lane ops)", "frac": achieved / ALU_PEAK_TOPS,
-                             "candidates_per_s": cands / (kms * 1e-3),
+                             "achieved": achieved, "peak": FP64_VECTOR_PEAK_TFLOPS,
+                             "unit": "TFLOP/s", "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
+                             "flops_per_candidate": OPT_FLOPS_PER_CANDIDATE,
+                             "lane_ops": {"achieved_tops": tops, "peak_tops": ALU_PEAK_TOPS,
+                                          "frac": tops / ALU_PEAK_TOPS,
+                                          "ops_per_candidate": OPT_OPS_PER_CANDIDATE},
+                             "candidates_per_s": rate,
                              "avg_launch_ms": kms / max(launches, 1)}
         out[name] = r
     out["speedup_monotone"] = out["full"]["ms_per_solve"] / out["monotone"]["ms_per_solve"]
@@ -578,18 +596,27 @@ def main():
     else:
         avg_ms = ms / max(launches, 1)
         fpc = flops_per_cell(LAMBDAS_PER_PASS)
-        achieved = fpc * (cells / max(launches, 1)) / (avg_ms * 1e-3) / 1e12 if ms > 0 else 0.0
+        flc = layer_flops_per_cell(LAMBDAS_PER_PASS)
+        rate = (cells / max(launches, 1)) / (avg_ms * 1e-3) if ms > 0 else 0.0
+        achieved = flc * rate / 1e12
+        tops = fpc * rate / 1e12
         roofline = {
             "bound": "alu",
             "kernel": "k_dp_layer, 8 multipliers per launch (fp64 VALU)",
             "achieved": achieved,
-            "peak": ALU_PEAK_TOPS,
-            "unit": "TOP/s (fp64 lane ops)",
-            "frac": achieved / ALU_PEAK_TOPS,
+            "peak": FP64_VECTOR_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / FP64_VECTOR_PEAK_TFLOPS,
             "traffic": (TRAFFIC_BYTES_PER_LAUNCH
                         if measured and kernel_sources_sha() == TRAFFIC_SOURCES_SHA else None),
             "traffic_unit": "bytes/launch",
-            "ops_per_cell": fpc,
+            "flops_per_cell": flc,
+            "flops_accounting": ("per (k, j) cell of a launch: %d for C and Phi, then %d per "
+                                 "multiplier (the + lambda' Phi FMA and the candidate's add); "
+                                 "FMA = 2, division and log2 = 1 each, min/max/compare = 0"
+                                 % (FLOPS_PAIR - FLOPS_Q, FLOPS_Q + FLOPS_CELL)),
+            "lane_ops": {"achieved_tops": tops, "peak_tops": ALU_PEAK_TOPS,
+                         "frac": tops / ALU_PEAK_TOPS, "ops_per_cell": fpc},
             "avg_launch_ms": avg_ms,
             "launches": launches,
             "cells_per_s": cells / (ms * 1e-3) if ms > 0 else None,
