@@ -140,6 +140,40 @@ def test_dp_layers_bit_exact(name, d, s, lam, schedule):
     assert int(out[3]) == r["t"] and int(out[4]) == r["cells"]
 
 
+def _random_shape(seed):
+    """A seeded (input, s, lambda) with d from 65 to 2600 (ragged column
+    blocks), s in one of the sweep's layer-group ranges (up to 10, 11 to 18,
+    19 to 40 with s = 32 among them, 41 to 70: two groups) and lambda = 0 one
+    time in four."""
+    rng = np.random.default_rng(1000 + seed)
+    d = int(rng.integers(65, 2601))
+    lo, hi = [(3, 10), (11, 18), (19, 40), (41, 70)][seed % 4]
+    s = 32 if seed % 8 == 2 else int(rng.integers(lo, hi + 1))
+    lam = 0.0 if rng.random() < 0.25 else float(10 ** rng.uniform(-4, 0.5))
+    name = ["normal", "lognormal", "weights", "dups", "wide_range"][int(rng.integers(0, 5))]
+    return name, d, s, lam
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_sweep_layers_random_shapes(seed):
+    """Every layer's values and argmins of the sweep bit for bit against the
+    oracle's dumped DP, on seeded random sizes, layer counts, multipliers
+    and input kinds."""
+    name, d, s, lam = _random_shape(seed)
+    x = _dp_input(name, d)
+    _say("random shape", seed, name, d, s, lam)
+    F, K, _, _, out = ecasq.ecasq_dp_trace(_dev(x), s, lam, schedule=1)
+    F, K = F.cpu().numpy(), K.cpu().numpy()
+    H = pipeline.prepare(x)
+    p = H.p
+    r = pipeline.dp_forward(H, s, lam * H.s2tot, backpointers=True, dump=True)
+    for i in range(2, min(s, p) + 1):
+        lo = i - 1
+        np.testing.assert_array_equal(F[i, lo:p], r["F"][i, lo:p], err_msg=f"layer {i}")
+        np.testing.assert_array_equal(K[i, lo:p], r["bp"][i, lo:p], err_msg=f"argmin layer {i}")
+    assert out[0] == r["J"] and int(out[3]) == r["t"]
+
+
 PASS_GRID = (0.0, 1e-4, 1e-3, 1e-2, 1e-1, 1.0, 10.0, 100.0)
 
 
