@@ -23,7 +23,7 @@ constexpr int kSortItems = 16;
 constexpr int kSortTile = kSortBlock * kSortItems;
 
 constexpr int kRec = 16;  // u64 words per chunk record: S, S2, run ends
-constexpr int kChunk = 16;
+constexpr int kChunk = 8;
 constexpr int kScanBlock = 256;
 
 template <int DT>
@@ -64,28 +64,51 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t* __res
     hist[(int64_t)tid * nblk + blockIdx.x] = cnt[tid];
 }
 
-// Exclusive scan of m uint32 values in place, one block of 1024 threads.
+// Exclusive scan of m uint32 values in place, one block of 1024 threads, in
+// tiles of 8192 values staged through LDS (coalesced loads and stores):
+// each thread scans 8 consecutive values of the tile, the thread totals are
+// scanned by wavefront shuffles and then across the 16 wavefronts, and a
+// carry takes each tile's total to the next.
 __global__ __launch_bounds__(1024) void k_scan_u32(uint32_t* __restrict__ a, int64_t m) {
-    __shared__ uint32_t part[1024];
+    constexpr int V = 8, T = 1024 * V;
+    __shared__ uint32_t buf[T];
+    __shared__ uint32_t part[16];
     const int tid = threadIdx.x;
-    const int64_t per = (m + 1023) / 1024;
-    const int64_t lo = tid * per;
-    const int64_t hi = lo + per < m ? lo + per : m;
-    uint32_t s = 0;
-    for (int64_t i = lo; i < hi; i++) s += a[i];
-    part[tid] = s;
-    __syncthreads();
-    for (int off = 1; off < 1024; off <<= 1) {
-        uint32_t t = tid >= off ? part[tid - off] : 0u;
+    const int lane = tid & 63, wave = tid >> 6;
+    uint32_t carry = 0;
+    for (int64_t base = 0; base < m; base += T) {
+        const int n = m - base < T ? (int)(m - base) : T;
+        for (int i = tid; i < T; i += 1024) buf[i] = i < n ? a[base + i] : 0u;
         __syncthreads();
-        part[tid] += t;
+        uint32_t v[V], s = 0;
+#pragma unroll
+        for (int u = 0; u < V; u++) {
+            v[u] = buf[tid * V + u];
+            s += v[u];
+        }
+        // every lane takes part in every shuffle
+        uint32_t x = s;
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint32_t y = __shfl_up(x, off);
+            if (lane >= off) x += y;
+        }
+        if (lane == 63) part[wave] = x;
         __syncthreads();
-    }
-    uint32_t run = part[tid] - s;  // exclusive
-    for (int64_t i = lo; i < hi; i++) {
-        uint32_t v = a[i];
-        a[i] = run;
-        run += v;
+        uint32_t wpre = 0, total = 0;
+        for (int w = 0; w < 16; w++) {
+            wpre += w < wave ? part[w] : 0u;
+            total += part[w];
+        }
+        uint32_t run = carry + wpre + x - s;  // exclusive
+#pragma unroll
+        for (int u = 0; u < V; u++) {
+            buf[tid * V + u] = run;
+            run += v[u];
+        }
+        __syncthreads();
+        for (int i = tid; i < n; i += 1024) a[base + i] = buf[i];
+        carry += total;
+        __syncthreads();  // buf and part are reused by the next tile
     }
 }
 
@@ -166,6 +189,33 @@ __device__ __forceinline__ void rec_add(uint64_t* a, const uint64_t* b) {
     a[kRec - 1] += b[kRec - 1];
 }
 
+// Exclusive scan of each run of kScanBlock chunk records in place, one
+// workgroup per run (record c at thread c mod kScanBlock), and the run's
+// total to tot[run].  The records hold exact integers, so the order of the
+// additions does not change any sum.
+__global__ __launch_bounds__(kScanBlock) void k_scan_runs(uint64_t* __restrict__ rec,
+                                                          int64_t nchunk,
+                                                          uint64_t* __restrict__ tot) {
+    __shared__ uint64_t part[kScanBlock][kRec];
+    const int tid = threadIdx.x;
+    const int64_t c = (int64_t)blockIdx.x * kScanBlock + tid;
+    const bool live = c < nchunk;
+    for (int l = 0; l < kRec; l++) part[tid][l] = live ? rec[c * kRec + l] : 0ull;
+    __syncthreads();
+    for (int off = 1; off < kScanBlock; off <<= 1) {
+        uint64_t t[kRec];
+        const bool on = tid >= off;
+        for (int l = 0; l < kRec; l++) t[l] = on ? part[tid - off][l] : 0ull;
+        __syncthreads();
+        if (on) rec_add(part[tid], t);
+        __syncthreads();
+    }
+    if (live)
+        for (int l = 0; l < kRec; l++) rec[c * kRec + l] = tid ? part[tid - 1][l] : 0ull;
+    if (tid == kScanBlock - 1)
+        for (int l = 0; l < kRec; l++) tot[(int64_t)blockIdx.x * kRec + l] = part[tid][l];
+}
+
 // Exclusive scan of the chunk records in place (one block); writes the number
 // of distinct values to *p_out.
 __global__ __launch_bounds__(kScanBlock) void k_scan_records(uint64_t* __restrict__ rec,
@@ -199,19 +249,24 @@ __global__ __launch_bounds__(kScanBlock) void k_scan_records(uint64_t* __restric
     }
 }
 
-// Walk each chunk from its exclusive prefix and write the histogram entry of
-// every run end: v[u], N[u] (inclusive count), S[u], S2[u] (rounded once).
+// Walk each chunk from its exclusive prefix (its run's, from tot, plus its
+// own within the run) and write the histogram entry of every run end: v[u], N[u] (inclusive count), S[u], S2[u] (rounded once).
 __global__ __launch_bounds__(kScanBlock) void k_scan_emit(const uint32_t* __restrict__ keys,
                                                           int64_t d, int64_t nchunk,
                                                           const uint64_t* __restrict__ rec,
+                                                          const uint64_t* __restrict__ tot,
                                                           double* __restrict__ v,
                                                           double* __restrict__ N,
                                                           double* __restrict__ S,
                                                           double* __restrict__ S2) {
     const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (c >= nchunk) return;
+    // the chunk's exclusive prefix: its run's prefix plus its place in the run
+    uint64_t r[kRec];
+#pragma unroll
+    for (int l = 0; l < kRec; l++) r[l] = tot[(c / kScanBlock) * kRec + l];
+    rec_add(r, rec + c * kRec);
     uint64_t s[kSL], q[kS2L];
-    const uint64_t* r = rec + c * kRec;
 #pragma unroll
     for (int l = 0; l < kSL; l++) s[l] = r[l];
 #pragma unroll
@@ -243,6 +298,7 @@ size_t prep_scratch_bytes(int64_t d) {
     b += align256(sizeof(uint32_t) * d) * 2;           // keys, ping-pong
     b += align256(sizeof(uint32_t) * 256 * nblk);      // digit histogram
     b += align256(sizeof(uint64_t) * kRec * nchunk);   // chunk records
+    b += align256(sizeof(uint64_t) * kRec * ((nchunk + kScanBlock - 1) / kScanBlock));  // runs
     b += align256(sizeof(uint32_t) * 4);               // flags
     return b;
 }
@@ -259,6 +315,8 @@ hipError_t launch_prep(const void* x, int dt, int64_t d, void* scratch, hipStrea
     uint32_t* hist = reinterpret_cast<uint32_t*>(w);
     w += align256(sizeof(uint32_t) * 256 * nblk);
     uint64_t* rec = reinterpret_cast<uint64_t*>(w);
+    w += align256(sizeof(uint64_t) * kRec * nchunk);
+    uint64_t* tot = reinterpret_cast<uint64_t*>(w);
 
     const int ig = (int)((d + 255) / 256 < 65536 ? (d + 255) / 256 : 65536);
     if (dt == 0) k_ingest<0><<<ig, 256, 0, st>>>(x, d, k0, flags_dev);
@@ -274,9 +332,12 @@ hipError_t launch_prep(const void* x, int dt, int64_t d, void* scratch, hipStrea
         k1 = t;
     }
     const unsigned sg = (unsigned)((nchunk + kScanBlock - 1) / kScanBlock);
+    // chunk totals; each run of kScanBlock chunks scanned by a workgroup;
+    // the run totals scanned by one; then every chunk walked from its prefix
     k_scan_local<<<sg, kScanBlock, 0, st>>>(k0, d, nchunk, rec);
-    k_scan_records<<<1, kScanBlock, 0, st>>>(rec, nchunk, p_dev);
-    k_scan_emit<<<sg, kScanBlock, 0, st>>>(k0, d, nchunk, rec, v, N, S, S2);
+    k_scan_runs<<<sg, kScanBlock, 0, st>>>(rec, nchunk, tot);
+    k_scan_records<<<1, kScanBlock, 0, st>>>(tot, (int64_t)sg, p_dev);
+    k_scan_emit<<<sg, kScanBlock, 0, st>>>(k0, d, nchunk, rec, tot, v, N, S, S2);
     return hipGetLastError();
 }
 

@@ -222,18 +222,21 @@ __device__ __forceinline__ void stage_chunk(const SweepArgs& a, int64_t u0, int 
     }
 }
 
-// Rows 2..I of F := +inf (nothing seen yet; also the value of every entry
-// outside a layer's valid columns, which makes such predecessors lose).
+// Rows 2..I of F := +inf in columns 0..p-1 (nothing seen yet; also the value
+// of every entry outside a layer's valid columns, which makes such
+// predecessors lose; columns from p on are never read), row 2 + blockIdx.y.
 // Also clears the steps' counters and failure word (K[0..nblk (1 + kHelpMax)]).
 __global__ __launch_bounds__(256) void k_sweep_fill(SweepArgs a) {
     if (!sweep_live(a)) return;
-    const int64_t n = (int64_t)(a.I - 1) * a.ld;
-    for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; x < n;
-         x += (int64_t)gridDim.x * blockDim.x)
-        a.F[2 * a.ld + x] = __builtin_huge_val();
-    for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-         x <= a.nblk * (1 + kHelpMax); x += (int64_t)gridDim.x * blockDim.x)
-        a.K[x] = 0;
+    const int64_t p = a.H.p;
+    double* row = a.F + (int64_t)(2 + blockIdx.y) * a.ld;
+    for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < p;
+         j += (int64_t)gridDim.x * blockDim.x)
+        row[j] = __builtin_huge_val();
+    if (blockIdx.y == 0)
+        for (int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+             x <= a.nblk * (1 + kHelpMax); x += (int64_t)gridDim.x * blockDim.x)
+            a.K[x] = 0;
 }
 
 // Shared memory of one step workgroup.
@@ -1151,10 +1154,11 @@ template <int LG, int NL = LG>
 hipError_t sweep_launch(const SweepArgs& a, hipStream_t st) {
     const int32_t ngroups = (a.I - 2 + LG - 1) / LG;
     {
-        const int64_t n = (int64_t)(a.I - 1) * a.ld;
-        int64_t g = (n + 255) / 256;
-        if (g > 4096) g = 4096;
-        k_sweep_fill<<<(unsigned)g, 256, 0, st>>>(a);
+        const int64_t rows = a.I - 1;  // >= 1
+        int64_t g = (a.H.p + 255) / 256;
+        const int64_t cap = 4096 / rows > 0 ? 4096 / rows : 1;
+        if (g > cap) g = cap;
+        k_sweep_fill<<<dim3((unsigned)g, (unsigned)rows), 256, 0, st>>>(a);
     }
     // a step makes blocks t..t+nb-1 final; blocks tp..t-1 (the last step's)
     // are final and not yet added to the column blocks after t - 1
