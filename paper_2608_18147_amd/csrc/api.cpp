@@ -209,7 +209,9 @@ ecasq_status ctx_prep(Ctx& c, const void* x, int dt, int32_t alphabet = 0, int64
     HIP_TRY(launch_prep(x, dt, c.d, c.base + c.L.prep, c.st, c.at<double>(c.L.v),
                         c.at<double>(c.L.N), c.at<double>(c.L.S), c.at<double>(c.L.S2), small,
                         flags));
-    int64_t hs[2] = {0, 0};
+    // p, the non-finite flag, then S2[p-1] and N[0] (written by the last
+    // preparation kernel as doubles): one read
+    int64_t hs[4] = {0, 0, 0, 0};
     HIP_TRY(hipMemcpyAsync(hs, small, sizeof hs, hipMemcpyDeviceToHost, c.st));
     HIP_TRY(hipStreamSynchronize(c.st));
     if ((uint32_t)hs[1] & 1u) return ECASQ_ENONFINITE;
@@ -218,8 +220,9 @@ ecasq_status ctx_prep(Ctx& c, const void* x, int dt, int32_t alphabet = 0, int64
     c.H.N = c.at<double>(c.L.N);
     c.H.S = c.at<double>(c.L.S);
     c.H.S2 = c.at<double>(c.L.S2);
-    double s2 = 0;
-    HIP_TRY(hipMemcpyAsync(&s2, c.H.S2 + (c.p - 1), sizeof(double), hipMemcpyDeviceToHost, c.st));
+    double s2 = 0, c0 = 0;
+    std::memcpy(&s2, &hs[2], sizeof s2);
+    std::memcpy(&c0, &hs[3], sizeof c0);
     if (alphabet != 0 && c.p >= 2) {
         int64_t* count = small + 5;
         HIP_TRY(launch_alphabet(alphabet, m, c.d, c.H.v, c.H.N, c.H.S, c.H.S2, c.p,
@@ -234,10 +237,10 @@ ecasq_status ctx_prep(Ctx& c, const void* x, int dt, int32_t alphabet = 0, int64
         c.H.N = c.at<double>(c.L.gN);
         c.H.S = c.at<double>(c.L.gS);
         c.H.S2 = c.at<double>(c.L.gS2);
+        // the grid's first count
+        HIP_TRY(hipMemcpyAsync(&c0, c.H.N, sizeof(double), hipMemcpyDeviceToHost, c.st));
+        HIP_TRY(hipStreamSynchronize(c.st));
     }
-    double c0 = 0;
-    HIP_TRY(hipMemcpyAsync(&c0, c.H.N, sizeof(double), hipMemcpyDeviceToHost, c.st));
-    HIP_TRY(hipStreamSynchronize(c.st));
     c.s2tot = s2;
     c.H.p = c.p;
     c.H.dd = (double)c.d;

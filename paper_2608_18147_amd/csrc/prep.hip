@@ -289,6 +289,16 @@ __global__ __launch_bounds__(kScanBlock) void k_scan_emit(const uint32_t* __rest
     }
 }
 
+// ||X||^2 = S2[p-1] and the count of the smallest value N[0] beside p in
+// the host-read slots (one read after preparation instead of two).
+__global__ void k_prep_tail(const int64_t* __restrict__ p, const double* __restrict__ N,
+                            const double* __restrict__ S2, double* __restrict__ out) {
+    if (threadIdx.x != 0) return;
+    const int64_t n = p[0];
+    out[0] = n >= 1 ? S2[n - 1] : 0.0;
+    out[1] = n >= 1 ? N[0] : 0.0;
+}
+
 }  // namespace
 
 size_t prep_scratch_bytes(int64_t d) {
@@ -338,6 +348,7 @@ hipError_t launch_prep(const void* x, int dt, int64_t d, void* scratch, hipStrea
     k_scan_runs<<<sg, kScanBlock, 0, st>>>(rec, nchunk, tot);
     k_scan_records<<<1, kScanBlock, 0, st>>>(tot, (int64_t)sg, p_dev);
     k_scan_emit<<<sg, kScanBlock, 0, st>>>(k0, d, nchunk, rec, tot, v, N, S, S2);
+    k_prep_tail<<<1, 64, 0, st>>>(p_dev, N, S2, reinterpret_cast<double*>(p_dev + 2));
     return hipGetLastError();
 }
 
