@@ -126,20 +126,46 @@ __global__ __launch_bounds__(256) void k_refine(Hist H, int32_t t, int32_t* __re
 }
 
 // out: MSE, vNMSE, H(Xhat), H(I,B), vNMSE + lambda H(Xhat), H(Xhat) + 32t/d.
+// The interval terms and the values' entropy terms are formed one per
+// thread; one thread then sums them in index order (the sums of the chain
+// walk in chain_hout and of the path accumulators, bit for bit).
 __global__ void k_metrics(Hist H, int32_t t, const int32_t* __restrict__ u, double lam,
                           double s2tot, double* __restrict__ out) {
     __shared__ double2 tab[kLog2Size];
+    __shared__ double sC[kMaxT], sP[kMaxT], sU[kMaxT], sD[kMaxT], sh[kMaxT];
     load_log2_table(tab);
+    __syncthreads();
+    for (int32_t r = threadIdx.x; r + 1 < t; r += blockDim.x) {
+        double C, P, U, D;
+        cell_at(H, u[r], u[r + 1], tab, C, P);
+        ud_at(H, u[r], u[r + 1], U, D);
+        sC[r] = C;
+        sP[r] = P;
+        sU[r] = U;
+        sD[r] = D;
+    }
+    __syncthreads();
+    // expected frequency of value q (as chain_hout forms it), then h(f / d)
+    for (int32_t q = threadIdx.x; q < t; q += blockDim.x) {
+        double f;
+        if (t == 1) f = H.dd;
+        else if (q == 0) f = H.c0 + sD[0];
+        else if (q == t - 1) f = sU[t - 2];
+        else f = sU[q - 1] + sD[q];
+        sh[q] = hf(H, f, tab);
+    }
     __syncthreads();
     if (threadIdx.x != 0) return;
     double mse = 0.0, hs = 0.0;
     for (int32_t r = 0; r + 1 < t; r++) {
-        double C, P;
-        cell_at(H, u[r], u[r + 1], tab, C, P);
-        mse = mse + C;
-        hs = hs - P;
+        mse = mse + sC[r];
+        hs = hs - sP[r];
     }
-    const double ho = chain_hout(H, t, u, tab);
+    double ho = sh[0];
+    if (t > 1) {
+        ho = 0.0;
+        for (int32_t q = 0; q < t; q++) ho = ho + sh[q];
+    }
     const double vn = s2tot > 0.0 ? mse / s2tot : 0.0;
     const double lr = __builtin_isfinite(lam) ? lam : 0.0;
     out[0] = mse;
@@ -457,7 +483,8 @@ hipError_t launch_refine(const Hist& H, int32_t t, int32_t* u, double lamp, doub
 
 hipError_t launch_metrics(const Hist& H, int32_t t, const int32_t* u, double lam, double s2tot,
                           double* out, hipStream_t st) {
-    k_metrics<<<1, 64, 0, st>>>(H, t, u, lam, s2tot, out);
+    if (t < 1 || t > kMaxT) return hipErrorInvalidValue;
+    k_metrics<<<1, 256, 0, st>>>(H, t, u, lam, s2tot, out);
     return hipGetLastError();
 }
 

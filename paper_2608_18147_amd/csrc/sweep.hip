@@ -889,27 +889,48 @@ constexpr int kStChain = 8;
 // A solve whose steps gave up a wait (failure word set) reports i* = 0: the
 // traceback kernels then return at once and the result has t = 0, which the
 // callers take as a failed solve.
-__global__ void k_sweep_pick(SweepArgs a, int32_t exact_s, double* out, int32_t* st) {
-    if (threadIdx.x != 0 || blockIdx.x != 0 || !sweep_live(a)) return;
+__global__ __launch_bounds__(64) void k_sweep_pick(SweepArgs a, int32_t exact_s, double* out,
+                                                    int32_t* st) {
+    if (blockIdx.x != 0 || !sweep_live(a)) return;  // uniform
+    const int lane = threadIdx.x;
     const int64_t p = a.H.p;
     if (a.K[a.nblk] != 0) {
-        st[0] = 0;
-        out[0] = __builtin_huge_val();
+        if (lane == 0) {
+            st[0] = 0;
+            out[0] = __builtin_huge_val();
+        }
         return;
     }
-    int32_t bi = 2;
-    double bj = a.F[2 * a.ld + p - 1];
-    for (int32_t i = 3; i <= a.I; i++) {
-        const double f = a.F[(int64_t)i * a.ld + p - 1];
-        if (exact_s ? (i == a.I) : (f < bj)) {
-            bj = f;
-            bi = i;
+    // the lowest i among the least F_i[p-1]: each lane the lowest of its
+    // layers 2 + lane, 66 + lane, ..., then (value, i) minima across lanes
+    double bj = __builtin_huge_val();
+    int32_t bi = 0x7fffffff;
+    if (exact_s) {
+        bi = a.I;
+        bj = a.F[(int64_t)a.I * a.ld + p - 1];
+    } else {
+        for (int32_t i = 2 + lane; i <= a.I; i += 64) {
+            const double f = a.F[(int64_t)i * a.ld + p - 1];
+            if (bi == 0x7fffffff || f < bj) {
+                bj = f;
+                bi = i;
+            }
+        }
+        for (int off = 32; off >= 1; off >>= 1) {
+            const double ov = __shfl_xor(bj, off);
+            const int32_t oi = __shfl_xor(bi, off);
+            if (ov < bj || (ov == bj && oi < bi)) {
+                bj = ov;
+                bi = oi;
+            }
         }
     }
-    st[0] = bi;
-    st[kStChain + bi - 1] = (int32_t)(p - 1);
-    st[kStChain] = 0;
-    out[0] = bj;
+    if (lane == 0) {
+        st[0] = bi;
+        st[kStChain + bi - 1] = (int32_t)(p - 1);
+        st[kStChain] = 0;
+        out[0] = bj;
+    }
 }
 
 // The lowest argmin k of F_{i-1}[k] + C[k,j] + lambda' Phi[k,j] over k in
