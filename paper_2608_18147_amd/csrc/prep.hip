@@ -196,7 +196,7 @@ __device__ __forceinline__ void rec_add(uint64_t* a, const uint64_t* b) {
 __global__ __launch_bounds__(kScanBlock) void k_scan_runs(uint64_t* __restrict__ rec,
                                                           int64_t nchunk,
                                                           uint64_t* __restrict__ tot) {
-    __shared__ uint64_t part[kScanBlock][kRec];
+    __shared__ uint64_t part[kScanBlock][kRec + 1];  // padded: lanes spread over the banks
     const int tid = threadIdx.x;
     const int64_t c = (int64_t)blockIdx.x * kScanBlock + tid;
     const bool live = c < nchunk;
@@ -221,7 +221,7 @@ __global__ __launch_bounds__(kScanBlock) void k_scan_runs(uint64_t* __restrict__
 __global__ __launch_bounds__(kScanBlock) void k_scan_records(uint64_t* __restrict__ rec,
                                                              int64_t nchunk,
                                                              int64_t* __restrict__ p_out) {
-    __shared__ uint64_t part[kScanBlock][kRec];
+    __shared__ uint64_t part[kScanBlock][kRec + 1];  // padded: lanes spread over the banks
     const int tid = threadIdx.x;
     const int64_t per = (nchunk + kScanBlock - 1) / kScanBlock;
     const int64_t lo = tid * per;
