@@ -85,11 +85,11 @@ KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
 SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 1.259e8
-SWEEP_TRAFFIC_SHA = "eed750c1de5c0db1"
+SWEEP_TRAFFIC_SHA = "d95e2b43a9e0b00b"
 # hardware counters of the same profile: SQ_INSTS_VALU_FLOPS_FP64 per solve over
 # the seconds per solve, and the share of VALU issue slots used
-SWEEP_COUNTER_FP64_TFLOPS = 22.4
-SWEEP_COUNTER_VALU_BUSY = 0.750
+SWEEP_COUNTER_FP64_TFLOPS = 22.3
+SWEEP_COUNTER_VALU_BUSY = 0.748
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the (workload, s) both traffic figures were measured on; null for others
 TRAFFIC_WORKLOAD = ("weights_256k", 32)
