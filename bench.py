@@ -90,6 +90,10 @@ SWEEP_TRAFFIC_SHA = "d95e2b43a9e0b00b"
 # the seconds per solve, and the share of VALU issue slots used
 SWEEP_COUNTER_FP64_TFLOPS = 22.3
 SWEEP_COUNTER_VALU_BUSY = 0.748
+# VALU wave instructions per solve of the same profile (SQ_INSTS_VALU): at
+# one instruction per SIMD every 4 cycles they bound the solve from below,
+# and with it the flop fraction this instruction stream can reach
+SWEEP_COUNTER_VALU_INSTS_PER_SOLVE = 5.991e10
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the (workload, s) both traffic figures were measured on; null for others
 TRAFFIC_WORKLOAD = ("weights_256k", 32)
@@ -118,6 +122,14 @@ def sweep_launches(p, s):
     blocks of 64 columns, SWEEP_STEP_BLOCKS per launch)."""
     nblk = (p + 63) // 64
     return (nblk + SWEEP_STEP_BLOCKS - 1) // SWEEP_STEP_BLOCKS
+
+
+def sweep_issue_bound_frac(flops):
+    """The flop fraction at which the profiled instruction stream would run
+    with every SIMD issuing a VALU instruction every 4 cycles (1024 SIMDs x
+    2.4 GHz): the ceiling of `frac` for this kernel's instruction mix."""
+    t_min = SWEEP_COUNTER_VALU_INSTS_PER_SOLVE * 4.0 / (1024 * 2.4e9)
+    return flops / t_min / 1e12 / FP64_VECTOR_PEAK_TFLOPS
 
 
 def sweep_roofline(p, s, ms, solves, cells, measured=True):
@@ -158,7 +170,9 @@ def sweep_roofline(p, s, ms, solves, cells, measured=True):
                      "frac": lane / ALU_PEAK_TOPS, "ops_per_solve": ops},
         "counters": ({"fp64_tflops": SWEEP_COUNTER_FP64_TFLOPS,
                       "frac_of_fp64_peak": SWEEP_COUNTER_FP64_TFLOPS / FP64_VECTOR_PEAK_TFLOPS,
-                      "valu_busy": SWEEP_COUNTER_VALU_BUSY} if current else None),
+                      "valu_busy": SWEEP_COUNTER_VALU_BUSY,
+                      "frac_at_full_valu_issue": sweep_issue_bound_frac(flops)}
+                     if current else None),
         "avg_launch_ms": per_ms / steps,
         "launches": solves * steps,
         "ms_per_solve": per_ms,
