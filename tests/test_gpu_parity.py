@@ -59,6 +59,12 @@ def _hist_cases():
     yield "all_equal", np.full(777, 1.5, dtype=np.float32)
     yield "single", np.array([-2.25], dtype=np.float32)
     yield "ragged_3333", rng.integers(-50, 50, 3333).astype(np.float32) * np.float32(0.125)
+    # several scan tiles of the sort's digit counts with a partial last one
+    # (35 tiles of 4096 keys: 8960 counts per digit pass) and 69 runs of
+    # chunk records, the last partial; wide exponents, both signs, repeats
+    y = rng.standard_normal(140001) * 10.0 ** rng.integers(-30, 30, 140001)
+    y[rng.integers(0, 140001, 20000)] = 0.75
+    yield "tiles_140001", y.astype(np.float32)
 
 
 @pytest.mark.parametrize("name,x", list(_hist_cases()), ids=lambda v: v if isinstance(v, str) else "")
