@@ -52,3 +52,31 @@ def test_traffic_reported_only_for_its_workload():
         assert base["traffic"] == bench.SWEEP_TRAFFIC_BYTES_PER_LAUNCH
     else:
         assert base["traffic"] is None
+
+
+@pytest.mark.parametrize("p,s", [(5, 3), (17, 8), (70, 40), (200, 32)])
+def test_roofline_flops_are_the_enumerated_cells(p, s):
+    """The roofline's flop count written out cell by cell: every (k, j) pair
+    (k < j) costs FLOPS_PAIR, every layer-2 column FLOPS_LAYER2_COL, and every
+    (k, j, layer) cell of layers 3..min(s, p) with i - 2 <= k < j
+    (j >= i - 1) FLOPS_CELL."""
+    pairs = sum(1 for j in range(p) for k in range(j))
+    cells = sum(1 for i in range(3, min(s, p) + 1)
+                for j in range(i - 1, p) for k in range(i - 2, j))
+    want = bench.FLOPS_PAIR * pairs + bench.FLOPS_CELL * cells + bench.FLOPS_LAYER2_COL * (p - 1)
+    r = bench.sweep_roofline(p, s, 1.0, 1, 0, measured=False)
+    assert r["flops_per_solve"] == want
+    assert r["frac"] == pytest.approx(want / 1e-3 / 1e12 / bench.FP64_VECTOR_PEAK_TFLOPS)
+
+
+def test_issue_bound_ceiling_covers_the_profiled_rate():
+    """The flop fraction at full VALU issue for the profiled instruction
+    stream lies above the fraction at the profiled time, by the profiled
+    VALU busy share."""
+    p, s = 261755, 32
+    r = bench.sweep_roofline(p, s, 130.42 * 10, 10, 0, measured=True)
+    if r["counters"] is None:
+        pytest.skip("profile constants are for other kernel sources")
+    ceil = r["counters"]["frac_at_full_valu_issue"]
+    assert r["frac"] < ceil < 1.0
+    assert r["frac"] / ceil == pytest.approx(bench.SWEEP_COUNTER_VALU_BUSY, abs=0.01)
