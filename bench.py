@@ -114,7 +114,7 @@ def log(*a):
 
 
 # diagonal blocks k_sweep_step makes final per launch (the last launch: the rest)
-SWEEP_STEP_BLOCKS = 12
+SWEEP_STEP_BLOCKS = 16
 
 
 def sweep_launches(p, s):

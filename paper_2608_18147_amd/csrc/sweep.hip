@@ -62,7 +62,7 @@ constexpr int kTileWaves = 4;  // wavefronts per workgroup
 // diagonal blocks a step makes final (one workgroup each, in a chain within
 // the launch; fewer launches share their fixed cost between more blocks)
 #ifndef ECASQ_SWEEP_NB
-#define ECASQ_SWEEP_NB 12
+#define ECASQ_SWEEP_NB 16
 #endif
 // polls of a block's flag before a wait gives up (about a second)
 #ifndef ECASQ_SWEEP_SPIN

@@ -33,8 +33,8 @@ def test_sweep_launches_cover_every_block_once(p, s):
 
 
 def test_default_workload_launch_count():
-    # 4090 blocks of 64 columns, twelve per launch
-    assert bench.sweep_launches(261755, 32) == 341
+    # 4090 blocks of 64 columns, sixteen per launch
+    assert bench.sweep_launches(261755, 32) == 256
 
 
 def test_bench_refuses_more_than_one_gpu():
