@@ -84,16 +84,16 @@ TRAFFIC_SOURCES_SHA = "4d97e06384505869"
 KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
-SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 1.259e8
-SWEEP_TRAFFIC_SHA = "d95e2b43a9e0b00b"
+SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 1.412e8
+SWEEP_TRAFFIC_SHA = "4de032f6b03aad54"
 # hardware counters of the same profile: SQ_INSTS_VALU_FLOPS_FP64 per solve over
 # the seconds per solve, and the share of VALU issue slots used
-SWEEP_COUNTER_FP64_TFLOPS = 22.3
-SWEEP_COUNTER_VALU_BUSY = 0.748
+SWEEP_COUNTER_FP64_TFLOPS = 22.7
+SWEEP_COUNTER_VALU_BUSY = 0.759
 # VALU wave instructions per solve of the same profile (SQ_INSTS_VALU): at
 # one instruction per SIMD every 4 cycles they bound the solve from below,
 # and with it the flop fraction this instruction stream can reach
-SWEEP_COUNTER_VALU_INSTS_PER_SOLVE = 5.991e10
+SWEEP_COUNTER_VALU_INSTS_PER_SOLVE = 5.982e10
 SWEEP_SOURCES = ("sweep.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the (workload, s) both traffic figures were measured on; null for others
 TRAFFIC_WORKLOAD = ("weights_256k", 32)
