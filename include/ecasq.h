@@ -173,7 +173,8 @@ ecasq_status ecasq_solve(const void *x, ecasq_dtype dt, int64_t d, int32_t s,
  *      from stored argmins (recovery 1);
  *   1  one sweep over column blocks in which the interval cost and entropy
  *      term of each cell serve every layer; keeps F of all layers, 8 (s+1) d
- *      bytes, and about d bytes of step counters and traceback scratch
+ *      bytes, 48 MB of per-launch cost tables and partial minima (any d),
+ *      and about d bytes of step counters and traceback scratch
  *      (an int32 argmin table of F's shape only when an inspection call asks
  *      for argmins or accumulators).  The
  *      codebook comes from the argmin traceback of the solve it was found
