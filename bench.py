@@ -85,7 +85,7 @@ KERNEL_SOURCES = ("dp.hip", "device.hpp", "launch.hpp", "log2_table.inc")
 # the same, averaged over the k_sweep_step launches of the default workload
 # (profiles/k_sweep_step_weights_256k.md)
 SWEEP_TRAFFIC_BYTES_PER_LAUNCH = 1.412e8
-SWEEP_TRAFFIC_SHA = "4de032f6b03aad54"
+SWEEP_TRAFFIC_SHA = "cf524e0f9632736c"
 # hardware counters of the same profile: SQ_INSTS_VALU_FLOPS_FP64 per solve over
 # the seconds per solve, and the share of VALU issue slots used
 SWEEP_COUNTER_FP64_TFLOPS = 22.7

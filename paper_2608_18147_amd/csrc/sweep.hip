@@ -110,6 +110,8 @@ constexpr int kTileWaves = 4;  // wavefronts per workgroup
 // by side and leave their partial minima of every layer of block b in a
 // buffer of their own.
 constexpr int kHelpBlocks = 2;
+// (helper_block keeps the costs of exactly two blocks: q0 and q1)
+static_assert(kHelpBlocks == 2, "a helper adds two blocks");
 constexpr int kHelpMax = ECASQ_SWEEP_NB > 1 ? ECASQ_SWEEP_NB - 1 : 1;  // per diagonal block
 
 // Cost tables Q = C - lambda' Phi (they do not depend on F), formed by the
