@@ -18,8 +18,8 @@ namespace ecasq {
 
 namespace {
 
-constexpr int kSortBlock = 256;
-constexpr int kSortItems = 16;
+constexpr int kSortBlock = 1024;  // threads per sort workgroup (>= 256 digits)
+constexpr int kSortItems = 4;
 constexpr int kSortTile = kSortBlock * kSortItems;
 
 constexpr int kRec = 16;  // u64 words per chunk record: S, S2, run ends
@@ -53,7 +53,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t* __res
                                                            uint32_t* __restrict__ hist, int nblk) {
     __shared__ uint32_t cnt[256];
     const int tid = threadIdx.x;
-    cnt[tid] = 0;
+    if (tid < 256) cnt[tid] = 0;
     __syncthreads();
     const int64_t base = (int64_t)blockIdx.x * kSortTile;
     for (int it = 0; it < kSortItems; it++) {
@@ -61,7 +61,7 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_hist(const uint32_t* __res
         if (idx < n) atomicAdd(&cnt[(keys[idx] >> shift) & 255u], 1u);
     }
     __syncthreads();
-    hist[(int64_t)tid * nblk + blockIdx.x] = cnt[tid];
+    if (tid < 256) hist[(int64_t)tid * nblk + blockIdx.x] = cnt[tid];
 }
 
 // Exclusive scan of m uint32 values in place, one block of 1024 threads, in
@@ -124,8 +124,10 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(const uint32_t* __
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    base[tid] = hist[(int64_t)tid * nblk + blockIdx.x];
-    for (int w = 0; w < kSortBlock / 64; w++) wcnt[w][tid] = 0;
+    if (tid < 256) {
+        base[tid] = hist[(int64_t)tid * nblk + blockIdx.x];
+        for (int w = 0; w < kSortBlock / 64; w++) wcnt[w][tid] = 0;
+    }
     __syncthreads();
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     const int64_t tile = (int64_t)blockIdx.x * kSortTile;
@@ -149,12 +151,14 @@ __global__ __launch_bounds__(kSortBlock) void k_radix_scatter(const uint32_t* __
             kout[pos] = key;
         }
         __syncthreads();
-        uint32_t tot = 0;
-        for (int w = 0; w < kSortBlock / 64; w++) {
-            tot += wcnt[w][tid];
-            wcnt[w][tid] = 0;
+        if (tid < 256) {
+            uint32_t tot = 0;
+            for (int w = 0; w < kSortBlock / 64; w++) {
+                tot += wcnt[w][tid];
+                wcnt[w][tid] = 0;
+            }
+            base[tid] += tot;
         }
-        base[tid] += tot;
         __syncthreads();
     }
 }
